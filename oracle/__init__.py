@@ -1,0 +1,181 @@
+"""Plain fp64 CPU oracle for the SENSE retrieval + soft-gated evaluation path.
+
+TEST INFRASTRUCTURE ONLY.  Only the test-suite, ``__graft_entry__.smoke()``
+and the benchmark's ``cpu_baseline`` leg may import this package.  The HIP
+library never imports, links or calls it, and it imports nothing from the HIP
+library (the two share no code).
+
+The arithmetic lives in ``sense_oracle.c`` (plain C loops in double precision;
+see its header for the paper passages it follows and the readings taken).
+This module only marshals numpy arrays into that library through ctypes.
+
+Array conventions: float32 data is passed as ``np.float32`` arrays; binary16
+and bfloat16 data are passed as ``np.uint16`` arrays of raw bit patterns with
+``dtype='f16'`` or ``dtype='bf16'``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "sense_oracle.c")
+_LIB = os.path.join(_HERE, "libsense_oracle.so")
+
+DTYPES = {"f32": 0, "f16": 1, "bf16": 2}
+METRICS = {"ip": 0, "cosine": 1}
+
+
+def build(force: bool = False) -> str:
+    """Compile the oracle with the host C compiler (OpenMP over rows)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(
+            ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp", _SRC, "-o", tmp, "-lm"]
+        )
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        lib = ctypes.CDLL(build())
+        P, I32, I64, D = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_double
+        lib.oracle_decode_f16.argtypes = [ctypes.c_uint16]
+        lib.oracle_decode_f16.restype = D
+        lib.oracle_decode_bf16.argtypes = [ctypes.c_uint16]
+        lib.oracle_decode_bf16.restype = D
+        lib.oracle_scores.argtypes = [P, ctypes.c_int, I64, I32, I64, P, ctypes.c_int, I32, ctypes.c_int, P]
+        lib.oracle_topk.argtypes = [P, I64, I32, P, P]
+        lib.oracle_gather.argtypes = [P, P, I32, P, I32, P, P]
+        lib.oracle_row_stats.argtypes = [P, ctypes.c_int, I32, I32, P, P, P]
+        lib.oracle_soft_gate_verify.argtypes = [
+            P, ctypes.c_int, I64, P, P, I32, I32, I32, I32, D, I32, I32, I32, I32, P, P, P, P, P, P
+        ]
+        for f in ("oracle_scores", "oracle_topk", "oracle_gather", "oracle_row_stats",
+                  "oracle_soft_gate_verify"):
+            getattr(lib, f).restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _raw(a, dtype):
+    want = np.float32 if dtype == "f32" else np.uint16
+    a = np.ascontiguousarray(a)
+    if a.dtype != want:
+        raise TypeError(f"dtype {dtype} wants {want}, got {a.dtype}")
+    return a
+
+
+def decode(bits, dtype: str) -> np.ndarray:
+    """Decode raw f16/bf16 bit patterns (or pass f32 through) to float64."""
+    lib = _load()
+    if dtype == "f32":
+        return np.asarray(bits, dtype=np.float32).astype(np.float64)
+    fn = lib.oracle_decode_f16 if dtype == "f16" else lib.oracle_decode_bf16
+    flat = np.asarray(bits, dtype=np.uint16).ravel()
+    return np.array([fn(int(b)) for b in flat], dtype=np.float64).reshape(np.shape(bits))
+
+
+def scores(keys, key_dtype: str, queries, q_dtype: str, metric: str = "cosine",
+           key_stride: int | None = None, d: int | None = None) -> np.ndarray:
+    """Exact similarity of every query to every key row: (Q, N) float64."""
+    keys = _raw(keys, key_dtype)
+    queries = _raw(queries, q_dtype)
+    n = keys.shape[0]
+    stride = keys.shape[1] if key_stride is None else key_stride
+    d = stride if d is None else d
+    q2 = queries.reshape(-1, d)
+    out = np.empty((q2.shape[0], n), dtype=np.float64)
+    rc = _load().oracle_scores(_ptr(keys), DTYPES[key_dtype], n, d, stride, _ptr(q2),
+                               DTYPES[q_dtype], q2.shape[0], METRICS[metric], _ptr(out))
+    if rc:
+        raise ValueError("oracle_scores rejected its arguments")
+    return out
+
+
+def topk(score_row: np.ndarray, k: int):
+    """Full sort by (score desc, index asc); first k (ids int64, scores f64)."""
+    s = np.ascontiguousarray(score_row, dtype=np.float64)
+    ids = np.empty(k, dtype=np.int64)
+    sc = np.empty(k, dtype=np.float64)
+    if _load().oracle_topk(_ptr(s), s.shape[0], k, _ptr(ids), _ptr(sc)):
+        raise ValueError("oracle_topk rejected its arguments")
+    return ids, sc
+
+
+def gather(spans: np.ndarray, span_len, ids: np.ndarray):
+    """Candidate draft batch of the given hits: (drafts[k, M] int32, len[k])."""
+    spans = np.ascontiguousarray(spans, dtype=np.int32)
+    max_span = spans.shape[1]
+    sl = None if span_len is None else np.ascontiguousarray(span_len, dtype=np.int32)
+    ids = np.ascontiguousarray(ids, dtype=np.int64)
+    k = ids.shape[0]
+    drafts = np.empty((k, max_span), dtype=np.int32)
+    dl = np.empty(k, dtype=np.int32)
+    if _load().oracle_gather(_ptr(spans), _ptr(sl), max_span, _ptr(ids), k, _ptr(drafts), _ptr(dl)):
+        raise ValueError("oracle_gather rejected its arguments")
+    return drafts, dl
+
+
+def retrieve(keys, key_dtype, queries, q_dtype, k, spans, span_len=None, metric="cosine"):
+    """Exact retrieval: per query the top-k (ids, scores) and gathered drafts."""
+    s = scores(keys, key_dtype, queries, q_dtype, metric)
+    out_ids, out_sc, out_dr, out_dl = [], [], [], []
+    for q in range(s.shape[0]):
+        ids, sc = topk(s[q], k)
+        dr, dl = gather(spans, span_len, ids)
+        out_ids.append(ids); out_sc.append(sc); out_dr.append(dr); out_dl.append(dl)
+    return np.stack(out_ids), np.stack(out_sc), np.stack(out_dr), np.stack(out_dl)
+
+
+def row_stats(row, dtype: str, tok: int):
+    """(argmax, entropy in nats, rank of tok) of one logit row."""
+    row = _raw(row, dtype)
+    y = ctypes.c_int32()
+    e = ctypes.c_double()
+    r = ctypes.c_int32()
+    if _load().oracle_row_stats(_ptr(row), DTYPES[dtype], row.shape[-1], tok,
+                                ctypes.byref(y), ctypes.byref(e), ctypes.byref(r)):
+        raise ValueError("oracle_row_stats rejected its arguments")
+    return y.value, e.value, r.value
+
+
+def soft_gate_verify(logits, dtype: str, drafts, draft_len=None, n_groups: int = 1,
+                     gamma: float = 0.05, topk: int = 3, window: int = 6, tau: int = 0,
+                     entropy_normalized: bool = True, vocab: int | None = None):
+    """Alg. 4 literally.  logits: (C, M, stride) array; drafts: (C, M) int32.
+
+    Returns a dict with accept_len (C,), best (n_groups,), gate_score (C, M),
+    masks (C, M) uint8, argmax (C, M), rank (C, M)."""
+    logits = _raw(logits, dtype)
+    drafts = np.ascontiguousarray(drafts, dtype=np.int32)
+    c, m = drafts.shape
+    stride = logits.shape[-1]
+    v = stride if vocab is None else vocab
+    dl = None if draft_len is None else np.ascontiguousarray(draft_len, dtype=np.int32)
+    acc = np.empty(c, dtype=np.int32)
+    best = np.empty(max(n_groups, 1), dtype=np.int32)
+    gs = np.empty((c, m), dtype=np.float64)
+    masks = np.empty((c, m), dtype=np.uint8)
+    am = np.empty((c, m), dtype=np.int32)
+    rk = np.empty((c, m), dtype=np.int32)
+    rc = _load().oracle_soft_gate_verify(
+        _ptr(logits), DTYPES[dtype], stride, _ptr(drafts), _ptr(dl), c, m, v, n_groups,
+        float(gamma), topk, window, tau, int(bool(entropy_normalized)),
+        _ptr(acc), _ptr(best), _ptr(gs), _ptr(masks), _ptr(am), _ptr(rk))
+    if rc:
+        raise ValueError("oracle_soft_gate_verify rejected its arguments")
+    return {"accept_len": acc, "best": best[:n_groups], "gate_score": gs, "masks": masks,
+            "argmax": am, "rank": rk}

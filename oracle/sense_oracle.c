@@ -1,0 +1,358 @@
+/*
+ * sense_oracle.c -- plain, slow, obviously-correct CPU reference for the
+ * SENSE retrieval + soft-gated evaluation hot path.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the checker, not the product: only
+ * the test-suite, the smoke check and the benchmark's CPU-baseline leg may
+ * load it.  It shares no source, header, table or helper with the HIP library
+ * and includes nothing from it.
+ *
+ * Every quantity is computed in IEEE double precision, following the paper's
+ * definitions literally:
+ *
+ *   Retrieval (Sec. 2.1 Eq. 3 "retriever R", Sec. 2.2 Eq. 7 "sim",
+ *   Alg. 2 "L2Norm" and "FAISS" steps):  the exact similarity of the query to
+ *   every stored key (inner product, or cosine = inner product of the
+ *   L2-normalised vectors), then a FULL sort of all N rows by
+ *   (score descending, row index ascending) and the first k rows; the stored
+ *   continuation span of each hit is gathered into the candidate batch.
+ *   The paper's own retriever is an approximate (IVF-PQ) index; the exact
+ *   scan is the plain definition that index approximates.
+ *
+ *   Verification (Sec. 2.3 Eqs. 11-17, Alg. 4 "SGE"): per candidate c and
+ *   draft position j, the greedy token Y = argmax (first occurrence), the
+ *   exact-match mask, softmax entropy (optionally divided by log|V|) against
+ *   gamma, top-k membership of the draft token (full stable sort of the
+ *   vocabulary), the padded mismatch window of width W, the final gate G,
+ *   the leading run of accepted positions and the best candidate per group.
+ *
+ * Readings taken where the paper is silent or inconsistent (each one is also
+ * listed with its reason in the design notes of the repository):
+ *   - entropy is normalised by ln|V| when entropy_normalized != 0 (Alg. 4),
+ *     raw nats otherwise (Eq. 12's text form);
+ *   - softmax is applied to raw logits at temperature 1;
+ *   - top-k ties are broken by lower vocabulary index; argmax takes the first
+ *     maximum; the best candidate is the first one with the largest length;
+ *   - the look-ahead window of position j is the W positions strictly after
+ *     j, the draft right-padded with W mismatches (Alg. 4's Pad + Conv1D +
+ *     [1:M+1] slice); B_con = (R <= tau), tau = 0 being Alg. 4's "R = 0";
+ *   - positions j >= draft_len[c] are rejected and count as mismatches;
+ *   - a draft id outside [0, V) matches nothing and is in no top-k set;
+ *   - accept_len is the count of leading accepted positions n in [0, len];
+ *     Alg. 4's L equals n - 1;
+ *   - retrieval ties go to the lower row index; NaN scores sort last; a
+ *     zero-norm key or query has cosine 0.
+ *
+ * dtype codes: 0 = float32, 1 = IEEE binary16, 2 = bfloat16.
+ * All functions return 0 on success, -1 on a bad argument.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+enum { OR_F32 = 0, OR_F16 = 1, OR_BF16 = 2 };
+
+/* IEEE 754 binary16: 1 sign bit, 5 exponent bits (bias 15), 10 fraction bits.
+ * Written from the format's definition; every binary16 value is exact in
+ * double. */
+double oracle_decode_f16(uint16_t h)
+{
+    int sign = (h >> 15) & 1;
+    int e = (h >> 10) & 0x1f;
+    int f = h & 0x3ff;
+    double v;
+    if (e == 0)
+        v = ldexp((double)f, -24);               /* zero / subnormal */
+    else if (e == 31)
+        v = (f == 0) ? INFINITY : NAN;           /* inf / NaN */
+    else
+        v = ldexp((double)(1024 + f), e - 25);   /* (1 + f/1024) * 2^(e-15) */
+    return sign ? -v : v;
+}
+
+/* bfloat16 is the upper half of an IEEE binary32 pattern. */
+double oracle_decode_bf16(uint16_t b)
+{
+    uint32_t u = ((uint32_t)b) << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return (double)f;
+}
+
+static double elem(const void *base, int dtype, int64_t i)
+{
+    switch (dtype) {
+    case OR_F32: return (double)((const float *)base)[i];
+    case OR_F16: return oracle_decode_f16(((const uint16_t *)base)[i]);
+    default:     return oracle_decode_bf16(((const uint16_t *)base)[i]);
+    }
+}
+
+static int dtype_ok(int dt) { return dt == OR_F32 || dt == OR_F16 || dt == OR_BF16; }
+
+/* ---------------------------------------------------------------- retrieval */
+
+/* scores[q * n + i] = sim(query q, key row i) for rows [0, n) of the block
+ * given.  metric 0 = inner product, 1 = cosine.  Rows are independent, so the
+ * row loop may run on several threads; each row's sum is taken in element
+ * order. */
+int oracle_scores(const void *keys, int key_dtype, int64_t n, int32_t d,
+                  int64_t key_stride, const void *queries, int q_dtype,
+                  int32_t n_queries, int metric, double *out_scores)
+{
+    if (!keys || !queries || !out_scores || n < 0 || d < 1 || key_stride < d ||
+        n_queries < 1 || !dtype_ok(key_dtype) || !dtype_ok(q_dtype) ||
+        (metric != 0 && metric != 1))
+        return -1;
+    for (int32_t q = 0; q < n_queries; ++q) {
+        double qn2 = 0.0;
+        for (int32_t t = 0; t < d; ++t) {
+            double a = elem(queries, q_dtype, (int64_t)q * d + t);
+            qn2 += a * a;
+        }
+        double qnorm = sqrt(qn2);
+#pragma omp parallel for schedule(static)
+        for (int64_t i = 0; i < n; ++i) {
+            double dot = 0.0, kn2 = 0.0;
+            for (int32_t t = 0; t < d; ++t) {
+                double kv = elem(keys, key_dtype, i * key_stride + t);
+                double qv = elem(queries, q_dtype, (int64_t)q * d + t);
+                dot += qv * kv;
+                kn2 += kv * kv;
+            }
+            double s;
+            if (metric == 0) {
+                s = dot;
+            } else {
+                double knorm = sqrt(kn2);
+                s = (knorm == 0.0 || qnorm == 0.0) ? 0.0 : dot / (qnorm * knorm);
+            }
+            out_scores[(int64_t)q * n + i] = s;
+        }
+    }
+    return 0;
+}
+
+typedef struct { double s; int64_t i; } scored_row;
+
+/* (score descending, index ascending); NaN after every number. */
+static int cmp_rows(const void *pa, const void *pb)
+{
+    const scored_row *a = (const scored_row *)pa, *b = (const scored_row *)pb;
+    int an = isnan(a->s), bn = isnan(b->s);
+    if (an != bn) return an ? 1 : -1;
+    if (!an) {
+        if (a->s > b->s) return -1;
+        if (a->s < b->s) return 1;
+    }
+    return (a->i < b->i) ? -1 : (a->i > b->i);
+}
+
+/* Full sort of all n scores, first k kept.  k may exceed n: the tail is
+ * filled with id -1 and score NaN. */
+int oracle_topk(const double *scores, int64_t n, int32_t k, int64_t *out_ids,
+                double *out_scores)
+{
+    if (!scores || !out_ids || !out_scores || n < 0 || k < 0) return -1;
+    scored_row *all = (scored_row *)malloc(sizeof(scored_row) * (size_t)(n > 0 ? n : 1));
+    if (!all) return -1;
+    for (int64_t i = 0; i < n; ++i) { all[i].s = scores[i]; all[i].i = i; }
+    qsort(all, (size_t)n, sizeof(scored_row), cmp_rows);
+    for (int32_t r = 0; r < k; ++r) {
+        if (r < n) { out_ids[r] = all[r].i; out_scores[r] = all[r].s; }
+        else { out_ids[r] = -1; out_scores[r] = NAN; }
+    }
+    free(all);
+    return 0;
+}
+
+/* drafts[r][j] = spans[ids[r]][j] for j < span_len[ids[r]], else -1.
+ * span_len may be NULL (every span is max_span long).  An id of -1 yields an
+ * empty draft. */
+int oracle_gather(const int32_t *spans, const int32_t *span_len, int32_t max_span,
+                  const int64_t *ids, int32_t k, int32_t *out_drafts,
+                  int32_t *out_draft_len)
+{
+    if (!spans || !ids || !out_drafts || !out_draft_len || max_span < 1 || k < 0)
+        return -1;
+    for (int32_t r = 0; r < k; ++r) {
+        int64_t id = ids[r];
+        int32_t len = 0;
+        if (id >= 0) {
+            len = span_len ? span_len[id] : max_span;
+            if (len < 0) len = 0;
+            if (len > max_span) len = max_span;
+        }
+        for (int32_t j = 0; j < max_span; ++j)
+            out_drafts[(int64_t)r * max_span + j] =
+                (j < len) ? spans[id * max_span + j] : -1;
+        out_draft_len[r] = len;
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------- verification */
+
+typedef struct { double x; int32_t v; } vocab_entry;
+
+static int cmp_vocab(const void *pa, const void *pb)
+{
+    const vocab_entry *a = (const vocab_entry *)pa, *b = (const vocab_entry *)pb;
+    if (a->x > b->x) return -1;
+    if (a->x < b->x) return 1;
+    return (a->v < b->v) ? -1 : (a->v > b->v);
+}
+
+/* Statistics of one logit row x[0..V) judged against draft token tok:
+ *   argmax (first occurrence), entropy of softmax(x) in nats,
+ *   rank = position of tok in the stable sort by (x desc, v asc) (V if tok is
+ *   outside [0, V)).  tok is in the top-k set iff rank < k. */
+int oracle_row_stats(const void *row, int dtype, int32_t vocab, int32_t tok,
+                     int32_t *out_argmax, double *out_entropy, int32_t *out_rank)
+{
+    if (!row || vocab < 1 || !dtype_ok(dtype)) return -1;
+    vocab_entry *e = (vocab_entry *)malloc(sizeof(vocab_entry) * (size_t)vocab);
+    if (!e) return -1;
+    int32_t y = 0;
+    double m = elem(row, dtype, 0);
+    for (int32_t v = 0; v < vocab; ++v) {
+        e[v].x = elem(row, dtype, v);
+        e[v].v = v;
+        if (e[v].x > m) { m = e[v].x; y = v; }
+    }
+    /* softmax p_v = exp(x_v - m) / sum_u exp(x_u - m); entropy -sum p ln p */
+    double z = 0.0;
+    for (int32_t v = 0; v < vocab; ++v) z += exp(e[v].x - m);
+    double ent = 0.0;
+    for (int32_t v = 0; v < vocab; ++v) {
+        double p = exp(e[v].x - m) / z;
+        if (p > 0.0) ent -= p * log(p);
+    }
+    int32_t rank = vocab;
+    if (tok >= 0 && tok < vocab) {
+        qsort(e, (size_t)vocab, sizeof(vocab_entry), cmp_vocab);
+        for (int32_t r = 0; r < vocab; ++r)
+            if (e[r].v == tok) { rank = r; break; }
+    }
+    free(e);
+    if (out_argmax) *out_argmax = y;
+    if (out_entropy) *out_entropy = ent;
+    if (out_rank) *out_rank = rank;
+    return 0;
+}
+
+/* Soft-gated evaluation of n_cand drafts (row-major n_cand x max_len) against
+ * the aligned logits: row (c, j) starts at logits + (c*max_len + j)*row_stride
+ * and predicts drafts[c][j].  draft_len may be NULL (all max_len).  Rows at
+ * j >= draft_len[c] are never read.
+ *
+ * Outputs (NULL allowed for the optional ones):
+ *   accept_len[c]  leading accepted count n_c
+ *   best[g]        index within group g of its first candidate of largest n
+ *   gate_score[c*max_len + j]  the value compared with gamma (0 beyond len)
+ *   masks[c*max_len + j]       em | ent<<1 | topk<<2 | con<<3 | G<<4
+ *   argmax / rank  per position (-1 / V beyond len) */
+int oracle_soft_gate_verify(const void *logits, int logits_dtype, int64_t row_stride,
+                            const int32_t *drafts, const int32_t *draft_len,
+                            int32_t n_cand, int32_t max_len, int32_t vocab,
+                            int32_t n_groups, double gamma, int32_t topk,
+                            int32_t window, int32_t tau, int32_t entropy_normalized,
+                            int32_t *out_accept_len, int32_t *out_best,
+                            double *out_gate_score, uint8_t *out_masks,
+                            int32_t *out_argmax, int32_t *out_rank)
+{
+    if (n_cand < 0 || max_len < 1 || vocab < 1 || row_stride < vocab ||
+        topk < 1 || window < 0 || tau < 0 || !dtype_ok(logits_dtype) ||
+        (n_cand > 0 && (!logits || !drafts || !out_accept_len)))
+        return -1;
+    if (n_cand > 0 && (n_groups < 1 || n_cand % n_groups != 0)) return -1;
+    const int64_t npos = (int64_t)n_cand * max_len;
+    uint8_t *em = (uint8_t *)calloc((size_t)(npos > 0 ? npos : 1), 1);
+    uint8_t *ent = (uint8_t *)calloc((size_t)(npos > 0 ? npos : 1), 1);
+    uint8_t *tk = (uint8_t *)calloc((size_t)(npos > 0 ? npos : 1), 1);
+    double *gs = (double *)calloc((size_t)(npos > 0 ? npos : 1), sizeof(double));
+    int32_t *am = (int32_t *)malloc(sizeof(int32_t) * (size_t)(npos > 0 ? npos : 1));
+    int32_t *rk = (int32_t *)malloc(sizeof(int32_t) * (size_t)(npos > 0 ? npos : 1));
+    int32_t *lens = (int32_t *)malloc(sizeof(int32_t) * (size_t)(n_cand > 0 ? n_cand : 1));
+    if (!em || !ent || !tk || !gs || !am || !rk || !lens) {
+        free(em); free(ent); free(tk); free(gs); free(am); free(rk); free(lens);
+        return -1;
+    }
+    const double log_v = log((double)vocab);
+    for (int32_t c = 0; c < n_cand; ++c) {
+        int32_t len = draft_len ? draft_len[c] : max_len;
+        if (len < 0) len = 0;
+        if (len > max_len) len = max_len;
+        lens[c] = len;
+    }
+
+    /* Per-position masks: exact match, entropy gate, top-k membership. */
+    int err = 0;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t p = 0; p < npos; ++p) {
+        int32_t c = (int32_t)(p / max_len), j = (int32_t)(p % max_len);
+        am[p] = -1;
+        rk[p] = vocab;
+        if (j >= lens[c]) continue;              /* beyond the draft: rejected */
+        int32_t tok = drafts[p];
+        int32_t y, r;
+        double e;
+        const char *row = (const char *)logits +
+                          (size_t)p * (size_t)row_stride *
+                              (logits_dtype == OR_F32 ? 4 : 2);
+        if (oracle_row_stats(row, logits_dtype, vocab, tok, &y, &e, &r)) { err = 1; continue; }
+        double g = entropy_normalized ? e / log_v : e;
+        am[p] = y;
+        rk[p] = r;
+        em[p] = (tok == y);                      /* Y = argmax; B_em = I(D = Y) */
+        ent[p] = (g > gamma);                    /* strict */
+        tk[p] = (r < topk);                      /* D in TopK(P, k) */
+        gs[p] = g;
+    }
+    if (err) {
+        free(em); free(ent); free(tk); free(gs); free(am); free(rk); free(lens);
+        return -1;
+    }
+
+    /* Per candidate: padded mismatch window, gate, leading accepted run. */
+    int32_t padded_len = max_len + window;
+    uint8_t *bbar = (uint8_t *)malloc((size_t)padded_len);
+    for (int32_t c = 0; c < n_cand; ++c) {
+        /* B-bar = Pad(1 - B_em, (0, W), value 1) */
+        for (int32_t j = 0; j < padded_len; ++j)
+            bbar[j] = (j < max_len) ? (uint8_t)(1 - em[(int64_t)c * max_len + j]) : 1;
+        int32_t n = 0, still = 1;
+        for (int32_t j = 0; j < max_len; ++j) {
+            int64_t p = (int64_t)c * max_len + j;
+            /* R[j] = sum over the W positions after j */
+            int32_t r = 0;
+            for (int32_t u = 1; u <= window; ++u) r += bbar[j + u];
+            int con = (r <= tau);
+            int g = (j < lens[c]) &&
+                    (em[p] || (ent[p] && (tk[p] || con)));
+            if (still && g) ++n; else still = 0;   /* sum of cumprod(G) */
+            if (out_masks)
+                out_masks[p] = (uint8_t)(em[p] | (ent[p] << 1) | (tk[p] << 2) |
+                                         (con << 3) | (g << 4));
+            if (out_gate_score) out_gate_score[p] = gs[p];
+            if (out_argmax) out_argmax[p] = am[p];
+            if (out_rank) out_rank[p] = rk[p];
+        }
+        out_accept_len[c] = n;
+    }
+    free(bbar);
+
+    /* Best candidate of each group: first maximiser of n. */
+    if (out_best && n_cand > 0) {
+        int32_t gsz = n_cand / n_groups;
+        for (int32_t g = 0; g < n_groups; ++g) {
+            int32_t b = 0;
+            for (int32_t i = 1; i < gsz; ++i)
+                if (out_accept_len[g * gsz + i] > out_accept_len[g * gsz + b]) b = i;
+            out_best[g] = b;
+        }
+    }
+    free(em); free(ent); free(tk); free(gs); free(am); free(rk); free(lens);
+    return 0;
+}
