@@ -307,7 +307,7 @@ int oracle_soft_gate_verify(const void *logits, int logits_dtype, int64_t row_st
         rk[p] = r;
         em[p] = (tok == y);                      /* Y = argmax; B_em = I(D = Y) */
         ent[p] = (g > gamma);                    /* strict */
-        tk[p] = (r < topk);                      /* D in TopK(P, k) */
+        tk[p] = (r < vocab) && (r < topk);       /* D in TopK(P, k): a vocabulary index */
         gs[p] = g;
     }
     if (err) {

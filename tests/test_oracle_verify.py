@@ -182,11 +182,12 @@ def test_out_of_range_draft_ids_match_nothing():
     rng = np.random.default_rng(6)
     logits, drafts = _structured(rng, 3, 4, 40)
     drafts[0, 0], drafts[1, 1], drafts[2, 3] = -1, 40, 10**6
-    out = oracle.soft_gate_verify(logits, "f32", drafts, topk=40)
-    for c, j in ((0, 0), (1, 1), (2, 3)):
-        assert out["rank"][c, j] == 40
-        assert out["masks"][c, j] & (EM | TOPK) == 0
-    assert out["accept_len"][0] == 0
+    for k in (40, 45):                          # k >= V: every real token is in the set
+        out = oracle.soft_gate_verify(logits, "f32", drafts, topk=k)
+        for c, j in ((0, 0), (1, 1), (2, 3)):
+            assert out["rank"][c, j] == 40
+            assert out["masks"][c, j] & (EM | TOPK) == 0
+        assert out["accept_len"][0] == 0
 
 
 def test_positions_beyond_draft_length_are_rejected_and_never_read():
