@@ -1,0 +1,237 @@
+#!/usr/bin/env python3
+"""Throughput of the SENSE retrieval + soft-gated evaluation hot path on one
+MI355X.
+
+One step = one sense_retrieve over the whole datastore (similarity scan,
+top-k, gather of the continuations) followed by one sense_soft_gate_verify
+of the retrieved drafts of the verified queries against their aligned
+logits.  Inputs are synthetic (see paper_2606_00021_amd/synth.py) and
+resident in HBM before the timed region starts.
+
+Prints ONE JSON line on stdout; progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0   # MI355X HBM3E, published
+METRIC = "retrieval+verify queries/sec and achieved HBM GB/s (% of peak) at N=1M, d=4096"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default=None, help="workload name (default: the headline)")
+    ap.add_argument("--seed", type=int, default=1003)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="approximate CPU time spent timing the oracle baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def traffic_from_profiles(workload: str):
+    """Measured HBM bytes per scan launch, if a counter summary for this
+    workload and the current scan kernel is committed under profiles/."""
+    path = os.path.join(ROOT, "profiles", f"scan_traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path))
+    except Exception:
+        return None
+    src = os.path.join(ROOT, "paper_2606_00021_amd", "csrc", "scan.hip")
+    import hashlib
+    digest = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    if rec.get("scan_source_sha256_16") != digest:
+        return None       # the kernel changed since the counters were taken
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline(w, ds, q, logits, drafts, budget_s: float):
+    """The oracle as it stands, timed on this host on a bounded sample of the
+    same workload, scaled to one query (its scan + sort + gather + verify)."""
+    import numpy as np
+    import torch
+
+    import oracle
+
+    cores = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or os.cpu_count()
+    kb_dt = w.key_dtype
+    qh = q.cpu().numpy()
+    # Calibrate the scan on a small block, then size the sample to the budget.
+    cal = 2048
+    keys_cal = ds.keys[:cal].cpu().view(torch.int16).numpy().view(np.uint16)
+    t0 = time.perf_counter()
+    oracle.scores(keys_cal, kb_dt, qh[:1], "f32", metric=w.metric)
+    per_row = (time.perf_counter() - t0) / cal
+    rows = int(min(w.n, max(cal, 0.6 * budget_s / max(per_row, 1e-9))))
+    keys_s = ds.keys[:rows].cpu().view(torch.int16).numpy().view(np.uint16)
+    t0 = time.perf_counter()
+    oracle.scores(keys_s, kb_dt, qh[:1], "f32", metric=w.metric)
+    t_scan_row = (time.perf_counter() - t0) / rows
+    # Full sort of N scores (the oracle's top-k) and the gather.
+    rng = np.random.default_rng(0)
+    fake = rng.standard_normal(w.n)
+    t0 = time.perf_counter()
+    ids, _ = oracle.topk(fake, w.k)
+    oracle.gather(ds.spans[:1024].cpu().numpy(), None, ids % 1024)
+    t_sort = time.perf_counter() - t0
+    # Verify: a sample of candidates, scaled per position.
+    dt_name = {torch.float32: "f32", torch.float16: "f16", torch.bfloat16: "bf16"}[logits.dtype]
+    c_s = max(1, min(drafts.shape[0], 8))
+    lg = logits[:c_s].cpu()
+    lg = lg.view(torch.int16).numpy().view(np.uint16) if dt_name != "f32" else lg.numpy()
+    t0 = time.perf_counter()
+    oracle.soft_gate_verify(lg, dt_name, drafts[:c_s].cpu().numpy())
+    t_verify_pos = (time.perf_counter() - t0) / (c_s * drafts.shape[1])
+    pos_per_query = w.n_cand * w.span / w.n_queries
+    t_query = t_scan_row * w.n + t_sort + t_verify_pos * pos_per_query
+    return {
+        "value": 1.0 / t_query,
+        "unit": "queries/s",
+        "cores": cores,
+        "kind": "oracle",
+        "sample": (f"fp64 oracle on host: scan of {rows} of {w.n} rows x d={w.d} "
+                   f"({t_scan_row * 1e6:.3f} us/row), full sort of {w.n} scores "
+                   f"({t_sort:.3f} s), verify of {c_s}x{drafts.shape[1]} positions x "
+                   f"V={w.vocab} ({t_verify_pos * 1e3:.2f} ms/position); scaled to one "
+                   f"query = {w.n} rows + sort + {pos_per_query:.0f} positions"),
+    }
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(the row-sharded design is described in DESIGN.md); run with --gpus 1",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2606_00021_amd import sense, synth
+
+    name = args.workload or synth.HEADLINE
+    w = synth.WORKLOADS[name]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    log(f"[bench] workload {name}: n={w.n} d={w.d} {w.key_dtype} Q={w.n_queries} k={w.k} "
+        f"M={w.span} V={w.vocab} {w.logits_dtype}")
+    t0 = time.perf_counter()
+    ds = synth.make_datastore(w, args.seed, dev)
+    q, _ = synth.make_queries(w, ds, args.seed)
+    index = sense.sense_build_index(ds.keys, ds.spans, ds.span_len, metric=w.metric)
+    nq, k, m = w.n_queries, w.k, w.span
+    ws_r = torch.empty(max(1, sense.sense_retrieve_workspace_size(index, nq, k)),
+                       dtype=torch.uint8, device=dev)
+    outs = (torch.empty((nq, k), dtype=torch.int64, device=dev),
+            torch.empty((nq, k), dtype=torch.float32, device=dev),
+            torch.empty((nq, k, m), dtype=torch.int32, device=dev),
+            torch.empty((nq, k), dtype=torch.int32, device=dev))
+    sense.sense_retrieve(index, q, k, workspace=ws_r, out=outs)
+    vq = w.verify_queries
+    drafts = outs[2][:vq].view(vq * k, m)
+    dlen = outs[3][:vq].view(vq * k)
+    logits = synth.make_logits(w, drafts, args.seed)
+    c = vq * k
+    ws_v = torch.empty(max(1, sense.sense_soft_gate_verify_workspace_size(c, m, w.vocab)),
+                       dtype=torch.uint8, device=dev)
+    out_v = {"accept_len": torch.empty(c, dtype=torch.int32, device=dev),
+             "best": torch.empty(vq, dtype=torch.int32, device=dev)}
+    torch.cuda.synchronize()
+    log(f"[bench] setup {time.perf_counter() - t0:.1f} s")
+
+    def step():
+        sense.sense_retrieve(index, q, k, workspace=ws_r, out=outs)
+        sense.sense_soft_gate_verify(logits, drafts, dlen, n_groups=vq, gamma=0.05, topk=3,
+                                     window=6, tau=0, workspace=ws_v, out=out_v)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    K = args.steps
+    ev = {t: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(K)] for t in ("scan", "topk", "verify")}
+    timer_id = {"scan": sense.SENSE_TIMER_SCAN, "topk": sense.SENSE_TIMER_TOPK,
+                "verify": sense.SENSE_TIMER_VERIFY}
+    t_begin = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t_begin.record()
+    for i in range(K):
+        for t in ev:
+            sense.sense_set_timer_events(timer_id[t], *ev[t][i])
+        step()
+    t_end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    for t in ev:
+        sense.sense_set_timer_events(timer_id[t], None, None)
+    ms_step = t_begin.elapsed_time(t_end) / K
+    dur = {t: sum(a.elapsed_time(b) for a, b in ev[t]) / K for t in ev}
+    log(f"[bench] {K} steps: {ms_step:.4f} ms/step (wall {wall * 1e3 / K:.4f} ms/step); "
+        f"scan {dur['scan']:.4f} ms, topk {dur['topk']:.4f} ms, verify {dur['verify']:.4f} ms")
+
+    # Algorithmic bytes: every key once (+ the fp32 inverse-norm table for
+    # cosine), the gathered continuations, and every live logit row once.
+    cos_extra = 4 * w.n if w.metric == "cosine" else 0
+    scan_bytes = w.n * w.d * 2 + cos_extra
+    gather_bytes = nq * k * m * 4
+    live = int(dlen.clamp(0, m).sum().item())
+    verify_bytes = live * w.vocab * (4 if w.logits_dtype == "f32" else 2)
+    step_bytes = scan_bytes + gather_bytes + verify_bytes
+    scan_gbps = scan_bytes / (dur["scan"] * 1e-3) / 1e9
+    res = {
+        "metric": METRIC,
+        "value": nq / (ms_step * 1e-3),
+        "unit": "queries/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": name, "n": w.n, "d": w.d, "key_dtype": w.key_dtype,
+                   "n_queries": nq, "k": k, "span": m, "vocab": w.vocab,
+                   "logits_dtype": w.logits_dtype, "verify_candidates": c,
+                   "metric": w.metric, "parallelism": "single-gpu"},
+        "hbm_gbps": step_bytes / (ms_step * 1e-3) / 1e9,
+        "hbm_frac": step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+        "scan_ms": dur["scan"],
+        "topk_ms": dur["topk"],
+        "verify_ms": dur["verify"],
+        "verify_gbps": verify_bytes / (dur["verify"] * 1e-3) / 1e9 if dur["verify"] > 0 else None,
+        "roofline": {"bound": "hbm", "kernel": "scan_gemv_kernel", "achieved": scan_gbps,
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": scan_gbps / HBM_PEAK_GBPS,
+                     "traffic": traffic_from_profiles(name)},
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the oracle on the host (cpu_baseline)")
+        t0 = time.perf_counter()
+        res["cpu_baseline"] = cpu_baseline(w, ds, q, logits, drafts, args.cpu_seconds)
+        log(f"[bench] cpu_baseline took {time.perf_counter() - t0:.1f} s")
+    index.close()
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

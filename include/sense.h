@@ -1,0 +1,245 @@
+/*
+ * sense.h -- C ABI of the SENSE retrieval + soft-gated evaluation hot path on
+ * one AMD Instinct MI355X (gfx950).
+ *
+ * The method (SENSE: Semantic Embedding Navigation with Soft-gated
+ * Evaluation) drafts tokens for speculative decoding by retrieving stored
+ * continuations whose hidden-state keys are most similar to the target
+ * model's current hidden state, then accepts a prefix of each draft with a
+ * cascade of masks over the target model's logits.  This library implements
+ * the data-parallel part of that loop:
+ *
+ *   sense_build_index       the datastore C_db of (key, continuation) pairs
+ *                           (Sec. 2.1 Eq. 2; Sec. 2.2 Eq. 6)
+ *   sense_retrieve          exact similarity scan + per-query top-k + gather
+ *                           of each hit's continuation into a draft batch
+ *                           (Sec. 2.1 Eq. 3; Sec. 2.2 Eqs. 7-8; Alg. 2's
+ *                           L2Norm and retrieval steps)
+ *   sense_soft_gate_verify  soft-gated evaluation of a draft batch against
+ *                           aligned logits: accepted prefix length per draft
+ *                           and the best draft per group
+ *                           (Sec. 2.3 Eqs. 11-17; Alg. 4)
+ *
+ * Conventions shared by every entry point
+ *   - Pointers named keys, spans, span_len, queries, logits, drafts,
+ *     draft_len, workspace and out_* are DEVICE pointers (HBM of the current
+ *     HIP device).  Descriptor structs and size_t* results are host memory.
+ *   - `stream` is a hipStream_t (NULL = the legacy default stream).  All
+ *     device work is enqueued on it and the call returns before it finishes:
+ *     outputs are valid once the stream is synchronised, and inputs must stay
+ *     alive and unchanged until then.
+ *   - Arguments are validated on the host before anything is enqueued; a
+ *     rejected call enqueues nothing and writes no output.  No C++ exception
+ *     crosses this boundary.  sense_last_error_message() describes the last
+ *     failure on the calling thread.
+ *   - Conditions inside the data are defined results, not errors (a draft id
+ *     outside [0, V), a zero-norm key, ties).
+ *   - The library never synchronises the device except in
+ *     sense_destroy_index (which frees device memory).
+ */
+#ifndef SENSE_H_
+#define SENSE_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    SENSE_OK = 0,
+    SENSE_ERR_INVALID_ARGUMENT = 1, /* NULL pointer, size out of range, mismatch */
+    SENSE_ERR_MISALIGNED = 2,       /* pointer or stride breaks the 16-byte layout */
+    SENSE_ERR_UNSUPPORTED = 3,      /* legal but outside what is implemented */
+    SENSE_ERR_OUT_OF_MEMORY = 4,    /* a device allocation failed */
+    SENSE_ERR_WORKSPACE = 5,        /* workspace NULL or smaller than required */
+    SENSE_ERR_HIP = 6               /* the HIP runtime reported an error */
+} sense_status_t;
+
+typedef enum { SENSE_F32 = 0, SENSE_F16 = 1, SENSE_BF16 = 2 } sense_dtype_t;
+
+/* Similarity of Sec. 2.2 Eq. 7.  COSINE is the inner product of the
+ * L2-normalised query and key (the paper L2-normalises both before search);
+ * the key norms are those of the stored fp16/bf16 values. */
+typedef enum { SENSE_METRIC_IP = 0, SENSE_METRIC_COSINE = 1 } sense_metric_t;
+
+/* Index flag: keep an owned, re-laid-out copy of the keys instead of
+ * borrowing the caller's buffer (needed when the caller's row stride or base
+ * address breaks the 16-byte layout). */
+#define SENSE_INDEX_COPY_KEYS 1u
+
+typedef struct sense_index sense_index_t; /* opaque host handle */
+
+/* Datastore descriptor (Sec. 2.1 Eq. 2: pairs (k_i, c_i) with |c_i| <= M).
+ *   keys       N x key_stride elements of key_dtype (F16 or BF16), row-major,
+ *              row i's d elements contiguous.  Borrowed: must outlive the
+ *              index unless SENSE_INDEX_COPY_KEYS.  Without the copy flag the
+ *              base must be 16-byte aligned and key_stride % 8 == 0.
+ *   n          number of rows, 1 <= n <= 2^31 - 1.
+ *   d          key dimension, 1 <= d <= 8192 (the hidden sizes of the target
+ *              models); d % 8 == 0.
+ *   key_stride elements between consecutive rows, >= d.
+ *   spans      N x max_span int32 token ids: row i is the continuation c_i
+ *              stored with key i.  Borrowed.
+ *   max_span   M, 1 <= M <= 64.
+ *   span_len   N int32 lengths in [0, M] (values outside are clamped), or
+ *              NULL when every continuation is M tokens long.  Borrowed.
+ *   metric     similarity used by sense_retrieve.
+ *   flags      0 or SENSE_INDEX_COPY_KEYS. */
+typedef struct {
+    const void *keys;
+    sense_dtype_t key_dtype;
+    int64_t n;
+    int32_t d;
+    int64_t key_stride;
+    const int32_t *spans;
+    int32_t max_span;
+    const int32_t *span_len;
+    sense_metric_t metric;
+    uint32_t flags;
+} sense_index_desc_t;
+
+/* Build an index over the datastore.  For COSINE it computes the fp32 side
+ * table 1/||k_i|| (0 for a zero row) with one read of the keys, enqueued on
+ * `stream`.  The index owns only that table (N * 4 bytes) and, with
+ * SENSE_INDEX_COPY_KEYS, the key copy.  *out receives the handle; it is
+ * immutable afterwards, so concurrent sense_retrieve calls on different
+ * streams with separate workspaces are safe.
+ * Errors: INVALID_ARGUMENT (NULL desc/out/keys/spans, sizes out of range,
+ * non-key dtype), MISALIGNED, OUT_OF_MEMORY, HIP. */
+sense_status_t sense_build_index(const sense_index_desc_t *desc, void *stream,
+                                 sense_index_t **out);
+
+/* Free the index and the device memory it owns (synchronises the device
+ * first, so in-flight work that reads it completes).  NULL is a no-op. */
+sense_status_t sense_destroy_index(sense_index_t *index);
+
+/* Shape queries of an index (host values; any out pointer may be NULL). */
+sense_status_t sense_index_info(const sense_index_t *index, int64_t *n, int32_t *d,
+                                int32_t *max_span, sense_metric_t *metric,
+                                sense_dtype_t *key_dtype);
+
+/* Bytes of device workspace sense_retrieve needs for these sizes. */
+sense_status_t sense_retrieve_workspace_size(const sense_index_t *index, int32_t n_queries,
+                                             int32_t k, size_t *bytes);
+
+/* Retrieval (Sec. 2.1 Eq. 3; Sec. 2.2 Eqs. 7-8; Alg. 2's L2Norm and search
+ * steps), exact: for each query q,
+ *   s[q, i] = sum_t q_t K[i, t]                    (IP)
+ *   s[q, i] = that / (||q|| ||K_i||), 0 if a norm is 0   (COSINE)
+ * accumulated in fp32 from the stored fp16/bf16 keys and the query as given;
+ * the k rows with the largest s in the order (score desc, row index asc),
+ * and their continuations.
+ *   queries      n_queries x d, dtype q_dtype (F32, or the key dtype),
+ *                row-major, 16-byte aligned.
+ *   n_queries    >= 1.   k: 1 <= k <= min(n, 1024).
+ *   out_ids      n_queries x k int64 row ids (required).
+ *   out_scores   n_queries x k fp32 scores, or NULL.
+ *   out_drafts   n_queries x k x max_span int32: spans[id][j] for
+ *                j < span_len[id], -1 after; or NULL.
+ *   out_draft_len n_queries x k int32 span lengths, or NULL.
+ *   workspace    device scratch of at least sense_retrieve_workspace_size
+ *                bytes, 256-byte aligned; its contents are not preserved.
+ * Errors: INVALID_ARGUMENT, UNSUPPORTED (k > 1024), MISALIGNED,
+ * WORKSPACE, HIP. */
+sense_status_t sense_retrieve(const sense_index_t *index, const void *queries,
+                              sense_dtype_t q_dtype, int32_t n_queries, int32_t k,
+                              int64_t *out_ids, float *out_scores, int32_t *out_drafts,
+                              int32_t *out_draft_len, void *workspace,
+                              size_t workspace_bytes, void *stream);
+
+/* Soft-gate hyper-parameters (Alg. 4 inputs; Sec. 2.3; defaults of the
+ * paper's experiments: gamma 0.05, top-k 3, W 6).
+ *   gamma              entropy threshold: B_ent = I(E' > gamma)
+ *   topk               k of the top-k membership mask, >= 1
+ *   window             W of the look-ahead window, 0 <= W <= 64
+ *   tau                window tolerance: B_con = I(R <= tau), tau >= 0
+ *                      (0 is Alg. 4's R = 0)
+ *   entropy_normalized 1: E' = E / ln|V| (Alg. 4); 0: E' = E in nats. */
+typedef struct {
+    float gamma;
+    int32_t topk;
+    int32_t window;
+    int32_t tau;
+    int32_t entropy_normalized;
+} sense_gate_params_t;
+
+/* Bytes of device workspace sense_soft_gate_verify needs for these sizes. */
+sense_status_t sense_soft_gate_verify_workspace_size(int32_t n_cand, int32_t max_len,
+                                                     int32_t vocab, size_t *bytes);
+
+/* Soft-gated evaluation (Sec. 2.3 Eqs. 11-17; Alg. 4) of n_cand drafts.
+ *   logits     n_cand x max_len rows of row_stride elements (F32, F16 or
+ *              BF16); row (c, j) starts at element (c*max_len + j)*row_stride
+ *              and is the target's distribution PREDICTING drafts[c][j] (the
+ *              aligned rows of Sec. 2.2: row 0 of every draft is the shared
+ *              distribution at the current position).  Only rows with
+ *              j < draft_len[c] are read.  Vector loads are used when the
+ *              base is 16-byte aligned and row_stride*elem_size % 16 == 0.
+ *   row_stride elements between rows, >= vocab.
+ *   drafts     n_cand x max_len int32 token ids.
+ *   draft_len  n_cand int32 in [0, max_len] (clamped), or NULL (= max_len).
+ *   n_cand >= 0; 1 <= max_len <= 64; vocab >= 1; n_groups >= 1 divides
+ *   n_cand: candidates [g*n_cand/n_groups, (g+1)*n_cand/n_groups) form group
+ *   g (for instance the drafts retrieved for one query).
+ * Per position (c, j < draft_len[c]), with x the row and t = drafts[c][j]:
+ *   rank  = #{v : x_v > x_t} + #{v < t : x_v = x_t}  (V when t is outside
+ *           [0, V)): t's place in the order (logit desc, index asc)
+ *   B_em  = I(rank == 0)  (t is the first argmax of x)
+ *   E     = -sum_v p_v ln p_v with p = softmax(x)
+ *   B_ent = I(E' > gamma);  B_topk = I(rank < topk)
+ * Per draft: B-bar = 1 - B_em, right-padded with W ones (positions
+ * j >= draft_len count as mismatches); R[j] = sum_{u=1..W} B-bar[j+u];
+ * B_con = I(R <= tau); G = B_em | (B_ent & (B_topk | B_con)), forced to 0 at
+ * j >= draft_len; the accepted length n_c = number of leading ones of G.
+ * Outputs:
+ *   out_accept_len n_cand int32, n_c in [0, draft_len[c]] (required).  The
+ *                  paper's L of Alg. 4 is n_c - 1.
+ *   out_best       n_groups int32: index within its group of the first draft
+ *                  with the largest n_c (required).
+ *   out_gate_score n_cand x max_len fp32 E' (0 at j >= draft_len), or NULL.
+ *   out_masks      n_cand x max_len uint8 em | ent<<1 | topk<<2 | con<<3 |
+ *                  G<<4 (em, ent, topk are 0 at j >= draft_len), or NULL.
+ *   out_rank       n_cand x max_len int32 rank (V at j >= draft_len), or NULL.
+ *   workspace      at least sense_soft_gate_verify_workspace_size bytes,
+ *                  256-byte aligned; contents not preserved.
+ * Errors: INVALID_ARGUMENT, MISALIGNED (workspace), WORKSPACE, HIP. */
+sense_status_t sense_soft_gate_verify(const void *logits, sense_dtype_t logits_dtype,
+                                      int64_t row_stride, const int32_t *drafts,
+                                      const int32_t *draft_len, int32_t n_cand,
+                                      int32_t max_len, int32_t vocab, int32_t n_groups,
+                                      const sense_gate_params_t *params,
+                                      int32_t *out_accept_len, int32_t *out_best,
+                                      float *out_gate_score, uint8_t *out_masks,
+                                      int32_t *out_rank, void *workspace,
+                                      size_t workspace_bytes, void *stream);
+
+/* Diagnostics for benchmarks and profilers.  Which part of the path a pair
+ * of timing events brackets. */
+typedef enum {
+    SENSE_TIMER_SCAN = 0,   /* similarity scan kernel(s) of sense_retrieve */
+    SENSE_TIMER_TOPK = 1,   /* top-k selection + gather kernels of sense_retrieve */
+    SENSE_TIMER_VERIFY = 2  /* both kernels of sense_soft_gate_verify */
+} sense_timer_t;
+
+/* Register two hipEvent_t handles (created by the caller with timing
+ * enabled) that the NEXT calls on this thread record, on their own stream,
+ * immediately before and after the kernels named by `which`; NULL events
+ * switch the timer off.  The setting is per calling thread and stays until
+ * changed.  Events are only recorded, never waited on: read them with
+ * hipEventElapsedTime after synchronising.  INVALID_ARGUMENT for an unknown
+ * `which` or exactly one NULL event. */
+sense_status_t sense_set_timer_events(sense_timer_t which, void *start_event, void *stop_event);
+
+/* Static description of a status code. */
+const char *sense_status_string(sense_status_t status);
+
+/* Detail of the last failure on the calling thread ("" if none). */
+const char *sense_last_error_message(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SENSE_H_ */

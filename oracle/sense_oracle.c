@@ -302,7 +302,8 @@ int oracle_soft_gate_verify(const void *logits, int logits_dtype, int64_t row_st
                           (size_t)p * (size_t)row_stride *
                               (logits_dtype == OR_F32 ? 4 : 2);
         if (oracle_row_stats(row, logits_dtype, vocab, tok, &y, &e, &r)) { err = 1; continue; }
-        double g = entropy_normalized ? e / log_v : e;
+        /* |V| = 1: E = 0 and E / ln|V| is 0/0; it is read as 0 */
+        double g = entropy_normalized ? (vocab > 1 ? e / log_v : 0.0) : e;
         am[p] = y;
         rk[p] = r;
         em[p] = (tok == y);                      /* Y = argmax; B_em = I(D = Y) */

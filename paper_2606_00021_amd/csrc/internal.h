@@ -1,0 +1,94 @@
+// Internal declarations shared by the host layer and the kernel files of the
+// SENSE hot-path library.  Nothing here is part of the C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace sense {
+
+// Element encodings (same numbering as sense_dtype_t).
+enum : int { DT_F32 = 0, DT_F16 = 1, DT_BF16 = 2 };
+
+// Rows of the similarity scan handled by one 16-byte load of one lane:
+// eight 2-byte key elements.  A wave (64 lanes) covers 512 elements of a row
+// per load instruction.
+constexpr int kLaneElems = 8;
+constexpr int kWaveElems = 64 * kLaneElems;
+constexpr int kMaxDim = 8192;       // 16 chunks of 512 elements per lane
+constexpr int kMaxK = 1024;         // largest retrieval top-k
+constexpr int kMaxLen = 64;         // longest draft
+constexpr int kSelectChunk = 8192;  // elements per top-k selection block
+
+// Order-preserving map of an fp32 score to an unsigned key: larger score ->
+// larger key; every NaN -> 0 (below everything); -0 is folded onto +0.
+__host__ __device__ inline uint32_t score_key(float s) {
+    if (s != s) return 0u;
+    s = s + 0.0f;
+    uint32_t u;
+    __builtin_memcpy(&u, &s, 4);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__host__ __device__ inline float key_score(uint32_t k) {
+    uint32_t u = (k & 0x80000000u) ? (k ^ 0x80000000u) : ~k;
+    float s;
+    __builtin_memcpy(&s, &u, 4);
+    return s;
+}
+// 64-bit selection key: (score key, then lower row index first).  Row ids
+// are below 2^31, so a real key is always above 0 (the padding key).
+__host__ __device__ inline uint64_t pack_key(float s, uint32_t row) {
+    return ((uint64_t)score_key(s) << 32) | (uint64_t)(0xFFFFFFFFu - row);
+}
+__host__ __device__ inline uint32_t key_row(uint64_t k) {
+    return 0xFFFFFFFFu - (uint32_t)(k & 0xFFFFFFFFu);
+}
+
+// ----------------------------------------------------------------- launchers
+// Each returns hipSuccess or the launch error.  Shapes are validated by the
+// caller (sense_api.hip) before these are reached.
+
+// inv_norm[i] = 1 / ||keys[i, :d]|| (0 for a zero row), fp32 accumulation.
+hipError_t launch_key_norms(const void* keys, int key_dtype, int64_t n, int d, int64_t ld,
+                            float* inv_norm, hipStream_t stream);
+
+// scores[q * n + i] = similarity of query q and row i for q in [0, nq).
+// queries: nq x d fp32 (already converted).  inv_norm NULL for IP.
+hipError_t launch_scan(const void* keys, int key_dtype, int64_t n, int d, int64_t ld,
+                       const float* queries, int nq, const float* inv_norm, float* scores,
+                       hipStream_t stream);
+
+// Converts nq x d queries of dtype q_dtype to fp32 (plain copy for fp32).
+hipError_t launch_query_to_f32(const void* q, int q_dtype, int nq, int d, float* out,
+                               hipStream_t stream);
+
+// Workspace of the top-k stage, in bytes, for nq queries over n scores.
+size_t topk_workspace_bytes(int64_t n, int nq, int k);
+
+// Per-query top-k of scores (nq x n) in the order (score desc, row asc),
+// plus the gather of each hit's continuation.
+hipError_t launch_topk_gather(const float* scores, int64_t n, int nq, int k,
+                              const int32_t* spans, const int32_t* span_len, int max_span,
+                              int64_t* out_ids, float* out_scores, int32_t* out_drafts,
+                              int32_t* out_draft_len, void* workspace, hipStream_t stream);
+
+// Verification workspace in bytes.
+size_t verify_workspace_bytes(int n_cand, int max_len, int vocab);
+
+struct GateParams {
+    float gamma;
+    int topk;
+    int window;
+    int tau;
+    float ent_scale;  // 1/ln V when normalised, 1 otherwise
+};
+
+hipError_t launch_verify(const void* logits, int logits_dtype, int64_t row_stride,
+                         const int32_t* drafts, const int32_t* draft_len, int n_cand,
+                         int max_len, int vocab, int n_groups, const GateParams& gp,
+                         int32_t* out_accept_len, int32_t* out_best, float* out_gate_score,
+                         uint8_t* out_masks, int32_t* out_rank, void* workspace,
+                         hipStream_t stream);
+
+}  // namespace sense

@@ -1,0 +1,345 @@
+// Host layer of the C ABI declared in include/sense.h: argument validation,
+// workspace layout, index ownership, and the launch sequence of each entry
+// point.  No C++ exception crosses the boundary; every failure returns a
+// status and leaves a message for sense_last_error_message().
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <new>
+
+#include "internal.h"
+#include "sense.h"
+
+#define SENSE_EXPORT extern "C" __attribute__((visibility("default")))
+
+struct sense_index {
+    const void* keys;       // borrowed or owned (== owned_keys)
+    void* owned_keys;       // SENSE_INDEX_COPY_KEYS copy, else NULL
+    int key_dtype;
+    int64_t n;
+    int32_t d;
+    int64_t ld;
+    const int32_t* spans;
+    int32_t max_span;
+    const int32_t* span_len;
+    int metric;
+    float* inv_norm;        // owned; NULL for the inner-product metric
+};
+
+namespace {
+
+thread_local char g_msg[512];
+
+// Timing events per sense_timer_t, set by sense_set_timer_events.
+thread_local hipEvent_t g_timer[3][2] = {{nullptr, nullptr}, {nullptr, nullptr}, {nullptr, nullptr}};
+
+hipError_t timer_mark(int which, int edge, hipStream_t st) {
+    hipEvent_t ev = g_timer[which][edge];
+    return ev ? hipEventRecord(ev, st) : hipSuccess;
+}
+
+sense_status_t fail(sense_status_t st, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_msg, sizeof g_msg, fmt, ap);
+    va_end(ap);
+    return st;
+}
+
+sense_status_t ok() {
+    g_msg[0] = '\0';
+    return SENSE_OK;
+}
+
+sense_status_t hip_fail(hipError_t e, const char* where) {
+    return fail(SENSE_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+int elem_size(int dt) { return dt == SENSE_F32 ? 4 : 2; }
+
+bool dtype_ok(int dt) { return dt == SENSE_F32 || dt == SENSE_F16 || dt == SENSE_BF16; }
+
+// Retrieval workspace layout: [fp32 queries | scores | top-k buffers].
+struct RetrieveLayout {
+    size_t q_off, s_off, t_off, total;
+};
+
+RetrieveLayout retrieve_layout(const sense_index* ix, int nq, int k) {
+    RetrieveLayout l;
+    l.q_off = 0;
+    l.s_off = round_up((size_t)nq * ix->d * sizeof(float), 256);
+    l.t_off = l.s_off + round_up((size_t)nq * (size_t)ix->n * sizeof(float), 256);
+    l.total = l.t_off + sense::topk_workspace_bytes(ix->n, nq, k);
+    return l;
+}
+
+}  // namespace
+
+SENSE_EXPORT const char* sense_status_string(sense_status_t s) {
+    switch (s) {
+        case SENSE_OK: return "ok";
+        case SENSE_ERR_INVALID_ARGUMENT: return "invalid argument";
+        case SENSE_ERR_MISALIGNED: return "misaligned pointer or stride";
+        case SENSE_ERR_UNSUPPORTED: return "unsupported size";
+        case SENSE_ERR_OUT_OF_MEMORY: return "out of device memory";
+        case SENSE_ERR_WORKSPACE: return "workspace missing or too small";
+        case SENSE_ERR_HIP: return "HIP runtime error";
+    }
+    return "unknown status";
+}
+
+SENSE_EXPORT const char* sense_last_error_message(void) { return g_msg; }
+
+SENSE_EXPORT sense_status_t sense_set_timer_events(sense_timer_t which, void* start_event,
+                                                   void* stop_event) {
+    if ((int)which < 0 || (int)which > 2)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "unknown timer %d", (int)which);
+    if ((start_event == nullptr) != (stop_event == nullptr))
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "give both events or neither");
+    g_timer[which][0] = (hipEvent_t)start_event;
+    g_timer[which][1] = (hipEvent_t)stop_event;
+    return ok();
+}
+
+SENSE_EXPORT sense_status_t sense_build_index(const sense_index_desc_t* desc, void* stream,
+                                              sense_index_t** out) {
+    if (!desc || !out) return fail(SENSE_ERR_INVALID_ARGUMENT, "desc and out must be non-NULL");
+    *out = nullptr;
+    const sense_index_desc_t& D = *desc;
+    if (!D.keys || !D.spans) return fail(SENSE_ERR_INVALID_ARGUMENT, "keys and spans must be non-NULL");
+    if (D.key_dtype != SENSE_F16 && D.key_dtype != SENSE_BF16)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "key_dtype must be SENSE_F16 or SENSE_BF16");
+    if (D.n < 1 || D.n > 0x7FFFFFFFLL)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "n = %lld outside [1, 2^31-1]", (long long)D.n);
+    if (D.d < 1 || D.d > sense::kMaxDim || D.d % 8 != 0)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "d = %d must be a multiple of 8 in [8, %d]", D.d,
+                    sense::kMaxDim);
+    if (D.key_stride < D.d)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "key_stride %lld < d %d", (long long)D.key_stride, D.d);
+    if (D.max_span < 1 || D.max_span > sense::kMaxLen)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "max_span = %d outside [1, %d]", D.max_span,
+                    sense::kMaxLen);
+    if (D.metric != SENSE_METRIC_IP && D.metric != SENSE_METRIC_COSINE)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "unknown metric %d", (int)D.metric);
+    if ((D.flags & ~SENSE_INDEX_COPY_KEYS) != 0)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "unknown flags 0x%x", D.flags);
+    const bool copy = (D.flags & SENSE_INDEX_COPY_KEYS) != 0;
+    if (!copy && (!aligned(D.keys, 16) || D.key_stride % 8 != 0))
+        return fail(SENSE_ERR_MISALIGNED,
+                    "keys must be 16-byte aligned with key_stride %% 8 == 0 "
+                    "(or pass SENSE_INDEX_COPY_KEYS)");
+
+    sense_index* ix = new (std::nothrow) sense_index();
+    if (!ix) return fail(SENSE_ERR_OUT_OF_MEMORY, "host allocation failed");
+    ix->key_dtype = D.key_dtype;
+    ix->n = D.n;
+    ix->d = D.d;
+    ix->spans = D.spans;
+    ix->max_span = D.max_span;
+    ix->span_len = D.span_len;
+    ix->metric = D.metric;
+    hipStream_t st = (hipStream_t)stream;
+    hipError_t e;
+    if (copy) {
+        ix->ld = D.d;  // d % 8 == 0, so rows stay 16-byte aligned
+        const size_t bytes = (size_t)D.n * D.d * 2;
+        if ((e = hipMalloc(&ix->owned_keys, bytes)) != hipSuccess) {
+            delete ix;
+            return fail(SENSE_ERR_OUT_OF_MEMORY, "key copy of %zu bytes: %s", bytes,
+                        hipGetErrorString(e));
+        }
+        e = hipMemcpy2DAsync(ix->owned_keys, (size_t)D.d * 2, D.keys, (size_t)D.key_stride * 2,
+                             (size_t)D.d * 2, (size_t)D.n, hipMemcpyDeviceToDevice, st);
+        if (e != hipSuccess) {
+            (void)hipFree(ix->owned_keys);
+            delete ix;
+            return hip_fail(e, "key copy");
+        }
+        ix->keys = ix->owned_keys;
+    } else {
+        ix->keys = D.keys;
+        ix->ld = D.key_stride;
+    }
+    if (D.metric == SENSE_METRIC_COSINE) {
+        if ((e = hipMalloc(&ix->inv_norm, (size_t)D.n * sizeof(float))) != hipSuccess) {
+            if (ix->owned_keys) (void)hipFree(ix->owned_keys);
+            delete ix;
+            return fail(SENSE_ERR_OUT_OF_MEMORY, "norm table: %s", hipGetErrorString(e));
+        }
+        e = sense::launch_key_norms(ix->keys, ix->key_dtype, ix->n, ix->d, ix->ld, ix->inv_norm, st);
+        if (e != hipSuccess) {
+            (void)hipFree(ix->inv_norm);
+            if (ix->owned_keys) (void)hipFree(ix->owned_keys);
+            delete ix;
+            return hip_fail(e, "key norms");
+        }
+    }
+    *out = ix;
+    return ok();
+}
+
+SENSE_EXPORT sense_status_t sense_destroy_index(sense_index_t* ix) {
+    if (!ix) return ok();
+    hipError_t e = hipDeviceSynchronize();
+    if (ix->inv_norm) (void)hipFree(ix->inv_norm);
+    if (ix->owned_keys) (void)hipFree(ix->owned_keys);
+    delete ix;
+    if (e != hipSuccess) return hip_fail(e, "destroy");
+    return ok();
+}
+
+SENSE_EXPORT sense_status_t sense_index_info(const sense_index_t* ix, int64_t* n, int32_t* d,
+                                             int32_t* max_span, sense_metric_t* metric,
+                                             sense_dtype_t* key_dtype) {
+    if (!ix) return fail(SENSE_ERR_INVALID_ARGUMENT, "index is NULL");
+    if (n) *n = ix->n;
+    if (d) *d = ix->d;
+    if (max_span) *max_span = ix->max_span;
+    if (metric) *metric = (sense_metric_t)ix->metric;
+    if (key_dtype) *key_dtype = (sense_dtype_t)ix->key_dtype;
+    return ok();
+}
+
+static sense_status_t check_retrieve_sizes(const sense_index_t* ix, int32_t nq, int32_t k) {
+    if (!ix) return fail(SENSE_ERR_INVALID_ARGUMENT, "index is NULL");
+    if (nq < 1) return fail(SENSE_ERR_INVALID_ARGUMENT, "n_queries = %d < 1", nq);
+    if (k < 1) return fail(SENSE_ERR_INVALID_ARGUMENT, "k = %d < 1", k);
+    if (k > sense::kMaxK) return fail(SENSE_ERR_UNSUPPORTED, "k = %d > %d", k, sense::kMaxK);
+    if ((int64_t)k > ix->n)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "k = %d exceeds the %lld stored rows", k,
+                    (long long)ix->n);
+    return SENSE_OK;
+}
+
+SENSE_EXPORT sense_status_t sense_retrieve_workspace_size(const sense_index_t* ix, int32_t nq,
+                                                          int32_t k, size_t* bytes) {
+    if (!bytes) return fail(SENSE_ERR_INVALID_ARGUMENT, "bytes is NULL");
+    const sense_status_t s = check_retrieve_sizes(ix, nq, k);
+    if (s != SENSE_OK) return s;
+    *bytes = retrieve_layout(ix, nq, k).total;
+    return ok();
+}
+
+SENSE_EXPORT sense_status_t sense_retrieve(const sense_index_t* ix, const void* queries,
+                                           sense_dtype_t q_dtype, int32_t nq, int32_t k,
+                                           int64_t* out_ids, float* out_scores,
+                                           int32_t* out_drafts, int32_t* out_draft_len,
+                                           void* workspace, size_t workspace_bytes,
+                                           void* stream) {
+    sense_status_t s = check_retrieve_sizes(ix, nq, k);
+    if (s != SENSE_OK) return s;
+    if (!queries || !out_ids)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "queries and out_ids must be non-NULL");
+    if (!dtype_ok(q_dtype)) return fail(SENSE_ERR_INVALID_ARGUMENT, "unknown q_dtype %d", (int)q_dtype);
+    if (!aligned(queries, q_dtype == SENSE_F32 ? 16 : 2))
+        return fail(SENSE_ERR_MISALIGNED, "fp32 queries must be 16-byte aligned");
+    const RetrieveLayout L = retrieve_layout(ix, nq, k);
+    if (!workspace || workspace_bytes < L.total)
+        return fail(SENSE_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", L.total,
+                    workspace ? workspace_bytes : (size_t)0);
+    if (!aligned(workspace, 256)) return fail(SENSE_ERR_MISALIGNED, "workspace must be 256-byte aligned");
+
+    hipStream_t st = (hipStream_t)stream;
+    char* ws = (char*)workspace;
+    float* qf = (float*)(ws + L.q_off);
+    float* scores = (float*)(ws + L.s_off);
+    hipError_t e;
+    const float* qptr = (const float*)queries;
+    if (q_dtype != SENSE_F32) {
+        if ((e = sense::launch_query_to_f32(queries, q_dtype, nq, ix->d, qf, st)) != hipSuccess)
+            return hip_fail(e, "query conversion");
+        qptr = qf;
+    }
+    if ((e = timer_mark(SENSE_TIMER_SCAN, 0, st)) != hipSuccess) return hip_fail(e, "timer");
+    if ((e = sense::launch_scan(ix->keys, ix->key_dtype, ix->n, ix->d, ix->ld, qptr, nq,
+                                ix->inv_norm, scores, st)) != hipSuccess)
+        return hip_fail(e, "similarity scan");
+    if ((e = timer_mark(SENSE_TIMER_SCAN, 1, st)) != hipSuccess) return hip_fail(e, "timer");
+    if ((e = timer_mark(SENSE_TIMER_TOPK, 0, st)) != hipSuccess) return hip_fail(e, "timer");
+    if ((e = sense::launch_topk_gather(scores, ix->n, nq, k, ix->spans, ix->span_len,
+                                       ix->max_span, out_ids, out_scores, out_drafts,
+                                       out_draft_len, ws + L.t_off, st)) != hipSuccess)
+        return hip_fail(e, "top-k");
+    if ((e = timer_mark(SENSE_TIMER_TOPK, 1, st)) != hipSuccess) return hip_fail(e, "timer");
+    return ok();
+}
+
+static sense_status_t check_verify_sizes(int32_t n_cand, int32_t max_len, int32_t vocab) {
+    if (n_cand < 0) return fail(SENSE_ERR_INVALID_ARGUMENT, "n_cand = %d < 0", n_cand);
+    if (max_len < 1 || max_len > sense::kMaxLen)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "max_len = %d outside [1, %d]", max_len,
+                    sense::kMaxLen);
+    if (vocab < 1) return fail(SENSE_ERR_INVALID_ARGUMENT, "vocab = %d < 1", vocab);
+    if ((int64_t)n_cand * max_len > 0x7FFFFFFFLL)
+        return fail(SENSE_ERR_UNSUPPORTED, "n_cand * max_len too large");
+    return SENSE_OK;
+}
+
+SENSE_EXPORT sense_status_t sense_soft_gate_verify_workspace_size(int32_t n_cand,
+                                                                  int32_t max_len,
+                                                                  int32_t vocab,
+                                                                  size_t* bytes) {
+    if (!bytes) return fail(SENSE_ERR_INVALID_ARGUMENT, "bytes is NULL");
+    const sense_status_t s = check_verify_sizes(n_cand, max_len, vocab);
+    if (s != SENSE_OK) return s;
+    *bytes = sense::verify_workspace_bytes(n_cand, max_len, vocab);
+    return ok();
+}
+
+SENSE_EXPORT sense_status_t sense_soft_gate_verify(
+    const void* logits, sense_dtype_t logits_dtype, int64_t row_stride, const int32_t* drafts,
+    const int32_t* draft_len, int32_t n_cand, int32_t max_len, int32_t vocab, int32_t n_groups,
+    const sense_gate_params_t* params, int32_t* out_accept_len, int32_t* out_best,
+    float* out_gate_score, uint8_t* out_masks, int32_t* out_rank, void* workspace,
+    size_t workspace_bytes, void* stream) {
+    sense_status_t s = check_verify_sizes(n_cand, max_len, vocab);
+    if (s != SENSE_OK) return s;
+    if (!params) return fail(SENSE_ERR_INVALID_ARGUMENT, "params is NULL");
+    if (!dtype_ok(logits_dtype))
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "unknown logits dtype %d", (int)logits_dtype);
+    if (row_stride < vocab)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "row_stride %lld < vocab %d", (long long)row_stride, vocab);
+    if (params->topk < 1) return fail(SENSE_ERR_INVALID_ARGUMENT, "topk = %d < 1", params->topk);
+    if (params->window < 0 || params->window > sense::kMaxLen)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "window = %d outside [0, %d]", params->window,
+                    sense::kMaxLen);
+    if (params->tau < 0) return fail(SENSE_ERR_INVALID_ARGUMENT, "tau = %d < 0", params->tau);
+    if (params->gamma != params->gamma) return fail(SENSE_ERR_INVALID_ARGUMENT, "gamma is NaN");
+    if (n_cand == 0) return ok();
+    if (n_groups < 1 || n_cand % n_groups != 0)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "n_groups = %d must divide n_cand = %d", n_groups,
+                    n_cand);
+    if (!logits || !drafts || !out_accept_len || !out_best)
+        return fail(SENSE_ERR_INVALID_ARGUMENT,
+                    "logits, drafts, out_accept_len and out_best must be non-NULL");
+    if (!aligned(logits, (size_t)elem_size(logits_dtype)))
+        return fail(SENSE_ERR_MISALIGNED, "logits not aligned to their element size");
+    const size_t need = sense::verify_workspace_bytes(n_cand, max_len, vocab);
+    if (!workspace || workspace_bytes < need)
+        return fail(SENSE_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
+                    workspace ? workspace_bytes : (size_t)0);
+    if (!aligned(workspace, 256)) return fail(SENSE_ERR_MISALIGNED, "workspace must be 256-byte aligned");
+
+    sense::GateParams gp;
+    gp.gamma = params->gamma;
+    gp.topk = params->topk;
+    gp.window = params->window;
+    gp.tau = params->tau;
+    gp.ent_scale = params->entropy_normalized ? (float)(1.0 / log((double)vocab)) : 1.0f;
+    if (vocab == 1) gp.ent_scale = params->entropy_normalized ? 0.0f : 1.0f;  // E = 0 = ln 1
+    hipStream_t st = (hipStream_t)stream;
+    hipError_t e;
+    if ((e = timer_mark(SENSE_TIMER_VERIFY, 0, st)) != hipSuccess) return hip_fail(e, "timer");
+    e = sense::launch_verify(logits, logits_dtype, row_stride, drafts, draft_len, n_cand, max_len,
+                             vocab, n_groups, gp, out_accept_len, out_best, out_gate_score,
+                             out_masks, out_rank, workspace, st);
+    if (e != hipSuccess) return hip_fail(e, "soft-gated evaluation");
+    if ((e = timer_mark(SENSE_TIMER_VERIFY, 1, st)) != hipSuccess) return hip_fail(e, "timer");
+    return ok();
+}

@@ -1,0 +1,237 @@
+// Per-query top-k of the similarity scores (Sec. 2.1 Eq. 3: the retriever
+// returns the N most relevant continuations; Sec. 2.2 Eq. 8 "top-N'") and
+// the gather of each hit's continuation into the draft batch (the (k_i, s_i)
+// pairs of Sec. 2.2).
+//
+// Order: score descending, then row index ascending.  Each (score, row) pair
+// is packed into one unique 64-bit key (order-preserving score bits in the
+// high word, the complemented row in the low word), so "top-k" is "the k
+// largest keys" and ties need no special handling.
+//
+// Selection is hierarchical.  A block of 512 threads takes a chunk of 8192
+// keys into LDS and finds the chunk's k largest with an 8-bit radix select:
+// per pass a 256-bin LDS histogram of the next digit among the keys that
+// still match the chosen prefix, then one wave finds the digit holding the
+// k-th key with a suffix scan.  The pass loop stops as soon as the chosen
+// digit's bucket is taken whole, so most chunks need 2-4 passes.  The k
+// survivors of every chunk form the next level's input until one chunk
+// remains; its k keys are sorted with a bitonic network in LDS and written
+// out together with the gathered continuations.
+#include "internal.h"
+
+namespace sense {
+namespace {
+
+constexpr int kThreads = 512;
+
+struct SelectState {
+    uint64_t prefix;
+    uint64_t mask;
+};
+
+// Finds prefix/mask such that exactly `need` of the len keys in s_keys have
+// (key & mask) >= prefix.  Requires 1 <= need <= len.  All threads of the
+// block must call it; it ends with a barrier.
+__device__ SelectState radix_select(const uint64_t* s_keys, int len, int need,
+                                    uint32_t* s_hist, uint32_t* s_info) {
+    const int tid = threadIdx.x;
+    uint64_t prefix = 0, mask = 0;
+    for (int shift = 56; shift >= 0; shift -= 8) {
+        for (int b = tid; b < 256; b += kThreads) s_hist[b] = 0;
+        __syncthreads();
+        for (int i = tid; i < len; i += kThreads) {
+            const uint64_t key = s_keys[i];
+            if ((key & mask) == prefix) atomicAdd(&s_hist[(key >> shift) & 0xFF], 1u);
+        }
+        __syncthreads();
+        if (tid < 64) {
+            const int l = tid;
+            const uint32_t h0 = s_hist[4 * l], h1 = s_hist[4 * l + 1], h2 = s_hist[4 * l + 2],
+                           h3 = s_hist[4 * l + 3];
+            const uint32_t local = h0 + h1 + h2 + h3;
+            // inclusive suffix sum over lanes l..63 (higher digits)
+            uint32_t incl = local;
+#pragma unroll
+            for (int off = 1; off < 64; off <<= 1) {
+                const uint32_t t = __shfl_down(incl, off, 64);
+                if (l + off < 64) incl += t;
+            }
+            uint32_t above = incl - local;
+            if (above < (uint32_t)need && (uint32_t)need <= incl) {
+                const uint32_t hs[4] = {h0, h1, h2, h3};
+                for (int j = 3; j >= 0; --j) {
+                    if (above + hs[j] >= (uint32_t)need) {
+                        s_info[0] = (uint32_t)(4 * l + j);
+                        s_info[1] = above;
+                        s_info[2] = hs[j];
+                        break;
+                    }
+                    above += hs[j];
+                }
+            }
+        }
+        __syncthreads();
+        const uint32_t digit = s_info[0], above = s_info[1], in_bucket = s_info[2];
+        need -= (int)above;
+        prefix |= (uint64_t)digit << shift;
+        mask |= (uint64_t)0xFF << shift;
+        __syncthreads();  // s_info / s_hist are rewritten by the next pass
+        if ((int)in_bucket == need) break;
+    }
+    return SelectState{prefix, mask};
+}
+
+// Bitonic sort of s[0..p) into descending order; p a power of two.
+__device__ void bitonic_desc(uint64_t* s, int p) {
+    for (int size = 2; size <= p; size <<= 1) {
+        for (int stride = size >> 1; stride > 0; stride >>= 1) {
+            for (int i = threadIdx.x; i < (p >> 1); i += kThreads) {
+                const int pos = 2 * i - (i & (stride - 1));
+                const int partner = pos + stride;
+                const bool desc = (pos & size) == 0;
+                const uint64_t a = s[pos], b = s[partner];
+                if ((a < b) == desc) {
+                    s[pos] = b;
+                    s[partner] = a;
+                }
+            }
+            __syncthreads();
+        }
+    }
+}
+
+// One block per (chunk, query).  FROM_SCORES: input is the fp32 score matrix
+// (nq x count, row index = position); otherwise packed keys (nq x count).
+// FINAL: exactly one chunk per query; writes sorted ids/scores and drafts.
+template <bool FROM_SCORES, bool FINAL>
+__global__ __launch_bounds__(kThreads) void select_kernel(
+    const float* __restrict__ scores, const uint64_t* __restrict__ in_keys, int64_t count,
+    int k, uint64_t* __restrict__ out_keys, int64_t* __restrict__ out_ids,
+    float* __restrict__ out_scores, int32_t* __restrict__ out_drafts,
+    int32_t* __restrict__ out_draft_len, const int32_t* __restrict__ spans,
+    const int32_t* __restrict__ span_len, int max_span) {
+    __shared__ uint64_t s_keys[kSelectChunk];
+    __shared__ uint64_t s_sel[kMaxK];
+    __shared__ uint32_t s_hist[256];
+    __shared__ uint32_t s_info[4];
+    __shared__ uint32_t s_cnt;
+
+    const int tid = threadIdx.x;
+    const int q = blockIdx.y;
+    const int64_t start = (int64_t)blockIdx.x * kSelectChunk;
+    const int64_t remain = count - start;
+    const int len = (int)(remain < kSelectChunk ? remain : kSelectChunk);
+    const int kk = k < kSelectChunk ? k : kSelectChunk;
+
+    for (int i = tid; i < len; i += kThreads) {
+        const int64_t pos = start + i;
+        if constexpr (FROM_SCORES)
+            s_keys[i] = pack_key(scores[(int64_t)q * count + pos], (uint32_t)pos);
+        else
+            s_keys[i] = in_keys[(int64_t)q * count + pos];
+    }
+    if (tid == 0) s_cnt = 0;
+    __syncthreads();
+
+    // Keys taken: all of them if the chunk holds no more than kk.
+    SelectState st{0, 0};
+    if (len > kk) st = radix_select(s_keys, len, kk, s_hist, s_info);
+
+    if constexpr (!FINAL) {
+        uint64_t* out = out_keys + ((int64_t)q * gridDim.x + blockIdx.x) * kk;
+        for (int i = tid; i < len; i += kThreads) {
+            const uint64_t key = s_keys[i];
+            if ((key & st.mask) >= st.prefix) {
+                const uint32_t at = atomicAdd(&s_cnt, 1u);
+                if (at < (uint32_t)kk) out[at] = key;
+            }
+        }
+        __syncthreads();
+        const int taken = (int)s_cnt < kk ? (int)s_cnt : kk;
+        for (int i = taken + tid; i < kk; i += kThreads) out[i] = 0;  // padding key
+    } else {
+        for (int i = tid; i < len; i += kThreads) {
+            const uint64_t key = s_keys[i];
+            if ((key & st.mask) >= st.prefix) {
+                const uint32_t at = atomicAdd(&s_cnt, 1u);
+                if (at < (uint32_t)kk) s_sel[at] = key;
+            }
+        }
+        __syncthreads();
+        int p = 1;
+        while (p < kk) p <<= 1;
+        const int taken = (int)s_cnt < kk ? (int)s_cnt : kk;
+        for (int i = taken + tid; i < p; i += kThreads) s_sel[i] = 0;
+        __syncthreads();
+        bitonic_desc(s_sel, p);
+        for (int r = tid; r < k; r += kThreads) {
+            const uint64_t key = s_sel[r];
+            out_ids[(int64_t)q * k + r] = (int64_t)key_row(key);
+            if (out_scores) out_scores[(int64_t)q * k + r] = key_score((uint32_t)(key >> 32));
+        }
+        if (out_drafts || out_draft_len) {
+            for (int t = tid; t < k * max_span; t += kThreads) {
+                const int r = t / max_span, j = t - r * max_span;
+                const uint64_t key = s_sel[r];
+                const int64_t id = (int64_t)key_row(key);
+                // A padding key (0) can only surface if k exceeded the row
+                // count, which the host rejects; it would give an empty draft.
+                int len_r = (key == 0) ? 0 : (span_len ? span_len[id] : max_span);
+                len_r = len_r < 0 ? 0 : (len_r > max_span ? max_span : len_r);
+                const int64_t o = ((int64_t)q * k + r);
+                if (out_drafts)
+                    out_drafts[o * max_span + j] = (j < len_r) ? spans[id * max_span + j] : -1;
+                if (out_draft_len && j == 0) out_draft_len[o] = len_r;
+            }
+        }
+    }
+}
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+}  // namespace
+
+size_t topk_workspace_bytes(int64_t n, int nq, int k) {
+    const int64_t chunks = ceil_div(n, kSelectChunk);
+    if (chunks <= 1) return 0;
+    const int64_t kk = k < kSelectChunk ? k : kSelectChunk;
+    const size_t one = (size_t)nq * (size_t)chunks * (size_t)kk * sizeof(uint64_t);
+    return 2 * ((one + 255) / 256 * 256);
+}
+
+hipError_t launch_topk_gather(const float* scores, int64_t n, int nq, int k,
+                              const int32_t* spans, const int32_t* span_len, int max_span,
+                              int64_t* out_ids, float* out_scores, int32_t* out_drafts,
+                              int32_t* out_draft_len, void* workspace, hipStream_t stream) {
+    const int64_t kk = k < kSelectChunk ? k : kSelectChunk;
+    int64_t chunks = ceil_div(n, kSelectChunk);
+    if (chunks <= 1) {
+        hipLaunchKernelGGL((select_kernel<true, true>), dim3(1, nq), dim3(kThreads), 0, stream,
+                           scores, nullptr, n, k, nullptr, out_ids, out_scores, out_drafts,
+                           out_draft_len, spans, span_len, max_span);
+        return hipGetLastError();
+    }
+    const size_t one = topk_workspace_bytes(n, nq, k) / 2;
+    uint64_t* buf[2] = {(uint64_t*)workspace, (uint64_t*)((char*)workspace + one)};
+    hipLaunchKernelGGL((select_kernel<true, false>), dim3((unsigned)chunks, nq), dim3(kThreads),
+                       0, stream, scores, nullptr, n, k, buf[0], nullptr, nullptr, nullptr,
+                       nullptr, nullptr, nullptr, 0);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    int64_t count = chunks * kk;
+    int cur = 0;
+    while ((chunks = ceil_div(count, kSelectChunk)) > 1) {
+        hipLaunchKernelGGL((select_kernel<false, false>), dim3((unsigned)chunks, nq),
+                           dim3(kThreads), 0, stream, nullptr, buf[cur], count, k, buf[cur ^ 1],
+                           nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 0);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        count = chunks * kk;
+        cur ^= 1;
+    }
+    hipLaunchKernelGGL((select_kernel<false, true>), dim3(1, nq), dim3(kThreads), 0, stream,
+                       nullptr, buf[cur], count, k, nullptr, out_ids, out_scores, out_drafts,
+                       out_draft_len, spans, span_len, max_span);
+    return hipGetLastError();
+}
+
+}  // namespace sense

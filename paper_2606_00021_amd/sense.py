@@ -1,0 +1,307 @@
+"""Python binding of ``libsense.so`` (the SENSE hot-path C ABI, include/sense.h).
+
+Argument marshalling only: every step of retrieval and verification runs in
+the library's HIP kernels.  PyTorch provides device memory (the tensors passed
+in, the outputs and workspaces allocated here) and the current HIP stream.
+There is no CPU fallback: if the library is missing or the tensors are not on
+a GPU, the calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsense.so")
+
+SENSE_OK = 0
+STATUS_NAMES = {
+    0: "SENSE_OK",
+    1: "SENSE_ERR_INVALID_ARGUMENT",
+    2: "SENSE_ERR_MISALIGNED",
+    3: "SENSE_ERR_UNSUPPORTED",
+    4: "SENSE_ERR_OUT_OF_MEMORY",
+    5: "SENSE_ERR_WORKSPACE",
+    6: "SENSE_ERR_HIP",
+}
+SENSE_F32, SENSE_F16, SENSE_BF16 = 0, 1, 2
+METRICS = {"ip": 0, "cosine": 1}
+SENSE_INDEX_COPY_KEYS = 1
+
+_TORCH_DTYPE = {torch.float32: SENSE_F32, torch.float16: SENSE_F16, torch.bfloat16: SENSE_BF16}
+
+# Every symbol include/sense.h declares.
+EXPORTED = (
+    "sense_build_index",
+    "sense_destroy_index",
+    "sense_index_info",
+    "sense_retrieve_workspace_size",
+    "sense_retrieve",
+    "sense_soft_gate_verify_workspace_size",
+    "sense_soft_gate_verify",
+    "sense_set_timer_events",
+    "sense_status_string",
+    "sense_last_error_message",
+)
+SENSE_TIMER_SCAN, SENSE_TIMER_TOPK, SENSE_TIMER_VERIFY = 0, 1, 2
+
+
+class SenseError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str):
+        self.status = status
+        self.status_name = STATUS_NAMES.get(status, str(status))
+        super().__init__(f"{where}: {self.status_name}: {detail}")
+
+
+class IndexDesc(ctypes.Structure):
+    _fields_ = [
+        ("keys", ctypes.c_void_p),
+        ("key_dtype", ctypes.c_int),
+        ("n", ctypes.c_int64),
+        ("d", ctypes.c_int32),
+        ("key_stride", ctypes.c_int64),
+        ("spans", ctypes.c_void_p),
+        ("max_span", ctypes.c_int32),
+        ("span_len", ctypes.c_void_p),
+        ("metric", ctypes.c_int),
+        ("flags", ctypes.c_uint32),
+    ]
+
+
+class GateParams(ctypes.Structure):
+    _fields_ = [
+        ("gamma", ctypes.c_float),
+        ("topk", ctypes.c_int32),
+        ("window", ctypes.c_int32),
+        ("tau", ctypes.c_int32),
+        ("entropy_normalized", ctypes.c_int32),
+    ]
+
+
+_lib = None
+
+
+def load_library() -> ctypes.CDLL:
+    """Load libsense.so and declare its signatures (no device work)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"{LIB_PATH} is not built; run paper_2606_00021_amd.build.build() "
+            "(or __graft_entry__.build())")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I32, I64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    PP = ctypes.POINTER(ctypes.c_void_p)
+    PSZ = ctypes.POINTER(ctypes.c_size_t)
+    sig = {
+        "sense_build_index": [ctypes.POINTER(IndexDesc), P, PP],
+        "sense_destroy_index": [P],
+        "sense_index_info": [P, ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_int32),
+                             ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int),
+                             ctypes.POINTER(ctypes.c_int)],
+        "sense_retrieve_workspace_size": [P, I32, I32, PSZ],
+        "sense_retrieve": [P, P, ctypes.c_int, I32, I32, P, P, P, P, P, SZ, P],
+        "sense_soft_gate_verify_workspace_size": [I32, I32, I32, PSZ],
+        "sense_soft_gate_verify": [P, ctypes.c_int, I64, P, P, I32, I32, I32, I32,
+                                   ctypes.POINTER(GateParams), P, P, P, P, P, P, SZ, P],
+    }
+    for name, args in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = ctypes.c_int
+    lib.sense_set_timer_events.argtypes = [ctypes.c_int, P, P]
+    lib.sense_set_timer_events.restype = ctypes.c_int
+    lib.sense_status_string.argtypes = [ctypes.c_int]
+    lib.sense_status_string.restype = ctypes.c_char_p
+    lib.sense_last_error_message.argtypes = []
+    lib.sense_last_error_message.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def _check(status: int, where: str) -> None:
+    if status != SENSE_OK:
+        detail = load_library().sense_last_error_message().decode(errors="replace")
+        raise SenseError(status, where, detail)
+
+
+def _dev_ptr(t: torch.Tensor | None, name: str):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor (got {t.device})")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream_handle(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    if isinstance(stream, torch.cuda.Stream):
+        return ctypes.c_void_p(stream.cuda_stream)
+    return ctypes.c_void_p(int(stream))
+
+
+@dataclass
+class Index:
+    """A built datastore index.  Holds references to the borrowed tensors so
+    they outlive the handle."""
+
+    handle: ctypes.c_void_p
+    keys: torch.Tensor
+    spans: torch.Tensor
+    span_len: torch.Tensor | None
+    n: int
+    d: int
+    max_span: int
+    metric: str
+
+    def close(self) -> None:
+        if self.handle:
+            h, self.handle = self.handle, None
+            _check(load_library().sense_destroy_index(h), "sense_destroy_index")
+
+    def __del__(self):  # best effort; explicit close() reports errors
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def sense_build_index(keys: torch.Tensor, spans: torch.Tensor, span_len: torch.Tensor | None = None,
+                      metric: str = "cosine", copy_keys: bool = False, stream=None) -> Index:
+    """Build the datastore index over ``keys`` (N x d fp16/bf16, rows may be
+    strided) with continuations ``spans`` (N x M int32) and optional
+    ``span_len`` (N int32)."""
+    lib = load_library()
+    if keys.dim() != 2 or keys.dtype not in (torch.float16, torch.bfloat16):
+        raise ValueError("keys must be a 2-D float16/bfloat16 tensor")
+    if keys.stride(1) != 1:
+        raise ValueError("keys rows must be contiguous (stride(1) == 1)")
+    if spans.dtype != torch.int32 or spans.dim() != 2 or not spans.is_contiguous():
+        raise ValueError("spans must be a contiguous N x M int32 tensor")
+    if span_len is not None and (span_len.dtype != torch.int32 or not span_len.is_contiguous()):
+        raise ValueError("span_len must be a contiguous int32 tensor")
+    desc = IndexDesc(
+        keys=_dev_ptr(keys, "keys"), key_dtype=_TORCH_DTYPE[keys.dtype], n=keys.shape[0],
+        d=keys.shape[1], key_stride=keys.stride(0), spans=_dev_ptr(spans, "spans"),
+        max_span=spans.shape[1], span_len=_dev_ptr(span_len, "span_len"),
+        metric=METRICS[metric], flags=SENSE_INDEX_COPY_KEYS if copy_keys else 0)
+    handle = ctypes.c_void_p()
+    _check(lib.sense_build_index(ctypes.byref(desc), _stream_handle(stream), ctypes.byref(handle)),
+           "sense_build_index")
+    return Index(handle, keys, spans, span_len, keys.shape[0], keys.shape[1], spans.shape[1], metric)
+
+
+def sense_retrieve_workspace_size(index: Index, n_queries: int, k: int) -> int:
+    size = ctypes.c_size_t()
+    _check(load_library().sense_retrieve_workspace_size(index.handle, n_queries, k,
+                                                        ctypes.byref(size)),
+           "sense_retrieve_workspace_size")
+    return size.value
+
+
+def sense_retrieve(index: Index, queries: torch.Tensor, k: int, workspace: torch.Tensor | None = None,
+                   out: tuple | None = None, stream=None):
+    """Exact top-k retrieval for ``queries`` (Q x d, fp32 or the key dtype).
+
+    Returns (ids int64 [Q,k], scores fp32 [Q,k], drafts int32 [Q,k,M],
+    draft_len int32 [Q,k]).  ``out`` may supply those four tensors and
+    ``workspace`` a uint8 tensor of sense_retrieve_workspace_size bytes."""
+    lib = load_library()
+    if queries.dim() == 1:
+        queries = queries.unsqueeze(0)
+    if queries.dtype not in _TORCH_DTYPE or not queries.is_contiguous():
+        raise ValueError("queries must be a contiguous float32/float16/bfloat16 tensor")
+    if queries.shape[1] != index.d:
+        raise ValueError(f"queries have d={queries.shape[1]}, index has d={index.d}")
+    nq = queries.shape[0]
+    dev = queries.device
+    if out is None:
+        ids = torch.empty((nq, k), dtype=torch.int64, device=dev)
+        scores = torch.empty((nq, k), dtype=torch.float32, device=dev)
+        drafts = torch.empty((nq, k, index.max_span), dtype=torch.int32, device=dev)
+        dlen = torch.empty((nq, k), dtype=torch.int32, device=dev)
+    else:
+        ids, scores, drafts, dlen = out
+    if workspace is None:
+        workspace = torch.empty(max(sense_retrieve_workspace_size(index, nq, k), 1),
+                                dtype=torch.uint8, device=dev)
+    _check(lib.sense_retrieve(index.handle, _dev_ptr(queries, "queries"), _TORCH_DTYPE[queries.dtype],
+                              nq, k, _dev_ptr(ids, "out_ids"), _dev_ptr(scores, "out_scores"),
+                              _dev_ptr(drafts, "out_drafts"), _dev_ptr(dlen, "out_draft_len"),
+                              _dev_ptr(workspace, "workspace"), workspace.numel(),
+                              _stream_handle(stream)),
+           "sense_retrieve")
+    return ids, scores, drafts, dlen
+
+
+def sense_soft_gate_verify_workspace_size(n_cand: int, max_len: int, vocab: int) -> int:
+    size = ctypes.c_size_t()
+    _check(load_library().sense_soft_gate_verify_workspace_size(n_cand, max_len, vocab,
+                                                                ctypes.byref(size)),
+           "sense_soft_gate_verify_workspace_size")
+    return size.value
+
+
+def sense_soft_gate_verify(logits: torch.Tensor, drafts: torch.Tensor,
+                           draft_len: torch.Tensor | None = None, n_groups: int = 1,
+                           gamma: float = 0.05, topk: int = 3, window: int = 6, tau: int = 0,
+                           entropy_normalized: bool = True, vocab: int | None = None,
+                           want_gate_score: bool = True, want_masks: bool = True,
+                           want_rank: bool = True, workspace: torch.Tensor | None = None,
+                           out: dict | None = None, stream=None) -> dict:
+    """Soft-gated evaluation of drafts (C x M int32) against aligned logits
+    (C x M x stride, rows contiguous).  Returns a dict of device tensors:
+    accept_len [C], best [n_groups], and optionally gate_score [C,M] fp32,
+    masks [C,M] uint8, rank [C,M] int32."""
+    lib = load_library()
+    if drafts.dtype != torch.int32 or drafts.dim() != 2 or not drafts.is_contiguous():
+        raise ValueError("drafts must be a contiguous C x M int32 tensor")
+    c, m = drafts.shape
+    if logits.dtype not in _TORCH_DTYPE or logits.dim() != 3 or tuple(logits.shape[:2]) != (c, m):
+        raise ValueError("logits must be C x M x V float32/float16/bfloat16")
+    if logits.stride(2) != 1:
+        raise ValueError("logits rows must be contiguous (stride(2) == 1)")
+    row_stride = logits.stride(1) if m > 1 else logits.stride(0)
+    if m > 1 and logits.stride(0) != m * row_stride:
+        raise ValueError("logits must have stride(0) == M * stride(1)")
+    if draft_len is not None and (draft_len.dtype != torch.int32 or not draft_len.is_contiguous()
+                                  or draft_len.numel() != c):
+        raise ValueError("draft_len must be a contiguous int32 tensor of C entries")
+    v = logits.shape[2] if vocab is None else vocab
+    dev = drafts.device
+    if out is None:
+        out = {"accept_len": torch.empty(c, dtype=torch.int32, device=dev),
+               "best": torch.empty(max(n_groups, 1), dtype=torch.int32, device=dev)}
+        if want_gate_score:
+            out["gate_score"] = torch.empty((c, m), dtype=torch.float32, device=dev)
+        if want_masks:
+            out["masks"] = torch.empty((c, m), dtype=torch.uint8, device=dev)
+        if want_rank:
+            out["rank"] = torch.empty((c, m), dtype=torch.int32, device=dev)
+    if workspace is None:
+        workspace = torch.empty(max(sense_soft_gate_verify_workspace_size(c, m, v), 1),
+                                dtype=torch.uint8, device=dev)
+    params = GateParams(gamma=gamma, topk=topk, window=window, tau=tau,
+                        entropy_normalized=int(bool(entropy_normalized)))
+    _check(lib.sense_soft_gate_verify(
+        _dev_ptr(logits, "logits"), _TORCH_DTYPE[logits.dtype], row_stride,
+        _dev_ptr(drafts, "drafts"), _dev_ptr(draft_len, "draft_len"), c, m, v, n_groups,
+        ctypes.byref(params), _dev_ptr(out["accept_len"], "out_accept_len"),
+        _dev_ptr(out["best"], "out_best"), _dev_ptr(out.get("gate_score"), "out_gate_score"),
+        _dev_ptr(out.get("masks"), "out_masks"), _dev_ptr(out.get("rank"), "out_rank"),
+        _dev_ptr(workspace, "workspace"), workspace.numel(), _stream_handle(stream)),
+        "sense_soft_gate_verify")
+    return out
+
+
+def sense_set_timer_events(which: int, start: "torch.cuda.Event | None",
+                           stop: "torch.cuda.Event | None") -> None:
+    """Have the next calls on this thread record ``start``/``stop`` around the
+    kernels named by ``which`` (SENSE_TIMER_*); None switches it off."""
+    sp = None if start is None else ctypes.c_void_p(start.cuda_event)
+    ep = None if stop is None else ctypes.c_void_p(stop.cuda_event)
+    _check(load_library().sense_set_timer_events(which, sp, ep), "sense_set_timer_events")

@@ -1,0 +1,168 @@
+"""Seeded synthetic workloads for the SENSE hot path.
+
+Input generation only: nothing here computes similarity, top-k or any part of
+the gate.  The same bytes feed both the HIP library and the CPU oracle.
+
+The datastores stand in for hidden states of the paper's target models
+(Llama-2/3 and Qwen families; their datastores and datasets are not
+available).  Keys are a Gaussian mixture: centroids ~ N(0, 1), rows = a
+uniformly chosen centroid + N(0, 0.3^2) noise, and a few "outlier" channels
+(the first n_outliers entries of a seeded permutation of the dimensions)
+scaled by 20, mimicking the large-magnitude channels of LLM hidden states.
+A query is a stored row plus N(0, 0.05^2) noise (queries of a batch come from
+distinct clusters).  Continuations are uniform token ids.  Logits are
+N(0, 2^2) with the draft token boosted by +6 at a Bernoulli(0.6) subset of
+positions.  Every normal law is written (mean, standard deviation).
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, replace
+
+import torch
+
+DTYPES = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    n: int               # stored rows
+    d: int               # key dimension (target hidden size)
+    key_dtype: str       # "f16" | "bf16"
+    n_queries: int
+    k: int               # retrieval top-k
+    span: int            # continuation length M
+    vocab: int
+    logits_dtype: str    # "f32" | "f16" | "bf16"
+    n_clusters: int
+    n_outliers: int
+    verify_queries: int  # queries whose k drafts are verified (groups)
+    metric: str = "cosine"
+
+    @property
+    def key_bytes(self) -> int:
+        return self.n * self.d * 2
+
+    @property
+    def n_cand(self) -> int:
+        return self.verify_queries * self.k
+
+    @property
+    def logit_bytes(self) -> int:
+        return self.n_cand * self.span * self.vocab * (4 if self.logits_dtype == "f32" else 2)
+
+
+WORKLOADS = {
+    w.name: w
+    for w in [
+        Workload("tiny-16k-d4096", 16_384, 4096, "f16", 1, 8, 8, 32_000, "f32", 256, 4, 1),
+        Workload("llama3-8b-262k-d4096", 262_144, 4096, "bf16", 1, 32, 10, 128_256, "f32",
+                 1024, 4, 1),
+        Workload("qwen2-7b-1m-d3584", 1_048_576, 3584, "bf16", 1, 64, 8, 152_064, "bf16",
+                 4096, 8, 1),
+        # Headline shape: 1M keys at d = 4096, otherwise the Qwen2-7B shape.
+        Workload("store-1m-d4096", 1_048_576, 4096, "bf16", 1, 64, 8, 152_064, "bf16",
+                 4096, 8, 1),
+        Workload("13b-batched-4m-d5120", 4_194_304, 5120, "f16", 16, 64, 8, 32_000, "f32",
+                 16_384, 4, 16),
+        Workload("70b-8m-d8192", 8_388_608, 8192, "bf16", 64, 128, 12, 128_256, "f32",
+                 16_384, 16, 4),
+    ]
+}
+HEADLINE = "store-1m-d4096"
+
+
+def scaled(w: Workload, **changes) -> Workload:
+    """A workload of the same recipe with some sizes changed."""
+    return replace(w, **changes)
+
+
+def _gen(seed: int, device) -> torch.Generator:
+    g = torch.Generator(device=device)
+    g.manual_seed(int(seed))
+    return g
+
+
+@dataclass
+class Datastore:
+    keys: torch.Tensor      # n x d (key dtype)
+    assign: torch.Tensor    # n int64 cluster of each row
+    outliers: torch.Tensor  # n_outliers int64 dims
+    spans: torch.Tensor     # n x span int32
+    span_len: torch.Tensor | None
+
+
+def make_datastore(w: Workload, seed: int, device, chunk_rows: int = 1 << 15,
+                   ragged_spans: bool = False, key_stride: int | None = None) -> Datastore:
+    """Keys, cluster labels and continuations of a workload.  key_stride > d
+    lays the rows out with padding (the padding holds a constant)."""
+    g = _gen(seed, device)
+    d = w.d
+    cent = torch.randn(w.n_clusters, d, generator=g, device=device)
+    assign = torch.randint(0, w.n_clusters, (w.n,), generator=g, device=device)
+    outl = torch.randperm(d, generator=g, device=device)[: w.n_outliers]
+    dt = DTYPES[w.key_dtype]
+    ld = d if key_stride is None else key_stride
+    if ld == d:
+        store = torch.empty((w.n, ld), dtype=dt, device=device)
+    else:
+        store = torch.full((w.n, ld), 7.0, dtype=dt, device=device)
+    keys = store[:, :d]
+    for r in range(0, w.n, chunk_rows):
+        c = min(chunk_rows, w.n - r)
+        x = cent[assign[r:r + c]]
+        x.add_(torch.randn(c, d, generator=g, device=device), alpha=0.3)
+        x[:, outl] *= 20.0
+        keys[r:r + c] = x.to(dt)
+        del x
+    spans = torch.randint(0, w.vocab, (w.n, w.span), generator=g, device=device, dtype=torch.int32)
+    span_len = None
+    if ragged_spans:
+        span_len = torch.randint(0, w.span + 1, (w.n,), generator=g, device=device,
+                                 dtype=torch.int32)
+    return Datastore(keys, assign, outl, spans, span_len)
+
+
+def make_queries(w: Workload, ds: Datastore, seed: int, n_queries: int | None = None):
+    """Queries = stored rows + N(0, 0.05^2) noise, fp32.  Returns (queries,
+    source rows).  Several queries come from distinct clusters."""
+    device = ds.keys.device
+    g = _gen(seed + 7919, device)
+    nq = w.n_queries if n_queries is None else n_queries
+    if nq == 1:
+        rows = torch.randint(0, w.n, (1,), generator=g, device=device)
+    else:
+        present = torch.unique(ds.assign)
+        pick = present[torch.randperm(present.numel(), generator=g, device=device)[:nq]]
+        rows = []
+        for c in pick.tolist():
+            members = torch.nonzero(ds.assign == c).flatten()
+            rows.append(members[torch.randint(0, members.numel(), (1,), generator=g,
+                                              device=device)])
+        rows = torch.cat(rows)
+    q = ds.keys[rows].float()
+    q.add_(torch.randn(q.shape, generator=g, device=device), alpha=0.05)
+    return q.contiguous(), rows
+
+
+def make_logits(w: Workload, drafts: torch.Tensor, seed: int, dtype: str | None = None,
+                boost: float = 6.0, p_boost: float = 0.6, std: float = 2.0,
+                chunk: int = 64) -> torch.Tensor:
+    """C x M x V logits ~ N(0, std^2); the draft token of each position gets
+    +boost with probability p_boost (draft ids outside [0, V) are skipped)."""
+    device = drafts.device
+    g = _gen(seed + 104729, device)
+    c, m = drafts.shape
+    dt = DTYPES[dtype or w.logits_dtype]
+    out = torch.empty((c, m, w.vocab), dtype=dt, device=device)
+    for c0 in range(0, c, chunk):
+        c1 = min(c, c0 + chunk)
+        x = torch.randn((c1 - c0, m, w.vocab), generator=g, device=device).mul_(std)
+        dr = drafts[c0:c1].long()
+        hit = (torch.rand((c1 - c0, m), generator=g, device=device) < p_boost)
+        hit &= (dr >= 0) & (dr < w.vocab)
+        idx = dr.clamp(0, w.vocab - 1).unsqueeze(-1)
+        x.scatter_add_(2, idx, (hit.float() * boost).unsqueeze(-1))
+        out[c0:c1] = x.to(dt)
+        del x
+    return out

@@ -1,0 +1,170 @@
+"""Host-side tests of the C ABI (no GPU needed, nothing is launched).
+
+The library must load, export every entry point include/sense.h declares,
+and reject bad arguments with the documented status before any device work.
+Pointers passed here are fake, aligned addresses: each call returns during
+validation, so none is dereferenced.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sense.h")
+
+from paper_2606_00021_amd import sense  # noqa: E402
+
+INVALID, MISALIGNED, UNSUPPORTED, WORKSPACE = 1, 2, 3, 5
+FAKE = 1 << 20          # 1 MiB-aligned fake device address
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return sense.load_library()
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sense_[a-z_]+)\s*\(", text)))
+
+
+def test_header_and_binding_agree():
+    assert declared_symbols() == sorted(sense.EXPORTED)
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in declared_symbols():
+        assert hasattr(lib, name), name
+
+
+def test_library_is_gfx950_only():
+    # The embedded offload bundle names its target; only gfx950 is built.
+    data = open(sense.LIB_PATH, "rb").read()
+    assert b"gfx950" in data
+    for other in (b"gfx942", b"gfx90a", b"gfx1100"):
+        assert other not in data
+
+
+def test_status_strings(lib):
+    for code in range(7):
+        assert lib.sense_status_string(code)
+    assert lib.sense_status_string(99) == b"unknown status"
+
+
+def p(x):
+    return ctypes.c_void_p(x)
+
+
+def desc(**kw):
+    base = dict(keys=p(FAKE), key_dtype=sense.SENSE_BF16, n=1000, d=256, key_stride=256,
+                spans=p(FAKE), max_span=8, span_len=None, metric=1, flags=0)
+    base.update(kw)
+    return sense.IndexDesc(**base)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(keys=None), INVALID),
+    (dict(spans=None), INVALID),
+    (dict(key_dtype=sense.SENSE_F32), INVALID),
+    (dict(n=0), INVALID),
+    (dict(n=1 << 31), INVALID),
+    (dict(d=0), INVALID),
+    (dict(d=8200, key_stride=8200), INVALID),
+    (dict(d=100, key_stride=104), INVALID),          # d % 8 != 0
+    (dict(key_stride=128), INVALID),                 # stride < d
+    (dict(max_span=0), INVALID),
+    (dict(max_span=65), INVALID),
+    (dict(metric=7), INVALID),
+    (dict(flags=4), INVALID),
+    (dict(keys=p(FAKE + 8)), MISALIGNED),
+    (dict(key_stride=260), MISALIGNED),
+])
+def test_build_index_rejects(lib, kw, status):
+    out = ctypes.c_void_p(123)
+    d = desc(**kw)
+    assert lib.sense_build_index(ctypes.byref(d), None, ctypes.byref(out)) == status
+    assert out.value is None                         # *out cleared
+    assert lib.sense_last_error_message()
+
+
+def test_build_index_null_args(lib):
+    out = ctypes.c_void_p()
+    assert lib.sense_build_index(None, None, ctypes.byref(out)) == INVALID
+    d = desc()
+    assert lib.sense_build_index(ctypes.byref(d), None, None) == INVALID
+
+
+def test_retrieve_rejects_null_index(lib):
+    size = ctypes.c_size_t()
+    assert lib.sense_retrieve_workspace_size(None, 1, 8, ctypes.byref(size)) == INVALID
+    assert lib.sense_retrieve(None, p(FAKE), 0, 1, 8, p(FAKE), None, None, None, p(FAKE),
+                              1 << 30, None) == INVALID
+    assert lib.sense_destroy_index(None) == 0
+
+
+def verify_call(lib, **kw):
+    a = dict(logits=p(FAKE), dtype=0, row_stride=1000, drafts=p(FAKE), draft_len=None,
+             n_cand=8, max_len=8, vocab=1000, n_groups=1,
+             params=sense.GateParams(gamma=0.05, topk=3, window=6, tau=0, entropy_normalized=1),
+             acc=p(FAKE), best=p(FAKE), gs=None, masks=None, rank=None, ws=p(FAKE),
+             ws_bytes=1 << 30)
+    a.update(kw)
+    prm = a["params"]
+    return lib.sense_soft_gate_verify(
+        a["logits"], a["dtype"], a["row_stride"], a["drafts"], a["draft_len"], a["n_cand"],
+        a["max_len"], a["vocab"], a["n_groups"], None if prm is None else ctypes.byref(prm),
+        a["acc"], a["best"], a["gs"], a["masks"], a["rank"], a["ws"], a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(params=None), INVALID),
+    (dict(n_cand=-1), INVALID),
+    (dict(max_len=0), INVALID),
+    (dict(max_len=65), INVALID),
+    (dict(vocab=0), INVALID),
+    (dict(row_stride=999), INVALID),
+    (dict(dtype=5), INVALID),
+    (dict(n_groups=3), INVALID),                     # 8 % 3 != 0
+    (dict(n_groups=0), INVALID),
+    (dict(logits=None), INVALID),
+    (dict(drafts=None), INVALID),
+    (dict(acc=None), INVALID),
+    (dict(best=None), INVALID),
+    (dict(params=sense.GateParams(gamma=0.05, topk=0, window=6, tau=0, entropy_normalized=1)), INVALID),
+    (dict(params=sense.GateParams(gamma=0.05, topk=3, window=-1, tau=0, entropy_normalized=1)), INVALID),
+    (dict(params=sense.GateParams(gamma=0.05, topk=3, window=65, tau=0, entropy_normalized=1)), INVALID),
+    (dict(params=sense.GateParams(gamma=0.05, topk=3, window=6, tau=-1, entropy_normalized=1)), INVALID),
+    (dict(params=sense.GateParams(gamma=float("nan"), topk=3, window=6, tau=0, entropy_normalized=1)), INVALID),
+    (dict(ws=None), WORKSPACE),
+    (dict(ws_bytes=16), WORKSPACE),
+    (dict(ws=p(FAKE + 64)), MISALIGNED),
+    (dict(logits=p(FAKE + 2)), MISALIGNED),          # fp32 logits off their element size
+])
+def test_verify_rejects(lib, kw, status):
+    assert verify_call(lib, **kw) == status
+    assert lib.sense_last_error_message()
+
+
+def test_verify_empty_batch_is_a_no_op(lib):
+    assert verify_call(lib, n_cand=0, logits=None, drafts=None, acc=None, best=None, ws=None) == 0
+
+
+def test_verify_workspace_size(lib):
+    size = ctypes.c_size_t()
+    assert lib.sense_soft_gate_verify_workspace_size(64, 8, 152064, ctypes.byref(size)) == 0
+    assert size.value >= 64 * 8 * 16                 # one 16-byte partial per row at least
+    assert lib.sense_soft_gate_verify_workspace_size(8, 65, 100, ctypes.byref(size)) == INVALID
+    assert lib.sense_soft_gate_verify_workspace_size(8, 8, 100, None) == INVALID
+
+
+def test_binding_refuses_host_tensors():
+    import torch
+    keys = torch.zeros(16, 8, dtype=torch.bfloat16)
+    spans = torch.zeros(16, 4, dtype=torch.int32)
+    with pytest.raises(ValueError):
+        sense.sense_build_index(keys, spans)
+    with pytest.raises(ValueError):
+        sense.sense_soft_gate_verify(torch.zeros(2, 3, 10), torch.zeros(2, 3, dtype=torch.int32))

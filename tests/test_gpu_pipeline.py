@@ -1,0 +1,44 @@
+"""End-to-end parity: retrieval feeds verification exactly as the benchmark
+step does (same entry points, same preallocated workspaces and outputs)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_00021_amd import sense, synth
+from parity import check_topk, check_verify, dt_name, host_bits
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("name,scale", [("tiny-16k-d4096", {}),
+                                        ("store-1m-d4096", {"n": 40000, "n_clusters": 160})])
+def test_retrieve_then_verify(name, scale):
+    w = synth.scaled(synth.WORKLOADS[name], **scale)
+    dev = torch.device("cuda")
+    print(f"[pipeline] {w.name} n={w.n}", flush=True)
+    ds = synth.make_datastore(w, 77, dev)
+    q, _ = synth.make_queries(w, ds, 77)
+    index = sense.sense_build_index(ds.keys, ds.spans, ds.span_len)
+    nq, k, m = w.n_queries, w.k, w.span
+    ws_r = torch.empty(sense.sense_retrieve_workspace_size(index, nq, k), dtype=torch.uint8,
+                       device=dev)
+    outs = (torch.empty((nq, k), dtype=torch.int64, device=dev),
+            torch.empty((nq, k), dtype=torch.float32, device=dev),
+            torch.empty((nq, k, m), dtype=torch.int32, device=dev),
+            torch.empty((nq, k), dtype=torch.int32, device=dev))
+    sense.sense_retrieve(index, q, k, workspace=ws_r, out=outs)
+    drafts = outs[2][:w.verify_queries].reshape(-1, m)
+    dlen = outs[3][:w.verify_queries].reshape(-1)
+    logits = synth.make_logits(w, drafts, 77)
+    out = sense.sense_soft_gate_verify(logits, drafts, dlen, n_groups=w.verify_queries)
+    torch.cuda.synchronize()
+
+    o_s = oracle.scores(host_bits(ds.keys), w.key_dtype, q.cpu().numpy(), "f32")
+    check_topk(outs[0][0].cpu().numpy(), outs[1][0].cpu().numpy(), o_s[0], k)
+    o_dr, o_dl = oracle.gather(ds.spans.cpu().numpy(), None, outs[0][0].cpu().numpy())
+    assert np.array_equal(drafts[:k].cpu().numpy(), o_dr)
+    ref = oracle.soft_gate_verify(host_bits(logits), dt_name(logits), drafts.cpu().numpy(),
+                                  dlen.cpu().numpy(), n_groups=w.verify_queries)
+    check_verify(out, ref, 0.05, dlen.cpu().numpy())
+    index.close()
