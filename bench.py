@@ -169,6 +169,12 @@ def main():
               for _ in range(K)] for t in ("scan", "topk", "verify")}
     timer_id = {"scan": sense.SENSE_TIMER_SCAN, "topk": sense.SENSE_TIMER_TOPK,
                 "verify": sense.SENSE_TIMER_VERIFY}
+    # torch creates the underlying hipEvent_t lazily at the first record():
+    # record every event once here so that the handles exist.
+    for t in ev:
+        for a, b in ev[t]:
+            a.record()
+            b.record()
     t_begin = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()

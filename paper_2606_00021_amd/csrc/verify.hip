@@ -126,19 +126,20 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 template <int LT>
 __device__ __forceinline__ void unpack(const u32x4& w, float (&x)[LT == DT_F32 ? 4 : 8]) {
-    if constexpr (LT == DT_F32) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) x[i] = __builtin_bit_cast(float, w[i]);
-    } else {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            if constexpr (LT == DT_BF16) {
-                x[2 * i] = __builtin_bit_cast(float, w[i] << 16);
-                x[2 * i + 1] = __builtin_bit_cast(float, w[i] & 0xFFFF0000u);
-            } else {
-                x[2 * i] = (float)__builtin_bit_cast(_Float16, (uint16_t)(w[i] & 0xFFFFu));
-                x[2 * i + 1] = (float)__builtin_bit_cast(_Float16, (uint16_t)(w[i] >> 16));
-            }
+    for (int i = 0; i < 4; ++i) {
+        // Copy the lane out first: a bit_cast applied directly to an element
+        // of an ext_vector_type is mis-compiled by this hipcc (it reads the
+        // wrong element).
+        const uint32_t u = w[i];
+        if constexpr (LT == DT_F32) {
+            x[i] = __builtin_bit_cast(float, u);
+        } else if constexpr (LT == DT_BF16) {
+            x[2 * i] = __builtin_bit_cast(float, u << 16);
+            x[2 * i + 1] = __builtin_bit_cast(float, u & 0xFFFF0000u);
+        } else {
+            x[2 * i] = (float)__builtin_bit_cast(_Float16, (uint16_t)(u & 0xFFFFu));
+            x[2 * i + 1] = (float)__builtin_bit_cast(_Float16, (uint16_t)(u >> 16));
         }
     }
 }

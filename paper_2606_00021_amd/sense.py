@@ -304,4 +304,7 @@ def sense_set_timer_events(which: int, start: "torch.cuda.Event | None",
     kernels named by ``which`` (SENSE_TIMER_*); None switches it off."""
     sp = None if start is None else ctypes.c_void_p(start.cuda_event)
     ep = None if stop is None else ctypes.c_void_p(stop.cuda_event)
+    if start is not None and (not sp.value or not ep.value):
+        raise ValueError("record the events once before registering them (torch creates "
+                         "the underlying hipEvent_t at the first record())")
     _check(load_library().sense_set_timer_events(which, sp, ep), "sense_set_timer_events")
