@@ -39,25 +39,42 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="approximate CPU time spent timing the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="after the timed region, run one plain device copy of this many MiB "
+                         "(a reference kernel of known traffic for HBM counter runs)")
     return ap.parse_args()
 
 
+def scan_source_digest() -> str:
+    """Digest of the scan kernel's source code with comments and blank space
+    removed (comment edits do not invalidate measured counters)."""
+    import hashlib
+    import re
+
+    src = open(os.path.join(ROOT, "paper_2606_00021_amd", "csrc", "scan.hip")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", "", src)
+    src = "".join(src.split())
+    return hashlib.sha256(src.encode()).hexdigest()[:16]
+
+
 def traffic_from_profiles(workload: str):
-    """Measured HBM bytes per scan launch, if a counter summary for this
-    workload and the current scan kernel is committed under profiles/."""
-    path = os.path.join(ROOT, "profiles", f"scan_traffic_{workload}.json")
+    """Measured HBM bytes per scan launch, read from the committed rocprofv3
+    counter summary of this workload, or None when there is none or the scan
+    source changed since the counters were taken."""
+    import hashlib
+
+    path = os.path.join(ROOT, "profiles", f"scan_gemv_kernel_{workload}.md")
     if not os.path.exists(path):
         return None
-    try:
-        rec = json.load(open(path))
-    except Exception:
+    fields = {}
+    for line in open(path):
+        if ":" in line and not line.startswith(("|", "-", "#", "`")):
+            key, _, val = line.partition(":")
+            fields[key.strip()] = val.strip()
+    if fields.get("scan_source_sha256_16") != scan_source_digest() or "bytes_per_launch" not in fields:
         return None
-    src = os.path.join(ROOT, "paper_2606_00021_amd", "csrc", "scan.hip")
-    import hashlib
-    digest = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
-    if rec.get("scan_source_sha256_16") != digest:
-        return None       # the kernel changed since the counters were taken
-    return rec.get("bytes_per_launch")
+    return int(fields["bytes_per_launch"])
 
 
 def cpu_baseline(w, ds, q, logits, drafts, budget_s: float):
@@ -230,6 +247,16 @@ def main():
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": scan_gbps / HBM_PEAK_GBPS,
                      "traffic": traffic_from_profiles(name)},
     }
+    if args.copy_probe_mib > 0:
+        n_el = args.copy_probe_mib * (1 << 20) // 4
+        src = torch.ones(n_el, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] copy probe: {args.copy_probe_mib} MiB read + {args.copy_probe_mib} MiB "
+            f"written by one copy kernel")
+        del src, dst
     if not args.no_cpu_baseline:
         log("[bench] timing the oracle on the host (cpu_baseline)")
         t0 = time.perf_counter()

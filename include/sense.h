@@ -10,15 +10,15 @@
  * the data-parallel part of that loop:
  *
  *   sense_build_index       the datastore C_db of (key, continuation) pairs
- *                           (Sec. 2.1 Eq. 2; Sec. 2.2 Eq. 6)
+ *                           (Sec. 3.1 Eq. 2; Sec. 3.2 Eq. 6)
  *   sense_retrieve          exact similarity scan + per-query top-k + gather
  *                           of each hit's continuation into a draft batch
- *                           (Sec. 2.1 Eq. 3; Sec. 2.2 Eqs. 7-8; Alg. 2's
+ *                           (Sec. 3.1 Eq. 3; Sec. 3.2 Eqs. 7-8; Alg. 2's
  *                           L2Norm and retrieval steps)
  *   sense_soft_gate_verify  soft-gated evaluation of a draft batch against
  *                           aligned logits: accepted prefix length per draft
  *                           and the best draft per group
- *                           (Sec. 2.3 Eqs. 11-17; Alg. 4)
+ *                           (Sec. 3.3 Eqs. 12-18; Alg. 4)
  *
  * Conventions shared by every entry point
  *   - Pointers named keys, spans, span_len, queries, logits, drafts,
@@ -59,7 +59,7 @@ typedef enum {
 
 typedef enum { SENSE_F32 = 0, SENSE_F16 = 1, SENSE_BF16 = 2 } sense_dtype_t;
 
-/* Similarity of Sec. 2.2 Eq. 7.  COSINE is the inner product of the
+/* Similarity of Sec. 3.2 Eq. 8.  COSINE is the inner product of the
  * L2-normalised query and key (the paper L2-normalises both before search);
  * the key norms are those of the stored fp16/bf16 values. */
 typedef enum { SENSE_METRIC_IP = 0, SENSE_METRIC_COSINE = 1 } sense_metric_t;
@@ -71,7 +71,7 @@ typedef enum { SENSE_METRIC_IP = 0, SENSE_METRIC_COSINE = 1 } sense_metric_t;
 
 typedef struct sense_index sense_index_t; /* opaque host handle */
 
-/* Datastore descriptor (Sec. 2.1 Eq. 2: pairs (k_i, c_i) with |c_i| <= M).
+/* Datastore descriptor (Sec. 3.1 Eq. 2: pairs (k_i, c_i) with |c_i| <= M).
  *   keys       N x key_stride elements of key_dtype (F16 or BF16), row-major,
  *              row i's d elements contiguous.  Borrowed: must outlive the
  *              index unless SENSE_INDEX_COPY_KEYS.  Without the copy flag the
@@ -124,7 +124,7 @@ sense_status_t sense_index_info(const sense_index_t *index, int64_t *n, int32_t 
 sense_status_t sense_retrieve_workspace_size(const sense_index_t *index, int32_t n_queries,
                                              int32_t k, size_t *bytes);
 
-/* Retrieval (Sec. 2.1 Eq. 3; Sec. 2.2 Eqs. 7-8; Alg. 2's L2Norm and search
+/* Retrieval (Sec. 3.1 Eq. 3; Sec. 3.2 Eqs. 7-8; Alg. 2's L2Norm and search
  * steps), exact: for each query q,
  *   s[q, i] = sum_t q_t K[i, t]                    (IP)
  *   s[q, i] = that / (||q|| ||K_i||), 0 if a norm is 0   (COSINE)
@@ -149,7 +149,7 @@ sense_status_t sense_retrieve(const sense_index_t *index, const void *queries,
                               int32_t *out_draft_len, void *workspace,
                               size_t workspace_bytes, void *stream);
 
-/* Soft-gate hyper-parameters (Alg. 4 inputs; Sec. 2.3; defaults of the
+/* Soft-gate hyper-parameters (Alg. 4 inputs; Sec. 3.3; defaults of the
  * paper's experiments: gamma 0.05, top-k 3, W 6).
  *   gamma              entropy threshold: B_ent = I(E' > gamma)
  *   topk               k of the top-k membership mask, >= 1
@@ -169,11 +169,11 @@ typedef struct {
 sense_status_t sense_soft_gate_verify_workspace_size(int32_t n_cand, int32_t max_len,
                                                      int32_t vocab, size_t *bytes);
 
-/* Soft-gated evaluation (Sec. 2.3 Eqs. 11-17; Alg. 4) of n_cand drafts.
+/* Soft-gated evaluation (Sec. 3.3 Eqs. 12-18; Alg. 4) of n_cand drafts.
  *   logits     n_cand x max_len rows of row_stride elements (F32, F16 or
  *              BF16); row (c, j) starts at element (c*max_len + j)*row_stride
  *              and is the target's distribution PREDICTING drafts[c][j] (the
- *              aligned rows of Sec. 2.2: row 0 of every draft is the shared
+ *              aligned rows of Sec. 3.2 Eq. 11: row 0 of every draft is the shared
  *              distribution at the current position).  Only rows with
  *              j < draft_len[c] are read.  Vector loads are used when the
  *              base is 16-byte aligned and row_stride*elem_size % 16 == 0.

@@ -10,7 +10,7 @@
  * Every quantity is computed in IEEE double precision, following the paper's
  * definitions literally:
  *
- *   Retrieval (Sec. 2.1 Eq. 3 "retriever R", Sec. 2.2 Eq. 7 "sim",
+ *   Retrieval (Sec. 3.1 Eq. 3 "retriever R", Sec. 3.2 Eq. 8 "sim",
  *   Alg. 2 "L2Norm" and "FAISS" steps):  the exact similarity of the query to
  *   every stored key (inner product, or cosine = inner product of the
  *   L2-normalised vectors), then a FULL sort of all N rows by
@@ -19,7 +19,7 @@
  *   The paper's own retriever is an approximate (IVF-PQ) index; the exact
  *   scan is the plain definition that index approximates.
  *
- *   Verification (Sec. 2.3 Eqs. 11-17, Alg. 4 "SGE"): per candidate c and
+ *   Verification (Sec. 3.3 Eqs. 12-18, Alg. 4 "SGE"): per candidate c and
  *   draft position j, the greedy token Y = argmax (first occurrence), the
  *   exact-match mask, softmax entropy (optionally divided by log|V|) against
  *   gamma, top-k membership of the draft token (full stable sort of the
@@ -29,7 +29,7 @@
  * Readings taken where the paper is silent or inconsistent (each one is also
  * listed with its reason in the design notes of the repository):
  *   - entropy is normalised by ln|V| when entropy_normalized != 0 (Alg. 4),
- *     raw nats otherwise (Eq. 12's text form);
+ *     raw nats otherwise (Eq. 14's text form);
  *   - softmax is applied to raw logits at temperature 1;
  *   - top-k ties are broken by lower vocabulary index; argmax takes the first
  *     maximum; the best candidate is the first one with the largest length;

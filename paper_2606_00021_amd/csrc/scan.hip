@@ -1,4 +1,4 @@
-// Similarity scan of the SENSE retrieval step (Sec. 2.2 Eq. 7 "sim",
+// Similarity scan of the SENSE retrieval step (Sec. 3.2 Eq. 8 "sim",
 // Alg. 2's L2Norm and search steps), exact over all stored keys.
 //
 // Single-query GEMV on the vector ALUs.  The scan moves N*d*2 bytes of keys

@@ -1,7 +1,7 @@
-// Per-query top-k of the similarity scores (Sec. 2.1 Eq. 3: the retriever
-// returns the N most relevant continuations; Sec. 2.2 Eq. 8 "top-N'") and
+// Per-query top-k of the similarity scores (Sec. 3.1 Eq. 3: the retriever
+// returns the N most relevant continuations; Sec. 3.2 Eq. 7 "top-N'") and
 // the gather of each hit's continuation into the draft batch (the (k_i, s_i)
-// pairs of Sec. 2.2).
+// pairs of Sec. 3.2).
 //
 // Order: score descending, then row index ascending.  Each (score, row) pair
 // is packed into one unique 64-bit key (order-preserving score bits in the

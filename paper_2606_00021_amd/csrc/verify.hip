@@ -1,4 +1,4 @@
-// Soft-gated evaluation (Sec. 2.3 Eqs. 11-17; Alg. 4) of a candidate draft
+// Soft-gated evaluation (Sec. 3.3 Eqs. 12-18; Alg. 4) of a candidate draft
 // batch against the target's aligned logits.
 //
 // The cost is one read of the logits of every live (candidate, position)

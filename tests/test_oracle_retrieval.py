@@ -4,7 +4,7 @@ Each test checks the oracle against something other than itself: hand-worked
 values (golden fixture), numpy's own float16 decoding and BLAS products with
 lexsort, closed forms (a planted copy has cosine 1), and invariances of the
 definition (cosine under positive power-of-two scaling, IP = cosine for unit
-keys).  Sec. 2.1 Eq. 3, Sec. 2.2 Eq. 7 and Alg. 2 define the computation.
+keys).  Sec. 3.1 Eq. 3, Sec. 3.2 Eqs. 7-8 and Alg. 2 define the computation.
 """
 import json
 import os

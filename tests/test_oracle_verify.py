@@ -1,4 +1,4 @@
-"""Pins for the soft-gated evaluation half of the oracle (Alg. 4, Sec. 2.3).
+"""Pins for the soft-gated evaluation half of the oracle (Alg. 4, Sec. 3.3).
 
 The oracle is checked against closed forms (entropy of uniform and two-valued
 distributions), the hand-worked look-ahead window fixture, special cases that
