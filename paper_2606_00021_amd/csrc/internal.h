@@ -53,11 +53,21 @@ __host__ __device__ inline uint32_t key_row(uint64_t k) {
 hipError_t launch_key_norms(const void* keys, int key_dtype, int64_t n, int d, int64_t ld,
                             float* inv_norm, hipStream_t stream);
 
+// Query batches of at least this many run as an MFMA contraction; smaller
+// ones run the single-query GEMV once per query.
+constexpr int kMfmaMinQueries = 4;
+
 // scores[q * n + i] = similarity of query q and row i for q in [0, nq).
-// queries: nq x d fp32 (already converted).  inv_norm NULL for IP.
+// queries: nq x d fp32 (already converted).  inv_norm NULL for IP.  split:
+// the queries are not exactly representable in the key type (MFMA path
+// multiplies a hi and a lo half).  scratch: scan_scratch_bytes(nq, d) bytes.
 hipError_t launch_scan(const void* keys, int key_dtype, int64_t n, int d, int64_t ld,
-                       const float* queries, int nq, const float* inv_norm, float* scores,
-                       hipStream_t stream);
+                       const float* queries, int nq, bool split, const float* inv_norm,
+                       float* scores, void* scratch, hipStream_t stream);
+size_t scan_mfma_scratch_bytes(int nq, int d);
+hipError_t launch_scan_mfma(const void* keys, int key_dtype, int64_t n, int d, int64_t ld,
+                            const float* queries, int nq, bool split, const float* inv_norm,
+                            float* scores, void* scratch, hipStream_t stream);
 
 // Converts nq x d queries of dtype q_dtype to fp32 (plain copy for fp32).
 hipError_t launch_query_to_f32(const void* q, int q_dtype, int nq, int d, float* out,

@@ -272,8 +272,11 @@ hipError_t launch_query_to_f32(const void* q, int q_dtype, int nq, int d, float*
 }
 
 hipError_t launch_scan(const void* keys, int key_dtype, int64_t n, int d, int64_t ld,
-                       const float* queries, int nq, const float* inv_norm, float* scores,
-                       hipStream_t stream) {
+                       const float* queries, int nq, bool split, const float* inv_norm,
+                       float* scores, void* scratch, hipStream_t stream) {
+    if (nq >= kMfmaMinQueries)
+        return launch_scan_mfma(keys, key_dtype, n, d, ld, queries, nq, split, inv_norm, scores,
+                                scratch, stream);
     for (int q = 0; q < nq; ++q) {
         const float* qp = queries + (int64_t)q * d;
         float* sp = scores + (int64_t)q * n;

@@ -1,0 +1,352 @@
+// Similarity scan for a batch of queries as a dense contraction on the
+// matrix cores (Sec. 3.2 Eq. 8 "sim" for every query of a batch against
+// every stored key: S = Q K^T).
+//
+// With Q queries each key element carries 2Q flops, so at Q >= 16 the vector
+// ALUs could not keep up with HBM; v_mfma_f32_16x16x32_{bf16,f16} does.  The
+// queries are the A operand (16 queries x 32 dims per instruction), the keys
+// the B operand (32 dims x 16 keys); fp32 accumulation.  An fp32 query is
+// split into q = hi + lo, both in the key's 16-bit type, and both halves are
+// multiplied (two instructions), which keeps ~16 (bf16) / ~22 (fp16)
+// mantissa bits of the query instead of 8 / 11; queries already given in the
+// key type need only the hi half.
+//
+// Lane layout of the instruction (checked on gfx950): lane l supplies
+// A[m = l%16][k = 8*(l/16) .. +8], B[k = 8*(l/16) .. +8][n = l%16] and
+// receives D[m = 4*(l/16) + i][n = l%16], i = 0..3.  So each lane loads 16
+// contiguous bytes of one key row straight from HBM into its B fragment: one
+// load instruction covers 64 bytes of each of 16 rows.  A wave owns blocks
+// of 16*T keys, holds T x MT accumulator tiles, and walks the dimension in
+// steps of 32 with the next step's fragments already in flight.  Query
+// fragments (at most 64 queries x d x 2 halves) are read through the caches;
+// they are shared by every wave.
+#include "internal.h"
+
+namespace sense {
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+
+template <int KT>
+__device__ __forceinline__ f32x4 mfma(const u32x4& a, const u32x4& b, const f32x4& c) {
+    if constexpr (KT == DT_BF16) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                       __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+    } else {
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a),
+                                                      __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+    }
+}
+
+// Round-to-nearest-even fp32 -> 16-bit key type, as raw bits.
+template <int KT>
+__device__ __forceinline__ uint16_t to_key_bits(float x) {
+    if constexpr (KT == DT_BF16) {
+        const uint32_t u = __builtin_bit_cast(uint32_t, x);
+        if ((u & 0x7F800000u) == 0x7F800000u) return (uint16_t)((u >> 16) | ((u & 0xFFFFu) ? 0x40u : 0u));
+        return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+    } else {
+        return __builtin_bit_cast(uint16_t, (_Float16)x);
+    }
+}
+template <int KT>
+__device__ __forceinline__ float from_key_bits(uint16_t b) {
+    if constexpr (KT == DT_BF16) {
+        return __builtin_bit_cast(float, (uint32_t)b << 16);
+    } else {
+        return (float)__builtin_bit_cast(_Float16, b);
+    }
+}
+
+// Pads the query batch to qpad rows and splits each fp32 value into hi + lo
+// in the key type; inv_qn[q] = 1/||q|| (cosine), 1 (inner product), 0 for
+// padding rows.  One block (256 threads) per padded query row.
+template <int KT>
+__global__ __launch_bounds__(256) void query_split_kernel(const float* __restrict__ q, int nq,
+                                                          int d, bool cosine,
+                                                          uint16_t* __restrict__ qhi,
+                                                          uint16_t* __restrict__ qlo,
+                                                          float* __restrict__ inv_qn) {
+    const int row = blockIdx.x;
+    float ss = 0.0f;
+    for (int t = threadIdx.x; t < d; t += 256) {
+        const float x = row < nq ? q[(int64_t)row * d + t] : 0.0f;
+        const uint16_t hb = to_key_bits<KT>(x);
+        const float lo = x - from_key_bits<KT>(hb);
+        qhi[(int64_t)row * d + t] = hb;
+        qlo[(int64_t)row * d + t] = to_key_bits<KT>(lo);
+        ss = __builtin_fmaf(x, x, ss);
+    }
+    __shared__ float s_part[256];
+    s_part[threadIdx.x] = ss;
+    __syncthreads();
+    for (int off = 128; off > 0; off >>= 1) {
+        if ((int)threadIdx.x < off) s_part[threadIdx.x] += s_part[threadIdx.x + off];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        const float s = s_part[0];
+        float v = 1.0f;
+        if (row >= nq) v = 0.0f;
+        else if (cosine) v = (s > 0.0f) ? 1.0f / __builtin_sqrtf(s) : 0.0f;
+        inv_qn[row] = v;
+    }
+}
+
+// Waits until at most N vector-memory operations of this wave are still
+// outstanding (they complete in issue order).  Also a compiler barrier for
+// memory accesses.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// 16 bytes per lane from global memory straight into LDS: lane l's bytes land
+// at lds + 16*l (lds is wave-uniform).  Written as inline assembly so that
+// the compiler's wait-count model does not see an LDS write it cannot
+// attribute to a ring slot (it would then wait for every outstanding load
+// before each LDS read); the waits are explicit instead.
+// m0 is a reserved register: the compiler never keeps a value in it across
+// code it does not control and sets it right before each of its own uses, so
+// listing it as clobbered here is safe (clang warns about it regardless).
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16(const void* g, void* lds) {
+    const uint32_t base = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(base)
+                 : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// Workgroup barrier without the memory fence __syncthreads() adds (the fence
+// would wait for every outstanding load, draining the pipeline).  LDS data
+// written by DMA is complete once the issuing wave's vmcnt wait returns.
+__device__ __forceinline__ void barrier_no_fence() { asm volatile("s_barrier" ::: "memory"); }
+
+// One workgroup (4 waves) per contiguous run of key blocks; a block is 4*T
+// tiles of 16 keys, T tiles per wave; MT tiles of 16 queries (nq <= 16*MT of
+// them are real).
+//
+// Everything the matrix cores read goes through LDS, filled by
+// global_load_lds_dwordx4 (HBM/L2 -> LDS without registers) into a ring of P
+// stages; a stage is one 32-dimension step: each wave's T key fragments
+// (1 KiB each, lane-ordered, private to the wave) and the MT*(1+SPLIT) query
+// fragments shared by the four waves (each wave loads its share).  Loading
+// stays P-1 steps ahead of the matrix cores.  Every step a wave issues the
+// same number of loads (steps past the end reload a valid clamped address),
+// so the wait for a step is a fixed vmcnt; a workgroup barrier then makes the
+// other waves' query fragments visible and frees the slot that is refilled
+// next.  The loop holds no register-destination global load, because the
+// compiler's wait-count model does not follow LDS-DMA loads and would
+// otherwise drain the whole pipeline.  Lanes whose row lies past n load the
+// last row (their outputs are never stored); dimensions past d occur only in
+// the last step and are zeroed there.
+template <int KT, int MT, int T, int P, bool SPLIT>
+__global__ __launch_bounds__(256) void scan_mfma_kernel(
+    const uint16_t* __restrict__ keys, int64_t ld, int64_t n, int d,
+    const uint16_t* __restrict__ qhi, const uint16_t* __restrict__ qlo,
+    const float* __restrict__ inv_qn, int nq, const float* __restrict__ inv_norm,
+    float* __restrict__ scores, int64_t blocks_per_group) {
+    constexpr int NA = MT * (SPLIT ? 2 : 1);      // query fragments per step
+    constexpr int NA_W = (NA + 3) / 4;            // loaded per wave (some waves idle)
+    constexpr int OPS = T + NA_W;                 // DMA loads per wave per step
+    constexpr int KB = 64 * T;                    // keys per workgroup block
+    static_assert((P - 2) * OPS < 64, "vmcnt range");
+    __shared__ __attribute__((aligned(16))) u32x4 kring[P][4][T][64];
+    __shared__ __attribute__((aligned(16))) u32x4 aring[P][NA_W * 4][64];
+    const int lane = threadIdx.x & 63;
+    const int wv = threadIdx.x >> 6;
+    const int col = lane & 15, grp = lane >> 4;
+    const int64_t nblk = (n + KB - 1) / KB;
+    const int64_t b0 = (int64_t)blockIdx.x * blocks_per_group;
+    if (b0 >= nblk) return;                       // uniform over the workgroup
+    const int64_t b1 = (b0 + blocks_per_group < nblk) ? b0 + blocks_per_group : nblk;
+    const int nks = (d + 31) / 32;
+    const bool ragged = (d & 31) != 0;
+
+    // Query fragment a of this wave's share: a = wv + 4*j; fragment index f
+    // in [0, NA): f < MT -> hi tile f, else lo tile f - MT.
+    const uint16_t* qsrc[NA_W];
+#pragma unroll
+    for (int j = 0; j < NA_W; ++j) {
+        int f = wv + 4 * j;
+        if (f >= NA) f = NA - 1;                  // idle slot: harmless duplicate
+        const uint16_t* base = (f < MT) ? qhi : qlo;
+        const int mt = (f < MT) ? f : f - MT;
+        qsrc[j] = base + (int64_t)(mt * 16 + col) * d;
+    }
+    auto kofs = [&](int s) -> int {               // clamped dimension offset
+        const int sc = s < nks ? s : nks - 1;
+        const int kd = sc * 32 + grp * 8;
+        return kd < d ? kd : 0;
+    };
+
+    for (int64_t blk = b0; blk < b1; ++blk) {
+        const int64_t key0 = blk * KB + (int64_t)wv * 16 * T;
+        const uint16_t* kp[T];
+        bool kv[T];
+#pragma unroll
+        for (int t = 0; t < T; ++t) {
+            const int64_t row = key0 + t * 16 + col;
+            kv[t] = row < n;
+            kp[t] = keys + (kv[t] ? row : n - 1) * ld;
+        }
+        auto issue = [&](int s) {
+            const int ko = kofs(s);
+            const int slot = s % P;
+#pragma unroll
+            for (int t = 0; t < T; ++t)
+                dma16(kp[t] + ko, &kring[slot][wv][t][0]);
+#pragma unroll
+            for (int j = 0; j < NA_W; ++j)
+                dma16(qsrc[j] + ko, &aring[slot][wv + 4 * j][0]);
+        };
+        f32x4 acc[T][MT];
+#pragma unroll
+        for (int t = 0; t < T; ++t)
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) acc[t][mt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+
+#pragma unroll
+        for (int s = 0; s < P - 1; ++s) issue(s);
+        for (int ks = 0; ks < nks; ++ks) {
+            // Loads issued after step ks: steps ks+1 .. ks+P-2.
+            wait_vmcnt<(P - 2) * OPS>();
+            barrier_no_fence();
+            issue(ks + P - 1);                    // refills the slot read at ks-1
+            const int slot = ks % P;
+            const bool mask = ragged && ks == nks - 1 && ks * 32 + grp * 8 >= d;
+            u32x4 a[NA];
+#pragma unroll
+            for (int f = 0; f < NA; ++f) {
+                a[f] = aring[slot][f][lane];
+                if (mask) a[f] = u32x4{0u, 0u, 0u, 0u};
+            }
+#pragma unroll
+            for (int t = 0; t < T; ++t) {
+                u32x4 b = kring[slot][wv][t][lane];
+                if (mask) b = u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) {
+                    acc[t][mt] = mfma<KT>(a[mt], b, acc[t][mt]);
+                    if constexpr (SPLIT) acc[t][mt] = mfma<KT>(a[MT + mt], b, acc[t][mt]);
+                }
+            }
+        }
+        // Drain the surplus loads and let every wave finish reading the ring
+        // before the next block's prologue refills it.
+        wait_vmcnt<0>();
+        barrier_no_fence();
+
+#pragma unroll
+        for (int t = 0; t < T; ++t) {
+            const int64_t key = key0 + t * 16 + col;
+            if (!kv[t]) continue;
+            const float kscale = inv_norm ? inv_norm[key] : 1.0f;
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int q = mt * 16 + grp * 4 + i;
+                    if (q < nq) {
+                        float v = acc[t][mt][i];
+                        if (inv_norm) v = v * kscale;
+                        scores[(int64_t)q * n + key] = v * inv_qn[q];
+                    }
+                }
+            }
+        }
+    }
+}
+
+int g_cus = 0;
+int cus() {
+    if (g_cus == 0) {
+        int dev = 0;
+        hipDeviceProp_t prop;
+        g_cus = (hipGetDevice(&dev) == hipSuccess &&
+                 hipGetDeviceProperties(&prop, dev) == hipSuccess && prop.multiProcessorCount > 0)
+                    ? prop.multiProcessorCount
+                    : 256;
+    }
+    return g_cus;
+}
+
+template <int KT, int MT, int T, int P, bool SPLIT>
+hipError_t launch_tile(const void* keys, int64_t n, int d, int64_t ld, const uint16_t* qhi,
+                       const uint16_t* qlo, const float* inv_qn, int nq, const float* inv_norm,
+                       float* scores, hipStream_t stream) {
+    auto kern = scan_mfma_kernel<KT, MT, T, P, SPLIT>;
+    static int per_cu = 0;
+    if (per_cu < 1 &&
+        (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, 256, 0) != hipSuccess ||
+         per_cu < 1))
+        per_cu = 1;
+    const int64_t nblk = (n + 64 * T - 1) / (64 * T);
+    const int64_t groups_max = (int64_t)cus() * per_cu;
+    int64_t bpg = (nblk + groups_max - 1) / groups_max;
+    if (bpg < 1) bpg = 1;
+    const int64_t groups = (nblk + bpg - 1) / bpg;
+    hipLaunchKernelGGL(kern, dim3((unsigned)groups), dim3(256), 0, stream, (const uint16_t*)keys,
+                       ld, n, d, qhi, qlo, inv_qn, nq, inv_norm, scores, bpg);
+    return hipGetLastError();
+}
+
+template <int KT, bool SPLIT>
+hipError_t launch_group(const void* keys, int64_t n, int d, int64_t ld, const uint16_t* qhi,
+                        const uint16_t* qlo, const float* inv_qn, int nq, const float* inv_norm,
+                        float* scores, hipStream_t stream) {
+    switch ((nq + 15) / 16) {
+        case 1: return launch_tile<KT, 1, 8, 4, SPLIT>(keys, n, d, ld, qhi, qlo, inv_qn, nq, inv_norm, scores, stream);
+        case 2: return launch_tile<KT, 2, 4, 5, SPLIT>(keys, n, d, ld, qhi, qlo, inv_qn, nq, inv_norm, scores, stream);
+        case 3: return launch_tile<KT, 3, 4, 5, SPLIT>(keys, n, d, ld, qhi, qlo, inv_qn, nq, inv_norm, scores, stream);
+        default: return launch_tile<KT, 4, 4, 5, SPLIT>(keys, n, d, ld, qhi, qlo, inv_qn, nq, inv_norm, scores, stream);
+    }
+}
+
+}  // namespace
+
+size_t scan_mfma_scratch_bytes(int nq, int d) {
+    const size_t qpad = (size_t)((nq + 15) / 16) * 16;
+    const size_t half = (qpad * (size_t)d * 2 + 255) / 256 * 256;
+    return 2 * half + (qpad * 4 + 255) / 256 * 256;
+}
+
+hipError_t launch_scan_mfma(const void* keys, int key_dtype, int64_t n, int d, int64_t ld,
+                            const float* queries, int nq, bool split, const float* inv_norm,
+                            float* scores, void* scratch, hipStream_t stream) {
+    const int qpad = (nq + 15) / 16 * 16;
+    const size_t half = ((size_t)qpad * d * 2 + 255) / 256 * 256;
+    uint16_t* qhi = (uint16_t*)scratch;
+    uint16_t* qlo = (uint16_t*)((char*)scratch + half);
+    float* inv_qn = (float*)((char*)scratch + 2 * half);
+    const bool cosine = inv_norm != nullptr;
+    if (key_dtype == DT_BF16)
+        hipLaunchKernelGGL(query_split_kernel<DT_BF16>, dim3(qpad), dim3(256), 0, stream, queries,
+                           nq, d, cosine, qhi, qlo, inv_qn);
+    else
+        hipLaunchKernelGGL(query_split_kernel<DT_F16>, dim3(qpad), dim3(256), 0, stream, queries,
+                           nq, d, cosine, qhi, qlo, inv_qn);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    for (int g0 = 0; g0 < nq; g0 += 64) {
+        const int ng = (nq - g0 < 64) ? nq - g0 : 64;
+        const uint16_t* h = qhi + (int64_t)g0 * d;
+        const uint16_t* lo = qlo + (int64_t)g0 * d;
+        float* sc = scores + (int64_t)g0 * n;
+        if (key_dtype == DT_BF16)
+            e = split ? launch_group<DT_BF16, true>(keys, n, d, ld, h, lo, inv_qn + g0, ng, inv_norm, sc, stream)
+                      : launch_group<DT_BF16, false>(keys, n, d, ld, h, lo, inv_qn + g0, ng, inv_norm, sc, stream);
+        else
+            e = split ? launch_group<DT_F16, true>(keys, n, d, ld, h, lo, inv_qn + g0, ng, inv_norm, sc, stream)
+                      : launch_group<DT_F16, false>(keys, n, d, ld, h, lo, inv_qn + g0, ng, inv_norm, sc, stream);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+}  // namespace sense

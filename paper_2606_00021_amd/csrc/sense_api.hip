@@ -65,15 +65,18 @@ int elem_size(int dt) { return dt == SENSE_F32 ? 4 : 2; }
 
 bool dtype_ok(int dt) { return dt == SENSE_F32 || dt == SENSE_F16 || dt == SENSE_BF16; }
 
-// Retrieval workspace layout: [fp32 queries | scores | top-k buffers].
+// Retrieval workspace layout:
+// [fp32 queries | split queries (MFMA path) | scores | top-k buffers].
 struct RetrieveLayout {
-    size_t q_off, s_off, t_off, total;
+    size_t q_off, m_off, s_off, t_off, total;
 };
 
 RetrieveLayout retrieve_layout(const sense_index* ix, int nq, int k) {
     RetrieveLayout l;
     l.q_off = 0;
-    l.s_off = round_up((size_t)nq * ix->d * sizeof(float), 256);
+    l.m_off = round_up((size_t)nq * ix->d * sizeof(float), 256);
+    const size_t mfma = nq >= sense::kMfmaMinQueries ? sense::scan_mfma_scratch_bytes(nq, ix->d) : 0;
+    l.s_off = l.m_off + round_up(mfma, 256);
     l.t_off = l.s_off + round_up((size_t)nq * (size_t)ix->n * sizeof(float), 256);
     l.total = l.t_off + sense::topk_workspace_bytes(ix->n, nq, k);
     return l;
@@ -257,8 +260,9 @@ SENSE_EXPORT sense_status_t sense_retrieve(const sense_index_t* ix, const void* 
         qptr = qf;
     }
     if ((e = timer_mark(SENSE_TIMER_SCAN, 0, st)) != hipSuccess) return hip_fail(e, "timer");
-    if ((e = sense::launch_scan(ix->keys, ix->key_dtype, ix->n, ix->d, ix->ld, qptr, nq,
-                                ix->inv_norm, scores, st)) != hipSuccess)
+    const bool split = q_dtype != ix->key_dtype;  // key-typed queries need no lo half
+    if ((e = sense::launch_scan(ix->keys, ix->key_dtype, ix->n, ix->d, ix->ld, qptr, nq, split,
+                                ix->inv_norm, scores, ws + L.m_off, st)) != hipSuccess)
         return hip_fail(e, "similarity scan");
     if ((e = timer_mark(SENSE_TIMER_SCAN, 1, st)) != hipSuccess) return hip_fail(e, "timer");
     if ((e = timer_mark(SENSE_TIMER_TOPK, 0, st)) != hipSuccess) return hip_fail(e, "timer");

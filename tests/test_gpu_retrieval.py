@@ -83,6 +83,40 @@ def test_several_queries_gemv_loop():
     run_case(w, seed=9)
 
 
+BATCHED = [
+    # (name, n, d, dtype, n_queries, k): the MFMA path (4 or more queries)
+    ("q4-d1000-f16", 7001, 1000, "f16", 4, 16),          # ragged 32-dim step, ragged tiles
+    ("q16-d5120-f16", 20000, 5120, "f16", 16, 64),
+    ("q17-d3584-bf16", 12345, 3584, "bf16", 17, 32),     # two query tiles, one padded
+    ("q40-d4096-bf16", 9000, 4096, "bf16", 40, 8),
+    ("q64-d8192-bf16", 5000, 8192, "bf16", 64, 128),
+    ("q70-d512-bf16", 3000, 512, "bf16", 70, 16),         # two query groups of <= 64
+]
+
+
+@pytest.mark.parametrize("name,n,d,dt,nq,k", BATCHED)
+@pytest.mark.parametrize("metric", ["cosine", "ip"])
+def test_batched_queries(name, n, d, dt, nq, k, metric):
+    w = synth.scaled(synth.WORKLOADS["13b-batched-4m-d5120"], name=name, n=n, d=d, key_dtype=dt,
+                     k=k, n_queries=nq, n_clusters=max(nq + 4, n // 128))
+    run_case(w, seed=hash(name) % 1000 + 1, metric=metric, ragged_spans=True)
+
+
+def test_batched_key_typed_queries():
+    """Queries given in the key type use one MFMA per tile (no lo half)."""
+    w = synth.scaled(synth.WORKLOADS["13b-batched-4m-d5120"], n=6000, d=2048, k=32, n_queries=16,
+                     key_dtype="bf16", n_clusters=60)
+    ds = synth.make_datastore(w, 12, DEV)
+    q, _ = synth.make_queries(w, ds, 12)
+    index = sense.sense_build_index(ds.keys, ds.spans)
+    qq = q.to(torch.bfloat16)
+    ids, scores, _, _ = sense.sense_retrieve(index, qq, w.k)
+    o_s = oracle.scores(host_bits(ds.keys), "bf16", host_bits(qq), "bf16")
+    for qi in range(16):
+        check_topk(ids[qi].cpu().numpy(), scores[qi].cpu().numpy(), o_s[qi], w.k)
+    index.close()
+
+
 def test_planted_exact_copy_ranks_first():
     w = synth.scaled(synth.WORKLOADS["tiny-16k-d4096"], n=12345, d=768, k=4, n_clusters=48)
     ds = synth.make_datastore(w, 3, DEV)
