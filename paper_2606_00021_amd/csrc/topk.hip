@@ -9,11 +9,12 @@
 // largest keys" and ties need no special handling.
 //
 // Selection is hierarchical.  A block of 512 threads takes a chunk of 8192
-// keys into LDS and finds the chunk's k largest with an 8-bit radix select:
-// per pass a 256-bin LDS histogram of the next digit among the keys that
-// still match the chosen prefix, then one wave finds the digit holding the
-// k-th key with a suffix scan.  The pass loop stops as soon as the chosen
-// digit's bucket is taken whole, so most chunks need 2-4 passes.  The k
+// keys into registers (16 per thread) and finds the chunk's k largest with an
+// 8-bit radix select: per pass a 256-bin LDS histogram of the next digit
+// among the keys that still match the chosen prefix, then one wave finds the
+// digit holding the k-th key with a suffix scan.  The pass loop stops as
+// soon as the chosen digit's bucket is taken whole, so most chunks need 2-4
+// passes.  The k
 // survivors of every chunk form the next level's input until one chunk
 // remains; its k keys are sorted with a bitonic network in LDS and written
 // out together with the gathered continuations.
@@ -29,25 +30,59 @@ struct SelectState {
     uint64_t mask;
 };
 
-// Finds prefix/mask such that exactly `need` of the len keys in s_keys have
-// (key & mask) >= prefix.  Requires 1 <= need <= len.  All threads of the
-// block must call it; it ends with a barrier.
-__device__ SelectState radix_select(const uint64_t* s_keys, int len, int need,
-                                    uint32_t* s_hist, uint32_t* s_info) {
+constexpr int kWaves = kThreads / 64;
+constexpr int kPer = kSelectChunk / kThreads;   // keys per thread
+
+// Finds prefix/mask such that exactly `need` of the block's keys (kPer per
+// thread, held in registers; unused slots hold the padding key 0) satisfy
+// (key & mask) >= prefix.  Requires 1 <= need <= number of keys above 0.
+// All threads of the block must call it.
+//
+// 8-bit digits from the top; a pass stops the search as soon as the digit
+// holding the need-th key is taken whole.  Each wave counts into its own
+// 256-bin LDS histogram.  Scores cluster in a few digit values (the leading
+// byte holds sign and exponent) and LDS atomics of one instruction to one
+// address serialise, so each wave first adds all lanes sharing its first
+// active lane's digit with one atomic (ballot + popcount) and only the other
+// lanes add one by one.
+__device__ SelectState radix_select(const uint64_t (&key)[kPer], int need, uint32_t* s_hist,
+                                    uint32_t* s_tot, uint32_t* s_info) {
     const int tid = threadIdx.x;
+    const int lane = tid & 63, wv = tid >> 6;
+    uint32_t* my = s_hist + wv * 256;
+    for (int b = tid; b < kWaves * 256; b += kThreads) s_hist[b] = 0;
+    __syncthreads();
     uint64_t prefix = 0, mask = 0;
     for (int shift = 56; shift >= 0; shift -= 8) {
-        for (int b = tid; b < 256; b += kThreads) s_hist[b] = 0;
+#pragma unroll
+        for (int e = 0; e < kPer; ++e) {
+            const bool act = (key[e] & mask) == prefix;
+            const uint32_t dg = (uint32_t)(key[e] >> shift) & 0xFFu;
+            const uint64_t am = __ballot(act);
+            if (am) {
+                const int first = __ffsll((unsigned long long)am) - 1;
+                const uint32_t d0 = (uint32_t)__builtin_amdgcn_readlane((int)dg, first);
+                const uint64_t same = __ballot(act && dg == d0);
+                if (lane == first) atomicAdd(&my[d0], (uint32_t)__popcll(same));
+                if (act && dg != d0) atomicAdd(&my[dg], 1u);
+            }
+        }
         __syncthreads();
-        for (int i = tid; i < len; i += kThreads) {
-            const uint64_t key = s_keys[i];
-            if ((key & mask) == prefix) atomicAdd(&s_hist[(key >> shift) & 0xFF], 1u);
+        // Totals; the per-wave histograms are cleared for the next pass.
+        for (int b = tid; b < 256; b += kThreads) {
+            uint32_t t = 0;
+#pragma unroll
+            for (int w = 0; w < kWaves; ++w) {
+                t += s_hist[w * 256 + b];
+                s_hist[w * 256 + b] = 0;
+            }
+            s_tot[b] = t;
         }
         __syncthreads();
         if (tid < 64) {
             const int l = tid;
-            const uint32_t h0 = s_hist[4 * l], h1 = s_hist[4 * l + 1], h2 = s_hist[4 * l + 2],
-                           h3 = s_hist[4 * l + 3];
+            const uint32_t h0 = s_tot[4 * l], h1 = s_tot[4 * l + 1], h2 = s_tot[4 * l + 2],
+                           h3 = s_tot[4 * l + 3];
             const uint32_t local = h0 + h1 + h2 + h3;
             // inclusive suffix sum over lanes l..63 (higher digits)
             uint32_t incl = local;
@@ -71,13 +106,15 @@ __device__ SelectState radix_select(const uint64_t* s_keys, int len, int need,
             }
         }
         __syncthreads();
+        // Every thread reads s_info before any thread passes the next pass's
+        // first barrier, after which wave 0 may rewrite it.
         const uint32_t digit = s_info[0], above = s_info[1], in_bucket = s_info[2];
         need -= (int)above;
         prefix |= (uint64_t)digit << shift;
         mask |= (uint64_t)0xFF << shift;
-        __syncthreads();  // s_info / s_hist are rewritten by the next pass
         if ((int)in_bucket == need) break;
     }
+    __syncthreads();
     return SelectState{prefix, mask};
 }
 
@@ -110,9 +147,9 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
     float* __restrict__ out_scores, int32_t* __restrict__ out_drafts,
     int32_t* __restrict__ out_draft_len, const int32_t* __restrict__ spans,
     const int32_t* __restrict__ span_len, int max_span) {
-    __shared__ uint64_t s_keys[kSelectChunk];
     __shared__ uint64_t s_sel[kMaxK];
-    __shared__ uint32_t s_hist[256];
+    __shared__ uint32_t s_hist[kWaves * 256];
+    __shared__ uint32_t s_tot[256];
     __shared__ uint32_t s_info[4];
     __shared__ uint32_t s_cnt;
 
@@ -123,45 +160,59 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
     const int len = (int)(remain < kSelectChunk ? remain : kSelectChunk);
     const int kk = k < kSelectChunk ? k : kSelectChunk;
 
-    for (int i = tid; i < len; i += kThreads) {
+    // Key i of the chunk is held by thread i % kThreads (all loads in flight
+    // at once); slots past the chunk hold the padding key 0.
+    uint64_t key[kPer];
+#pragma unroll
+    for (int e = 0; e < kPer; ++e) {
+        const int i = tid + e * kThreads;
         const int64_t pos = start + i;
-        if constexpr (FROM_SCORES)
-            s_keys[i] = pack_key(scores[(int64_t)q * count + pos], (uint32_t)pos);
-        else
-            s_keys[i] = in_keys[(int64_t)q * count + pos];
+        if (i < len) {
+            if constexpr (FROM_SCORES)
+                key[e] = pack_key(scores[(int64_t)q * count + pos], (uint32_t)pos);
+            else
+                key[e] = in_keys[(int64_t)q * count + pos];
+        } else {
+            key[e] = 0;
+        }
     }
     if (tid == 0) s_cnt = 0;
-    __syncthreads();
 
-    // Keys taken: all of them if the chunk holds no more than kk.
+    // Keys taken: all real ones if the chunk holds no more than kk, else the
+    // kk largest.
     SelectState st{0, 0};
-    if (len > kk) st = radix_select(s_keys, len, kk, s_hist, s_info);
+    const bool all = len <= kk;
+    if (!all) st = radix_select(key, kk, s_hist, s_tot, s_info);
+    else __syncthreads();
+    auto taken = [&](int e) {
+        return all ? (tid + e * kThreads < len) : ((key[e] & st.mask) >= st.prefix);
+    };
 
     if constexpr (!FINAL) {
         uint64_t* out = out_keys + ((int64_t)q * gridDim.x + blockIdx.x) * kk;
-        for (int i = tid; i < len; i += kThreads) {
-            const uint64_t key = s_keys[i];
-            if ((key & st.mask) >= st.prefix) {
+#pragma unroll
+        for (int e = 0; e < kPer; ++e) {
+            if (taken(e)) {
                 const uint32_t at = atomicAdd(&s_cnt, 1u);
-                if (at < (uint32_t)kk) out[at] = key;
+                if (at < (uint32_t)kk) out[at] = key[e];
             }
         }
         __syncthreads();
-        const int taken = (int)s_cnt < kk ? (int)s_cnt : kk;
-        for (int i = taken + tid; i < kk; i += kThreads) out[i] = 0;  // padding key
+        const int nt = (int)s_cnt < kk ? (int)s_cnt : kk;
+        for (int i = nt + tid; i < kk; i += kThreads) out[i] = 0;  // padding key
     } else {
-        for (int i = tid; i < len; i += kThreads) {
-            const uint64_t key = s_keys[i];
-            if ((key & st.mask) >= st.prefix) {
+#pragma unroll
+        for (int e = 0; e < kPer; ++e) {
+            if (taken(e)) {
                 const uint32_t at = atomicAdd(&s_cnt, 1u);
-                if (at < (uint32_t)kk) s_sel[at] = key;
+                if (at < (uint32_t)kk) s_sel[at] = key[e];
             }
         }
         __syncthreads();
         int p = 1;
         while (p < kk) p <<= 1;
-        const int taken = (int)s_cnt < kk ? (int)s_cnt : kk;
-        for (int i = taken + tid; i < p; i += kThreads) s_sel[i] = 0;
+        const int nt = (int)s_cnt < kk ? (int)s_cnt : kk;
+        for (int i = nt + tid; i < p; i += kThreads) s_sel[i] = 0;
         __syncthreads();
         bitonic_desc(s_sel, p);
         for (int r = tid; r < k; r += kThreads) {

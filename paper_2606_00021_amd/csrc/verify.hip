@@ -4,32 +4,38 @@
 // The cost is one read of the logits of every live (candidate, position)
 // row; everything else is per-row scalars.  Two kernels:
 //
-// verify_rows: one block of 256 threads per (row, vocabulary slice).  Each
-//   thread streams its part of the slice with 16-byte loads and keeps, in
-//   one pass,
-//     m   running maximum,
-//     S   sum of 2^(t) with t = (x - m) log2 e     (= sum e^(x-m)),
-//     T2  sum of 2^(t) * t                          (= log2 e * sum e^(x-m)(x-m)),
-//     cnt #{v : x_v > x_d} + #{v < d : x_v = x_d},  x_d the draft token's logit,
-//   rescaling S and T2 when the maximum grows.  The block merges its 256
-//   states (DPP butterflies in a fixed order, then the four waves in order)
-//   and stores one 16-byte partial per (row, slice).  With p = softmax(x),
-//   E = -sum p ln p = ln S - ln2 * T2 / S.  The draft token is the first
-//   argmax exactly when cnt = 0, and it is in the top-k set exactly when
-//   cnt < k, so neither an argmax nor a sort of the vocabulary is needed.
-//   Slices exist only to give small batches enough blocks.
+// verify_rows: one block of 256 threads per (row, vocabulary slice).  A
+//   slice is what the block can hold in registers: every thread issues all
+//   of its sixteen 16-byte loads at once (deep memory-level parallelism, no
+//   dependent chain), then
+//     phase 1: m = max of the slice (wave max, then the four waves);
+//     phase 2: with t = (x - m) log2 e,
+//       S   = sum 2^t                 (= sum e^(x-m)),
+//       T2  = sum 2^t * t             (= log2 e * sum e^(x-m)(x-m)),
+//       cnt = #{v : x_v > x_d} + #{v < d : x_v = x_d},  x_d the draft token's
+//             logit, counted as x_v >= x_d left of d and x_v >= next(x_d)
+//             from d on (one compare per element).
+//   and stores one 16-byte partial (m, S, T2, cnt) per (row, slice).  With
+//   p = softmax(x), E = -sum p ln p = ln S - ln2 * T2 / S.  The draft token
+//   is the first argmax exactly when cnt = 0 and is in the top-k set exactly
+//   when cnt < k, so neither an argmax nor a sort of the vocabulary is needed.
+//   Sums are formed in a fixed order (DPP butterflies, then the waves in
+//   order), so results are deterministic.
 //
-// verify_finalize: one block per candidate group.  Each thread takes a
-//   candidate, merges the slices of its rows in slice order, forms the
-//   masks, counts window mismatches with a popcount over 64-bit masks, finds
-//   the leading run of accepted positions, and the block picks the group's
-//   first longest candidate.
+// verify_finalize: one block per candidate group.  Phase 1 gives every
+//   (candidate, position) row its own thread, which merges the row's slices
+//   in slice order and forms the exact-match / entropy / top-k bits; phase 2
+//   gives every candidate a thread that counts window mismatches with a
+//   popcount over 64-bit masks and finds the leading run of accepted
+//   positions; the block then picks the group's first longest candidate.
 #include "internal.h"
 
 namespace sense {
 namespace {
 
 constexpr int kRowThreads = 256;
+constexpr int kNV = 16;            // 16-byte vectors per thread per slice
+constexpr int kScalarPer = 32;     // elements per thread per slice, unaligned rows
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -46,7 +52,7 @@ struct Stats {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// Merge of two (m, S, T2) states; symmetric in its arguments bit for bit.
+// Merge of two (m, S, T2) states of disjoint element sets.
 __device__ __forceinline__ Stats merge(const Stats& a, const Stats& b) {
     if (a.m == -__builtin_inff()) return b;
     if (b.m == -__builtin_inff()) return a;
@@ -61,28 +67,44 @@ __device__ __forceinline__ Stats merge(const Stats& a, const Stats& b) {
 }
 
 template <int CTRL>
-__device__ __forceinline__ float dpp_f(float x) {
-    return __builtin_bit_cast(
-        float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
-}
-template <int CTRL>
 __device__ __forceinline__ int dpp_i(int x) {
     return __builtin_amdgcn_update_dpp(0, x, CTRL, 0xF, 0xF, false);
 }
 template <int CTRL>
-__device__ __forceinline__ void butterfly_step(Stats& st, int& cnt) {
-    Stats o{dpp_f<CTRL>(st.m), dpp_f<CTRL>(st.s), dpp_f<CTRL>(st.t2)};
-    st = merge(st, o);
-    cnt += dpp_i<CTRL>(cnt);
+__device__ __forceinline__ float dpp_f(float x) {
+    return __builtin_bit_cast(float, dpp_i<CTRL>(__builtin_bit_cast(int, x)));
 }
-__device__ __forceinline__ Stats lane_read(const Stats& st, int lane) {
-    return Stats{__builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, st.m), lane)),
-                 __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, st.s), lane)),
-                 __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, st.t2), lane))};
+__device__ __forceinline__ float lane_f(float x, int lane) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), lane));
+}
+
+// Wave-uniform sum / max over 64 lanes in a fixed order.
+__device__ __forceinline__ float wave_sum_f(float x) {
+    x += dpp_f<0xB1>(x);
+    x += dpp_f<0x4E>(x);
+    x += dpp_f<0x141>(x);
+    x += dpp_f<0x140>(x);
+    return (lane_f(x, 0) + lane_f(x, 16)) + (lane_f(x, 32) + lane_f(x, 48));
+}
+__device__ __forceinline__ int wave_sum_i(int x) {
+    x += dpp_i<0xB1>(x);
+    x += dpp_i<0x4E>(x);
+    x += dpp_i<0x141>(x);
+    x += dpp_i<0x140>(x);
+    return (__builtin_amdgcn_readlane(x, 0) + __builtin_amdgcn_readlane(x, 16)) +
+           (__builtin_amdgcn_readlane(x, 32) + __builtin_amdgcn_readlane(x, 48));
+}
+__device__ __forceinline__ float wave_max_f(float x) {
+    x = __builtin_fmaxf(x, dpp_f<0xB1>(x));
+    x = __builtin_fmaxf(x, dpp_f<0x4E>(x));
+    x = __builtin_fmaxf(x, dpp_f<0x141>(x));
+    x = __builtin_fmaxf(x, dpp_f<0x140>(x));
+    return __builtin_fmaxf(__builtin_fmaxf(lane_f(x, 0), lane_f(x, 16)),
+                           __builtin_fmaxf(lane_f(x, 32), lane_f(x, 48)));
 }
 
 template <int LT>
-__device__ __forceinline__ float load_one(const void* base, int64_t i) {
+__device__ __forceinline__ float load_one(const char* base, int64_t i) {
     if constexpr (LT == DT_F32) {
         return ((const float*)base)[i];
     } else if constexpr (LT == DT_BF16) {
@@ -90,36 +112,6 @@ __device__ __forceinline__ float load_one(const void* base, int64_t i) {
     } else {
         return (float)__builtin_bit_cast(_Float16, ((const uint16_t*)base)[i]);
     }
-}
-
-struct RowState {
-    float m, nm, s, t2;  // nm = -m * log2 e
-    int cnt;
-};
-
-__device__ __forceinline__ void absorb_max(RowState& st, float vmax) {
-    if (vmax > st.m) {
-        if (st.m == -__builtin_inff()) {
-            st.s = 0.0f;
-            st.t2 = 0.0f;
-        } else {
-            const float dl = (st.m - vmax) * kLog2e;
-            const float a = fast_exp2(dl);
-            st.t2 = a * __builtin_fmaf(dl, st.s, st.t2);
-            st.s = a * st.s;
-        }
-        st.m = vmax;
-        st.nm = -vmax * kLog2e;
-    }
-}
-
-__device__ __forceinline__ void absorb(RowState& st, float x, int v, float xd, int tok) {
-    // The clamp keeps a -inf logit at weight 0 and contribution 0 (not 0*inf).
-    const float t = __builtin_fmaxf(__builtin_fmaf(x, kLog2e, st.nm), -256.0f);
-    const float e = fast_exp2(t);
-    st.s += e;
-    st.t2 = __builtin_fmaf(e, t, st.t2);
-    st.cnt += (x > xd) | ((x == xd) & (v < tok));
 }
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -144,6 +136,29 @@ __device__ __forceinline__ void unpack(const u32x4& w, float (&x)[LT == DT_F32 ?
     }
 }
 
+// Smallest float above x (x finite); +inf and NaN map to themselves.
+__device__ __forceinline__ float next_up(float x) {
+    if (x != x || x == __builtin_inff()) return x;
+    if (x == 0.0f) return __builtin_bit_cast(float, 1u);
+    const uint32_t u = __builtin_bit_cast(uint32_t, x);
+    return __builtin_bit_cast(float, x > 0.0f ? u + 1u : u - 1u);
+}
+
+struct Acc {
+    float s = 0.0f, t2 = 0.0f;
+    int cnt = 0;
+};
+
+// One element of phase 2.  The clamp keeps a -inf logit at weight 0 and
+// contribution 0 (instead of 0 * -inf).
+__device__ __forceinline__ void absorb(Acc& a, float x, float nm, float thr) {
+    const float t = __builtin_fmaxf(__builtin_fmaf(x, kLog2e, nm), -256.0f);
+    const float e = fast_exp2(t);
+    a.s += e;
+    a.t2 = __builtin_fmaf(e, t, a.t2);
+    a.cnt += (x >= thr) ? 1 : 0;
+}
+
 template <int LT, bool VEC>
 __global__ __launch_bounds__(kRowThreads) void verify_rows_kernel(
     const void* __restrict__ logits, int64_t row_stride, const int32_t* __restrict__ drafts,
@@ -153,74 +168,115 @@ __global__ __launch_bounds__(kRowThreads) void verify_rows_kernel(
     constexpr int ES = (LT == DT_F32) ? 4 : 2;      // element size
     const int row = blockIdx.x;
     const int slice = blockIdx.y;
+    const int tid = threadIdx.x;
     const int c = row / max_len, j = row - c * max_len;
     int len = draft_len ? draft_len[c] : max_len;
     len = len < 0 ? 0 : (len > max_len ? max_len : len);
-    if (j >= len) return;
+    if (j >= len) return;                            // uniform over the block
 
     const int tok = drafts[row];
     const bool valid = tok >= 0 && tok < vocab;
     const char* rowp = (const char*)logits + (int64_t)row * row_stride * ES;
     const float xd = valid ? load_one<LT>(rowp, tok) : 0.0f;
-    const int tk = valid ? tok : -1;   // with tk = -1 and xd = 0 the count is unused
+    const int tk = valid ? tok : -1;                 // -1: the count is unused
+    const float thr_lo = xd, thr_hi = next_up(xd);   // left of d / from d on
 
     const int v0 = slice * slice_len;
     const int v1 = (v0 + slice_len < vocab) ? v0 + slice_len : vocab;
-    RowState st{-__builtin_inff(), 0.0f, 0.0f, 0.0f, 0};
+    Acc acc;
+    float mx = -__builtin_inff();
+    __shared__ float s_max[kRowThreads / 64];
 
-    int vtail = v0;
     if constexpr (VEC) {
         const int nvec = (v1 - v0) / VW;
         const u32x4* vp = (const u32x4*)(rowp + (int64_t)v0 * ES);
-        for (int i = threadIdx.x; i < nvec; i += kRowThreads) {
-            const u32x4 w = __builtin_nontemporal_load(vp + i);
-            float x[VW];
-            unpack<LT>(w, x);
-            float vmax = x[0];
+        u32x4 buf[kNV];
 #pragma unroll
-            for (int u = 1; u < VW; ++u) vmax = x[u] > vmax ? x[u] : vmax;
-            absorb_max(st, vmax);
-            const int vb = v0 + i * VW;
-#pragma unroll
-            for (int u = 0; u < VW; ++u) absorb(st, x[u], vb + u, xd, tk);
+        for (int k = 0; k < kNV; ++k) {
+            const int i = tid + k * kRowThreads;
+            buf[k] = (i < nvec) ? __builtin_nontemporal_load(vp + i) : u32x4{0u, 0u, 0u, 0u};
         }
-        vtail = v0 + nvec * VW;
-    }
-    for (int v = vtail + threadIdx.x; v < v1; v += kRowThreads) {
-        const float x = load_one<LT>(rowp, v);
-        absorb_max(st, x);
-        absorb(st, x, v, xd, tk);
+        // Fewer than VW trailing elements (last slice only).
+        const int vt = v0 + nvec * VW + tid;
+        const bool has_t = vt < v1;
+        const float xt = has_t ? load_one<LT>(rowp, vt) : -__builtin_inff();
+#pragma unroll
+        for (int k = 0; k < kNV; ++k) {
+            if (tid + k * kRowThreads < nvec) {
+                float x[VW];
+                unpack<LT>(buf[k], x);
+#pragma unroll
+                for (int u = 0; u < VW; ++u) mx = __builtin_fmaxf(mx, x[u]);
+            }
+        }
+        mx = __builtin_fmaxf(mx, xt);
+        const float wm = wave_max_f(mx);
+        if ((tid & 63) == 0) s_max[tid >> 6] = wm;
+        __syncthreads();
+        const float m = __builtin_fmaxf(__builtin_fmaxf(s_max[0], s_max[1]),
+                                        __builtin_fmaxf(s_max[2], s_max[3]));
+        mx = m;
+        {
+            // An all -inf slice keeps weight 0 (t clamps) but still counts ties.
+            const float nm = (m == -__builtin_inff()) ? 0.0f : -m * kLog2e;
+#pragma unroll
+            for (int k = 0; k < kNV; ++k) {
+                const int i = tid + k * kRowThreads;
+                if (i < nvec) {
+                    float x[VW];
+                    unpack<LT>(buf[k], x);
+                    const int vb = v0 + i * VW;
+                    const float thr = (vb + VW <= tk) ? thr_lo : thr_hi;
+#pragma unroll
+                    for (int u = 0; u < VW; ++u) absorb(acc, x[u], nm, thr);
+                    if (vb < tk && tk < vb + VW) {   // the vector holding d: ties left of d
+#pragma unroll
+                        for (int u = 0; u < VW; ++u) acc.cnt += (vb + u < tk && x[u] == xd) ? 1 : 0;
+                    }
+                }
+            }
+            if (has_t) absorb(acc, xt, nm, vt < tk ? thr_lo : thr_hi);
+        }
+    } else {
+        float x[kScalarPer];
+#pragma unroll
+        for (int k = 0; k < kScalarPer; ++k) {
+            const int v = v0 + tid + k * kRowThreads;
+            x[k] = (v < v1) ? load_one<LT>(rowp, v) : -__builtin_inff();
+            mx = __builtin_fmaxf(mx, x[k]);
+        }
+        const float wm = wave_max_f(mx);
+        if ((tid & 63) == 0) s_max[tid >> 6] = wm;
+        __syncthreads();
+        const float m = __builtin_fmaxf(__builtin_fmaxf(s_max[0], s_max[1]),
+                                        __builtin_fmaxf(s_max[2], s_max[3]));
+        mx = m;
+        {
+            const float nm = (m == -__builtin_inff()) ? 0.0f : -m * kLog2e;
+#pragma unroll
+            for (int k = 0; k < kScalarPer; ++k) {
+                const int v = v0 + tid + k * kRowThreads;
+                if (v < v1) absorb(acc, x[k], nm, v < tk ? thr_lo : thr_hi);
+            }
+        }
     }
 
-    // Block merge: butterflies inside each 16-lane row, rows in order, waves
-    // in order.
-    Stats s{st.m, st.s, st.t2};
-    int cnt = st.cnt;
-    butterfly_step<0xB1>(s, cnt);
-    butterfly_step<0x4E>(s, cnt);
-    butterfly_step<0x141>(s, cnt);
-    butterfly_step<0x140>(s, cnt);
-    Stats w = merge(merge(lane_read(s, 0), lane_read(s, 16)),
-                    merge(lane_read(s, 32), lane_read(s, 48)));
-    const int wc = __builtin_amdgcn_readlane(cnt, 0) + __builtin_amdgcn_readlane(cnt, 16) +
-                   __builtin_amdgcn_readlane(cnt, 32) + __builtin_amdgcn_readlane(cnt, 48);
+    // Block sums in a fixed order.
+    const float ws = wave_sum_f(acc.s), wt = wave_sum_f(acc.t2);
+    const int wc = wave_sum_i(acc.cnt);
     __shared__ Partial s_w[kRowThreads / 64];
-    const int wave = threadIdx.x >> 6;
-    if ((threadIdx.x & 63) == 0) s_w[wave] = Partial{w.m, w.s, w.t2, wc};
+    if ((tid & 63) == 0) s_w[tid >> 6] = Partial{mx, ws, wt, wc};
     __syncthreads();
-    if (threadIdx.x == 0) {
-        Stats a{s_w[0].m, s_w[0].s, s_w[0].t2};
-        int tc = s_w[0].cnt;
-#pragma unroll
-        for (int i = 1; i < kRowThreads / 64; ++i) {
-            a = merge(a, Stats{s_w[i].m, s_w[i].s, s_w[i].t2});
-            tc += s_w[i].cnt;
-        }
-        partial[(int64_t)row * n_slices + slice] = Partial{a.m, a.s, a.t2, tc};
+    if (tid == 0) {
+        Partial p{mx, (s_w[0].s + s_w[1].s) + (s_w[2].s + s_w[3].s),
+                  (s_w[0].t2 + s_w[1].t2) + (s_w[2].t2 + s_w[3].t2),
+                  (s_w[0].cnt + s_w[1].cnt) + (s_w[2].cnt + s_w[3].cnt)};
+        partial[(int64_t)row * n_slices + slice] = p;
     }
 }
 
 constexpr int kFinThreads = 256;
+constexpr int kFinChunkRows = 4096;   // (candidate, position) rows per LDS chunk
 
 __device__ __forceinline__ uint64_t bits_upto(int x) {  // bits 0..x set (x may be -1)
     return (x >= 63) ? ~0ull : ((x < 0) ? 0ull : ((1ull << (x + 1)) - 1ull));
@@ -232,60 +288,81 @@ __global__ __launch_bounds__(kFinThreads) void verify_finalize_kernel(
     GateParams gp, int32_t* __restrict__ out_accept_len, int32_t* __restrict__ out_best,
     float* __restrict__ out_gate_score, uint8_t* __restrict__ out_masks,
     int32_t* __restrict__ out_rank) {
+    __shared__ uint8_t s_bits[kFinChunkRows];   // em | ent<<1 | topk<<2 per row
     const int g = blockIdx.x;
+    const int chunk_cands = kFinChunkRows / max_len;
     int best_n = -1, best_i = 0;
-    for (int cc = threadIdx.x; cc < group_size; cc += kFinThreads) {
-        const int c = g * group_size + cc;
-        int len = draft_len ? draft_len[c] : max_len;
-        len = len < 0 ? 0 : (len > max_len ? max_len : len);
-        uint64_t em = 0, ent = 0, tkm = 0;
-        for (int j = 0; j < len; ++j) {
-            const int64_t row = (int64_t)c * max_len + j;
-            const Partial* p = partial + row * n_slices;
-            Stats a{p[0].m, p[0].s, p[0].t2};
-            int cnt = p[0].cnt;
-            for (int s = 1; s < n_slices; ++s) {
-                a = merge(a, Stats{p[s].m, p[s].s, p[s].t2});
-                cnt += p[s].cnt;
-            }
-            const float e_nats = __logf(a.s) - (kLn2 * a.t2) / a.s;
-            const float score = e_nats * gp.ent_scale;
-            const int tok = drafts[row];
-            const bool valid = tok >= 0 && tok < vocab;
-            const int rank = valid ? cnt : vocab;
-            if (valid && rank == 0) em |= 1ull << j;
-            if (score > gp.gamma) ent |= 1ull << j;
-            if (valid && rank < gp.topk) tkm |= 1ull << j;
-            if (out_gate_score) out_gate_score[row] = score;
-            if (out_rank) out_rank[row] = rank;
-        }
-        // Mismatches: 1 - B_em inside the draft, and W padding ones after it.
-        const uint64_t notem = ~em & bits_upto(max_len - 1);
-        int n = 0;
-        bool still = true;
-        for (int j = 0; j < max_len; ++j) {
-            const int hi = j + gp.window;
-            const int in_hi = hi < max_len - 1 ? hi : max_len - 1;
-            const uint64_t range = bits_upto(in_hi) & ~bits_upto(j);
-            const int r = __popcll(notem & range) + (hi > max_len - 1 ? hi - (max_len - 1) : 0);
-            const bool con = r <= gp.tau;
-            const bool bem = (em >> j) & 1, bent = (ent >> j) & 1, btk = (tkm >> j) & 1;
-            const bool gate = (j < len) && (bem || (bent && (btk || con)));
-            if (still && gate) ++n; else still = false;
-            const int64_t row = (int64_t)c * max_len + j;
-            if (out_masks)
-                out_masks[row] = (uint8_t)((int)bem | ((int)bent << 1) | ((int)btk << 2) |
-                                           ((int)con << 3) | ((int)gate << 4));
-            if (j >= len) {
+    for (int cc0 = 0; cc0 < group_size; cc0 += chunk_cands) {
+        const int ncc = (group_size - cc0 < chunk_cands) ? group_size - cc0 : chunk_cands;
+        // Phase 1: one thread per (candidate, position).
+        for (int r = threadIdx.x; r < ncc * max_len; r += kFinThreads) {
+            const int cl = r / max_len, jj = r - cl * max_len;
+            const int c = g * group_size + cc0 + cl;
+            int len = draft_len ? draft_len[c] : max_len;
+            len = len < 0 ? 0 : (len > max_len ? max_len : len);
+            const int64_t row = (int64_t)c * max_len + jj;
+            uint8_t bits = 0;
+            if (jj < len) {
+                const Partial* p = partial + row * n_slices;
+                Stats a{p[0].m, p[0].s, p[0].t2};
+                int cnt = p[0].cnt;
+                for (int s = 1; s < n_slices; ++s) {
+                    a = merge(a, Stats{p[s].m, p[s].s, p[s].t2});
+                    cnt += p[s].cnt;
+                }
+                const float e_nats = __logf(a.s) - (kLn2 * a.t2) / a.s;
+                const float score = e_nats * gp.ent_scale;
+                const int tok = drafts[row];
+                const bool valid = tok >= 0 && tok < vocab;
+                const int rank = valid ? cnt : vocab;
+                bits = (uint8_t)((valid && rank == 0 ? 1 : 0) | (score > gp.gamma ? 2 : 0) |
+                                 (valid && rank < gp.topk ? 4 : 0));
+                if (out_gate_score) out_gate_score[row] = score;
+                if (out_rank) out_rank[row] = rank;
+            } else {
                 if (out_gate_score) out_gate_score[row] = 0.0f;
                 if (out_rank) out_rank[row] = vocab;
             }
+            s_bits[r] = bits;
         }
-        out_accept_len[c] = n;
-        if (n > best_n) {
-            best_n = n;
-            best_i = cc;
+        __syncthreads();
+        // Phase 2: one thread per candidate.
+        for (int cl = threadIdx.x; cl < ncc; cl += kFinThreads) {
+            const int c = g * group_size + cc0 + cl;
+            int len = draft_len ? draft_len[c] : max_len;
+            len = len < 0 ? 0 : (len > max_len ? max_len : len);
+            uint64_t em = 0, ent = 0, tkm = 0;
+            for (int jj = 0; jj < max_len; ++jj) {
+                const uint8_t b = s_bits[cl * max_len + jj];
+                em |= (uint64_t)(b & 1) << jj;
+                ent |= (uint64_t)((b >> 1) & 1) << jj;
+                tkm |= (uint64_t)((b >> 2) & 1) << jj;
+            }
+            // Mismatches: 1 - B_em inside the draft, and W padding ones after it.
+            const uint64_t notem = ~em & bits_upto(max_len - 1);
+            int n = 0;
+            bool still = true;
+            for (int jj = 0; jj < max_len; ++jj) {
+                const int hi = jj + gp.window;
+                const int in_hi = hi < max_len - 1 ? hi : max_len - 1;
+                const uint64_t range = bits_upto(in_hi) & ~bits_upto(jj);
+                const int r = __popcll(notem & range) + (hi > max_len - 1 ? hi - (max_len - 1) : 0);
+                const bool con = r <= gp.tau;
+                const bool bem = (em >> jj) & 1, bent = (ent >> jj) & 1, btk = (tkm >> jj) & 1;
+                const bool gate = (jj < len) && (bem || (bent && (btk || con)));
+                if (still && gate) ++n; else still = false;
+                if (out_masks)
+                    out_masks[(int64_t)c * max_len + jj] =
+                        (uint8_t)((int)bem | ((int)bent << 1) | ((int)btk << 2) | ((int)con << 3) |
+                                  ((int)gate << 4));
+            }
+            out_accept_len[c] = n;
+            if (n > best_n) {
+                best_n = n;
+                best_i = cc0 + cl;
+            }
         }
+        __syncthreads();
     }
     // First candidate with the largest n in the group.
     __shared__ int s_n[kFinThreads], s_i[kFinThreads];
@@ -306,33 +383,23 @@ __global__ __launch_bounds__(kFinThreads) void verify_finalize_kernel(
 }
 
 struct Plan {
+    bool vec;
     int n_slices;
     int slice_len;
 };
 
-Plan plan_slices(int n_cand, int max_len, int vocab, int dtype) {
+Plan plan_slices(int vocab, int dtype, bool vec) {
     const int vw = (dtype == DT_F32) ? 4 : 8;
-    const int64_t rows = (int64_t)n_cand * max_len;
-    const int unit = kRowThreads * vw;                 // one vector per thread
-    int max_slices = vocab / (4 * unit);               // >= 4 vectors per thread
-    if (max_slices < 1) max_slices = 1;
-    int64_t want = rows > 0 ? (2048 + rows - 1) / rows : 1;
-    int ns = (int)(want < max_slices ? want : max_slices);
-    if (ns < 1) ns = 1;
-    int slice_len = (vocab + ns - 1) / ns;
-    slice_len = (slice_len + unit - 1) / unit * unit;  // multiple of the vector width
-    ns = (vocab + slice_len - 1) / slice_len;
-    return Plan{ns, slice_len};
+    const int slice_len = vec ? kRowThreads * kNV * vw : kRowThreads * kScalarPer;
+    return Plan{vec, (vocab + slice_len - 1) / slice_len, slice_len};
 }
 
 template <int LT>
 hipError_t launch_rows(const void* logits, int64_t row_stride, const int32_t* drafts,
                        const int32_t* draft_len, int n_cand, int max_len, int vocab,
                        const Plan& pl, Partial* part, hipStream_t stream) {
-    constexpr int ES = (LT == DT_F32) ? 4 : 2;
-    const bool vec = ((uintptr_t)logits % 16 == 0) && ((row_stride * ES) % 16 == 0);
     const dim3 grid((unsigned)((int64_t)n_cand * max_len), (unsigned)pl.n_slices);
-    if (vec)
+    if (pl.vec)
         hipLaunchKernelGGL((verify_rows_kernel<LT, true>), grid, dim3(kRowThreads), 0, stream,
                            logits, row_stride, drafts, draft_len, max_len, vocab, pl.slice_len,
                            pl.n_slices, part);
@@ -346,12 +413,9 @@ hipError_t launch_rows(const void* logits, int64_t row_stride, const int32_t* dr
 }  // namespace
 
 size_t verify_workspace_bytes(int n_cand, int max_len, int vocab) {
-    // Sized for the widest plan (fp32 and 16-bit logits give the same or
-    // fewer slices than this bound).
-    const Plan a = plan_slices(n_cand, max_len, vocab, DT_F32);
-    const Plan b = plan_slices(n_cand, max_len, vocab, DT_BF16);
-    const int ns = a.n_slices > b.n_slices ? a.n_slices : b.n_slices;
-    return (size_t)n_cand * (size_t)max_len * (size_t)ns * sizeof(Partial);
+    // The unaligned-row plan has the most slices.
+    const Plan p = plan_slices(vocab, DT_BF16, false);
+    return (size_t)n_cand * (size_t)max_len * (size_t)p.n_slices * sizeof(Partial);
 }
 
 hipError_t launch_verify(const void* logits, int logits_dtype, int64_t row_stride,
@@ -361,7 +425,9 @@ hipError_t launch_verify(const void* logits, int logits_dtype, int64_t row_strid
                          uint8_t* out_masks, int32_t* out_rank, void* workspace,
                          hipStream_t stream) {
     if (n_cand == 0) return hipSuccess;
-    const Plan pl = plan_slices(n_cand, max_len, vocab, logits_dtype);
+    const int es = (logits_dtype == DT_F32) ? 4 : 2;
+    const bool vec = ((uintptr_t)logits % 16 == 0) && ((row_stride * es) % 16 == 0);
+    const Plan pl = plan_slices(vocab, logits_dtype, vec);
     Partial* part = (Partial*)workspace;
     hipError_t e;
     switch (logits_dtype) {
