@@ -131,3 +131,18 @@ def test_full_size_batches(name):
     idx = drafts.long().unsqueeze(-1)
     logits.scatter_add_(2, idx, (sharp.to(logits.dtype) * 40).unsqueeze(-1))
     run(logits.cpu(), drafts.cpu(), n_groups=w.verify_queries)
+
+
+@pytest.mark.parametrize("name", ["13b-batched-4m-d5120", "70b-8m-d8192"])
+def test_full_size_batched_groups(name):
+    """The verify batches of the batched workloads: 16 groups x 64 drafts x 8
+    (fp32, V = 32000) and 4 groups x 128 drafts x 12 (fp32, V = 128256)."""
+    w = synth.WORKLOADS[name]
+    g = torch.Generator(device=DEV).manual_seed(9)
+    drafts = torch.randint(0, w.vocab, (w.n_cand, w.span), generator=g, device=DEV,
+                           dtype=torch.int32)
+    logits = synth.make_logits(w, drafts, seed=9)
+    sharp = torch.rand((w.n_cand, w.span), generator=g, device=DEV) < 0.4
+    logits.scatter_add_(2, drafts.long().unsqueeze(-1), (sharp.to(logits.dtype) * 40).unsqueeze(-1))
+    dl = torch.randint(0, w.span + 1, (w.n_cand,), generator=g, device=DEV, dtype=torch.int32)
+    run(logits.cpu(), drafts.cpu(), dl.cpu().numpy(), n_groups=w.verify_queries)
