@@ -232,6 +232,18 @@ typedef enum {
  * `which` or exactly one NULL event. */
 sense_status_t sense_set_timer_events(sense_timer_t which, void *start_event, void *stop_event);
 
+/* Diagnostic: one plain streaming read of `bytes` of device memory at `buf`
+ * (16-byte non-temporal loads, a grid of 8 blocks of 256 threads per compute
+ * unit, grid-stride, 8 loads in flight per thread), enqueued on `stream`.  It
+ * measures the practical HBM read bandwidth of the device beside its
+ * published peak; time it with events around the call.  `sink` is a device
+ * word the kernel writes only in the (practically impossible) case that the
+ * XOR of all words read equals a fixed constant, which keeps the loads alive.
+ * buf 16-byte aligned, bytes a multiple of 16.  INVALID_ARGUMENT, MISALIGNED,
+ * HIP. */
+sense_status_t sense_read_bandwidth_probe(const void *buf, size_t bytes, uint32_t *sink,
+                                          void *stream);
+
 /* Static description of a status code. */
 const char *sense_status_string(sense_status_t status);
 

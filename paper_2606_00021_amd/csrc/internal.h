@@ -69,6 +69,9 @@ hipError_t launch_scan_mfma(const void* keys, int key_dtype, int64_t n, int d, i
                             const float* queries, int nq, bool split, const float* inv_norm,
                             float* scores, void* scratch, hipStream_t stream);
 
+// Plain streaming read of a device buffer (bandwidth probe).
+hipError_t launch_stream_read(const void* buf, size_t bytes, uint32_t* sink, hipStream_t stream);
+
 // Converts nq x d queries of dtype q_dtype to fp32 (plain copy for fp32).
 hipError_t launch_query_to_f32(const void* q, int q_dtype, int nq, int d, float* out,
                                hipStream_t stream);

@@ -347,3 +347,14 @@ SENSE_EXPORT sense_status_t sense_soft_gate_verify(
     if ((e = timer_mark(SENSE_TIMER_VERIFY, 1, st)) != hipSuccess) return hip_fail(e, "timer");
     return ok();
 }
+
+SENSE_EXPORT sense_status_t sense_read_bandwidth_probe(const void* buf, size_t bytes,
+                                                       uint32_t* sink, void* stream) {
+    if (!buf || !sink || bytes == 0)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "buf and sink must be non-NULL, bytes > 0");
+    if (!aligned(buf, 16) || bytes % 16 != 0)
+        return fail(SENSE_ERR_MISALIGNED, "buf must be 16-byte aligned and bytes a multiple of 16");
+    const hipError_t e = sense::launch_stream_read(buf, bytes, sink, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "read probe");
+    return ok();
+}

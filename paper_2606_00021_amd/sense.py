@@ -42,6 +42,7 @@ EXPORTED = (
     "sense_soft_gate_verify_workspace_size",
     "sense_soft_gate_verify",
     "sense_set_timer_events",
+    "sense_read_bandwidth_probe",
     "sense_status_string",
     "sense_last_error_message",
 )
@@ -112,6 +113,8 @@ def load_library() -> ctypes.CDLL:
         fn = getattr(lib, name)
         fn.argtypes = args
         fn.restype = ctypes.c_int
+    lib.sense_read_bandwidth_probe.argtypes = [P, SZ, P, P]
+    lib.sense_read_bandwidth_probe.restype = ctypes.c_int
     lib.sense_set_timer_events.argtypes = [ctypes.c_int, P, P]
     lib.sense_set_timer_events.restype = ctypes.c_int
     lib.sense_status_string.argtypes = [ctypes.c_int]
@@ -308,3 +311,14 @@ def sense_set_timer_events(which: int, start: "torch.cuda.Event | None",
         raise ValueError("record the events once before registering them (torch creates "
                          "the underlying hipEvent_t at the first record())")
     _check(load_library().sense_set_timer_events(which, sp, ep), "sense_set_timer_events")
+
+
+def sense_read_bandwidth_probe(buf: torch.Tensor, sink: torch.Tensor, stream=None) -> None:
+    """Enqueue one plain streaming read of ``buf`` (a contiguous GPU tensor);
+    ``sink`` is a 1-element int32/uint32 GPU tensor the kernel may write."""
+    if not buf.is_contiguous():
+        raise ValueError("buf must be contiguous")
+    nbytes = buf.numel() * buf.element_size() // 16 * 16
+    _check(load_library().sense_read_bandwidth_probe(_dev_ptr(buf, "buf"), nbytes,
+                                                     _dev_ptr(sink, "sink"), _stream_handle(stream)),
+           "sense_read_bandwidth_probe")

@@ -148,6 +148,13 @@ def test_verify_rejects(lib, kw, status):
     assert lib.sense_last_error_message()
 
 
+def test_read_probe_rejects(lib):
+    assert lib.sense_read_bandwidth_probe(None, 1024, p(FAKE), None) == INVALID
+    assert lib.sense_read_bandwidth_probe(p(FAKE), 0, p(FAKE), None) == INVALID
+    assert lib.sense_read_bandwidth_probe(p(FAKE + 8), 1024, p(FAKE), None) == MISALIGNED
+    assert lib.sense_read_bandwidth_probe(p(FAKE), 1000, p(FAKE), None) == MISALIGNED
+
+
 def test_verify_empty_batch_is_a_no_op(lib):
     assert verify_call(lib, n_cand=0, logits=None, drafts=None, acc=None, best=None, ws=None) == 0
 
