@@ -127,24 +127,38 @@ __device__ __forceinline__ void dma16(const void* g, void* lds) {
 // written by DMA is complete once the issuing wave's vmcnt wait returns.
 __device__ __forceinline__ void barrier_no_fence() { asm volatile("s_barrier" ::: "memory"); }
 
+// Key-tile layout in LDS (one tile = 16 rows x 128 bytes = two 32-dimension
+// steps).  Reading HBM in runs of only 64 bytes per row per load instruction
+// (the matrix-core operand layout: 16 rows x 4 lanes) caps the achieved
+// bandwidth near 4-5 TB/s on this device; runs of 128 bytes (8 rows per
+// instruction) reach the ~7 TB/s ceiling.  So each DMA instruction fetches 8
+// rows x 128 bytes and the operand layout is produced in LDS: rows 0-7 of a
+// tile go to entries [0, 64), rows 8-15 to [72, 136) (16-byte entries); lane
+// L = 8p + w of an instruction writes entry w of row p and fetches unit
+// (w + p) mod 8 of that row, so unit u of row p sits at entry (u - p) mod 8.
+// The rotation and the 72-entry offset of the second instruction make the
+// 16 rows a matrix-core read touches fall in 16 distinct 16-byte bank groups.
+constexpr int kTileVec = 136;                 // 16-byte entries per key tile
+constexpr int kTileSecond = 72;               // first entry of rows 8-15
+
 // One workgroup (4 waves) per contiguous run of key blocks; a block is 4*T
 // tiles of 16 keys, T tiles per wave; MT tiles of 16 queries (nq <= 16*MT of
 // them are real).
 //
 // Everything the matrix cores read goes through LDS, filled by
 // global_load_lds_dwordx4 (HBM/L2 -> LDS without registers) into a ring of P
-// stages; a stage is one 32-dimension step: each wave's T key fragments
-// (1 KiB each, lane-ordered, private to the wave) and the MT*(1+SPLIT) query
-// fragments shared by the four waves (each wave loads its share).  Loading
-// stays P-1 steps ahead of the matrix cores.  Every step a wave issues the
-// same number of loads (steps past the end reload a valid clamped address),
-// so the wait for a step is a fixed vmcnt; a workgroup barrier then makes the
-// other waves' query fragments visible and frees the slot that is refilled
-// next.  The loop holds no register-destination global load, because the
-// compiler's wait-count model does not follow LDS-DMA loads and would
-// otherwise drain the whole pipeline.  Lanes whose row lies past n load the
-// last row (their outputs are never stored); dimensions past d occur only in
-// the last step and are zeroed there.
+// stages; a stage is two 32-dimension steps: each wave's T key tiles (private
+// to the wave, laid out as above) and the 2*MT*(1+SPLIT) query fragments of
+// the two steps, shared by the four waves (each wave loads its share).
+// Loading stays P-1 stages ahead of the matrix cores.  Every stage a wave
+// issues the same number of loads (stages past the end reload a valid
+// clamped address), so the wait for a stage is a fixed vmcnt; a workgroup
+// barrier then makes the other waves' query fragments visible and frees the
+// slot that is refilled next.  The loop holds no register-destination global
+// load, because the compiler's wait-count model does not follow LDS-DMA loads
+// and would otherwise drain the whole pipeline.  Rows past n load the last
+// row (their outputs are never stored); dimensions past d occur only in the
+// last stage, load a clamped address and are zeroed at use.
 template <int KT, int MT, int T, int P, bool SPLIT>
 __global__ __launch_bounds__(256) void scan_mfma_kernel(
     const uint16_t* __restrict__ keys, int64_t ld, int64_t n, int d,
@@ -152,58 +166,74 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
     const float* __restrict__ inv_qn, int nq, const float* __restrict__ inv_norm,
     float* __restrict__ scores, int64_t blocks_per_group) {
     constexpr int NA = MT * (SPLIT ? 2 : 1);      // query fragments per step
-    constexpr int NA_W = (NA + 3) / 4;            // loaded per wave (some waves idle)
-    constexpr int OPS = T + NA_W;                 // DMA loads per wave per step
+    constexpr int NAS = 2 * NA;                   // per stage
+    constexpr int NA_W = (NAS + 3) / 4;           // loaded per wave
+    constexpr int OPS = 2 * T + NA_W;             // DMA loads per wave per stage
     constexpr int KB = 64 * T;                    // keys per workgroup block
     static_assert((P - 2) * OPS < 64, "vmcnt range");
-    __shared__ __attribute__((aligned(16))) u32x4 kring[P][4][T][64];
+    __shared__ __attribute__((aligned(16))) u32x4 kring[P][4][T][kTileVec];
     __shared__ __attribute__((aligned(16))) u32x4 aring[P][NA_W * 4][64];
     const int lane = threadIdx.x & 63;
     const int wv = threadIdx.x >> 6;
     const int col = lane & 15, grp = lane >> 4;
+    const int dp = lane >> 3;                     // DMA: row within the instruction
+    const int du = ((lane & 7) + dp) & 7;         // DMA: 16-byte unit fetched
     const int64_t nblk = (n + KB - 1) / KB;
     const int64_t b0 = (int64_t)blockIdx.x * blocks_per_group;
     if (b0 >= nblk) return;                       // uniform over the workgroup
     const int64_t b1 = (b0 + blocks_per_group < nblk) ? b0 + blocks_per_group : nblk;
     const int nks = (d + 31) / 32;
+    const int nst = (nks + 1) / 2;
     const bool ragged = (d & 31) != 0;
 
-    // Query fragment a of this wave's share: a = wv + 4*j; fragment index f
-    // in [0, NA): f < MT -> hi tile f, else lo tile f - MT.
+    // This wave's share of the query fragments: fs = wv + 4*j in [0, NAS),
+    // step-in-stage fs / NA, fragment fs % NA (< MT: hi tile, else lo tile).
     const uint16_t* qsrc[NA_W];
+    int qstep[NA_W];
 #pragma unroll
     for (int j = 0; j < NA_W; ++j) {
-        int f = wv + 4 * j;
-        if (f >= NA) f = NA - 1;                  // idle slot: harmless duplicate
+        int fs = wv + 4 * j;
+        if (fs >= NAS) fs = NAS - 1;              // idle slot: harmless duplicate
+        const int f = fs % NA;
         const uint16_t* base = (f < MT) ? qhi : qlo;
-        const int mt = (f < MT) ? f : f - MT;
-        qsrc[j] = base + (int64_t)(mt * 16 + col) * d;
+        const int mt = f % MT;
+        qsrc[j] = base + (int64_t)(mt * 16 + col) * d + grp * 8;
+        qstep[j] = fs / NA;
     }
-    auto kofs = [&](int s) -> int {               // clamped dimension offset
-        const int sc = s < nks ? s : nks - 1;
-        const int kd = sc * 32 + grp * 8;
-        return kd < d ? kd : 0;
-    };
+    // B-operand entry of this lane inside a key tile, for unit u = 4*step + grp.
+    const int ri = col >> 3, rp = col & 7;
+    auto bentry = [&](int step) { return ri * kTileSecond + 8 * rp + (((4 * step + grp) - rp) & 7); };
 
     for (int64_t blk = b0; blk < b1; ++blk) {
         const int64_t key0 = blk * KB + (int64_t)wv * 16 * T;
-        const uint16_t* kp[T];
+        const uint16_t* kp[T][2];
         bool kv[T];
 #pragma unroll
         for (int t = 0; t < T; ++t) {
-            const int64_t row = key0 + t * 16 + col;
-            kv[t] = row < n;
-            kp[t] = keys + (kv[t] ? row : n - 1) * ld;
+            kv[t] = key0 + t * 16 + col < n;
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                int64_t row = key0 + t * 16 + 8 * i + dp;
+                if (row >= n) row = n - 1;
+                kp[t][i] = keys + row * ld + du * 8;
+            }
         }
-        auto issue = [&](int s) {
-            const int ko = kofs(s);
-            const int slot = s % P;
+        auto issue = [&](int st) {
+            const int sc = st < nst ? st : nst - 1;
+            const int slot = st % P;
+            // kp already points at this lane's unit; past d it falls back to
+            // the row's first 16 bytes (a valid address, zeroed at use).
+            const int ko = (sc * 64 + du * 8 < d) ? sc * 64 : -du * 8;
 #pragma unroll
             for (int t = 0; t < T; ++t)
-                dma16(kp[t] + ko, &kring[slot][wv][t][0]);
 #pragma unroll
-            for (int j = 0; j < NA_W; ++j)
-                dma16(qsrc[j] + ko, &aring[slot][wv + 4 * j][0]);
+                for (int i = 0; i < 2; ++i) dma16(kp[t][i] + ko, &kring[slot][wv][t][i * kTileSecond]);
+#pragma unroll
+            for (int j = 0; j < NA_W; ++j) {
+                const int qd = (sc * 2 + qstep[j]) * 32 + grp * 8;
+                const int qo = qd < d ? qd - grp * 8 : -grp * 8;   // past d: the row's start
+                dma16(qsrc[j] + qo, &aring[slot][wv + 4 * j][0]);
+            }
         };
         f32x4 acc[T][MT];
 #pragma unroll
@@ -213,27 +243,33 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
 
 #pragma unroll
         for (int s = 0; s < P - 1; ++s) issue(s);
-        for (int ks = 0; ks < nks; ++ks) {
-            // Loads issued after step ks: steps ks+1 .. ks+P-2.
+        for (int st = 0; st < nst; ++st) {
+            // Loads issued after stage st: stages st+1 .. st+P-2.
             wait_vmcnt<(P - 2) * OPS>();
             barrier_no_fence();
-            issue(ks + P - 1);                    // refills the slot read at ks-1
-            const int slot = ks % P;
-            const bool mask = ragged && ks == nks - 1 && ks * 32 + grp * 8 >= d;
-            u32x4 a[NA];
+            issue(st + P - 1);                    // refills the slot read at st-1
+            const int slot = st % P;
 #pragma unroll
-            for (int f = 0; f < NA; ++f) {
-                a[f] = aring[slot][f][lane];
-                if (mask) a[f] = u32x4{0u, 0u, 0u, 0u};
-            }
+            for (int j = 0; j < 2; ++j) {
+                const int ks = 2 * st + j;
+                if (ks >= nks) break;
+                const bool mask = ragged && ks == nks - 1 && ks * 32 + grp * 8 >= d;
+                u32x4 a[NA];
 #pragma unroll
-            for (int t = 0; t < T; ++t) {
-                u32x4 b = kring[slot][wv][t][lane];
-                if (mask) b = u32x4{0u, 0u, 0u, 0u};
+                for (int f = 0; f < NA; ++f) {
+                    a[f] = aring[slot][j * NA + f][lane];
+                    if (mask) a[f] = u32x4{0u, 0u, 0u, 0u};
+                }
+                const int be = bentry(j);
 #pragma unroll
-                for (int mt = 0; mt < MT; ++mt) {
-                    acc[t][mt] = mfma<KT>(a[mt], b, acc[t][mt]);
-                    if constexpr (SPLIT) acc[t][mt] = mfma<KT>(a[MT + mt], b, acc[t][mt]);
+                for (int t = 0; t < T; ++t) {
+                    u32x4 b = kring[slot][wv][t][be];
+                    if (mask) b = u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+                    for (int mt = 0; mt < MT; ++mt) {
+                        acc[t][mt] = mfma<KT>(a[mt], b, acc[t][mt]);
+                        if constexpr (SPLIT) acc[t][mt] = mfma<KT>(a[MT + mt], b, acc[t][mt]);
+                    }
                 }
             }
         }
@@ -301,10 +337,10 @@ hipError_t launch_group(const void* keys, int64_t n, int d, int64_t ld, const ui
                         const uint16_t* qlo, const float* inv_qn, int nq, const float* inv_norm,
                         float* scores, hipStream_t stream) {
     switch ((nq + 15) / 16) {
-        case 1: return launch_tile<KT, 1, 8, 4, SPLIT>(keys, n, d, ld, qhi, qlo, inv_qn, nq, inv_norm, scores, stream);
-        case 2: return launch_tile<KT, 2, 4, 5, SPLIT>(keys, n, d, ld, qhi, qlo, inv_qn, nq, inv_norm, scores, stream);
-        case 3: return launch_tile<KT, 3, 4, 5, SPLIT>(keys, n, d, ld, qhi, qlo, inv_qn, nq, inv_norm, scores, stream);
-        default: return launch_tile<KT, 4, 4, 5, SPLIT>(keys, n, d, ld, qhi, qlo, inv_qn, nq, inv_norm, scores, stream);
+        case 1: return launch_tile<KT, 1, 4, 4, SPLIT>(keys, n, d, ld, qhi, qlo, inv_qn, nq, inv_norm, scores, stream);
+        case 2: return launch_tile<KT, 2, 4, 3, SPLIT>(keys, n, d, ld, qhi, qlo, inv_qn, nq, inv_norm, scores, stream);
+        case 3: return launch_tile<KT, 3, 2, 4, SPLIT>(keys, n, d, ld, qhi, qlo, inv_qn, nq, inv_norm, scores, stream);
+        default: return launch_tile<KT, 4, 2, 4, SPLIT>(keys, n, d, ld, qhi, qlo, inv_qn, nq, inv_norm, scores, stream);
     }
 }
 
