@@ -59,8 +59,10 @@ def _load():
         lib.oracle_soft_gate_verify.argtypes = [
             P, ctypes.c_int, I64, P, P, I32, I32, I32, I32, D, I32, I32, I32, I32, P, P, P, P, P, P
         ]
+        lib.oracle_select_candidates.argtypes = [P, P, P, I32, P, P, P, I32, I32, I32, I32, D, D,
+                                                 D, I32, P, P, P, P]
         for f in ("oracle_scores", "oracle_topk", "oracle_gather", "oracle_row_stats",
-                  "oracle_soft_gate_verify"):
+                  "oracle_soft_gate_verify", "oracle_select_candidates"):
             getattr(lib, f).restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -179,3 +181,32 @@ def soft_gate_verify(logits, dtype: str, drafts, draft_len=None, n_groups: int =
         raise ValueError("oracle_soft_gate_verify rejected its arguments")
     return {"accept_len": acc, "best": best[:n_groups], "gate_score": gs, "masks": masks,
             "argmax": am, "rank": rk}
+
+
+def select_candidates(scores_s, drafts_s, len_s, anchor: int, top_n: int, alpha: float,
+                      beta: float, delta: float = 0.0, anchor_override: bool = True,
+                      scores_d=None, drafts_d=None, len_d=None):
+    """Composite-score Top-N over static + dynamic hits with the anchor
+    override (Sec. 3.2 Eq. 8, Alg. 2).  Returns (drafts, lengths, source,
+    composite scores)."""
+    def prep(sc, dr, ln):
+        if sc is None:
+            return None, None, None, 0
+        sc = np.ascontiguousarray(sc, dtype=np.float64)
+        dr = np.ascontiguousarray(dr, dtype=np.int32)
+        ln = None if ln is None else np.ascontiguousarray(ln, dtype=np.int32)
+        return sc, dr, ln, sc.shape[0]
+    ss, ds, ls, ns = prep(scores_s, drafts_s, len_s)
+    sd, dd, ld, nd = prep(scores_d, drafts_d, len_d)
+    m = (ds if ds is not None else dd).shape[1]
+    out_dr = np.empty((top_n, m), dtype=np.int32)
+    out_len = np.empty(top_n, dtype=np.int32)
+    out_src = np.empty(top_n, dtype=np.int32)
+    out_sc = np.empty(top_n, dtype=np.float64)
+    rc = _load().oracle_select_candidates(
+        _ptr(ss), _ptr(ds), _ptr(ls), ns, _ptr(sd), _ptr(dd), _ptr(ld), nd, int(anchor), m,
+        top_n, float(alpha), float(beta), float(delta), int(bool(anchor_override)),
+        _ptr(out_dr), _ptr(out_len), _ptr(out_src), _ptr(out_sc))
+    if rc:
+        raise ValueError("oracle_select_candidates rejected its arguments")
+    return out_dr, out_len, out_src, out_sc

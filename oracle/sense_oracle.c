@@ -357,3 +357,84 @@ int oracle_soft_gate_verify(const void *logits, int logits_dtype, int64_t row_st
     free(em); free(ent); free(tk); free(gs); free(am); free(rk); free(lens);
     return 0;
 }
+
+/* ------------------------------------------------------ candidate selection */
+
+typedef struct { double s; int32_t i; } ranked_cand;
+
+/* (composite score descending, position in D_all ascending); NaN last. */
+static int cmp_cand(const void *pa, const void *pb)
+{
+    const ranked_cand *a = (const ranked_cand *)pa, *b = (const ranked_cand *)pb;
+    int an = isnan(a->s), bn = isnan(b->s);
+    if (an != bn) return an ? 1 : -1;
+    if (!an) {
+        if (a->s > b->s) return -1;
+        if (a->s < b->s) return 1;
+    }
+    return (a->i < b->i) ? -1 : (a->i > b->i);
+}
+
+/* Candidate selection of one query (Sec. 3.2 Eq. 8; Alg. 2 hybrid retrieval,
+ * composite score, Top-N and anchor override), literally:
+ *   D_all = static hits (n_s) followed by dynamic hits (n_d);
+ *   s     = [scores_s ; scores_d + delta];
+ *   S_i   = alpha * I(D_all[i][0] == anchor) + beta * s_i   (a draft of
+ *           length 0 has no first token: I = 0);
+ *   D     = the top_n rows of D_all by (S desc, i asc), full sort;
+ *   if anchor_override: D[0][0] = anchor and D[top_n-1][0] = anchor (a row
+ *           of length 0 becomes length 1).
+ * Drafts are n x max_len int32 padded with -1, lengths n.  Outputs
+ * top_n x max_len drafts, top_n lengths, the position of each selected row in
+ * D_all (source) and its composite score.  top_n <= n_s + n_d. */
+int oracle_select_candidates(const double *scores_s, const int32_t *drafts_s,
+                             const int32_t *len_s, int32_t n_s,
+                             const double *scores_d, const int32_t *drafts_d,
+                             const int32_t *len_d, int32_t n_d, int32_t anchor,
+                             int32_t max_len, int32_t top_n, double alpha, double beta,
+                             double delta, int32_t anchor_override, int32_t *out_drafts,
+                             int32_t *out_len, int32_t *out_source, double *out_score)
+{
+    int32_t n_all = n_s + n_d;
+    if (n_s < 0 || n_d < 0 || max_len < 1 || top_n < 1 || top_n > n_all ||
+        !out_drafts || !out_len || (n_s > 0 && (!scores_s || !drafts_s)) ||
+        (n_d > 0 && (!scores_d || !drafts_d)))
+        return -1;
+    ranked_cand *c = (ranked_cand *)malloc(sizeof(ranked_cand) * (size_t)n_all);
+    if (!c) return -1;
+    for (int32_t i = 0; i < n_all; ++i) {
+        int dyn = i >= n_s;
+        int32_t r = dyn ? i - n_s : i;
+        const int32_t *row = (dyn ? drafts_d : drafts_s) + (int64_t)r * max_len;
+        int32_t len = dyn ? (len_d ? len_d[r] : max_len) : (len_s ? len_s[r] : max_len);
+        double s = dyn ? scores_d[r] + delta : scores_s[r];
+        double match = (len > 0 && row[0] == anchor) ? 1.0 : 0.0;
+        c[i].s = alpha * match + beta * s;
+        c[i].i = i;
+    }
+    qsort(c, (size_t)n_all, sizeof(ranked_cand), cmp_cand);
+    for (int32_t r = 0; r < top_n; ++r) {
+        int32_t i = c[r].i;
+        int dyn = i >= n_s;
+        int32_t src = dyn ? i - n_s : i;
+        const int32_t *row = (dyn ? drafts_d : drafts_s) + (int64_t)src * max_len;
+        int32_t len = dyn ? (len_d ? len_d[src] : max_len) : (len_s ? len_s[src] : max_len);
+        if (len < 0) len = 0;
+        if (len > max_len) len = max_len;
+        for (int32_t j = 0; j < max_len; ++j)
+            out_drafts[(int64_t)r * max_len + j] = j < len ? row[j] : -1;
+        out_len[r] = len;
+        if (out_source) out_source[r] = i;
+        if (out_score) out_score[r] = c[r].s;
+    }
+    if (anchor_override) {
+        int32_t ends[2] = {0, top_n - 1};
+        for (int e = 0; e < 2; ++e) {
+            int32_t r = ends[e];
+            out_drafts[(int64_t)r * max_len] = anchor;
+            if (out_len[r] < 1) out_len[r] = 1;
+        }
+    }
+    free(c);
+    return 0;
+}

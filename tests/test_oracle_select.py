@@ -1,0 +1,99 @@
+"""Pins for the candidate-selection oracle (Sec. 3.2 Eq. 8; Alg. 2 composite
+score, Top-N, dynamic boost delta and anchor override): a hand-worked golden
+example, the lexicographic order that alpha >> beta imposes, the pure
+similarity order at alpha = 0 (numpy lexsort), the delta boost, position
+tie-breaks and the override's guarantee."""
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def test_golden_example():
+    g = json.load(open(os.path.join(GOLDEN, "candidate_selection_example.json")))
+    dr, ln, src, sc = oracle.select_candidates(
+        np.array(g["static_scores"]), np.array(g["static_drafts"]), np.array(g["static_len"]),
+        g["anchor"], g["top_n"], g["alpha"], g["beta"], g["delta"],
+        scores_d=np.array(g["dynamic_scores"]), drafts_d=np.array(g["dynamic_drafts"]),
+        len_d=np.array(g["dynamic_len"]))
+    assert src.tolist() == g["expected_source"]
+    np.testing.assert_allclose(sc, g["expected_scores"], rtol=0, atol=1e-12)
+    assert dr.tolist() == g["expected_drafts"]
+    assert ln.tolist() == g["expected_len"]
+    _, _, src_all, sc_all = oracle.select_candidates(
+        np.array(g["static_scores"]), np.array(g["static_drafts"]), np.array(g["static_len"]),
+        g["anchor"], 7, g["alpha"], g["beta"], g["delta"], anchor_override=False,
+        scores_d=np.array(g["dynamic_scores"]), drafts_d=np.array(g["dynamic_drafts"]),
+        len_d=np.array(g["dynamic_len"]))
+    assert src_all.tolist() == g["order"]
+    np.testing.assert_allclose(sc_all, np.array(g["composite_all"])[g["order"]], atol=1e-12)
+
+
+def _random(rng, n, m=6, vocab=20):
+    s = rng.uniform(-1, 1, n)
+    d = rng.integers(0, vocab, (n, m)).astype(np.int32)
+    ln = rng.integers(0, m + 1, n).astype(np.int32)
+    for i in range(n):
+        d[i, ln[i]:] = -1
+    return s, d, ln
+
+
+def test_alpha_much_larger_than_beta_is_lexicographic():
+    rng = np.random.default_rng(3)
+    s, d, ln = _random(rng, 200)
+    anchor = 4
+    dr, _, src, _ = oracle.select_candidates(s, d, ln, anchor, 50, 1e6, 1.0, anchor_override=False)
+    match = (ln > 0) & (d[:, 0] == anchor)
+    ref = sorted(range(200), key=lambda i: (not match[i], -s[i], i))[:50]
+    assert src.tolist() == ref
+
+
+def test_alpha_zero_is_similarity_order_over_both_sources():
+    rng = np.random.default_rng(5)
+    s, d, ln = _random(rng, 120)
+    sd_, dd, ld = _random(rng, 40)
+    delta = 0.25
+    _, _, src, _ = oracle.select_candidates(s, d, ln, 1, 60, 0.0, 1.0, delta,
+                                            anchor_override=False, scores_d=sd_, drafts_d=dd,
+                                            len_d=ld)
+    allsc = np.concatenate([s, sd_ + delta])
+    ref = np.lexsort((np.arange(160), -allsc))[:60]
+    assert src.tolist() == ref.tolist()
+
+
+def test_large_delta_puts_dynamic_hits_first():
+    rng = np.random.default_rng(8)
+    s, d, ln = _random(rng, 30)
+    sd_, dd, ld = _random(rng, 10)
+    _, _, src, _ = oracle.select_candidates(s, d, ln, 1, 12, 0.0, 1.0, 100.0,
+                                            anchor_override=False, scores_d=sd_, drafts_d=dd,
+                                            len_d=ld)
+    assert sorted(src.tolist()[:10]) == list(range(30, 40))
+
+
+def test_equal_scores_keep_position_order():
+    s = np.full(6, 0.5)
+    d = np.tile(np.arange(4, dtype=np.int32), (6, 1))
+    _, _, src, _ = oracle.select_candidates(s, d, None, 99, 6, 1.0, 1.0, anchor_override=False,
+                                            scores_d=np.full(3, 0.5), drafts_d=d[:3])
+    assert src.tolist() == [0, 1, 2, 3, 4, 5]
+
+
+@pytest.mark.parametrize("top_n", [1, 2, 7])
+def test_override_puts_the_anchor_first_in_first_and_last_row(top_n):
+    rng = np.random.default_rng(top_n)
+    s, d, ln = _random(rng, 20)
+    anchor = 17
+    dr0, ln0, src0, _ = oracle.select_candidates(s, d, ln, anchor, top_n, 0.0, 1.0,
+                                                 anchor_override=False)
+    dr, lns, src, _ = oracle.select_candidates(s, d, ln, anchor, top_n, 0.0, 1.0)
+    assert np.array_equal(src, src0)
+    assert dr[0, 0] == anchor and dr[-1, 0] == anchor
+    assert lns[0] >= 1 and lns[-1] >= 1
+    assert np.array_equal(dr[1:-1], dr0[1:-1])
+    assert np.array_equal(dr[:, 1:], dr0[:, 1:])
