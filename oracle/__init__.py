@@ -60,7 +60,7 @@ def _load():
             P, ctypes.c_int, I64, P, P, I32, I32, I32, I32, D, I32, I32, I32, I32, P, P, P, P, P, P
         ]
         lib.oracle_select_candidates.argtypes = [P, P, P, I32, P, P, P, I32, I32, I32, I32, D, D,
-                                                 D, I32, P, P, P, P]
+                                                 D, I32, I32, P, P, P, P]
         for f in ("oracle_scores", "oracle_topk", "oracle_gather", "oracle_row_stats",
                   "oracle_soft_gate_verify", "oracle_select_candidates"):
             getattr(lib, f).restype = ctypes.c_int
@@ -185,10 +185,11 @@ def soft_gate_verify(logits, dtype: str, drafts, draft_len=None, n_groups: int =
 
 def select_candidates(scores_s, drafts_s, len_s, anchor: int, top_n: int, alpha: float,
                       beta: float, delta: float = 0.0, anchor_override: bool = True,
-                      scores_d=None, drafts_d=None, len_d=None):
+                      scores_d=None, drafts_d=None, len_d=None, precision: str = "f64"):
     """Composite-score Top-N over static + dynamic hits with the anchor
     override (Sec. 3.2 Eq. 8, Alg. 2).  Returns (drafts, lengths, source,
-    composite scores)."""
+    composite scores).  precision "f32" takes the composite score in binary32
+    (delta added in binary32, one fused multiply-add)."""
     def prep(sc, dr, ln):
         if sc is None:
             return None, None, None, 0
@@ -206,7 +207,24 @@ def select_candidates(scores_s, drafts_s, len_s, anchor: int, top_n: int, alpha:
     rc = _load().oracle_select_candidates(
         _ptr(ss), _ptr(ds), _ptr(ls), ns, _ptr(sd), _ptr(dd), _ptr(ld), nd, int(anchor), m,
         top_n, float(alpha), float(beta), float(delta), int(bool(anchor_override)),
-        _ptr(out_dr), _ptr(out_len), _ptr(out_src), _ptr(out_sc))
+        {"f64": 0, "f32": 1}[precision], _ptr(out_dr), _ptr(out_len), _ptr(out_src), _ptr(out_sc))
     if rc:
         raise ValueError("oracle_select_candidates rejected its arguments")
     return out_dr, out_len, out_src, out_sc
+
+
+def dynamic_spans(tokens, max_span: int):
+    """Continuation table of a dynamic context cache (Alg. 1's retriever
+    update; Alg. 2's dynamic search): the key stored at position p predicted
+    token p, so its continuation is tokens[p : p + max_span], cut at the end
+    of what has been generated.  Returns (spans n x max_span int32 padded
+    with -1, lengths n int32)."""
+    tokens = np.asarray(tokens, dtype=np.int32)
+    n = tokens.shape[0]
+    spans = np.full((n, max_span), -1, dtype=np.int32)
+    lens = np.empty(n, dtype=np.int32)
+    for p in range(n):
+        seg = tokens[p:p + max_span]
+        spans[p, :seg.shape[0]] = seg
+        lens[p] = seg.shape[0]
+    return spans, lens

@@ -386,14 +386,18 @@ static int cmp_cand(const void *pa, const void *pb)
  *           of length 0 becomes length 1).
  * Drafts are n x max_len int32 padded with -1, lengths n.  Outputs
  * top_n x max_len drafts, top_n lengths, the position of each selected row in
- * D_all (source) and its composite score.  top_n <= n_s + n_d. */
+ * D_all (source) and its composite score.  top_n <= n_s + n_d.
+ * f32 != 0 takes the composite score in binary32 (see the loop) so that an
+ * implementation computing in binary32 can be compared order-exactly; the
+ * order is still a full sort by the same rule. */
 int oracle_select_candidates(const double *scores_s, const int32_t *drafts_s,
                              const int32_t *len_s, int32_t n_s,
                              const double *scores_d, const int32_t *drafts_d,
                              const int32_t *len_d, int32_t n_d, int32_t anchor,
                              int32_t max_len, int32_t top_n, double alpha, double beta,
-                             double delta, int32_t anchor_override, int32_t *out_drafts,
-                             int32_t *out_len, int32_t *out_source, double *out_score)
+                             double delta, int32_t anchor_override, int32_t f32,
+                             int32_t *out_drafts, int32_t *out_len, int32_t *out_source,
+                             double *out_score)
 {
     int32_t n_all = n_s + n_d;
     if (n_s < 0 || n_d < 0 || max_len < 1 || top_n < 1 || top_n > n_all ||
@@ -407,9 +411,17 @@ int oracle_select_candidates(const double *scores_s, const int32_t *drafts_s,
         int32_t r = dyn ? i - n_s : i;
         const int32_t *row = (dyn ? drafts_d : drafts_s) + (int64_t)r * max_len;
         int32_t len = dyn ? (len_d ? len_d[r] : max_len) : (len_s ? len_s[r] : max_len);
-        double s = dyn ? scores_d[r] + delta : scores_s[r];
-        double match = (len > 0 && row[0] == anchor) ? 1.0 : 0.0;
-        c[i].s = alpha * match + beta * s;
+        int match = len > 0 && row[0] == anchor;
+        if (f32) {
+            /* The same formula taken in binary32, rounding each step:
+             * s = fl(s_d + delta) for dynamic hits, S = fl(beta * s + alpha * I)
+             * as one fused multiply-add (C99 fmaf rounds once). */
+            float sf = dyn ? (float)scores_d[r] + (float)delta : (float)scores_s[r];
+            c[i].s = (double)fmaf((float)beta, sf, match ? (float)alpha : 0.0f);
+        } else {
+            double s = dyn ? scores_d[r] + delta : scores_s[r];
+            c[i].s = alpha * (match ? 1.0 : 0.0) + beta * s;
+        }
         c[i].i = i;
     }
     qsort(c, (size_t)n_all, sizeof(ranked_cand), cmp_cand);

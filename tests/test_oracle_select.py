@@ -97,3 +97,49 @@ def test_override_puts_the_anchor_first_in_first_and_last_row(top_n):
     assert lns[0] >= 1 and lns[-1] >= 1
     assert np.array_equal(dr[1:-1], dr0[1:-1])
     assert np.array_equal(dr[:, 1:], dr0[:, 1:])
+
+
+def test_binary32_mode_orders_like_the_f64_mode_when_scores_are_apart():
+    g = json.load(open(os.path.join(GOLDEN, "candidate_selection_example.json")))
+    args = (np.array(g["static_scores"]), np.array(g["static_drafts"]), np.array(g["static_len"]),
+            g["anchor"], g["top_n"], g["alpha"], g["beta"], g["delta"])
+    kw = dict(scores_d=np.array(g["dynamic_scores"]), drafts_d=np.array(g["dynamic_drafts"]),
+              len_d=np.array(g["dynamic_len"]))
+    dr, ln, src, sc = oracle.select_candidates(*args, precision="f32", **kw)
+    assert src.tolist() == g["expected_source"]
+    assert dr.tolist() == g["expected_drafts"]
+    np.testing.assert_allclose(sc, g["expected_scores"], rtol=1e-6)
+    assert np.array_equal(sc.astype(np.float32).astype(np.float64), sc)
+
+
+def test_binary32_mode_ties_scores_that_round_together():
+    s = np.array([0.5, 0.5 + 1e-12])
+    d = np.array([[1, 2], [3, 4]], dtype=np.int32)
+    _, _, src64, _ = oracle.select_candidates(s, d, None, 9, 2, 0.0, 1.0, anchor_override=False)
+    _, _, src32, _ = oracle.select_candidates(s, d, None, 9, 2, 0.0, 1.0, anchor_override=False,
+                                              precision="f32")
+    assert src64.tolist() == [1, 0]
+    assert src32.tolist() == [0, 1]
+
+
+def test_dynamic_spans_are_the_following_tokens():
+    spans, lens = oracle.dynamic_spans([5, 6, 7, 8], 3)
+    assert spans.tolist() == [[5, 6, 7], [6, 7, 8], [7, 8, -1], [8, -1, -1]]
+    assert lens.tolist() == [3, 3, 2, 1]
+
+
+def test_override_gives_the_first_and_last_draft_an_accepted_token():
+    """Alg. 2's override forces both ends of the pool to start with the greedy
+    anchor, and row 0 of every draft is judged by the shared distribution
+    whose argmax is that anchor, so the exact-match gate accepts it."""
+    rng = np.random.default_rng(11)
+    vocab, m, n = 50, 5, 12
+    s, d, ln = _random(rng, n, m=m, vocab=vocab)
+    shared = rng.normal(0, 2, vocab).astype(np.float32)
+    anchor = int(np.argmax(shared))
+    top_n = 6
+    dr, lns, _, _ = oracle.select_candidates(s, d, ln, anchor, top_n, 0.0, 1.0)
+    logits = rng.normal(0, 2, (top_n, m, vocab)).astype(np.float32)
+    logits[:, 0, :] = shared
+    out = oracle.soft_gate_verify(logits, "f32", dr, lns, gamma=10.0)
+    assert out["accept_len"][0] >= 1 and out["accept_len"][-1] >= 1
