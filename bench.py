@@ -39,6 +39,10 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="approximate CPU time spent timing the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-sen", action="store_true",
+                    help="skip the candidate-selection leg (dynamic cache + composite Top-N)")
+    ap.add_argument("--sen-context", type=int, default=4096,
+                    help="rows of generation context in the dynamic cache of the SEN leg")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after the timed region, run one plain device copy of this many MiB "
                          "(a reference kernel of known traffic for HBM counter runs)")
@@ -129,6 +133,89 @@ def cpu_baseline(w, ds, q, logits, drafts, budget_s: float):
     }
 
 
+def sen_leg(args, w, ds, q, src_rows, index, ws_r, outs, K, dev):
+    """Candidate-selection extension of the step, timed apart from the headline
+    step: static retrieval (k hits), dynamic-cache retrieval over a
+    generation context, composite Top-N (alpha 100, beta 1, delta 0.05, the
+    anchor override) and verification of the N selected drafts.  Also times
+    the selection kernel alone, the dynamic retrieval alone and one cache
+    append of 4 accepted positions."""
+    import torch
+
+    from paper_2606_00021_amd import sense, synth
+
+    k, m, nq = w.k, w.span, w.n_queries
+    k_dyn, top_n, ctx_len = 16, w.k, args.sen_context
+    anchors = ds.spans[src_rows, 0].to(torch.int32).contiguous()
+    ctx = synth.make_context(w, ds, args.seed, ctx_len, int(src_rows[0]), int(anchors[0]))
+    kdt = synth.DTYPES[w.key_dtype]
+    cache = sense.sense_build_dynamic_index(w.d, ctx_len, m, key_dtype=kdt, metric=w.metric)
+    sense.sense_index_append(cache, ctx.keys, ctx.tokens)
+    ws_d = torch.empty(max(1, sense.sense_retrieve_workspace_size(cache, nq, k_dyn)),
+                       dtype=torch.uint8, device=dev)
+    outs_d = (torch.empty((nq, k_dyn), dtype=torch.int64, device=dev),
+              torch.empty((nq, k_dyn), dtype=torch.float32, device=dev),
+              torch.empty((nq, k_dyn, m), dtype=torch.int32, device=dev),
+              torch.empty((nq, k_dyn), dtype=torch.int32, device=dev))
+    sel = (torch.empty((nq, top_n, m), dtype=torch.int32, device=dev),
+           torch.empty((nq, top_n), dtype=torch.int32, device=dev),
+           torch.empty((nq, top_n), dtype=torch.int32, device=dev),
+           torch.empty((nq, top_n), dtype=torch.float32, device=dev))
+    vq = w.verify_queries
+    c = vq * top_n
+
+    def retrieve_select():
+        sense.sense_retrieve(index, q, k, workspace=ws_r, out=outs)
+        sense.sense_retrieve(cache, q, k_dyn, workspace=ws_d, out=outs_d)
+        sense.sense_select_candidates((outs[1], outs[2], outs[3]),
+                                      (outs_d[1], outs_d[2], outs_d[3]), anchors, top_n,
+                                      100.0, 1.0, 0.05, True, out=sel)
+
+    retrieve_select()
+    drafts = sel[0][:vq].view(c, m)
+    dlen = sel[1][:vq].view(c)
+    logits = synth.make_logits(w, drafts, args.seed + 1)
+    ws_v = torch.empty(max(1, sense.sense_soft_gate_verify_workspace_size(c, m, w.vocab)),
+                       dtype=torch.uint8, device=dev)
+    out_v = {"accept_len": torch.empty(c, dtype=torch.int32, device=dev),
+             "best": torch.empty(vq, dtype=torch.int32, device=dev)}
+
+    def step():
+        retrieve_select()
+        sense.sense_soft_gate_verify(logits, drafts, dlen, n_groups=vq, workspace=ws_v,
+                                     out=out_v)
+
+    def timed(fn, reps):
+        for _ in range(3):
+            fn()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    ms_step = timed(step, K)
+    dyn_ms = timed(lambda: sense.sense_retrieve(cache, q, k_dyn, workspace=ws_d, out=outs_d), K)
+    sel_ms = timed(lambda: sense.sense_select_candidates(
+        (outs[1], outs[2], outs[3]), (outs_d[1], outs_d[2], outs_d[3]), anchors, top_n, 100.0,
+        1.0, 0.05, True, out=sel), K)
+    grow = sense.sense_build_dynamic_index(w.d, 4 * (K + 3), m, key_dtype=kdt, metric=w.metric)
+    new_keys, new_tok = ctx.keys[:4].contiguous(), ctx.tokens[:4].contiguous()
+    append_ms = timed(lambda: sense.sense_index_append(grow, new_keys, new_tok), K)
+    grow.close()
+    cache.close()
+    log(f"[bench] SEN step {ms_step:.4f} ms (dynamic retrieval {dyn_ms * 1e3:.1f} us over "
+        f"{ctx_len} rows, selection {sel_ms * 1e3:.1f} us, append {append_ms * 1e3:.1f} us)")
+    return {"queries_per_s": nq / (ms_step * 1e-3), "ms_per_step": ms_step,
+            "context_rows": ctx_len, "k_static": k, "k_dynamic": k_dyn, "top_n": top_n,
+            "alpha": 100.0, "beta": 1.0, "delta": 0.05,
+            "dynamic_retrieve_us": dyn_ms * 1e3, "select_us": sel_ms * 1e3,
+            "append4_us": append_ms * 1e3}
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -150,7 +237,7 @@ def main():
         f"M={w.span} V={w.vocab} {w.logits_dtype}")
     t0 = time.perf_counter()
     ds = synth.make_datastore(w, args.seed, dev)
-    q, _ = synth.make_queries(w, ds, args.seed)
+    q, src_rows = synth.make_queries(w, ds, args.seed)
     index = sense.sense_build_index(ds.keys, ds.spans, ds.span_len, metric=w.metric)
     nq, k, m = w.n_queries, w.k, w.span
     ws_r = torch.empty(max(1, sense.sense_retrieve_workspace_size(index, nq, k)),
@@ -282,6 +369,8 @@ def main():
         log(f"[bench] copy probe: {args.copy_probe_mib} MiB read + {args.copy_probe_mib} MiB "
             f"written by one copy kernel")
         del src, dst
+    if not args.no_sen:
+        res["sen"] = sen_leg(args, w, ds, q, src_rows, index, ws_r, outs, K, dev)
     if not args.no_cpu_baseline:
         log("[bench] timing the oracle on the host (cpu_baseline)")
         t0 = time.perf_counter()

@@ -19,6 +19,13 @@
  *                           aligned logits: accepted prefix length per draft
  *                           and the best draft per group
  *                           (Sec. 3.3 Eqs. 12-18; Alg. 4)
+ *   sense_build_dynamic_index, sense_index_append
+ *                           the dynamic context cache C_d and its update
+ *                           (Sec. 3.2 Eq. 6; Alg. 1's retriever update;
+ *                           Alg. 2's dynamic search is sense_retrieve on it)
+ *   sense_select_candidates composite-score Top-N over the static and
+ *                           dynamic hits with the anchor override
+ *                           (Sec. 3.2 Eq. 8; Alg. 2)
  *
  * Conventions shared by every entry point
  *   - Pointers named keys, spans, span_len, queries, logits, drafts,
@@ -103,9 +110,9 @@ typedef struct {
 /* Build an index over the datastore.  For COSINE it computes the fp32 side
  * table 1/||k_i|| (0 for a zero row) with one read of the keys, enqueued on
  * `stream`.  The index owns only that table (N * 4 bytes) and, with
- * SENSE_INDEX_COPY_KEYS, the key copy.  *out receives the handle; it is
- * immutable afterwards, so concurrent sense_retrieve calls on different
- * streams with separate workspaces are safe.
+ * SENSE_INDEX_COPY_KEYS, the key copy.  *out receives the handle; a static
+ * index is immutable afterwards, so concurrent sense_retrieve calls on
+ * different streams with separate workspaces are safe.
  * Errors: INVALID_ARGUMENT (NULL desc/out/keys/spans, sizes out of range,
  * non-key dtype), MISALIGNED, OUT_OF_MEMORY, HIP. */
 sense_status_t sense_build_index(const sense_index_desc_t *desc, void *stream,
@@ -115,12 +122,60 @@ sense_status_t sense_build_index(const sense_index_desc_t *desc, void *stream,
  * first, so in-flight work that reads it completes).  NULL is a no-op. */
 sense_status_t sense_destroy_index(sense_index_t *index);
 
-/* Shape queries of an index (host values; any out pointer may be NULL). */
+/* Shape queries of an index (host values; any out pointer may be NULL).  For
+ * a dynamic cache n is the number of rows appended so far. */
 sense_status_t sense_index_info(const sense_index_t *index, int64_t *n, int32_t *d,
                                 int32_t *max_span, sense_metric_t *metric,
                                 sense_dtype_t *key_dtype);
 
-/* Bytes of device workspace sense_retrieve needs for these sizes. */
+/* Dynamic context cache (Sec. 3.2 Eq. 6: C_db = C_s u C_d; Alg. 1's
+ * retriever update; Alg. 2's dynamic search).  For every generated position
+ * p the cache holds the key that predicted token p and the token itself; the
+ * continuation of row p is the generated text from p on, tokens[p .. p+M),
+ * cut at the end of what has been appended (length min(M, n - p)).
+ * sense_retrieve searches it exactly like a static index over its current n
+ * rows.  The library owns all of its device memory:
+ * capacity*d*2 bytes of keys, capacity*12 bytes of tokens, lengths and (for
+ * COSINE) inverse norms.
+ *   key_dtype  F16 or BF16 (appended keys are rounded to it, nearest-even).
+ *   d          1 <= d <= 8192, d % 8 == 0.
+ *   capacity   rows the cache can hold, 1 <= capacity <= 2^31 - 1.
+ *   max_span   M, 1 <= M <= 64.
+ *   metric     similarity used by sense_retrieve. */
+typedef struct {
+    sense_dtype_t key_dtype;
+    int32_t d;
+    int64_t capacity;
+    int32_t max_span;
+    sense_metric_t metric;
+} sense_dynamic_index_desc_t;
+
+/* Create an empty dynamic cache (n = 0); free it with sense_destroy_index.
+ * Allocates synchronously and enqueues nothing.  Errors: INVALID_ARGUMENT,
+ * OUT_OF_MEMORY. */
+sense_status_t sense_build_dynamic_index(const sense_dynamic_index_desc_t *desc,
+                                         sense_index_t **out);
+
+/* Append `count` generated positions to a dynamic cache (Alg. 1's retriever
+ * update R.Update(h, y)).
+ *   keys       count x d elements of keys_dtype (F32, F16 or BF16),
+ *              row-major and contiguous, element-aligned: row j is the
+ *              hidden-state key that predicted tokens[j].
+ *   tokens     count int32 token ids.
+ *   count      >= 0 (0 is a no-op); n + count <= capacity.
+ * The row count n grows when the call returns; the copy is enqueued on
+ * `stream`.  A dynamic cache is the one mutable index: enqueue its appends
+ * and the retrievals that read it on one stream (or order them with
+ * events), because an append rewrites the continuation lengths of the last
+ * M - 1 rows.  Errors: INVALID_ARGUMENT (not a dynamic cache, NULL pointers,
+ * count < 0, capacity exceeded, unknown dtype), MISALIGNED, HIP. */
+sense_status_t sense_index_append(sense_index_t *index, const void *keys,
+                                  sense_dtype_t keys_dtype, const int32_t *tokens,
+                                  int32_t count, void *stream);
+
+/* Bytes of device workspace sense_retrieve needs for these sizes (for a
+ * dynamic cache: at its capacity, so the size does not change as rows are
+ * appended). */
 sense_status_t sense_retrieve_workspace_size(const sense_index_t *index, int32_t n_queries,
                                              int32_t k, size_t *bytes);
 
@@ -133,7 +188,9 @@ sense_status_t sense_retrieve_workspace_size(const sense_index_t *index, int32_t
  * and their continuations.
  *   queries      n_queries x d, dtype q_dtype (F32, or the key dtype),
  *                row-major, 16-byte aligned.
- *   n_queries    >= 1.   k: 1 <= k <= min(n, 1024).
+ *   n_queries    >= 1.   k: 1 <= k <= min(n, 1024) (an empty dynamic cache
+ *                cannot be searched: skip it and pass n_dynamic = 0 to
+ *                sense_select_candidates).
  *   out_ids      n_queries x k int64 row ids (required).
  *   out_scores   n_queries x k fp32 scores, or NULL.
  *   out_drafts   n_queries x k x max_span int32: spans[id][j] for
@@ -215,12 +272,67 @@ sense_status_t sense_soft_gate_verify(const void *logits, sense_dtype_t logits_d
                                       int32_t *out_rank, void *workspace,
                                       size_t workspace_bytes, void *stream);
 
+/* Candidate-selection hyper-parameters (Sec. 3.2 Eq. 8; Alg. 2).  The
+ * paper requires alpha >> beta and gives no values.
+ *   alpha           weight of the first-token match I(D[i][0] == anchor)
+ *   beta            weight of the similarity
+ *   delta           boost added to every dynamic-cache similarity
+ *   anchor_override 1: write the anchor into the first token of the first
+ *                   and last selected drafts (Alg. 2); 0: leave them. */
+typedef struct {
+    float alpha;
+    float beta;
+    float delta;
+    int32_t anchor_override;
+} sense_select_params_t;
+
+/* Candidate selection (Sec. 3.2 Eq. 8; Alg. 2's hybrid pool, composite
+ * score, Top-N and anchor override) for n_queries queries at once.  Per query
+ * q the pool D_all is its n_static static hits followed by its n_dynamic
+ * dynamic-cache hits (the outputs of sense_retrieve on the two indexes), and
+ * member i gets
+ *   s_i = static score, or dynamic score + delta      (binary32 addition)
+ *   S_i = fma(beta, s_i, I_i ? alpha : 0)              (binary32, one rounding)
+ * with I_i = 1 when the draft's length is > 0 and its first token equals
+ * anchors[q].  The top_n members by (S desc, position in D_all asc; NaN
+ * scores last) are copied out; then, if anchor_override, the first token of
+ * selected drafts 0 and top_n - 1 becomes anchors[q] (length at least 1).
+ *   static_scores   n_queries x n_static fp32; static_drafts
+ *                   n_queries x n_static x max_len int32; static_len
+ *                   n_queries x n_static int32 or NULL (= max_len).
+ *   dynamic_*       the same with n_dynamic (pointers may be NULL when
+ *                   n_dynamic == 0).
+ *   anchors         n_queries int32: the greedy token x~ of each query.
+ *   n_static, n_dynamic >= 0 with 1 <= n_static + n_dynamic <= 2048;
+ *   1 <= top_n <= n_static + n_dynamic; 1 <= max_len <= 64; n_queries >= 1.
+ *   out_drafts      n_queries x top_n x max_len int32: the selected rows,
+ *                   -1 past each length (required).
+ *   out_len         n_queries x top_n int32 lengths clamped to [0, max_len]
+ *                   (required).
+ *   out_source      n_queries x top_n int32 position in D_all (< n_static:
+ *                   static hit; else dynamic hit n_static + j), or NULL.
+ *   out_score       n_queries x top_n fp32 composite scores S, or NULL.
+ * Inputs are read, not modified.  Needs no workspace.  Errors:
+ * INVALID_ARGUMENT (NULL required pointers, sizes out of range, NaN
+ * parameters), UNSUPPORTED (pool above 2048), HIP. */
+sense_status_t sense_select_candidates(const float *static_scores, const int32_t *static_drafts,
+                                       const int32_t *static_len, int32_t n_static,
+                                       const float *dynamic_scores,
+                                       const int32_t *dynamic_drafts,
+                                       const int32_t *dynamic_len, int32_t n_dynamic,
+                                       const int32_t *anchors, int32_t n_queries,
+                                       int32_t max_len, int32_t top_n,
+                                       const sense_select_params_t *params,
+                                       int32_t *out_drafts, int32_t *out_len,
+                                       int32_t *out_source, float *out_score, void *stream);
+
 /* Diagnostics for benchmarks and profilers.  Which part of the path a pair
  * of timing events brackets. */
 typedef enum {
     SENSE_TIMER_SCAN = 0,   /* similarity scan kernel(s) of sense_retrieve */
     SENSE_TIMER_TOPK = 1,   /* top-k selection + gather kernels of sense_retrieve */
-    SENSE_TIMER_VERIFY = 2  /* both kernels of sense_soft_gate_verify */
+    SENSE_TIMER_VERIFY = 2, /* both kernels of sense_soft_gate_verify */
+    SENSE_TIMER_SELECT = 3  /* the kernel of sense_select_candidates */
 } sense_timer_t;
 
 /* Register two hipEvent_t handles (created by the caller with timing

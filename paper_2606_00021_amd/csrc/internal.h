@@ -20,6 +20,7 @@ constexpr int kMaxDim = 8192;       // 16 chunks of 512 elements per lane
 constexpr int kMaxK = 1024;         // largest retrieval top-k
 constexpr int kMaxLen = 64;         // longest draft
 constexpr int kSelectChunk = 8192;  // elements per top-k selection block
+constexpr int kMaxPool = 2048;      // largest static + dynamic candidate pool
 
 // Order-preserving map of an fp32 score to an unsigned key: larger score ->
 // larger key; every NaN -> 0 (below everything); -0 is folded onto +0.
@@ -43,6 +44,27 @@ __host__ __device__ inline uint64_t pack_key(float s, uint32_t row) {
 }
 __host__ __device__ inline uint32_t key_row(uint64_t k) {
     return 0xFFFFFFFFu - (uint32_t)(k & 0xFFFFFFFFu);
+}
+
+// Bitonic sort of s[0..p) (LDS) into descending order by the kT threads of
+// the block; p a power of two.  Every thread of the block must call it.
+template <int kT>
+__device__ inline void bitonic_desc(uint64_t* s, int p) {
+    for (int size = 2; size <= p; size <<= 1) {
+        for (int stride = size >> 1; stride > 0; stride >>= 1) {
+            for (int i = threadIdx.x; i < (p >> 1); i += kT) {
+                const int pos = 2 * i - (i & (stride - 1));
+                const int partner = pos + stride;
+                const bool desc = (pos & size) == 0;
+                const uint64_t a = s[pos], b = s[partner];
+                if ((a < b) == desc) {
+                    s[pos] = b;
+                    s[partner] = a;
+                }
+            }
+            __syncthreads();
+        }
+    }
 }
 
 // ----------------------------------------------------------------- launchers
@@ -80,10 +102,12 @@ hipError_t launch_query_to_f32(const void* q, int q_dtype, int nq, int d, float*
 size_t topk_workspace_bytes(int64_t n, int nq, int k);
 
 // Per-query top-k of scores (nq x n) in the order (score desc, row asc),
-// plus the gather of each hit's continuation.
+// plus the gather of each hit's continuation: row i's tokens start at
+// spans[i * span_stride] (span_stride = max_span for a table of rows, 1 for
+// a token history whose continuations overlap).
 hipError_t launch_topk_gather(const float* scores, int64_t n, int nq, int k,
                               const int32_t* spans, const int32_t* span_len, int max_span,
-                              int64_t* out_ids, float* out_scores, int32_t* out_drafts,
+                              int64_t span_stride, int64_t* out_ids, float* out_scores, int32_t* out_drafts,
                               int32_t* out_draft_len, void* workspace, hipStream_t stream);
 
 // Verification workspace in bytes.
@@ -103,5 +127,29 @@ hipError_t launch_verify(const void* logits, int logits_dtype, int64_t row_strid
                          int32_t* out_accept_len, int32_t* out_best, float* out_gate_score,
                          uint8_t* out_masks, int32_t* out_rank, void* workspace,
                          hipStream_t stream);
+
+// Composite-score selection (one block per query); pool n_s + n_d <= kMaxPool.
+struct SelectParams {
+    float alpha;
+    float beta;
+    float delta;
+    int anchor_override;
+};
+
+hipError_t launch_select_candidates(const float* scores_s, const int32_t* drafts_s,
+                                    const int32_t* len_s, int n_s, const float* scores_d,
+                                    const int32_t* drafts_d, const int32_t* len_d, int n_d,
+                                    const int32_t* anchors, int n_queries, int max_len,
+                                    int top_n, const SelectParams& sp, int32_t* out_drafts,
+                                    int32_t* out_len, int32_t* out_source, float* out_score,
+                                    hipStream_t stream);
+
+// Appends `count` rows to a dynamic cache of n_old rows: keys (count x d of
+// src_dtype, converted to key_dtype) into keys (row stride d), tokens into
+// the history, and the continuation lengths min(max_span, n - p).
+hipError_t launch_append_rows(const void* src, int src_dtype, int key_dtype,
+                              const int32_t* tokens, int d, int64_t n_old, int count,
+                              int max_span, void* keys, int32_t* hist, int32_t* span_len,
+                              hipStream_t stream);
 
 }  // namespace sense

@@ -24,8 +24,14 @@ struct sense_index {
     const int32_t* spans;
     int32_t max_span;
     const int32_t* span_len;
+    int64_t span_stride;    // elements between consecutive rows of `spans`
     int metric;
     float* inv_norm;        // owned; NULL for the inner-product metric
+    // Dynamic context cache only: capacity > 0, owned token history (the
+    // span table, row stride 1) and continuation lengths.
+    int64_t capacity;
+    int32_t* owned_hist;
+    int32_t* owned_span_len;
 };
 
 namespace {
@@ -33,7 +39,8 @@ namespace {
 thread_local char g_msg[512];
 
 // Timing events per sense_timer_t, set by sense_set_timer_events.
-thread_local hipEvent_t g_timer[3][2] = {{nullptr, nullptr}, {nullptr, nullptr}, {nullptr, nullptr}};
+constexpr int kTimers = 4;
+thread_local hipEvent_t g_timer[kTimers][2] = {};
 
 hipError_t timer_mark(int which, int edge, hipStream_t st) {
     hipEvent_t ev = g_timer[which][edge];
@@ -77,8 +84,11 @@ RetrieveLayout retrieve_layout(const sense_index* ix, int nq, int k) {
     l.m_off = round_up((size_t)nq * ix->d * sizeof(float), 256);
     const size_t mfma = nq >= sense::kMfmaMinQueries ? sense::scan_mfma_scratch_bytes(nq, ix->d) : 0;
     l.s_off = l.m_off + round_up(mfma, 256);
-    l.t_off = l.s_off + round_up((size_t)nq * (size_t)ix->n * sizeof(float), 256);
-    l.total = l.t_off + sense::topk_workspace_bytes(ix->n, nq, k);
+    // A dynamic cache is sized for its capacity, so one workspace serves
+    // every later row count.
+    const int64_t rows = ix->capacity > 0 ? ix->capacity : ix->n;
+    l.t_off = l.s_off + round_up((size_t)nq * (size_t)rows * sizeof(float), 256);
+    l.total = l.t_off + sense::topk_workspace_bytes(rows, nq, k);
     return l;
 }
 
@@ -101,7 +111,7 @@ SENSE_EXPORT const char* sense_last_error_message(void) { return g_msg; }
 
 SENSE_EXPORT sense_status_t sense_set_timer_events(sense_timer_t which, void* start_event,
                                                    void* stop_event) {
-    if ((int)which < 0 || (int)which > 2)
+    if ((int)which < 0 || (int)which >= kTimers)
         return fail(SENSE_ERR_INVALID_ARGUMENT, "unknown timer %d", (int)which);
     if ((start_event == nullptr) != (stop_event == nullptr))
         return fail(SENSE_ERR_INVALID_ARGUMENT, "give both events or neither");
@@ -146,6 +156,7 @@ SENSE_EXPORT sense_status_t sense_build_index(const sense_index_desc_t* desc, vo
     ix->spans = D.spans;
     ix->max_span = D.max_span;
     ix->span_len = D.span_len;
+    ix->span_stride = D.max_span;
     ix->metric = D.metric;
     hipStream_t st = (hipStream_t)stream;
     hipError_t e;
@@ -187,11 +198,93 @@ SENSE_EXPORT sense_status_t sense_build_index(const sense_index_desc_t* desc, vo
     return ok();
 }
 
+SENSE_EXPORT sense_status_t sense_build_dynamic_index(const sense_dynamic_index_desc_t* desc,
+                                                      sense_index_t** out) {
+    if (!desc || !out) return fail(SENSE_ERR_INVALID_ARGUMENT, "desc and out must be non-NULL");
+    *out = nullptr;
+    const sense_dynamic_index_desc_t& D = *desc;
+    if (D.key_dtype != SENSE_F16 && D.key_dtype != SENSE_BF16)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "key_dtype must be SENSE_F16 or SENSE_BF16");
+    if (D.capacity < 1 || D.capacity > 0x7FFFFFFFLL)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "capacity = %lld outside [1, 2^31-1]",
+                    (long long)D.capacity);
+    if (D.d < 1 || D.d > sense::kMaxDim || D.d % 8 != 0)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "d = %d must be a multiple of 8 in [8, %d]", D.d,
+                    sense::kMaxDim);
+    if (D.max_span < 1 || D.max_span > sense::kMaxLen)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "max_span = %d outside [1, %d]", D.max_span,
+                    sense::kMaxLen);
+    if (D.metric != SENSE_METRIC_IP && D.metric != SENSE_METRIC_COSINE)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "unknown metric %d", (int)D.metric);
+    sense_index* ix = new (std::nothrow) sense_index();
+    if (!ix) return fail(SENSE_ERR_OUT_OF_MEMORY, "host allocation failed");
+    ix->key_dtype = D.key_dtype;
+    ix->n = 0;
+    ix->d = D.d;
+    ix->ld = D.d;
+    ix->max_span = D.max_span;
+    ix->span_stride = 1;
+    ix->metric = D.metric;
+    ix->capacity = D.capacity;
+    const size_t rows = (size_t)D.capacity;
+    hipError_t e = hipMalloc(&ix->owned_keys, rows * D.d * 2);
+    if (e == hipSuccess) e = hipMalloc((void**)&ix->owned_hist, rows * sizeof(int32_t));
+    if (e == hipSuccess) e = hipMalloc((void**)&ix->owned_span_len, rows * sizeof(int32_t));
+    if (e == hipSuccess && D.metric == SENSE_METRIC_COSINE)
+        e = hipMalloc((void**)&ix->inv_norm, rows * sizeof(float));
+    if (e != hipSuccess) {
+        if (ix->owned_keys) (void)hipFree(ix->owned_keys);
+        if (ix->owned_hist) (void)hipFree(ix->owned_hist);
+        if (ix->owned_span_len) (void)hipFree(ix->owned_span_len);
+        if (ix->inv_norm) (void)hipFree(ix->inv_norm);
+        delete ix;
+        return fail(SENSE_ERR_OUT_OF_MEMORY, "dynamic cache of %lld rows: %s",
+                    (long long)D.capacity, hipGetErrorString(e));
+    }
+    ix->keys = ix->owned_keys;
+    ix->spans = ix->owned_hist;
+    ix->span_len = ix->owned_span_len;
+    *out = ix;
+    return ok();
+}
+
+SENSE_EXPORT sense_status_t sense_index_append(sense_index_t* ix, const void* keys,
+                                               sense_dtype_t keys_dtype, const int32_t* tokens,
+                                               int32_t count, void* stream) {
+    if (!ix) return fail(SENSE_ERR_INVALID_ARGUMENT, "index is NULL");
+    if (ix->capacity == 0)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "index is not a dynamic cache");
+    if (count < 0) return fail(SENSE_ERR_INVALID_ARGUMENT, "count = %d < 0", count);
+    if (!dtype_ok(keys_dtype))
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "unknown keys dtype %d", (int)keys_dtype);
+    if (ix->n + count > ix->capacity)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "append of %d rows to %lld exceeds capacity %lld",
+                    count, (long long)ix->n, (long long)ix->capacity);
+    if (count == 0) return ok();
+    if (!keys || !tokens) return fail(SENSE_ERR_INVALID_ARGUMENT, "keys and tokens must be non-NULL");
+    if (!aligned(keys, (size_t)elem_size(keys_dtype)) || !aligned(tokens, 4))
+        return fail(SENSE_ERR_MISALIGNED, "keys or tokens not aligned to their element size");
+    hipStream_t st = (hipStream_t)stream;
+    hipError_t e = sense::launch_append_rows(keys, keys_dtype, ix->key_dtype, tokens, ix->d, ix->n,
+                                             count, ix->max_span, ix->owned_keys, ix->owned_hist,
+                                             ix->owned_span_len, st);
+    if (e != hipSuccess) return hip_fail(e, "append");
+    if (ix->inv_norm) {
+        e = sense::launch_key_norms((const char*)ix->owned_keys + (size_t)ix->n * ix->d * 2,
+                                    ix->key_dtype, count, ix->d, ix->d, ix->inv_norm + ix->n, st);
+        if (e != hipSuccess) return hip_fail(e, "append norms");
+    }
+    ix->n += count;
+    return ok();
+}
+
 SENSE_EXPORT sense_status_t sense_destroy_index(sense_index_t* ix) {
     if (!ix) return ok();
     hipError_t e = hipDeviceSynchronize();
     if (ix->inv_norm) (void)hipFree(ix->inv_norm);
     if (ix->owned_keys) (void)hipFree(ix->owned_keys);
+    if (ix->owned_hist) (void)hipFree(ix->owned_hist);
+    if (ix->owned_span_len) (void)hipFree(ix->owned_span_len);
     delete ix;
     if (e != hipSuccess) return hip_fail(e, "destroy");
     return ok();
@@ -267,7 +360,7 @@ SENSE_EXPORT sense_status_t sense_retrieve(const sense_index_t* ix, const void* 
     if ((e = timer_mark(SENSE_TIMER_SCAN, 1, st)) != hipSuccess) return hip_fail(e, "timer");
     if ((e = timer_mark(SENSE_TIMER_TOPK, 0, st)) != hipSuccess) return hip_fail(e, "timer");
     if ((e = sense::launch_topk_gather(scores, ix->n, nq, k, ix->spans, ix->span_len,
-                                       ix->max_span, out_ids, out_scores, out_drafts,
+                                       ix->max_span, ix->span_stride, out_ids, out_scores, out_drafts,
                                        out_draft_len, ws + L.t_off, st)) != hipSuccess)
         return hip_fail(e, "top-k");
     if ((e = timer_mark(SENSE_TIMER_TOPK, 1, st)) != hipSuccess) return hip_fail(e, "timer");
@@ -356,5 +449,50 @@ SENSE_EXPORT sense_status_t sense_read_bandwidth_probe(const void* buf, size_t b
         return fail(SENSE_ERR_MISALIGNED, "buf must be 16-byte aligned and bytes a multiple of 16");
     const hipError_t e = sense::launch_stream_read(buf, bytes, sink, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "read probe");
+    return ok();
+}
+
+SENSE_EXPORT sense_status_t sense_select_candidates(
+    const float* static_scores, const int32_t* static_drafts, const int32_t* static_len,
+    int32_t n_static, const float* dynamic_scores, const int32_t* dynamic_drafts,
+    const int32_t* dynamic_len, int32_t n_dynamic, const int32_t* anchors, int32_t n_queries,
+    int32_t max_len, int32_t top_n, const sense_select_params_t* params, int32_t* out_drafts,
+    int32_t* out_len, int32_t* out_source, float* out_score, void* stream) {
+    if (!params) return fail(SENSE_ERR_INVALID_ARGUMENT, "params is NULL");
+    if (n_static < 0 || n_dynamic < 0)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "n_static = %d and n_dynamic = %d must be >= 0",
+                    n_static, n_dynamic);
+    const int64_t pool = (int64_t)n_static + n_dynamic;
+    if (pool < 1) return fail(SENSE_ERR_INVALID_ARGUMENT, "empty candidate pool");
+    if (pool > sense::kMaxPool)
+        return fail(SENSE_ERR_UNSUPPORTED, "pool of %lld candidates > %d", (long long)pool,
+                    sense::kMaxPool);
+    if (top_n < 1 || top_n > pool)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "top_n = %d outside [1, %lld]", top_n,
+                    (long long)pool);
+    if (max_len < 1 || max_len > sense::kMaxLen)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "max_len = %d outside [1, %d]", max_len,
+                    sense::kMaxLen);
+    if (n_queries < 1) return fail(SENSE_ERR_INVALID_ARGUMENT, "n_queries = %d < 1", n_queries);
+    if (n_static > 0 && (!static_scores || !static_drafts))
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "static_scores and static_drafts must be non-NULL");
+    if (n_dynamic > 0 && (!dynamic_scores || !dynamic_drafts))
+        return fail(SENSE_ERR_INVALID_ARGUMENT,
+                    "dynamic_scores and dynamic_drafts must be non-NULL");
+    if (!anchors || !out_drafts || !out_len)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "anchors, out_drafts and out_len must be non-NULL");
+    const sense_select_params_t& P = *params;
+    if (P.alpha != P.alpha || P.beta != P.beta || P.delta != P.delta)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "alpha, beta and delta must not be NaN");
+    const sense::SelectParams sp{P.alpha, P.beta, P.delta, P.anchor_override != 0};
+    hipStream_t st = (hipStream_t)stream;
+    hipError_t e;
+    if ((e = timer_mark(SENSE_TIMER_SELECT, 0, st)) != hipSuccess) return hip_fail(e, "timer");
+    e = sense::launch_select_candidates(static_scores, static_drafts, static_len, n_static,
+                                        dynamic_scores, dynamic_drafts, dynamic_len, n_dynamic,
+                                        anchors, n_queries, max_len, top_n, sp, out_drafts,
+                                        out_len, out_source, out_score, st);
+    if (e != hipSuccess) return hip_fail(e, "candidate selection");
+    if ((e = timer_mark(SENSE_TIMER_SELECT, 1, st)) != hipSuccess) return hip_fail(e, "timer");
     return ok();
 }

@@ -118,25 +118,6 @@ __device__ SelectState radix_select(const uint64_t (&key)[kPer], int need, uint3
     return SelectState{prefix, mask};
 }
 
-// Bitonic sort of s[0..p) into descending order; p a power of two.
-__device__ void bitonic_desc(uint64_t* s, int p) {
-    for (int size = 2; size <= p; size <<= 1) {
-        for (int stride = size >> 1; stride > 0; stride >>= 1) {
-            for (int i = threadIdx.x; i < (p >> 1); i += kThreads) {
-                const int pos = 2 * i - (i & (stride - 1));
-                const int partner = pos + stride;
-                const bool desc = (pos & size) == 0;
-                const uint64_t a = s[pos], b = s[partner];
-                if ((a < b) == desc) {
-                    s[pos] = b;
-                    s[partner] = a;
-                }
-            }
-            __syncthreads();
-        }
-    }
-}
-
 // One block per (chunk, query).  FROM_SCORES: input is the fp32 score matrix
 // (nq x count, row index = position); otherwise packed keys (nq x count).
 // FINAL: exactly one chunk per query; writes sorted ids/scores and drafts.
@@ -146,7 +127,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
     int k, uint64_t* __restrict__ out_keys, int64_t* __restrict__ out_ids,
     float* __restrict__ out_scores, int32_t* __restrict__ out_drafts,
     int32_t* __restrict__ out_draft_len, const int32_t* __restrict__ spans,
-    const int32_t* __restrict__ span_len, int max_span) {
+    const int32_t* __restrict__ span_len, int max_span, int64_t span_stride) {
     __shared__ uint64_t s_sel[kMaxK];
     __shared__ uint32_t s_hist[kWaves * 256];
     __shared__ uint32_t s_tot[256];
@@ -214,7 +195,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
         const int nt = (int)s_cnt < kk ? (int)s_cnt : kk;
         for (int i = nt + tid; i < p; i += kThreads) s_sel[i] = 0;
         __syncthreads();
-        bitonic_desc(s_sel, p);
+        bitonic_desc<kThreads>(s_sel, p);
         for (int r = tid; r < k; r += kThreads) {
             const uint64_t key = s_sel[r];
             out_ids[(int64_t)q * k + r] = (int64_t)key_row(key);
@@ -231,7 +212,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
                 len_r = len_r < 0 ? 0 : (len_r > max_span ? max_span : len_r);
                 const int64_t o = ((int64_t)q * k + r);
                 if (out_drafts)
-                    out_drafts[o * max_span + j] = (j < len_r) ? spans[id * max_span + j] : -1;
+                    out_drafts[o * max_span + j] = (j < len_r) ? spans[id * span_stride + j] : -1;
                 if (out_draft_len && j == 0) out_draft_len[o] = len_r;
             }
         }
@@ -252,21 +233,21 @@ size_t topk_workspace_bytes(int64_t n, int nq, int k) {
 
 hipError_t launch_topk_gather(const float* scores, int64_t n, int nq, int k,
                               const int32_t* spans, const int32_t* span_len, int max_span,
-                              int64_t* out_ids, float* out_scores, int32_t* out_drafts,
+                              int64_t span_stride, int64_t* out_ids, float* out_scores, int32_t* out_drafts,
                               int32_t* out_draft_len, void* workspace, hipStream_t stream) {
     const int64_t kk = k < kSelectChunk ? k : kSelectChunk;
     int64_t chunks = ceil_div(n, kSelectChunk);
     if (chunks <= 1) {
         hipLaunchKernelGGL((select_kernel<true, true>), dim3(1, nq), dim3(kThreads), 0, stream,
                            scores, nullptr, n, k, nullptr, out_ids, out_scores, out_drafts,
-                           out_draft_len, spans, span_len, max_span);
+                           out_draft_len, spans, span_len, max_span, span_stride);
         return hipGetLastError();
     }
     const size_t one = topk_workspace_bytes(n, nq, k) / 2;
     uint64_t* buf[2] = {(uint64_t*)workspace, (uint64_t*)((char*)workspace + one)};
     hipLaunchKernelGGL((select_kernel<true, false>), dim3((unsigned)chunks, nq), dim3(kThreads),
                        0, stream, scores, nullptr, n, k, buf[0], nullptr, nullptr, nullptr,
-                       nullptr, nullptr, nullptr, 0);
+                       nullptr, nullptr, nullptr, 0, 0);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     int64_t count = chunks * kk;
@@ -274,14 +255,14 @@ hipError_t launch_topk_gather(const float* scores, int64_t n, int nq, int k,
     while ((chunks = ceil_div(count, kSelectChunk)) > 1) {
         hipLaunchKernelGGL((select_kernel<false, false>), dim3((unsigned)chunks, nq),
                            dim3(kThreads), 0, stream, nullptr, buf[cur], count, k, buf[cur ^ 1],
-                           nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 0);
+                           nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 0, 0);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         count = chunks * kk;
         cur ^= 1;
     }
     hipLaunchKernelGGL((select_kernel<false, true>), dim3(1, nq), dim3(kThreads), 0, stream,
                        nullptr, buf[cur], count, k, nullptr, out_ids, out_scores, out_drafts,
-                       out_draft_len, spans, span_len, max_span);
+                       out_draft_len, spans, span_len, max_span, span_stride);
     return hipGetLastError();
 }
 

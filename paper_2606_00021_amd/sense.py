@@ -41,12 +41,15 @@ EXPORTED = (
     "sense_retrieve",
     "sense_soft_gate_verify_workspace_size",
     "sense_soft_gate_verify",
+    "sense_build_dynamic_index",
+    "sense_index_append",
+    "sense_select_candidates",
     "sense_set_timer_events",
     "sense_read_bandwidth_probe",
     "sense_status_string",
     "sense_last_error_message",
 )
-SENSE_TIMER_SCAN, SENSE_TIMER_TOPK, SENSE_TIMER_VERIFY = 0, 1, 2
+SENSE_TIMER_SCAN, SENSE_TIMER_TOPK, SENSE_TIMER_VERIFY, SENSE_TIMER_SELECT = 0, 1, 2, 3
 
 
 class SenseError(RuntimeError):
@@ -68,6 +71,25 @@ class IndexDesc(ctypes.Structure):
         ("span_len", ctypes.c_void_p),
         ("metric", ctypes.c_int),
         ("flags", ctypes.c_uint32),
+    ]
+
+
+class DynamicIndexDesc(ctypes.Structure):
+    _fields_ = [
+        ("key_dtype", ctypes.c_int),
+        ("d", ctypes.c_int32),
+        ("capacity", ctypes.c_int64),
+        ("max_span", ctypes.c_int32),
+        ("metric", ctypes.c_int),
+    ]
+
+
+class SelectParams(ctypes.Structure):
+    _fields_ = [
+        ("alpha", ctypes.c_float),
+        ("beta", ctypes.c_float),
+        ("delta", ctypes.c_float),
+        ("anchor_override", ctypes.c_int32),
     ]
 
 
@@ -106,6 +128,10 @@ def load_library() -> ctypes.CDLL:
         "sense_retrieve_workspace_size": [P, I32, I32, PSZ],
         "sense_retrieve": [P, P, ctypes.c_int, I32, I32, P, P, P, P, P, SZ, P],
         "sense_soft_gate_verify_workspace_size": [I32, I32, I32, PSZ],
+        "sense_build_dynamic_index": [ctypes.POINTER(DynamicIndexDesc), PP],
+        "sense_index_append": [P, P, ctypes.c_int, P, I32, P],
+        "sense_select_candidates": [P, P, P, I32, P, P, P, I32, P, I32, I32, I32,
+                                    ctypes.POINTER(SelectParams), P, P, P, P, P],
         "sense_soft_gate_verify": [P, ctypes.c_int, I64, P, P, I32, I32, I32, I32,
                                    ctypes.POINTER(GateParams), P, P, P, P, P, P, SZ, P],
     }
@@ -196,6 +222,118 @@ def sense_build_index(keys: torch.Tensor, spans: torch.Tensor, span_len: torch.T
     _check(lib.sense_build_index(ctypes.byref(desc), _stream_handle(stream), ctypes.byref(handle)),
            "sense_build_index")
     return Index(handle, keys, spans, span_len, keys.shape[0], keys.shape[1], spans.shape[1], metric)
+
+
+class DynamicIndex:
+    """A dynamic context cache (owned device memory; grows by append)."""
+
+    def __init__(self, handle: ctypes.c_void_p, d: int, capacity: int, max_span: int,
+                 metric: str, key_dtype: torch.dtype):
+        self.handle = handle
+        self.d = d
+        self.capacity = capacity
+        self.max_span = max_span
+        self.metric = metric
+        self.key_dtype = key_dtype
+
+    @property
+    def n(self) -> int:
+        n = ctypes.c_int64()
+        _check(load_library().sense_index_info(self.handle, ctypes.byref(n), None, None, None,
+                                               None), "sense_index_info")
+        return n.value
+
+    def close(self) -> None:
+        if self.handle:
+            h, self.handle = self.handle, None
+            _check(load_library().sense_destroy_index(h), "sense_destroy_index")
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def sense_build_dynamic_index(d: int, capacity: int, max_span: int,
+                              key_dtype: torch.dtype = torch.bfloat16,
+                              metric: str = "cosine") -> DynamicIndex:
+    """Create an empty dynamic context cache of ``capacity`` rows."""
+    lib = load_library()
+    if key_dtype not in (torch.float16, torch.bfloat16):
+        raise ValueError("key_dtype must be float16 or bfloat16")
+    desc = DynamicIndexDesc(key_dtype=_TORCH_DTYPE[key_dtype], d=d, capacity=capacity,
+                            max_span=max_span, metric=METRICS[metric])
+    handle = ctypes.c_void_p()
+    _check(lib.sense_build_dynamic_index(ctypes.byref(desc), ctypes.byref(handle)),
+           "sense_build_dynamic_index")
+    return DynamicIndex(handle, d, capacity, max_span, metric, key_dtype)
+
+
+def sense_index_append(index: DynamicIndex, keys: torch.Tensor, tokens: torch.Tensor,
+                       stream=None) -> None:
+    """Append generated positions: ``keys`` (count x d, fp32/fp16/bf16,
+    contiguous; row j predicted tokens[j]) and ``tokens`` (count int32)."""
+    if keys.dim() == 1:
+        keys = keys.unsqueeze(0)
+    if keys.dtype not in _TORCH_DTYPE or not keys.is_contiguous() or keys.shape[1] != index.d:
+        raise ValueError("keys must be a contiguous count x d float32/float16/bfloat16 tensor")
+    if tokens.dtype != torch.int32 or not tokens.is_contiguous() or tokens.numel() != keys.shape[0]:
+        raise ValueError("tokens must be a contiguous int32 tensor with one id per key row")
+    _check(load_library().sense_index_append(index.handle, _dev_ptr(keys, "keys"),
+                                             _TORCH_DTYPE[keys.dtype], _dev_ptr(tokens, "tokens"),
+                                             keys.shape[0], _stream_handle(stream)),
+           "sense_index_append")
+
+
+def sense_select_candidates(static: tuple, dynamic: tuple | None, anchors: torch.Tensor,
+                            top_n: int, alpha: float, beta: float, delta: float = 0.0,
+                            anchor_override: bool = True, out: tuple | None = None,
+                            stream=None):
+    """Composite-score Top-N over each query's static and dynamic hits.
+
+    ``static`` and ``dynamic`` are (scores [Q,n] fp32, drafts [Q,n,M] int32,
+    lengths [Q,n] int32 or None) as sense_retrieve returns them (``dynamic``
+    may be None).  Returns (drafts [Q,top_n,M], lengths [Q,top_n], source
+    [Q,top_n] positions in the pool, composite scores [Q,top_n])."""
+    lib = load_library()
+
+    def parts(t):
+        if t is None:
+            return None, None, None, 0
+        sc, dr, ln = t
+        for x, nm in ((sc, "scores"), (dr, "drafts"), (ln, "lengths")):
+            if x is not None and not x.is_contiguous():
+                raise ValueError(f"{nm} must be contiguous")
+        if sc.dtype != torch.float32 or dr.dtype != torch.int32 or dr.dim() != 3:
+            raise ValueError("scores must be fp32 [Q,n] and drafts int32 [Q,n,M]")
+        if ln is not None and ln.dtype != torch.int32:
+            raise ValueError("lengths must be int32")
+        return sc, dr, ln, sc.shape[-1]
+
+    ss, ds, ls, ns = parts(static)
+    sd, dd, ld, nd = parts(dynamic)
+    ref = ds if ds is not None else dd
+    nq, m = ref.shape[0], ref.shape[2]
+    if anchors.dtype != torch.int32 or anchors.numel() != nq or not anchors.is_contiguous():
+        raise ValueError("anchors must be a contiguous int32 tensor of one id per query")
+    dev = anchors.device
+    if out is None:
+        out = (torch.empty((nq, top_n, m), dtype=torch.int32, device=dev),
+               torch.empty((nq, top_n), dtype=torch.int32, device=dev),
+               torch.empty((nq, top_n), dtype=torch.int32, device=dev),
+               torch.empty((nq, top_n), dtype=torch.float32, device=dev))
+    odr, oln, osrc, osc = out
+    params = SelectParams(alpha=alpha, beta=beta, delta=delta,
+                          anchor_override=int(bool(anchor_override)))
+    _check(lib.sense_select_candidates(
+        _dev_ptr(ss, "static_scores"), _dev_ptr(ds, "static_drafts"), _dev_ptr(ls, "static_len"),
+        ns, _dev_ptr(sd, "dynamic_scores"), _dev_ptr(dd, "dynamic_drafts"),
+        _dev_ptr(ld, "dynamic_len"), nd, _dev_ptr(anchors, "anchors"), nq, m, top_n,
+        ctypes.byref(params), _dev_ptr(odr, "out_drafts"), _dev_ptr(oln, "out_len"),
+        _dev_ptr(osrc, "out_source"), _dev_ptr(osc, "out_score"), _stream_handle(stream)),
+        "sense_select_candidates")
+    return out
 
 
 def sense_retrieve_workspace_size(index: Index, n_queries: int, k: int) -> int:

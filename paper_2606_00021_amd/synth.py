@@ -166,3 +166,72 @@ def make_logits(w: Workload, drafts: torch.Tensor, seed: int, dtype: str | None 
         out[c0:c1] = x.to(dt)
         del x
     return out
+
+
+@dataclass
+class Context:
+    keys: torch.Tensor      # length x d fp32 hidden states of generated positions
+    tokens: torch.Tensor    # length int32: the token each state predicted
+    near: torch.Tensor      # positions planted near the query's source row
+
+
+def make_context(w: Workload, ds: Datastore, seed: int, length: int, source_row: int,
+                 anchor: int, n_near: int = 8, p_anchor: float = 0.1) -> Context:
+    """Generation context for a dynamic cache: `length` fp32 states, each a
+    stored row chosen uniformly plus N(0, 0.1^2) noise, except n_near
+    positions that revisit the query's source row (+ N(0, 0.05^2)), as when
+    the generation repeats itself.  Tokens are uniform ids with a fraction
+    p_anchor set to `anchor` (so first-token matches occur)."""
+    device = ds.keys.device
+    g = _gen(seed + 15485863, device)
+    rows = torch.randint(0, w.n, (length,), generator=g, device=device)
+    x = ds.keys[rows].float()
+    x.add_(torch.randn(x.shape, generator=g, device=device), alpha=0.1)
+    near = torch.randperm(length, generator=g, device=device)[:min(n_near, length)]
+    src = ds.keys[source_row].float()
+    x[near] = src + 0.05 * torch.randn((near.numel(), w.d), generator=g, device=device)
+    tokens = torch.randint(0, w.vocab, (length,), generator=g, device=device, dtype=torch.int32)
+    hit = torch.rand(length, generator=g, device=device) < p_anchor
+    tokens[hit] = int(anchor)
+    return Context(x.contiguous(), tokens, near)
+
+
+@dataclass
+class Pool:
+    scores: torch.Tensor    # Q x n fp32 similarities
+    drafts: torch.Tensor    # Q x n x M int32
+    lengths: torch.Tensor   # Q x n int32 (may lie outside [0, M])
+
+
+def make_pool(seed: int, n_queries: int, n: int, max_len: int, vocab: int,
+              anchors: torch.Tensor, device, p_anchor: float = 0.3, ragged: bool = True,
+              ties: bool = True, specials: bool = False) -> Pool:
+    """Retrieval-shaped hits for candidate selection: scores ~ U(-1, 1) (a
+    quarter rounded to multiples of 1/64, so exact ties occur), drafts of
+    uniform token ids whose first token is the query's anchor with
+    probability p_anchor, lengths uniform in [-1, M + 1] when ragged (tokens
+    past the length are left as random ids), and, with specials, NaN, +-inf
+    and -0 scores sprinkled in."""
+    g = _gen(seed + 32452843, device)
+    sc = torch.rand((n_queries, n), generator=g, device=device) * 2 - 1
+    if ties:
+        q = torch.rand((n_queries, n), generator=g, device=device) < 0.25
+        sc = torch.where(q, torch.round(sc * 64) / 64, sc)
+    if specials and n > 0:
+        kind = torch.randint(0, 12, (n_queries, n), generator=g, device=device)
+        sc = torch.where(kind == 0, torch.full_like(sc, float("nan")), sc)
+        sc = torch.where(kind == 1, torch.full_like(sc, float("inf")), sc)
+        sc = torch.where(kind == 2, torch.full_like(sc, float("-inf")), sc)
+        sc = torch.where(kind == 3, torch.full_like(sc, -0.0), sc)
+    dr = torch.randint(0, vocab, (n_queries, n, max_len), generator=g, device=device,
+                       dtype=torch.int32)
+    hit = torch.rand((n_queries, n), generator=g, device=device) < p_anchor
+    first = torch.where(hit, anchors.view(-1, 1).to(torch.int32).expand(n_queries, n),
+                        dr[:, :, 0])
+    dr[:, :, 0] = first
+    if ragged:
+        ln = torch.randint(-1, max_len + 2, (n_queries, n), generator=g, device=device,
+                           dtype=torch.int32)
+    else:
+        ln = torch.full((n_queries, n), max_len, dtype=torch.int32, device=device)
+    return Pool(sc.float().contiguous(), dr.contiguous(), ln.contiguous())

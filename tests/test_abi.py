@@ -175,3 +175,80 @@ def test_binding_refuses_host_tensors():
         sense.sense_build_index(keys, spans)
     with pytest.raises(ValueError):
         sense.sense_soft_gate_verify(torch.zeros(2, 3, 10), torch.zeros(2, 3, dtype=torch.int32))
+
+
+def dyn_desc(**kw):
+    base = dict(key_dtype=sense.SENSE_BF16, d=256, capacity=4096, max_span=8, metric=1)
+    base.update(kw)
+    return sense.DynamicIndexDesc(**base)
+
+
+@pytest.mark.parametrize("kw", [
+    dict(key_dtype=sense.SENSE_F32),
+    dict(d=0), dict(d=100), dict(d=8200),
+    dict(capacity=0), dict(capacity=1 << 31),
+    dict(max_span=0), dict(max_span=65),
+    dict(metric=3),
+])
+def test_build_dynamic_index_rejects(lib, kw):
+    out = ctypes.c_void_p(123)
+    d = dyn_desc(**kw)
+    assert lib.sense_build_dynamic_index(ctypes.byref(d), ctypes.byref(out)) == INVALID
+    assert out.value is None
+    assert lib.sense_last_error_message()
+
+
+def test_dynamic_index_null_args(lib):
+    out = ctypes.c_void_p()
+    assert lib.sense_build_dynamic_index(None, ctypes.byref(out)) == INVALID
+    d = dyn_desc()
+    assert lib.sense_build_dynamic_index(ctypes.byref(d), None) == INVALID
+    assert lib.sense_index_append(None, p(FAKE), 0, p(FAKE), 4, None) == INVALID
+
+
+def select_call(lib, **kw):
+    a = dict(ss=p(FAKE), ds=p(FAKE), ls=None, ns=64, sd=p(FAKE), dd=p(FAKE), ld=None, nd=16,
+             anchors=p(FAKE), nq=1, m=8, top_n=32,
+             params=sense.SelectParams(alpha=100.0, beta=1.0, delta=0.1, anchor_override=1),
+             od=p(FAKE), ol=p(FAKE), osrc=None, osc=None)
+    a.update(kw)
+    prm = a["params"]
+    return lib.sense_select_candidates(
+        a["ss"], a["ds"], a["ls"], a["ns"], a["sd"], a["dd"], a["ld"], a["nd"], a["anchors"],
+        a["nq"], a["m"], a["top_n"], None if prm is None else ctypes.byref(prm), a["od"],
+        a["ol"], a["osrc"], a["osc"], None)
+
+
+NAN = float("nan")
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(params=None), INVALID),
+    (dict(ns=-1), INVALID),
+    (dict(nd=-1), INVALID),
+    (dict(ns=0, nd=0, top_n=1), INVALID),
+    (dict(ns=2000, nd=49), UNSUPPORTED),
+    (dict(top_n=0), INVALID),
+    (dict(top_n=81), INVALID),
+    (dict(m=0), INVALID),
+    (dict(m=65), INVALID),
+    (dict(nq=0), INVALID),
+    (dict(ss=None), INVALID),
+    (dict(ds=None), INVALID),
+    (dict(sd=None), INVALID),
+    (dict(dd=None), INVALID),
+    (dict(anchors=None), INVALID),
+    (dict(od=None), INVALID),
+    (dict(ol=None), INVALID),
+    (dict(params=sense.SelectParams(alpha=NAN, beta=1.0, delta=0.0, anchor_override=1)), INVALID),
+    (dict(params=sense.SelectParams(alpha=1.0, beta=NAN, delta=0.0, anchor_override=1)), INVALID),
+    (dict(params=sense.SelectParams(alpha=1.0, beta=1.0, delta=NAN, anchor_override=1)), INVALID),
+])
+def test_select_rejects(lib, kw, status):
+    assert select_call(lib, **kw) == status
+    assert lib.sense_last_error_message()
+
+
+def test_timer_ids(lib):
+    assert lib.sense_set_timer_events(sense.SENSE_TIMER_SELECT, None, None) == 0
+    assert lib.sense_set_timer_events(4, None, None) == INVALID

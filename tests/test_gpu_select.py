@@ -1,0 +1,288 @@
+"""GPU parity of the SEN candidate-selection stage and the dynamic context
+cache (Sec. 3.2 Eqs. 6 and 8; Alg. 1's retriever update; Alg. 2's hybrid
+retrieval, composite score, Top-N and anchor override).
+
+Selection alone is compared element by element with the oracle taking the
+composite score in binary32 (the precision the kernel decides the order in):
+drafts, lengths, sources and scores must be identical.  The dynamic cache is
+compared with the oracle's exact retrieval over the same rounded keys and the
+continuation table of the token history.  The full SEN chain (static and
+dynamic retrieval, selection, soft-gated verification) is compared with the
+oracle's chain in double precision.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_00021_amd import sense, synth
+from parity import REL_TIE, check_topk, check_verify, dt_name, host_bits
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+def run_select(pool_s, pool_d, anchors, top_n, alpha, beta, delta, override, with_len=True):
+    st = (pool_s.scores, pool_s.drafts, pool_s.lengths if with_len else None) if pool_s else None
+    dy = (pool_d.scores, pool_d.drafts, pool_d.lengths if with_len else None) if pool_d else None
+    if st is None:
+        # the binding infers Q and M from the first pool it is given
+        nq, m = pool_d.drafts.shape[0], pool_d.drafts.shape[2]
+        st = (torch.empty((nq, 0), dtype=torch.float32, device=DEV),
+              torch.empty((nq, 0, m), dtype=torch.int32, device=DEV), None)
+    return sense.sense_select_candidates(st, dy, anchors, top_n, alpha, beta, delta, override)
+
+
+def oracle_select_query(pool_s, pool_d, q, anchor, top_n, alpha, beta, delta, override,
+                        with_len=True, precision="f32"):
+    def host(pool):
+        if pool is None or pool.scores.shape[1] == 0:
+            return None, None, None
+        return (pool.scores[q].cpu().numpy().astype(np.float64), pool.drafts[q].cpu().numpy(),
+                pool.lengths[q].cpu().numpy() if with_len else None)
+    ss, ds, ls = host(pool_s)
+    sd, dd, ld = host(pool_d)
+    if ss is None:
+        m = pool_d.drafts.shape[2]
+        ss, ds = np.zeros(0), np.zeros((0, m), dtype=np.int32)
+    return oracle.select_candidates(ss, ds, ls, anchor, top_n, alpha, beta, delta,
+                                    anchor_override=override, scores_d=sd, drafts_d=dd,
+                                    len_d=ld, precision=precision)
+
+
+SELECT_CASES = [
+    # nq, n_s, n_d, M, top_n, alpha, beta, delta, override, ragged, specials
+    (1, 64, 0, 8, 64, 100.0, 1.0, 0.0, True, True, False),
+    (3, 64, 16, 8, 32, 100.0, 1.0, 0.05, True, True, False),
+    (2, 1024, 1024, 12, 100, 1e4, 1.0, 0.1, True, True, True),
+    (4, 5, 3, 1, 8, 0.0, 1.0, 0.0, False, True, False),
+    (1, 1, 0, 64, 1, 100.0, 1.0, 0.0, True, True, False),
+    (2, 0, 40, 8, 10, 100.0, 1.0, 0.2, True, True, False),
+    (5, 300, 77, 10, 3, 2.0, -1.0, -0.3, True, True, True),
+    (2, 128, 64, 8, 128, -5.0, 0.5, 1.0, False, False, True),
+    (16, 64, 16, 8, 64, 1000.0, 1.0, 0.05, True, True, False),
+]
+
+
+@pytest.mark.parametrize("case", SELECT_CASES, ids=[str(i) for i in range(len(SELECT_CASES))])
+@pytest.mark.parametrize("with_len", [True, False])
+def test_select_matches_oracle(case, with_len):
+    nq, ns, nd, m, top_n, alpha, beta, delta, override, ragged, specials = case
+    print(f"[select] case={case} with_len={with_len}", flush=True)
+    vocab = 50
+    anchors = torch.randint(0, vocab, (nq,), dtype=torch.int32,
+                            generator=torch.Generator().manual_seed(nq * 31 + ns)).to(DEV)
+    pool_s = synth.make_pool(1, nq, ns, m, vocab, anchors, DEV, ragged=ragged,
+                             specials=specials) if ns else None
+    pool_d = synth.make_pool(2, nq, nd, m, vocab, anchors, DEV, ragged=ragged,
+                             specials=specials) if nd else None
+    dr, ln, src, sc = run_select(pool_s, pool_d, anchors, top_n, alpha, beta, delta, override,
+                                 with_len)
+    torch.cuda.synchronize()
+    dr, ln, src, sc = dr.cpu().numpy(), ln.cpu().numpy(), src.cpu().numpy(), sc.cpu().numpy()
+    for q in range(nq):
+        o_dr, o_ln, o_src, o_sc = oracle_select_query(pool_s, pool_d, q, int(anchors[q]), top_n,
+                                                      alpha, beta, delta, override, with_len)
+        assert np.array_equal(src[q], o_src), f"query {q}: order differs"
+        assert np.array_equal(dr[q], o_dr), f"query {q}: drafts differ"
+        assert np.array_equal(ln[q], o_ln), f"query {q}: lengths differ"
+        o32 = o_sc.astype(np.float32)
+        same = (sc[q] == o32) | (np.isnan(sc[q]) & np.isnan(o32))
+        assert same.all(), f"query {q}: composite scores differ"
+
+
+def test_select_is_deterministic():
+    anchors = torch.tensor([3, 7], dtype=torch.int32, device=DEV)
+    ps = synth.make_pool(5, 2, 1000, 8, 20, anchors, DEV, specials=True)
+    pd = synth.make_pool(6, 2, 500, 8, 20, anchors, DEV, specials=True)
+    a = [t.clone() for t in run_select(ps, pd, anchors, 300, 100.0, 1.0, 0.1, True)]
+    b = run_select(ps, pd, anchors, 300, 100.0, 1.0, 0.1, True)
+    torch.cuda.synchronize()
+    for x, y in zip(a, b):
+        assert torch.equal(x.view(torch.int32), y.view(torch.int32))
+
+
+def test_select_leaves_inputs_and_padding_alone():
+    anchors = torch.tensor([4], dtype=torch.int32, device=DEV)
+    ps = synth.make_pool(9, 1, 64, 8, 10, anchors, DEV)
+    before = [t.clone() for t in (ps.scores, ps.drafts, ps.lengths)]
+    out = (torch.full((1, 20, 8), -7, dtype=torch.int32, device=DEV),
+           torch.full((1, 20), -7, dtype=torch.int32, device=DEV),
+           torch.full((1, 20), -7, dtype=torch.int32, device=DEV),
+           torch.full((1, 20), -7.0, dtype=torch.float32, device=DEV))
+    big = torch.full((1, 40, 8), -9, dtype=torch.int32, device=DEV)
+    sense.sense_select_candidates((ps.scores, ps.drafts, ps.lengths), None, anchors, 20, 10.0,
+                                  1.0, out=(big[:, :20], out[1], out[2], out[3]))
+    torch.cuda.synchronize()
+    for x, y in zip(before, (ps.scores, ps.drafts, ps.lengths)):
+        assert torch.equal(x, y)
+    assert (big[:, 20:] == -9).all()            # nothing written past the output
+
+
+# ------------------------------------------------------------------ dynamic cache
+
+def to_key_dtype(x: torch.Tensor, dt: torch.dtype) -> torch.Tensor:
+    """Round fp32 rows to the key type on the host (round-to-nearest-even)."""
+    return x.detach().cpu().to(dt)
+
+
+DYN_CASES = [
+    # d, key dtype, source dtype, metric, append counts, k, n_queries
+    (256, torch.bfloat16, torch.float32, "cosine", [1, 7, 300, 0, 1000], 16, 1),
+    (256, torch.float16, torch.float16, "ip", [5, 64, 500], 8, 2),
+    (4096, torch.bfloat16, torch.bfloat16, "cosine", [100, 2000, 37], 16, 1),
+    (4096, torch.bfloat16, torch.float32, "cosine", [600, 1500], 16, 5),
+    (1024, torch.float16, torch.float32, "cosine", [3, 3], 4, 1),
+]
+
+
+@pytest.mark.parametrize("case", DYN_CASES, ids=[str(i) for i in range(len(DYN_CASES))])
+def test_dynamic_cache_retrieval(case):
+    d, kdt, sdt, metric, counts, k, nq = case
+    print(f"[dynamic] case={case}", flush=True)
+    total = sum(counts)
+    m = 8
+    w = synth.scaled(synth.WORKLOADS["tiny-16k-d4096"], n=4096, d=d, n_clusters=64)
+    ds = synth.make_datastore(w, 31, DEV)
+    q, src_rows = synth.make_queries(w, ds, 31, n_queries=nq)
+    ctx = synth.make_context(w, ds, 31, total, int(src_rows[0]), anchor=5)
+    cache = sense.sense_build_dynamic_index(d, total + 17, m, key_dtype=kdt, metric=metric)
+    at = 0
+    for c in counts:
+        sense.sense_index_append(cache, ctx.keys[at:at + c].to(sdt).contiguous(),
+                                 ctx.tokens[at:at + c].contiguous())
+        at += c
+        assert cache.n == at
+        if at < k:
+            continue
+        ids, sc, dr, dl = sense.sense_retrieve(cache, q, k)
+        torch.cuda.synchronize()
+        # the oracle sees the same rounded keys (source types that round
+        # through fp32 to the key type give the same bits)
+        keys_now = to_key_dtype(ctx.keys[:at].to(sdt).float(), kdt)
+        o_s = oracle.scores(host_bits(keys_now), dt_name(keys_now), q.cpu().numpy(), "f32",
+                            metric)
+        spans, lens = oracle.dynamic_spans(ctx.tokens[:at].cpu().numpy(), m)
+        for qq in range(nq):
+            g_ids = ids[qq].cpu().numpy()
+            check_topk(g_ids, sc[qq].cpu().numpy(), o_s[qq], k)
+            o_dr, o_dl = oracle.gather(spans, lens, g_ids)
+            assert np.array_equal(dr[qq].cpu().numpy(), o_dr), "dynamic drafts differ"
+            assert np.array_equal(dl[qq].cpu().numpy(), o_dl), "dynamic lengths differ"
+    cache.close()
+
+
+def test_dynamic_cache_planted_repeat_ranks_first():
+    w = synth.scaled(synth.WORKLOADS["tiny-16k-d4096"], n=2048, d=512, n_clusters=32)
+    ds = synth.make_datastore(w, 3, DEV)
+    q, src_rows = synth.make_queries(w, ds, 3)
+    ctx = synth.make_context(w, ds, 3, 3000, int(src_rows[0]), anchor=1, n_near=4)
+    cache = sense.sense_build_dynamic_index(512, 3000, 8)
+    sense.sense_index_append(cache, ctx.keys, ctx.tokens)
+    ids, _, _, _ = sense.sense_retrieve(cache, q, 4)
+    torch.cuda.synchronize()
+    assert set(ids[0].cpu().tolist()) == set(ctx.near.cpu().tolist())
+
+
+def test_dynamic_cache_limits():
+    cache = sense.sense_build_dynamic_index(64, 10, 4)
+    keys = torch.randn(8, 64, device=DEV)
+    toks = torch.arange(8, dtype=torch.int32, device=DEV)
+    with pytest.raises(sense.SenseError):
+        sense.sense_retrieve(cache, keys[:1], 1)           # empty cache
+    sense.sense_index_append(cache, keys, toks)
+    with pytest.raises(sense.SenseError):
+        sense.sense_index_append(cache, keys[:3], toks[:3])  # beyond capacity
+    assert cache.n == 8
+    sense.sense_index_append(cache, keys[:2], toks[:2])
+    assert cache.n == 10
+    ids, _, dr, dl = sense.sense_retrieve(cache, keys[1:2].contiguous(), 10)
+    torch.cuda.synchronize()
+    # every row is returned (k = n), so each id's continuation is checked
+    spans, lens = oracle.dynamic_spans(np.r_[np.arange(8), np.arange(2)].astype(np.int32), 4)
+    o_dr, o_dl = oracle.gather(spans, lens, ids[0].cpu().numpy())
+    assert sorted(ids[0].cpu().tolist()) == list(range(10))
+    assert np.array_equal(dl[0].cpu().numpy(), o_dl)
+    assert np.array_equal(dr[0].cpu().numpy(), o_dr)
+    cache.close()
+
+
+# ------------------------------------------------------------------ SEN chain
+
+def check_selection(g_src, o_comp, o_sim, beta, top_n):
+    """The GPU's pool positions (ordered) against the oracle's composite
+    scores of the same pool: identical except where two composite scores are
+    within REL_TIE of the similarity term (a near tie)."""
+    o_order = sorted(range(len(o_comp)), key=lambda i: (-o_comp[i], i))[:top_n]
+    tol = lambda a, b: REL_TIE * abs(beta) * max(abs(o_sim[a]), abs(o_sim[b]), 1e-30)
+    assert len(set(g_src.tolist())) == top_n
+    for r in range(top_n):
+        a, b = int(g_src[r]), o_order[r]
+        if a != b:
+            assert abs(o_comp[a] - o_comp[b]) <= tol(a, b), f"rank {r}: {a} vs {b}"
+    return o_order
+
+
+@pytest.mark.parametrize("wname,scale,ctx_len,k_dyn,top_n", [
+    ("tiny-16k-d4096", {}, 512, 8, 8),
+    ("store-1m-d4096", {"n": 40000, "n_clusters": 160}, 4096, 16, 64),
+])
+def test_sen_chain(wname, scale, ctx_len, k_dyn, top_n):
+    """Static retrieval + dynamic retrieval + selection + verification, as a
+    decoding step of the method runs them, against the oracle's chain."""
+    w = synth.scaled(synth.WORKLOADS[wname], **scale)
+    print(f"[sen-chain] {w.name} n={w.n} ctx={ctx_len}", flush=True)
+    alpha, beta, delta = 100.0, 1.0, 0.05
+    ds = synth.make_datastore(w, 12, DEV)
+    q, src_rows = synth.make_queries(w, ds, 12)
+    anchor = int(ds.spans[src_rows[0], 0])
+    ctx = synth.make_context(w, ds, 12, ctx_len, int(src_rows[0]), anchor)
+    index = sense.sense_build_index(ds.keys, ds.spans, ds.span_len)
+    cache = sense.sense_build_dynamic_index(w.d, ctx_len, w.span,
+                                            key_dtype=synth.DTYPES[w.key_dtype])
+    sense.sense_index_append(cache, ctx.keys, ctx.tokens)
+    anchors = torch.tensor([anchor], dtype=torch.int32, device=DEV)
+    hs = sense.sense_retrieve(index, q, w.k)
+    hd = sense.sense_retrieve(cache, q, k_dyn)
+    dr, ln, src, sc = sense.sense_select_candidates((hs[1], hs[2], hs[3]), (hd[1], hd[2], hd[3]),
+                                                    anchors, top_n, alpha, beta, delta)
+    torch.cuda.synchronize()
+
+    # oracle chain, double precision throughout
+    o_ss = oracle.scores(host_bits(ds.keys), w.key_dtype, q.cpu().numpy(), "f32")[0]
+    keys_d = to_key_dtype(ctx.keys, synth.DTYPES[w.key_dtype])
+    o_sd = oracle.scores(host_bits(keys_d), w.key_dtype, q.cpu().numpy(), "f32")[0]
+    assert check_topk(hs[0][0].cpu().numpy(), hs[1][0].cpu().numpy(), o_ss, w.k) == 0
+    assert check_topk(hd[0][0].cpu().numpy(), hd[1][0].cpu().numpy(), o_sd, k_dyn) == 0
+    o_ids_s, o_sc_s = oracle.topk(o_ss, w.k)
+    o_ids_d, o_sc_d = oracle.topk(o_sd, k_dyn)
+    o_dr_s, o_dl_s = oracle.gather(ds.spans.cpu().numpy(), None, o_ids_s)
+    spans_d, lens_d = oracle.dynamic_spans(ctx.tokens.cpu().numpy(), w.span)
+    o_dr_d, o_dl_d = oracle.gather(spans_d, lens_d, o_ids_d)
+    o_dr, o_ln, o_src, o_comp = oracle.select_candidates(
+        o_sc_s, o_dr_s, o_dl_s, anchor, w.k + k_dyn, alpha, beta, delta, anchor_override=False,
+        scores_d=o_sc_d, drafts_d=o_dr_d, len_d=o_dl_d)
+    comp_of = np.empty(w.k + k_dyn)
+    comp_of[o_src] = o_comp
+    sim_of = np.r_[o_sc_s, o_sc_d + delta]
+    check_selection(src[0].cpu().numpy(), comp_of, sim_of, beta, top_n)
+    o_dr, o_ln, o_src, _ = oracle.select_candidates(
+        o_sc_s, o_dr_s, o_dl_s, anchor, top_n, alpha, beta, delta, scores_d=o_sc_d,
+        drafts_d=o_dr_d, len_d=o_dl_d)
+    # these seeded inputs have no near tie among the selected members
+    assert np.array_equal(src[0].cpu().numpy(), o_src)
+    assert np.array_equal(dr[0].cpu().numpy(), o_dr)
+    assert np.array_equal(ln[0].cpu().numpy(), o_ln)
+    assert (dr[0, [0, top_n - 1], 0] == anchor).all()
+
+    # verification of the selected pool, on logits generated from the
+    # oracle's drafts (identical to the GPU's when the orders agree)
+    drafts_host = torch.from_numpy(o_dr)
+    logits = synth.make_logits(w, drafts_host.to(DEV), 12)
+    out = sense.sense_soft_gate_verify(logits, dr[0].contiguous(), ln[0].contiguous())
+    torch.cuda.synchronize()
+    ref = oracle.soft_gate_verify(host_bits(logits), dt_name(logits), o_dr, o_ln)
+    check_verify(out, ref, 0.05, o_ln)
+    index.close()
+    cache.close()
