@@ -6,8 +6,9 @@ library never imports, links or calls it, and it imports nothing from the HIP
 library (the two share no code).
 
 The arithmetic lives in ``sense_oracle.c`` (plain C loops in double precision;
-see its header for the paper passages it follows and the readings taken).
-This module only marshals numpy arrays into that library through ctypes.
+see its header for the paper passages it follows and the readings taken) and,
+for the loose trie of Alg. 3, in ``trie.py`` (plain numpy).  This module
+marshals numpy arrays into the C library through ctypes.
 
 Array conventions: float32 data is passed as ``np.float32`` arrays; binary16
 and bfloat16 data are passed as ``np.uint16`` arrays of raw bit patterns with
