@@ -26,6 +26,14 @@
  *   sense_select_candidates composite-score Top-N over the static and
  *                           dynamic hits with the anchor override
  *                           (Sec. 3.2 Eq. 8; Alg. 2)
+ *   sense_build_loose_trie  LexSort and the loose trie of a draft pool: the
+ *                           flattened tree, the map Gamma, the tree mask and
+ *                           the static-KV mask (Sec. 3.2 Eq. 9; Alg. 2;
+ *                           Alg. 3; App. tree attention mask)
+ *   sense_soft_gate_verify_tree
+ *                           soft-gated evaluation reading the flattened
+ *                           tree's logits through Gamma (Sec. 3.2 Eq. 11;
+ *                           Sec. 3.3; Alg. 4)
  *
  * Conventions shared by every entry point
  *   - Pointers named keys, spans, span_len, queries, logits, drafts,
@@ -326,13 +334,117 @@ sense_status_t sense_select_candidates(const float *static_scores, const int32_t
                                        int32_t *out_drafts, int32_t *out_len,
                                        int32_t *out_source, float *out_score, void *stream);
 
+/* Outputs of sense_build_loose_trie (all DEVICE pointers).  Per group g of
+ * G = n_cand / n_groups drafts, the per-node arrays hold NODES = G * max_len
+ * entries starting at g * NODES; tree nodes are numbered 0 .. L_g - 1 in
+ * the order Alg. 3 extracts them (row-major over the sorted drafts, which
+ * is a preorder of the tree); entries L_g .. NODES - 1 are set to -1.
+ * Required:
+ *   order       n_cand int32: order[g*G + r] = index within group g of its
+ *               r-th draft in LexSort order.
+ *   gamma       n_cand x max_len int32 in sorted order: the tree node of
+ *               every position that exists (j < length), -1 elsewhere.
+ *   tree_tokens, tree_parent, tree_depth, tree_cand
+ *               n_groups x NODES int32: node u's token, its parent node (-1
+ *               at depth 0), its depth (the draft position) and the first
+ *               sorted draft whose path creates it (Gamma's inverse).
+ *   tree_len    n_groups int32: L_g.
+ * Optional (NULL = not written):
+ *   sorted_drafts n_cand x max_len int32 (-1 past each length);
+ *   sorted_len    n_cand int32 (clamped to [0, max_len]);
+ *   mask          n_groups x NODES rows of mask_ld >= NODES uint8: row u,
+ *                 columns v < L_g: 1 when v is on u's path (v = u
+ *                 included), else 0; other entries untouched;
+ *   full_mask     n_groups x NODES rows of cache_len elements of
+ *                 full_mask_dtype (F32, F16 or BF16): row u < L_g is the
+ *                 additive attention mask of tree token u over a static KV
+ *                 cache whose first prefix_len positions hold the context
+ *                 and the next L_g the tree: 0 where visible, -inf
+ *                 elsewhere; rows >= L_g untouched. */
+typedef struct {
+    int32_t *order;
+    int32_t *gamma;
+    int32_t *tree_tokens;
+    int32_t *tree_parent;
+    int32_t *tree_depth;
+    int32_t *tree_cand;
+    int32_t *tree_len;
+    int32_t *sorted_drafts;
+    int32_t *sorted_len;
+    uint8_t *mask;
+    int64_t mask_ld;
+    void *full_mask;
+    sense_dtype_t full_mask_dtype;
+    int32_t prefix_len;
+    int64_t cache_len;
+} sense_trie_t;
+
+/* LexSort + loose trie of each group's drafts (Sec. 3.2 Eq. 9 and the tree
+ * mask after it; Alg. 2's LexSort; Alg. 3; App. tree attention mask for a
+ * static KV cache).
+ *   drafts     n_cand x max_len int32 token ids (any values).
+ *   draft_len  n_cand int32 lengths (clamped to [0, max_len]) or NULL
+ *              (= max_len).  Positions j >= length do not exist: they match
+ *              nothing and are no tree node.
+ *   n_groups   >= 1, divides n_cand; G = n_cand / n_groups <= 1024 and
+ *              G * max_len <= 4096; 1 <= max_len <= 64.
+ * LexSort orders a group's drafts by their token sequences (signed int32
+ * comparison; a proper prefix first; identical drafts by index).  Sorted
+ * draft r's position j is shared when draft r-1 has the same tokens at
+ * positions 0..j; every existing position that is not shared is a new tree
+ * node.  The node count L_g is the number of distinct non-empty prefixes.
+ * Errors: INVALID_ARGUMENT (NULL required pointers, sizes out of range,
+ * mask_ld < NODES, unknown full_mask_dtype, prefix_len < 0, cache_len < 1),
+ * UNSUPPORTED (group larger than 1024 drafts or 4096 tokens), HIP. */
+sense_status_t sense_build_loose_trie(const int32_t *drafts, const int32_t *draft_len,
+                                      int32_t n_cand, int32_t max_len, int32_t n_groups,
+                                      const sense_trie_t *out, void *stream);
+
+/* Bytes of device workspace sense_soft_gate_verify_tree needs. */
+sense_status_t sense_soft_gate_verify_tree_workspace_size(int32_t n_cand, int32_t max_len,
+                                                          int32_t vocab, int32_t n_groups,
+                                                          size_t *bytes);
+
+/* Soft-gated evaluation through the loose trie (Sec. 3.2 Eq. 11: the
+ * aligned rows are [p_{t-1}; Gamma(P)]; Sec. 3.3 Eqs. 12-18; Alg. 4).
+ *   logits     per group g, 1 + NODES rows of row_stride elements (F32, F16
+ *              or BF16) starting at row g * (1 + NODES): row 0 is the
+ *              distribution at the current position (p_{t-1}), row 1 + u the
+ *              distribution after tree node u (P of the tree forward).  Only
+ *              rows 0 and 1 + u for nodes with children are read.
+ *   tree_tokens, tree_parent, tree_len, gamma
+ *              as written by sense_build_loose_trie (n_groups x NODES,
+ *              n_groups, n_cand x max_len).
+ * Tree node u (u < L_g, parent in [-1, NODES)) is judged once, by row
+ * 1 + parent(u) (row 0 at depth 0), with the statistics of
+ * sense_soft_gate_verify; draft c's position j takes node gamma[c][j].  A
+ * draft's length is its leading run of positions whose gamma is a judged
+ * node; the gate, window, accepted length and best draft are then those of
+ * sense_soft_gate_verify, per draft in gamma's (sorted) order: out_best is a
+ * sorted position (order[] gives the original draft).  The outputs have the
+ * layout of sense_soft_gate_verify's.  Needs n_cand % n_groups == 0 and the
+ * group limits of sense_build_loose_trie.
+ * Errors: INVALID_ARGUMENT, UNSUPPORTED, MISALIGNED (workspace), WORKSPACE,
+ * HIP. */
+sense_status_t sense_soft_gate_verify_tree(const void *logits, sense_dtype_t logits_dtype,
+                                           int64_t row_stride, const int32_t *tree_tokens,
+                                           const int32_t *tree_parent, const int32_t *tree_len,
+                                           const int32_t *gamma, int32_t n_cand,
+                                           int32_t max_len, int32_t vocab, int32_t n_groups,
+                                           const sense_gate_params_t *params,
+                                           int32_t *out_accept_len, int32_t *out_best,
+                                           float *out_gate_score, uint8_t *out_masks,
+                                           int32_t *out_rank, void *workspace,
+                                           size_t workspace_bytes, void *stream);
+
 /* Diagnostics for benchmarks and profilers.  Which part of the path a pair
  * of timing events brackets. */
 typedef enum {
     SENSE_TIMER_SCAN = 0,   /* similarity scan kernel(s) of sense_retrieve */
     SENSE_TIMER_TOPK = 1,   /* top-k selection + gather kernels of sense_retrieve */
-    SENSE_TIMER_VERIFY = 2, /* both kernels of sense_soft_gate_verify */
-    SENSE_TIMER_SELECT = 3  /* the kernel of sense_select_candidates */
+    SENSE_TIMER_VERIFY = 2, /* both kernels of sense_soft_gate_verify(_tree) */
+    SENSE_TIMER_SELECT = 3, /* the kernel of sense_select_candidates */
+    SENSE_TIMER_TRIE = 4    /* the kernels of sense_build_loose_trie */
 } sense_timer_t;
 
 /* Register two hipEvent_t handles (created by the caller with timing

@@ -104,12 +104,11 @@ def full_mask(mask, prefix_len: int, cache_len: int) -> np.ndarray:
     everything else is -inf.  float64 (L x cache_len)."""
     L = mask.shape[0]
     out = np.full((L, cache_len), -np.inf)
-    for i in range(L):
-        for j in range(cache_len):
-            if j < prefix_len:
-                out[i, j] = 0.0
-            elif j < prefix_len + L and mask[i, j - prefix_len] == 1:
-                out[i, j] = 0.0
+    out[:, :min(prefix_len, cache_len)] = 0.0
+    cols = np.arange(prefix_len, min(prefix_len + L, cache_len))
+    block = out[:, cols]
+    block[mask[:, cols - prefix_len] == 1] = 0.0
+    out[:, cols] = block
     return out
 
 

@@ -21,6 +21,8 @@ constexpr int kMaxK = 1024;         // largest retrieval top-k
 constexpr int kMaxLen = 64;         // longest draft
 constexpr int kSelectChunk = 8192;  // elements per top-k selection block
 constexpr int kMaxPool = 2048;      // largest static + dynamic candidate pool
+constexpr int kMaxGroup = 1024;     // largest candidate group of the loose trie
+constexpr int kMaxNodes = 4096;     // largest group x draft length of the loose trie
 
 // Order-preserving map of an fp32 score to an unsigned key: larger score ->
 // larger key; every NaN -> 0 (below everything); -0 is folded onto +0.
@@ -150,6 +152,42 @@ hipError_t launch_select_candidates(const float* scores_s, const int32_t* drafts
 hipError_t launch_append_rows(const void* src, int src_dtype, int key_dtype,
                               const int32_t* tokens, int d, int64_t n_old, int count,
                               int max_span, void* keys, int32_t* hist, int32_t* span_len,
+                              hipStream_t stream);
+
+// Outputs of the loose-trie build (device pointers; NULL = not wanted for
+// the optional ones).  Per group g of gs drafts of m tokens, nodes = gs * m
+// entries of the per-node arrays start at g * nodes.
+struct TrieOut {
+    int32_t* order;          // n_cand: original index of each sorted draft
+    int32_t* gamma;          // n_cand x m: tree id of each existing position, else -1
+    int32_t* tokens;         // node tokens (-1 past L)
+    int32_t* parent;         // node parent (-1 at depth 0 and past L)
+    int32_t* depth;          // node depth (-1 past L)
+    int32_t* cand;           // sorted draft creating the node (-1 past L)
+    int32_t* tree_len;       // n_groups: L
+    int32_t* sorted_drafts;  // optional n_cand x m (-1 padded)
+    int32_t* sorted_len;     // optional n_cand
+    uint8_t* mask;           // optional ancestor mask, nodes rows per group
+    int64_t mask_ld;
+    void* full_mask;         // optional static-KV mask, nodes rows x cache_len
+    int full_dtype;
+    int prefix_len;
+    int64_t cache_len;
+};
+
+hipError_t launch_trie(const int32_t* drafts, const int32_t* draft_len, int n_cand, int max_len,
+                       int n_groups, const TrieOut& out, hipStream_t stream);
+
+// Verification through the tree: logits hold, per group, row 0 = the
+// current position's distribution and row 1 + u = the distribution after
+// tree node u; candidate c's token j is tree node gamma[c][j].
+size_t verify_tree_workspace_bytes(int n_cand, int max_len, int vocab, int n_groups);
+hipError_t launch_verify_tree(const void* logits, int logits_dtype, int64_t row_stride,
+                              const int32_t* tree_tokens, const int32_t* tree_parent,
+                              const int32_t* tree_len, const int32_t* gamma, int n_cand,
+                              int max_len, int vocab, int n_groups, const GateParams& gp,
+                              int32_t* out_accept_len, int32_t* out_best, float* out_gate_score,
+                              uint8_t* out_masks, int32_t* out_rank, void* workspace,
                               hipStream_t stream);
 
 }  // namespace sense

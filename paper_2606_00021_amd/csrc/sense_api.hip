@@ -39,7 +39,7 @@ namespace {
 thread_local char g_msg[512];
 
 // Timing events per sense_timer_t, set by sense_set_timer_events.
-constexpr int kTimers = 4;
+constexpr int kTimers = 5;
 thread_local hipEvent_t g_timer[kTimers][2] = {};
 
 hipError_t timer_mark(int which, int edge, hipStream_t st) {
@@ -378,6 +378,24 @@ static sense_status_t check_verify_sizes(int32_t n_cand, int32_t max_len, int32_
     return SENSE_OK;
 }
 
+static sense_status_t check_gate_params(const sense_gate_params_t* params, int32_t vocab,
+                                        sense::GateParams* gp) {
+    if (!params) return fail(SENSE_ERR_INVALID_ARGUMENT, "params is NULL");
+    if (params->topk < 1) return fail(SENSE_ERR_INVALID_ARGUMENT, "topk = %d < 1", params->topk);
+    if (params->window < 0 || params->window > sense::kMaxLen)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "window = %d outside [0, %d]", params->window,
+                    sense::kMaxLen);
+    if (params->tau < 0) return fail(SENSE_ERR_INVALID_ARGUMENT, "tau = %d < 0", params->tau);
+    if (params->gamma != params->gamma) return fail(SENSE_ERR_INVALID_ARGUMENT, "gamma is NaN");
+    gp->gamma = params->gamma;
+    gp->topk = params->topk;
+    gp->window = params->window;
+    gp->tau = params->tau;
+    gp->ent_scale = params->entropy_normalized ? (float)(1.0 / log((double)vocab)) : 1.0f;
+    if (vocab == 1) gp->ent_scale = params->entropy_normalized ? 0.0f : 1.0f;  // E = 0 = ln 1
+    return SENSE_OK;
+}
+
 SENSE_EXPORT sense_status_t sense_soft_gate_verify_workspace_size(int32_t n_cand,
                                                                   int32_t max_len,
                                                                   int32_t vocab,
@@ -402,12 +420,8 @@ SENSE_EXPORT sense_status_t sense_soft_gate_verify(
         return fail(SENSE_ERR_INVALID_ARGUMENT, "unknown logits dtype %d", (int)logits_dtype);
     if (row_stride < vocab)
         return fail(SENSE_ERR_INVALID_ARGUMENT, "row_stride %lld < vocab %d", (long long)row_stride, vocab);
-    if (params->topk < 1) return fail(SENSE_ERR_INVALID_ARGUMENT, "topk = %d < 1", params->topk);
-    if (params->window < 0 || params->window > sense::kMaxLen)
-        return fail(SENSE_ERR_INVALID_ARGUMENT, "window = %d outside [0, %d]", params->window,
-                    sense::kMaxLen);
-    if (params->tau < 0) return fail(SENSE_ERR_INVALID_ARGUMENT, "tau = %d < 0", params->tau);
-    if (params->gamma != params->gamma) return fail(SENSE_ERR_INVALID_ARGUMENT, "gamma is NaN");
+    sense::GateParams gp;
+    if ((s = check_gate_params(params, vocab, &gp)) != SENSE_OK) return s;
     if (n_cand == 0) return ok();
     if (n_groups < 1 || n_cand % n_groups != 0)
         return fail(SENSE_ERR_INVALID_ARGUMENT, "n_groups = %d must divide n_cand = %d", n_groups,
@@ -423,13 +437,6 @@ SENSE_EXPORT sense_status_t sense_soft_gate_verify(
                     workspace ? workspace_bytes : (size_t)0);
     if (!aligned(workspace, 256)) return fail(SENSE_ERR_MISALIGNED, "workspace must be 256-byte aligned");
 
-    sense::GateParams gp;
-    gp.gamma = params->gamma;
-    gp.topk = params->topk;
-    gp.window = params->window;
-    gp.tau = params->tau;
-    gp.ent_scale = params->entropy_normalized ? (float)(1.0 / log((double)vocab)) : 1.0f;
-    if (vocab == 1) gp.ent_scale = params->entropy_normalized ? 0.0f : 1.0f;  // E = 0 = ln 1
     hipStream_t st = (hipStream_t)stream;
     hipError_t e;
     if ((e = timer_mark(SENSE_TIMER_VERIFY, 0, st)) != hipSuccess) return hip_fail(e, "timer");
@@ -494,5 +501,127 @@ SENSE_EXPORT sense_status_t sense_select_candidates(
                                         out_len, out_source, out_score, st);
     if (e != hipSuccess) return hip_fail(e, "candidate selection");
     if ((e = timer_mark(SENSE_TIMER_SELECT, 1, st)) != hipSuccess) return hip_fail(e, "timer");
+    return ok();
+}
+
+static sense_status_t check_groups(int32_t n_cand, int32_t max_len, int32_t n_groups) {
+    if (n_groups < 1 || n_cand % n_groups != 0)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "n_groups = %d must divide n_cand = %d", n_groups,
+                    n_cand);
+    const int gs = n_cand / n_groups;
+    if (gs > sense::kMaxGroup || (int64_t)gs * max_len > sense::kMaxNodes)
+        return fail(SENSE_ERR_UNSUPPORTED,
+                    "group of %d drafts x %d tokens exceeds %d drafts or %d tokens", gs, max_len,
+                    sense::kMaxGroup, sense::kMaxNodes);
+    return SENSE_OK;
+}
+
+SENSE_EXPORT sense_status_t sense_build_loose_trie(const int32_t* drafts, const int32_t* draft_len,
+                                                   int32_t n_cand, int32_t max_len,
+                                                   int32_t n_groups, const sense_trie_t* out,
+                                                   void* stream) {
+    if (!out) return fail(SENSE_ERR_INVALID_ARGUMENT, "out is NULL");
+    if (n_cand < 1) return fail(SENSE_ERR_INVALID_ARGUMENT, "n_cand = %d < 1", n_cand);
+    if (max_len < 1 || max_len > sense::kMaxLen)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "max_len = %d outside [1, %d]", max_len,
+                    sense::kMaxLen);
+    sense_status_t s = check_groups(n_cand, max_len, n_groups);
+    if (s != SENSE_OK) return s;
+    const sense_trie_t& O = *out;
+    if (!drafts || !O.order || !O.gamma || !O.tree_tokens || !O.tree_parent || !O.tree_depth ||
+        !O.tree_cand || !O.tree_len)
+        return fail(SENSE_ERR_INVALID_ARGUMENT,
+                    "drafts, order, gamma, tree_tokens, tree_parent, tree_depth, tree_cand and "
+                    "tree_len must be non-NULL");
+    const int64_t nodes = (int64_t)(n_cand / n_groups) * max_len;
+    if (O.mask && O.mask_ld < nodes)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "mask_ld = %lld < %lld nodes per group",
+                    (long long)O.mask_ld, (long long)nodes);
+    if (O.full_mask) {
+        if (!dtype_ok(O.full_mask_dtype))
+            return fail(SENSE_ERR_INVALID_ARGUMENT, "unknown full_mask_dtype %d",
+                        (int)O.full_mask_dtype);
+        if (O.prefix_len < 0 || O.cache_len < 1)
+            return fail(SENSE_ERR_INVALID_ARGUMENT, "prefix_len = %d and cache_len = %lld",
+                        O.prefix_len, (long long)O.cache_len);
+        if (!aligned(O.full_mask, (size_t)elem_size(O.full_mask_dtype)))
+            return fail(SENSE_ERR_MISALIGNED, "full_mask not aligned to its element size");
+    }
+    sense::TrieOut T;
+    T.order = O.order;
+    T.gamma = O.gamma;
+    T.tokens = O.tree_tokens;
+    T.parent = O.tree_parent;
+    T.depth = O.tree_depth;
+    T.cand = O.tree_cand;
+    T.tree_len = O.tree_len;
+    T.sorted_drafts = O.sorted_drafts;
+    T.sorted_len = O.sorted_len;
+    T.mask = O.mask;
+    T.mask_ld = O.mask_ld;
+    T.full_mask = O.full_mask;
+    T.full_dtype = O.full_mask_dtype;
+    T.prefix_len = O.prefix_len;
+    T.cache_len = O.full_mask ? O.cache_len : 0;
+    hipStream_t st = (hipStream_t)stream;
+    hipError_t e;
+    if ((e = timer_mark(SENSE_TIMER_TRIE, 0, st)) != hipSuccess) return hip_fail(e, "timer");
+    e = sense::launch_trie(drafts, draft_len, n_cand, max_len, n_groups, T, st);
+    if (e != hipSuccess) return hip_fail(e, "loose trie");
+    if ((e = timer_mark(SENSE_TIMER_TRIE, 1, st)) != hipSuccess) return hip_fail(e, "timer");
+    return ok();
+}
+
+SENSE_EXPORT sense_status_t sense_soft_gate_verify_tree_workspace_size(int32_t n_cand,
+                                                                       int32_t max_len,
+                                                                       int32_t vocab,
+                                                                       int32_t n_groups,
+                                                                       size_t* bytes) {
+    if (!bytes) return fail(SENSE_ERR_INVALID_ARGUMENT, "bytes is NULL");
+    sense_status_t s = check_verify_sizes(n_cand, max_len, vocab);
+    if (s != SENSE_OK) return s;
+    if (n_cand > 0 && (s = check_groups(n_cand, max_len, n_groups)) != SENSE_OK) return s;
+    *bytes = sense::verify_tree_workspace_bytes(n_cand, max_len, vocab, n_groups);
+    return ok();
+}
+
+SENSE_EXPORT sense_status_t sense_soft_gate_verify_tree(
+    const void* logits, sense_dtype_t logits_dtype, int64_t row_stride,
+    const int32_t* tree_tokens, const int32_t* tree_parent, const int32_t* tree_len,
+    const int32_t* gamma, int32_t n_cand, int32_t max_len, int32_t vocab, int32_t n_groups,
+    const sense_gate_params_t* params, int32_t* out_accept_len, int32_t* out_best,
+    float* out_gate_score, uint8_t* out_masks, int32_t* out_rank, void* workspace,
+    size_t workspace_bytes, void* stream) {
+    sense_status_t s = check_verify_sizes(n_cand, max_len, vocab);
+    if (s != SENSE_OK) return s;
+    sense::GateParams gp;
+    if ((s = check_gate_params(params, vocab, &gp)) != SENSE_OK) return s;
+    if (!dtype_ok(logits_dtype))
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "unknown logits dtype %d", (int)logits_dtype);
+    if (row_stride < vocab)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "row_stride %lld < vocab %d", (long long)row_stride, vocab);
+    if (n_cand == 0) return ok();
+    if ((s = check_groups(n_cand, max_len, n_groups)) != SENSE_OK) return s;
+    if (!logits || !tree_tokens || !tree_parent || !tree_len || !gamma || !out_accept_len ||
+        !out_best)
+        return fail(SENSE_ERR_INVALID_ARGUMENT,
+                    "logits, tree_tokens, tree_parent, tree_len, gamma, out_accept_len and "
+                    "out_best must be non-NULL");
+    if (!aligned(logits, (size_t)elem_size(logits_dtype)))
+        return fail(SENSE_ERR_MISALIGNED, "logits not aligned to their element size");
+    const size_t need = sense::verify_tree_workspace_bytes(n_cand, max_len, vocab, n_groups);
+    if (!workspace || workspace_bytes < need)
+        return fail(SENSE_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
+                    workspace ? workspace_bytes : (size_t)0);
+    if (!aligned(workspace, 256)) return fail(SENSE_ERR_MISALIGNED, "workspace must be 256-byte aligned");
+    hipStream_t st = (hipStream_t)stream;
+    hipError_t e;
+    if ((e = timer_mark(SENSE_TIMER_VERIFY, 0, st)) != hipSuccess) return hip_fail(e, "timer");
+    e = sense::launch_verify_tree(logits, logits_dtype, row_stride, tree_tokens, tree_parent,
+                                  tree_len, gamma, n_cand, max_len, vocab, n_groups, gp,
+                                  out_accept_len, out_best, out_gate_score, out_masks, out_rank,
+                                  workspace, st);
+    if (e != hipSuccess) return hip_fail(e, "soft-gated evaluation through the tree");
+    if ((e = timer_mark(SENSE_TIMER_VERIFY, 1, st)) != hipSuccess) return hip_fail(e, "timer");
     return ok();
 }

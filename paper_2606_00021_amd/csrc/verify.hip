@@ -159,24 +159,46 @@ __device__ __forceinline__ void absorb(Acc& a, float x, float nm, float thr) {
     a.cnt += (x >= thr) ? 1 : 0;
 }
 
-template <int LT, bool VEC>
+// A tree node is judged when it lies below the group's node count and its
+// parent is a node of the group (or none): then its logits row is
+// 1 + parent within the group's 1 + nodes rows.
+__device__ __forceinline__ bool tree_item(int item, int nodes, const int32_t* tree_parent,
+                                          const int32_t* tree_len, int64_t* row) {
+    const int g = item / nodes, u = item - g * nodes;
+    if (u >= tree_len[g]) return false;
+    const int par = tree_parent[item];
+    if (par < -1 || par >= nodes) return false;
+    *row = (int64_t)g * (nodes + 1) + 1 + par;
+    return true;
+}
+
+// One block per (item, vocabulary slice).  Dense: item = candidate * max_len
+// + position, its own logits row, token drafts[item].  TREE: item = group *
+// nodes + tree node, token tree_tokens[item], row from tree_item.
+template <int LT, bool VEC, bool TREE>
 __global__ __launch_bounds__(kRowThreads) void verify_rows_kernel(
     const void* __restrict__ logits, int64_t row_stride, const int32_t* __restrict__ drafts,
     const int32_t* __restrict__ draft_len, int max_len, int vocab, int slice_len, int n_slices,
-    Partial* __restrict__ partial) {
+    Partial* __restrict__ partial, const int32_t* __restrict__ tree_parent,
+    const int32_t* __restrict__ tree_len, int nodes) {
     constexpr int VW = (LT == DT_F32) ? 4 : 8;      // elements per 16-byte load
     constexpr int ES = (LT == DT_F32) ? 4 : 2;      // element size
-    const int row = blockIdx.x;
+    const int item = blockIdx.x;
     const int slice = blockIdx.y;
     const int tid = threadIdx.x;
-    const int c = row / max_len, j = row - c * max_len;
-    int len = draft_len ? draft_len[c] : max_len;
-    len = len < 0 ? 0 : (len > max_len ? max_len : len);
-    if (j >= len) return;                            // uniform over the block
+    int64_t row = item;
+    if constexpr (TREE) {
+        if (!tree_item(item, nodes, tree_parent, tree_len, &row)) return;   // uniform
+    } else {
+        const int c = item / max_len, j = item - c * max_len;
+        int len = draft_len ? draft_len[c] : max_len;
+        len = len < 0 ? 0 : (len > max_len ? max_len : len);
+        if (j >= len) return;                        // uniform over the block
+    }
 
-    const int tok = drafts[row];
+    const int tok = drafts[item];
     const bool valid = tok >= 0 && tok < vocab;
-    const char* rowp = (const char*)logits + (int64_t)row * row_stride * ES;
+    const char* rowp = (const char*)logits + row * row_stride * ES;
     const float xd = valid ? load_one<LT>(rowp, tok) : 0.0f;
     const int tk = valid ? tok : -1;                 // -1: the count is unused
     const float thr_lo = xd, thr_hi = next_up(xd);   // left of d / from d on
@@ -271,7 +293,7 @@ __global__ __launch_bounds__(kRowThreads) void verify_rows_kernel(
         Partial p{mx, (s_w[0].s + s_w[1].s) + (s_w[2].s + s_w[3].s),
                   (s_w[0].t2 + s_w[1].t2) + (s_w[2].t2 + s_w[3].t2),
                   (s_w[0].cnt + s_w[1].cnt) + (s_w[2].cnt + s_w[3].cnt)};
-        partial[(int64_t)row * n_slices + slice] = p;
+        partial[(int64_t)item * n_slices + slice] = p;
     }
 }
 
@@ -280,6 +302,68 @@ constexpr int kFinChunkRows = 4096;   // (candidate, position) rows per LDS chun
 
 __device__ __forceinline__ uint64_t bits_upto(int x) {  // bits 0..x set (x may be -1)
     return (x >= 63) ? ~0ull : ((x < 0) ? 0ull : ((1ull << (x + 1)) - 1ull));
+}
+
+// Row statistics of one item from its slice partials: the entropy score
+// and the rank of the judged token; bits em | ent<<1 | topk<<2.
+__device__ __forceinline__ uint8_t item_bits(const Partial* p, int n_slices, int tok, int vocab,
+                                             const GateParams& gp, float* score, int* rank) {
+    Stats a{p[0].m, p[0].s, p[0].t2};
+    int cnt = p[0].cnt;
+    for (int s = 1; s < n_slices; ++s) {
+        a = merge(a, Stats{p[s].m, p[s].s, p[s].t2});
+        cnt += p[s].cnt;
+    }
+    const float e_nats = __logf(a.s) - (kLn2 * a.t2) / a.s;
+    *score = e_nats * gp.ent_scale;
+    const bool valid = tok >= 0 && tok < vocab;
+    *rank = valid ? cnt : vocab;
+    return (uint8_t)((valid && *rank == 0 ? 1 : 0) | (*score > gp.gamma ? 2 : 0) |
+                     (valid && *rank < gp.topk ? 4 : 0));
+}
+
+// The gate of one draft from its per-position bits (Alg. 4's window,
+// cascade and leading run).  Writes the masks row if asked; returns n.
+__device__ __forceinline__ int gate_draft(uint64_t em, uint64_t ent, uint64_t tkm, int len,
+                                          int max_len, const GateParams& gp,
+                                          uint8_t* masks_row) {
+    // Mismatches: 1 - B_em inside the draft, and W padding ones after it.
+    const uint64_t notem = ~em & bits_upto(max_len - 1);
+    int n = 0;
+    bool still = true;
+    for (int jj = 0; jj < max_len; ++jj) {
+        const int hi = jj + gp.window;
+        const int in_hi = hi < max_len - 1 ? hi : max_len - 1;
+        const uint64_t range = bits_upto(in_hi) & ~bits_upto(jj);
+        const int r = __popcll(notem & range) + (hi > max_len - 1 ? hi - (max_len - 1) : 0);
+        const bool con = r <= gp.tau;
+        const bool bem = (em >> jj) & 1, bent = (ent >> jj) & 1, btk = (tkm >> jj) & 1;
+        const bool gate = (jj < len) && (bem || (bent && (btk || con)));
+        if (still && gate) ++n; else still = false;
+        if (masks_row)
+            masks_row[jj] = (uint8_t)((int)bem | ((int)bent << 1) | ((int)btk << 2) |
+                                      ((int)con << 3) | ((int)gate << 4));
+    }
+    return n;
+}
+
+// First candidate with the largest n in the block (all threads call it).
+__device__ void group_best(int best_n, int best_i, int32_t* out) {
+    __shared__ int s_n[kFinThreads], s_i[kFinThreads];
+    s_n[threadIdx.x] = best_n;
+    s_i[threadIdx.x] = best_i;
+    __syncthreads();
+    for (int off = kFinThreads / 2; off > 0; off >>= 1) {
+        if ((int)threadIdx.x < off) {
+            const int on = s_n[threadIdx.x + off], oi = s_i[threadIdx.x + off];
+            if (on > s_n[threadIdx.x] || (on == s_n[threadIdx.x] && oi < s_i[threadIdx.x])) {
+                s_n[threadIdx.x] = on;
+                s_i[threadIdx.x] = oi;
+            }
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) *out = s_i[0];
 }
 
 __global__ __launch_bounds__(kFinThreads) void verify_finalize_kernel(
@@ -302,27 +386,12 @@ __global__ __launch_bounds__(kFinThreads) void verify_finalize_kernel(
             len = len < 0 ? 0 : (len > max_len ? max_len : len);
             const int64_t row = (int64_t)c * max_len + jj;
             uint8_t bits = 0;
-            if (jj < len) {
-                const Partial* p = partial + row * n_slices;
-                Stats a{p[0].m, p[0].s, p[0].t2};
-                int cnt = p[0].cnt;
-                for (int s = 1; s < n_slices; ++s) {
-                    a = merge(a, Stats{p[s].m, p[s].s, p[s].t2});
-                    cnt += p[s].cnt;
-                }
-                const float e_nats = __logf(a.s) - (kLn2 * a.t2) / a.s;
-                const float score = e_nats * gp.ent_scale;
-                const int tok = drafts[row];
-                const bool valid = tok >= 0 && tok < vocab;
-                const int rank = valid ? cnt : vocab;
-                bits = (uint8_t)((valid && rank == 0 ? 1 : 0) | (score > gp.gamma ? 2 : 0) |
-                                 (valid && rank < gp.topk ? 4 : 0));
-                if (out_gate_score) out_gate_score[row] = score;
-                if (out_rank) out_rank[row] = rank;
-            } else {
-                if (out_gate_score) out_gate_score[row] = 0.0f;
-                if (out_rank) out_rank[row] = vocab;
-            }
+            float score = 0.0f;
+            int rank = vocab;
+            if (jj < len) bits = item_bits(partial + row * n_slices, n_slices, drafts[row], vocab,
+                                           gp, &score, &rank);
+            if (out_gate_score) out_gate_score[row] = score;
+            if (out_rank) out_rank[row] = rank;
             s_bits[r] = bits;
         }
         __syncthreads();
@@ -338,24 +407,8 @@ __global__ __launch_bounds__(kFinThreads) void verify_finalize_kernel(
                 ent |= (uint64_t)((b >> 1) & 1) << jj;
                 tkm |= (uint64_t)((b >> 2) & 1) << jj;
             }
-            // Mismatches: 1 - B_em inside the draft, and W padding ones after it.
-            const uint64_t notem = ~em & bits_upto(max_len - 1);
-            int n = 0;
-            bool still = true;
-            for (int jj = 0; jj < max_len; ++jj) {
-                const int hi = jj + gp.window;
-                const int in_hi = hi < max_len - 1 ? hi : max_len - 1;
-                const uint64_t range = bits_upto(in_hi) & ~bits_upto(jj);
-                const int r = __popcll(notem & range) + (hi > max_len - 1 ? hi - (max_len - 1) : 0);
-                const bool con = r <= gp.tau;
-                const bool bem = (em >> jj) & 1, bent = (ent >> jj) & 1, btk = (tkm >> jj) & 1;
-                const bool gate = (jj < len) && (bem || (bent && (btk || con)));
-                if (still && gate) ++n; else still = false;
-                if (out_masks)
-                    out_masks[(int64_t)c * max_len + jj] =
-                        (uint8_t)((int)bem | ((int)bent << 1) | ((int)btk << 2) | ((int)con << 3) |
-                                  ((int)gate << 4));
-            }
+            const int n = gate_draft(em, ent, tkm, len, max_len, gp,
+                                     out_masks ? out_masks + (int64_t)c * max_len : nullptr);
             out_accept_len[c] = n;
             if (n > best_n) {
                 best_n = n;
@@ -364,22 +417,69 @@ __global__ __launch_bounds__(kFinThreads) void verify_finalize_kernel(
         }
         __syncthreads();
     }
-    // First candidate with the largest n in the group.
-    __shared__ int s_n[kFinThreads], s_i[kFinThreads];
-    s_n[threadIdx.x] = best_n;
-    s_i[threadIdx.x] = best_i;
-    __syncthreads();
-    for (int off = kFinThreads / 2; off > 0; off >>= 1) {
-        if ((int)threadIdx.x < off) {
-            const int on = s_n[threadIdx.x + off], oi = s_i[threadIdx.x + off];
-            if (on > s_n[threadIdx.x] || (on == s_n[threadIdx.x] && oi < s_i[threadIdx.x])) {
-                s_n[threadIdx.x] = on;
-                s_i[threadIdx.x] = oi;
-            }
-        }
-        __syncthreads();
+    group_best(best_n, best_i, out_best + g);
+}
+
+// Tree variant, one block per group: phase 1 gives every tree node of the
+// group a thread (bits, score and rank into LDS); phase 2 gives every draft
+// a thread that reads its positions' nodes through Gamma.  A draft's length
+// is its leading run of positions with a judged node.
+__global__ __launch_bounds__(kFinThreads) void verify_finalize_tree_kernel(
+    const Partial* __restrict__ partial, int n_slices, const int32_t* __restrict__ tree_tokens,
+    const int32_t* __restrict__ tree_parent, const int32_t* __restrict__ tree_len,
+    const int32_t* __restrict__ gamma, int max_len, int vocab, int group_size, GateParams gp,
+    int32_t* __restrict__ out_accept_len, int32_t* __restrict__ out_best,
+    float* __restrict__ out_gate_score, uint8_t* __restrict__ out_masks,
+    int32_t* __restrict__ out_rank) {
+    __shared__ uint8_t s_bits[kMaxNodes];       // em | ent<<1 | topk<<2 | judged<<3
+    __shared__ float s_score[kMaxNodes];
+    __shared__ int32_t s_rank[kMaxNodes];
+    const int g = blockIdx.x;
+    const int nodes = group_size * max_len;
+    const int L = tree_len[g] < nodes ? tree_len[g] : nodes;
+    for (int u = threadIdx.x; u < L; u += kFinThreads) {
+        const int item = g * nodes + u;
+        int64_t row;
+        uint8_t bits = 0;
+        float score = 0.0f;
+        int rank = vocab;
+        if (tree_item(item, nodes, tree_parent, tree_len, &row))
+            bits = 8 | item_bits(partial + (int64_t)item * n_slices, n_slices, tree_tokens[item],
+                                 vocab, gp, &score, &rank);
+        s_bits[u] = bits;
+        s_score[u] = score;
+        s_rank[u] = rank;
     }
-    if (threadIdx.x == 0) out_best[g] = s_i[0];
+    __syncthreads();
+    int best_n = -1, best_i = 0;
+    for (int cl = threadIdx.x; cl < group_size; cl += kFinThreads) {
+        const int c = g * group_size + cl;
+        uint64_t em = 0, ent = 0, tkm = 0;
+        int len = 0;
+        bool run = true;
+        for (int jj = 0; jj < max_len; ++jj) {
+            const int u = gamma[(int64_t)c * max_len + jj];
+            const bool judged = run && u >= 0 && u < L && (s_bits[u] & 8);
+            run = judged;
+            const uint8_t b = judged ? s_bits[u] : 0;
+            len += judged ? 1 : 0;
+            em |= (uint64_t)(b & 1) << jj;
+            ent |= (uint64_t)((b >> 1) & 1) << jj;
+            tkm |= (uint64_t)((b >> 2) & 1) << jj;
+            const int64_t o = (int64_t)c * max_len + jj;
+            if (out_gate_score) out_gate_score[o] = judged ? s_score[u] : 0.0f;
+            if (out_rank) out_rank[o] = judged ? s_rank[u] : vocab;
+        }
+        const int n = gate_draft(em, ent, tkm, len, max_len, gp,
+                                 out_masks ? out_masks + (int64_t)c * max_len : nullptr);
+        out_accept_len[c] = n;
+        if (n > best_n) {
+            best_n = n;
+            best_i = cl;
+        }
+    }
+    __syncthreads();
+    group_best(best_n, best_i, out_best + g);
 }
 
 struct Plan {
@@ -394,20 +494,49 @@ Plan plan_slices(int vocab, int dtype, bool vec) {
     return Plan{vec, (vocab + slice_len - 1) / slice_len, slice_len};
 }
 
-template <int LT>
-hipError_t launch_rows(const void* logits, int64_t row_stride, const int32_t* drafts,
-                       const int32_t* draft_len, int n_cand, int max_len, int vocab,
-                       const Plan& pl, Partial* part, hipStream_t stream) {
-    const dim3 grid((unsigned)((int64_t)n_cand * max_len), (unsigned)pl.n_slices);
+template <int LT, bool TREE>
+hipError_t launch_rows_t(const void* logits, int64_t row_stride, const int32_t* tokens,
+                         const int32_t* draft_len, int64_t n_items, int max_len, int vocab,
+                         const Plan& pl, Partial* part, const int32_t* tree_parent,
+                         const int32_t* tree_len, int nodes, hipStream_t stream) {
+    const dim3 grid((unsigned)n_items, (unsigned)pl.n_slices);
     if (pl.vec)
-        hipLaunchKernelGGL((verify_rows_kernel<LT, true>), grid, dim3(kRowThreads), 0, stream,
-                           logits, row_stride, drafts, draft_len, max_len, vocab, pl.slice_len,
-                           pl.n_slices, part);
+        hipLaunchKernelGGL((verify_rows_kernel<LT, true, TREE>), grid, dim3(kRowThreads), 0,
+                           stream, logits, row_stride, tokens, draft_len, max_len, vocab,
+                           pl.slice_len, pl.n_slices, part, tree_parent, tree_len, nodes);
     else
-        hipLaunchKernelGGL((verify_rows_kernel<LT, false>), grid, dim3(kRowThreads), 0, stream,
-                           logits, row_stride, drafts, draft_len, max_len, vocab, pl.slice_len,
-                           pl.n_slices, part);
+        hipLaunchKernelGGL((verify_rows_kernel<LT, false, TREE>), grid, dim3(kRowThreads), 0,
+                           stream, logits, row_stride, tokens, draft_len, max_len, vocab,
+                           pl.slice_len, pl.n_slices, part, tree_parent, tree_len, nodes);
     return hipGetLastError();
+}
+
+template <bool TREE>
+hipError_t launch_rows(const void* logits, int logits_dtype, int64_t row_stride,
+                       const int32_t* tokens, const int32_t* draft_len, int64_t n_items,
+                       int max_len, int vocab, const Plan& pl, Partial* part,
+                       const int32_t* tree_parent, const int32_t* tree_len, int nodes,
+                       hipStream_t stream) {
+    switch (logits_dtype) {
+        case DT_F32:
+            return launch_rows_t<DT_F32, TREE>(logits, row_stride, tokens, draft_len, n_items,
+                                               max_len, vocab, pl, part, tree_parent, tree_len,
+                                               nodes, stream);
+        case DT_F16:
+            return launch_rows_t<DT_F16, TREE>(logits, row_stride, tokens, draft_len, n_items,
+                                               max_len, vocab, pl, part, tree_parent, tree_len,
+                                               nodes, stream);
+        default:
+            return launch_rows_t<DT_BF16, TREE>(logits, row_stride, tokens, draft_len, n_items,
+                                                max_len, vocab, pl, part, tree_parent, tree_len,
+                                                nodes, stream);
+    }
+}
+
+Plan make_plan(const void* logits, int logits_dtype, int64_t row_stride, int vocab) {
+    const int es = (logits_dtype == DT_F32) ? 4 : 2;
+    const bool vec = ((uintptr_t)logits % 16 == 0) && ((row_stride * es) % 16 == 0);
+    return plan_slices(vocab, logits_dtype, vec);
 }
 
 }  // namespace
@@ -418,6 +547,13 @@ size_t verify_workspace_bytes(int n_cand, int max_len, int vocab) {
     return (size_t)n_cand * (size_t)max_len * (size_t)p.n_slices * sizeof(Partial);
 }
 
+size_t verify_tree_workspace_bytes(int n_cand, int max_len, int vocab, int n_groups) {
+    // One partial per (tree node, slice); a group has at most n_cand / n_groups
+    // * max_len nodes, so the dense bound is also the tree bound.
+    (void)n_groups;
+    return verify_workspace_bytes(n_cand, max_len, vocab);
+}
+
 hipError_t launch_verify(const void* logits, int logits_dtype, int64_t row_stride,
                          const int32_t* drafts, const int32_t* draft_len, int n_cand,
                          int max_len, int vocab, int n_groups, const GateParams& gp,
@@ -425,29 +561,38 @@ hipError_t launch_verify(const void* logits, int logits_dtype, int64_t row_strid
                          uint8_t* out_masks, int32_t* out_rank, void* workspace,
                          hipStream_t stream) {
     if (n_cand == 0) return hipSuccess;
-    const int es = (logits_dtype == DT_F32) ? 4 : 2;
-    const bool vec = ((uintptr_t)logits % 16 == 0) && ((row_stride * es) % 16 == 0);
-    const Plan pl = plan_slices(vocab, logits_dtype, vec);
+    const Plan pl = make_plan(logits, logits_dtype, row_stride, vocab);
     Partial* part = (Partial*)workspace;
-    hipError_t e;
-    switch (logits_dtype) {
-        case DT_F32:
-            e = launch_rows<DT_F32>(logits, row_stride, drafts, draft_len, n_cand, max_len,
-                                    vocab, pl, part, stream);
-            break;
-        case DT_F16:
-            e = launch_rows<DT_F16>(logits, row_stride, drafts, draft_len, n_cand, max_len,
-                                    vocab, pl, part, stream);
-            break;
-        default:
-            e = launch_rows<DT_BF16>(logits, row_stride, drafts, draft_len, n_cand, max_len,
-                                     vocab, pl, part, stream);
-            break;
-    }
+    hipError_t e = launch_rows<false>(logits, logits_dtype, row_stride, drafts, draft_len,
+                                      (int64_t)n_cand * max_len, max_len, vocab, pl, part,
+                                      nullptr, nullptr, 0, stream);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(verify_finalize_kernel, dim3((unsigned)n_groups), dim3(kFinThreads), 0,
                        stream, part, pl.n_slices, drafts, draft_len, max_len, vocab,
                        n_cand / n_groups, gp, out_accept_len, out_best, out_gate_score,
+                       out_masks, out_rank);
+    return hipGetLastError();
+}
+
+hipError_t launch_verify_tree(const void* logits, int logits_dtype, int64_t row_stride,
+                              const int32_t* tree_tokens, const int32_t* tree_parent,
+                              const int32_t* tree_len, const int32_t* gamma, int n_cand,
+                              int max_len, int vocab, int n_groups, const GateParams& gp,
+                              int32_t* out_accept_len, int32_t* out_best, float* out_gate_score,
+                              uint8_t* out_masks, int32_t* out_rank, void* workspace,
+                              hipStream_t stream) {
+    if (n_cand == 0) return hipSuccess;
+    const Plan pl = make_plan(logits, logits_dtype, row_stride, vocab);
+    Partial* part = (Partial*)workspace;
+    const int gs = n_cand / n_groups;
+    const int nodes = gs * max_len;
+    hipError_t e = launch_rows<true>(logits, logits_dtype, row_stride, tree_tokens, nullptr,
+                                     (int64_t)n_groups * nodes, max_len, vocab, pl, part,
+                                     tree_parent, tree_len, nodes, stream);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(verify_finalize_tree_kernel, dim3((unsigned)n_groups), dim3(kFinThreads),
+                       0, stream, part, pl.n_slices, tree_tokens, tree_parent, tree_len, gamma,
+                       max_len, vocab, gs, gp, out_accept_len, out_best, out_gate_score,
                        out_masks, out_rank);
     return hipGetLastError();
 }

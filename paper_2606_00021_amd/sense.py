@@ -44,12 +44,16 @@ EXPORTED = (
     "sense_build_dynamic_index",
     "sense_index_append",
     "sense_select_candidates",
+    "sense_build_loose_trie",
+    "sense_soft_gate_verify_tree_workspace_size",
+    "sense_soft_gate_verify_tree",
     "sense_set_timer_events",
     "sense_read_bandwidth_probe",
     "sense_status_string",
     "sense_last_error_message",
 )
 SENSE_TIMER_SCAN, SENSE_TIMER_TOPK, SENSE_TIMER_VERIFY, SENSE_TIMER_SELECT = 0, 1, 2, 3
+SENSE_TIMER_TRIE = 4
 
 
 class SenseError(RuntimeError):
@@ -90,6 +94,26 @@ class SelectParams(ctypes.Structure):
         ("beta", ctypes.c_float),
         ("delta", ctypes.c_float),
         ("anchor_override", ctypes.c_int32),
+    ]
+
+
+class TrieDesc(ctypes.Structure):
+    _fields_ = [
+        ("order", ctypes.c_void_p),
+        ("gamma", ctypes.c_void_p),
+        ("tree_tokens", ctypes.c_void_p),
+        ("tree_parent", ctypes.c_void_p),
+        ("tree_depth", ctypes.c_void_p),
+        ("tree_cand", ctypes.c_void_p),
+        ("tree_len", ctypes.c_void_p),
+        ("sorted_drafts", ctypes.c_void_p),
+        ("sorted_len", ctypes.c_void_p),
+        ("mask", ctypes.c_void_p),
+        ("mask_ld", ctypes.c_int64),
+        ("full_mask", ctypes.c_void_p),
+        ("full_mask_dtype", ctypes.c_int),
+        ("prefix_len", ctypes.c_int32),
+        ("cache_len", ctypes.c_int64),
     ]
 
 
@@ -134,6 +158,10 @@ def load_library() -> ctypes.CDLL:
                                     ctypes.POINTER(SelectParams), P, P, P, P, P],
         "sense_soft_gate_verify": [P, ctypes.c_int, I64, P, P, I32, I32, I32, I32,
                                    ctypes.POINTER(GateParams), P, P, P, P, P, P, SZ, P],
+        "sense_build_loose_trie": [P, P, I32, I32, I32, ctypes.POINTER(TrieDesc), P],
+        "sense_soft_gate_verify_tree_workspace_size": [I32, I32, I32, I32, PSZ],
+        "sense_soft_gate_verify_tree": [P, ctypes.c_int, I64, P, P, P, P, I32, I32, I32, I32,
+                                        ctypes.POINTER(GateParams), P, P, P, P, P, P, SZ, P],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -460,3 +488,123 @@ def sense_read_bandwidth_probe(buf: torch.Tensor, sink: torch.Tensor, stream=Non
     _check(load_library().sense_read_bandwidth_probe(_dev_ptr(buf, "buf"), nbytes,
                                                      _dev_ptr(sink, "sink"), _stream_handle(stream)),
            "sense_read_bandwidth_probe")
+
+
+def sense_build_loose_trie(drafts: torch.Tensor, draft_len: torch.Tensor | None = None,
+                           n_groups: int = 1, want_sorted: bool = True, want_mask: bool = False,
+                           full_mask: dict | None = None, out: dict | None = None,
+                           stream=None) -> dict:
+    """LexSort + loose trie of each group of ``drafts`` (C x M int32).
+
+    Returns a dict of device tensors: order [C], gamma [C,M] (sorted order),
+    tree_tokens / tree_parent / tree_depth / tree_cand [G, nodes],
+    tree_len [G], and optionally sorted_drafts [C,M], sorted_len [C],
+    mask [G, nodes, nodes] uint8 and full_mask [G, nodes, cache_len]
+    (``full_mask`` = {"dtype": torch dtype, "prefix_len": m, "cache_len": n})."""
+    lib = load_library()
+    if drafts.dtype != torch.int32 or drafts.dim() != 2 or not drafts.is_contiguous():
+        raise ValueError("drafts must be a contiguous C x M int32 tensor")
+    if draft_len is not None and (draft_len.dtype != torch.int32 or not draft_len.is_contiguous()
+                                  or draft_len.numel() != drafts.shape[0]):
+        raise ValueError("draft_len must be a contiguous int32 tensor of C entries")
+    c, m = drafts.shape
+    if n_groups < 1 or c % n_groups:
+        raise ValueError("n_groups must divide the number of drafts")
+    nodes = c // n_groups * m
+    dev = drafts.device
+    if out is None:
+        i32 = dict(dtype=torch.int32, device=dev)
+        out = {"order": torch.empty(c, **i32), "gamma": torch.empty((c, m), **i32),
+               "tree_tokens": torch.empty((n_groups, nodes), **i32),
+               "tree_parent": torch.empty((n_groups, nodes), **i32),
+               "tree_depth": torch.empty((n_groups, nodes), **i32),
+               "tree_cand": torch.empty((n_groups, nodes), **i32),
+               "tree_len": torch.empty(n_groups, **i32)}
+        if want_sorted:
+            out["sorted_drafts"] = torch.empty((c, m), **i32)
+            out["sorted_len"] = torch.empty(c, **i32)
+        if want_mask:
+            out["mask"] = torch.zeros((n_groups, nodes, nodes), dtype=torch.uint8, device=dev)
+        if full_mask is not None:
+            out["full_mask"] = torch.zeros((n_groups, nodes, full_mask["cache_len"]),
+                                           dtype=full_mask["dtype"], device=dev)
+    fm = out.get("full_mask")
+    if fm is not None and full_mask is None:
+        raise ValueError("out holds a full_mask: pass full_mask={'prefix_len': ...} as well")
+    desc = TrieDesc(
+        order=_dev_ptr(out["order"], "order"), gamma=_dev_ptr(out["gamma"], "gamma"),
+        tree_tokens=_dev_ptr(out["tree_tokens"], "tree_tokens"),
+        tree_parent=_dev_ptr(out["tree_parent"], "tree_parent"),
+        tree_depth=_dev_ptr(out["tree_depth"], "tree_depth"),
+        tree_cand=_dev_ptr(out["tree_cand"], "tree_cand"),
+        tree_len=_dev_ptr(out["tree_len"], "tree_len"),
+        sorted_drafts=_dev_ptr(out.get("sorted_drafts"), "sorted_drafts"),
+        sorted_len=_dev_ptr(out.get("sorted_len"), "sorted_len"),
+        mask=_dev_ptr(out.get("mask"), "mask"),
+        mask_ld=out["mask"].shape[-1] if "mask" in out else 0,
+        full_mask=_dev_ptr(fm, "full_mask"),
+        full_mask_dtype=_TORCH_DTYPE[fm.dtype] if fm is not None else 0,
+        prefix_len=full_mask["prefix_len"] if full_mask is not None else 0,
+        cache_len=fm.shape[-1] if fm is not None else 0)
+    _check(lib.sense_build_loose_trie(_dev_ptr(drafts, "drafts"), _dev_ptr(draft_len, "draft_len"),
+                                      c, m, n_groups, ctypes.byref(desc), _stream_handle(stream)),
+           "sense_build_loose_trie")
+    return out
+
+
+def sense_soft_gate_verify_tree_workspace_size(n_cand: int, max_len: int, vocab: int,
+                                               n_groups: int) -> int:
+    size = ctypes.c_size_t()
+    _check(load_library().sense_soft_gate_verify_tree_workspace_size(
+        n_cand, max_len, vocab, n_groups, ctypes.byref(size)),
+        "sense_soft_gate_verify_tree_workspace_size")
+    return size.value
+
+
+def sense_soft_gate_verify_tree(logits: torch.Tensor, trie: dict, n_groups: int = 1,
+                                gamma: float = 0.05, topk: int = 3, window: int = 6,
+                                tau: int = 0, entropy_normalized: bool = True,
+                                vocab: int | None = None, want_gate_score: bool = True,
+                                want_masks: bool = True, want_rank: bool = True,
+                                workspace: torch.Tensor | None = None, out: dict | None = None,
+                                stream=None) -> dict:
+    """Soft-gated evaluation through the loose trie.  ``logits`` holds per
+    group 1 + nodes rows (G x (1 + nodes) x V, or (G * (1 + nodes)) x V):
+    row 0 the current position's distribution, row 1 + u the distribution
+    after tree node u.  ``trie`` is sense_build_loose_trie's result.  Returns
+    the outputs of sense_soft_gate_verify, per draft in sorted order."""
+    lib = load_library()
+    gam = trie["gamma"]
+    c, m = gam.shape
+    if logits.dtype not in _TORCH_DTYPE or logits.stride(-1) != 1:
+        raise ValueError("logits must be float32/float16/bfloat16 with contiguous rows")
+    rows = logits.reshape(-1, logits.shape[-1]) if logits.dim() == 3 else logits
+    if rows.dim() != 2 or rows.shape[0] != n_groups * (1 + c // n_groups * m):
+        raise ValueError("logits must hold n_groups x (1 + nodes) rows")
+    row_stride = rows.stride(0)
+    v = rows.shape[1] if vocab is None else vocab
+    dev = gam.device
+    if out is None:
+        out = {"accept_len": torch.empty(c, dtype=torch.int32, device=dev),
+               "best": torch.empty(max(n_groups, 1), dtype=torch.int32, device=dev)}
+        if want_gate_score:
+            out["gate_score"] = torch.empty((c, m), dtype=torch.float32, device=dev)
+        if want_masks:
+            out["masks"] = torch.empty((c, m), dtype=torch.uint8, device=dev)
+        if want_rank:
+            out["rank"] = torch.empty((c, m), dtype=torch.int32, device=dev)
+    if workspace is None:
+        workspace = torch.empty(max(sense_soft_gate_verify_tree_workspace_size(c, m, v, n_groups),
+                                    1), dtype=torch.uint8, device=dev)
+    params = GateParams(gamma=gamma, topk=topk, window=window, tau=tau,
+                        entropy_normalized=int(bool(entropy_normalized)))
+    _check(lib.sense_soft_gate_verify_tree(
+        _dev_ptr(rows, "logits"), _TORCH_DTYPE[logits.dtype], row_stride,
+        _dev_ptr(trie["tree_tokens"], "tree_tokens"), _dev_ptr(trie["tree_parent"], "tree_parent"),
+        _dev_ptr(trie["tree_len"], "tree_len"), _dev_ptr(gam, "gamma"), c, m, v, n_groups,
+        ctypes.byref(params), _dev_ptr(out["accept_len"], "out_accept_len"),
+        _dev_ptr(out["best"], "out_best"), _dev_ptr(out.get("gate_score"), "out_gate_score"),
+        _dev_ptr(out.get("masks"), "out_masks"), _dev_ptr(out.get("rank"), "out_rank"),
+        _dev_ptr(workspace, "workspace"), workspace.numel(), _stream_handle(stream)),
+        "sense_soft_gate_verify_tree")
+    return out

@@ -235,3 +235,53 @@ def make_pool(seed: int, n_queries: int, n: int, max_len: int, vocab: int,
     else:
         ln = torch.full((n_queries, n), max_len, dtype=torch.int32, device=device)
     return Pool(sc.float().contiguous(), dr.contiguous(), ln.contiguous())
+
+
+def make_drafts(seed: int, n_cand: int, m: int, vocab: int, device, p_share: float = 0.7,
+                ragged: bool = True, n_groups: int = 1):
+    """Draft batches with shared prefixes, as retrieved continuations of
+    neighbouring keys have: within each group, a draft copies the first
+    `cut` tokens (cut uniform in [0, M]) of an earlier draft of its group
+    with probability p_share; the rest are uniform ids.  Lengths uniform in
+    [0, M] when ragged.  Returns (drafts C x M int32, lengths C int32)."""
+    g = _gen(seed + 49979687, "cpu")
+    d = torch.randint(0, vocab, (n_cand, m), generator=g, dtype=torch.int32)
+    gs = n_cand // n_groups
+    share = torch.rand(n_cand, generator=g) < p_share
+    cut = torch.randint(0, m + 1, (n_cand,), generator=g)
+    pick = torch.rand(n_cand, generator=g)
+    for i in range(n_cand):
+        r = i % gs
+        if r > 0 and bool(share[i]):
+            src = i - r + int(pick[i] * r)
+            c = int(cut[i])
+            d[i, :c] = d[src, :c]
+    if ragged:
+        ln = torch.randint(0, m + 1, (n_cand,), generator=g, dtype=torch.int32)
+    else:
+        ln = torch.full((n_cand,), m, dtype=torch.int32)
+    return d.to(device), ln.to(device)
+
+
+def make_tree_logits(vocab: int, dtype: str, n_groups: int, nodes: int, tokens, parent, tree_len,
+                     seed: int, device, boost: float = 6.0, p_boost: float = 0.6,
+                     std: float = 2.0) -> torch.Tensor:
+    """Logits of a flattened tree, G x (1 + nodes) x V: rows ~ N(0, std^2);
+    for each tree node u, the row that judges it (1 + parent, row 0 at depth
+    0) gets +boost at u's token with probability p_boost.  tokens / parent
+    are G x nodes host arrays (node u of group g), tree_len the node counts."""
+    g = _gen(seed + 86028121, device)
+    x = torch.randn((n_groups, 1 + nodes, vocab), generator=g, device=device).mul_(std)
+    hit = torch.rand((n_groups, nodes), generator=g, device=device).cpu()
+    gi_l, row_l, tok_l = [], [], []
+    for gi in range(n_groups):
+        for u in range(int(tree_len[gi])):
+            tok = int(tokens[gi][u])
+            if 0 <= tok < vocab and float(hit[gi, u]) < p_boost:
+                gi_l.append(gi)
+                row_l.append(1 + int(parent[gi][u]))
+                tok_l.append(tok)
+    if gi_l:
+        idx = tuple(torch.tensor(a, dtype=torch.int64, device=device) for a in (gi_l, row_l, tok_l))
+        x.index_put_(idx, torch.full((len(gi_l),), boost, device=device), accumulate=True)
+    return x.to(DTYPES[dtype]).contiguous()

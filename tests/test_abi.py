@@ -251,4 +251,95 @@ def test_select_rejects(lib, kw, status):
 
 def test_timer_ids(lib):
     assert lib.sense_set_timer_events(sense.SENSE_TIMER_SELECT, None, None) == 0
-    assert lib.sense_set_timer_events(4, None, None) == INVALID
+    assert lib.sense_set_timer_events(sense.SENSE_TIMER_TRIE, None, None) == 0
+    assert lib.sense_set_timer_events(5, None, None) == INVALID
+
+
+def trie_desc(**kw):
+    base = dict(order=p(FAKE), gamma=p(FAKE), tree_tokens=p(FAKE), tree_parent=p(FAKE),
+                tree_depth=p(FAKE), tree_cand=p(FAKE), tree_len=p(FAKE), sorted_drafts=None,
+                sorted_len=None, mask=None, mask_ld=0, full_mask=None, full_mask_dtype=0,
+                prefix_len=0, cache_len=0)
+    base.update(kw)
+    return sense.TrieDesc(**base)
+
+
+@pytest.mark.parametrize("args,kw,status", [
+    (dict(n_cand=0), {}, INVALID),
+    (dict(max_len=0), {}, INVALID),
+    (dict(max_len=65), {}, INVALID),
+    (dict(n_groups=3), {}, INVALID),                 # 64 % 3 != 0
+    (dict(n_groups=0), {}, INVALID),
+    (dict(n_cand=2048, n_groups=1, max_len=1), {}, UNSUPPORTED),   # > 1024 drafts
+    (dict(n_cand=128, max_len=64), {}, UNSUPPORTED),               # > 4096 tokens
+    (dict(drafts=None), {}, INVALID),
+    ({}, dict(order=None), INVALID),
+    ({}, dict(gamma=None), INVALID),
+    ({}, dict(tree_tokens=None), INVALID),
+    ({}, dict(tree_parent=None), INVALID),
+    ({}, dict(tree_depth=None), INVALID),
+    ({}, dict(tree_cand=None), INVALID),
+    ({}, dict(tree_len=None), INVALID),
+    ({}, dict(mask=p(FAKE), mask_ld=100), INVALID),               # < 512 nodes
+    ({}, dict(full_mask=p(FAKE), full_mask_dtype=9, cache_len=10), INVALID),
+    ({}, dict(full_mask=p(FAKE), full_mask_dtype=0, cache_len=0), INVALID),
+    ({}, dict(full_mask=p(FAKE), full_mask_dtype=0, prefix_len=-1, cache_len=10), INVALID),
+    ({}, dict(full_mask=p(FAKE + 2), full_mask_dtype=0, cache_len=10), MISALIGNED),
+])
+def test_trie_rejects(lib, args, kw, status):
+    a = dict(drafts=p(FAKE), dl=None, n_cand=64, max_len=8, n_groups=1)
+    a.update(args)
+    d = trie_desc(**kw)
+    assert lib.sense_build_loose_trie(a["drafts"], a["dl"], a["n_cand"], a["max_len"],
+                                      a["n_groups"], ctypes.byref(d), None) == status
+    assert lib.sense_last_error_message()
+    assert lib.sense_build_loose_trie(p(FAKE), None, 64, 8, 1, None, None) == INVALID
+
+
+def tree_verify_call(lib, **kw):
+    a = dict(logits=p(FAKE), dtype=0, row_stride=1000, tok=p(FAKE), par=p(FAKE), tl=p(FAKE),
+             gam=p(FAKE), n_cand=8, max_len=8, vocab=1000, n_groups=1,
+             params=sense.GateParams(gamma=0.05, topk=3, window=6, tau=0, entropy_normalized=1),
+             acc=p(FAKE), best=p(FAKE), ws=p(FAKE), ws_bytes=1 << 30)
+    a.update(kw)
+    prm = a["params"]
+    return lib.sense_soft_gate_verify_tree(
+        a["logits"], a["dtype"], a["row_stride"], a["tok"], a["par"], a["tl"], a["gam"],
+        a["n_cand"], a["max_len"], a["vocab"], a["n_groups"],
+        None if prm is None else ctypes.byref(prm), a["acc"], a["best"], None, None, None,
+        a["ws"], a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(params=None), INVALID),
+    (dict(n_cand=-1), INVALID),
+    (dict(max_len=0), INVALID),
+    (dict(vocab=0), INVALID),
+    (dict(row_stride=999), INVALID),
+    (dict(dtype=5), INVALID),
+    (dict(n_groups=3), INVALID),
+    (dict(n_cand=2048, max_len=1), UNSUPPORTED),
+    (dict(logits=None), INVALID),
+    (dict(tok=None), INVALID),
+    (dict(par=None), INVALID),
+    (dict(tl=None), INVALID),
+    (dict(gam=None), INVALID),
+    (dict(acc=None), INVALID),
+    (dict(best=None), INVALID),
+    (dict(ws=None), WORKSPACE),
+    (dict(ws_bytes=16), WORKSPACE),
+    (dict(ws=p(FAKE + 64)), MISALIGNED),
+    (dict(logits=p(FAKE + 2)), MISALIGNED),
+])
+def test_tree_verify_rejects(lib, kw, status):
+    assert tree_verify_call(lib, **kw) == status
+    assert lib.sense_last_error_message()
+
+
+def test_tree_verify_empty_and_workspace(lib):
+    assert tree_verify_call(lib, n_cand=0, logits=None, tok=None, ws=None) == 0
+    size = ctypes.c_size_t()
+    assert lib.sense_soft_gate_verify_tree_workspace_size(64, 8, 152064, 1, ctypes.byref(size)) == 0
+    assert size.value >= 64 * 8 * 16
+    assert lib.sense_soft_gate_verify_tree_workspace_size(64, 8, 100, 3,
+                                                         ctypes.byref(size)) == INVALID
