@@ -6,7 +6,10 @@ One step = one sense_retrieve over the whole datastore (similarity scan,
 top-k, gather of the continuations) followed by one sense_soft_gate_verify
 of the retrieved drafts of the verified queries against their aligned
 logits.  Inputs are synthetic (see paper_2606_00021_amd/synth.py) and
-resident in HBM before the timed region starts.
+resident in HBM before the timed region starts.  The "sen" object times the
+method's full drafting step apart from it: static and dynamic-cache
+retrieval, composite Top-N selection, the loose trie and verification
+through it.
 
 Prints ONE JSON line on stdout; progress goes to stderr.
 """
@@ -133,57 +136,82 @@ def cpu_baseline(w, ds, q, logits, drafts, budget_s: float):
     }
 
 
-def sen_leg(args, w, ds, q, src_rows, index, ws_r, outs, K, dev):
-    """Candidate-selection extension of the step, timed apart from the headline
-    step: static retrieval (k hits), dynamic-cache retrieval over a
-    generation context, composite Top-N (alpha 100, beta 1, delta 0.05, the
-    anchor override) and verification of the N selected drafts.  Also times
-    the selection kernel alone, the dynamic retrieval alone and one cache
-    append of 4 accepted positions."""
+def sen_leg(args, w, ds, q, src_rows, K, dev):
+    """The paper's full drafting + verification step, timed apart from the
+    headline step: static retrieval (k hits) over the same keys with
+    continuations that overlap between neighbours, dynamic-cache retrieval
+    over a generation context, composite Top-N (alpha 100, beta 1, delta 0.05,
+    anchor override), LexSort + loose trie of the N drafts, and verification
+    through Gamma.  Also times each stage alone, the dense verification of
+    the same drafts (one logits row per draft position) and one cache append
+    of 4 accepted positions."""
     import torch
 
     from paper_2606_00021_amd import sense, synth
 
     k, m, nq = w.k, w.span, w.n_queries
     k_dyn, top_n, ctx_len = 16, w.k, args.sen_context
-    anchors = ds.spans[src_rows, 0].to(torch.int32).contiguous()
+    spans = synth.make_shared_spans(w, ds, args.seed)
+    index = sense.sense_build_index(ds.keys, spans, None, metric=w.metric)
+    anchors = spans[src_rows, 0].to(torch.int32).contiguous()
     ctx = synth.make_context(w, ds, args.seed, ctx_len, int(src_rows[0]), int(anchors[0]))
     kdt = synth.DTYPES[w.key_dtype]
     cache = sense.sense_build_dynamic_index(w.d, ctx_len, m, key_dtype=kdt, metric=w.metric)
     sense.sense_index_append(cache, ctx.keys, ctx.tokens)
+
+    def retr_bufs(kk):
+        return (torch.empty((nq, kk), dtype=torch.int64, device=dev),
+                torch.empty((nq, kk), dtype=torch.float32, device=dev),
+                torch.empty((nq, kk, m), dtype=torch.int32, device=dev),
+                torch.empty((nq, kk), dtype=torch.int32, device=dev))
+    ws_s = torch.empty(max(1, sense.sense_retrieve_workspace_size(index, nq, k)),
+                       dtype=torch.uint8, device=dev)
     ws_d = torch.empty(max(1, sense.sense_retrieve_workspace_size(cache, nq, k_dyn)),
                        dtype=torch.uint8, device=dev)
-    outs_d = (torch.empty((nq, k_dyn), dtype=torch.int64, device=dev),
-              torch.empty((nq, k_dyn), dtype=torch.float32, device=dev),
-              torch.empty((nq, k_dyn, m), dtype=torch.int32, device=dev),
-              torch.empty((nq, k_dyn), dtype=torch.int32, device=dev))
+    outs_s, outs_d = retr_bufs(k), retr_bufs(k_dyn)
     sel = (torch.empty((nq, top_n, m), dtype=torch.int32, device=dev),
            torch.empty((nq, top_n), dtype=torch.int32, device=dev),
            torch.empty((nq, top_n), dtype=torch.int32, device=dev),
            torch.empty((nq, top_n), dtype=torch.float32, device=dev))
     vq = w.verify_queries
     c = vq * top_n
+    drafts = sel[0][:vq].view(c, m)
+    dlen = sel[1][:vq].view(c)
 
-    def retrieve_select():
-        sense.sense_retrieve(index, q, k, workspace=ws_r, out=outs)
+    def draft_stage():
+        sense.sense_retrieve(index, q, k, workspace=ws_s, out=outs_s)
         sense.sense_retrieve(cache, q, k_dyn, workspace=ws_d, out=outs_d)
-        sense.sense_select_candidates((outs[1], outs[2], outs[3]),
+        sense.sense_select_candidates((outs_s[1], outs_s[2], outs_s[3]),
                                       (outs_d[1], outs_d[2], outs_d[3]), anchors, top_n,
                                       100.0, 1.0, 0.05, True, out=sel)
 
-    retrieve_select()
-    drafts = sel[0][:vq].view(c, m)
-    dlen = sel[1][:vq].view(c)
-    logits = synth.make_logits(w, drafts, args.seed + 1)
-    ws_v = torch.empty(max(1, sense.sense_soft_gate_verify_workspace_size(c, m, w.vocab)),
+    draft_stage()
+    tr = sense.sense_build_loose_trie(drafts, dlen, n_groups=vq)
+    torch.cuda.synchronize()
+    nodes = top_n * m
+    tl = tr["tree_len"].cpu().numpy()
+    logits = synth.make_tree_logits(w.vocab, w.logits_dtype, vq, nodes,
+                                    tr["tree_tokens"].cpu().numpy(),
+                                    tr["tree_parent"].cpu().numpy(), tl, args.seed + 1, dev)
+    ws_v = torch.empty(max(1, sense.sense_soft_gate_verify_tree_workspace_size(c, m, w.vocab, vq)),
                        dtype=torch.uint8, device=dev)
     out_v = {"accept_len": torch.empty(c, dtype=torch.int32, device=dev),
              "best": torch.empty(vq, dtype=torch.int32, device=dev)}
+    # Dense comparison: the same aligned rows copied out, one per position.
+    gam = tr["gamma"].long().view(vq, top_n, m)
+    rows = torch.zeros_like(gam)
+    rows[..., 1:] = torch.where(gam[..., :-1] >= 0, gam[..., :-1] + 1, torch.zeros_like(gam[..., :-1]))
+    dense = torch.stack([logits[g][rows[g]] for g in range(vq)]).view(c, m, w.vocab).contiguous()
+    sdr, sln = tr["sorted_drafts"], tr["sorted_len"]
+    ws_dv = torch.empty(max(1, sense.sense_soft_gate_verify_workspace_size(c, m, w.vocab)),
+                        dtype=torch.uint8, device=dev)
+    out_dv = {"accept_len": torch.empty(c, dtype=torch.int32, device=dev),
+              "best": torch.empty(vq, dtype=torch.int32, device=dev)}
 
     def step():
-        retrieve_select()
-        sense.sense_soft_gate_verify(logits, drafts, dlen, n_groups=vq, workspace=ws_v,
-                                     out=out_v)
+        draft_stage()
+        sense.sense_build_loose_trie(drafts, dlen, n_groups=vq, out=tr)
+        sense.sense_soft_gate_verify_tree(logits, tr, n_groups=vq, workspace=ws_v, out=out_v)
 
     def timed(fn, reps):
         for _ in range(3):
@@ -198,21 +226,68 @@ def sen_leg(args, w, ds, q, src_rows, index, ws_r, outs, K, dev):
         return a.elapsed_time(b) / reps
 
     ms_step = timed(step, K)
-    dyn_ms = timed(lambda: sense.sense_retrieve(cache, q, k_dyn, workspace=ws_d, out=outs_d), K)
-    sel_ms = timed(lambda: sense.sense_select_candidates(
-        (outs[1], outs[2], outs[3]), (outs_d[1], outs_d[2], outs_d[3]), anchors, top_n, 100.0,
-        1.0, 0.05, True, out=sel), K)
+
+    # Per-stage kernel durations: hipEvents recorded by the library around
+    # each stage's kernels (a second pass; the host's launch rate does not
+    # enter these, unlike back-to-back calls of one small stage).
+    def events():
+        pair = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+        for e in pair:
+            e.record()                       # creates the hipEvent
+        return pair
+    stages = ("dyn_scan", "dyn_topk", "select", "trie", "verify_tree", "verify_dense", "append")
+    ev = {t: [events() for _ in range(K)] for t in stages}
     grow = sense.sense_build_dynamic_index(w.d, 4 * (K + 3), m, key_dtype=kdt, metric=w.metric)
     new_keys, new_tok = ctx.keys[:4].contiguous(), ctx.tokens[:4].contiguous()
-    append_ms = timed(lambda: sense.sense_index_append(grow, new_keys, new_tok), K)
+    torch.cuda.synchronize()
+    T = sense
+    for i in range(K):
+        sense.sense_retrieve(index, q, k, workspace=ws_s, out=outs_s)
+        T.sense_set_timer_events(T.SENSE_TIMER_SCAN, *ev["dyn_scan"][i])
+        T.sense_set_timer_events(T.SENSE_TIMER_TOPK, *ev["dyn_topk"][i])
+        sense.sense_retrieve(cache, q, k_dyn, workspace=ws_d, out=outs_d)
+        T.sense_set_timer_events(T.SENSE_TIMER_SCAN, None, None)
+        T.sense_set_timer_events(T.SENSE_TIMER_TOPK, None, None)
+        T.sense_set_timer_events(T.SENSE_TIMER_SELECT, *ev["select"][i])
+        sense.sense_select_candidates((outs_s[1], outs_s[2], outs_s[3]),
+                                      (outs_d[1], outs_d[2], outs_d[3]), anchors, top_n,
+                                      100.0, 1.0, 0.05, True, out=sel)
+        T.sense_set_timer_events(T.SENSE_TIMER_TRIE, *ev["trie"][i])
+        sense.sense_build_loose_trie(drafts, dlen, n_groups=vq, out=tr)
+        T.sense_set_timer_events(T.SENSE_TIMER_VERIFY, *ev["verify_tree"][i])
+        sense.sense_soft_gate_verify_tree(logits, tr, n_groups=vq, workspace=ws_v, out=out_v)
+        T.sense_set_timer_events(T.SENSE_TIMER_VERIFY, *ev["verify_dense"][i])
+        sense.sense_soft_gate_verify(dense, sdr, sln, n_groups=vq, workspace=ws_dv, out=out_dv)
+        T.sense_set_timer_events(T.SENSE_TIMER_VERIFY, None, None)
+        a, b = ev["append"][i]
+        a.record()
+        sense.sense_index_append(grow, new_keys, new_tok)
+        b.record()
+    torch.cuda.synchronize()
+    for t in (T.SENSE_TIMER_SELECT, T.SENSE_TIMER_TRIE):
+        T.sense_set_timer_events(t, None, None)
+    dur = {t: sum(a.elapsed_time(b) for a, b in ev[t]) / K for t in stages}
+    dyn_ms = dur["dyn_scan"] + dur["dyn_topk"]
+    sel_ms, trie_ms = dur["select"], dur["trie"]
+    vt_ms, vd_ms, append_ms = dur["verify_tree"], dur["verify_dense"], dur["append"]
     grow.close()
+    L = int(tl.sum())
+    positions = int(sln.clamp(0, m).sum().item())
+    ebytes = 4 if w.logits_dtype == "f32" else 2
     cache.close()
-    log(f"[bench] SEN step {ms_step:.4f} ms (dynamic retrieval {dyn_ms * 1e3:.1f} us over "
-        f"{ctx_len} rows, selection {sel_ms * 1e3:.1f} us, append {append_ms * 1e3:.1f} us)")
+    index.close()
+    log(f"[bench] SEN step {ms_step:.4f} ms: dynamic retrieval {dyn_ms * 1e3:.1f} us over "
+        f"{ctx_len} rows, selection {sel_ms * 1e3:.1f} us, trie {trie_ms * 1e3:.1f} us "
+        f"({L} nodes for {positions} draft tokens), verify through the tree "
+        f"{vt_ms * 1e3:.1f} us vs dense {vd_ms * 1e3:.1f} us, append {append_ms * 1e3:.1f} us")
     return {"queries_per_s": nq / (ms_step * 1e-3), "ms_per_step": ms_step,
             "context_rows": ctx_len, "k_static": k, "k_dynamic": k_dyn, "top_n": top_n,
             "alpha": 100.0, "beta": 1.0, "delta": 0.05,
             "dynamic_retrieve_us": dyn_ms * 1e3, "select_us": sel_ms * 1e3,
+            "trie_us": trie_ms * 1e3, "tree_nodes": L, "draft_tokens": positions,
+            "tree_fraction": L / max(positions, 1),
+            "verify_tree_us": vt_ms * 1e3, "verify_dense_us": vd_ms * 1e3,
+            "verify_tree_gbps": L * w.vocab * ebytes / (vt_ms * 1e-3) / 1e9,
             "append4_us": append_ms * 1e3}
 
 
@@ -370,7 +445,7 @@ def main():
             f"written by one copy kernel")
         del src, dst
     if not args.no_sen:
-        res["sen"] = sen_leg(args, w, ds, q, src_rows, index, ws_r, outs, K, dev)
+        res["sen"] = sen_leg(args, w, ds, q, src_rows, K, dev)
     if not args.no_cpu_baseline:
         log("[bench] timing the oracle on the host (cpu_baseline)")
         t0 = time.perf_counter()

@@ -285,3 +285,23 @@ def make_tree_logits(vocab: int, dtype: str, n_groups: int, nodes: int, tokens, 
         idx = tuple(torch.tensor(a, dtype=torch.int64, device=device) for a in (gi_l, row_l, tok_l))
         x.index_put_(idx, torch.full((len(gi_l),), boost, device=device), accumulate=True)
     return x.to(DTYPES[dtype]).contiguous()
+
+
+def make_shared_spans(w: Workload, ds: Datastore, seed: int, phrases: int = 4,
+                      p_diverge: float = 0.25) -> torch.Tensor:
+    """Continuations that overlap between neighbours, as text retrieved for
+    similar hidden states does: each cluster has `phrases` base
+    continuations; a row takes one of its cluster's phrases and, from a
+    position onwards where each position diverges with probability
+    p_diverge, uniform ids instead.  Returns n x M int32 (same device)."""
+    device = ds.keys.device
+    g = _gen(seed + 67867967, device)
+    base = torch.randint(0, w.vocab, (w.n_clusters, phrases, w.span), generator=g, device=device,
+                         dtype=torch.int32)
+    pick = torch.randint(0, phrases, (w.n,), generator=g, device=device)
+    # first diverging position ~ geometric(p_diverge), by inversion
+    u = torch.rand(w.n, generator=g, device=device).clamp_min(1e-12)
+    first = torch.floor(torch.log(u) / torch.log(torch.tensor(1.0 - p_diverge))).long()
+    div = torch.arange(w.span, device=device)[None, :] >= first[:, None]
+    rnd = torch.randint(0, w.vocab, (w.n, w.span), generator=g, device=device, dtype=torch.int32)
+    return torch.where(div, rnd, base[ds.assign, pick]).contiguous()

@@ -15,6 +15,7 @@ import pytest
 import torch
 
 import oracle
+from oracle import trie as otrie
 from paper_2606_00021_amd import sense, synth
 from parity import REL_TIE, check_topk, check_verify, dt_name, host_bits
 
@@ -284,5 +285,24 @@ def test_sen_chain(wname, scale, ctx_len, k_dyn, top_n):
     torch.cuda.synchronize()
     ref = oracle.soft_gate_verify(host_bits(logits), dt_name(logits), o_dr, o_ln)
     check_verify(out, ref, 0.05, o_ln)
+
+    # the paper's route: LexSort + loose trie of the pool, one logits row per
+    # tree node, verification through Gamma
+    tr = sense.sense_build_loose_trie(dr[0].contiguous(), ln[0].contiguous())
+    order = otrie.lexsort_candidates(o_dr, o_ln)
+    S, SL = o_dr[order], o_ln[order]
+    T, gam, _ = otrie.loose_trie(S, SL)
+    parent, _, _ = otrie.node_table(gam)
+    nodes = top_n * w.span
+    pad = -np.ones(nodes - T.shape[0], dtype=np.int64)
+    tl = synth.make_tree_logits(w.vocab, w.logits_dtype, 1, nodes, [np.r_[T, pad]],
+                                [np.r_[parent, pad]], [T.shape[0]], 12, DEV)
+    out_t = sense.sense_soft_gate_verify_tree(tl, tr)
+    torch.cuda.synchronize()
+    assert np.array_equal(tr["order"].cpu().numpy(), order)
+    assert np.array_equal(tr["gamma"].cpu().numpy(), gam)
+    ref_t = oracle.soft_gate_verify(otrie.aligned_logits(host_bits(tl)[0], gam), dt_name(tl),
+                                    S.astype(np.int32), np.clip(SL, 0, w.span).astype(np.int32))
+    check_verify(out_t, ref_t, 0.05, np.clip(SL, 0, w.span))
     index.close()
     cache.close()
