@@ -178,9 +178,19 @@ def sen_leg(args, w, ds, q, src_rows, K, dev):
     drafts = sel[0][:vq].view(c, m)
     dlen = sel[1][:vq].view(c)
 
+    # The dynamic search is independent of the static one: it runs on a
+    # second stream (default priority) while the static scan streams HBM.
+    side = torch.cuda.Stream()
+    fork, join = torch.cuda.Event(), torch.cuda.Event()
+
     def draft_stage():
+        main_stream = torch.cuda.current_stream()
+        fork.record(main_stream)
+        side.wait_event(fork)
+        sense.sense_retrieve(cache, q, k_dyn, workspace=ws_d, out=outs_d, stream=side)
+        join.record(side)
         sense.sense_retrieve(index, q, k, workspace=ws_s, out=outs_s)
-        sense.sense_retrieve(cache, q, k_dyn, workspace=ws_d, out=outs_d)
+        main_stream.wait_event(join)
         sense.sense_select_candidates((outs_s[1], outs_s[2], outs_s[3]),
                                       (outs_d[1], outs_d[2], outs_d[3]), anchors, top_n,
                                       100.0, 1.0, 0.05, True, out=sel)

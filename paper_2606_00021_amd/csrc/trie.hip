@@ -3,8 +3,10 @@
 //
 // trie_build: one block per candidate group (at most 1024 drafts and 4096
 //   draft tokens, all held in LDS):
-//     1. LexSort: a bitonic sort of the draft indices by their token
-//        sequences (a proper prefix first, identical drafts by index);
+//     1. LexSort of the draft indices by their token sequences (a proper
+//        prefix first, identical drafts by index): groups of up to 256
+//        drafts place each draft at the count of drafts before it (all
+//        pairs in one round), larger ones use a bitonic network;
 //     2. prefix detection: sorted draft r position j repeats draft r-1 when
 //        both exist and every token up to j is equal (the running product
 //        along the row);
@@ -27,6 +29,7 @@ namespace {
 
 constexpr int kTrieThreads = 1024;
 constexpr int kTriePer = kMaxNodes / kTrieThreads;   // elements per thread (4)
+constexpr int kRankSortMax = 256;   // groups up to this size are ranked by counting
 
 // Draft a sorts before draft b: lexicographic on the sequences, then index.
 // Indices >= n are padding and sort after every draft.
@@ -70,7 +73,30 @@ __global__ __launch_bounds__(kTrieThreads) void trie_build_kernel(
     }
     __syncthreads();
 
-    // 1. LexSort (ascending bitonic network over p entries).
+    // 1. LexSort.  Small groups: every draft's place is the number of drafts
+    //    before it (all pairs compared at once, one round).  Larger groups:
+    //    an ascending bitonic network over p entries.
+    if (gs <= kRankSortMax) {
+        for (int r = tid; r < gs; r += kTrieThreads) s_idx[r] = 0;
+        __syncthreads();
+        const int pairs = gs * gs;
+        const int per = (pairs + kTrieThreads - 1) / kTrieThreads;
+        int a_cur = -1, cnt = 0;
+        for (int t = tid * per; t < pairs && t < (tid + 1) * per; ++t) {
+            const int a = t / gs, b = t - a * gs;
+            if (a != a_cur) {
+                if (cnt) atomicAdd(&s_idx[a_cur], cnt);
+                a_cur = a;
+                cnt = 0;
+            }
+            cnt += (b != a && lex_less(b, a, gs, m, s_d, s_len)) ? 1 : 0;
+        }
+        if (cnt) atomicAdd(&s_idx[a_cur], cnt);
+        __syncthreads();
+        for (int r = tid; r < gs; r += kTrieThreads) s_perm[s_idx[r]] = r;
+        __syncthreads();
+        p = 1;                           // the network below is skipped
+    }
     for (int size = 2; size <= p; size <<= 1) {
         for (int stride = size >> 1; stride > 0; stride >>= 1) {
             for (int i = tid; i < (p >> 1); i += kTrieThreads) {
