@@ -62,8 +62,9 @@ def _load():
         ]
         lib.oracle_select_candidates.argtypes = [P, P, P, I32, P, P, P, I32, I32, I32, I32, D, D,
                                                  D, I32, I32, P, P, P, P]
+        lib.oracle_project.argtypes = [P, ctypes.c_int, I64, I32, I64, P, P, I32, I32, P]
         for f in ("oracle_scores", "oracle_topk", "oracle_gather", "oracle_row_stats",
-                  "oracle_soft_gate_verify", "oracle_select_candidates"):
+                  "oracle_soft_gate_verify", "oracle_select_candidates", "oracle_project"):
             getattr(lib, f).restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -212,6 +213,26 @@ def select_candidates(scores_s, drafts_s, len_s, anchor: int, top_n: int, alpha:
     if rc:
         raise ValueError("oracle_select_candidates rejected its arguments")
     return out_dr, out_len, out_src, out_sc
+
+
+def project(x, x_dtype: str, basis, mean=None, normalize: bool = True,
+            x_stride: int | None = None, d_in: int | None = None) -> np.ndarray:
+    """PCA projection + optional L2 normalisation of the rows of x (Alg. 2's
+    L2Norm(PCA(h)); the datastore projection Z): (n, d_out) float64.  basis
+    is d_out x d_in (principal directions as rows), mean d_in or None."""
+    x = _raw(x, x_dtype)
+    basis = np.ascontiguousarray(basis, dtype=np.float64)
+    d_out, din = basis.shape
+    d_in = din if d_in is None else d_in
+    stride = x.shape[-1] if x_stride is None else x_stride
+    n = x.size // stride
+    mean = None if mean is None else np.ascontiguousarray(mean, dtype=np.float64)
+    out = np.empty((n, d_out), dtype=np.float64)
+    rc = _load().oracle_project(_ptr(x), DTYPES[x_dtype], n, d_in, stride, _ptr(mean),
+                                _ptr(basis), d_out, int(bool(normalize)), _ptr(out))
+    if rc:
+        raise ValueError("oracle_project rejected its arguments")
+    return out
 
 
 def dynamic_spans(tokens, max_span: int):

@@ -450,3 +450,42 @@ int oracle_select_candidates(const double *scores_s, const int32_t *drafts_s,
     free(c);
     return 0;
 }
+
+/* ---------------------------------------------------------------- projection */
+
+/* Query / key construction of Alg. 2 (k = L2Norm(PCA(h))) and the datastore
+ * projection Z of Sec. 3.2 Eq. 6 with the PCA of the implementation details:
+ *   out[i][o] = sum_t (x[i][t] - mean[t]) * basis[o][t]   (mean NULL = 0)
+ * then, if normalize, out[i] /= ||out[i]|| (a zero row stays zero).
+ * x is n x d_in of x_dtype with row stride x_stride; basis is d_out x d_in
+ * fp64 (the principal directions as rows); mean d_in fp64.  Sums in element
+ * order, in double precision. */
+int oracle_project(const void *x, int x_dtype, int64_t n, int32_t d_in, int64_t x_stride,
+                   const double *mean, const double *basis, int32_t d_out, int32_t normalize,
+                   double *out)
+{
+    if (!x || !basis || !out || !dtype_ok(x_dtype) || n < 0 || d_in < 1 || d_out < 1 ||
+        x_stride < d_in)
+        return -1;
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; ++i) {
+        double *row = out + i * d_out;
+        for (int32_t o = 0; o < d_out; ++o) {
+            double s = 0.0;
+            for (int32_t t = 0; t < d_in; ++t) {
+                double c = elem(x, x_dtype, i * x_stride + t) - (mean ? mean[t] : 0.0);
+                s += c * basis[(int64_t)o * d_in + t];
+            }
+            row[o] = s;
+        }
+        if (normalize) {
+            double nn = 0.0;
+            for (int32_t o = 0; o < d_out; ++o) nn += row[o] * row[o];
+            if (nn > 0.0) {
+                double inv = 1.0 / sqrt(nn);
+                for (int32_t o = 0; o < d_out; ++o) row[o] *= inv;
+            }
+        }
+    }
+    return 0;
+}
