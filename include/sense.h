@@ -34,6 +34,10 @@
  *                           soft-gated evaluation reading the flattened
  *                           tree's logits through Gamma (Sec. 3.2 Eq. 11;
  *                           Sec. 3.3; Alg. 4)
+ *   sense_project           PCA projection + L2 normalisation of hidden
+ *                           states: the query k = L2Norm(PCA(h)) of Alg. 2
+ *                           and the projected datastore keys (Sec. 3.2
+ *                           Eq. 6; App. implementation details)
  *
  * Conventions shared by every entry point
  *   - Pointers named keys, spans, span_len, queries, logits, drafts,
@@ -93,7 +97,9 @@ typedef struct sense_index sense_index_t; /* opaque host handle */
  *              base must be 16-byte aligned and key_stride % 8 == 0.
  *   n          number of rows, 1 <= n <= 2^31 - 1.
  *   d          key dimension, 1 <= d <= 8192 (the hidden sizes of the target
- *              models); d % 8 == 0.
+ *              models, or a projected dimension such as 64); d % 8 == 0.
+ *              Keys of d <= 64 are scanned several rows per load
+ *              instruction.
  *   key_stride elements between consecutive rows, >= d.
  *   spans      N x max_span int32 token ids: row i is the continuation c_i
  *              stored with key i.  Borrowed.
@@ -437,6 +443,47 @@ sense_status_t sense_soft_gate_verify_tree(const void *logits, sense_dtype_t log
                                            int32_t *out_rank, void *workspace,
                                            size_t workspace_bytes, void *stream);
 
+/* A given PCA projection (the fit itself is not part of this library).
+ *   mean       d_in fp32 (DEVICE), the mean subtracted first, or NULL.
+ *   basis      d_out x d_in fp32 (DEVICE), row-major: row o is the o-th
+ *              principal direction.
+ *   d_in       1 <= d_in <= 8192, d_in % 8 == 0.
+ *   d_out      1 <= d_out <= 256.
+ *   normalize  1: L2-normalise every projected row (a zero row stays zero). */
+typedef struct {
+    const float *mean;
+    const float *basis;
+    int32_t d_in;
+    int32_t d_out;
+    int32_t normalize;
+} sense_projection_t;
+
+/* Bytes of device workspace sense_project needs (0 when none). */
+sense_status_t sense_project_workspace_size(const sense_projection_t *proj,
+                                            sense_dtype_t x_dtype, int64_t n_rows,
+                                            size_t *bytes);
+
+/* Projection (Alg. 2: k = L2Norm(PCA(h)); Sec. 3.2 Eq. 6's Z applied to the
+ * datastore keys; App. implementation details: 4096 -> 64 dims, then
+ * L2-normalised):
+ *   out[i][o] = sum_t (x[i][t] - mean[t]) * basis[o][t], accumulated in
+ *   fp32, then out[i] /= ||out[i]|| if normalize, rounded to out_dtype
+ *   (nearest-even).
+ *   x          n_rows x d_in of x_dtype (F32, F16, BF16), row stride x_stride
+ *              >= d_in elements, element-aligned.
+ *   out        n_rows rows of out_stride >= d_out elements of out_dtype (F32,
+ *              F16 or BF16); only the first d_out of each row are written.
+ * 16-bit rows that are 16-byte aligned with x_stride % 8 == 0, 256 rows or
+ * more, run as a matrix-core contraction (the basis split into a hi and a lo
+ * half of the key type, ~16 mantissa bits for bf16, ~22 for fp16); other
+ * inputs run one block per row in fp32.  Needs workspace (256-byte aligned,
+ * sense_project_workspace_size bytes) only on the matrix-core route.
+ * Errors: INVALID_ARGUMENT, MISALIGNED, WORKSPACE, HIP. */
+sense_status_t sense_project(const sense_projection_t *proj, const void *x,
+                             sense_dtype_t x_dtype, int64_t n_rows, int64_t x_stride, void *out,
+                             sense_dtype_t out_dtype, int64_t out_stride, void *workspace,
+                             size_t workspace_bytes, void *stream);
+
 /* Diagnostics for benchmarks and profilers.  Which part of the path a pair
  * of timing events brackets. */
 typedef enum {
@@ -444,7 +491,8 @@ typedef enum {
     SENSE_TIMER_TOPK = 1,   /* top-k selection + gather kernels of sense_retrieve */
     SENSE_TIMER_VERIFY = 2, /* both kernels of sense_soft_gate_verify(_tree) */
     SENSE_TIMER_SELECT = 3, /* the kernel of sense_select_candidates */
-    SENSE_TIMER_TRIE = 4    /* the kernels of sense_build_loose_trie */
+    SENSE_TIMER_TRIE = 4,   /* the kernels of sense_build_loose_trie */
+    SENSE_TIMER_PROJECT = 5 /* the kernels of sense_project */
 } sense_timer_t;
 
 /* Register two hipEvent_t handles (created by the caller with timing

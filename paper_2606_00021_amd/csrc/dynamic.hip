@@ -28,21 +28,6 @@ __device__ inline float load_as_float(const void* p, int dt, int64_t i) {
     return f;
 }
 
-// Round-to-nearest-even of a binary32 value into the key encoding; NaN stays
-// a quiet NaN.  Exact for values that are already representable.
-__device__ inline uint16_t store_bits(float f, int dt) {
-    if (dt == DT_F16) {
-        const _Float16 h = (_Float16)f;
-        uint16_t b;
-        __builtin_memcpy(&b, &h, 2);
-        return b;
-    }
-    uint32_t u;
-    __builtin_memcpy(&u, &f, 4);
-    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (uint16_t)((u >> 16) | 0x40u);
-    return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
-}
-
 // Block b appends row n_old + b: its key (converted to the key type) and
 // token.  Block 0 also refreshes the lengths of the M - 1 rows before n_old.
 __global__ __launch_bounds__(kAppendThreads) void append_rows_kernel(
@@ -53,7 +38,7 @@ __global__ __launch_bounds__(kAppendThreads) void append_rows_kernel(
     const int64_t row = n_old + b;
     uint16_t* dst = keys + row * d;
     for (int t = threadIdx.x; t < d; t += kAppendThreads)
-        dst[t] = store_bits(load_as_float(src, src_dtype, b * d + t), key_dtype);
+        dst[t] = to_bits16(load_as_float(src, src_dtype, b * d + t), key_dtype);
     if (threadIdx.x == 0) {
         hist[row] = tokens[b];
         const int64_t left = n_new - row;

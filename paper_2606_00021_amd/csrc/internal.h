@@ -23,6 +23,9 @@ constexpr int kSelectChunk = 8192;  // elements per top-k selection block
 constexpr int kMaxPool = 2048;      // largest static + dynamic candidate pool
 constexpr int kMaxGroup = 1024;     // largest candidate group of the loose trie
 constexpr int kMaxNodes = 4096;     // largest group x draft length of the loose trie
+constexpr int kMaxProjOut = 256;    // largest projected dimension
+constexpr int kProjMfmaMinRows = 256;   // 16-bit projections of this many rows use MFMA
+constexpr int kSmallDim = 64;       // keys this short use the short-row scan
 
 // Order-preserving map of an fp32 score to an unsigned key: larger score ->
 // larger key; every NaN -> 0 (below everything); -0 is folded onto +0.
@@ -46,6 +49,21 @@ __host__ __device__ inline uint64_t pack_key(float s, uint32_t row) {
 }
 __host__ __device__ inline uint32_t key_row(uint64_t k) {
     return 0xFFFFFFFFu - (uint32_t)(k & 0xFFFFFFFFu);
+}
+
+// Round-to-nearest-even of a binary32 value into binary16 (dt = DT_F16) or
+// bfloat16 bits; NaN stays a quiet NaN.  Exact for representable values.
+__device__ inline uint16_t to_bits16(float f, int dt) {
+    if (dt == DT_F16) {
+        const _Float16 h = (_Float16)f;
+        uint16_t b;
+        __builtin_memcpy(&b, &h, 2);
+        return b;
+    }
+    uint32_t u;
+    __builtin_memcpy(&u, &f, 4);
+    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (uint16_t)((u >> 16) | 0x40u);
+    return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
 }
 
 // Bitonic sort of s[0..p) (LDS) into descending order by the kT threads of
@@ -92,6 +110,20 @@ size_t scan_mfma_scratch_bytes(int nq, int d);
 hipError_t launch_scan_mfma(const void* keys, int key_dtype, int64_t n, int d, int64_t ld,
                             const float* queries, int nq, bool split, const float* inv_norm,
                             float* scores, void* scratch, hipStream_t stream);
+
+// Single-query scans of keys with d <= kSmallDim (several rows per load
+// instruction), one launch per query.
+hipError_t launch_scan_small(const void* keys, int key_dtype, int64_t n, int d, int64_t ld,
+                             const float* queries, int nq, const float* inv_norm, float* scores,
+                             hipStream_t stream);
+
+// PCA projection (+ L2 normalisation) of n rows; see project.hip.
+bool project_uses_mfma(int x_dtype, const void* x, int64_t x_stride, int64_t n);
+size_t project_workspace_bytes(int x_dtype, int64_t n, int d_in, int d_out);
+hipError_t launch_project(const void* x, int x_dtype, int64_t n, int d_in, int64_t x_stride,
+                          const float* mean, const float* basis, int d_out, int normalize,
+                          void* out, int out_dtype, int64_t out_stride, void* workspace,
+                          hipStream_t stream);
 
 // Plain streaming read of a device buffer (bandwidth probe).
 hipError_t launch_stream_read(const void* buf, size_t bytes, uint32_t* sink, hipStream_t stream);

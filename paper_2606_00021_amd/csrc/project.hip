@@ -1,0 +1,170 @@
+// PCA projection with L2 normalisation: Alg. 2's query k = L2Norm(PCA(h))
+// and the datastore projection Z of Sec. 3.2 Eq. 6 (the implementation
+// details project 4096-dim hidden states to 64 dims and L2-normalise them).
+//
+//   out[i][o] = sum_t (x[i][t] - mean[t]) * basis[o][t],  then row i / ||row i||
+//
+// Two routes:
+//   * many 16-bit rows (building a projected datastore) is a dense
+//     contraction N x d_in x d_out: it runs on the matrix cores through the
+//     batched similarity kernel with the basis rows as the "queries" (fp32
+//     basis split into hi + lo halves of the key type), giving
+//     S[o][i] = x_i . w_o; then project_finish subtracts mean . w_o,
+//     normalises each row and stores it transposed in the output type;
+//   * a few rows (queries) or fp32 / unaligned rows: one block per row, the
+//     centred row staged in LDS, one wave per output with a fixed-order sum.
+#include "internal.h"
+
+namespace sense {
+namespace {
+
+constexpr int kProjThreads = 256;
+
+// Sum over the 64 lanes by an xor butterfly: every lane ends with the same
+// bits (each step adds the same two operands in every lane pair).
+__device__ __forceinline__ float wsum(float x) {
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) x += __shfl_xor(x, off, 64);
+    return x;
+}
+
+__device__ __forceinline__ float load_x(const void* p, int dt, int64_t i) {
+    if (dt == DT_F32) return ((const float*)p)[i];
+    const uint16_t b = ((const uint16_t*)p)[i];
+    if (dt == DT_F16) return (float)__builtin_bit_cast(_Float16, b);
+    return __builtin_bit_cast(float, (uint32_t)b << 16);
+}
+
+__device__ __forceinline__ void store_out(void* p, int dt, int64_t i, float v) {
+    if (dt == DT_F32) ((float*)p)[i] = v;
+    else ((uint16_t*)p)[i] = to_bits16(v, dt);
+}
+
+// centre[o] = mean . basis[o]  (one wave per output).
+__global__ __launch_bounds__(kProjThreads) void project_center_kernel(
+    const float* __restrict__ mean, const float* __restrict__ basis, int d_in, int d_out,
+    float* __restrict__ centre) {
+    const int lane = threadIdx.x & 63;
+    const int o = blockIdx.x * (kProjThreads / 64) + (threadIdx.x >> 6);
+    if (o >= d_out) return;
+    float a = 0.0f;
+    for (int t = lane; t < d_in; t += 64) a = __builtin_fmaf(mean[t], basis[(int64_t)o * d_in + t], a);
+    a = wsum(a);
+    if (lane == 0) centre[o] = a;
+}
+
+// Rows [i0, i0 + kFinRows) of S (d_out x n): subtract the centre, normalise,
+// store row-major in the output type.
+constexpr int kFinRows = 32;
+
+__global__ __launch_bounds__(kProjThreads) void project_finish_kernel(
+    const float* __restrict__ s, int64_t n, int d_out, const float* __restrict__ centre,
+    int normalize, void* __restrict__ out, int out_dtype, int64_t out_stride) {
+    __shared__ float tile[kFinRows * (kMaxProjOut + 1)];
+    const int ld = d_out + 1;
+    const int64_t i0 = (int64_t)blockIdx.x * kFinRows;
+    for (int idx = threadIdx.x; idx < kFinRows * d_out; idx += kProjThreads) {
+        const int o = idx / kFinRows, r = idx - o * kFinRows;
+        const int64_t i = i0 + r;
+        float v = 0.0f;
+        if (i < n) v = s[(int64_t)o * n + i] - (centre ? centre[o] : 0.0f);
+        tile[r * ld + o] = v;
+    }
+    __syncthreads();
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    for (int r = wv; r < kFinRows; r += kProjThreads / 64) {
+        const int64_t i = i0 + r;
+        if (i >= n) break;                               // uniform over the wave
+        float inv = 1.0f;
+        if (normalize) {
+            float ss = 0.0f;
+            for (int o = lane; o < d_out; o += 64) ss = __builtin_fmaf(tile[r * ld + o], tile[r * ld + o], ss);
+            ss = wsum(ss);
+            inv = (ss > 0.0f) ? 1.0f / __builtin_sqrtf(ss) : 0.0f;
+        }
+        for (int o = lane; o < d_out; o += 64)
+            store_out(out, out_dtype, i * out_stride + o, tile[r * ld + o] * inv);
+    }
+}
+
+// Direct route: one block per row.
+__global__ __launch_bounds__(kProjThreads) void project_rows_kernel(
+    const void* __restrict__ x, int x_dtype, int64_t x_stride, int d_in,
+    const float* __restrict__ mean, const float* __restrict__ basis, int d_out, int normalize,
+    void* __restrict__ out, int out_dtype, int64_t out_stride) {
+    __shared__ float xc[kMaxDim];
+    __shared__ float res[kMaxProjOut];
+    __shared__ float s_inv;
+    const int64_t i = blockIdx.x;
+    for (int t = threadIdx.x; t < d_in; t += kProjThreads)
+        xc[t] = load_x(x, x_dtype, i * x_stride + t) - (mean ? mean[t] : 0.0f);
+    __syncthreads();
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    for (int o = wv; o < d_out; o += kProjThreads / 64) {
+        const float* w = basis + (int64_t)o * d_in;
+        float a = 0.0f;
+        for (int t = lane; t < d_in; t += 64) a = __builtin_fmaf(xc[t], w[t], a);
+        a = wsum(a);
+        if (lane == 0) res[o] = a;
+    }
+    __syncthreads();
+    if (wv == 0) {
+        float ss = 0.0f;
+        for (int o = lane; o < d_out; o += 64) ss = __builtin_fmaf(res[o], res[o], ss);
+        ss = wsum(ss);
+        if (lane == 0) s_inv = normalize ? ((ss > 0.0f) ? 1.0f / __builtin_sqrtf(ss) : 0.0f) : 1.0f;
+    }
+    __syncthreads();
+    for (int o = threadIdx.x; o < d_out; o += kProjThreads)
+        store_out(out, out_dtype, i * out_stride + o, res[o] * s_inv);
+}
+
+}  // namespace
+
+bool project_uses_mfma(int x_dtype, const void* x, int64_t x_stride, int64_t n) {
+    return x_dtype != DT_F32 && n >= kProjMfmaMinRows && ((uintptr_t)x % 16) == 0 &&
+           x_stride % 8 == 0;
+}
+
+// Workspace: [centre (d_out fp32) | S (d_out x n fp32) | MFMA scratch].
+static size_t up256(size_t x) { return (x + 255) / 256 * 256; }
+
+size_t project_workspace_bytes(int x_dtype, int64_t n, int d_in, int d_out) {
+    if (x_dtype == DT_F32 || n < kProjMfmaMinRows) return 0;
+    return up256((size_t)d_out * sizeof(float)) + up256((size_t)d_out * n * sizeof(float)) +
+           up256(scan_mfma_scratch_bytes(d_out, d_in));
+}
+
+hipError_t launch_project(const void* x, int x_dtype, int64_t n, int d_in, int64_t x_stride,
+                          const float* mean, const float* basis, int d_out, int normalize,
+                          void* out, int out_dtype, int64_t out_stride, void* workspace,
+                          hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    if (!project_uses_mfma(x_dtype, x, x_stride, n)) {
+        hipLaunchKernelGGL(project_rows_kernel, dim3((unsigned)n), dim3(kProjThreads), 0, stream,
+                           x, x_dtype, x_stride, d_in, mean, basis, d_out, normalize, out,
+                           out_dtype, out_stride);
+        return hipGetLastError();
+    }
+    char* ws = (char*)workspace;
+    const size_t c_bytes = up256((size_t)d_out * sizeof(float));
+    float* centre = mean ? (float*)ws : nullptr;
+    float* s = (float*)(ws + c_bytes);
+    void* scratch = ws + c_bytes + up256((size_t)d_out * n * sizeof(float));
+    hipError_t e;
+    if (mean) {
+        hipLaunchKernelGGL(project_center_kernel,
+                           dim3((unsigned)((d_out + kProjThreads / 64 - 1) / (kProjThreads / 64))),
+                           dim3(kProjThreads), 0, stream, mean, basis, d_in, d_out, centre);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    if ((e = launch_scan_mfma(x, x_dtype, n, d_in, x_stride, basis, d_out, true, nullptr, s,
+                              scratch, stream)) != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(project_finish_kernel, dim3((unsigned)((n + kFinRows - 1) / kFinRows)),
+                       dim3(kProjThreads), 0, stream, s, n, d_out, centre, normalize, out,
+                       out_dtype, out_stride);
+    return hipGetLastError();
+}
+
+}  // namespace sense

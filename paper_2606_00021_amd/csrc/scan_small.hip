@@ -1,0 +1,169 @@
+// Single-query similarity scan for short keys (d <= 64), e.g. the 64-dim
+// PCA-projected datastore of the paper's implementation details (Sec. 3.2
+// Eq. 8 "sim"; Alg. 2's search step).
+//
+// A 64-dim bf16 row is 128 bytes, so a wave that gave every row all 64
+// lanes (the long-key GEMV) would leave 7 of 8 lanes idle.  Here LPR lanes
+// share a row (LPR = d/8 rounded up to a power of two, 16 bytes per lane),
+// one load instruction of the wave covers 64/LPR consecutive rows (1 KiB at
+// d = 64), and every lane keeps 8 loads in flight, so a wave streams 8 KiB
+// per iteration.  Each row's partials are summed across its LPR lanes with an
+// xor butterfly (every lane of the group gets the same bits), then the
+// scores are moved so that lane L holds row base + L and stored 64 at a time.
+#include "internal.h"
+
+namespace sense {
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+constexpr int kSmallLoads = 8;   // loads in flight per lane per iteration
+
+template <int KT>
+__device__ __forceinline__ float dot8(const u32x4& v, const float (&q)[8]) {
+    float a0 = 0.0f, a1 = 0.0f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+        const uint32_t u = v[w];
+        float lo, hi;
+        if constexpr (KT == DT_BF16) {
+            lo = __builtin_bit_cast(float, u << 16);
+            hi = __builtin_bit_cast(float, u & 0xFFFF0000u);
+        } else {
+            lo = (float)__builtin_bit_cast(_Float16, (uint16_t)(u & 0xFFFFu));
+            hi = (float)__builtin_bit_cast(_Float16, (uint16_t)(u >> 16));
+        }
+        a0 = __builtin_fmaf(lo, q[2 * w], a0);
+        a1 = __builtin_fmaf(hi, q[2 * w + 1], a1);
+    }
+    return a0 + a1;
+}
+
+template <int LPR>
+__device__ __forceinline__ float group_sum(float x) {
+#pragma unroll
+    for (int off = 1; off < LPR; off <<= 1) x += __shfl_xor(x, off, 64);
+    return x;
+}
+
+// One wave per contiguous run of rows_per_wave rows (a multiple of the rows
+// of one iteration, 512 / LPR).
+template <int KT, int LPR>
+__global__ __launch_bounds__(256) void scan_small_kernel(
+    const uint16_t* __restrict__ keys, int64_t ld, int64_t n, int d,
+    const float* __restrict__ query, const float* __restrict__ inv_norm,
+    float* __restrict__ scores, int64_t rows_per_wave) {
+    constexpr int RPI = 64 / LPR;                 // rows per load instruction
+    constexpr int RPIT = kSmallLoads * RPI;       // rows per iteration
+    constexpr int NG = RPIT / 64;                 // groups of 64 scores per iteration
+    const int lane = threadIdx.x & 63;
+    const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int64_t r0 = wave * rows_per_wave;
+    if (r0 >= n) return;
+    const int64_t r1 = (r0 + rows_per_wave < n) ? r0 + rows_per_wave : n;
+    const int g = lane / LPR, c = lane % LPR;
+    const int e = c * kLaneElems;
+    const bool col = e < d;
+
+    float q[8];
+    float qq = 0.0f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        q[i] = col ? query[e + i] : 0.0f;
+        qq = __builtin_fmaf(q[i], q[i], qq);
+    }
+    float inv_q = 1.0f;
+    if (inv_norm != nullptr) {
+        const float s = group_sum<LPR>(qq);
+        inv_q = (s > 0.0f) ? 1.0f / __builtin_sqrtf(s) : 0.0f;
+    }
+
+    for (int64_t base = r0; base < r1; base += RPIT) {
+        u32x4 buf[kSmallLoads];
+#pragma unroll
+        for (int u = 0; u < kSmallLoads; ++u) {
+            const int64_t row = base + u * RPI + g;
+            buf[u] = (col && row < r1)
+                         ? __builtin_nontemporal_load((const u32x4*)(keys + row * ld + e))
+                         : u32x4{0u, 0u, 0u, 0u};
+        }
+        float p[kSmallLoads];
+#pragma unroll
+        for (int u = 0; u < kSmallLoads; ++u) p[u] = group_sum<LPR>(dot8<KT>(buf[u], q));
+        // Row base + u*RPI + g sits in lanes g*LPR ... ; lane L of group k
+        // wants row base + 64k + L, i.e. u = k*LPR + L/RPI from lane
+        // (L % RPI) * LPR.
+        const int src = (lane % RPI) * LPR;
+#pragma unroll
+        for (int k = 0; k < NG; ++k) {
+            float mine = 0.0f;
+#pragma unroll
+            for (int j = 0; j < LPR; ++j) {
+                const float v = __shfl(p[k * LPR + j], src, 64);
+                if (lane / RPI == j) mine = v;
+            }
+            const int64_t i = base + (int64_t)k * 64 + lane;
+            if (i < r1) {
+                if (inv_norm != nullptr) mine = (mine * inv_norm[i]) * inv_q;
+                scores[i] = mine;
+            }
+        }
+    }
+}
+
+int g_cus = 0;
+
+template <int KT, int LPR>
+hipError_t launch_small_lpr(const void* keys, int64_t n, int d, int64_t ld, const float* query,
+                            const float* inv_norm, float* scores, hipStream_t stream) {
+    auto kern = scan_small_kernel<KT, LPR>;
+    static int per_cu = 0;
+    if (per_cu < 1 &&
+        (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, 256, 0) != hipSuccess ||
+         per_cu < 1))
+        per_cu = 2;
+    if (g_cus == 0) {
+        int dev = 0;
+        hipDeviceProp_t prop;
+        g_cus = (hipGetDevice(&dev) == hipSuccess &&
+                 hipGetDeviceProperties(&prop, dev) == hipSuccess && prop.multiProcessorCount > 0)
+                    ? prop.multiProcessorCount
+                    : 256;
+    }
+    constexpr int64_t rpit = kSmallLoads * (64 / LPR);
+    const int64_t max_waves = (int64_t)g_cus * per_cu * 4;
+    int64_t rpw = (n + max_waves - 1) / max_waves;
+    rpw = (rpw + rpit - 1) / rpit * rpit;
+    const int64_t waves = (n + rpw - 1) / rpw;
+    const int64_t blocks = (waves + 3) / 4;
+    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(256), 0, stream, (const uint16_t*)keys,
+                       ld, n, d, query, inv_norm, scores, rpw);
+    return hipGetLastError();
+}
+
+template <int KT>
+hipError_t launch_small(const void* keys, int64_t n, int d, int64_t ld, const float* query,
+                        const float* inv_norm, float* scores, hipStream_t stream) {
+    const int lanes = (d + kLaneElems - 1) / kLaneElems;
+    if (lanes <= 1) return launch_small_lpr<KT, 1>(keys, n, d, ld, query, inv_norm, scores, stream);
+    if (lanes <= 2) return launch_small_lpr<KT, 2>(keys, n, d, ld, query, inv_norm, scores, stream);
+    if (lanes <= 4) return launch_small_lpr<KT, 4>(keys, n, d, ld, query, inv_norm, scores, stream);
+    return launch_small_lpr<KT, 8>(keys, n, d, ld, query, inv_norm, scores, stream);
+}
+
+}  // namespace
+
+hipError_t launch_scan_small(const void* keys, int key_dtype, int64_t n, int d, int64_t ld,
+                             const float* queries, int nq, const float* inv_norm, float* scores,
+                             hipStream_t stream) {
+    for (int q = 0; q < nq; ++q) {
+        const float* qp = queries + (int64_t)q * d;
+        float* sp = scores + (int64_t)q * n;
+        const hipError_t e = (key_dtype == DT_BF16)
+                                 ? launch_small<DT_BF16>(keys, n, d, ld, qp, inv_norm, sp, stream)
+                                 : launch_small<DT_F16>(keys, n, d, ld, qp, inv_norm, sp, stream);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+}  // namespace sense

@@ -39,7 +39,7 @@ namespace {
 thread_local char g_msg[512];
 
 // Timing events per sense_timer_t, set by sense_set_timer_events.
-constexpr int kTimers = 5;
+constexpr int kTimers = 6;
 thread_local hipEvent_t g_timer[kTimers][2] = {};
 
 hipError_t timer_mark(int which, int edge, hipStream_t st) {
@@ -354,9 +354,13 @@ SENSE_EXPORT sense_status_t sense_retrieve(const sense_index_t* ix, const void* 
     }
     if ((e = timer_mark(SENSE_TIMER_SCAN, 0, st)) != hipSuccess) return hip_fail(e, "timer");
     const bool split = q_dtype != ix->key_dtype;  // key-typed queries need no lo half
-    if ((e = sense::launch_scan(ix->keys, ix->key_dtype, ix->n, ix->d, ix->ld, qptr, nq, split,
-                                ix->inv_norm, scores, ws + L.m_off, st)) != hipSuccess)
-        return hip_fail(e, "similarity scan");
+    if (ix->d <= sense::kSmallDim && nq < sense::kMfmaMinQueries)
+        e = sense::launch_scan_small(ix->keys, ix->key_dtype, ix->n, ix->d, ix->ld, qptr, nq,
+                                     ix->inv_norm, scores, st);
+    else
+        e = sense::launch_scan(ix->keys, ix->key_dtype, ix->n, ix->d, ix->ld, qptr, nq, split,
+                               ix->inv_norm, scores, ws + L.m_off, st);
+    if (e != hipSuccess) return hip_fail(e, "similarity scan");
     if ((e = timer_mark(SENSE_TIMER_SCAN, 1, st)) != hipSuccess) return hip_fail(e, "timer");
     if ((e = timer_mark(SENSE_TIMER_TOPK, 0, st)) != hipSuccess) return hip_fail(e, "timer");
     if ((e = sense::launch_topk_gather(scores, ix->n, nq, k, ix->spans, ix->span_len,
@@ -623,5 +627,71 @@ SENSE_EXPORT sense_status_t sense_soft_gate_verify_tree(
                                   workspace, st);
     if (e != hipSuccess) return hip_fail(e, "soft-gated evaluation through the tree");
     if ((e = timer_mark(SENSE_TIMER_VERIFY, 1, st)) != hipSuccess) return hip_fail(e, "timer");
+    return ok();
+}
+
+static sense_status_t check_projection(const sense_projection_t* p) {
+    if (!p) return fail(SENSE_ERR_INVALID_ARGUMENT, "projection is NULL");
+    if (!p->basis) return fail(SENSE_ERR_INVALID_ARGUMENT, "basis is NULL");
+    if (p->d_in < 1 || p->d_in > sense::kMaxDim || p->d_in % 8 != 0)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "d_in = %d must be a multiple of 8 in [8, %d]",
+                    p->d_in, sense::kMaxDim);
+    if (p->d_out < 1 || p->d_out > sense::kMaxProjOut)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "d_out = %d outside [1, %d]", p->d_out,
+                    sense::kMaxProjOut);
+    if (!aligned(p->basis, 4) || (p->mean && !aligned(p->mean, 4)))
+        return fail(SENSE_ERR_MISALIGNED, "basis and mean must be 4-byte aligned");
+    return SENSE_OK;
+}
+
+SENSE_EXPORT sense_status_t sense_project_workspace_size(const sense_projection_t* proj,
+                                                         sense_dtype_t x_dtype, int64_t n_rows,
+                                                         size_t* bytes) {
+    if (!bytes) return fail(SENSE_ERR_INVALID_ARGUMENT, "bytes is NULL");
+    sense_status_t s = check_projection(proj);
+    if (s != SENSE_OK) return s;
+    if (!dtype_ok(x_dtype)) return fail(SENSE_ERR_INVALID_ARGUMENT, "unknown x dtype %d", (int)x_dtype);
+    if (n_rows < 0) return fail(SENSE_ERR_INVALID_ARGUMENT, "n_rows < 0");
+    *bytes = sense::project_workspace_bytes(x_dtype, n_rows, proj->d_in, proj->d_out);
+    return ok();
+}
+
+SENSE_EXPORT sense_status_t sense_project(const sense_projection_t* proj, const void* x,
+                                          sense_dtype_t x_dtype, int64_t n_rows,
+                                          int64_t x_stride, void* out, sense_dtype_t out_dtype,
+                                          int64_t out_stride, void* workspace,
+                                          size_t workspace_bytes, void* stream) {
+    sense_status_t s = check_projection(proj);
+    if (s != SENSE_OK) return s;
+    if (!dtype_ok(x_dtype) || !dtype_ok(out_dtype))
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "unknown dtype (x %d, out %d)", (int)x_dtype,
+                    (int)out_dtype);
+    if (n_rows < 0 || n_rows > 0x7FFFFFFFLL)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "n_rows = %lld outside [0, 2^31-1]",
+                    (long long)n_rows);
+    if (x_stride < proj->d_in || out_stride < proj->d_out)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "x_stride %lld < d_in or out_stride %lld < d_out",
+                    (long long)x_stride, (long long)out_stride);
+    if (n_rows == 0) return ok();
+    if (!x || !out) return fail(SENSE_ERR_INVALID_ARGUMENT, "x and out must be non-NULL");
+    if (!aligned(x, (size_t)elem_size(x_dtype)) || !aligned(out, (size_t)elem_size(out_dtype)))
+        return fail(SENSE_ERR_MISALIGNED, "x or out not aligned to its element size");
+    const size_t need = sense::project_workspace_bytes(x_dtype, n_rows, proj->d_in, proj->d_out);
+    const bool mfma = sense::project_uses_mfma(x_dtype, x, x_stride, n_rows);
+    if (mfma) {
+        if (!workspace || workspace_bytes < need)
+            return fail(SENSE_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
+                        workspace ? workspace_bytes : (size_t)0);
+        if (!aligned(workspace, 256))
+            return fail(SENSE_ERR_MISALIGNED, "workspace must be 256-byte aligned");
+    }
+    hipStream_t st = (hipStream_t)stream;
+    hipError_t e;
+    if ((e = timer_mark(SENSE_TIMER_PROJECT, 0, st)) != hipSuccess) return hip_fail(e, "timer");
+    e = sense::launch_project(x, x_dtype, n_rows, proj->d_in, x_stride, proj->mean, proj->basis,
+                              proj->d_out, proj->normalize, out, out_dtype, out_stride,
+                              workspace, st);
+    if (e != hipSuccess) return hip_fail(e, "projection");
+    if ((e = timer_mark(SENSE_TIMER_PROJECT, 1, st)) != hipSuccess) return hip_fail(e, "timer");
     return ok();
 }

@@ -47,13 +47,15 @@ EXPORTED = (
     "sense_build_loose_trie",
     "sense_soft_gate_verify_tree_workspace_size",
     "sense_soft_gate_verify_tree",
+    "sense_project_workspace_size",
+    "sense_project",
     "sense_set_timer_events",
     "sense_read_bandwidth_probe",
     "sense_status_string",
     "sense_last_error_message",
 )
 SENSE_TIMER_SCAN, SENSE_TIMER_TOPK, SENSE_TIMER_VERIFY, SENSE_TIMER_SELECT = 0, 1, 2, 3
-SENSE_TIMER_TRIE = 4
+SENSE_TIMER_TRIE, SENSE_TIMER_PROJECT = 4, 5
 
 
 class SenseError(RuntimeError):
@@ -117,6 +119,16 @@ class TrieDesc(ctypes.Structure):
     ]
 
 
+class ProjDesc(ctypes.Structure):
+    _fields_ = [
+        ("mean", ctypes.c_void_p),
+        ("basis", ctypes.c_void_p),
+        ("d_in", ctypes.c_int32),
+        ("d_out", ctypes.c_int32),
+        ("normalize", ctypes.c_int32),
+    ]
+
+
 class GateParams(ctypes.Structure):
     _fields_ = [
         ("gamma", ctypes.c_float),
@@ -159,6 +171,9 @@ def load_library() -> ctypes.CDLL:
         "sense_soft_gate_verify": [P, ctypes.c_int, I64, P, P, I32, I32, I32, I32,
                                    ctypes.POINTER(GateParams), P, P, P, P, P, P, SZ, P],
         "sense_build_loose_trie": [P, P, I32, I32, I32, ctypes.POINTER(TrieDesc), P],
+        "sense_project_workspace_size": [ctypes.POINTER(ProjDesc), ctypes.c_int, I64, PSZ],
+        "sense_project": [ctypes.POINTER(ProjDesc), P, ctypes.c_int, I64, I64, P, ctypes.c_int,
+                          I64, P, SZ, P],
         "sense_soft_gate_verify_tree_workspace_size": [I32, I32, I32, I32, PSZ],
         "sense_soft_gate_verify_tree": [P, ctypes.c_int, I64, P, P, P, P, I32, I32, I32, I32,
                                         ctypes.POINTER(GateParams), P, P, P, P, P, P, SZ, P],
@@ -607,4 +622,54 @@ def sense_soft_gate_verify_tree(logits: torch.Tensor, trie: dict, n_groups: int 
         _dev_ptr(out.get("masks"), "out_masks"), _dev_ptr(out.get("rank"), "out_rank"),
         _dev_ptr(workspace, "workspace"), workspace.numel(), _stream_handle(stream)),
         "sense_soft_gate_verify_tree")
+    return out
+
+
+def _proj_desc(basis: torch.Tensor, mean: torch.Tensor | None, normalize: bool) -> ProjDesc:
+    if basis.dtype != torch.float32 or basis.dim() != 2 or not basis.is_contiguous():
+        raise ValueError("basis must be a contiguous d_out x d_in float32 tensor")
+    if mean is not None and (mean.dtype != torch.float32 or not mean.is_contiguous()
+                             or mean.numel() != basis.shape[1]):
+        raise ValueError("mean must be a contiguous float32 tensor of d_in entries")
+    return ProjDesc(mean=_dev_ptr(mean, "mean"), basis=_dev_ptr(basis, "basis"),
+                    d_in=basis.shape[1], d_out=basis.shape[0], normalize=int(bool(normalize)))
+
+
+def sense_project_workspace_size(basis: torch.Tensor, x_dtype: torch.dtype, n_rows: int,
+                                 mean: torch.Tensor | None = None, normalize: bool = True) -> int:
+    size = ctypes.c_size_t()
+    desc = _proj_desc(basis, mean, normalize)
+    _check(load_library().sense_project_workspace_size(ctypes.byref(desc), _TORCH_DTYPE[x_dtype],
+                                                       n_rows, ctypes.byref(size)),
+           "sense_project_workspace_size")
+    return size.value
+
+
+def sense_project(x: torch.Tensor, basis: torch.Tensor, mean: torch.Tensor | None = None,
+                  normalize: bool = True, out_dtype: torch.dtype = torch.float32,
+                  out: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
+                  stream=None) -> torch.Tensor:
+    """PCA projection (+ L2 normalisation) of the rows of ``x`` (n x d_in,
+    rows may be strided) with ``basis`` (d_out x d_in fp32, principal
+    directions as rows) and ``mean`` (d_in fp32 or None).  Returns n x d_out
+    of ``out_dtype`` (or writes ``out``)."""
+    if x.dim() == 1:
+        x = x.unsqueeze(0)
+    if x.dtype not in _TORCH_DTYPE or x.dim() != 2 or x.stride(1) != 1:
+        raise ValueError("x must be a 2-D float32/float16/bfloat16 tensor with contiguous rows")
+    desc = _proj_desc(basis, mean, normalize)
+    n = x.shape[0]
+    if x.shape[1] != desc.d_in:
+        raise ValueError(f"x has {x.shape[1]} columns, basis expects {desc.d_in}")
+    if out is None:
+        out = torch.empty((n, desc.d_out), dtype=out_dtype, device=x.device)
+    if out.dim() != 2 or out.stride(1) != 1 or out.shape[0] != n:
+        raise ValueError("out must be n x (>= d_out) with contiguous rows")
+    if workspace is None:
+        need = sense_project_workspace_size(basis, x.dtype, n, mean, normalize)
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
+    _check(load_library().sense_project(
+        ctypes.byref(desc), _dev_ptr(x, "x"), _TORCH_DTYPE[x.dtype], n, x.stride(0),
+        _dev_ptr(out, "out"), _TORCH_DTYPE[out.dtype], out.stride(0), _dev_ptr(workspace, "workspace"),
+        workspace.numel(), _stream_handle(stream)), "sense_project")
     return out

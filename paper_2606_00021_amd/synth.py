@@ -305,3 +305,23 @@ def make_shared_spans(w: Workload, ds: Datastore, seed: int, phrases: int = 4,
     div = torch.arange(w.span, device=device)[None, :] >= first[:, None]
     rnd = torch.randint(0, w.vocab, (w.n, w.span), generator=g, device=device, dtype=torch.int32)
     return torch.where(div, rnd, base[ds.assign, pick]).contiguous()
+
+
+def make_pca_basis(ds: Datastore, seed: int, d_out: int = 64, sample: int = 16384):
+    """A PCA fit of the kind the paper's datastore construction uses (the
+    fit is input preparation here, not part of the library): mean and the
+    top-d_out principal directions of a uniform sample of stored keys, from
+    the eigen-decomposition of the sample covariance in float64.  Returns
+    (mean [d] fp32, basis [d_out, d] fp32) on the keys' device."""
+    device = ds.keys.device
+    g = _gen(seed + 32416189, device)
+    n = ds.keys.shape[0]
+    rows = torch.randint(0, n, (min(sample, n),), generator=g, device=device)
+    x = ds.keys[rows].double()
+    mean = x.mean(dim=0)
+    xc = x - mean
+    cov = xc.T @ xc / x.shape[0]
+    w, v = torch.linalg.eigh(cov)
+    top = torch.argsort(w, descending=True)[:d_out]
+    basis = v[:, top].T.contiguous()
+    return mean.float().contiguous(), basis.float().contiguous()

@@ -252,7 +252,8 @@ def test_select_rejects(lib, kw, status):
 def test_timer_ids(lib):
     assert lib.sense_set_timer_events(sense.SENSE_TIMER_SELECT, None, None) == 0
     assert lib.sense_set_timer_events(sense.SENSE_TIMER_TRIE, None, None) == 0
-    assert lib.sense_set_timer_events(5, None, None) == INVALID
+    assert lib.sense_set_timer_events(sense.SENSE_TIMER_PROJECT, None, None) == 0
+    assert lib.sense_set_timer_events(6, None, None) == INVALID
 
 
 def trie_desc(**kw):
@@ -343,3 +344,54 @@ def test_tree_verify_empty_and_workspace(lib):
     assert size.value >= 64 * 8 * 16
     assert lib.sense_soft_gate_verify_tree_workspace_size(64, 8, 100, 3,
                                                          ctypes.byref(size)) == INVALID
+
+
+def proj(**kw):
+    base = dict(mean=None, basis=p(FAKE), d_in=4096, d_out=64, normalize=1)
+    base.update(kw)
+    return sense.ProjDesc(**base)
+
+
+@pytest.mark.parametrize("kw,args,status", [
+    (dict(basis=None), {}, INVALID),
+    (dict(d_in=0), {}, INVALID),
+    (dict(d_in=100), {}, INVALID),
+    (dict(d_in=8200), {}, INVALID),
+    (dict(d_out=0), {}, INVALID),
+    (dict(d_out=257), {}, INVALID),
+    (dict(basis=p(FAKE + 2)), {}, MISALIGNED),
+    ({}, dict(xdt=7), INVALID),
+    ({}, dict(odt=7), INVALID),
+    ({}, dict(n=-1), INVALID),
+    ({}, dict(xs=4000), INVALID),
+    ({}, dict(os=10), INVALID),
+    ({}, dict(x=None), INVALID),
+    ({}, dict(out=None), INVALID),
+    ({}, dict(x=p(FAKE + 1), xdt=2), MISALIGNED),
+    ({}, dict(ws=None), WORKSPACE),                  # 16-bit, aligned, 1000 rows: MFMA route
+    ({}, dict(wsb=64), WORKSPACE),
+    ({}, dict(ws=p(FAKE + 64)), MISALIGNED),
+])
+def test_project_rejects(lib, kw, args, status):
+    a = dict(x=p(FAKE), xdt=sense.SENSE_BF16, n=1000, xs=4096, out=p(FAKE), odt=sense.SENSE_BF16,
+             os=64, ws=p(FAKE), wsb=1 << 30)
+    a.update(args)
+    d = proj(**kw)
+    assert lib.sense_project(ctypes.byref(d), a["x"], a["xdt"], a["n"], a["xs"], a["out"],
+                             a["odt"], a["os"], a["ws"], a["wsb"], None) == status
+    assert lib.sense_last_error_message()
+
+
+def test_project_workspace_sizes(lib):
+    size = ctypes.c_size_t()
+    d = proj()
+    assert lib.sense_project_workspace_size(ctypes.byref(d), sense.SENSE_BF16, 1 << 20,
+                                            ctypes.byref(size)) == 0
+    assert size.value >= 64 * (1 << 20) * 4                # S = d_out x n fp32
+    assert lib.sense_project_workspace_size(ctypes.byref(d), sense.SENSE_F32, 1 << 20,
+                                            ctypes.byref(size)) == 0
+    assert size.value == 0                                 # fp32 rows: direct route
+    assert lib.sense_project_workspace_size(ctypes.byref(d), sense.SENSE_BF16, 3,
+                                            ctypes.byref(size)) == 0
+    assert size.value == 0
+    assert lib.sense_project(ctypes.byref(d), None, 2, 0, 4096, None, 2, 64, None, 0, None) == 0
