@@ -42,6 +42,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="approximate CPU time spent timing the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--graph", action="store_true",
+                    help="also time replays of the step captured as one HIP graph (on this "
+                         "ROCm the replays measured a few us slower than eager launches)")
     ap.add_argument("--no-sen", action="store_true",
                     help="skip the candidate-selection leg (dynamic cache + composite Top-N)")
     ap.add_argument("--sen-context", type=int, default=4096,
@@ -52,26 +55,28 @@ def parse():
     return ap.parse_args()
 
 
-def scan_source_digest() -> str:
-    """Digest of the scan kernel's source code with comments and blank space
+def scan_source_digest(fname: str = "scan.hip") -> str:
+    """Digest of a scan kernel's source file with comments and blank space
     removed (comment edits do not invalidate measured counters)."""
     import hashlib
     import re
 
-    src = open(os.path.join(ROOT, "paper_2606_00021_amd", "csrc", "scan.hip")).read()
+    src = open(os.path.join(ROOT, "paper_2606_00021_amd", "csrc", fname)).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
     src = re.sub(r"//[^\n]*", "", src)
     src = "".join(src.split())
     return hashlib.sha256(src.encode()).hexdigest()[:16]
 
 
-def traffic_from_profiles(workload: str):
-    """Measured HBM bytes per scan launch, read from the committed rocprofv3
-    counter summary of this workload, or None when there is none or the scan
-    source changed since the counters were taken."""
-    import hashlib
+SCAN_SOURCES = {"scan_gemv_kernel": "scan.hip", "scan_small_kernel": "scan_small.hip",
+                "scan_mfma_kernel": "scan_mfma.hip"}
 
-    path = os.path.join(ROOT, "profiles", f"scan_gemv_kernel_{workload}.md")
+
+def traffic_from_profiles(workload: str, kernel: str = "scan_gemv_kernel"):
+    """Measured HBM bytes per scan launch, read from the committed rocprofv3
+    counter summary of this kernel and workload, or None when there is none or
+    the kernel's source changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}.md")
     if not os.path.exists(path):
         return None
     fields = {}
@@ -79,7 +84,8 @@ def traffic_from_profiles(workload: str):
         if ":" in line and not line.startswith(("|", "-", "#", "`")):
             key, _, val = line.partition(":")
             fields[key.strip()] = val.strip()
-    if fields.get("scan_source_sha256_16") != scan_source_digest() or "bytes_per_launch" not in fields:
+    if (fields.get("scan_source_sha256_16") != scan_source_digest(SCAN_SOURCES[kernel])
+            or "bytes_per_launch" not in fields):
         return None
     return int(fields["bytes_per_launch"])
 
@@ -128,7 +134,7 @@ def cpu_baseline(w, ds, q, logits, drafts, budget_s: float):
         "unit": "queries/s",
         "cores": cores,
         "kind": "oracle",
-        "sample": (f"fp64 oracle on host: scan of {rows} of {w.n} rows x d={w.d} "
+        "sample": (f"fp64 oracle on host: scan of {rows} of {w.n} rows x d={ds.keys.shape[1]} "
                    f"({t_scan_row * 1e6:.3f} us/row), full sort of {w.n} scores "
                    f"({t_sort:.3f} s), verify of {c_s}x{drafts.shape[1]} positions x "
                    f"V={w.vocab} ({t_verify_pos * 1e3:.2f} ms/position); scaled to one "
@@ -323,14 +329,46 @@ def main():
     t0 = time.perf_counter()
     ds = synth.make_datastore(w, args.seed, dev)
     q, src_rows = synth.make_queries(w, ds, args.seed)
-    index = sense.sense_build_index(ds.keys, ds.spans, ds.span_len, metric=w.metric)
     nq, k, m = w.n_queries, w.k, w.span
+    proj_info = None
+    q_hidden = q
+    if w.proj:
+        # The paper's key geometry: PCA 4096 -> proj, L2-normalised, stored in
+        # the key type.  Projecting the store is the datastore build (timed
+        # here, outside the step); the query is projected inside every step.
+        mean, basis = synth.make_pca_basis(ds, args.seed, w.proj)
+        kdt = synth.DTYPES[w.key_dtype]
+        ws_p = torch.empty(max(1, sense.sense_project_workspace_size(basis, kdt, w.n, mean)),
+                           dtype=torch.uint8, device=dev)
+        keys_p = torch.empty((w.n, w.proj), dtype=kdt, device=dev)
+        sense.sense_project(ds.keys, basis, mean, True, out=keys_p, workspace=ws_p)
+        torch.cuda.synchronize()
+        a_ev, b_ev = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a_ev.record()
+        sense.sense_project(ds.keys, basis, mean, True, out=keys_p, workspace=ws_p)
+        b_ev.record()
+        torch.cuda.synchronize()
+        build_ms = a_ev.elapsed_time(b_ev)
+        proj_info = {"dim": w.proj, "basis": "top principal directions of a 16384-row sample",
+                     "store_projection_ms": build_ms,
+                     "store_projection_gbps": w.n * w.d * 2 / (build_ms * 1e-3) / 1e9}
+        log(f"[bench] projected the store {w.d} -> {w.proj}: {build_ms:.2f} ms "
+            f"({proj_info['store_projection_gbps']:.0f} GB/s of hidden states)")
+        del ws_p
+        ds.keys = keys_p                      # the searched datastore
+        torch.cuda.empty_cache()
+        q_proj = torch.empty((nq, w.proj), dtype=torch.float32, device=dev)
+        q = q_proj
+    d_idx = ds.keys.shape[1]
+    index = sense.sense_build_index(ds.keys, ds.spans, ds.span_len, metric=w.metric)
     ws_r = torch.empty(max(1, sense.sense_retrieve_workspace_size(index, nq, k)),
                        dtype=torch.uint8, device=dev)
     outs = (torch.empty((nq, k), dtype=torch.int64, device=dev),
             torch.empty((nq, k), dtype=torch.float32, device=dev),
             torch.empty((nq, k, m), dtype=torch.int32, device=dev),
             torch.empty((nq, k), dtype=torch.int32, device=dev))
+    if w.proj:
+        sense.sense_project(q_hidden, basis, mean, True, out=q_proj)
     sense.sense_retrieve(index, q, k, workspace=ws_r, out=outs)
     vq = w.verify_queries
     drafts = outs[2][:vq].view(vq * k, m)
@@ -345,6 +383,8 @@ def main():
     log(f"[bench] setup {time.perf_counter() - t0:.1f} s")
 
     def step():
+        if w.proj:
+            sense.sense_project(q_hidden, basis, mean, True, out=q_proj)
         sense.sense_retrieve(index, q, k, workspace=ws_r, out=outs)
         sense.sense_soft_gate_verify(logits, drafts, dlen, n_groups=vq, gamma=0.05, topk=3,
                                      window=6, tau=0, workspace=ws_v, out=out_v)
@@ -354,26 +394,49 @@ def main():
     torch.cuda.synchronize()
 
     K = args.steps
-    # Timed region: exactly K steps between two events, nothing else enqueued.
-    t_begin = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    wall0 = time.perf_counter()
-    t_begin.record()
-    for _ in range(K):
-        step()
-    t_end.record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
-    ms_step = t_begin.elapsed_time(t_end) / K
+
+    def time_steps(run):
+        # Timed region: exactly K steps between two events, nothing else
+        # enqueued.
+        t_begin = torch.cuda.Event(enable_timing=True)
+        t_end = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        wall0 = time.perf_counter()
+        t_begin.record()
+        for _ in range(K):
+            run()
+        t_end.record()
+        torch.cuda.synchronize()
+        return t_begin.elapsed_time(t_end) / K, (time.perf_counter() - wall0) / K
+
+    ms_eager, wall_eager = time_steps(step)
+    ms_step, wall_step = ms_eager, wall_eager
+    launch = "eager"
+    if args.graph:
+        # The step as one HIP graph: every entry point allocates nothing and
+        # records no memset, so the captured kernels replay the same work
+        # without the host's per-call launch cost.
+        graph = torch.cuda.CUDAGraph()
+        cap = torch.cuda.Stream()
+        cap.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(cap):
+            with torch.cuda.graph(graph, stream=cap):
+                step()
+        torch.cuda.current_stream().wait_stream(cap)
+        graph.replay()
+        torch.cuda.synchronize()
+        ms_step, wall_step = time_steps(graph.replay)
+        launch = "hip_graph"
+    wall = wall_step
 
     # Per-kernel durations: a second pass of K steps with hipEvents recorded
     # by the library around the scan, top-k and verify kernels (the events
     # themselves add a little time, so this pass is not the step time).
+    timed_parts = ("scan", "topk", "verify") + (("project",) if w.proj else ())
     ev = {t: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-              for _ in range(K)] for t in ("scan", "topk", "verify")}
+              for _ in range(K)] for t in timed_parts}
     timer_id = {"scan": sense.SENSE_TIMER_SCAN, "topk": sense.SENSE_TIMER_TOPK,
-                "verify": sense.SENSE_TIMER_VERIFY}
+                "verify": sense.SENSE_TIMER_VERIFY, "project": sense.SENSE_TIMER_PROJECT}
     # torch creates the underlying hipEvent_t lazily at the first record():
     # record every event once here so that the handles exist.
     for t in ev:
@@ -389,18 +452,26 @@ def main():
     for t in ev:
         sense.sense_set_timer_events(timer_id[t], None, None)
     dur = {t: sum(a.elapsed_time(b) for a, b in ev[t]) / K for t in ev}
-    log(f"[bench] {K} steps: {ms_step:.4f} ms/step (wall {wall * 1e3 / K:.4f} ms/step); "
-        f"scan {dur['scan']:.4f} ms, topk {dur['topk']:.4f} ms, verify {dur['verify']:.4f} ms")
+    log(f"[bench] {K} steps ({launch}): {ms_step:.4f} ms/step (wall {wall * 1e3:.4f} ms/step; "
+        f"eager launches {ms_eager:.4f} ms/step); "
+        f"scan {dur['scan']:.4f} ms, topk {dur['topk']:.4f} ms, verify {dur['verify']:.4f} ms"
+        + (f", query projection {dur['project']:.4f} ms" if w.proj else ""))
 
     # Algorithmic bytes: every key once (+ the fp32 inverse-norm table for
     # cosine), the gathered continuations, and every live logit row once.
     cos_extra = 4 * w.n if w.metric == "cosine" else 0
-    scan_bytes = w.n * w.d * 2 + cos_extra
+    scan_bytes = w.n * d_idx * 2 + cos_extra
     gather_bytes = nq * k * m * 4
     live = int(dlen.clamp(0, m).sum().item())
     verify_bytes = live * w.vocab * (4 if w.logits_dtype == "f32" else 2)
     step_bytes = scan_bytes + gather_bytes + verify_bytes
     scan_gbps = scan_bytes / (dur["scan"] * 1e-3) / 1e9
+    if nq >= 4:
+        scan_kernel = "scan_mfma_kernel"
+    elif d_idx <= 64:
+        scan_kernel = "scan_small_kernel"
+    else:
+        scan_kernel = "scan_gemv_kernel"
     res = {
         "metric": METRIC,
         "value": nq / (ms_step * 1e-3),
@@ -409,6 +480,8 @@ def main():
         "steps": K,
         "warmup": args.warmup,
         "ms_per_step": ms_step,
+        "launch": launch,
+        "ms_per_step_eager": ms_eager,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -423,11 +496,15 @@ def main():
         "scan_ms": dur["scan"],
         "topk_ms": dur["topk"],
         "verify_ms": dur["verify"],
+        **({"project_ms": dur["project"]} if w.proj else {}),
         "verify_gbps": verify_bytes / (dur["verify"] * 1e-3) / 1e9 if dur["verify"] > 0 else None,
-        "roofline": {"bound": "hbm", "kernel": "scan_gemv_kernel", "achieved": scan_gbps,
+        "roofline": {"bound": "hbm", "kernel": scan_kernel, "achieved": scan_gbps,
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": scan_gbps / HBM_PEAK_GBPS,
-                     "traffic": traffic_from_profiles(name)},
+                     "traffic": traffic_from_profiles(name, scan_kernel)},
     }
+    if proj_info is not None:
+        res["config"]["proj"] = w.proj
+        res["projection"] = proj_info
     # Practical HBM read ceiling: a plain streaming read of the key store.
     sink = torch.zeros(1, dtype=torch.int32, device=dev)
     sense.sense_read_bandwidth_probe(ds.keys, sink)
@@ -454,7 +531,7 @@ def main():
         log(f"[bench] copy probe: {args.copy_probe_mib} MiB read + {args.copy_probe_mib} MiB "
             f"written by one copy kernel")
         del src, dst
-    if not args.no_sen:
+    if not args.no_sen and not w.proj:
         res["sen"] = sen_leg(args, w, ds, q, src_rows, K, dev)
     if not args.no_cpu_baseline:
         log("[bench] timing the oracle on the host (cpu_baseline)")

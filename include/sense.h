@@ -458,7 +458,7 @@ typedef struct {
     int32_t normalize;
 } sense_projection_t;
 
-/* Bytes of device workspace sense_project needs (0 when none). */
+/* Bytes of device workspace sense_project needs (0 only for n_rows = 0). */
 sense_status_t sense_project_workspace_size(const sense_projection_t *proj,
                                             sense_dtype_t x_dtype, int64_t n_rows,
                                             size_t *bytes);
@@ -476,8 +476,8 @@ sense_status_t sense_project_workspace_size(const sense_projection_t *proj,
  * 16-bit rows that are 16-byte aligned with x_stride % 8 == 0, 256 rows or
  * more, run as a matrix-core contraction (the basis split into a hi and a lo
  * half of the key type, ~16 mantissa bits for bf16, ~22 for fp16); other
- * inputs run one block per row in fp32.  Needs workspace (256-byte aligned,
- * sense_project_workspace_size bytes) only on the matrix-core route.
+ * inputs run one block per (row, output) in fp32.  Needs workspace (256-byte
+ * aligned, sense_project_workspace_size bytes).
  * Errors: INVALID_ARGUMENT, MISALIGNED, WORKSPACE, HIP. */
 sense_status_t sense_project(const sense_projection_t *proj, const void *x,
                              sense_dtype_t x_dtype, int64_t n_rows, int64_t x_stride, void *out,

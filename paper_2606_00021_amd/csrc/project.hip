@@ -11,8 +11,9 @@
 //     basis split into hi + lo halves of the key type), giving
 //     S[o][i] = x_i . w_o; then project_finish subtracts mean . w_o,
 //     normalises each row and stores it transposed in the output type;
-//   * a few rows (queries) or fp32 / unaligned rows: one block per row, the
-//     centred row staged in LDS, one wave per output with a fixed-order sum.
+//   * a few rows (queries) or fp32 / unaligned rows: one block per (row,
+//     output) computes the centred dot product with a fixed-order sum, then
+//     one wave per row normalises and stores it.
 #include "internal.h"
 
 namespace sense {
@@ -87,36 +88,47 @@ __global__ __launch_bounds__(kProjThreads) void project_finish_kernel(
     }
 }
 
-// Direct route: one block per row.
-__global__ __launch_bounds__(kProjThreads) void project_rows_kernel(
+// Direct route, step 1: raw[i][o] = (x_i - mean) . w_o, one block of 256
+// threads per (row, output): each thread's 16-32 elements are loaded at
+// once (one round of memory latency), then a fixed-order block sum.
+constexpr int kDotThreads = 256;
+
+__global__ __launch_bounds__(kDotThreads) void project_dots_kernel(
     const void* __restrict__ x, int x_dtype, int64_t x_stride, int d_in,
-    const float* __restrict__ mean, const float* __restrict__ basis, int d_out, int normalize,
-    void* __restrict__ out, int out_dtype, int64_t out_stride) {
-    __shared__ float xc[kMaxDim];
-    __shared__ float res[kMaxProjOut];
-    __shared__ float s_inv;
+    const float* __restrict__ mean, const float* __restrict__ basis, int d_out,
+    float* __restrict__ raw) {
+    __shared__ float s_part[kDotThreads / 64];
+    const int o = blockIdx.y;
     const int64_t i = blockIdx.x;
-    for (int t = threadIdx.x; t < d_in; t += kProjThreads)
-        xc[t] = load_x(x, x_dtype, i * x_stride + t) - (mean ? mean[t] : 0.0f);
-    __syncthreads();
-    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-    for (int o = wv; o < d_out; o += kProjThreads / 64) {
-        const float* w = basis + (int64_t)o * d_in;
-        float a = 0.0f;
-        for (int t = lane; t < d_in; t += 64) a = __builtin_fmaf(xc[t], w[t], a);
-        a = wsum(a);
-        if (lane == 0) res[o] = a;
+    const float* w = basis + (int64_t)o * d_in;
+    float a[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll 16
+    for (int t = threadIdx.x; t < d_in; t += kDotThreads) {
+        const float c = load_x(x, x_dtype, i * x_stride + t) - (mean ? mean[t] : 0.0f);
+        const int k = (t / kDotThreads) & 3;
+        a[k] = __builtin_fmaf(c, w[t], a[k]);
     }
+    const float v = wsum((a[0] + a[1]) + (a[2] + a[3]));
+    if ((threadIdx.x & 63) == 0) s_part[threadIdx.x >> 6] = v;
     __syncthreads();
-    if (wv == 0) {
+    if (threadIdx.x == 0) raw[i * d_out + o] = (s_part[0] + s_part[1]) + (s_part[2] + s_part[3]);
+}
+
+// Direct route, step 2: normalise row i and store it in the output type.
+__global__ __launch_bounds__(64) void project_norm_kernel(
+    const float* __restrict__ raw, int d_out, int normalize, void* __restrict__ out,
+    int out_dtype, int64_t out_stride) {
+    const int64_t i = blockIdx.x;
+    const int lane = threadIdx.x;
+    const float* r = raw + i * d_out;
+    float inv = 1.0f;
+    if (normalize) {
         float ss = 0.0f;
-        for (int o = lane; o < d_out; o += 64) ss = __builtin_fmaf(res[o], res[o], ss);
+        for (int o = lane; o < d_out; o += 64) ss = __builtin_fmaf(r[o], r[o], ss);
         ss = wsum(ss);
-        if (lane == 0) s_inv = normalize ? ((ss > 0.0f) ? 1.0f / __builtin_sqrtf(ss) : 0.0f) : 1.0f;
+        inv = (ss > 0.0f) ? 1.0f / __builtin_sqrtf(ss) : 0.0f;
     }
-    __syncthreads();
-    for (int o = threadIdx.x; o < d_out; o += kProjThreads)
-        store_out(out, out_dtype, i * out_stride + o, res[o] * s_inv);
+    for (int o = lane; o < d_out; o += 64) store_out(out, out_dtype, i * out_stride + o, r[o] * inv);
 }
 
 }  // namespace
@@ -130,9 +142,10 @@ bool project_uses_mfma(int x_dtype, const void* x, int64_t x_stride, int64_t n) 
 static size_t up256(size_t x) { return (x + 255) / 256 * 256; }
 
 size_t project_workspace_bytes(int x_dtype, int64_t n, int d_in, int d_out) {
-    if (x_dtype == DT_F32 || n < kProjMfmaMinRows) return 0;
-    return up256((size_t)d_out * sizeof(float)) + up256((size_t)d_out * n * sizeof(float)) +
-           up256(scan_mfma_scratch_bytes(d_out, d_in));
+    if (n == 0) return 0;
+    size_t bytes = up256((size_t)d_out * sizeof(float)) + up256((size_t)d_out * n * sizeof(float));
+    if (x_dtype != DT_F32 && n >= kProjMfmaMinRows) bytes += up256(scan_mfma_scratch_bytes(d_out, d_in));
+    return bytes;
 }
 
 hipError_t launch_project(const void* x, int x_dtype, int64_t n, int d_in, int64_t x_stride,
@@ -140,18 +153,21 @@ hipError_t launch_project(const void* x, int x_dtype, int64_t n, int d_in, int64
                           void* out, int out_dtype, int64_t out_stride, void* workspace,
                           hipStream_t stream) {
     if (n == 0) return hipSuccess;
-    if (!project_uses_mfma(x_dtype, x, x_stride, n)) {
-        hipLaunchKernelGGL(project_rows_kernel, dim3((unsigned)n), dim3(kProjThreads), 0, stream,
-                           x, x_dtype, x_stride, d_in, mean, basis, d_out, normalize, out,
-                           out_dtype, out_stride);
-        return hipGetLastError();
-    }
     char* ws = (char*)workspace;
     const size_t c_bytes = up256((size_t)d_out * sizeof(float));
     float* centre = mean ? (float*)ws : nullptr;
     float* s = (float*)(ws + c_bytes);
     void* scratch = ws + c_bytes + up256((size_t)d_out * n * sizeof(float));
     hipError_t e;
+    if (!project_uses_mfma(x_dtype, x, x_stride, n)) {
+        const dim3 grid((unsigned)n, (unsigned)d_out);
+        hipLaunchKernelGGL(project_dots_kernel, grid, dim3(kDotThreads), 0, stream, x, x_dtype,
+                           x_stride, d_in, mean, basis, d_out, s);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        hipLaunchKernelGGL(project_norm_kernel, dim3((unsigned)n), dim3(64), 0, stream, s, d_out,
+                           normalize, out, out_dtype, out_stride);
+        return hipGetLastError();
+    }
     if (mean) {
         hipLaunchKernelGGL(project_center_kernel,
                            dim3((unsigned)((d_out + kProjThreads / 64 - 1) / (kProjThreads / 64))),

@@ -677,14 +677,10 @@ SENSE_EXPORT sense_status_t sense_project(const sense_projection_t* proj, const 
     if (!aligned(x, (size_t)elem_size(x_dtype)) || !aligned(out, (size_t)elem_size(out_dtype)))
         return fail(SENSE_ERR_MISALIGNED, "x or out not aligned to its element size");
     const size_t need = sense::project_workspace_bytes(x_dtype, n_rows, proj->d_in, proj->d_out);
-    const bool mfma = sense::project_uses_mfma(x_dtype, x, x_stride, n_rows);
-    if (mfma) {
-        if (!workspace || workspace_bytes < need)
-            return fail(SENSE_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
-                        workspace ? workspace_bytes : (size_t)0);
-        if (!aligned(workspace, 256))
-            return fail(SENSE_ERR_MISALIGNED, "workspace must be 256-byte aligned");
-    }
+    if (!workspace || workspace_bytes < need)
+        return fail(SENSE_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
+                    workspace ? workspace_bytes : (size_t)0);
+    if (!aligned(workspace, 256)) return fail(SENSE_ERR_MISALIGNED, "workspace must be 256-byte aligned");
     hipStream_t st = (hipStream_t)stream;
     hipError_t e;
     if ((e = timer_mark(SENSE_TIMER_PROJECT, 0, st)) != hipSuccess) return hip_fail(e, "timer");

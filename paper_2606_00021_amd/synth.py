@@ -38,6 +38,7 @@ class Workload:
     n_outliers: int
     verify_queries: int  # queries whose k drafts are verified (groups)
     metric: str = "cosine"
+    proj: int = 0        # PCA dimension of the searched keys (0: the hidden states as-is)
 
     @property
     def key_bytes(self) -> int:
@@ -67,6 +68,12 @@ WORKLOADS = {
                  16_384, 4, 16),
         Workload("70b-8m-d8192", 8_388_608, 8192, "bf16", 64, 128, 12, 128_256, "f32",
                  16_384, 16, 4),
+        # The paper's own key geometry: the headline store projected 4096 -> 64 by
+        # PCA and L2-normalised (bf16), the query projected the same way each step.
+        Workload("store-1m-pca64", 1_048_576, 4096, "bf16", 1, 64, 8, 152_064, "bf16",
+                 4096, 8, 1, proj=64),
+        Workload("store-1m-pca64-q64", 1_048_576, 4096, "bf16", 64, 64, 8, 152_064, "bf16",
+                 4096, 8, 1, proj=64),
     ]
 }
 HEADLINE = "store-1m-d4096"
