@@ -63,8 +63,13 @@ def _load():
         lib.oracle_select_candidates.argtypes = [P, P, P, I32, P, P, P, I32, I32, I32, I32, D, D,
                                                  D, I32, I32, P, P, P, P]
         lib.oracle_project.argtypes = [P, ctypes.c_int, I64, I32, I64, P, P, I32, I32, P]
+        lib.oracle_ivf_assign.argtypes = [P, ctypes.c_int, I64, I32, I64, P, I32, ctypes.c_int, P, P]
+        lib.oracle_pq_encode.argtypes = [P, ctypes.c_int, I64, I32, I64, P, P, P, I32, I32, P]
+        lib.oracle_ivf_search.argtypes = [P, I32, P, I32, ctypes.c_int, I32, P, I64, P,
+                                          ctypes.c_int, I64, P, P, I32, I32, I32, P, P, P, P]
         for f in ("oracle_scores", "oracle_topk", "oracle_gather", "oracle_row_stats",
-                  "oracle_soft_gate_verify", "oracle_select_candidates", "oracle_project"):
+                  "oracle_soft_gate_verify", "oracle_select_candidates", "oracle_project",
+                  "oracle_ivf_assign", "oracle_pq_encode", "oracle_ivf_search"):
             getattr(lib, f).restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -233,6 +238,63 @@ def project(x, x_dtype: str, basis, mean=None, normalize: bool = True,
     if rc:
         raise ValueError("oracle_project rejected its arguments")
     return out
+
+
+def ivf_assign(keys, key_dtype: str, centroids, metric: str = "cosine"):
+    """List of every key (most similar centroid, ties lower id) and that
+    similarity: (lists int32 [n], scores float64 [n])."""
+    keys = _raw(keys, key_dtype)
+    n, d = keys.shape
+    cen = np.ascontiguousarray(centroids, dtype=np.float64)
+    lists = np.empty(n, dtype=np.int32)
+    sc = np.empty(n, dtype=np.float64)
+    if _load().oracle_ivf_assign(_ptr(keys), DTYPES[key_dtype], n, d, d, _ptr(cen), cen.shape[0],
+                                 METRICS[metric], _ptr(lists), _ptr(sc)):
+        raise ValueError("oracle_ivf_assign rejected its arguments")
+    return lists, sc
+
+
+def pq_encode(keys, key_dtype: str, centroids, lists, codebooks):
+    """PQ codes (n x m uint8) of the residuals key - centroid[list];
+    codebooks is m x ksub x dsub."""
+    keys = _raw(keys, key_dtype)
+    n, d = keys.shape
+    cen = np.ascontiguousarray(centroids, dtype=np.float64)
+    lists = np.ascontiguousarray(lists, dtype=np.int32)
+    cb = np.ascontiguousarray(codebooks, dtype=np.float64)
+    m, ksub, _ = cb.shape
+    codes = np.empty((n, m), dtype=np.uint8)
+    if _load().oracle_pq_encode(_ptr(keys), DTYPES[key_dtype], n, d, d, _ptr(cen), _ptr(lists),
+                                _ptr(cb), m, ksub, _ptr(codes)):
+        raise ValueError("oracle_pq_encode rejected its arguments")
+    return codes
+
+
+def ivf_search(query, centroids, lists, nprobe: int, k: int, metric: str = "cosine",
+               keys=None, key_dtype: str = "bf16", codes=None, codebooks=None):
+    """IVF-Flat (keys given) or IVF-PQ (codes and codebooks given) search of
+    one fp64 query.  Returns (probe [nprobe] int32, coarse [nlist] float64,
+    ids [k] int64, scores [k] float64)."""
+    q = np.ascontiguousarray(query, dtype=np.float64).ravel()
+    cen = np.ascontiguousarray(centroids, dtype=np.float64)
+    nlist, d = cen.shape
+    lists = np.ascontiguousarray(lists, dtype=np.int32)
+    n = lists.shape[0]
+    kk = None if keys is None else _raw(keys, key_dtype)
+    cd = None if codes is None else np.ascontiguousarray(codes, dtype=np.uint8)
+    cb = None if codebooks is None else np.ascontiguousarray(codebooks, dtype=np.float64)
+    m, ksub = (cb.shape[0], cb.shape[1]) if cb is not None else (0, 0)
+    probe = np.empty(nprobe, dtype=np.int32)
+    coarse = np.empty(nlist, dtype=np.float64)
+    ids = np.empty(k, dtype=np.int64)
+    sc = np.empty(k, dtype=np.float64)
+    rc = _load().oracle_ivf_search(_ptr(q), d, _ptr(cen), nlist, METRICS[metric], nprobe,
+                                   _ptr(lists), n, _ptr(kk), DTYPES[key_dtype], d, _ptr(cd),
+                                   _ptr(cb), m, ksub, k, _ptr(probe), _ptr(coarse), _ptr(ids),
+                                   _ptr(sc))
+    if rc:
+        raise ValueError("oracle_ivf_search rejected its arguments")
+    return probe, coarse, ids, sc
 
 
 def dynamic_spans(tokens, max_span: int):

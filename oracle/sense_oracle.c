@@ -489,3 +489,171 @@ int oracle_project(const void *x, int x_dtype, int64_t n, int32_t d_in, int64_t 
     }
     return 0;
 }
+
+/* ---------------------------------------------------------------- IVF / IVF-PQ */
+
+/* Similarity of a key row to a double vector under the index metric:
+ * inner product, or cosine (0 when either norm is 0). */
+static double sim_row(const void *keys, int key_dtype, int64_t off, int32_t d, const double *v,
+                      int metric)
+{
+    double dot = 0.0, kn = 0.0, vn = 0.0;
+    for (int32_t t = 0; t < d; ++t) {
+        double x = elem(keys, key_dtype, off + t);
+        dot += x * v[t];
+        kn += x * x;
+        vn += v[t] * v[t];
+    }
+    if (metric == 0) return dot;
+    return (kn == 0.0 || vn == 0.0) ? 0.0 : dot / (sqrt(kn) * sqrt(vn));
+}
+
+/* Coarse quantizer of the inverted file (the FAISS IVF index of the
+ * implementation details): each key joins the list of the centroid it is most
+ * similar to under the index metric (ties: lower list id). */
+int oracle_ivf_assign(const void *keys, int key_dtype, int64_t n, int32_t d, int64_t key_stride,
+                      const double *centroids, int32_t nlist, int metric, int32_t *out_list,
+                      double *out_score)
+{
+    if (!keys || !centroids || !out_list || nlist < 1 || d < 1 || key_stride < d ||
+        !dtype_ok(key_dtype))
+        return -1;
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; ++i) {
+        int32_t best = 0;
+        double bs = -INFINITY;
+        for (int32_t l = 0; l < nlist; ++l) {
+            double s = sim_row(keys, key_dtype, i * key_stride, d, centroids + (int64_t)l * d, metric);
+            if (s > bs) { bs = s; best = l; }
+        }
+        out_list[i] = best;
+        if (out_score) out_score[i] = bs;
+    }
+    return 0;
+}
+
+/* Product quantizer of the residuals (IVF-PQ, m sub-quantizers of
+ * dsub = d / m dimensions, ksub centroids each): code j of key i is the
+ * codebook entry nearest (squared L2, ties: lower entry) to the j-th slice of
+ * r_i = key_i - centroid[list_i].  codebooks is m x ksub x dsub. */
+int oracle_pq_encode(const void *keys, int key_dtype, int64_t n, int32_t d, int64_t key_stride,
+                     const double *centroids, const int32_t *list_ids, const double *codebooks,
+                     int32_t m, int32_t ksub, uint8_t *out_codes)
+{
+    if (!keys || !centroids || !list_ids || !codebooks || !out_codes || m < 1 || d % m != 0 ||
+        ksub < 1 || ksub > 256 || !dtype_ok(key_dtype))
+        return -1;
+    int32_t dsub = d / m;
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; ++i) {
+        const double *c = centroids + (int64_t)list_ids[i] * d;
+        for (int32_t j = 0; j < m; ++j) {
+            int32_t best = 0;
+            double bd = INFINITY;
+            for (int32_t e = 0; e < ksub; ++e) {
+                const double *cb = codebooks + ((int64_t)j * ksub + e) * dsub;
+                double dist = 0.0;
+                for (int32_t t = 0; t < dsub; ++t) {
+                    double r = elem(keys, key_dtype, i * key_stride + j * dsub + t) - c[j * dsub + t];
+                    double df = r - cb[t];
+                    dist += df * df;
+                }
+                if (dist < bd) { bd = dist; best = e; }
+            }
+            out_codes[i * m + j] = (uint8_t)best;
+        }
+    }
+    return 0;
+}
+
+typedef struct { double s; int32_t i; } scored_list;
+
+static int cmp_lists(const void *pa, const void *pb)
+{
+    const scored_list *a = (const scored_list *)pa, *b = (const scored_list *)pb;
+    int an = isnan(a->s), bn = isnan(b->s);
+    if (an != bn) return an ? 1 : -1;
+    if (!an) {
+        if (a->s > b->s) return -1;
+        if (a->s < b->s) return 1;
+    }
+    return (a->i < b->i) ? -1 : (a->i > b->i);
+}
+
+/* IVF search of one query (exact re-ranking inside the probed lists for
+ * IVF-Flat, asymmetric distance computation for IVF-PQ):
+ *   coarse[l] = sim(q, centroid l) under the index metric;
+ *   probe     = the nprobe lists with the largest coarse score (full sort,
+ *               ties: lower list id);
+ *   candidates = every key whose list is probed, scored by
+ *     IVF-Flat: the exact similarity of the key (as oracle_scores), or
+ *     IVF-PQ (codes != NULL): u . (centroid[list] + reconstruction), with
+ *       u = q (IP) or q / ||q|| (cosine) and the reconstruction the
+ *       concatenated codebook entries of the key's codes;
+ *   result    = the k best candidates, full sort (score desc, row asc); k may
+ *               exceed the candidate count: the tail is id -1, score NaN.
+ * query is d doubles. */
+int oracle_ivf_search(const double *query, int32_t d, const double *centroids, int32_t nlist,
+                      int metric, int32_t nprobe, const int32_t *list_ids, int64_t n,
+                      const void *keys, int key_dtype, int64_t key_stride,
+                      const uint8_t *codes, const double *codebooks, int32_t m, int32_t ksub,
+                      int32_t k, int32_t *out_probe, double *out_coarse, int64_t *out_ids,
+                      double *out_scores)
+{
+    if (!query || !centroids || !list_ids || nlist < 1 || nprobe < 1 || nprobe > nlist ||
+        k < 1 || (!codes && !keys) || (codes && (!codebooks || m < 1 || d % m != 0)))
+        return -1;
+    double qn = 0.0;
+    for (int32_t t = 0; t < d; ++t) qn += query[t] * query[t];
+    qn = sqrt(qn);
+    scored_list *ls = (scored_list *)malloc(sizeof(scored_list) * (size_t)nlist);
+    if (!ls) return -1;
+    for (int32_t l = 0; l < nlist; ++l) {
+        const double *c = centroids + (int64_t)l * d;
+        double dot = 0.0, cn = 0.0;
+        for (int32_t t = 0; t < d; ++t) { dot += query[t] * c[t]; cn += c[t] * c[t]; }
+        cn = sqrt(cn);
+        ls[l].s = metric == 0 ? dot : ((cn == 0.0 || qn == 0.0) ? 0.0 : dot / (qn * cn));
+        ls[l].i = l;
+        if (out_coarse) out_coarse[l] = ls[l].s;
+    }
+    qsort(ls, (size_t)nlist, sizeof(scored_list), cmp_lists);
+    char *probed = (char *)calloc((size_t)nlist, 1);
+    if (!probed) { free(ls); return -1; }
+    for (int32_t p = 0; p < nprobe; ++p) {
+        probed[ls[p].i] = 1;
+        if (out_probe) out_probe[p] = ls[p].i;
+    }
+    int64_t cnt = 0;
+    for (int64_t i = 0; i < n; ++i) cnt += probed[list_ids[i]];
+    scored_row *cand = (scored_row *)malloc(sizeof(scored_row) * (size_t)(cnt > 0 ? cnt : 1));
+    if (!cand) { free(ls); free(probed); return -1; }
+    int32_t dsub = codes ? d / m : 0;
+    double u_scale = (metric == 0 || qn == 0.0) ? 1.0 : 1.0 / qn;
+    int64_t c = 0;
+    for (int64_t i = 0; i < n; ++i) {
+        if (!probed[list_ids[i]]) continue;
+        double s;
+        if (!codes) {
+            s = sim_row(keys, key_dtype, i * key_stride, d, query, metric);
+        } else {
+            const double *cen = centroids + (int64_t)list_ids[i] * d;
+            s = 0.0;
+            for (int32_t j = 0; j < m; ++j) {
+                const double *cb = codebooks + ((int64_t)j * ksub + codes[i * m + j]) * dsub;
+                for (int32_t t = 0; t < dsub; ++t)
+                    s += (query[j * dsub + t] * u_scale) * (cen[j * dsub + t] + cb[t]);
+            }
+        }
+        cand[c].s = s;
+        cand[c].i = i;
+        ++c;
+    }
+    qsort(cand, (size_t)cnt, sizeof(scored_row), cmp_rows);
+    for (int32_t r = 0; r < k; ++r) {
+        out_ids[r] = r < cnt ? cand[r].i : -1;
+        out_scores[r] = r < cnt ? cand[r].s : NAN;
+    }
+    free(ls); free(probed); free(cand);
+    return 0;
+}
