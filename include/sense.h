@@ -34,6 +34,10 @@
  *                           soft-gated evaluation reading the flattened
  *                           tree's logits through Gamma (Sec. 3.2 Eq. 11;
  *                           Sec. 3.3; Alg. 4)
+ *   sense_ivf_assign, sense_pq_encode, sense_build_ivf_index, sense_ivf_search
+ *                           the inverted-file ANN retrieval the paper uses
+ *                           (FAISS IVF-PQ of the implementation details):
+ *                           IVF-Flat and IVF-PQ over the same top-k kernels
  *   sense_project           PCA projection + L2 normalisation of hidden
  *                           states: the query k = L2Norm(PCA(h)) of Alg. 2
  *                           and the projected datastore keys (Sec. 3.2
@@ -213,7 +217,8 @@ sense_status_t sense_retrieve_workspace_size(const sense_index_t *index, int32_t
  *   workspace    device scratch of at least sense_retrieve_workspace_size
  *                bytes, 256-byte aligned; its contents are not preserved.
  * Errors: INVALID_ARGUMENT, UNSUPPORTED (k > 1024), MISALIGNED,
- * WORKSPACE, HIP. */
+ * WORKSPACE, HIP.  An inverted-file index is searched with sense_ivf_search
+ * instead (INVALID_ARGUMENT here). */
 sense_status_t sense_retrieve(const sense_index_t *index, const void *queries,
                               sense_dtype_t q_dtype, int32_t n_queries, int32_t k,
                               int64_t *out_ids, float *out_scores, int32_t *out_drafts,
@@ -484,6 +489,98 @@ sense_status_t sense_project(const sense_projection_t *proj, const void *x,
                              sense_dtype_t out_dtype, int64_t out_stride, void *workspace,
                              size_t workspace_bytes, void *stream);
 
+/* ---- Inverted file (the ANN retriever of Sec. 3.2 Eq. 7; App.
+ * implementation details: FAISS IVF-PQ, nlist 4096, nprobe 32, pq_m 16).
+ * The k-means fits of the coarse centroids and of the PQ codebooks are not
+ * part of this library; assignment, encoding, the index layout and the search
+ * are.  Key dimension d <= 128, d % 8 == 0 (the paper's keys are 64-dim). */
+
+/* List of every key: the centroid it is most similar to under `metric`
+ * (inner product, or cosine), accumulated in fp32; ties to the lower list.
+ *   keys       n x d of key_dtype (F16/BF16), row stride key_stride.
+ *   centroids  nlist x d fp32 (DEVICE), 1 <= nlist <= 65536.
+ *   out_list   n int32 (DEVICE).
+ * Errors: INVALID_ARGUMENT, MISALIGNED, HIP. */
+sense_status_t sense_ivf_assign(const void *keys, sense_dtype_t key_dtype, int64_t n, int32_t d,
+                                int64_t key_stride, const float *centroids, int32_t nlist,
+                                sense_metric_t metric, int32_t *out_list, void *stream);
+
+/* Product-quantisation codes of the residuals r_i = key_i - centroid[list_i]
+ * (IVF-PQ): code j of key i = the entry of codebook j nearest to the j-th
+ * d/m-dim slice of r_i (squared L2 in fp32, ties to the lower entry).
+ *   codebooks  m x ksub x (d/m) fp32 (DEVICE); d % m == 0, d/m <= 16,
+ *              1 <= ksub <= 256, ksub * d <= 16384.
+ *   list_ids   n int32 (a list outside [0, nlist) gives code 0 throughout).
+ *   out_codes  n x m uint8 (DEVICE).
+ * Errors: INVALID_ARGUMENT, MISALIGNED, HIP. */
+sense_status_t sense_pq_encode(const void *keys, sense_dtype_t key_dtype, int64_t n, int32_t d,
+                               int64_t key_stride, const float *centroids, int32_t nlist,
+                               const int32_t *list_ids, const float *codebooks, int32_t m,
+                               int32_t ksub, uint8_t *out_codes, void *stream);
+
+/* Inverted-file index descriptor.
+ *   keys ... metric  as sense_index_desc_t; keys may be NULL for IVF-PQ.
+ *   centroids        nlist x d fp32 (copied into the index).
+ *   list_ids         n int32, every key's list (e.g. sense_ivf_assign).
+ *   pq_codebooks     NULL: IVF-Flat (exact scores inside the probed lists);
+ *                    else pq_m x pq_ksub x (d/pq_m) fp32 (copied), and
+ *   pq_codes         n x pq_m uint8, every key's codes (e.g.
+ *                    sense_pq_encode), values < pq_ksub. */
+typedef struct {
+    const void *keys;
+    sense_dtype_t key_dtype;
+    int64_t n;
+    int32_t d;
+    int64_t key_stride;
+    const int32_t *spans;
+    int32_t max_span;
+    const int32_t *span_len;
+    sense_metric_t metric;
+    const float *centroids;
+    int32_t nlist;
+    const int32_t *list_ids;
+    const float *pq_codebooks;
+    int32_t pq_m;
+    int32_t pq_ksub;
+    const uint8_t *pq_codes;
+} sense_ivf_desc_t;
+
+/* Build an inverted-file index: each list's rows stored contiguously (the
+ * keys for IVF-Flat, with their 1/||k|| for cosine; the codes for IVF-PQ)
+ * with their original row ids.  The spans stay borrowed.  This call
+ * synchronises `stream` once: it reads the list sizes back to size the
+ * search buffers.  Errors: INVALID_ARGUMENT (also for list ids outside
+ * [0, nlist) or codes >= pq_ksub, found on the device), MISALIGNED,
+ * OUT_OF_MEMORY, HIP. */
+sense_status_t sense_build_ivf_index(const sense_ivf_desc_t *desc, void *stream,
+                                     sense_index_t **out);
+
+/* Bytes of device workspace sense_ivf_search needs. */
+sense_status_t sense_ivf_search_workspace_size(const sense_index_t *index, int32_t n_queries,
+                                               int32_t k, int32_t nprobe, size_t *bytes);
+
+/* Inverted-file search (Sec. 3.2 Eq. 7 with the paper's ANN retriever):
+ *   coarse[l] = sim(q, centroid l) (IP, or cosine), in fp32;
+ *   probes    = the nprobe lists with the largest coarse scores (ties: lower
+ *               list id);
+ *   each row of a probed list is scored: IVF-Flat as sense_retrieve scores
+ *   it; IVF-PQ as u.c_l + sum_j LUT[j][code_j] with u = q (IP) or q/||q||
+ *   (cosine), LUT[j][c] = u_j . codebook_j[c], summed in fp32 in the order
+ *   j = 0..m-1, then added to u.c_l;
+ *   the k best rows (score desc, original row asc), their continuations.
+ * Fewer than k candidates: the tail has id -1, score NaN, an empty draft.
+ *   queries    n_queries x d (F32 or the key dtype), 16-byte aligned.
+ *   1 <= k <= 1024; 1 <= nprobe <= min(nlist, 1024).
+ *   out_*      as sense_retrieve (out_ids required).
+ *   out_probe  n_queries x nprobe int64 probed lists (best first), or NULL.
+ * Errors: INVALID_ARGUMENT (also for an index that is not an inverted file),
+ * UNSUPPORTED, MISALIGNED, WORKSPACE, HIP. */
+sense_status_t sense_ivf_search(const sense_index_t *index, const void *queries,
+                                sense_dtype_t q_dtype, int32_t n_queries, int32_t k,
+                                int32_t nprobe, int64_t *out_ids, float *out_scores,
+                                int32_t *out_drafts, int32_t *out_draft_len, int64_t *out_probe,
+                                void *workspace, size_t workspace_bytes, void *stream);
+
 /* Diagnostics for benchmarks and profilers.  Which part of the path a pair
  * of timing events brackets. */
 typedef enum {
@@ -492,7 +589,8 @@ typedef enum {
     SENSE_TIMER_VERIFY = 2, /* both kernels of sense_soft_gate_verify(_tree) */
     SENSE_TIMER_SELECT = 3, /* the kernel of sense_select_candidates */
     SENSE_TIMER_TRIE = 4,   /* the kernels of sense_build_loose_trie */
-    SENSE_TIMER_PROJECT = 5 /* the kernels of sense_project */
+    SENSE_TIMER_PROJECT = 5, /* the kernels of sense_project */
+    SENSE_TIMER_IVF = 6      /* the kernels of sense_ivf_search */
 } sense_timer_t;
 
 /* Register two hipEvent_t handles (created by the caller with timing

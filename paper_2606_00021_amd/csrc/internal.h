@@ -26,6 +26,9 @@ constexpr int kMaxNodes = 4096;     // largest group x draft length of the loose
 constexpr int kMaxProjOut = 256;    // largest projected dimension
 constexpr int kProjMfmaMinRows = 256;   // 16-bit projections of this many rows use MFMA
 constexpr int kSmallDim = 64;       // keys this short use the short-row scan
+constexpr int kMaxIvfDim = 128;     // largest key dimension of an inverted-file index
+constexpr int kMaxDsub = 16;        // largest PQ sub-vector
+constexpr int kMaxNlist = 65536;    // most inverted lists
 
 // Order-preserving map of an fp32 score to an unsigned key: larger score ->
 // larger key; every NaN -> 0 (below everything); -0 is folded onto +0.
@@ -124,6 +127,67 @@ hipError_t launch_project(const void* x, int x_dtype, int64_t n, int d_in, int64
                           const float* mean, const float* basis, int d_out, int normalize,
                           void* out, int out_dtype, int64_t out_stride, void* workspace,
                           hipStream_t stream);
+
+// Top-k of packed keys (nq x count, padding key 0) in the order of the
+// keys, with the gather; ids of padding keys are -1.
+hipError_t launch_topk_keys(const uint64_t* keys, int64_t count, int nq, int k,
+                            const int32_t* spans, const int32_t* span_len, int max_span,
+                            int64_t span_stride, int64_t* out_ids, float* out_scores,
+                            int32_t* out_drafts, int32_t* out_draft_len, void* workspace,
+                            hipStream_t stream);
+
+// Inverted file (ivf.hip).
+hipError_t launch_ivf_assign(const void* keys, int key_dtype, int64_t n, int d, int64_t ld,
+                             const float* centroids, int nlist, int cosine, int32_t* out_list,
+                             hipStream_t stream);
+hipError_t launch_pq_encode(const void* keys, int key_dtype, int64_t n, int d, int64_t ld,
+                            const float* centroids, int nlist, const int32_t* list_ids,
+                            const float* codebooks, int m, int ksub, uint8_t* codes,
+                            hipStream_t stream);
+hipError_t launch_f32_inv_norms(const float* rows, int n, int d, float* inv, hipStream_t stream);
+// Counting sort of the rows by list; counts has nlist + 2 entries (the last
+// two count out-of-range list ids and codes).
+hipError_t launch_ivf_layout(const int32_t* list_ids, int64_t n, int nlist, const void* keys,
+                             int64_t ld, int d, const uint8_t* codes, int m, int ksub,
+                             int32_t* counts, int64_t* offsets, int32_t* cursor,
+                             int32_t* row_ids, void* keys_sorted, uint8_t* codes_sorted,
+                             hipStream_t stream);
+
+struct IvfSearch {
+    const float* queries;      // nq x d fp32
+    int d, nq;
+    const float* centroids;    // nlist x d fp32
+    const float* cen_inv;      // nlist (cosine)
+    int nlist, cosine;
+    float* coarse;             // nq x nlist
+    float* coarse_ip;          // nq x nlist (PQ)
+    int64_t* probe;            // nq x nprobe
+    void* probe_ws;
+    int nprobe;
+    const int64_t* offsets;    // nlist + 1
+    int32_t* base;             // nq x nprobe
+    int64_t cap;               // candidate slots per query
+    uint64_t* cand;            // nq x cap
+    const uint8_t* codes_sorted;   // PQ, NULL for Flat
+    int m, ksub;
+    const float* codebooks;
+    float* lut;                // nq x m x ksub
+    const void* keys_sorted;   // Flat
+    int key_dtype;
+    const float* inv_norm;     // Flat cosine, per sorted row
+    const int32_t* row_ids;    // sorted position -> original row
+    int k;
+    const int32_t* spans;
+    const int32_t* span_len;
+    int max_span;
+    int64_t span_stride;
+    int64_t* out_ids;
+    float* out_scores;
+    int32_t* out_drafts;
+    int32_t* out_draft_len;
+    void* final_ws;
+};
+hipError_t launch_ivf_search(const IvfSearch& s, hipStream_t stream);
 
 // Plain streaming read of a device buffer (bandwidth probe).
 hipError_t launch_stream_read(const void* buf, size_t bytes, uint32_t* sink, hipStream_t stream);

@@ -7,6 +7,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <new>
 
 #include "internal.h"
@@ -32,6 +33,18 @@ struct sense_index {
     int64_t capacity;
     int32_t* owned_hist;
     int32_t* owned_span_len;
+    // Inverted file only (nlist > 0).
+    int32_t nlist;
+    float* centroids;        // nlist x d
+    float* cen_inv;          // nlist
+    int32_t* counts;         // nlist + 2
+    int32_t* cursor;         // nlist
+    int64_t* offsets;        // nlist + 1
+    int32_t* row_ids;        // n
+    uint8_t* codes_sorted;   // n x pq_m (PQ)
+    float* codebooks;        // pq_m x pq_ksub x d / pq_m (PQ)
+    int32_t pq_m, pq_ksub;
+    int64_t* cap_prefix;     // host: sums of the p largest list sizes, p = 0..nlist
 };
 
 namespace {
@@ -39,7 +52,7 @@ namespace {
 thread_local char g_msg[512];
 
 // Timing events per sense_timer_t, set by sense_set_timer_events.
-constexpr int kTimers = 6;
+constexpr int kTimers = 7;
 thread_local hipEvent_t g_timer[kTimers][2] = {};
 
 hipError_t timer_mark(int which, int edge, hipStream_t st) {
@@ -285,6 +298,11 @@ SENSE_EXPORT sense_status_t sense_destroy_index(sense_index_t* ix) {
     if (ix->owned_keys) (void)hipFree(ix->owned_keys);
     if (ix->owned_hist) (void)hipFree(ix->owned_hist);
     if (ix->owned_span_len) (void)hipFree(ix->owned_span_len);
+    for (void* p : {(void*)ix->centroids, (void*)ix->cen_inv, (void*)ix->counts,
+                    (void*)ix->cursor, (void*)ix->offsets, (void*)ix->row_ids,
+                    (void*)ix->codes_sorted, (void*)ix->codebooks})
+        if (p) (void)hipFree(p);
+    delete[] ix->cap_prefix;
     delete ix;
     if (e != hipSuccess) return hip_fail(e, "destroy");
     return ok();
@@ -304,6 +322,9 @@ SENSE_EXPORT sense_status_t sense_index_info(const sense_index_t* ix, int64_t* n
 
 static sense_status_t check_retrieve_sizes(const sense_index_t* ix, int32_t nq, int32_t k) {
     if (!ix) return fail(SENSE_ERR_INVALID_ARGUMENT, "index is NULL");
+    if (ix->nlist > 0)
+        return fail(SENSE_ERR_INVALID_ARGUMENT,
+                    "an inverted-file index is searched with sense_ivf_search");
     if (nq < 1) return fail(SENSE_ERR_INVALID_ARGUMENT, "n_queries = %d < 1", nq);
     if (k < 1) return fail(SENSE_ERR_INVALID_ARGUMENT, "k = %d < 1", k);
     if (k > sense::kMaxK) return fail(SENSE_ERR_UNSUPPORTED, "k = %d > %d", k, sense::kMaxK);
@@ -689,5 +710,304 @@ SENSE_EXPORT sense_status_t sense_project(const sense_projection_t* proj, const 
                               workspace, st);
     if (e != hipSuccess) return hip_fail(e, "projection");
     if ((e = timer_mark(SENSE_TIMER_PROJECT, 1, st)) != hipSuccess) return hip_fail(e, "timer");
+    return ok();
+}
+
+// ------------------------------------------------------------ inverted file
+
+static sense_status_t check_ivf_keys(const void* keys, sense_dtype_t key_dtype, int64_t n,
+                                     int32_t d, int64_t key_stride) {
+    if (key_dtype != SENSE_F16 && key_dtype != SENSE_BF16)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "key_dtype must be SENSE_F16 or SENSE_BF16");
+    if (n < 1 || n > 0x7FFFFFFFLL)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "n = %lld outside [1, 2^31-1]", (long long)n);
+    if (d < 8 || d > sense::kMaxIvfDim || d % 8 != 0)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "d = %d must be a multiple of 8 in [8, %d]", d,
+                    sense::kMaxIvfDim);
+    if (key_stride < d)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "key_stride %lld < d %d", (long long)key_stride, d);
+    if (keys && (!aligned(keys, 16) || key_stride % 8 != 0))
+        return fail(SENSE_ERR_MISALIGNED, "keys must be 16-byte aligned with key_stride %% 8 == 0");
+    return SENSE_OK;
+}
+
+static sense_status_t check_pq(int32_t d, int32_t m, int32_t ksub) {
+    if (m < 1 || d % m != 0 || d / m > sense::kMaxDsub)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "pq_m = %d must divide d = %d into <= %d dims", m,
+                    d, sense::kMaxDsub);
+    if (ksub < 1 || ksub > 256 || (int64_t)ksub * d > 16384)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "ksub = %d must be in [1, 256] with ksub * d <= 16384",
+                    ksub);
+    return SENSE_OK;
+}
+
+SENSE_EXPORT sense_status_t sense_ivf_assign(const void* keys, sense_dtype_t key_dtype, int64_t n,
+                                             int32_t d, int64_t key_stride,
+                                             const float* centroids, int32_t nlist,
+                                             sense_metric_t metric, int32_t* out_list,
+                                             void* stream) {
+    sense_status_t s = check_ivf_keys(keys, key_dtype, n, d, key_stride);
+    if (s != SENSE_OK) return s;
+    if (!keys || !centroids || !out_list)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "keys, centroids and out_list must be non-NULL");
+    if (nlist < 1 || nlist > sense::kMaxNlist)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "nlist = %d outside [1, %d]", nlist, sense::kMaxNlist);
+    if (metric != SENSE_METRIC_IP && metric != SENSE_METRIC_COSINE)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "unknown metric %d", (int)metric);
+    if (!aligned(centroids, 4) || !aligned(out_list, 4))
+        return fail(SENSE_ERR_MISALIGNED, "centroids and out_list must be 4-byte aligned");
+    hipError_t e = sense::launch_ivf_assign(keys, key_dtype, n, d, key_stride, centroids, nlist,
+                                            metric == SENSE_METRIC_COSINE, out_list,
+                                            (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "ivf assign");
+    return ok();
+}
+
+SENSE_EXPORT sense_status_t sense_pq_encode(const void* keys, sense_dtype_t key_dtype, int64_t n,
+                                            int32_t d, int64_t key_stride,
+                                            const float* centroids, int32_t nlist,
+                                            const int32_t* list_ids, const float* codebooks,
+                                            int32_t m, int32_t ksub, uint8_t* out_codes,
+                                            void* stream) {
+    sense_status_t s = check_ivf_keys(keys, key_dtype, n, d, key_stride);
+    if (s != SENSE_OK) return s;
+    if ((s = check_pq(d, m, ksub)) != SENSE_OK) return s;
+    if (!keys || !centroids || !list_ids || !codebooks || !out_codes)
+        return fail(SENSE_ERR_INVALID_ARGUMENT,
+                    "keys, centroids, list_ids, codebooks and out_codes must be non-NULL");
+    if (nlist < 1 || nlist > sense::kMaxNlist)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "nlist = %d outside [1, %d]", nlist, sense::kMaxNlist);
+    if (!aligned(centroids, 4) || !aligned(codebooks, 4) || !aligned(list_ids, 4))
+        return fail(SENSE_ERR_MISALIGNED, "centroids, codebooks and list_ids must be 4-byte aligned");
+    hipError_t e = sense::launch_pq_encode(keys, key_dtype, n, d, key_stride, centroids, nlist,
+                                           list_ids, codebooks, m, ksub, out_codes,
+                                           (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "pq encode");
+    return ok();
+}
+
+SENSE_EXPORT sense_status_t sense_build_ivf_index(const sense_ivf_desc_t* desc, void* stream,
+                                                  sense_index_t** out) {
+    if (!desc || !out) return fail(SENSE_ERR_INVALID_ARGUMENT, "desc and out must be non-NULL");
+    *out = nullptr;
+    const sense_ivf_desc_t& D = *desc;
+    const bool pq = D.pq_codebooks != nullptr;
+    sense_status_t s = check_ivf_keys(D.keys, D.key_dtype, D.n, D.d, D.key_stride);
+    if (s != SENSE_OK) return s;
+    if (pq && (s = check_pq(D.d, D.pq_m, D.pq_ksub)) != SENSE_OK) return s;
+    if ((!pq && !D.keys) || (pq && !D.pq_codes) || !D.spans || !D.centroids || !D.list_ids)
+        return fail(SENSE_ERR_INVALID_ARGUMENT,
+                    "spans, centroids, list_ids and keys (IVF-Flat) or pq_codes (IVF-PQ) must be "
+                    "non-NULL");
+    if (D.nlist < 1 || D.nlist > sense::kMaxNlist)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "nlist = %d outside [1, %d]", D.nlist,
+                    sense::kMaxNlist);
+    if (D.max_span < 1 || D.max_span > sense::kMaxLen)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "max_span = %d outside [1, %d]", D.max_span,
+                    sense::kMaxLen);
+    if (D.metric != SENSE_METRIC_IP && D.metric != SENSE_METRIC_COSINE)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "unknown metric %d", (int)D.metric);
+    sense_index* ix = new (std::nothrow) sense_index();
+    if (!ix) return fail(SENSE_ERR_OUT_OF_MEMORY, "host allocation failed");
+    ix->key_dtype = D.key_dtype;
+    ix->n = D.n;
+    ix->d = D.d;
+    ix->ld = D.d;
+    ix->spans = D.spans;
+    ix->max_span = D.max_span;
+    ix->span_len = D.span_len;
+    ix->span_stride = D.max_span;
+    ix->metric = D.metric;
+    ix->nlist = D.nlist;
+    ix->pq_m = pq ? D.pq_m : 0;
+    ix->pq_ksub = pq ? D.pq_ksub : 0;
+    hipStream_t st = (hipStream_t)stream;
+    const size_t n = (size_t)D.n, nl = (size_t)D.nlist;
+    hipError_t e = hipSuccess;
+    auto alloc = [&](void** p, size_t bytes) {
+        if (e == hipSuccess) e = hipMalloc(p, bytes);
+    };
+    alloc((void**)&ix->centroids, nl * D.d * sizeof(float));
+    alloc((void**)&ix->cen_inv, nl * sizeof(float));
+    alloc((void**)&ix->counts, (nl + 2) * sizeof(int32_t));
+    alloc((void**)&ix->cursor, nl * sizeof(int32_t));
+    alloc((void**)&ix->offsets, (nl + 1) * sizeof(int64_t));
+    alloc((void**)&ix->row_ids, n * sizeof(int32_t));
+    if (pq) {
+        alloc((void**)&ix->codes_sorted, n * D.pq_m);
+        alloc((void**)&ix->codebooks, (size_t)D.pq_ksub * D.d * sizeof(float));
+    } else {
+        alloc(&ix->owned_keys, n * D.d * 2);
+        if (D.metric == SENSE_METRIC_COSINE) alloc((void**)&ix->inv_norm, n * sizeof(float));
+    }
+    ix->cap_prefix = new (std::nothrow) int64_t[nl + 1];
+    int32_t* host_counts = new (std::nothrow) int32_t[nl + 2];
+    if (e != hipSuccess || !ix->cap_prefix || !host_counts) {
+        delete[] host_counts;
+        (void)sense_destroy_index(ix);
+        return fail(SENSE_ERR_OUT_OF_MEMORY, "inverted-file index allocation failed");
+    }
+    ix->keys = ix->owned_keys;
+    e = hipMemcpyAsync(ix->centroids, D.centroids, nl * D.d * sizeof(float),
+                       hipMemcpyDeviceToDevice, st);
+    if (e == hipSuccess && pq)
+        e = hipMemcpyAsync(ix->codebooks, D.pq_codebooks, (size_t)D.pq_ksub * D.d * sizeof(float),
+                           hipMemcpyDeviceToDevice, st);
+    if (e == hipSuccess) e = sense::launch_f32_inv_norms(ix->centroids, D.nlist, D.d, ix->cen_inv, st);
+    if (e == hipSuccess)
+        e = sense::launch_ivf_layout(D.list_ids, D.n, D.nlist, D.keys, D.key_stride, D.d,
+                                     D.pq_codes, ix->pq_m, ix->pq_ksub, ix->counts, ix->offsets,
+                                     ix->cursor, ix->row_ids, pq ? nullptr : ix->owned_keys,
+                                     ix->codes_sorted, st);
+    if (e == hipSuccess && ix->inv_norm)
+        e = sense::launch_key_norms(ix->owned_keys, D.key_dtype, D.n, D.d, D.d, ix->inv_norm, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e == hipSuccess)
+        e = hipMemcpy(host_counts, ix->counts, (nl + 2) * sizeof(int32_t), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) {
+        delete[] host_counts;
+        (void)sense_destroy_index(ix);
+        return hip_fail(e, "inverted-file build");
+    }
+    if (host_counts[nl] != 0 || host_counts[nl + 1] != 0) {
+        const int bad_l = host_counts[nl], bad_c = host_counts[nl + 1];
+        delete[] host_counts;
+        (void)sense_destroy_index(ix);
+        return fail(SENSE_ERR_INVALID_ARGUMENT,
+                    "%d list ids outside [0, %d) and %d codes >= pq_ksub", bad_l, D.nlist, bad_c);
+    }
+    // Sums of the p largest list sizes: the candidate slots nprobe lists can need.
+    std::sort(host_counts, host_counts + nl, [](int32_t a, int32_t b) { return a > b; });
+    ix->cap_prefix[0] = 0;
+    for (size_t p = 0; p < nl; ++p) ix->cap_prefix[p + 1] = ix->cap_prefix[p] + host_counts[p];
+    delete[] host_counts;
+    *out = ix;
+    return ok();
+}
+
+namespace {
+
+struct IvfLayout {
+    size_t q_off, coarse_off, ip_off, probe_off, pws_off, base_off, lut_off, cand_off, fws_off,
+        total;
+    int64_t cap;
+};
+
+IvfLayout ivf_layout(const sense_index* ix, int nq, int k, int nprobe) {
+    IvfLayout l;
+    int64_t cap = ix->cap_prefix[nprobe];
+    if (cap < 1) cap = 1;
+    l.cap = cap;
+    size_t at = 0;
+    auto take = [&](size_t bytes) {
+        const size_t o = at;
+        at = round_up(at + bytes, 256);
+        return o;
+    };
+    l.q_off = take((size_t)nq * ix->d * sizeof(float));
+    l.coarse_off = take((size_t)nq * ix->nlist * sizeof(float));
+    l.ip_off = take(ix->pq_m ? (size_t)nq * ix->nlist * sizeof(float) : 0);
+    l.probe_off = take((size_t)nq * nprobe * sizeof(int64_t));
+    l.pws_off = take(sense::topk_workspace_bytes(ix->nlist, nq, nprobe));
+    l.base_off = take((size_t)nq * nprobe * sizeof(int32_t));
+    l.lut_off = take(ix->pq_m ? (size_t)nq * ix->pq_m * ix->pq_ksub * sizeof(float) : 0);
+    l.cand_off = take((size_t)nq * cap * sizeof(uint64_t));
+    l.fws_off = take(sense::topk_workspace_bytes(cap, nq, k));
+    l.total = at;
+    return l;
+}
+
+}  // namespace
+
+static sense_status_t check_ivf_search(const sense_index_t* ix, int32_t nq, int32_t k,
+                                       int32_t nprobe) {
+    if (!ix) return fail(SENSE_ERR_INVALID_ARGUMENT, "index is NULL");
+    if (ix->nlist < 1) return fail(SENSE_ERR_INVALID_ARGUMENT, "index is not an inverted file");
+    if (nq < 1) return fail(SENSE_ERR_INVALID_ARGUMENT, "n_queries = %d < 1", nq);
+    if (k < 1) return fail(SENSE_ERR_INVALID_ARGUMENT, "k = %d < 1", k);
+    if (k > sense::kMaxK) return fail(SENSE_ERR_UNSUPPORTED, "k = %d > %d", k, sense::kMaxK);
+    if (nprobe < 1 || nprobe > ix->nlist)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "nprobe = %d outside [1, %d]", nprobe, ix->nlist);
+    if (nprobe > sense::kMaxK) return fail(SENSE_ERR_UNSUPPORTED, "nprobe = %d > %d", nprobe, sense::kMaxK);
+    return SENSE_OK;
+}
+
+SENSE_EXPORT sense_status_t sense_ivf_search_workspace_size(const sense_index_t* ix, int32_t nq,
+                                                            int32_t k, int32_t nprobe,
+                                                            size_t* bytes) {
+    if (!bytes) return fail(SENSE_ERR_INVALID_ARGUMENT, "bytes is NULL");
+    const sense_status_t s = check_ivf_search(ix, nq, k, nprobe);
+    if (s != SENSE_OK) return s;
+    *bytes = ivf_layout(ix, nq, k, nprobe).total;
+    return ok();
+}
+
+SENSE_EXPORT sense_status_t sense_ivf_search(const sense_index_t* ix, const void* queries,
+                                             sense_dtype_t q_dtype, int32_t nq, int32_t k,
+                                             int32_t nprobe, int64_t* out_ids, float* out_scores,
+                                             int32_t* out_drafts, int32_t* out_draft_len,
+                                             int64_t* out_probe, void* workspace,
+                                             size_t workspace_bytes, void* stream) {
+    sense_status_t s = check_ivf_search(ix, nq, k, nprobe);
+    if (s != SENSE_OK) return s;
+    if (!queries || !out_ids)
+        return fail(SENSE_ERR_INVALID_ARGUMENT, "queries and out_ids must be non-NULL");
+    if (!dtype_ok(q_dtype)) return fail(SENSE_ERR_INVALID_ARGUMENT, "unknown q_dtype %d", (int)q_dtype);
+    if (!aligned(queries, q_dtype == SENSE_F32 ? 16 : 2))
+        return fail(SENSE_ERR_MISALIGNED, "fp32 queries must be 16-byte aligned");
+    const IvfLayout L = ivf_layout(ix, nq, k, nprobe);
+    if (!workspace || workspace_bytes < L.total)
+        return fail(SENSE_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", L.total,
+                    workspace ? workspace_bytes : (size_t)0);
+    if (!aligned(workspace, 256)) return fail(SENSE_ERR_MISALIGNED, "workspace must be 256-byte aligned");
+    hipStream_t st = (hipStream_t)stream;
+    char* ws = (char*)workspace;
+    hipError_t e;
+    const float* qptr = (const float*)queries;
+    if (q_dtype != SENSE_F32) {
+        if ((e = sense::launch_query_to_f32(queries, q_dtype, nq, ix->d, (float*)(ws + L.q_off),
+                                            st)) != hipSuccess)
+            return hip_fail(e, "query conversion");
+        qptr = (const float*)(ws + L.q_off);
+    }
+    sense::IvfSearch S{};
+    S.queries = qptr;
+    S.d = ix->d;
+    S.nq = nq;
+    S.centroids = ix->centroids;
+    S.cen_inv = ix->cen_inv;
+    S.nlist = ix->nlist;
+    S.cosine = ix->metric == SENSE_METRIC_COSINE;
+    S.coarse = (float*)(ws + L.coarse_off);
+    S.coarse_ip = ix->pq_m ? (float*)(ws + L.ip_off) : nullptr;
+    S.probe = out_probe ? out_probe : (int64_t*)(ws + L.probe_off);
+    S.probe_ws = ws + L.pws_off;
+    S.nprobe = nprobe;
+    S.offsets = ix->offsets;
+    S.base = (int32_t*)(ws + L.base_off);
+    S.cap = L.cap;
+    S.cand = (uint64_t*)(ws + L.cand_off);
+    S.codes_sorted = ix->codes_sorted;
+    S.m = ix->pq_m;
+    S.ksub = ix->pq_ksub;
+    S.codebooks = ix->codebooks;
+    S.lut = ix->pq_m ? (float*)(ws + L.lut_off) : nullptr;
+    S.keys_sorted = ix->owned_keys;
+    S.key_dtype = ix->key_dtype;
+    S.inv_norm = ix->inv_norm;
+    S.row_ids = ix->row_ids;
+    S.k = k;
+    S.spans = ix->spans;
+    S.span_len = ix->span_len;
+    S.max_span = ix->max_span;
+    S.span_stride = ix->span_stride;
+    S.out_ids = out_ids;
+    S.out_scores = out_scores;
+    S.out_drafts = out_drafts;
+    S.out_draft_len = out_draft_len;
+    S.final_ws = ws + L.fws_off;
+    if ((e = timer_mark(SENSE_TIMER_IVF, 0, st)) != hipSuccess) return hip_fail(e, "timer");
+    if ((e = sense::launch_ivf_search(S, st)) != hipSuccess) return hip_fail(e, "ivf search");
+    if ((e = timer_mark(SENSE_TIMER_IVF, 1, st)) != hipSuccess) return hip_fail(e, "timer");
     return ok();
 }

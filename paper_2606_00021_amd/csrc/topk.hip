@@ -198,7 +198,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
         bitonic_desc<kThreads>(s_sel, p);
         for (int r = tid; r < k; r += kThreads) {
             const uint64_t key = s_sel[r];
-            out_ids[(int64_t)q * k + r] = (int64_t)key_row(key);
+            out_ids[(int64_t)q * k + r] = key == 0 ? -1 : (int64_t)key_row(key);
             if (out_scores) out_scores[(int64_t)q * k + r] = key_score((uint32_t)(key >> 32));
         }
         if (out_drafts || out_draft_len) {
@@ -206,8 +206,9 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
                 const int r = t / max_span, j = t - r * max_span;
                 const uint64_t key = s_sel[r];
                 const int64_t id = (int64_t)key_row(key);
-                // A padding key (0) can only surface if k exceeded the row
-                // count, which the host rejects; it would give an empty draft.
+                // A padding key (0) surfaces only when fewer than k
+                // candidates exist (an inverted-file search of short lists):
+                // id -1, score NaN, an empty draft.
                 int len_r = (key == 0) ? 0 : (span_len ? span_len[id] : max_span);
                 len_r = len_r < 0 ? 0 : (len_r > max_span ? max_span : len_r);
                 const int64_t o = ((int64_t)q * k + r);
@@ -262,6 +263,35 @@ hipError_t launch_topk_gather(const float* scores, int64_t n, int nq, int k,
     }
     hipLaunchKernelGGL((select_kernel<false, true>), dim3(1, nq), dim3(kThreads), 0, stream,
                        nullptr, buf[cur], count, k, nullptr, out_ids, out_scores, out_drafts,
+                       out_draft_len, spans, span_len, max_span, span_stride);
+    return hipGetLastError();
+}
+
+hipError_t launch_topk_keys(const uint64_t* keys, int64_t count, int nq, int k,
+                            const int32_t* spans, const int32_t* span_len, int max_span,
+                            int64_t span_stride, int64_t* out_ids, float* out_scores,
+                            int32_t* out_drafts, int32_t* out_draft_len, void* workspace,
+                            hipStream_t stream) {
+    const int64_t kk = k < kSelectChunk ? k : kSelectChunk;
+    int64_t chunks = ceil_div(count, kSelectChunk);
+    const uint64_t* cur_in = keys;
+    int64_t cur_count = count;
+    const size_t one = topk_workspace_bytes(count, nq, k) / 2;
+    uint64_t* buf[2] = {(uint64_t*)workspace, (uint64_t*)((char*)workspace + one)};
+    int cur = 0;
+    hipError_t e;
+    while (chunks > 1) {
+        hipLaunchKernelGGL((select_kernel<false, false>), dim3((unsigned)chunks, nq),
+                           dim3(kThreads), 0, stream, nullptr, cur_in, cur_count, k, buf[cur],
+                           nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 0, 0);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        cur_in = buf[cur];
+        cur_count = chunks * kk;
+        cur ^= 1;
+        chunks = ceil_div(cur_count, kSelectChunk);
+    }
+    hipLaunchKernelGGL((select_kernel<false, true>), dim3(1, nq), dim3(kThreads), 0, stream,
+                       nullptr, cur_in, cur_count, k, nullptr, out_ids, out_scores, out_drafts,
                        out_draft_len, spans, span_len, max_span, span_stride);
     return hipGetLastError();
 }

@@ -49,13 +49,18 @@ EXPORTED = (
     "sense_soft_gate_verify_tree",
     "sense_project_workspace_size",
     "sense_project",
+    "sense_ivf_assign",
+    "sense_pq_encode",
+    "sense_build_ivf_index",
+    "sense_ivf_search_workspace_size",
+    "sense_ivf_search",
     "sense_set_timer_events",
     "sense_read_bandwidth_probe",
     "sense_status_string",
     "sense_last_error_message",
 )
 SENSE_TIMER_SCAN, SENSE_TIMER_TOPK, SENSE_TIMER_VERIFY, SENSE_TIMER_SELECT = 0, 1, 2, 3
-SENSE_TIMER_TRIE, SENSE_TIMER_PROJECT = 4, 5
+SENSE_TIMER_TRIE, SENSE_TIMER_PROJECT, SENSE_TIMER_IVF = 4, 5, 6
 
 
 class SenseError(RuntimeError):
@@ -129,6 +134,27 @@ class ProjDesc(ctypes.Structure):
     ]
 
 
+class IvfDesc(ctypes.Structure):
+    _fields_ = [
+        ("keys", ctypes.c_void_p),
+        ("key_dtype", ctypes.c_int),
+        ("n", ctypes.c_int64),
+        ("d", ctypes.c_int32),
+        ("key_stride", ctypes.c_int64),
+        ("spans", ctypes.c_void_p),
+        ("max_span", ctypes.c_int32),
+        ("span_len", ctypes.c_void_p),
+        ("metric", ctypes.c_int),
+        ("centroids", ctypes.c_void_p),
+        ("nlist", ctypes.c_int32),
+        ("list_ids", ctypes.c_void_p),
+        ("pq_codebooks", ctypes.c_void_p),
+        ("pq_m", ctypes.c_int32),
+        ("pq_ksub", ctypes.c_int32),
+        ("pq_codes", ctypes.c_void_p),
+    ]
+
+
 class GateParams(ctypes.Structure):
     _fields_ = [
         ("gamma", ctypes.c_float),
@@ -172,6 +198,11 @@ def load_library() -> ctypes.CDLL:
                                    ctypes.POINTER(GateParams), P, P, P, P, P, P, SZ, P],
         "sense_build_loose_trie": [P, P, I32, I32, I32, ctypes.POINTER(TrieDesc), P],
         "sense_project_workspace_size": [ctypes.POINTER(ProjDesc), ctypes.c_int, I64, PSZ],
+        "sense_ivf_assign": [P, ctypes.c_int, I64, I32, I64, P, I32, ctypes.c_int, P, P],
+        "sense_pq_encode": [P, ctypes.c_int, I64, I32, I64, P, I32, P, P, I32, I32, P, P],
+        "sense_build_ivf_index": [ctypes.POINTER(IvfDesc), P, PP],
+        "sense_ivf_search_workspace_size": [P, I32, I32, I32, PSZ],
+        "sense_ivf_search": [P, P, ctypes.c_int, I32, I32, I32, P, P, P, P, P, P, SZ, P],
         "sense_project": [ctypes.POINTER(ProjDesc), P, ctypes.c_int, I64, I64, P, ctypes.c_int,
                           I64, P, SZ, P],
         "sense_soft_gate_verify_tree_workspace_size": [I32, I32, I32, I32, PSZ],
@@ -673,3 +704,129 @@ def sense_project(x: torch.Tensor, basis: torch.Tensor, mean: torch.Tensor | Non
         _dev_ptr(out, "out"), _TORCH_DTYPE[out.dtype], out.stride(0), _dev_ptr(workspace, "workspace"),
         workspace.numel(), _stream_handle(stream)), "sense_project")
     return out
+
+
+def _keys_2d(keys: torch.Tensor):
+    if keys.dim() != 2 or keys.dtype not in (torch.float16, torch.bfloat16) or keys.stride(1) != 1:
+        raise ValueError("keys must be a 2-D float16/bfloat16 tensor with contiguous rows")
+    return keys.shape[0], keys.shape[1], keys.stride(0)
+
+
+def sense_ivf_assign(keys: torch.Tensor, centroids: torch.Tensor, metric: str = "cosine",
+                     out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Most similar centroid of every key row (int32 [n])."""
+    n, d, ld = _keys_2d(keys)
+    if centroids.dtype != torch.float32 or not centroids.is_contiguous() or centroids.shape[1] != d:
+        raise ValueError("centroids must be a contiguous nlist x d float32 tensor")
+    if out is None:
+        out = torch.empty(n, dtype=torch.int32, device=keys.device)
+    _check(load_library().sense_ivf_assign(_dev_ptr(keys, "keys"), _TORCH_DTYPE[keys.dtype], n, d,
+                                           ld, _dev_ptr(centroids, "centroids"), centroids.shape[0],
+                                           METRICS[metric], _dev_ptr(out, "out_list"),
+                                           _stream_handle(stream)), "sense_ivf_assign")
+    return out
+
+
+def sense_pq_encode(keys: torch.Tensor, centroids: torch.Tensor, list_ids: torch.Tensor,
+                    codebooks: torch.Tensor, out: torch.Tensor | None = None,
+                    stream=None) -> torch.Tensor:
+    """PQ codes (uint8 [n, m]) of the residuals key - centroid[list];
+    codebooks is m x ksub x (d/m) float32."""
+    n, d, ld = _keys_2d(keys)
+    if codebooks.dtype != torch.float32 or codebooks.dim() != 3 or not codebooks.is_contiguous():
+        raise ValueError("codebooks must be a contiguous m x ksub x dsub float32 tensor")
+    m, ksub, _ = codebooks.shape
+    if out is None:
+        out = torch.empty((n, m), dtype=torch.uint8, device=keys.device)
+    _check(load_library().sense_pq_encode(
+        _dev_ptr(keys, "keys"), _TORCH_DTYPE[keys.dtype], n, d, ld, _dev_ptr(centroids, "centroids"),
+        centroids.shape[0], _dev_ptr(list_ids, "list_ids"), _dev_ptr(codebooks, "codebooks"), m,
+        ksub, _dev_ptr(out, "out_codes"), _stream_handle(stream)), "sense_pq_encode")
+    return out
+
+
+class IvfIndex:
+    """An inverted-file index (owns its device memory; borrows the spans)."""
+
+    def __init__(self, handle, d, nlist, max_span, metric, pq_m, spans, span_len):
+        self.handle, self.d, self.nlist, self.max_span = handle, d, nlist, max_span
+        self.metric, self.pq_m, self.spans, self.span_len = metric, pq_m, spans, span_len
+
+    def close(self) -> None:
+        if self.handle:
+            h, self.handle = self.handle, None
+            _check(load_library().sense_destroy_index(h), "sense_destroy_index")
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def sense_build_ivf_index(keys: torch.Tensor | None, spans: torch.Tensor, centroids: torch.Tensor,
+                          list_ids: torch.Tensor, span_len: torch.Tensor | None = None,
+                          metric: str = "cosine", codebooks: torch.Tensor | None = None,
+                          codes: torch.Tensor | None = None, key_dtype: torch.dtype | None = None,
+                          stream=None) -> IvfIndex:
+    """IVF-Flat (codebooks None) or IVF-PQ index.  For IVF-PQ ``keys`` may be
+    None (then ``key_dtype`` names the query-compatible key type)."""
+    lib = load_library()
+    if keys is not None:
+        n, d, ld = _keys_2d(keys)
+        kdt = keys.dtype
+    else:
+        n, d, ld = list_ids.shape[0], centroids.shape[1], centroids.shape[1]
+        kdt = key_dtype or torch.bfloat16
+    m, ksub = (codebooks.shape[0], codebooks.shape[1]) if codebooks is not None else (0, 0)
+    desc = IvfDesc(keys=_dev_ptr(keys, "keys"), key_dtype=_TORCH_DTYPE[kdt], n=n, d=d,
+                   key_stride=ld, spans=_dev_ptr(spans, "spans"), max_span=spans.shape[1],
+                   span_len=_dev_ptr(span_len, "span_len"), metric=METRICS[metric],
+                   centroids=_dev_ptr(centroids, "centroids"), nlist=centroids.shape[0],
+                   list_ids=_dev_ptr(list_ids, "list_ids"),
+                   pq_codebooks=_dev_ptr(codebooks, "codebooks"), pq_m=m, pq_ksub=ksub,
+                   pq_codes=_dev_ptr(codes, "codes"))
+    handle = ctypes.c_void_p()
+    _check(lib.sense_build_ivf_index(ctypes.byref(desc), _stream_handle(stream),
+                                     ctypes.byref(handle)), "sense_build_ivf_index")
+    return IvfIndex(handle, d, centroids.shape[0], spans.shape[1], metric, m, spans, span_len)
+
+
+def sense_ivf_search_workspace_size(index: IvfIndex, n_queries: int, k: int, nprobe: int) -> int:
+    size = ctypes.c_size_t()
+    _check(load_library().sense_ivf_search_workspace_size(index.handle, n_queries, k, nprobe,
+                                                          ctypes.byref(size)),
+           "sense_ivf_search_workspace_size")
+    return size.value
+
+
+def sense_ivf_search(index: IvfIndex, queries: torch.Tensor, k: int, nprobe: int,
+                     workspace: torch.Tensor | None = None, out: tuple | None = None,
+                     want_probe: bool = False, stream=None):
+    """Inverted-file search.  Returns (ids int64 [Q,k], scores fp32 [Q,k],
+    drafts int32 [Q,k,M], draft_len int32 [Q,k]) and, with want_probe, the
+    probed lists int64 [Q,nprobe]."""
+    lib = load_library()
+    if queries.dim() == 1:
+        queries = queries.unsqueeze(0)
+    if queries.dtype not in _TORCH_DTYPE or not queries.is_contiguous() or queries.shape[1] != index.d:
+        raise ValueError("queries must be a contiguous Q x d float32/float16/bfloat16 tensor")
+    nq = queries.shape[0]
+    dev = queries.device
+    if out is None:
+        out = (torch.empty((nq, k), dtype=torch.int64, device=dev),
+               torch.empty((nq, k), dtype=torch.float32, device=dev),
+               torch.empty((nq, k, index.max_span), dtype=torch.int32, device=dev),
+               torch.empty((nq, k), dtype=torch.int32, device=dev))
+    probe = torch.empty((nq, nprobe), dtype=torch.int64, device=dev) if want_probe else None
+    if workspace is None:
+        workspace = torch.empty(max(sense_ivf_search_workspace_size(index, nq, k, nprobe), 1),
+                                dtype=torch.uint8, device=dev)
+    ids, sc, dr, dl = out
+    _check(lib.sense_ivf_search(index.handle, _dev_ptr(queries, "queries"),
+                                _TORCH_DTYPE[queries.dtype], nq, k, nprobe, _dev_ptr(ids, "ids"),
+                                _dev_ptr(sc, "scores"), _dev_ptr(dr, "drafts"),
+                                _dev_ptr(dl, "draft_len"), _dev_ptr(probe, "probe"),
+                                _dev_ptr(workspace, "workspace"), workspace.numel(),
+                                _stream_handle(stream)), "sense_ivf_search")
+    return (ids, sc, dr, dl, probe) if want_probe else (ids, sc, dr, dl)

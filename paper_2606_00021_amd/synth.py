@@ -332,3 +332,39 @@ def make_pca_basis(ds: Datastore, seed: int, d_out: int = 64, sample: int = 1638
     top = torch.argsort(w, descending=True)[:d_out]
     basis = v[:, top].T.contiguous()
     return mean.float().contiguous(), basis.float().contiguous()
+
+
+def fit_ivf(keys: torch.Tensor, seed: int, nlist: int, pq_m: int = 0, ksub: int = 256,
+            iters: int = 6, sample: int = 65536):
+    """Coarse centroids (spherical k-means: inner-product assignment, mean
+    update) and, with pq_m > 0, PQ codebooks (k-means per sub-space on the
+    residuals) of a uniform sample of the keys, in fp32 with torch: the
+    FAISS-style training of the paper's index, here input preparation.
+    Returns (centroids [nlist, d], codebooks [pq_m, ksub, d/pq_m] or None)."""
+    device = keys.device
+    g = _gen(seed + 15485867, device)
+    n, d = keys.shape
+    rows = torch.randint(0, n, (min(sample, n),), generator=g, device=device)
+    x = keys[rows].float()
+    cen = x[torch.randperm(x.shape[0], generator=g, device=device)[:nlist]].clone()
+    for _ in range(iters):
+        lab = torch.argmax(x @ cen.T, dim=1)
+        sums = torch.zeros_like(cen).index_add_(0, lab, x)
+        cnt = torch.bincount(lab, minlength=nlist).float().unsqueeze(1)
+        cen = torch.where(cnt > 0, sums / cnt.clamp_min(1.0), cen)
+    if pq_m <= 0:
+        return cen.contiguous(), None
+    lab = torch.argmax(x @ cen.T, dim=1)
+    res = (x - cen[lab]).view(x.shape[0], pq_m, d // pq_m)
+    books = []
+    for j in range(pq_m):
+        r = res[:, j, :]
+        cb = r[torch.randperm(r.shape[0], generator=g, device=device)[:ksub]].clone()
+        for _ in range(iters):
+            dist = torch.cdist(r, cb)
+            a = torch.argmin(dist, dim=1)
+            sums = torch.zeros_like(cb).index_add_(0, a, r)
+            cnt = torch.bincount(a, minlength=ksub).float().unsqueeze(1)
+            cb = torch.where(cnt > 0, sums / cnt.clamp_min(1.0), cb)
+        books.append(cb)
+    return cen.contiguous(), torch.stack(books).contiguous()
