@@ -361,15 +361,55 @@ def main():
         q = q_proj
     d_idx = ds.keys.shape[1]
     index = sense.sense_build_index(ds.keys, ds.spans, ds.span_len, metric=w.metric)
-    ws_r = torch.empty(max(1, sense.sense_retrieve_workspace_size(index, nq, k)),
-                       dtype=torch.uint8, device=dev)
+    ivf = None
+    ivf_info = None
+    if w.ivf_nlist:
+        # The paper's ANN retriever over the projected keys.  Training (the
+        # k-means fits) is input preparation; assignment, encoding and the
+        # list layout are the library's build, timed here.
+        cen, books = synth.fit_ivf(ds.keys, args.seed, w.ivf_nlist, pq_m=w.pq_m)
+        torch.cuda.synchronize()
+        tb = time.perf_counter()
+        lists = sense.sense_ivf_assign(ds.keys, cen, w.metric)
+        codes = sense.sense_pq_encode(ds.keys, cen, lists, books) if w.pq_m else None
+        ivf = sense.sense_build_ivf_index(None if w.pq_m else ds.keys, ds.spans, cen, lists,
+                                          ds.span_len, metric=w.metric,
+                                          codebooks=books if w.pq_m else None, codes=codes,
+                                          key_dtype=ds.keys.dtype)
+        torch.cuda.synchronize()
+        ivf_info = {"nlist": w.ivf_nlist, "nprobe": w.ivf_nprobe, "pq_m": w.pq_m,
+                    "pq_ksub": 256 if w.pq_m else None,
+                    "kind": "ivf-pq" if w.pq_m else "ivf-flat",
+                    "build_s": time.perf_counter() - tb}
+        log(f"[bench] inverted file {ivf_info['kind']} nlist={w.ivf_nlist}: assignment, "
+            f"encoding and layout {ivf_info['build_s']:.2f} s")
+    if ivf is not None:
+        ws_r = torch.empty(max(1, sense.sense_ivf_search_workspace_size(ivf, nq, k, w.ivf_nprobe)),
+                           dtype=torch.uint8, device=dev)
+    else:
+        ws_r = torch.empty(max(1, sense.sense_retrieve_workspace_size(index, nq, k)),
+                           dtype=torch.uint8, device=dev)
+
+    def retrieve():
+        if ivf is not None:
+            sense.sense_ivf_search(ivf, q, k, w.ivf_nprobe, workspace=ws_r, out=outs)
+        else:
+            sense.sense_retrieve(index, q, k, workspace=ws_r, out=outs)
     outs = (torch.empty((nq, k), dtype=torch.int64, device=dev),
             torch.empty((nq, k), dtype=torch.float32, device=dev),
             torch.empty((nq, k, m), dtype=torch.int32, device=dev),
             torch.empty((nq, k), dtype=torch.int32, device=dev))
     if w.proj:
         sense.sense_project(q_hidden, basis, mean, True, out=q_proj)
-    sense.sense_retrieve(index, q, k, workspace=ws_r, out=outs)
+    retrieve()
+    if ivf is not None:
+        # recall@k of the approximate search against the exact scan of the
+        # same (projected) keys, over this step's queries
+        ex = sense.sense_retrieve(index, q, k)[0]
+        torch.cuda.synchronize()
+        hits = sum(len(set(outs[0][i].tolist()) & set(ex[i].tolist())) for i in range(nq))
+        ivf_info["recall_at_k"] = hits / (nq * k)
+        log(f"[bench] recall@{k} against the exact scan: {ivf_info['recall_at_k']:.4f}")
     vq = w.verify_queries
     drafts = outs[2][:vq].view(vq * k, m)
     dlen = outs[3][:vq].view(vq * k)
@@ -385,7 +425,7 @@ def main():
     def step():
         if w.proj:
             sense.sense_project(q_hidden, basis, mean, True, out=q_proj)
-        sense.sense_retrieve(index, q, k, workspace=ws_r, out=outs)
+        retrieve()
         sense.sense_soft_gate_verify(logits, drafts, dlen, n_groups=vq, gamma=0.05, topk=3,
                                      window=6, tau=0, workspace=ws_v, out=out_v)
 
@@ -432,11 +472,13 @@ def main():
     # Per-kernel durations: a second pass of K steps with hipEvents recorded
     # by the library around the scan, top-k and verify kernels (the events
     # themselves add a little time, so this pass is not the step time).
-    timed_parts = ("scan", "topk", "verify") + (("project",) if w.proj else ())
+    timed_parts = ((("ivf",) if ivf is not None else ("scan", "topk")) + ("verify",)
+                   + (("project",) if w.proj else ()))
     ev = {t: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
               for _ in range(K)] for t in timed_parts}
     timer_id = {"scan": sense.SENSE_TIMER_SCAN, "topk": sense.SENSE_TIMER_TOPK,
-                "verify": sense.SENSE_TIMER_VERIFY, "project": sense.SENSE_TIMER_PROJECT}
+                "verify": sense.SENSE_TIMER_VERIFY, "project": sense.SENSE_TIMER_PROJECT,
+                "ivf": sense.SENSE_TIMER_IVF}
     # torch creates the underlying hipEvent_t lazily at the first record():
     # record every event once here so that the handles exist.
     for t in ev:
@@ -452,9 +494,10 @@ def main():
     for t in ev:
         sense.sense_set_timer_events(timer_id[t], None, None)
     dur = {t: sum(a.elapsed_time(b) for a, b in ev[t]) / K for t in ev}
+    parts = (f"inverted-file search {dur['ivf']:.4f} ms" if ivf is not None
+             else f"scan {dur['scan']:.4f} ms, topk {dur['topk']:.4f} ms")
     log(f"[bench] {K} steps ({launch}): {ms_step:.4f} ms/step (wall {wall * 1e3:.4f} ms/step; "
-        f"eager launches {ms_eager:.4f} ms/step); "
-        f"scan {dur['scan']:.4f} ms, topk {dur['topk']:.4f} ms, verify {dur['verify']:.4f} ms"
+        f"eager launches {ms_eager:.4f} ms/step); {parts}, verify {dur['verify']:.4f} ms"
         + (f", query projection {dur['project']:.4f} ms" if w.proj else ""))
 
     # Algorithmic bytes: every key once (+ the fp32 inverse-norm table for
@@ -464,14 +507,31 @@ def main():
     gather_bytes = nq * k * m * 4
     live = int(dlen.clamp(0, m).sum().item())
     verify_bytes = live * w.vocab * (4 if w.logits_dtype == "f32" else 2)
-    step_bytes = scan_bytes + gather_bytes + verify_bytes
-    scan_gbps = scan_bytes / (dur["scan"] * 1e-3) / 1e9
-    if nq >= 4:
-        scan_kernel = "scan_mfma_kernel"
-    elif d_idx <= 64:
-        scan_kernel = "scan_small_kernel"
+    if ivf is not None:
+        # Bytes one search must read: the centroids, and per query the probed
+        # rows (codes, or keys + norms) of the lists actually probed.
+        sizes = torch.bincount(lists.long(), minlength=w.ivf_nlist)
+        probe_rows = 0
+        for i in range(nq):
+            sc_c = q[i].float() @ cen.T
+            if w.metric == "cosine":
+                sc_c = sc_c / cen.norm(dim=1).clamp_min(1e-30)
+            probe_rows += int(sizes[torch.topk(sc_c, w.ivf_nprobe).indices].sum().item())
+        row_bytes = w.pq_m if w.pq_m else d_idx * 2 + (4 if w.metric == "cosine" else 0)
+        scan_bytes = w.ivf_nlist * d_idx * 4 + probe_rows * (row_bytes + 4)
+        ivf_info["probed_rows_per_query"] = probe_rows / nq
+        scan_ms = dur["ivf"]
+        scan_kernel = "ivf_search"
     else:
-        scan_kernel = "scan_gemv_kernel"
+        scan_ms = dur["scan"]
+        if nq >= 4:
+            scan_kernel = "scan_mfma_kernel"
+        elif d_idx <= 64:
+            scan_kernel = "scan_small_kernel"
+        else:
+            scan_kernel = "scan_gemv_kernel"
+    step_bytes = scan_bytes + gather_bytes + verify_bytes
+    scan_gbps = scan_bytes / (scan_ms * 1e-3) / 1e9
     res = {
         "metric": METRIC,
         "value": nq / (ms_step * 1e-3),
@@ -493,15 +553,19 @@ def main():
                    "metric": w.metric, "parallelism": "single-gpu"},
         "hbm_gbps": step_bytes / (ms_step * 1e-3) / 1e9,
         "hbm_frac": step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS,
-        "scan_ms": dur["scan"],
-        "topk_ms": dur["topk"],
+        **({"ivf_search_ms": dur["ivf"]} if ivf is not None
+           else {"scan_ms": dur["scan"], "topk_ms": dur["topk"]}),
         "verify_ms": dur["verify"],
         **({"project_ms": dur["project"]} if w.proj else {}),
         "verify_gbps": verify_bytes / (dur["verify"] * 1e-3) / 1e9 if dur["verify"] > 0 else None,
         "roofline": {"bound": "hbm", "kernel": scan_kernel, "achieved": scan_gbps,
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": scan_gbps / HBM_PEAK_GBPS,
-                     "traffic": traffic_from_profiles(name, scan_kernel)},
+                     "traffic": (traffic_from_profiles(name, scan_kernel)
+                                 if scan_kernel in SCAN_SOURCES else None)},
     }
+    if ivf_info is not None:
+        res["config"]["ivf"] = ivf_info["kind"]
+        res["ivf"] = ivf_info
     if proj_info is not None:
         res["config"]["proj"] = w.proj
         res["projection"] = proj_info
@@ -539,6 +603,8 @@ def main():
         res["cpu_baseline"] = cpu_baseline(w, ds, q, logits, drafts, args.cpu_seconds)
         log(f"[bench] cpu_baseline took {time.perf_counter() - t0:.1f} s")
     index.close()
+    if ivf is not None:
+        ivf.close()
     print(json.dumps(res), flush=True)
 
 

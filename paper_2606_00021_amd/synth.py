@@ -39,6 +39,9 @@ class Workload:
     verify_queries: int  # queries whose k drafts are verified (groups)
     metric: str = "cosine"
     proj: int = 0        # PCA dimension of the searched keys (0: the hidden states as-is)
+    ivf_nlist: int = 0   # inverted lists (0: exact scan)
+    ivf_nprobe: int = 0  # lists searched per query
+    pq_m: int = 0        # PQ sub-quantizers (0: IVF-Flat)
 
     @property
     def key_bytes(self) -> int:
@@ -74,6 +77,14 @@ WORKLOADS = {
                  4096, 8, 1, proj=64),
         Workload("store-1m-pca64-q64", 1_048_576, 4096, "bf16", 64, 64, 8, 152_064, "bf16",
                  4096, 8, 1, proj=64),
+        # The paper's retriever: FAISS-style IVF-PQ (nlist 4096, nprobe 32, pq_m 16)
+        # over the PCA-64 keys, and IVF-Flat with the same lists.
+        Workload("store-1m-pca64-ivfpq", 1_048_576, 4096, "bf16", 1, 64, 8, 152_064, "bf16",
+                 4096, 8, 1, proj=64, ivf_nlist=4096, ivf_nprobe=32, pq_m=16),
+        Workload("store-1m-pca64-ivfpq-q64", 1_048_576, 4096, "bf16", 64, 64, 8, 152_064,
+                 "bf16", 4096, 8, 1, proj=64, ivf_nlist=4096, ivf_nprobe=32, pq_m=16),
+        Workload("store-1m-pca64-ivfflat", 1_048_576, 4096, "bf16", 1, 64, 8, 152_064, "bf16",
+                 4096, 8, 1, proj=64, ivf_nlist=4096, ivf_nprobe=32),
     ]
 }
 HEADLINE = "store-1m-d4096"
