@@ -129,12 +129,13 @@ hipError_t launch_project(const void* x, int x_dtype, int64_t n, int d_in, int64
                           hipStream_t stream);
 
 // Top-k of packed keys (nq x count, padding key 0) in the order of the
-// keys, with the gather; ids of padding keys are -1.
+// keys, with the gather; ids of padding keys are -1.  dev_count (optional,
+// device): query q has only its first dev_count[q] <= count keys.
 hipError_t launch_topk_keys(const uint64_t* keys, int64_t count, int nq, int k,
                             const int32_t* spans, const int32_t* span_len, int max_span,
                             int64_t span_stride, int64_t* out_ids, float* out_scores,
                             int32_t* out_drafts, int32_t* out_draft_len, void* workspace,
-                            hipStream_t stream);
+                            hipStream_t stream, const int32_t* dev_count = nullptr);
 
 // Inverted file (ivf.hip).
 hipError_t launch_ivf_assign(const void* keys, int key_dtype, int64_t n, int d, int64_t ld,
@@ -188,6 +189,54 @@ struct IvfSearch {
     void* final_ws;
 };
 hipError_t launch_ivf_search(const IvfSearch& s, hipStream_t stream);
+
+// The queries of a batch padded to qpad = 16*ceil(nq/16) rows and split
+// into hi + lo halves of the key type (a scratch of scan_mfma_scratch_bytes),
+// with inv_qn[q] = 1/||q|| (cosine), 1 (inner product), 0 (padding).
+struct QuerySplit {
+    uint16_t* hi;
+    uint16_t* lo;
+    float* inv_qn;
+    int qpad;
+};
+QuerySplit query_split_parts(void* scratch, int nq, int d);
+hipError_t launch_query_split(const float* queries, int nq, int d, int key_dtype, bool cosine,
+                              void* scratch, hipStream_t stream);
+
+// Batched scan of short keys (d <= kSmallDim) on the matrix cores, for at
+// most 64 queries of a split batch (see scan_short.hip).  Row r of the scan
+// is stored row r * row_step.  WRITE: scores[q * n_rows + r].  FILTER: a row
+// whose packed key (score, r * row_step) is at least tau[q] goes to
+// cand[q * cap + ...]: wave w of short_scan_waves(n_rows) fills its slots
+// [w * kShortSlots, (w + 1) * kShortSlots) (the rest padding keys), and the
+// overflow is appended at counts[q] (which starts at the slot area's size).
+constexpr int kShortSlots = 16;
+int64_t short_scan_waves(int64_t n_rows);
+struct ShortScan {
+    const void* keys;
+    int key_dtype;
+    int64_t ld;
+    int64_t n_rows;
+    int64_t row_step;
+    int d;
+    const uint16_t* qhi;
+    const uint16_t* qlo;
+    const float* inv_qn;
+    int nq;
+    bool split;
+    const float* inv_norm;
+    float* scores;            // WRITE mode
+    const uint64_t* tau;      // FILTER mode
+    int32_t* counts;
+    uint64_t* cand;
+    int64_t cap;
+};
+hipError_t launch_scan_short(const ShortScan& s, hipStream_t stream);
+// tau[q] = packed key of the k-th best row of a strided sample (the sample
+// top-k's ids are sample positions; row = id * row_step).
+hipError_t launch_short_tau(const int64_t* ids, const float* scores, int nq, int k,
+                            int64_t row_step, int32_t slot_area, uint64_t* tau, int32_t* counts,
+                            hipStream_t stream);
 
 // Plain streaming read of a device buffer (bandwidth probe).
 hipError_t launch_stream_read(const void* buf, size_t bytes, uint32_t* sink, hipStream_t stream);

@@ -352,22 +352,34 @@ size_t scan_mfma_scratch_bytes(int nq, int d) {
     return 2 * half + (qpad * 4 + 255) / 256 * 256;
 }
 
+QuerySplit query_split_parts(void* scratch, int nq, int d) {
+    const int qpad = (nq + 15) / 16 * 16;
+    const size_t half = ((size_t)qpad * d * 2 + 255) / 256 * 256;
+    return QuerySplit{(uint16_t*)scratch, (uint16_t*)((char*)scratch + half),
+                      (float*)((char*)scratch + 2 * half), qpad};
+}
+
+hipError_t launch_query_split(const float* queries, int nq, int d, int key_dtype, bool cosine,
+                              void* scratch, hipStream_t stream) {
+    const QuerySplit p = query_split_parts(scratch, nq, d);
+    if (key_dtype == DT_BF16)
+        hipLaunchKernelGGL(query_split_kernel<DT_BF16>, dim3(p.qpad), dim3(256), 0, stream,
+                           queries, nq, d, cosine, p.hi, p.lo, p.inv_qn);
+    else
+        hipLaunchKernelGGL(query_split_kernel<DT_F16>, dim3(p.qpad), dim3(256), 0, stream,
+                           queries, nq, d, cosine, p.hi, p.lo, p.inv_qn);
+    return hipGetLastError();
+}
+
 hipError_t launch_scan_mfma(const void* keys, int key_dtype, int64_t n, int d, int64_t ld,
                             const float* queries, int nq, bool split, const float* inv_norm,
                             float* scores, void* scratch, hipStream_t stream) {
-    const int qpad = (nq + 15) / 16 * 16;
-    const size_t half = ((size_t)qpad * d * 2 + 255) / 256 * 256;
-    uint16_t* qhi = (uint16_t*)scratch;
-    uint16_t* qlo = (uint16_t*)((char*)scratch + half);
-    float* inv_qn = (float*)((char*)scratch + 2 * half);
-    const bool cosine = inv_norm != nullptr;
-    if (key_dtype == DT_BF16)
-        hipLaunchKernelGGL(query_split_kernel<DT_BF16>, dim3(qpad), dim3(256), 0, stream, queries,
-                           nq, d, cosine, qhi, qlo, inv_qn);
-    else
-        hipLaunchKernelGGL(query_split_kernel<DT_F16>, dim3(qpad), dim3(256), 0, stream, queries,
-                           nq, d, cosine, qhi, qlo, inv_qn);
-    hipError_t e = hipGetLastError();
+    const QuerySplit p = query_split_parts(scratch, nq, d);
+    uint16_t* qhi = p.hi;
+    uint16_t* qlo = p.lo;
+    float* inv_qn = p.inv_qn;
+    hipError_t e = launch_query_split(queries, nq, d, key_dtype, inv_norm != nullptr, scratch,
+                                      stream);
     if (e != hipSuccess) return e;
     for (int g0 = 0; g0 < nq; g0 += 64) {
         const int ng = (nq - g0 < 64) ? nq - g0 : 64;

@@ -1,0 +1,285 @@
+// Batched similarity scan of short keys (d <= 64, e.g. the 64-dim PCA keys)
+// on the matrix cores, with an optional filter that keeps only rows able to
+// enter a query's top k (Sec. 3.2 Eq. 8 for a batch of queries; the top-N'
+// retrieval of Eq. 7).
+//
+// A 64-dim key is 128 bytes, so the long-key MFMA design (a ring of key
+// stages walking d) has nothing to pipeline across.  Here every wave keeps
+// the whole query batch (up to 64 queries x 64 dims, hi and lo halves) in
+// registers as A fragments and streams 16-key tiles as B fragments straight
+// from HBM: lane l loads 16 bytes of key (base + l%16) at dims 8*(l/16) and
+// 32 + 8*(l/16), so one tile is 16 contiguous rows (2 KiB at d = 64).  Four
+// tiles are in flight per wave.  Per tile: 4 query tiles x 2 k-steps x
+// (hi, lo) MFMA 16x16x32 instructions.
+//
+// The 64 x n score matrix would be 256 MB at n = 1M: writing it and reading
+// it back for the top-k costs more than reading the keys.  So the scan runs
+// twice: first over a strided sample of rows writing scores, whose per-query
+// k-th best packed key tau bounds the final k-th best from below; then over
+// all rows, keeping only rows whose packed key reaches tau: each wave has 16
+// slots per query, filled in order (ballot + popcount), and a query's
+// overflow list takes what does not fit.
+// Every true top-k row passes, so the result is exact; the scores of both
+// passes come from the same instructions, hence the same bits.
+#include "internal.h"
+
+namespace sense {
+
+int64_t short_rows_per_wave(int64_t n_rows);
+
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+
+constexpr int kShortThreads = 256;
+constexpr int kShortDepth = 4;     // 16-key tiles in flight per wave
+static_assert(kShortSlots == 16, "one padding slot per lane of a 16-lane group");
+
+template <int KT>
+__device__ __forceinline__ f32x4 mfma(const u32x4& a, const u32x4& b, const f32x4& c) {
+    if constexpr (KT == DT_BF16)
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                       __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+    else
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a),
+                                                      __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+}
+
+// NT query tiles of 16, KS k-steps of 32 dims (d <= 32 * KS).
+template <int KT, int NT, int KS, bool SPLIT, bool FILTER>
+__global__ __launch_bounds__(kShortThreads, 2) void scan_short_kernel(ShortScan s,
+                                                                  int64_t rows_per_wave) {
+    // Per-query scale and threshold in LDS (read in the epilogue without a
+    // wait on the key loads in flight, and without registers).
+    __shared__ float s_iq[64];
+    __shared__ uint64_t s_tau[64];
+    if (threadIdx.x < 64) {
+        const int q = threadIdx.x;
+        s_iq[q] = q < 16 * NT ? s.inv_qn[q] : 0.0f;
+        if constexpr (FILTER) s_tau[q] = q < s.nq ? s.tau[q] : ~0ull;
+    }
+    __syncthreads();
+    const int lane = threadIdx.x & 63;
+    const int64_t wave = (int64_t)blockIdx.x * (kShortThreads / 64) + (threadIdx.x >> 6);
+    const int64_t r0 = wave * rows_per_wave;
+    if (r0 >= s.n_rows) return;                      // uniform over the wave
+    const int64_t r1 = (r0 + rows_per_wave < s.n_rows) ? r0 + rows_per_wave : s.n_rows;
+    const int col = lane & 15, grp = lane >> 4;
+
+    // Query fragments: A[m = col][k = 8*grp + 32*ks], for every query tile.
+    u32x4 ahi[NT][KS], alo[NT][KS];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            const int dim = 8 * grp + 32 * ks;
+            const int64_t qrow = 16 * t + col;
+            const bool ok = dim < s.d;
+            ahi[t][ks] = ok ? *(const u32x4*)(s.qhi + qrow * s.d + dim) : u32x4{0u, 0u, 0u, 0u};
+            if constexpr (SPLIT)
+                alo[t][ks] = ok ? *(const u32x4*)(s.qlo + qrow * s.d + dim) : u32x4{0u, 0u, 0u, 0u};
+        }
+    }
+    int cnt[NT][4];       // FILTER: survivors so far per query (same in a 16-lane group)
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) cnt[t][i] = 0;
+
+    // Everything an iteration reads comes in with the tile (keys and the key
+    // norm): a load issued later and consumed earlier would make the wave
+    // wait for all the tiles in flight before it.
+    const uint16_t* keys = (const uint16_t*)s.keys;
+    auto load_tile = [&](int64_t base, u32x4 (&b)[KS], float& kn) {
+        const int64_t r = base + col;
+        const bool ok = r < r1;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            const int dim = 8 * grp + 32 * ks;
+            b[ks] = (ok && dim < s.d)
+                        ? __builtin_nontemporal_load(
+                              (const u32x4*)(keys + r * s.row_step * s.ld + dim))
+                        : u32x4{0u, 0u, 0u, 0u};
+        }
+        kn = (ok && s.inv_norm) ? s.inv_norm[r * s.row_step] : 1.0f;
+    };
+    auto consume = [&](int64_t base, const u32x4 (&b)[KS], float kn) {
+        const int64_t r = base + col;                // this lane's key (column)
+        f32x4 acc[NT];
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            acc[t] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                acc[t] = mfma<KT>(ahi[t][ks], b[ks], acc[t]);
+                if constexpr (SPLIT) acc[t] = mfma<KT>(alo[t][ks], b[ks], acc[t]);
+            }
+        }
+        if (r >= r1) return;
+        const int64_t orig = r * s.row_step;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int qq = 16 * t + 4 * grp + i;
+                float v = acc[t][i];
+                if (s.inv_norm) v = v * kn;
+                v = v * s_iq[qq];
+                if constexpr (FILTER) {
+                    // Survivors go to this wave's own slots of the query (a
+                    // slot index from a ballot, no atomic: a returned atomic
+                    // would make the wave wait for its tiles in flight); a
+                    // wave with more than kShortSlots survivors for one query
+                    // appends the rest to the query's overflow list.
+                    const uint64_t key = pack_key(v, (uint32_t)orig);
+                    const bool pass = key >= s_tau[qq];
+                    const uint64_t bal = __ballot(pass);
+                    if (bal) {
+                        const uint32_t gm = (uint32_t)(bal >> (16 * grp)) & 0xFFFFu;
+                        const int slot = cnt[t][i] + __popc(gm & ((1u << col) - 1u));
+                        if (pass) {
+                            const int q = 16 * t + 4 * grp + i;
+                            uint64_t* cq = s.cand + (int64_t)q * s.cap;
+                            if (slot < kShortSlots) {
+                                cq[wave * kShortSlots + slot] = key;
+                            } else {
+                                const int pos = atomicAdd(&s.counts[q], 1);
+                                cq[pos] = key;
+                            }
+                        }
+                        cnt[t][i] += __popc(gm);
+                    }
+                } else {
+                    const int q = 16 * t + 4 * grp + i;
+                    if (q < s.nq) s.scores[(int64_t)q * s.n_rows + r] = v;
+                }
+            }
+        }
+    };
+
+    u32x4 buf[kShortDepth][KS];
+    float kn[kShortDepth];
+#pragma unroll
+    for (int u = 0; u < kShortDepth; ++u) load_tile(r0 + 16 * u, buf[u], kn[u]);
+    for (int64_t base = r0; base < r1; base += 16 * kShortDepth) {
+#pragma unroll
+        for (int u = 0; u < kShortDepth; ++u) {
+            consume(base + 16 * u, buf[u], kn[u]);
+            load_tile(base + 16 * (u + kShortDepth), buf[u], kn[u]);
+        }
+    }
+    if constexpr (FILTER) {
+        // Unused slots become padding keys.  Lane col 0 of each group saw
+        // every tile its group saw, so its counts are the group's.
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int c0 = __shfl(cnt[t][i], lane & ~15, 64);
+                const int q = 16 * t + 4 * grp + i;
+                if (q < s.nq && col >= c0 && col < kShortSlots)
+                    s.cand[(int64_t)q * s.cap + wave * kShortSlots + col] = 0;
+            }
+    }
+}
+
+__global__ void short_tau_kernel(const int64_t* __restrict__ ids, const float* __restrict__ scores,
+                                 int nq, int k, int64_t row_step, int32_t slot_area,
+                                 uint64_t* __restrict__ tau, int32_t* __restrict__ counts) {
+    const int q = blockIdx.x * blockDim.x + threadIdx.x;
+    if (q >= nq) return;
+    const int64_t id = ids[(int64_t)q * k + (k - 1)];
+    // A sample shorter than k leaves a padding id: then every row passes.
+    tau[q] = id < 0 ? 0ull : pack_key(scores[(int64_t)q * k + (k - 1)], (uint32_t)(id * row_step));
+    counts[q] = slot_area;          // overflow entries follow the wave slots
+}
+
+int g_cus_short = 0;
+
+template <int KT, int NT, int KS, bool SPLIT, bool FILTER>
+hipError_t launch_variant(const ShortScan& s, hipStream_t stream) {
+    auto kern = scan_short_kernel<KT, NT, KS, SPLIT, FILTER>;
+    static int per_cu = 0;
+    if (per_cu < 1 &&
+        (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, kShortThreads, 0) !=
+             hipSuccess ||
+         per_cu < 1))
+        per_cu = 2;
+    if (g_cus_short == 0) {
+        int dev = 0;
+        hipDeviceProp_t prop;
+        g_cus_short = (hipGetDevice(&dev) == hipSuccess &&
+                       hipGetDeviceProperties(&prop, dev) == hipSuccess &&
+                       prop.multiProcessorCount > 0)
+                          ? prop.multiProcessorCount
+                          : 256;
+    }
+    const int64_t rpw = short_rows_per_wave(s.n_rows);
+    const int64_t waves = (s.n_rows + rpw - 1) / rpw;
+    const int64_t blocks = (waves + (kShortThreads / 64) - 1) / (kShortThreads / 64);
+    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kShortThreads), 0, stream, s, rpw);
+    return hipGetLastError();
+}
+
+template <int KT, int NT, int KS>
+hipError_t launch_mode(const ShortScan& s, hipStream_t stream) {
+    const bool filter = s.cand != nullptr;
+    if (s.split)
+        return filter ? launch_variant<KT, NT, KS, true, true>(s, stream)
+                      : launch_variant<KT, NT, KS, true, false>(s, stream);
+    return filter ? launch_variant<KT, NT, KS, false, true>(s, stream)
+                  : launch_variant<KT, NT, KS, false, false>(s, stream);
+}
+
+template <int KT, int KS>
+hipError_t launch_tiles(const ShortScan& s, hipStream_t stream) {
+    switch ((s.nq + 15) / 16) {
+        case 1: return launch_mode<KT, 1, KS>(s, stream);
+        case 2: return launch_mode<KT, 2, KS>(s, stream);
+        case 3: return launch_mode<KT, 3, KS>(s, stream);
+        default: return launch_mode<KT, 4, KS>(s, stream);
+    }
+}
+
+}  // namespace
+
+int64_t short_rows_per_wave(int64_t n_rows) {
+    if (g_cus_short == 0) {
+        int dev = 0;
+        hipDeviceProp_t prop;
+        g_cus_short = (hipGetDevice(&dev) == hipSuccess &&
+                       hipGetDeviceProperties(&prop, dev) == hipSuccess &&
+                       prop.multiProcessorCount > 0)
+                          ? prop.multiProcessorCount
+                          : 256;
+    }
+    // Two resident waves per SIMD (the kernels' register use allows two).
+    const int64_t waves_max = (int64_t)g_cus_short * 8;
+    int64_t rpw = (n_rows + waves_max - 1) / waves_max;
+    return (rpw + 16 * kShortDepth - 1) / (16 * kShortDepth) * (16 * kShortDepth);
+}
+
+int64_t short_scan_waves(int64_t n_rows) {
+    const int64_t rpw = short_rows_per_wave(n_rows);
+    return (n_rows + rpw - 1) / rpw;
+}
+
+hipError_t launch_scan_short(const ShortScan& s, hipStream_t stream) {
+    const bool two = s.d > 32;
+    if (s.key_dtype == DT_BF16)
+        return two ? launch_tiles<DT_BF16, 2>(s, stream) : launch_tiles<DT_BF16, 1>(s, stream);
+    return two ? launch_tiles<DT_F16, 2>(s, stream) : launch_tiles<DT_F16, 1>(s, stream);
+}
+
+hipError_t launch_short_tau(const int64_t* ids, const float* scores, int nq, int k,
+                            int64_t row_step, int32_t slot_area, uint64_t* tau, int32_t* counts,
+                            hipStream_t stream) {
+    hipLaunchKernelGGL(short_tau_kernel, dim3((unsigned)((nq + 63) / 64)), dim3(64), 0, stream,
+                       ids, scores, nq, k, row_step, slot_area, tau, counts);
+    return hipGetLastError();
+}
+
+}  // namespace sense

@@ -127,7 +127,8 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
     int k, uint64_t* __restrict__ out_keys, int64_t* __restrict__ out_ids,
     float* __restrict__ out_scores, int32_t* __restrict__ out_drafts,
     int32_t* __restrict__ out_draft_len, const int32_t* __restrict__ spans,
-    const int32_t* __restrict__ span_len, int max_span, int64_t span_stride) {
+    const int32_t* __restrict__ span_len, int max_span, int64_t span_stride,
+    const int32_t* __restrict__ dev_count) {
     __shared__ uint64_t s_sel[kMaxK];
     __shared__ uint32_t s_hist[kWaves * 256];
     __shared__ uint32_t s_tot[256];
@@ -137,7 +138,9 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
     const int tid = threadIdx.x;
     const int q = blockIdx.y;
     const int64_t start = (int64_t)blockIdx.x * kSelectChunk;
-    const int64_t remain = count - start;
+    // dev_count: a per-query count on the device (at most count).
+    const int64_t cnt_q = (dev_count && dev_count[q] < count) ? dev_count[q] : count;
+    const int64_t remain = cnt_q - start;
     const int len = (int)(remain < kSelectChunk ? remain : kSelectChunk);
     const int kk = k < kSelectChunk ? k : kSelectChunk;
 
@@ -157,16 +160,28 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
             key[e] = 0;
         }
     }
-    if (tid == 0) s_cnt = 0;
+    __shared__ uint32_t s_nz;
+    if (tid == 0) {
+        s_cnt = 0;
+        s_nz = 0;
+    }
+    __syncthreads();
+    // Real (non-padding) keys of the chunk: a candidate buffer may hold
+    // padding keys anywhere, so the chunk length alone does not tell.
+#pragma unroll
+    for (int e = 0; e < kPer; ++e) {
+        const uint64_t m = __ballot(key[e] != 0);
+        if ((tid & 63) == 0 && m) atomicAdd(&s_nz, (uint32_t)__popcll(m));
+    }
+    __syncthreads();
 
-    // Keys taken: all real ones if the chunk holds no more than kk, else the
-    // kk largest.
+    // Keys taken: every real one if there are no more than kk, else the kk
+    // largest (then at least kk keys are real, as the radix select needs).
     SelectState st{0, 0};
-    const bool all = len <= kk;
+    const bool all = s_nz <= (uint32_t)kk;
     if (!all) st = radix_select(key, kk, s_hist, s_tot, s_info);
-    else __syncthreads();
     auto taken = [&](int e) {
-        return all ? (tid + e * kThreads < len) : ((key[e] & st.mask) >= st.prefix);
+        return all ? (key[e] != 0) : ((key[e] & st.mask) >= st.prefix);
     };
 
     if constexpr (!FINAL) {
@@ -241,14 +256,14 @@ hipError_t launch_topk_gather(const float* scores, int64_t n, int nq, int k,
     if (chunks <= 1) {
         hipLaunchKernelGGL((select_kernel<true, true>), dim3(1, nq), dim3(kThreads), 0, stream,
                            scores, nullptr, n, k, nullptr, out_ids, out_scores, out_drafts,
-                           out_draft_len, spans, span_len, max_span, span_stride);
+                           out_draft_len, spans, span_len, max_span, span_stride, nullptr);
         return hipGetLastError();
     }
     const size_t one = topk_workspace_bytes(n, nq, k) / 2;
     uint64_t* buf[2] = {(uint64_t*)workspace, (uint64_t*)((char*)workspace + one)};
     hipLaunchKernelGGL((select_kernel<true, false>), dim3((unsigned)chunks, nq), dim3(kThreads),
                        0, stream, scores, nullptr, n, k, buf[0], nullptr, nullptr, nullptr,
-                       nullptr, nullptr, nullptr, 0, 0);
+                       nullptr, nullptr, nullptr, 0, 0, nullptr);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     int64_t count = chunks * kk;
@@ -256,14 +271,14 @@ hipError_t launch_topk_gather(const float* scores, int64_t n, int nq, int k,
     while ((chunks = ceil_div(count, kSelectChunk)) > 1) {
         hipLaunchKernelGGL((select_kernel<false, false>), dim3((unsigned)chunks, nq),
                            dim3(kThreads), 0, stream, nullptr, buf[cur], count, k, buf[cur ^ 1],
-                           nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 0, 0);
+                           nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 0, 0, nullptr);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         count = chunks * kk;
         cur ^= 1;
     }
     hipLaunchKernelGGL((select_kernel<false, true>), dim3(1, nq), dim3(kThreads), 0, stream,
                        nullptr, buf[cur], count, k, nullptr, out_ids, out_scores, out_drafts,
-                       out_draft_len, spans, span_len, max_span, span_stride);
+                       out_draft_len, spans, span_len, max_span, span_stride, nullptr);
     return hipGetLastError();
 }
 
@@ -271,7 +286,7 @@ hipError_t launch_topk_keys(const uint64_t* keys, int64_t count, int nq, int k,
                             const int32_t* spans, const int32_t* span_len, int max_span,
                             int64_t span_stride, int64_t* out_ids, float* out_scores,
                             int32_t* out_drafts, int32_t* out_draft_len, void* workspace,
-                            hipStream_t stream) {
+                            hipStream_t stream, const int32_t* dev_count) {
     const int64_t kk = k < kSelectChunk ? k : kSelectChunk;
     int64_t chunks = ceil_div(count, kSelectChunk);
     const uint64_t* cur_in = keys;
@@ -280,11 +295,13 @@ hipError_t launch_topk_keys(const uint64_t* keys, int64_t count, int nq, int k,
     uint64_t* buf[2] = {(uint64_t*)workspace, (uint64_t*)((char*)workspace + one)};
     int cur = 0;
     hipError_t e;
+    const int32_t* counts = dev_count;         // the input's counts (first level only)
     while (chunks > 1) {
         hipLaunchKernelGGL((select_kernel<false, false>), dim3((unsigned)chunks, nq),
                            dim3(kThreads), 0, stream, nullptr, cur_in, cur_count, k, buf[cur],
-                           nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 0, 0);
+                           nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 0, 0, counts);
         if ((e = hipGetLastError()) != hipSuccess) return e;
+        counts = nullptr;
         cur_in = buf[cur];
         cur_count = chunks * kk;
         cur ^= 1;
@@ -292,7 +309,7 @@ hipError_t launch_topk_keys(const uint64_t* keys, int64_t count, int nq, int k,
     }
     hipLaunchKernelGGL((select_kernel<false, true>), dim3(1, nq), dim3(kThreads), 0, stream,
                        nullptr, cur_in, cur_count, k, nullptr, out_ids, out_scores, out_drafts,
-                       out_draft_len, spans, span_len, max_span, span_stride);
+                       out_draft_len, spans, span_len, max_span, span_stride, counts);
     return hipGetLastError();
 }
 

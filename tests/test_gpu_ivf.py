@@ -181,3 +181,36 @@ def test_ivf_rejects_bad_list_ids():
     bad[17] = 16
     with pytest.raises(sense.SenseError):
         sense.sense_build_ivf_index(ds.keys, ds.spans, cen, bad)
+
+
+def test_ivf_skewed_lists_with_fewer_candidates_than_k():
+    """One list holds most rows and is not probed, so the candidate buffer
+    (sized for the largest lists) is mostly padding: every real candidate
+    must come back, then padding (a chunk of the buffer can hold more than k
+    entries but fewer than k real ones)."""
+    n, d, nlist = 12000, 64, 40
+    w, ds = store(n, d, "bf16", 11)
+    g = torch.Generator(device=DEV).manual_seed(11)
+    cen = torch.randn(nlist, d, generator=g, device=DEV)
+    q = cen[5:6].clone().contiguous()
+    cen[0] = -q[0]                                   # the big list points away from the query
+    lists = torch.zeros(n, dtype=torch.int32, device=DEV)
+    small = torch.arange(10000, n, device=DEV)
+    lists[small] = (1 + (small - 10000) % (nlist - 1)).to(torch.int32)
+    index = sense.sense_build_ivf_index(ds.keys, ds.spans, cen, lists)
+    ids, sc, _, _, probe = sense.sense_ivf_search(index, q, 100, 1, want_probe=True)
+    torch.cuda.synchronize()
+    kb = host_bits(ds.keys)
+    o_probe, coarse, o_ids, o_sc = oracle.ivf_search(q[0].cpu().numpy(), cen.cpu().numpy(),
+                                                      lists.cpu().numpy(), 1, 100, "cosine",
+                                                      keys=kb, key_dtype="bf16")
+    assert 0 not in probe[0].cpu().tolist()
+    real = int((o_ids >= 0).sum())
+    assert 0 < real < 100
+    g_ids = ids[0].cpu().numpy()
+    assert (g_ids[real:] == -1).all()
+    x = decoded(ds.keys)
+    cs = candidate_scores(x, lists.cpu().numpy(), probe[0].cpu().numpy(), q[0].cpu().numpy()
+                          .astype(np.float64), "cosine")
+    check_topk(g_ids[:real], sc[0, :real].cpu().numpy(), cs, real)
+    index.close()

@@ -114,6 +114,10 @@ SMALL_SCAN = [
     (70001, 40, "bf16", 1, 64, "cosine"),
     (3000, 56, "f16", 1, 5, "cosine"),
     (9000, 64, "bf16", 16, 64, "cosine"),       # query batch: matrix-core scan at d = 64
+    (300000, 64, "bf16", 16, 64, "cosine"),     # batch over a large store: sampled threshold
+    (200003, 32, "f16", 5, 100, "ip"),
+    (150001, 64, "bf16", 70, 16, "cosine"),     # two query groups
+    (140000, 48, "bf16", 4, 1024, "cosine"),    # largest k
 ]
 
 
@@ -122,7 +126,7 @@ def test_short_key_scan_matches_oracle(case):
     n, d, kdt, nq, k, metric = case
     print(f"[short-scan] case={case}", flush=True)
     w = synth.scaled(synth.WORKLOADS["tiny-16k-d4096"], n=n, d=d, key_dtype=kdt,
-                     n_clusters=64, n_outliers=2, metric=metric)
+                     n_clusters=max(64, 2 * nq), n_outliers=2, metric=metric)
     ds = synth.make_datastore(w, 13, DEV)
     q, src = synth.make_queries(w, ds, 13, n_queries=nq)
     index = sense.sense_build_index(ds.keys, ds.spans, metric=metric)
@@ -155,4 +159,30 @@ def test_pca_retrieval_chain():
     o_s = oracle.scores(ok_bits, "bf16", oq, "f32")
     check_topk(ids[0].cpu().numpy(), sc[0].cpu().numpy(), o_s[0], 32)
     assert int(ids[0, 0]) == int(src[0])
+    index.close()
+
+
+def test_batched_short_scan_when_every_row_passes_the_threshold():
+    """Rows at the sample positions (multiples of n // 32768) point away from
+    the queries and every other row points at them, so the sampled
+    threshold is the lowest score and every row passes the filter: the
+    result must still be the exact top-k (ties to the lower row)."""
+    n, d = 200000, 64
+    step = n // 32768
+    g = torch.Generator(device=DEV).manual_seed(5)
+    x = torch.randn(d, generator=g, device=DEV)
+    keys = x.repeat(n, 1)
+    keys[::step] = -x
+    keys = keys.to(torch.bfloat16).contiguous()
+    spans = torch.arange(n, dtype=torch.int32, device=DEV).unsqueeze(1).repeat(1, 4).contiguous()
+    q = torch.stack([x * s for s in (1.0, 2.0, 0.5, 3.0)]).contiguous()
+    index = sense.sense_build_index(keys, spans)
+    ids, sc, dr, _ = sense.sense_retrieve(index, q, 64)
+    torch.cuda.synchronize()
+    want = [i for i in range(n) if i % step != 0][:64]
+    for r in range(4):
+        assert ids[r].cpu().tolist() == want
+        assert dr[r, :, 0].cpu().tolist() == want
+    o_s = oracle.scores(host_bits(keys[:200]), "bf16", q.cpu().numpy(), "f32", "cosine")
+    np.testing.assert_allclose(sc[:, 0].cpu().numpy(), o_s[:, 1], rtol=1e-3)
     index.close()
