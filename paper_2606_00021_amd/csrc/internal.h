@@ -210,7 +210,7 @@ hipError_t launch_query_split(const float* queries, int nq, int d, int key_dtype
 // cand[q * cap + ...]: wave w of short_scan_waves(n_rows) fills its slots
 // [w * kShortSlots, (w + 1) * kShortSlots) (the rest padding keys), and the
 // overflow is appended at counts[q] (which starts at the slot area's size).
-constexpr int kShortSlots = 16;
+constexpr int kShortSlots = 4;
 int64_t short_scan_waves(int64_t n_rows);
 struct ShortScan {
     const void* keys;

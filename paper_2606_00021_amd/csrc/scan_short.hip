@@ -16,9 +16,10 @@
 // it back for the top-k costs more than reading the keys.  So the scan runs
 // twice: first over a strided sample of rows writing scores, whose per-query
 // k-th best packed key tau bounds the final k-th best from below; then over
-// all rows, keeping only rows whose packed key reaches tau: each wave has 16
-// slots per query, filled in order (ballot + popcount), and a query's
-// overflow list takes what does not fit.
+// all rows, keeping only rows whose packed key reaches tau: each wave has a
+// few slots per query (about k * rows_per_wave / sample rows survive per
+// wave, ~1-2 at the bench shape), filled in order (ballot + popcount), and a
+// query's overflow list takes what does not fit.
 // Every true top-k row passes, so the result is exact; the scores of both
 // passes come from the same instructions, hence the same bits.
 #include "internal.h"
@@ -36,7 +37,7 @@ typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 
 constexpr int kShortThreads = 256;
 constexpr int kShortDepth = 4;     // 16-key tiles in flight per wave
-static_assert(kShortSlots == 16, "one padding slot per lane of a 16-lane group");
+static_assert(kShortSlots <= 16, "one padding slot per lane of a 16-lane group");
 
 template <int KT>
 __device__ __forceinline__ f32x4 mfma(const u32x4& a, const u32x4& b, const f32x4& c) {

@@ -128,7 +128,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
     float* __restrict__ out_scores, int32_t* __restrict__ out_drafts,
     int32_t* __restrict__ out_draft_len, const int32_t* __restrict__ spans,
     const int32_t* __restrict__ span_len, int max_span, int64_t span_stride,
-    const int32_t* __restrict__ dev_count) {
+    const int32_t* __restrict__ dev_count, int32_t* __restrict__ next_count) {
     __shared__ uint64_t s_sel[kMaxK];
     __shared__ uint32_t s_hist[kWaves * 256];
     __shared__ uint32_t s_tot[256];
@@ -141,6 +141,16 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
     // dev_count: a per-query count on the device (at most count).
     const int64_t cnt_q = (dev_count && dev_count[q] < count) ? dev_count[q] : count;
     const int64_t remain = cnt_q - start;
+    if constexpr (!FINAL) {
+        // With device counts the next level reads only the chunks that hold
+        // keys: their number is published, and empty chunks write nothing.
+        if (dev_count) {
+            const int kk0 = k < kSelectChunk ? k : kSelectChunk;
+            if (blockIdx.x == 0 && threadIdx.x == 0)
+                next_count[q] = (int32_t)(((cnt_q + kSelectChunk - 1) / kSelectChunk) * kk0);
+            if (remain <= 0) return;                 // uniform over the block
+        }
+    }
     const int len = (int)(remain < kSelectChunk ? remain : kSelectChunk);
     const int kk = k < kSelectChunk ? k : kSelectChunk;
 
@@ -239,12 +249,20 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 }  // namespace
 
+// One of the two key buffers of the selection levels, 256-byte rounded.
+static size_t key_buffer_bytes(int64_t n, int nq, int k) {
+    const int64_t chunks = ceil_div(n, kSelectChunk);
+    const int64_t kk = k < kSelectChunk ? k : kSelectChunk;
+    return ((size_t)nq * (size_t)chunks * (size_t)kk * sizeof(uint64_t) + 255) / 256 * 256;
+}
+
 size_t topk_workspace_bytes(int64_t n, int nq, int k) {
     const int64_t chunks = ceil_div(n, kSelectChunk);
     if (chunks <= 1) return 0;
     const int64_t kk = k < kSelectChunk ? k : kSelectChunk;
     const size_t one = (size_t)nq * (size_t)chunks * (size_t)kk * sizeof(uint64_t);
-    return 2 * ((one + 255) / 256 * 256);
+    // two key buffers, then two per-query count buffers (device-count inputs)
+    return 2 * ((one + 255) / 256 * 256) + 2 * (((size_t)nq * 4 + 255) / 256 * 256);
 }
 
 hipError_t launch_topk_gather(const float* scores, int64_t n, int nq, int k,
@@ -256,14 +274,14 @@ hipError_t launch_topk_gather(const float* scores, int64_t n, int nq, int k,
     if (chunks <= 1) {
         hipLaunchKernelGGL((select_kernel<true, true>), dim3(1, nq), dim3(kThreads), 0, stream,
                            scores, nullptr, n, k, nullptr, out_ids, out_scores, out_drafts,
-                           out_draft_len, spans, span_len, max_span, span_stride, nullptr);
+                           out_draft_len, spans, span_len, max_span, span_stride, nullptr, nullptr);
         return hipGetLastError();
     }
-    const size_t one = topk_workspace_bytes(n, nq, k) / 2;
+    const size_t one = key_buffer_bytes(n, nq, k);
     uint64_t* buf[2] = {(uint64_t*)workspace, (uint64_t*)((char*)workspace + one)};
     hipLaunchKernelGGL((select_kernel<true, false>), dim3((unsigned)chunks, nq), dim3(kThreads),
                        0, stream, scores, nullptr, n, k, buf[0], nullptr, nullptr, nullptr,
-                       nullptr, nullptr, nullptr, 0, 0, nullptr);
+                       nullptr, nullptr, nullptr, 0, 0, nullptr, nullptr);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     int64_t count = chunks * kk;
@@ -271,14 +289,15 @@ hipError_t launch_topk_gather(const float* scores, int64_t n, int nq, int k,
     while ((chunks = ceil_div(count, kSelectChunk)) > 1) {
         hipLaunchKernelGGL((select_kernel<false, false>), dim3((unsigned)chunks, nq),
                            dim3(kThreads), 0, stream, nullptr, buf[cur], count, k, buf[cur ^ 1],
-                           nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 0, 0, nullptr);
+                           nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 0, 0, nullptr,
+                           nullptr);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         count = chunks * kk;
         cur ^= 1;
     }
     hipLaunchKernelGGL((select_kernel<false, true>), dim3(1, nq), dim3(kThreads), 0, stream,
                        nullptr, buf[cur], count, k, nullptr, out_ids, out_scores, out_drafts,
-                       out_draft_len, spans, span_len, max_span, span_stride, nullptr);
+                       out_draft_len, spans, span_len, max_span, span_stride, nullptr, nullptr);
     return hipGetLastError();
 }
 
@@ -291,17 +310,25 @@ hipError_t launch_topk_keys(const uint64_t* keys, int64_t count, int nq, int k,
     int64_t chunks = ceil_div(count, kSelectChunk);
     const uint64_t* cur_in = keys;
     int64_t cur_count = count;
-    const size_t one = topk_workspace_bytes(count, nq, k) / 2;
+    const size_t one = key_buffer_bytes(count, nq, k);
     uint64_t* buf[2] = {(uint64_t*)workspace, (uint64_t*)((char*)workspace + one)};
     int cur = 0;
     hipError_t e;
-    const int32_t* counts = dev_count;         // the input's counts (first level only)
+    // Per-query counts on the device, level by level (ping-pong after the
+    // key buffers).
+    int32_t* cnt_buf[2] = {(int32_t*)((char*)workspace + 2 * one),
+                           (int32_t*)((char*)workspace + 2 * one + ((size_t)nq * 4 + 255) / 256 * 256)};
+    const int32_t* counts = dev_count;
+    int cc = 0;
     while (chunks > 1) {
+        int32_t* next = counts ? cnt_buf[cc] : nullptr;
         hipLaunchKernelGGL((select_kernel<false, false>), dim3((unsigned)chunks, nq),
                            dim3(kThreads), 0, stream, nullptr, cur_in, cur_count, k, buf[cur],
-                           nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 0, 0, counts);
+                           nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 0, 0, counts,
+                           next);
         if ((e = hipGetLastError()) != hipSuccess) return e;
-        counts = nullptr;
+        counts = next;
+        cc ^= 1;
         cur_in = buf[cur];
         cur_count = chunks * kk;
         cur ^= 1;
@@ -309,7 +336,7 @@ hipError_t launch_topk_keys(const uint64_t* keys, int64_t count, int nq, int k,
     }
     hipLaunchKernelGGL((select_kernel<false, true>), dim3(1, nq), dim3(kThreads), 0, stream,
                        nullptr, cur_in, cur_count, k, nullptr, out_ids, out_scores, out_drafts,
-                       out_draft_len, spans, span_len, max_span, span_stride, counts);
+                       out_draft_len, spans, span_len, max_span, span_stride, counts, nullptr);
     return hipGetLastError();
 }
 
