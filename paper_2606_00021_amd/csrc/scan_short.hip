@@ -53,18 +53,26 @@ __device__ __forceinline__ f32x4 mfma(const u32x4& a, const u32x4& b, const f32x
 template <int KT, int NT, int KS, bool SPLIT, bool FILTER>
 __global__ __launch_bounds__(kShortThreads, 2) void scan_short_kernel(ShortScan s,
                                                                   int64_t rows_per_wave) {
-    // Per-query scale and threshold in LDS (read in the epilogue without a
-    // wait on the key loads in flight, and without registers).
-    __shared__ float s_iq[64];
-    __shared__ uint64_t s_tau[64];
+    // Per query: {scale 1/|q|, threshold score}, in LDS (read in the
+    // epilogue without a wait on the key loads in flight, and without
+    // registers).  A row passes the filter when its score is not below the
+    // threshold score: a superset of the rows whose packed key reaches tau
+    // (a NaN threshold, from a NaN tau or a sample without k rows, lets
+    // every row through).  Queries past nq get +inf and are also checked by
+    // index before anything is stored.
+    __shared__ float2 s_qt[64];
     if (threadIdx.x < 64) {
         const int q = threadIdx.x;
-        s_iq[q] = q < 16 * NT ? s.inv_qn[q] : 0.0f;
-        if constexpr (FILTER) s_tau[q] = q < s.nq ? s.tau[q] : ~0ull;
+        float th = 0.0f;
+        if constexpr (FILTER)
+            th = q < s.nq ? key_score((uint32_t)(s.tau[q] >> 32)) : __builtin_inff();
+        s_qt[q] = float2{q < 16 * NT ? s.inv_qn[q] : 0.0f, th};
     }
     __syncthreads();
     const int lane = threadIdx.x & 63;
-    const int64_t wave = (int64_t)blockIdx.x * (kShortThreads / 64) + (threadIdx.x >> 6);
+    // The wave index is uniform: the row loop below is then a scalar loop.
+    const int64_t wave = (int64_t)blockIdx.x * (kShortThreads / 64) +
+                         __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t r0 = wave * rows_per_wave;
     if (r0 >= s.n_rows) return;                      // uniform over the wave
     const int64_t r1 = (r0 + rows_per_wave < s.n_rows) ? r0 + rows_per_wave : s.n_rows;
@@ -90,26 +98,41 @@ __global__ __launch_bounds__(kShortThreads, 2) void scan_short_kernel(ShortScan 
 #pragma unroll
         for (int i = 0; i < 4; ++i) cnt[t][i] = 0;
 
-    // Everything an iteration reads comes in with the tile (keys and the key
-    // norm): a load issued later and consumed earlier would make the wave
-    // wait for all the tiles in flight before it.
-    const uint16_t* keys = (const uint16_t*)s.keys;
-    auto load_tile = [&](int64_t base, u32x4 (&b)[KS], float& kn) {
-        const int64_t r = base + col;
-        const bool ok = r < r1;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            const int dim = 8 * grp + 32 * ks;
-            b[ks] = (ok && dim < s.d)
-                        ? __builtin_nontemporal_load(
-                              (const u32x4*)(keys + r * s.row_step * s.ld + dim))
-                        : u32x4{0u, 0u, 0u, 0u};
+    // This lane's key row advances by 16 rows per tile: pointers step by a
+    // fixed stride (no 64-bit multiplies per tile).  Every load is issued
+    // unconditionally, so the compiler can count the loads in flight exactly
+    // (a load under a branch makes it wait for all of them): rows past r1
+    // re-read the lane's last row (their scores are discarded), dims past d
+    // read dim 0 and are zeroed before use.  Everything an iteration reads
+    // comes in with the tile (keys and the key norm): a load issued later and
+    // consumed earlier would make the wave wait for all the tiles in flight
+    // before it.
+    const int64_t key_step = 16 * s.row_step * s.ld;
+    const int64_t norm_step = s.inv_norm ? 16 * s.row_step : 0;
+    const int64_t row_first = (r0 + col < r1) ? r0 + col : r1 - 1;
+    const uint16_t* kp = (const uint16_t*)s.keys + row_first * s.row_step * s.ld;
+    // Without key norms the norm load reads a fixed valid word (unused).
+    const float* np = s.inv_norm ? s.inv_norm + row_first * s.row_step : s.inv_qn;
+    const bool dim0 = 8 * grp < s.d;                 // this lane's dims hold key elements
+    const bool dim1 = 8 * grp + 32 < s.d;            // ... in the second k-step
+    const int off0 = dim0 ? 8 * grp : 0;
+    const int off1 = dim1 ? 8 * grp + 32 : 0;
+    int64_t lr = r0 + col;                           // row of the next tile to load
+    auto load_tile = [&](u32x4 (&b)[KS], float& kn) {
+        b[0] = __builtin_nontemporal_load((const u32x4*)(kp + off0));
+        if constexpr (KS == 2) b[1] = __builtin_nontemporal_load((const u32x4*)(kp + off1));
+        kn = *np;
+        lr += 16;
+        if (lr < r1) {                               // the next load stays on a valid row
+            kp += key_step;
+            np += norm_step;
         }
-        kn = (ok && s.inv_norm) ? s.inv_norm[r * s.row_step] : 1.0f;
     };
-    auto consume = [&](int64_t base, const u32x4 (&b)[KS], float kn) {
-        const int64_t r = base + col;                // this lane's key (column)
-        f32x4 acc[NT];
+    // The products of one tile; the tile's registers are free afterwards.
+    auto products = [&](const u32x4 (&bt)[KS], f32x4 (&acc)[NT]) {
+        u32x4 b[KS];
+        b[0] = dim0 ? bt[0] : u32x4{0u, 0u, 0u, 0u};
+        if constexpr (KS == 2) b[1] = dim1 ? bt[1] : u32x4{0u, 0u, 0u, 0u};
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             acc[t] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
@@ -119,43 +142,70 @@ __global__ __launch_bounds__(kShortThreads, 2) void scan_short_kernel(ShortScan 
                 if constexpr (SPLIT) acc[t] = mfma<KT>(alo[t][ks], b[ks], acc[t]);
             }
         }
-        if (r >= r1) return;
-        const int64_t orig = r * s.row_step;
+    };
+    // Scores of row r (this lane's key) for every query, then the store
+    // (scores) or the filter (survivor keys).
+    auto epilogue = [&](int64_t r, const f32x4 (&acc)[NT], float kn) {
+        const bool ok = r < r1;
+        float v[NT][4];
 #pragma unroll
-        for (int t = 0; t < NT; ++t) {
+        for (int t = 0; t < NT; ++t)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const int qq = 16 * t + 4 * grp + i;
-                float v = acc[t][i];
-                if (s.inv_norm) v = v * kn;
-                v = v * s_iq[qq];
-                if constexpr (FILTER) {
-                    // Survivors go to this wave's own slots of the query (a
-                    // slot index from a ballot, no atomic: a returned atomic
-                    // would make the wave wait for its tiles in flight); a
-                    // wave with more than kShortSlots survivors for one query
-                    // appends the rest to the query's overflow list.
-                    const uint64_t key = pack_key(v, (uint32_t)orig);
-                    const bool pass = key >= s_tau[qq];
-                    const uint64_t bal = __ballot(pass);
-                    if (bal) {
-                        const uint32_t gm = (uint32_t)(bal >> (16 * grp)) & 0xFFFFu;
-                        const int slot = cnt[t][i] + __popc(gm & ((1u << col) - 1u));
-                        if (pass) {
-                            const int q = 16 * t + 4 * grp + i;
-                            uint64_t* cq = s.cand + (int64_t)q * s.cap;
-                            if (slot < kShortSlots) {
-                                cq[wave * kShortSlots + slot] = key;
-                            } else {
-                                const int pos = atomicAdd(&s.counts[q], 1);
-                                cq[pos] = key;
-                            }
-                        }
-                        cnt[t][i] += __popc(gm);
-                    }
-                } else {
+                v[t][i] = acc[t][i];
+                if (s.inv_norm) v[t][i] = v[t][i] * kn;
+                v[t][i] = v[t][i] * s_qt[16 * t + 4 * grp + i].x;
+            }
+        if constexpr (!FILTER) {
+            if (!ok) return;
+#pragma unroll
+            for (int t = 0; t < NT; ++t)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
                     const int q = 16 * t + 4 * grp + i;
-                    if (q < s.nq) s.scores[(int64_t)q * s.n_rows + r] = v;
+                    if (q < s.nq) s.scores[(int64_t)q * s.n_rows + r] = v[t][i];
+                }
+        } else {
+            // One float compare per score, all of them (and their threshold
+            // reads) before any branch; then a branch per query and key
+            // group only where something passed.
+            uint64_t bal[NT][4];
+#pragma unroll
+            for (int t = 0; t < NT; ++t)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    bal[t][i] = __ballot(ok & !(v[t][i] < s_qt[16 * t + 4 * grp + i].y));
+            // Survivors go to this wave's own slots of the query (a slot
+            // index from the ballot, no atomic: a returned atomic would make
+            // the wave wait for its tiles in flight); a wave with more than
+            // kShortSlots survivors for one query appends the rest to the
+            // query's overflow list.
+            const int64_t orig = r * s.row_step;
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    if (bal[t][i] == 0) continue;
+                    const int q = 16 * t + 4 * grp + i;
+                    const bool pass = (bal[t][i] >> lane) & 1;
+                    const uint32_t gm = (uint32_t)(bal[t][i] >> (16 * grp)) & 0xFFFFu;
+                    const int slot = cnt[t][i] + __popc(gm & ((1u << col) - 1u));
+                    if (pass && q < s.nq) {
+                        const uint64_t key = pack_key(v[t][i], (uint32_t)orig);
+                        uint64_t* cq = s.cand + (int64_t)q * s.cap;
+                        if (slot < kShortSlots) {
+                            cq[wave * kShortSlots + slot] = key;
+                        } else {
+                            // Rare.  The empty asm keeps this store apart
+                            // from the slot store: merged, every survivor
+                            // would wait for the atomic's result and with it
+                            // for all the tiles in flight.
+                            const int pos = atomicAdd(&s.counts[q], 1);
+                            cq[pos] = key;
+                            __asm__ volatile("" ::: "memory");
+                        }
+                    }
+                    cnt[t][i] += __popc(gm);
                 }
             }
         }
@@ -163,13 +213,24 @@ __global__ __launch_bounds__(kShortThreads, 2) void scan_short_kernel(ShortScan 
 
     u32x4 buf[kShortDepth][KS];
     float kn[kShortDepth];
+    // The first tiles in the loop's own order (keys, then norm, per tile):
+    // the wait at the loop head is computed for both ways in, so a
+    // different order here would make every iteration wait for more tiles.
 #pragma unroll
-    for (int u = 0; u < kShortDepth; ++u) load_tile(r0 + 16 * u, buf[u], kn[u]);
+    for (int u = 0; u < kShortDepth; ++u) {
+        load_tile(buf[u], kn[u]);
+        __builtin_amdgcn_sched_barrier(0);
+    }
     for (int64_t base = r0; base < r1; base += 16 * kShortDepth) {
 #pragma unroll
         for (int u = 0; u < kShortDepth; ++u) {
-            consume(base + 16 * u, buf[u], kn[u]);
-            load_tile(base + 16 * (u + kShortDepth), buf[u], kn[u]);
+            // The slot's next tile is requested before the epilogue, whose
+            // branches would otherwise keep the load behind them.
+            f32x4 acc[NT];
+            products(buf[u], acc);
+            const float knu = kn[u];
+            load_tile(buf[u], kn[u]);
+            epilogue(base + 16 * u + col, acc, knu);
         }
     }
     if constexpr (FILTER) {
