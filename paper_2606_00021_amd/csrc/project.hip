@@ -29,13 +29,6 @@ __device__ __forceinline__ float wsum(float x) {
     return x;
 }
 
-__device__ __forceinline__ float load_x(const void* p, int dt, int64_t i) {
-    if (dt == DT_F32) return ((const float*)p)[i];
-    const uint16_t b = ((const uint16_t*)p)[i];
-    if (dt == DT_F16) return (float)__builtin_bit_cast(_Float16, b);
-    return __builtin_bit_cast(float, (uint32_t)b << 16);
-}
-
 __device__ __forceinline__ void store_out(void* p, int dt, int64_t i, float v) {
     if (dt == DT_F32) ((float*)p)[i] = v;
     else ((uint16_t*)p)[i] = to_bits16(v, dt);
@@ -89,24 +82,50 @@ __global__ __launch_bounds__(kProjThreads) void project_finish_kernel(
 }
 
 // Direct route, step 1: raw[i][o] = (x_i - mean) . w_o, one block of 256
-// threads per (row, output): each thread's 16-32 elements are loaded at
-// once (one round of memory latency), then a fixed-order block sum.
+// threads per (row, output).  A thread's elements come in batches of 16
+// loads issued together (clamped indices, no branch around a load, so none
+// waits for the one before it), then a fixed-order block sum: element t goes
+// to partial (t / 256) % 4 of its thread.
 constexpr int kDotThreads = 256;
+constexpr int kDotBatch = 16;
 
+template <int XT>
+__device__ __forceinline__ float load_xt(const void* p, int64_t i) {
+    if constexpr (XT == DT_F32) return ((const float*)p)[i];
+    const uint16_t b = ((const uint16_t*)p)[i];
+    if constexpr (XT == DT_F16) return (float)__builtin_bit_cast(_Float16, b);
+    return __builtin_bit_cast(float, (uint32_t)b << 16);
+}
+
+template <int XT>
 __global__ __launch_bounds__(kDotThreads) void project_dots_kernel(
-    const void* __restrict__ x, int x_dtype, int64_t x_stride, int d_in,
-    const float* __restrict__ mean, const float* __restrict__ basis, int d_out,
-    float* __restrict__ raw) {
+    const void* __restrict__ x, int64_t x_stride, int d_in, const float* __restrict__ mean,
+    const float* __restrict__ basis, int d_out, float* __restrict__ raw) {
     __shared__ float s_part[kDotThreads / 64];
     const int o = blockIdx.y;
     const int64_t i = blockIdx.x;
     const float* w = basis + (int64_t)o * d_in;
+    const float* m = mean ? mean : w;             // a valid address; unused without a mean
     float a[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll 16
-    for (int t = threadIdx.x; t < d_in; t += kDotThreads) {
-        const float c = load_x(x, x_dtype, i * x_stride + t) - (mean ? mean[t] : 0.0f);
-        const int k = (t / kDotThreads) & 3;
-        a[k] = __builtin_fmaf(c, w[t], a[k]);
+    for (int t0 = 0; t0 < d_in; t0 += kDotBatch * kDotThreads) {
+        float xv[kDotBatch], wv[kDotBatch], mv[kDotBatch];
+#pragma unroll
+        for (int u = 0; u < kDotBatch; ++u) {
+            const int t = t0 + u * kDotThreads + (int)threadIdx.x;
+            const int tc = t < d_in ? t : d_in - 1;
+            xv[u] = load_xt<XT>(x, i * x_stride + tc);
+            wv[u] = w[tc];
+            mv[u] = m[tc];
+        }
+#pragma unroll
+        for (int u = 0; u < kDotBatch; ++u) {
+            const int t = t0 + u * kDotThreads + (int)threadIdx.x;
+            if (t < d_in) {
+                const float c = xv[u] - (mean ? mv[u] : 0.0f);
+                const int k = (t / kDotThreads) & 3;
+                a[k] = __builtin_fmaf(c, wv[u], a[k]);
+            }
+        }
     }
     const float v = wsum((a[0] + a[1]) + (a[2] + a[3]));
     if ((threadIdx.x & 63) == 0) s_part[threadIdx.x >> 6] = v;
@@ -161,8 +180,15 @@ hipError_t launch_project(const void* x, int x_dtype, int64_t n, int d_in, int64
     hipError_t e;
     if (!project_uses_mfma(x_dtype, x, x_stride, n)) {
         const dim3 grid((unsigned)n, (unsigned)d_out);
-        hipLaunchKernelGGL(project_dots_kernel, grid, dim3(kDotThreads), 0, stream, x, x_dtype,
-                           x_stride, d_in, mean, basis, d_out, s);
+        if (x_dtype == DT_F32)
+            hipLaunchKernelGGL(project_dots_kernel<DT_F32>, grid, dim3(kDotThreads), 0, stream, x,
+                               x_stride, d_in, mean, basis, d_out, s);
+        else if (x_dtype == DT_F16)
+            hipLaunchKernelGGL(project_dots_kernel<DT_F16>, grid, dim3(kDotThreads), 0, stream, x,
+                               x_stride, d_in, mean, basis, d_out, s);
+        else
+            hipLaunchKernelGGL(project_dots_kernel<DT_BF16>, grid, dim3(kDotThreads), 0, stream, x,
+                               x_stride, d_in, mean, basis, d_out, s);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         hipLaunchKernelGGL(project_norm_kernel, dim3((unsigned)n), dim3(64), 0, stream, s, d_out,
                            normalize, out, out_dtype, out_stride);

@@ -200,6 +200,15 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
         qsrc[j] = base + (int64_t)(mt * 16 + col) * d + grp * 8;
         qstep[j] = fs / NA;
     }
+    // 1/|q| of this lane's output rows, once: the batch is padded to whole
+    // 16-query tiles, so every index is in bounds.  (Loaded per block under
+    // the q < nq test, each load would wait for the one before it, with no
+    // other workgroup on the CU to cover the wait.)
+    float iq[MT][4];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) iq[mt][i] = inv_qn[mt * 16 + grp * 4 + i];
     // B-operand entry of this lane inside a key tile, for unit u = 4*step + grp.
     const int ri = col >> 3, rp = col & 7;
     auto bentry = [&](int step) { return ri * kTileSecond + 8 * rp + (((4 * step + grp) - rp) & 7); };
@@ -278,11 +287,27 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
         wait_vmcnt<0>();
         barrier_no_fence();
 
+        // Key norms of this lane's keys, all requested before any is used
+        // (rows past n read the last row; their scores are not stored).
+        float kscale[T];
+#pragma unroll
+        for (int t = 0; t < T; ++t) {
+            const int64_t key = key0 + t * 16 + col;
+            kscale[t] = inv_norm ? inv_norm[key < n ? key : n - 1] : 1.0f;
+        }
+        // Take delivery of the scales here, once: a load still pending when
+        // the conditional stores start would cost a full wait before each
+        // store (pending loads and stores share one counter).
+#pragma unroll
+        for (int t = 0; t < T; ++t) asm volatile("" : "+v"(kscale[t]));
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) asm volatile("" : "+v"(iq[mt][i]));
 #pragma unroll
         for (int t = 0; t < T; ++t) {
             const int64_t key = key0 + t * 16 + col;
             if (!kv[t]) continue;
-            const float kscale = inv_norm ? inv_norm[key] : 1.0f;
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
@@ -290,8 +315,8 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
                     const int q = mt * 16 + grp * 4 + i;
                     if (q < nq) {
                         float v = acc[t][mt][i];
-                        if (inv_norm) v = v * kscale;
-                        scores[(int64_t)q * n + key] = v * inv_qn[q];
+                        if (inv_norm) v = v * kscale[t];
+                        scores[(int64_t)q * n + key] = v * iq[mt][i];
                     }
                 }
             }

@@ -9,14 +9,18 @@
 // largest keys" and ties need no special handling.
 //
 // Selection is hierarchical.  A block of 512 threads takes a chunk of 8192
-// keys into registers (16 per thread) and finds the chunk's k largest with an
-// 8-bit radix select: per pass a 256-bin LDS histogram of the next digit
-// among the keys that still match the chosen prefix, then one wave finds the
-// digit holding the k-th key with a suffix scan.  The pass loop stops as
-// soon as the chosen digit's bucket is taken whole, so most chunks need 2-4
-// passes.  The k
-// survivors of every chunk form the next level's input until one chunk
-// remains; its k keys are sorted with a bitonic network in LDS and written
+// keys into registers (16 per thread).  One reduction gives the number of
+// real (non-padding) keys and the AND and OR of them: the bits above the
+// highest bit where they differ are shared by all, so the radix select
+// starts right below them (scores of one query share their sign and most of
+// their exponent, which a fixed top-down start would spend a whole pass on).
+// Each pass builds a 256-bin LDS histogram of the next 8-bit digit among the
+// keys that still match the chosen prefix, then one wave finds the digit
+// holding the k-th key with a suffix scan; the loop stops as soon as that
+// digit's bucket is taken whole.  The taken keys are compacted by ballot
+// prefix sums (no atomics).  The k survivors of every chunk form the next
+// level's input until one chunk remains; its keys are put in order by rank
+// (each key counts the keys above it, all reads LDS broadcasts) and written
 // out together with the gathered continuations.
 #include "internal.h"
 
@@ -31,33 +35,83 @@ struct SelectState {
 };
 
 constexpr int kWaves = kThreads / 64;
+constexpr int kRankMax = 256;   // final orders up to this many keys by rank, more by bitonic sort
 constexpr int kPer = kSelectChunk / kThreads;   // keys per thread
+
+// Real keys of the block (non-zero; a candidate buffer may hold padding keys
+// anywhere, so a chunk's length alone does not tell) and the AND / OR of
+// them.  All threads of the block must call it.
+struct ChunkStats {
+    uint32_t nz;
+    uint64_t all_and, any_or;
+};
+
+__device__ ChunkStats chunk_stats(const uint64_t (&key)[kPer], uint32_t* s_nzw, uint64_t* s_andw,
+                                  uint64_t* s_orw) {
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    uint32_t nz = 0;
+    uint64_t a = ~0ull, o = 0ull;
+#pragma unroll
+    for (int e = 0; e < kPer; ++e) {
+        nz += (uint32_t)__popcll(__ballot(key[e] != 0));
+        if (key[e] != 0) {
+            a &= key[e];
+            o |= key[e];
+        }
+    }
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        a &= __shfl_xor(a, off, 64);
+        o |= __shfl_xor(o, off, 64);
+    }
+    if (lane == 0) {
+        s_nzw[wv] = nz;
+        s_andw[wv] = a;
+        s_orw[wv] = o;
+    }
+    __syncthreads();
+    ChunkStats r{0u, ~0ull, 0ull};
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+        r.nz += s_nzw[w];
+        r.all_and &= s_andw[w];
+        r.any_or |= s_orw[w];
+    }
+    return r;
+}
 
 // Finds prefix/mask such that exactly `need` of the block's keys (kPer per
 // thread, held in registers; unused slots hold the padding key 0) satisfy
-// (key & mask) >= prefix.  Requires 1 <= need <= number of keys above 0.
-// All threads of the block must call it.
+// (key & mask) >= prefix.  Requires 1 <= need < cs.nz (the number of real
+// keys).  All threads of the block must call it.
 //
-// 8-bit digits from the top; a pass stops the search as soon as the digit
-// holding the need-th key is taken whole.  Each wave counts into its own
-// 256-bin LDS histogram.  Scores cluster in a few digit values (the leading
-// byte holds sign and exponent) and LDS atomics of one instruction to one
+// Digits of up to 8 bits from the highest bit where the real keys differ; a
+// pass stops the search as soon as the digit holding the need-th key is
+// taken whole.  Each wave counts into its own 256-bin LDS histogram.  Scores
+// cluster in a few digit values and LDS atomics of one instruction to one
 // address serialise, so each wave first adds all lanes sharing its first
 // active lane's digit with one atomic (ballot + popcount) and only the other
 // lanes add one by one.
-__device__ SelectState radix_select(const uint64_t (&key)[kPer], int need, uint32_t* s_hist,
-                                    uint32_t* s_tot, uint32_t* s_info) {
+__device__ SelectState radix_select(const uint64_t (&key)[kPer], int need, const ChunkStats& cs,
+                                    uint32_t* s_hist, uint32_t* s_tot, uint32_t* s_info) {
     const int tid = threadIdx.x;
     const int lane = tid & 63, wv = tid >> 6;
     uint32_t* my = s_hist + wv * 256;
+    const uint64_t diff = cs.all_and ^ cs.any_or;
+    if (diff == 0) return SelectState{cs.all_and, ~0ull};   // every real key is the same
+    const int hb = 63 - __clzll((long long)diff);
+    // Bits above hb are common to every real key (2 << 63 wraps to 0: no bits).
+    uint64_t mask = ~((2ull << hb) - 1ull);
+    uint64_t prefix = cs.all_and & mask;
     for (int b = tid; b < kWaves * 256; b += kThreads) s_hist[b] = 0;
     __syncthreads();
-    uint64_t prefix = 0, mask = 0;
-    for (int shift = 56; shift >= 0; shift -= 8) {
+    for (int hi = hb; hi >= 0; hi -= 8) {
+        const int lo = hi >= 7 ? hi - 7 : 0;
+        const uint32_t dmask = (1u << (hi - lo + 1)) - 1u;
 #pragma unroll
         for (int e = 0; e < kPer; ++e) {
             const bool act = (key[e] & mask) == prefix;
-            const uint32_t dg = (uint32_t)(key[e] >> shift) & 0xFFu;
+            const uint32_t dg = (uint32_t)(key[e] >> lo) & dmask;
             const uint64_t am = __ballot(act);
             if (am) {
                 const int first = __ffsll((unsigned long long)am) - 1;
@@ -110,12 +164,42 @@ __device__ SelectState radix_select(const uint64_t (&key)[kPer], int need, uint3
         // first barrier, after which wave 0 may rewrite it.
         const uint32_t digit = s_info[0], above = s_info[1], in_bucket = s_info[2];
         need -= (int)above;
-        prefix |= (uint64_t)digit << shift;
-        mask |= (uint64_t)0xFF << shift;
+        prefix |= (uint64_t)digit << lo;
+        mask |= (uint64_t)dmask << lo;
         if ((int)in_bucket == need) break;
     }
     __syncthreads();
     return SelectState{prefix, mask};
+}
+
+// Writes the block's taken keys to dst[0 .. min(taken, cap)) in some order,
+// positions from ballot prefix sums; returns the number taken (all threads).
+template <typename Taken>
+__device__ uint32_t compact_taken(const uint64_t (&key)[kPer], Taken taken, uint64_t* dst,
+                                  int cap, uint32_t* s_wc) {
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    uint32_t mine = 0;
+#pragma unroll
+    for (int e = 0; e < kPer; ++e) mine += (uint32_t)__popcll(__ballot(taken(e)));
+    if (lane == 0) s_wc[wv] = mine;
+    __syncthreads();
+    uint32_t base = 0, total = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+        const uint32_t c = s_wc[w];
+        base += (w < wv) ? c : 0u;
+        total += c;
+    }
+    const uint64_t below = (1ull << lane) - 1ull;
+#pragma unroll
+    for (int e = 0; e < kPer; ++e) {
+        const bool t = taken(e);
+        const uint64_t m = __ballot(t);
+        const uint32_t pos = base + (uint32_t)__popcll(m & below);
+        if (t && pos < (uint32_t)cap) dst[pos] = key[e];
+        base += (uint32_t)__popcll(m);
+    }
+    return total;
 }
 
 // One block per (chunk, query).  FROM_SCORES: input is the fp32 score matrix
@@ -130,10 +214,12 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
     const int32_t* __restrict__ span_len, int max_span, int64_t span_stride,
     const int32_t* __restrict__ dev_count, int32_t* __restrict__ next_count) {
     __shared__ uint64_t s_sel[kMaxK];
+    __shared__ uint64_t s_sorted[FINAL ? kMaxK : 1];
     __shared__ uint32_t s_hist[kWaves * 256];
     __shared__ uint32_t s_tot[256];
     __shared__ uint32_t s_info[4];
-    __shared__ uint32_t s_cnt;
+    __shared__ uint32_t s_nzw[kWaves], s_wc[kWaves];
+    __shared__ uint64_t s_andw[kWaves], s_orw[kWaves];
 
     const int tid = threadIdx.x;
     const int q = blockIdx.y;
@@ -154,82 +240,87 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
     const int len = (int)(remain < kSelectChunk ? remain : kSelectChunk);
     const int kk = k < kSelectChunk ? k : kSelectChunk;
 
-    // Key i of the chunk is held by thread i % kThreads (all loads in flight
-    // at once); slots past the chunk hold the padding key 0.
+    // Key i of the chunk is held by thread i % kThreads; slots past the chunk
+    // hold the padding key 0.  Scores are loaded unconditionally (positions
+    // past the chunk re-read its last one, a chunk is never empty here) so
+    // that all loads are in flight at once: a load under a branch makes the
+    // thread wait for it before issuing the next.
     uint64_t key[kPer];
+    if constexpr (FROM_SCORES) {
+        const float* src = scores + (int64_t)q * count + start;
+        const int last = len > 0 ? len - 1 : 0;
+        float sv[kPer];
 #pragma unroll
-    for (int e = 0; e < kPer; ++e) {
-        const int i = tid + e * kThreads;
-        const int64_t pos = start + i;
-        if (i < len) {
-            if constexpr (FROM_SCORES)
-                key[e] = pack_key(scores[(int64_t)q * count + pos], (uint32_t)pos);
-            else
-                key[e] = in_keys[(int64_t)q * count + pos];
-        } else {
-            key[e] = 0;
+        for (int e = 0; e < kPer; ++e) {
+            const int i = tid + e * kThreads;
+            sv[e] = src[i < len ? i : last];
+        }
+#pragma unroll
+        for (int e = 0; e < kPer; ++e) {
+            const int i = tid + e * kThreads;
+            key[e] = i < len ? pack_key(sv[e], (uint32_t)(start + i)) : 0;
+        }
+    } else {
+#pragma unroll
+        for (int e = 0; e < kPer; ++e) {
+            const int i = tid + e * kThreads;
+            key[e] = i < len ? in_keys[(int64_t)q * count + start + i] : 0;
         }
     }
-    __shared__ uint32_t s_nz;
-    if (tid == 0) {
-        s_cnt = 0;
-        s_nz = 0;
-    }
-    __syncthreads();
-    // Real (non-padding) keys of the chunk: a candidate buffer may hold
-    // padding keys anywhere, so the chunk length alone does not tell.
-#pragma unroll
-    for (int e = 0; e < kPer; ++e) {
-        const uint64_t m = __ballot(key[e] != 0);
-        if ((tid & 63) == 0 && m) atomicAdd(&s_nz, (uint32_t)__popcll(m));
-    }
-    __syncthreads();
+    const ChunkStats cs = chunk_stats(key, s_nzw, s_andw, s_orw);
 
     // Keys taken: every real one if there are no more than kk, else the kk
-    // largest (then at least kk keys are real, as the radix select needs).
+    // largest (then more than kk keys are real, as the radix select needs).
     SelectState st{0, 0};
-    const bool all = s_nz <= (uint32_t)kk;
-    if (!all) st = radix_select(key, kk, s_hist, s_tot, s_info);
+    const bool all = cs.nz <= (uint32_t)kk;
+    if (!all) st = radix_select(key, kk, cs, s_hist, s_tot, s_info);
     auto taken = [&](int e) {
         return all ? (key[e] != 0) : ((key[e] & st.mask) >= st.prefix);
     };
 
     if constexpr (!FINAL) {
         uint64_t* out = out_keys + ((int64_t)q * gridDim.x + blockIdx.x) * kk;
-#pragma unroll
-        for (int e = 0; e < kPer; ++e) {
-            if (taken(e)) {
-                const uint32_t at = atomicAdd(&s_cnt, 1u);
-                if (at < (uint32_t)kk) out[at] = key[e];
-            }
-        }
-        __syncthreads();
-        const int nt = (int)s_cnt < kk ? (int)s_cnt : kk;
+        const uint32_t tot = compact_taken(key, taken, out, kk, s_wc);
+        const int nt = (int)tot < kk ? (int)tot : kk;
         for (int i = nt + tid; i < kk; i += kThreads) out[i] = 0;  // padding key
     } else {
-#pragma unroll
-        for (int e = 0; e < kPer; ++e) {
-            if (taken(e)) {
-                const uint32_t at = atomicAdd(&s_cnt, 1u);
-                if (at < (uint32_t)kk) s_sel[at] = key[e];
+        const uint32_t tot = compact_taken(key, taken, s_sel, kk, s_wc);
+        const int nt = (int)tot < kk ? (int)tot : kk;
+        int p = 1;
+        while (p < nt) p <<= 1;
+        __syncthreads();
+        const uint64_t* sorted = s_sorted;
+        if (p <= kRankMax) {
+            // Rank of each taken key among the taken ones (ties, impossible
+            // for distinct (score, row) keys, by position): its place in the
+            // output.
+            for (int i = tid; i < nt; i += kThreads) {
+                const uint64_t ki = s_sel[i];
+                int rank = 0;
+                for (int j = 0; j < nt; ++j) {
+                    const uint64_t kj = s_sel[j];
+                    rank += (kj > ki) | ((kj == ki) & (j < i));
+                }
+                s_sorted[rank] = ki;
             }
+            for (int r = nt + tid; r < k; r += kThreads) s_sorted[r] = 0;
+        } else {
+            // padding keys up to the sort size and up to k (read as output)
+            for (int r = nt + tid; r < (p > k ? p : k); r += kThreads) s_sel[r] = 0;
+            __syncthreads();
+            bitonic_desc<kThreads>(s_sel, p);
+            sorted = s_sel;
         }
         __syncthreads();
-        int p = 1;
-        while (p < kk) p <<= 1;
-        const int nt = (int)s_cnt < kk ? (int)s_cnt : kk;
-        for (int i = nt + tid; i < p; i += kThreads) s_sel[i] = 0;
-        __syncthreads();
-        bitonic_desc<kThreads>(s_sel, p);
         for (int r = tid; r < k; r += kThreads) {
-            const uint64_t key = s_sel[r];
+            const uint64_t key = sorted[r];
             out_ids[(int64_t)q * k + r] = key == 0 ? -1 : (int64_t)key_row(key);
             if (out_scores) out_scores[(int64_t)q * k + r] = key_score((uint32_t)(key >> 32));
         }
         if (out_drafts || out_draft_len) {
             for (int t = tid; t < k * max_span; t += kThreads) {
                 const int r = t / max_span, j = t - r * max_span;
-                const uint64_t key = s_sel[r];
+                const uint64_t key = sorted[r];
                 const int64_t id = (int64_t)key_row(key);
                 // A padding key (0) surfaces only when fewer than k
                 // candidates exist (an inverted-file search of short lists):

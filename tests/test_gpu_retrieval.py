@@ -6,6 +6,7 @@ the 16K x 4096 fp16, 262K x 4096 bf16, 1M x 3584 bf16 and 1M x 4096 bf16
 datastores, compared row for row (the oracle scores every stored row).
 """
 import sys
+import zlib
 
 import numpy as np
 import pytest
@@ -67,7 +68,7 @@ SMALL = [
 def test_small_cases(name, n, d, dt, k, metric):
     w = synth.scaled(synth.WORKLOADS["tiny-16k-d4096"], name=name, n=n, d=d, key_dtype=dt, k=k,
                      n_clusters=max(4, n // 256))
-    run_case(w, seed=hash(name) % 1000, metric=metric, ragged_spans=True)
+    run_case(w, seed=zlib.crc32(name.encode()) % 1000, metric=metric, ragged_spans=True)
 
 
 def test_strided_rows_and_copy():
@@ -99,7 +100,7 @@ BATCHED = [
 def test_batched_queries(name, n, d, dt, nq, k, metric):
     w = synth.scaled(synth.WORKLOADS["13b-batched-4m-d5120"], name=name, n=n, d=d, key_dtype=dt,
                      k=k, n_queries=nq, n_clusters=max(nq + 4, n // 128))
-    run_case(w, seed=hash(name) % 1000 + 1, metric=metric, ragged_spans=True)
+    run_case(w, seed=zlib.crc32(name.encode()) % 1000 + 1, metric=metric, ragged_spans=True)
 
 
 def test_batched_key_typed_queries():
@@ -153,6 +154,29 @@ def test_deterministic():
     b = sense.sense_retrieve(index, q, w.k)
     for x, y in zip(a, b):
         assert torch.equal(x, y)
+    index.close()
+
+
+@pytest.mark.parametrize("n,d,k,nq", [(8192, 512, 64, 1), (8192, 256, 64, 8), (20000, 512, 128, 1),
+                                      (30000, 256, 1024, 1)])
+def test_repeated_selection_is_stable(n, d, k, nq):
+    """The same retrieval repeated many times: every result equal to the
+    first and checked against the oracle (a race inside the selection block
+    shows up as an occasional wrong or duplicated row)."""
+    w = synth.scaled(synth.WORKLOADS["tiny-16k-d4096"], name="repeat", n=n, d=d, k=k,
+                     key_dtype="bf16", n_clusters=max(4, n // 256))
+    ds = synth.make_datastore(w, 31, DEV)
+    q, _ = synth.make_queries(w, ds, 31, n_queries=nq)
+    index = sense.sense_build_index(ds.keys, ds.spans)
+    first = sense.sense_retrieve(index, q, k)
+    torch.cuda.synchronize()
+    o_s = oracle.scores(host_bits(ds.keys), "bf16", q.cpu().numpy(), "f32", metric="cosine")
+    for qi in range(nq):
+        check_topk(first[0][qi].cpu().numpy(), first[1][qi].cpu().numpy(), o_s[qi], k)
+    for _ in range(40):
+        again = sense.sense_retrieve(index, q, k)
+        for x, y in zip(first, again):
+            assert torch.equal(x, y)
     index.close()
 
 
