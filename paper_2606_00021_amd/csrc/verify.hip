@@ -199,9 +199,7 @@ __global__ __launch_bounds__(kRowThreads) void verify_rows_kernel(
     const int tok = drafts[item];
     const bool valid = tok >= 0 && tok < vocab;
     const char* rowp = (const char*)logits + row * row_stride * ES;
-    const float xd = valid ? load_one<LT>(rowp, tok) : 0.0f;
     const int tk = valid ? tok : -1;                 // -1: the count is unused
-    const float thr_lo = xd, thr_hi = next_up(xd);   // left of d / from d on
 
     const int v0 = slice * slice_len;
     const int v1 = (v0 + slice_len < vocab) ? v0 + slice_len : vocab;
@@ -222,6 +220,10 @@ __global__ __launch_bounds__(kRowThreads) void verify_rows_kernel(
         const int vt = v0 + nvec * VW + tid;
         const bool has_t = vt < v1;
         const float xt = has_t ? load_one<LT>(rowp, vt) : -__builtin_inff();
+        // The judged token's logit, requested after the slice (it is first
+        // needed in phase 2).
+        const float xd = valid ? load_one<LT>(rowp, tok) : 0.0f;
+        const float thr_lo = xd, thr_hi = next_up(xd);   // left of d / from d on
 #pragma unroll
         for (int k = 0; k < kNV; ++k) {
             if (tid + k * kRowThreads < nvec) {
@@ -251,22 +253,39 @@ __global__ __launch_bounds__(kRowThreads) void verify_rows_kernel(
                     const float thr = (vb + VW <= tk) ? thr_lo : thr_hi;
 #pragma unroll
                     for (int u = 0; u < VW; ++u) absorb(acc, x[u], nm, thr);
-                    if (vb < tk && tk < vb + VW) {   // the vector holding d: ties left of d
-#pragma unroll
-                        for (int u = 0; u < VW; ++u) acc.cnt += (vb + u < tk && x[u] == xd) ? 1 : 0;
-                    }
                 }
             }
             if (has_t) absorb(acc, xt, nm, vt < tk ? thr_lo : thr_hi);
+            // The vector holding d was counted with x > x_d throughout; its
+            // elements left of d equal to x_d also rank above d.  Only the
+            // thread that loaded it adds them, from a second (cached) read,
+            // so no other element pays for the test.
+            const int id = (tk - v0) / VW;
+            if (tk > v0 && id < nvec && id % kRowThreads == tid && tk - (v0 + id * VW) > 0) {
+                float x[VW];
+                unpack<LT>(vp[id], x);
+                const int nl = tk - (v0 + id * VW);
+#pragma unroll
+                for (int u = 0; u < VW; ++u) acc.cnt += (u < nl && x[u] == xd) ? 1 : 0;
+            }
         }
     } else {
+        // Unconditional loads (positions past the slice re-read its first
+        // element and are set to -inf), so all of them are in flight at once.
         float x[kScalarPer];
 #pragma unroll
         for (int k = 0; k < kScalarPer; ++k) {
             const int v = v0 + tid + k * kRowThreads;
-            x[k] = (v < v1) ? load_one<LT>(rowp, v) : -__builtin_inff();
+            x[k] = load_one<LT>(rowp, v < v1 ? v : v0);
+        }
+#pragma unroll
+        for (int k = 0; k < kScalarPer; ++k) {
+            const int v = v0 + tid + k * kRowThreads;
+            if (v >= v1) x[k] = -__builtin_inff();
             mx = __builtin_fmaxf(mx, x[k]);
         }
+        const float xd = valid ? load_one<LT>(rowp, tok) : 0.0f;
+        const float thr_lo = xd, thr_hi = next_up(xd);   // left of d / from d on
         const float wm = wave_max_f(mx);
         if ((tid & 63) == 0) s_max[tid >> 6] = wm;
         __syncthreads();
@@ -299,21 +318,44 @@ __global__ __launch_bounds__(kRowThreads) void verify_rows_kernel(
 
 constexpr int kFinThreads = 256;
 constexpr int kFinChunkRows = 4096;   // (candidate, position) rows per LDS chunk
+constexpr int kGammaBatch = 16;       // tree finalize: Gamma entries loaded together
 
 __device__ __forceinline__ uint64_t bits_upto(int x) {  // bits 0..x set (x may be -1)
     return (x >= 63) ? ~0ull : ((x < 0) ? 0ull : ((1ull << (x + 1)) - 1ull));
 }
 
-// Row statistics of one item from its slice partials: the entropy score
-// and the rank of the judged token; bits em | ent<<1 | topk<<2.
-__device__ __forceinline__ uint8_t item_bits(const Partial* p, int n_slices, int tok, int vocab,
-                                             const GateParams& gp, float* score, int* rank) {
-    Stats a{p[0].m, p[0].s, p[0].t2};
-    int cnt = p[0].cnt;
-    for (int s = 1; s < n_slices; ++s) {
-        a = merge(a, Stats{p[s].m, p[s].s, p[s].t2});
-        cnt += p[s].cnt;
+// Merge of an item's slice partials in slice order.  Loads go out in
+// batches of kMergeBatch (clamped indices, no branch around a load, so none
+// waits for the one before it); the first merge with the empty state returns
+// slice 0 unchanged.
+constexpr int kMergeBatch = 8;
+
+__device__ __forceinline__ void merge_partials(const Partial* p, int n_slices, Stats* st,
+                                               int* cnt) {
+    Stats a{-__builtin_inff(), 0.0f, 0.0f};
+    int c = 0;
+    for (int s0 = 0; s0 < n_slices; s0 += kMergeBatch) {
+        Partial q[kMergeBatch];
+#pragma unroll
+        for (int u = 0; u < kMergeBatch; ++u)
+            q[u] = p[(s0 + u < n_slices) ? s0 + u : n_slices - 1];
+#pragma unroll
+        for (int u = 0; u < kMergeBatch; ++u) {
+            if (s0 + u < n_slices) {
+                a = (s0 + u == 0) ? Stats{q[u].m, q[u].s, q[u].t2}
+                                  : merge(a, Stats{q[u].m, q[u].s, q[u].t2});
+                c += q[u].cnt;
+            }
+        }
     }
+    *st = a;
+    *cnt = c;
+}
+
+// Row statistics of one item from its merged partials: the entropy score
+// and the rank of the judged token; bits em | ent<<1 | topk<<2.
+__device__ __forceinline__ uint8_t item_bits(const Stats& a, int cnt, int tok, int vocab,
+                                             const GateParams& gp, float* score, int* rank) {
     const float e_nats = __logf(a.s) - (kLn2 * a.t2) / a.s;
     *score = e_nats * gp.ent_scale;
     const bool valid = tok >= 0 && tok < vocab;
@@ -382,14 +424,19 @@ __global__ __launch_bounds__(kFinThreads) void verify_finalize_kernel(
         for (int r = threadIdx.x; r < ncc * max_len; r += kFinThreads) {
             const int cl = r / max_len, jj = r - cl * max_len;
             const int c = g * group_size + cc0 + cl;
-            int len = draft_len ? draft_len[c] : max_len;
-            len = len < 0 ? 0 : (len > max_len ? max_len : len);
             const int64_t row = (int64_t)c * max_len + jj;
+            // Every load of the row first (the partials of a position past
+            // the draft were not written and are not used).
+            int len = draft_len ? draft_len[c] : max_len;
+            const int tok = drafts[row];
+            Stats st;
+            int cnt;
+            merge_partials(partial + row * n_slices, n_slices, &st, &cnt);
+            len = len < 0 ? 0 : (len > max_len ? max_len : len);
             uint8_t bits = 0;
             float score = 0.0f;
             int rank = vocab;
-            if (jj < len) bits = item_bits(partial + row * n_slices, n_slices, drafts[row], vocab,
-                                           gp, &score, &rank);
+            if (jj < len) bits = item_bits(st, cnt, tok, vocab, gp, &score, &rank);
             if (out_gate_score) out_gate_score[row] = score;
             if (out_rank) out_rank[row] = rank;
             s_bits[r] = bits;
@@ -439,13 +486,18 @@ __global__ __launch_bounds__(kFinThreads) void verify_finalize_tree_kernel(
     const int L = tree_len[g] < nodes ? tree_len[g] : nodes;
     for (int u = threadIdx.x; u < L; u += kFinThreads) {
         const int item = g * nodes + u;
+        // Every load of the node first (the partials of a node that is not
+        // judged were not written and are not used).
+        const int tok = tree_tokens[item];
+        Stats st;
+        int cnt;
+        merge_partials(partial + (int64_t)item * n_slices, n_slices, &st, &cnt);
         int64_t row;
         uint8_t bits = 0;
         float score = 0.0f;
         int rank = vocab;
         if (tree_item(item, nodes, tree_parent, tree_len, &row))
-            bits = 8 | item_bits(partial + (int64_t)item * n_slices, n_slices, tree_tokens[item],
-                                 vocab, gp, &score, &rank);
+            bits = 8 | item_bits(st, cnt, tok, vocab, gp, &score, &rank);
         s_bits[u] = bits;
         s_score[u] = score;
         s_rank[u] = rank;
@@ -457,8 +509,15 @@ __global__ __launch_bounds__(kFinThreads) void verify_finalize_tree_kernel(
         uint64_t em = 0, ent = 0, tkm = 0;
         int len = 0;
         bool run = true;
+        int gb[kGammaBatch];
         for (int jj = 0; jj < max_len; ++jj) {
-            const int u = gamma[(int64_t)c * max_len + jj];
+            // Gamma of the next kGammaBatch positions, requested together.
+            if (jj % kGammaBatch == 0) {
+#pragma unroll
+                for (int t = 0; t < kGammaBatch; ++t)
+                    gb[t] = gamma[(int64_t)c * max_len + ((jj + t < max_len) ? jj + t : max_len - 1)];
+            }
+            const int u = gb[jj % kGammaBatch];
             const bool judged = run && u >= 0 && u < L && (s_bits[u] & 8);
             run = judged;
             const uint8_t b = judged ? s_bits[u] : 0;
