@@ -87,15 +87,14 @@ __device__ ChunkStats chunk_stats(const uint64_t (&key)[kPer], uint32_t* s_nzw, 
 //
 // Digits of up to 8 bits from the highest bit where the real keys differ; a
 // pass stops the search as soon as the digit holding the need-th key is
-// taken whole.  Each wave counts into its own 256-bin LDS histogram.  Scores
-// cluster in a few digit values and LDS atomics of one instruction to one
-// address serialise, so each wave first adds all lanes sharing its first
-// active lane's digit with one atomic (ballot + popcount) and only the other
-// lanes add one by one.
+// taken whole.  Each wave counts into its own 256-bin LDS histogram with
+// plain LDS atomics (starting below the shared bits spreads the keys over
+// the digit values, so same-address collisions inside an instruction stay
+// few).
 __device__ SelectState radix_select(const uint64_t (&key)[kPer], int need, const ChunkStats& cs,
                                     uint32_t* s_hist, uint32_t* s_tot, uint32_t* s_info) {
     const int tid = threadIdx.x;
-    const int lane = tid & 63, wv = tid >> 6;
+    const int wv = tid >> 6;
     uint32_t* my = s_hist + wv * 256;
     const uint64_t diff = cs.all_and ^ cs.any_or;
     if (diff == 0) return SelectState{cs.all_and, ~0ull};   // every real key is the same
@@ -112,14 +111,7 @@ __device__ SelectState radix_select(const uint64_t (&key)[kPer], int need, const
         for (int e = 0; e < kPer; ++e) {
             const bool act = (key[e] & mask) == prefix;
             const uint32_t dg = (uint32_t)(key[e] >> lo) & dmask;
-            const uint64_t am = __ballot(act);
-            if (am) {
-                const int first = __ffsll((unsigned long long)am) - 1;
-                const uint32_t d0 = (uint32_t)__builtin_amdgcn_readlane((int)dg, first);
-                const uint64_t same = __ballot(act && dg == d0);
-                if (lane == first) atomicAdd(&my[d0], (uint32_t)__popcll(same));
-                if (act && dg != d0) atomicAdd(&my[dg], 1u);
-            }
+            if (act) atomicAdd(&my[dg], 1u);
         }
         __syncthreads();
         // Totals; the per-wave histograms are cleared for the next pass.
