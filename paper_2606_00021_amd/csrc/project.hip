@@ -11,9 +11,10 @@
 //     basis split into hi + lo halves of the key type), giving
 //     S[o][i] = x_i . w_o; then project_finish subtracts mean . w_o,
 //     normalises each row and stores it transposed in the output type;
-//   * a few rows (queries) or fp32 / unaligned rows: one block per (row,
-//     output) computes the centred dot product with a fixed-order sum, then
-//     one wave per row normalises and stores it.
+//   * a few rows (queries) or fp32 / unaligned rows: blocks of 2 rows x 16
+//     outputs centre their rows in LDS and form the dot products (one wave
+//     per output, fixed-order sums); then one wave per row normalises and
+//     stores it.
 #include "internal.h"
 
 namespace sense {
@@ -81,13 +82,17 @@ __global__ __launch_bounds__(kProjThreads) void project_finish_kernel(
     }
 }
 
-// Direct route, step 1: raw[i][o] = (x_i - mean) . w_o, one block of 256
-// threads per (row, output).  A thread's elements come in batches of 16
-// loads issued together (clamped indices, no branch around a load, so none
-// waits for the one before it), then a fixed-order block sum: element t goes
-// to partial (t / 256) % 4 of its thread.
-constexpr int kDotThreads = 256;
-constexpr int kDotBatch = 16;
+// Direct route, step 1: raw[i][o] = (x_i - mean) . w_o by tiles of kTileRows
+// rows x kTileOuts outputs, one block of 1024 threads (one wave per output)
+// per tile, so that the basis is read by many CUs at once while each block
+// reads its rows once.  The centred rows go to LDS (each thread's loads
+// issued together, on clamped indices); each wave then streams its basis row
+// (16-byte loads when the basis is 16-byte aligned, else one float per lane)
+// against them in batches of loads issued together, and a fixed-order
+// butterfly sums the lanes.
+constexpr int kTileThreads = 1024;
+constexpr int kTileOuts = kTileThreads / 64;
+constexpr int kTileRows = 2;
 
 template <int XT>
 __device__ __forceinline__ float load_xt(const void* p, int64_t i) {
@@ -97,40 +102,90 @@ __device__ __forceinline__ float load_xt(const void* p, int64_t i) {
     return __builtin_bit_cast(float, (uint32_t)b << 16);
 }
 
-template <int XT>
-__global__ __launch_bounds__(kDotThreads) void project_dots_kernel(
-    const void* __restrict__ x, int64_t x_stride, int d_in, const float* __restrict__ mean,
-    const float* __restrict__ basis, int d_out, float* __restrict__ raw) {
-    __shared__ float s_part[kDotThreads / 64];
-    const int o = blockIdx.y;
-    const int64_t i = blockIdx.x;
-    const float* w = basis + (int64_t)o * d_in;
-    const float* m = mean ? mean : w;             // a valid address; unused without a mean
-    float a[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-    for (int t0 = 0; t0 < d_in; t0 += kDotBatch * kDotThreads) {
-        float xv[kDotBatch], wv[kDotBatch], mv[kDotBatch];
+template <int XT, bool VEC>
+__global__ __launch_bounds__(kTileThreads) void project_tile_kernel(
+    const void* __restrict__ x, int64_t x_stride, int64_t n, int d_in,
+    const float* __restrict__ mean, const float* __restrict__ basis, int d_out,
+    float* __restrict__ raw) {
+    __shared__ __attribute__((aligned(16))) float s_c[kTileRows][kMaxDim];
+    const int64_t i0 = (int64_t)blockIdx.x * kTileRows;
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+
+    constexpr int kA = kMaxDim / kTileThreads;
+    const float* m = mean ? mean : basis;          // a valid address; unused without a mean
 #pragma unroll
-        for (int u = 0; u < kDotBatch; ++u) {
-            const int t = t0 + u * kDotThreads + (int)threadIdx.x;
+    for (int r = 0; r < kTileRows; ++r) {
+        const int64_t i = (i0 + r < n) ? i0 + r : n - 1;
+        float xv[kA], mv[kA];
+#pragma unroll
+        for (int e = 0; e < kA; ++e) {
+            const int t = tid + e * kTileThreads;
             const int tc = t < d_in ? t : d_in - 1;
-            xv[u] = load_xt<XT>(x, i * x_stride + tc);
-            wv[u] = w[tc];
-            mv[u] = m[tc];
+            xv[e] = load_xt<XT>(x, i * x_stride + tc);
+            mv[e] = m[tc];
         }
 #pragma unroll
-        for (int u = 0; u < kDotBatch; ++u) {
-            const int t = t0 + u * kDotThreads + (int)threadIdx.x;
-            if (t < d_in) {
-                const float c = xv[u] - (mean ? mv[u] : 0.0f);
-                const int k = (t / kDotThreads) & 3;
-                a[k] = __builtin_fmaf(c, wv[u], a[k]);
+        for (int e = 0; e < kA; ++e) {
+            const int t = tid + e * kTileThreads;
+            if (t < d_in) s_c[r][t] = xv[e] - (mean ? mv[e] : 0.0f);
+        }
+    }
+    __syncthreads();
+
+    const int o = blockIdx.y * kTileOuts + wv;
+    if (o >= d_out) return;                          // uniform over the wave
+    const float* w = basis + (int64_t)o * d_in;
+    float a[kTileRows];
+#pragma unroll
+    for (int r = 0; r < kTileRows; ++r) a[r] = 0.0f;
+    if constexpr (VEC) {
+        constexpr int kB = 16;                      // 16-byte loads per batch
+        for (int j0 = 0; 256 * j0 < d_in; j0 += kB) {
+            float4 wq[kB];
+#pragma unroll
+            for (int u = 0; u < kB; ++u) {
+                const int t = 4 * lane + 256 * (j0 + u);
+                wq[u] = *(const float4*)(w + (t < d_in ? t : 0));
+            }
+#pragma unroll
+            for (int u = 0; u < kB; ++u) {
+                const int t = 4 * lane + 256 * (j0 + u);
+                if (t < d_in) {
+#pragma unroll
+                    for (int r = 0; r < kTileRows; ++r) {
+                        const float4 c = *(const float4*)(&s_c[r][t]);
+                        a[r] = __builtin_fmaf(c.x, wq[u].x, a[r]);
+                        a[r] = __builtin_fmaf(c.y, wq[u].y, a[r]);
+                        a[r] = __builtin_fmaf(c.z, wq[u].z, a[r]);
+                        a[r] = __builtin_fmaf(c.w, wq[u].w, a[r]);
+                    }
+                }
+            }
+        }
+    } else {
+        constexpr int kB = 32;                      // scalar loads per batch
+        for (int j0 = 0; 64 * j0 < d_in; j0 += kB) {
+            float wq[kB];
+#pragma unroll
+            for (int u = 0; u < kB; ++u) {
+                const int t = lane + 64 * (j0 + u);
+                wq[u] = w[t < d_in ? t : 0];
+            }
+#pragma unroll
+            for (int u = 0; u < kB; ++u) {
+                const int t = lane + 64 * (j0 + u);
+                if (t < d_in) {
+#pragma unroll
+                    for (int r = 0; r < kTileRows; ++r) a[r] = __builtin_fmaf(s_c[r][t], wq[u], a[r]);
+                }
             }
         }
     }
-    const float v = wsum((a[0] + a[1]) + (a[2] + a[3]));
-    if ((threadIdx.x & 63) == 0) s_part[threadIdx.x >> 6] = v;
-    __syncthreads();
-    if (threadIdx.x == 0) raw[i * d_out + o] = (s_part[0] + s_part[1]) + (s_part[2] + s_part[3]);
+#pragma unroll
+    for (int r = 0; r < kTileRows; ++r) {
+        const float v = wsum(a[r]);
+        if (lane == 0 && i0 + r < n) raw[(i0 + r) * d_out + o] = v;
+    }
 }
 
 // Direct route, step 2: normalise row i and store it in the output type.
@@ -140,14 +195,39 @@ __global__ __launch_bounds__(64) void project_norm_kernel(
     const int64_t i = blockIdx.x;
     const int lane = threadIdx.x;
     const float* r = raw + i * d_out;
+    float v[kMaxProjOut / 64];
+#pragma unroll
+    for (int e = 0; e < kMaxProjOut / 64; ++e) {
+        const int o = lane + 64 * e;
+        v[e] = r[o < d_out ? o : 0];
+    }
     float inv = 1.0f;
     if (normalize) {
         float ss = 0.0f;
-        for (int o = lane; o < d_out; o += 64) ss = __builtin_fmaf(r[o], r[o], ss);
+#pragma unroll
+        for (int e = 0; e < kMaxProjOut / 64; ++e)
+            if (lane + 64 * e < d_out) ss = __builtin_fmaf(v[e], v[e], ss);
         ss = wsum(ss);
         inv = (ss > 0.0f) ? 1.0f / __builtin_sqrtf(ss) : 0.0f;
     }
-    for (int o = lane; o < d_out; o += 64) store_out(out, out_dtype, i * out_stride + o, r[o] * inv);
+#pragma unroll
+    for (int e = 0; e < kMaxProjOut / 64; ++e) {
+        const int o = lane + 64 * e;
+        if (o < d_out) store_out(out, out_dtype, i * out_stride + o, v[e] * inv);
+    }
+}
+
+template <int XT>
+void launch_tiles(const void* x, int64_t n, int d_in, int64_t x_stride, const float* mean,
+                  const float* basis, int d_out, float* raw, hipStream_t stream) {
+    const dim3 grid((unsigned)((n + kTileRows - 1) / kTileRows),
+                    (unsigned)((d_out + kTileOuts - 1) / kTileOuts));
+    if (((uintptr_t)basis % 16) == 0)
+        hipLaunchKernelGGL((project_tile_kernel<XT, true>), grid, dim3(kTileThreads), 0, stream,
+                           x, x_stride, n, d_in, mean, basis, d_out, raw);
+    else
+        hipLaunchKernelGGL((project_tile_kernel<XT, false>), grid, dim3(kTileThreads), 0, stream,
+                           x, x_stride, n, d_in, mean, basis, d_out, raw);
 }
 
 }  // namespace
@@ -179,16 +259,12 @@ hipError_t launch_project(const void* x, int x_dtype, int64_t n, int d_in, int64
     void* scratch = ws + c_bytes + up256((size_t)d_out * n * sizeof(float));
     hipError_t e;
     if (!project_uses_mfma(x_dtype, x, x_stride, n)) {
-        const dim3 grid((unsigned)n, (unsigned)d_out);
         if (x_dtype == DT_F32)
-            hipLaunchKernelGGL(project_dots_kernel<DT_F32>, grid, dim3(kDotThreads), 0, stream, x,
-                               x_stride, d_in, mean, basis, d_out, s);
+            launch_tiles<DT_F32>(x, n, d_in, x_stride, mean, basis, d_out, s, stream);
         else if (x_dtype == DT_F16)
-            hipLaunchKernelGGL(project_dots_kernel<DT_F16>, grid, dim3(kDotThreads), 0, stream, x,
-                               x_stride, d_in, mean, basis, d_out, s);
+            launch_tiles<DT_F16>(x, n, d_in, x_stride, mean, basis, d_out, s, stream);
         else
-            hipLaunchKernelGGL(project_dots_kernel<DT_BF16>, grid, dim3(kDotThreads), 0, stream, x,
-                               x_stride, d_in, mean, basis, d_out, s);
+            launch_tiles<DT_BF16>(x, n, d_in, x_stride, mean, basis, d_out, s, stream);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         hipLaunchKernelGGL(project_norm_kernel, dim3((unsigned)n), dim3(64), 0, stream, s, d_out,
                            normalize, out, out_dtype, out_stride);
