@@ -364,8 +364,8 @@ hipError_t launch_group(const void* keys, int64_t n, int d, int64_t ld, const ui
     switch ((nq + 15) / 16) {
         case 1: return launch_tile<KT, 1, 4, 4, SPLIT>(keys, n, d, ld, qhi, qlo, inv_qn, nq, inv_norm, scores, stream);
         case 2: return launch_tile<KT, 2, 4, 3, SPLIT>(keys, n, d, ld, qhi, qlo, inv_qn, nq, inv_norm, scores, stream);
-        case 3: return launch_tile<KT, 3, 2, 4, SPLIT>(keys, n, d, ld, qhi, qlo, inv_qn, nq, inv_norm, scores, stream);
-        default: return launch_tile<KT, 4, 2, 4, SPLIT>(keys, n, d, ld, qhi, qlo, inv_qn, nq, inv_norm, scores, stream);
+        case 3: return launch_tile<KT, 3, 4, 3, SPLIT>(keys, n, d, ld, qhi, qlo, inv_qn, nq, inv_norm, scores, stream);
+        default: return launch_tile<KT, 4, 4, 3, SPLIT>(keys, n, d, ld, qhi, qlo, inv_qn, nq, inv_norm, scores, stream);
     }
 }
 
