@@ -129,10 +129,18 @@ def cpu_baseline(w, ds, q, logits, drafts, budget_s: float):
     t_verify_pos = (time.perf_counter() - t0) / (c_s * drafts.shape[1])
     pos_per_query = w.n_cand * w.span / w.n_queries
     t_query = t_scan_row * w.n + t_sort + t_verify_pos * pos_per_query
+    cpu_model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu_model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")),
+                             None)
+    except OSError:
+        pass
     return {
         "value": 1.0 / t_query,
         "unit": "queries/s",
         "cores": cores,
+        "cpu_model": cpu_model,
         "kind": "oracle",
         "sample": (f"fp64 oracle on host: scan of {rows} of {w.n} rows x d={ds.keys.shape[1]} "
                    f"({t_scan_row * 1e6:.3f} us/row), full sort of {w.n} scores "
