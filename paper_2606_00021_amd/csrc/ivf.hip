@@ -261,20 +261,34 @@ __global__ __launch_bounds__(kIvfThreads) void ivf_coarse_kernel(
 // probe order), and padding keys from the total up to cap.
 __global__ __launch_bounds__(kIvfThreads) void ivf_offsets_kernel(
     const int64_t* __restrict__ probe, int nprobe, const int64_t* __restrict__ offsets,
-    int32_t* __restrict__ base, int64_t cap, uint64_t* __restrict__ cand) {
-    __shared__ int32_t s_total;
+    int32_t* __restrict__ base, int32_t* __restrict__ count) {
+    // Probe p's candidates start at the sum of the sizes of probes 0 .. p-1;
+    // the query's candidate count is the sum of all of them.  Sizes are
+    // read in parallel, then wave 0 scans them 64 at a time.
+    __shared__ int32_t s_size[kMaxK];
     const int q = blockIdx.x;
-    if (threadIdx.x == 0) {
-        int32_t run = 0;
-        for (int p = 0; p < nprobe; ++p) {
-            const int64_t l = probe[(int64_t)q * nprobe + p];
-            base[(int64_t)q * nprobe + p] = run;
-            run += (int32_t)(offsets[l + 1] - offsets[l]);
-        }
-        s_total = run;
+    for (int p = threadIdx.x; p < nprobe; p += kIvfThreads) {
+        const int64_t l = probe[(int64_t)q * nprobe + p];
+        s_size[p] = (int32_t)(offsets[l + 1] - offsets[l]);
     }
     __syncthreads();
-    for (int64_t e = s_total + threadIdx.x; e < cap; e += kIvfThreads) cand[(int64_t)q * cap + e] = 0;
+    if (threadIdx.x < 64) {
+        const int lane = threadIdx.x;
+        int32_t carry = 0;
+        for (int p0 = 0; p0 < nprobe; p0 += 64) {
+            const int p = p0 + lane;
+            const int32_t v = p < nprobe ? s_size[p] : 0;
+            int32_t incl = v;
+#pragma unroll
+            for (int off = 1; off < 64; off <<= 1) {
+                const int32_t t = __shfl_up(incl, off, 64);
+                if (lane >= off) incl += t;
+            }
+            if (p < nprobe) base[(int64_t)q * nprobe + p] = carry + incl - v;
+            carry += __shfl(incl, 63, 64);
+        }
+        if (lane == 0) count[q] = carry;
+    }
 }
 
 // LUT[q][j][c] = sum_t u[j*dsub + t] * C[j][c][t].
@@ -475,7 +489,7 @@ hipError_t launch_ivf_search(const IvfSearch& s, hipStream_t stream) {
         hipSuccess)
         return e;
     hipLaunchKernelGGL(ivf_offsets_kernel, dim3((unsigned)s.nq), dim3(kIvfThreads), 0, stream,
-                       s.probe, s.nprobe, s.offsets, s.base, s.cap, s.cand);
+                       s.probe, s.nprobe, s.offsets, s.base, s.count);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const dim3 grid((unsigned)s.nprobe, (unsigned)s.nq);
     if (s.codes_sorted) {
@@ -498,7 +512,7 @@ hipError_t launch_ivf_search(const IvfSearch& s, hipStream_t stream) {
     if ((e = hipGetLastError()) != hipSuccess) return e;
     return launch_topk_keys(s.cand, s.cap, s.nq, s.k, s.spans, s.span_len, s.max_span,
                             s.span_stride, s.out_ids, s.out_scores, s.out_drafts,
-                            s.out_draft_len, s.final_ws, stream);
+                            s.out_draft_len, s.final_ws, stream, s.count);
 }
 
 }  // namespace sense

@@ -1023,8 +1023,8 @@ SENSE_EXPORT sense_status_t sense_build_ivf_index(const sense_ivf_desc_t* desc, 
 namespace {
 
 struct IvfLayout {
-    size_t q_off, coarse_off, ip_off, probe_off, pws_off, base_off, lut_off, cand_off, fws_off,
-        total;
+    size_t q_off, coarse_off, ip_off, probe_off, pws_off, base_off, cnt_off, lut_off, cand_off,
+        fws_off, total;
     int64_t cap;
 };
 
@@ -1045,6 +1045,7 @@ IvfLayout ivf_layout(const sense_index* ix, int nq, int k, int nprobe) {
     l.probe_off = take((size_t)nq * nprobe * sizeof(int64_t));
     l.pws_off = take(sense::topk_workspace_bytes(ix->nlist, nq, nprobe));
     l.base_off = take((size_t)nq * nprobe * sizeof(int32_t));
+    l.cnt_off = take((size_t)nq * sizeof(int32_t));
     l.lut_off = take(ix->pq_m ? (size_t)nq * ix->pq_m * ix->pq_ksub * sizeof(float) : 0);
     l.cand_off = take((size_t)nq * cap * sizeof(uint64_t));
     l.fws_off = take(sense::topk_workspace_bytes(cap, nq, k));
@@ -1120,6 +1121,7 @@ SENSE_EXPORT sense_status_t sense_ivf_search(const sense_index_t* ix, const void
     S.nprobe = nprobe;
     S.offsets = ix->offsets;
     S.base = (int32_t*)(ws + L.base_off);
+    S.count = (int32_t*)(ws + L.cnt_off);
     S.cap = L.cap;
     S.cand = (uint64_t*)(ws + L.cand_off);
     S.codes_sorted = ix->codes_sorted;

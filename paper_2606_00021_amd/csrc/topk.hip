@@ -46,6 +46,7 @@ struct ChunkStats {
     uint64_t all_and, any_or;
 };
 
+template <int T>
 __device__ ChunkStats chunk_stats(const uint64_t (&key)[kPer], uint32_t* s_nzw, uint64_t* s_andw,
                                   uint64_t* s_orw) {
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
@@ -72,7 +73,7 @@ __device__ ChunkStats chunk_stats(const uint64_t (&key)[kPer], uint32_t* s_nzw, 
     __syncthreads();
     ChunkStats r{0u, ~0ull, 0ull};
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
+    for (int w = 0; w < T / 64; ++w) {
         r.nz += s_nzw[w];
         r.all_and &= s_andw[w];
         r.any_or |= s_orw[w];
@@ -91,6 +92,7 @@ __device__ ChunkStats chunk_stats(const uint64_t (&key)[kPer], uint32_t* s_nzw, 
 // plain LDS atomics (starting below the shared bits spreads the keys over
 // the digit values, so same-address collisions inside an instruction stay
 // few).
+template <int T>
 __device__ SelectState radix_select(const uint64_t (&key)[kPer], int need, const ChunkStats& cs,
                                     uint32_t* s_hist, uint32_t* s_tot, uint32_t* s_info) {
     const int tid = threadIdx.x;
@@ -102,7 +104,7 @@ __device__ SelectState radix_select(const uint64_t (&key)[kPer], int need, const
     // Bits above hb are common to every real key (2 << 63 wraps to 0: no bits).
     uint64_t mask = ~((2ull << hb) - 1ull);
     uint64_t prefix = cs.all_and & mask;
-    for (int b = tid; b < kWaves * 256; b += kThreads) s_hist[b] = 0;
+    for (int b = tid; b < (T / 64) * 256; b += T) s_hist[b] = 0;
     __syncthreads();
     for (int hi = hb; hi >= 0; hi -= 8) {
         const int lo = hi >= 7 ? hi - 7 : 0;
@@ -115,10 +117,10 @@ __device__ SelectState radix_select(const uint64_t (&key)[kPer], int need, const
         }
         __syncthreads();
         // Totals; the per-wave histograms are cleared for the next pass.
-        for (int b = tid; b < 256; b += kThreads) {
+        for (int b = tid; b < 256; b += T) {
             uint32_t t = 0;
 #pragma unroll
-            for (int w = 0; w < kWaves; ++w) {
+            for (int w = 0; w < T / 64; ++w) {
                 t += s_hist[w * 256 + b];
                 s_hist[w * 256 + b] = 0;
             }
@@ -166,7 +168,7 @@ __device__ SelectState radix_select(const uint64_t (&key)[kPer], int need, const
 
 // Writes the block's taken keys to dst[0 .. min(taken, cap)) in some order,
 // positions from ballot prefix sums; returns the number taken (all threads).
-template <typename Taken>
+template <int T, typename Taken>
 __device__ uint32_t compact_taken(const uint64_t (&key)[kPer], Taken taken, uint64_t* dst,
                                   int cap, uint32_t* s_wc) {
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
@@ -177,7 +179,7 @@ __device__ uint32_t compact_taken(const uint64_t (&key)[kPer], Taken taken, uint
     __syncthreads();
     uint32_t base = 0, total = 0;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
+    for (int w = 0; w < T / 64; ++w) {
         const uint32_t c = s_wc[w];
         base += (w < wv) ? c : 0u;
         total += c;
@@ -192,6 +194,67 @@ __device__ uint32_t compact_taken(const uint64_t (&key)[kPer], Taken taken, uint
         base += (uint32_t)__popcll(m);
     }
     return total;
+}
+
+// The final level's output: the nt taken keys of s_sel (nt <= k) in order
+// by rank (k <= kRankMax: each key counts the keys above it, LDS broadcast
+// reads) or by a bitonic network, then ids, scores and the gathered
+// continuations of query q; padding keys give id -1.  All threads of the
+// block must call it.
+template <int T>
+__device__ void final_output(uint64_t* s_sel, uint64_t* s_sorted, int nt, int k, int q,
+                             int64_t* __restrict__ out_ids, float* __restrict__ out_scores,
+                             int32_t* __restrict__ out_drafts, int32_t* __restrict__ out_draft_len,
+                             const int32_t* __restrict__ spans, const int32_t* __restrict__ span_len,
+                             int max_span, int64_t span_stride) {
+    const int tid = threadIdx.x;
+    int p = 1;
+    while (p < nt) p <<= 1;
+    __syncthreads();
+    const uint64_t* sorted = s_sorted;
+    if (p <= kRankMax) {
+        // Rank of each taken key among the taken ones (ties, impossible
+        // for distinct (score, row) keys, by position): its place in the
+        // output.
+        for (int i = tid; i < nt; i += T) {
+            const uint64_t ki = s_sel[i];
+            int rank = 0;
+            for (int j = 0; j < nt; ++j) {
+                const uint64_t kj = s_sel[j];
+                rank += (kj > ki) | ((kj == ki) & (j < i));
+            }
+            s_sorted[rank] = ki;
+        }
+        for (int r = nt + tid; r < k; r += T) s_sorted[r] = 0;
+    } else {
+        // padding keys up to the sort size and up to k (read as output)
+        for (int r = nt + tid; r < (p > k ? p : k); r += T) s_sel[r] = 0;
+        __syncthreads();
+        bitonic_desc<T>(s_sel, p);
+        sorted = s_sel;
+    }
+    __syncthreads();
+    for (int r = tid; r < k; r += T) {
+        const uint64_t key = sorted[r];
+        out_ids[(int64_t)q * k + r] = key == 0 ? -1 : (int64_t)key_row(key);
+        if (out_scores) out_scores[(int64_t)q * k + r] = key_score((uint32_t)(key >> 32));
+    }
+    if (out_drafts || out_draft_len) {
+        for (int t = tid; t < k * max_span; t += T) {
+            const int r = t / max_span, j = t - r * max_span;
+            const uint64_t key = sorted[r];
+            const int64_t id = (int64_t)key_row(key);
+            // A padding key (0) surfaces only when fewer than k
+            // candidates exist (an inverted-file search of short lists):
+            // id -1, score NaN, an empty draft.
+            int len_r = (key == 0) ? 0 : (span_len ? span_len[id] : max_span);
+            len_r = len_r < 0 ? 0 : (len_r > max_span ? max_span : len_r);
+            const int64_t o = ((int64_t)q * k + r);
+            if (out_drafts)
+                out_drafts[o * max_span + j] = (j < len_r) ? spans[id * span_stride + j] : -1;
+            if (out_draft_len && j == 0) out_draft_len[o] = len_r;
+        }
+    }
 }
 
 // One block per (chunk, query).  FROM_SCORES: input is the fp32 score matrix
@@ -259,73 +322,94 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
             key[e] = i < len ? in_keys[(int64_t)q * count + start + i] : 0;
         }
     }
-    const ChunkStats cs = chunk_stats(key, s_nzw, s_andw, s_orw);
+    const ChunkStats cs = chunk_stats<kThreads>(key, s_nzw, s_andw, s_orw);
 
     // Keys taken: every real one if there are no more than kk, else the kk
     // largest (then more than kk keys are real, as the radix select needs).
     SelectState st{0, 0};
     const bool all = cs.nz <= (uint32_t)kk;
-    if (!all) st = radix_select(key, kk, cs, s_hist, s_tot, s_info);
+    if (!all) st = radix_select<kThreads>(key, kk, cs, s_hist, s_tot, s_info);
     auto taken = [&](int e) {
         return all ? (key[e] != 0) : ((key[e] & st.mask) >= st.prefix);
     };
 
     if constexpr (!FINAL) {
         uint64_t* out = out_keys + ((int64_t)q * gridDim.x + blockIdx.x) * kk;
-        const uint32_t tot = compact_taken(key, taken, out, kk, s_wc);
+        const uint32_t tot = compact_taken<kThreads>(key, taken, out, kk, s_wc);
         const int nt = (int)tot < kk ? (int)tot : kk;
         for (int i = nt + tid; i < kk; i += kThreads) out[i] = 0;  // padding key
     } else {
-        const uint32_t tot = compact_taken(key, taken, s_sel, kk, s_wc);
+        const uint32_t tot = compact_taken<kThreads>(key, taken, s_sel, kk, s_wc);
         const int nt = (int)tot < kk ? (int)tot : kk;
-        int p = 1;
-        while (p < nt) p <<= 1;
-        __syncthreads();
-        const uint64_t* sorted = s_sorted;
-        if (p <= kRankMax) {
-            // Rank of each taken key among the taken ones (ties, impossible
-            // for distinct (score, row) keys, by position): its place in the
-            // output.
-            for (int i = tid; i < nt; i += kThreads) {
-                const uint64_t ki = s_sel[i];
-                int rank = 0;
-                for (int j = 0; j < nt; ++j) {
-                    const uint64_t kj = s_sel[j];
-                    rank += (kj > ki) | ((kj == ki) & (j < i));
-                }
-                s_sorted[rank] = ki;
-            }
-            for (int r = nt + tid; r < k; r += kThreads) s_sorted[r] = 0;
-        } else {
-            // padding keys up to the sort size and up to k (read as output)
-            for (int r = nt + tid; r < (p > k ? p : k); r += kThreads) s_sel[r] = 0;
-            __syncthreads();
-            bitonic_desc<kThreads>(s_sel, p);
-            sorted = s_sel;
-        }
-        __syncthreads();
-        for (int r = tid; r < k; r += kThreads) {
-            const uint64_t key = sorted[r];
-            out_ids[(int64_t)q * k + r] = key == 0 ? -1 : (int64_t)key_row(key);
-            if (out_scores) out_scores[(int64_t)q * k + r] = key_score((uint32_t)(key >> 32));
-        }
-        if (out_drafts || out_draft_len) {
-            for (int t = tid; t < k * max_span; t += kThreads) {
-                const int r = t / max_span, j = t - r * max_span;
-                const uint64_t key = sorted[r];
-                const int64_t id = (int64_t)key_row(key);
-                // A padding key (0) surfaces only when fewer than k
-                // candidates exist (an inverted-file search of short lists):
-                // id -1, score NaN, an empty draft.
-                int len_r = (key == 0) ? 0 : (span_len ? span_len[id] : max_span);
-                len_r = len_r < 0 ? 0 : (len_r > max_span ? max_span : len_r);
-                const int64_t o = ((int64_t)q * k + r);
-                if (out_drafts)
-                    out_drafts[o * max_span + j] = (j < len_r) ? spans[id * span_stride + j] : -1;
-                if (out_draft_len && j == 0) out_draft_len[o] = len_r;
-            }
-        }
+        final_output<kThreads>(s_sel, s_sorted, nt, k, q, out_ids, out_scores, out_drafts,
+                               out_draft_len, spans, span_len, max_span, span_stride);
     }
+}
+
+// One block per query over a key list whose length is a per-query count on
+// the device (candidate buffers: most of the capacity is unused): rounds of
+// kStreamKeys keys, each holding the running top k and the next new keys,
+// reduced to the top k by the same radix select; then the final output.  The
+// common case (the count fits one round) is one launch; any count is exact.
+constexpr int kStreamThreads = 1024;
+constexpr int kStreamKeys = kStreamThreads * kPer;
+
+__global__ __launch_bounds__(kStreamThreads) void select_stream_kernel(
+    const uint64_t* __restrict__ in_keys, int64_t count, int k,
+    const int32_t* __restrict__ dev_count, int64_t* __restrict__ out_ids,
+    float* __restrict__ out_scores, int32_t* __restrict__ out_drafts,
+    int32_t* __restrict__ out_draft_len, const int32_t* __restrict__ spans,
+    const int32_t* __restrict__ span_len, int max_span, int64_t span_stride) {
+    constexpr int W = kStreamThreads / 64;
+    __shared__ uint64_t s_sel[kMaxK];
+    __shared__ uint64_t s_sorted[kMaxK];
+    __shared__ uint32_t s_hist[W * 256];
+    __shared__ uint32_t s_tot[256];
+    __shared__ uint32_t s_info[4];
+    __shared__ uint32_t s_nzw[W], s_wc[W];
+    __shared__ uint64_t s_andw[W], s_orw[W];
+    const int tid = threadIdx.x;
+    const int q = blockIdx.x;
+    const int kk = k;                                  // k <= kMaxK < kStreamKeys
+    int64_t cnt_q = dev_count ? (int64_t)dev_count[q] : count;
+    cnt_q = cnt_q < 0 ? 0 : (cnt_q > count ? count : cnt_q);
+    const uint64_t* src = in_keys + (int64_t)q * count;
+    int nt = 0;                                        // running top keys in s_sel
+    int64_t pos = 0;
+    do {
+        const int64_t left = cnt_q - pos;
+        const int take = (int)((kStreamKeys - nt) < left ? (kStreamKeys - nt) : left);
+        // New keys on clamped positions (no branch around a load), the
+        // running ones from LDS.
+        uint64_t key[kPer];
+#pragma unroll
+        for (int e = 0; e < kPer; ++e) {
+            const int i = tid + e * kStreamThreads;
+            const int64_t j = pos + (i - nt);
+            const int64_t jc = j < 0 ? 0 : (j < count ? j : count - 1);
+            key[e] = src[jc];
+        }
+#pragma unroll
+        for (int e = 0; e < kPer; ++e) {
+            const int i = tid + e * kStreamThreads;
+            if (i < nt) key[e] = s_sel[i];
+            else if (i - nt >= take) key[e] = 0;
+        }
+        __syncthreads();                               // s_sel read before it is rewritten
+        const ChunkStats cs = chunk_stats<kStreamThreads>(key, s_nzw, s_andw, s_orw);
+        SelectState st{0, 0};
+        const bool all = cs.nz <= (uint32_t)kk;
+        if (!all) st = radix_select<kStreamThreads>(key, kk, cs, s_hist, s_tot, s_info);
+        auto taken = [&](int e) {
+            return all ? (key[e] != 0) : ((key[e] & st.mask) >= st.prefix);
+        };
+        const uint32_t tot = compact_taken<kStreamThreads>(key, taken, s_sel, kk, s_wc);
+        nt = (int)tot < kk ? (int)tot : kk;
+        pos += take;
+        __syncthreads();                               // s_sel complete for the next round
+    } while (pos < cnt_q);
+    final_output<kStreamThreads>(s_sel, s_sorted, nt, k, q, out_ids, out_scores, out_drafts,
+                                 out_draft_len, spans, span_len, max_span, span_stride);
 }
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -401,6 +485,13 @@ hipError_t launch_topk_keys(const uint64_t* keys, int64_t count, int nq, int k,
     // key buffers).
     int32_t* cnt_buf[2] = {(int32_t*)((char*)workspace + 2 * one),
                            (int32_t*)((char*)workspace + 2 * one + ((size_t)nq * 4 + 255) / 256 * 256)};
+    if (dev_count) {
+        // One block per query walks its own count.
+        hipLaunchKernelGGL(select_stream_kernel, dim3(nq), dim3(kStreamThreads), 0, stream, keys,
+                           count, k, dev_count, out_ids, out_scores, out_drafts, out_draft_len,
+                           spans, span_len, max_span, span_stride);
+        return hipGetLastError();
+    }
     const int32_t* counts = dev_count;
     int cc = 0;
     while (chunks > 1) {
