@@ -215,16 +215,24 @@ __device__ void final_output(uint64_t* s_sel, uint64_t* s_sorted, int nt, int k,
     if (p <= kRankMax) {
         // Rank of each taken key among the taken ones (ties, impossible
         // for distinct (score, row) keys, by position): its place in the
-        // output.
-        for (int i = tid; i < nt; i += T) {
-            const uint64_t ki = s_sel[i];
-            int rank = 0;
-            for (int j = 0; j < nt; ++j) {
+        // output.  g = T / p threads share a key's count, each over every
+        // g-th key, and add their parts in LDS.
+        __shared__ int s_rank[kRankMax];
+        for (int i = tid; i < nt; i += T) s_rank[i] = 0;
+        __syncthreads();
+        const int g = T / p;
+        const int i = tid / g, part = tid - (tid / g) * g;
+        const uint64_t ki = i < nt ? s_sel[i] : 0ull;
+        if (i < nt) {
+            int c = 0;
+            for (int j = part; j < nt; j += g) {
                 const uint64_t kj = s_sel[j];
-                rank += (kj > ki) | ((kj == ki) & (j < i));
+                c += (kj > ki) | ((kj == ki) & (j < i));
             }
-            s_sorted[rank] = ki;
+            if (c) atomicAdd(&s_rank[i], c);
         }
+        __syncthreads();
+        if (i < nt && part == 0) s_sorted[s_rank[i]] = ki;
         for (int r = nt + tid; r < k; r += T) s_sorted[r] = 0;
     } else {
         // padding keys up to the sort size and up to k (read as output)
