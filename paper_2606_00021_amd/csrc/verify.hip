@@ -316,7 +316,7 @@ __global__ __launch_bounds__(kRowThreads) void verify_rows_kernel(
     }
 }
 
-constexpr int kFinThreads = 256;
+constexpr int kFinThreads = 512;
 constexpr int kFinChunkRows = 4096;   // (candidate, position) rows per LDS chunk
 constexpr int kGammaBatch = 16;       // tree finalize: Gamma entries loaded together
 
