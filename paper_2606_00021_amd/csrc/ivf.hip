@@ -291,13 +291,21 @@ __global__ __launch_bounds__(kIvfThreads) void ivf_offsets_kernel(
     }
 }
 
-// LUT[q][j][c] = sum_t u[j*dsub + t] * C[j][c][t].
+// LUT[q][j][c] = sum_t u[j*dsub + t] * C[j][c][t]: one block per (query,
+// subspace j), thread c one code (ksub <= kIvfThreads); the thread's
+// codebook entry is requested together with the query.
 __global__ __launch_bounds__(kIvfThreads) void ivf_lut_kernel(
     const float* __restrict__ queries, int d, int cosine, const float* __restrict__ codebooks,
     int m, int ksub, float* __restrict__ lut) {
     __shared__ float s_u[kMaxIvfDim];
     __shared__ float s_scale;
-    const int q = blockIdx.x;
+    const int q = blockIdx.x, j = blockIdx.y;
+    const int c = threadIdx.x;
+    const int dsub = d / m;
+    const float* cb = codebooks + ((int64_t)j * ksub + (c < ksub ? c : 0)) * dsub;
+    float cbv[kMaxDsub];
+#pragma unroll
+    for (int t = 0; t < kMaxDsub; ++t) cbv[t] = cb[t < dsub ? t : 0];
     const float* qv = queries + (int64_t)q * d;
     for (int t = threadIdx.x; t < d; t += kIvfThreads) s_u[t] = qv[t];
     __syncthreads();
@@ -308,13 +316,12 @@ __global__ __launch_bounds__(kIvfThreads) void ivf_lut_kernel(
         if (threadIdx.x == 0) s_scale = cosine ? ((a > 0.0f) ? 1.0f / __builtin_sqrtf(a) : 0.0f) : 1.0f;
     }
     __syncthreads();
-    const int dsub = d / m;
-    for (int e = threadIdx.x; e < m * ksub; e += kIvfThreads) {
-        const int j = e / ksub;
-        const float* cb = codebooks + (int64_t)e * dsub;
+    if (c < ksub) {
         float a = 0.0f;
-        for (int t = 0; t < dsub; ++t) a = __builtin_fmaf(s_u[j * dsub + t] * s_scale, cb[t], a);
-        lut[(int64_t)q * m * ksub + e] = a;
+#pragma unroll
+        for (int t = 0; t < kMaxDsub; ++t)
+            if (t < dsub) a = __builtin_fmaf(s_u[j * dsub + t] * s_scale, cbv[t], a);
+        lut[((int64_t)q * m + j) * ksub + c] = a;
     }
 }
 
@@ -493,7 +500,7 @@ hipError_t launch_ivf_search(const IvfSearch& s, hipStream_t stream) {
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const dim3 grid((unsigned)s.nprobe, (unsigned)s.nq);
     if (s.codes_sorted) {
-        hipLaunchKernelGGL(ivf_lut_kernel, dim3((unsigned)s.nq), dim3(kIvfThreads), 0, stream,
+        hipLaunchKernelGGL(ivf_lut_kernel, dim3((unsigned)s.nq, (unsigned)s.m), dim3(kIvfThreads), 0, stream,
                            s.queries, s.d, s.cosine, s.codebooks, s.m, s.ksub, s.lut);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         hipLaunchKernelGGL(ivf_scan_pq_kernel, grid, dim3(kIvfThreads),
