@@ -174,6 +174,27 @@ def test_ivf_flat_probing_everything_equals_exact_retrieval():
     flat.close()
 
 
+@pytest.mark.parametrize("k", [200, 1024])
+def test_ivf_flat_probing_everything_many_rounds(k):
+    """40000 candidates per query: the candidate selection walks them in
+    several rounds (running top k plus the next keys); the result must still
+    be the exact retrieval, order, scores and drafts."""
+    w, ds = store(40000, 32, "bf16", 13)
+    q, _ = synth.make_queries(w, ds, 13, n_queries=3)
+    cen, _ = synth.fit_ivf(ds.keys, 13, 64, iters=2)
+    lists = sense.sense_ivf_assign(ds.keys, cen, "cosine")
+    index = sense.sense_build_ivf_index(ds.keys, ds.spans, cen, lists)
+    ids, sc, dr, _ = sense.sense_ivf_search(index, q, k, 64)
+    flat = sense.sense_build_index(ds.keys, ds.spans)
+    e_ids, e_sc, e_dr, _ = sense.sense_retrieve(flat, q, k)
+    torch.cuda.synchronize()
+    assert torch.equal(ids, e_ids)
+    assert torch.allclose(sc, e_sc, rtol=1e-6, atol=0)
+    assert torch.equal(dr, e_dr)
+    index.close()
+    flat.close()
+
+
 def test_ivf_rejects_bad_list_ids():
     w, ds = store(1000, 64, "bf16", 2)
     cen, _ = synth.fit_ivf(ds.keys, 2, 16, iters=1)
