@@ -166,14 +166,12 @@ struct IvfSearch {
     void* probe_ws;
     int nprobe;
     const int64_t* offsets;    // nlist + 1
-    int32_t* base;             // nq x nprobe
     int32_t* count;            // nq: candidates of each query (sum of its probed list sizes)
     int64_t cap;               // candidate slots per query
     uint64_t* cand;            // nq x cap
     const uint8_t* codes_sorted;   // PQ, NULL for Flat
     int m, ksub;
     const float* codebooks;
-    float* lut;                // nq x m x ksub
     const void* keys_sorted;   // Flat
     int key_dtype;
     const float* inv_norm;     // Flat cosine, per sorted row

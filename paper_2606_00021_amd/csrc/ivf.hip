@@ -17,11 +17,12 @@
 //     inner product of the (normalised) query with each centroid;
 //   the probes = per-query top-nprobe of the coarse scores (the retrieval
 //     top-k kernels);
-//   ivf_offsets: per query, the exclusive prefix of the probed list sizes and
-//     the padding of the candidate buffer;
-//   ivf_lut (PQ): LUT[q][j][c] = u_j . C_j[c];
-//   ivf_scan_flat / ivf_scan_pq: one block per (probe, query) scores its
-//     list's rows and writes packed (score, original row) keys;
+//   ivf_scan_flat / ivf_scan_pq: blocks per query take its probes in turn;
+//     each block finds where its probes' candidates start (exclusive prefix
+//     of the probed list sizes in probe order; one block also stores the
+//     query's candidate count), the PQ blocks build the query's tables
+//     LUT[j][c] = u_j . C_j[c] in LDS, and each list's rows are scored into
+//     packed (score, original row) keys;
 //   the top-k kernels then select the k best keys per query and gather
 //     their continuations.
 #include "internal.h"
@@ -233,109 +234,153 @@ __global__ __launch_bounds__(kIvfThreads) void list_scatter_kernel(
 }
 
 // Coarse scores: score[q][l] = sim(q, c_l) for probing; ip[q][l] = u . c_l
-// with u = q (IP) or q / ||q|| (cosine), for the PQ scores.  One wave per
-// centroid, the query slice in registers (d <= 128).
+// with u = q (IP) or q / ||q|| (cosine), for the PQ scores.  One block per
+// tile of 64 centroids and 4 * kCoarseQ queries: the tile is staged in LDS
+// with coalesced loads (rows padded so that each lane's row read is free of
+// bank conflicts), each lane holds one centroid in registers, each wave
+// takes kCoarseQ queries, read from LDS as broadcasts (d <= KD).
+constexpr int kCoarseTile = 64;
+constexpr int kCoarseQ = 4;
+
+template <int KD>
 __global__ __launch_bounds__(kIvfThreads) void ivf_coarse_kernel(
-    const float* __restrict__ queries, int d, const float* __restrict__ centroids,
+    const float* __restrict__ queries, int d, int nq, const float* __restrict__ centroids,
     const float* __restrict__ cen_inv, int nlist, int cosine, float* __restrict__ score,
     float* __restrict__ ip) {
-    const int lane = threadIdx.x & 63;
-    const int q = blockIdx.y;
-    const int l = blockIdx.x * (kIvfThreads / 64) + (threadIdx.x >> 6);
-    const float* qv = queries + (int64_t)q * d;
-    const float q0 = lane < d ? qv[lane] : 0.0f, q1 = lane + 64 < d ? qv[lane + 64] : 0.0f;
-    const float qq = wsum(__builtin_fmaf(q0, q0, q1 * q1));
-    const float inv_q = (qq > 0.0f) ? 1.0f / __builtin_sqrtf(qq) : 0.0f;
-    if (l >= nlist) return;
-    const float* c = centroids + (int64_t)l * d;
-    const float c0 = lane < d ? c[lane] : 0.0f, c1 = lane + 64 < d ? c[lane + 64] : 0.0f;
-    const float dot = wsum(__builtin_fmaf(q0, c0, q1 * c1));
-    if (lane == 0) {
-        const int64_t o = (int64_t)q * nlist + l;
-        score[o] = cosine ? (dot * cen_inv[l]) * inv_q : dot;
-        if (ip) ip[o] = cosine ? dot * inv_q : dot;
+    constexpr int W = kIvfThreads / 64;
+    constexpr int RS = KD + 4;                       // padded row stride (floats)
+    __shared__ float4 s_c[kCoarseTile * RS / 4];
+    __shared__ float4 s_q[W * kCoarseQ * KD / 4];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int l0 = blockIdx.x * kCoarseTile;
+    const int nt = (nlist - l0 < kCoarseTile) ? nlist - l0 : kCoarseTile;
+    const int q0 = blockIdx.y * (W * kCoarseQ);
+    // Tile rows l0 .. l0+nt-1 are contiguous and d % 4 == 0: float4 e of the
+    // tile is centroid e / (KD/4), dims 4 (e % (KD/4)) ..; unused slots (rows
+    // >= nt, dims >= d) are 0.  Every load is issued before the first store.
+    constexpr int TL = kCoarseTile * KD / 4 / kIvfThreads;
+    constexpr int QL = W * kCoarseQ * KD / kIvfThreads;
+    float4 tv[TL];
+#pragma unroll
+    for (int i = 0; i < TL; ++i) {
+        const int e = tid + i * kIvfThreads;
+        const int r = e / (KD / 4), t = 4 * (e % (KD / 4));
+        const bool in = r < nt && t < d;
+        tv[i] = *(const float4*)(centroids + (int64_t)l0 * d + (in ? r * d + t : 0));
     }
-}
-
-// Per query: base[q][p] = sum of the sizes of probes 0..p-1 (probe lists in
-// probe order), and padding keys from the total up to cap.
-__global__ __launch_bounds__(kIvfThreads) void ivf_offsets_kernel(
-    const int64_t* __restrict__ probe, int nprobe, const int64_t* __restrict__ offsets,
-    int32_t* __restrict__ base, int32_t* __restrict__ count) {
-    // Probe p's candidates start at the sum of the sizes of probes 0 .. p-1;
-    // the query's candidate count is the sum of all of them.  Sizes are
-    // read in parallel, then wave 0 scans them 64 at a time.
-    __shared__ int32_t s_size[kMaxK];
-    const int q = blockIdx.x;
-    for (int p = threadIdx.x; p < nprobe; p += kIvfThreads) {
-        const int64_t l = probe[(int64_t)q * nprobe + p];
-        s_size[p] = (int32_t)(offsets[l + 1] - offsets[l]);
+    float qv[QL];
+#pragma unroll
+    for (int i = 0; i < QL; ++i) {
+        const int e = tid + i * kIvfThreads;
+        const int r = e / KD, t = e % KD;
+        const bool in = q0 + r < nq && t < d;
+        qv[i] = queries[in ? (int64_t)(q0 + r) * d + t : 0];
+    }
+#pragma unroll
+    for (int i = 0; i < TL; ++i) {
+        const int e = tid + i * kIvfThreads;
+        const int r = e / (KD / 4), t = 4 * (e % (KD / 4));
+        const bool in = r < nt && t < d;
+        s_c[r * (RS / 4) + t / 4] = in ? tv[i] : float4{0.0f, 0.0f, 0.0f, 0.0f};
+    }
+    float* sq = (float*)s_q;
+#pragma unroll
+    for (int i = 0; i < QL; ++i) {
+        const int e = tid + i * kIvfThreads;
+        const int r = e / KD, t = e % KD;
+        sq[r * KD + t] = (q0 + r < nq && t < d) ? qv[i] : 0.0f;
     }
     __syncthreads();
-    if (threadIdx.x < 64) {
-        const int lane = threadIdx.x;
-        int32_t carry = 0;
-        for (int p0 = 0; p0 < nprobe; p0 += 64) {
-            const int p = p0 + lane;
-            const int32_t v = p < nprobe ? s_size[p] : 0;
-            int32_t incl = v;
+    const int qw = q0 + wv * kCoarseQ;
+    if (qw >= nq) return;
+    float inv_q[kCoarseQ];
 #pragma unroll
-            for (int off = 1; off < 64; off <<= 1) {
-                const int32_t t = __shfl_up(incl, off, 64);
-                if (lane >= off) incl += t;
-            }
-            if (p < nprobe) base[(int64_t)q * nprobe + p] = carry + incl - v;
-            carry += __shfl(incl, 63, 64);
-        }
-        if (lane == 0) count[q] = carry;
-    }
-}
-
-// LUT[q][j][c] = sum_t u[j*dsub + t] * C[j][c][t]: one block per (query,
-// subspace j), thread c one code (ksub <= kIvfThreads); the thread's
-// codebook entry is requested together with the query.
-__global__ __launch_bounds__(kIvfThreads) void ivf_lut_kernel(
-    const float* __restrict__ queries, int d, int cosine, const float* __restrict__ codebooks,
-    int m, int ksub, float* __restrict__ lut) {
-    __shared__ float s_u[kMaxIvfDim];
-    __shared__ float s_scale;
-    const int q = blockIdx.x, j = blockIdx.y;
-    const int c = threadIdx.x;
-    const int dsub = d / m;
-    const float* cb = codebooks + ((int64_t)j * ksub + (c < ksub ? c : 0)) * dsub;
-    float cbv[kMaxDsub];
-#pragma unroll
-    for (int t = 0; t < kMaxDsub; ++t) cbv[t] = cb[t < dsub ? t : 0];
-    const float* qv = queries + (int64_t)q * d;
-    for (int t = threadIdx.x; t < d; t += kIvfThreads) s_u[t] = qv[t];
-    __syncthreads();
-    if (threadIdx.x < 64) {
-        float a = 0.0f;
-        for (int t = threadIdx.x; t < d; t += 64) a = __builtin_fmaf(s_u[t], s_u[t], a);
+    for (int i = 0; i < kCoarseQ; ++i) {
+        const float* qr = sq + (wv * kCoarseQ + i) * KD;
+        float a = qr[lane] * qr[lane];
+        if constexpr (KD > 64) a = __builtin_fmaf(qr[lane + 64], qr[lane + 64], a);
         a = wsum(a);
-        if (threadIdx.x == 0) s_scale = cosine ? ((a > 0.0f) ? 1.0f / __builtin_sqrtf(a) : 0.0f) : 1.0f;
+        inv_q[i] = (a > 0.0f) ? 1.0f / __builtin_sqrtf(a) : 0.0f;
     }
-    __syncthreads();
-    if (c < ksub) {
-        float a = 0.0f;
+    float4 cv[KD / 4];
 #pragma unroll
-        for (int t = 0; t < kMaxDsub; ++t)
-            if (t < dsub) a = __builtin_fmaf(s_u[j * dsub + t] * s_scale, cbv[t], a);
-        lut[((int64_t)q * m + j) * ksub + c] = a;
+    for (int t = 0; t < KD / 4; ++t) cv[t] = s_c[lane * (RS / 4) + t];
+    const int l = l0 + lane;
+    float ci = 1.0f;
+    if (cosine) ci = cen_inv[lane < nt ? l : l0];
+#pragma unroll
+    for (int i = 0; i < kCoarseQ; ++i) {
+        const float4* qr = s_q + (wv * kCoarseQ + i) * (KD / 4);
+        float a0 = 0.0f, a1 = 0.0f;
+#pragma unroll
+        for (int t = 0; t < KD / 4; ++t) {
+            const float4 u = qr[t];
+            a0 = __builtin_fmaf(cv[t].x, u.x, a0);
+            a1 = __builtin_fmaf(cv[t].y, u.y, a1);
+            a0 = __builtin_fmaf(cv[t].z, u.z, a0);
+            a1 = __builtin_fmaf(cv[t].w, u.w, a1);
+        }
+        const float dot = a0 + a1;
+        if (lane < nt && qw + i < nq) {
+            const int64_t o = (int64_t)(qw + i) * nlist + l;
+            score[o] = cosine ? (dot * ci) * inv_q[i] : dot;
+            if (ip) ip[o] = cosine ? dot * inv_q[i] : dot;
+        }
     }
 }
 
-// IVF-Flat list scan: one block per (probe, query); LPR lanes per row as in
-// the short-key scan (d <= 128, 16 bytes per lane).
+// Probe bases, per query: probe p's candidates start at the sum of the
+// sizes of probes 0 .. p-1 (probe order), and the query's candidate count is
+// the sum of all of them.  Every thread stores sizes into s_size and each
+// probed list's first row into s_r0 (before a barrier); after it, wave 0
+// writes the exclusive prefixes of the sizes into s_pre, 64 at a time, and
+// returns the total (the caller's next barrier publishes s_pre).  With ip
+// given, s_qc[p] = ip[list of probe p] (the PQ scores' coarse term).
+__device__ __forceinline__ void load_probe_sizes(const int64_t* __restrict__ pq, int nprobe,
+                                                 const int64_t* __restrict__ offsets,
+                                                 int32_t* s_size, int64_t* s_r0,
+                                                 const float* __restrict__ ip, float* s_qc) {
+    for (int p = threadIdx.x; p < nprobe; p += kIvfThreads) {
+        const int64_t l = pq[p];
+        const int64_t r0 = offsets[l], r1 = offsets[l + 1];
+        if (ip) s_qc[p] = ip[l];
+        s_size[p] = (int32_t)(r1 - r0);
+        s_r0[p] = r0;
+    }
+}
+
+__device__ __forceinline__ int32_t scan_probe_sizes(const int32_t* s_size, int32_t* s_pre,
+                                                    int nprobe) {
+    const int lane = threadIdx.x & 63;
+    int32_t carry = 0;
+    for (int p0 = 0; p0 < nprobe; p0 += 64) {
+        const int p = p0 + lane;
+        const int32_t v = p < nprobe ? s_size[p] : 0;
+        int32_t incl = v;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int32_t t = __shfl_up(incl, off, 64);
+            if (lane >= off) incl += t;
+        }
+        if (p < nprobe) s_pre[p] = carry + incl - v;
+        carry += __shfl(incl, 63, 64);
+    }
+    return carry;
+}
+
+// IVF-Flat list scan: block (p, q) scans probe p of query q; LPR lanes per
+// row as in the short-key scan (d <= 128, 16 bytes per lane).
 template <int KT>
 __global__ __launch_bounds__(kIvfThreads) void ivf_scan_flat_kernel(
     const uint16_t* __restrict__ keys_sorted, int d, const float* __restrict__ inv_norm,
     const int32_t* __restrict__ row_ids, const int64_t* __restrict__ offsets,
     const float* __restrict__ queries, const int64_t* __restrict__ probe, int nprobe,
-    const int32_t* __restrict__ base, int64_t cap, uint64_t* __restrict__ cand) {
-    const int p = blockIdx.x, q = blockIdx.y;
-    const int64_t l = probe[(int64_t)q * nprobe + p];
-    const int64_t r0 = offsets[l], r1 = offsets[l + 1];
+    int32_t* __restrict__ count, int64_t cap, uint64_t* __restrict__ cand) {
+    __shared__ int32_t s_size[kMaxK], s_pre[kMaxK];
+    __shared__ int64_t s_r0[kMaxK];
+    const int q = blockIdx.y;
+    const int64_t* pq = probe + (int64_t)q * nprobe;
     const int lanes = (d + 7) / 8;
     int lpr = 1;
     while (lpr < lanes) lpr <<= 1;
@@ -345,64 +390,203 @@ __global__ __launch_bounds__(kIvfThreads) void ivf_scan_flat_kernel(
     const bool col = e < d;
     const float* qv = queries + (int64_t)q * d;
     float qf[8];
-    float qq = 0.0f;
 #pragma unroll
     for (int t = 0; t < 8; ++t) {
-        qf[t] = col ? qv[e + t] : 0.0f;
-        qq = __builtin_fmaf(qf[t], qf[t], qq);
+        const float x = qv[col ? e + t : 0];
+        qf[t] = col ? x : 0.0f;
     }
+    load_probe_sizes(pq, nprobe, offsets, s_size, s_r0, nullptr, nullptr);
+    float qq = 0.0f;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) qq = __builtin_fmaf(qf[t], qf[t], qq);
     for (int off = 1; off < lpr; off <<= 1) qq += __shfl_xor(qq, off, 64);
     const float inv_q = (qq > 0.0f) ? 1.0f / __builtin_sqrtf(qq) : 0.0f;
-    uint64_t* out = cand + (int64_t)q * cap + base[(int64_t)q * nprobe + p] - r0;
-    for (int64_t r = r0 + (int64_t)wv * rpi + g; r - g < r1; r += (int64_t)(kIvfThreads / 64) * rpi) {
-        float a0 = 0.0f, a1 = 0.0f;
-        if (col && r < r1) {
-            const u32x4 v = __builtin_nontemporal_load((const u32x4*)(keys_sorted + r * d + e));
+    __syncthreads();
+    if (threadIdx.x < 64) {
+        const int32_t total = scan_probe_sizes(s_size, s_pre, nprobe);
+        if (blockIdx.x == 0 && threadIdx.x == 0) count[q] = total;
+    }
+    __syncthreads();
+    {
+        const int p = blockIdx.x;                   // one probe per block
+        const int64_t r0 = s_r0[p], r1 = r0 + s_size[p];
+        uint64_t* out = cand + (int64_t)q * cap + s_pre[p] - r0;
+        for (int64_t r = r0 + (int64_t)wv * rpi + g; r - g < r1;
+             r += (int64_t)(kIvfThreads / 64) * rpi) {
+            float a0 = 0.0f, a1 = 0.0f;
+            if (col && r < r1) {
+                const u32x4 v =
+                    __builtin_nontemporal_load((const u32x4*)(keys_sorted + r * d + e));
 #pragma unroll
-            for (int w = 0; w < 4; ++w) {
-                const uint32_t u = v[w];
-                float lo, hi;
-                if constexpr (KT == DT_BF16) {
-                    lo = __builtin_bit_cast(float, u << 16);
-                    hi = __builtin_bit_cast(float, u & 0xFFFF0000u);
-                } else {
-                    lo = (float)__builtin_bit_cast(_Float16, (uint16_t)(u & 0xFFFFu));
-                    hi = (float)__builtin_bit_cast(_Float16, (uint16_t)(u >> 16));
+                for (int w = 0; w < 4; ++w) {
+                    const uint32_t u = v[w];
+                    float lo, hi;
+                    if constexpr (KT == DT_BF16) {
+                        lo = __builtin_bit_cast(float, u << 16);
+                        hi = __builtin_bit_cast(float, u & 0xFFFF0000u);
+                    } else {
+                        lo = (float)__builtin_bit_cast(_Float16, (uint16_t)(u & 0xFFFFu));
+                        hi = (float)__builtin_bit_cast(_Float16, (uint16_t)(u >> 16));
+                    }
+                    a0 = __builtin_fmaf(lo, qf[2 * w], a0);
+                    a1 = __builtin_fmaf(hi, qf[2 * w + 1], a1);
                 }
-                a0 = __builtin_fmaf(lo, qf[2 * w], a0);
-                a1 = __builtin_fmaf(hi, qf[2 * w + 1], a1);
             }
-        }
-        float s = a0 + a1;
-        for (int off = 1; off < lpr; off <<= 1) s += __shfl_xor(s, off, 64);
-        if (c == 0 && r < r1) {
-            if (inv_norm) s = (s * inv_norm[r]) * inv_q;
-            out[r] = pack_key(s, (uint32_t)row_ids[r]);
+            float s = a0 + a1;
+            for (int off = 1; off < lpr; off <<= 1) s += __shfl_xor(s, off, 64);
+            if (c == 0 && r < r1) {
+                if (inv_norm) s = (s * inv_norm[r]) * inv_q;
+                out[r] = pack_key(s, (uint32_t)row_ids[r]);
+            }
         }
     }
 }
 
-// IVF-PQ list scan: one block per (probe, query); the query's tables in LDS,
-// one thread per row: score = u.c_l + sum_j LUT[j][code_j] (j in order).
+// IVF-PQ list scan: block (g, q) builds query q's tables in LDS,
+// LUT[j][c] = sum_t u[j*dsub + t] * C[j][c][t] (u = q, or q / ||q|| for
+// cosine; thread c one code, its d codebook values requested up front), then
+// scans probes g, g + G, ... of the query, one thread per row:
+// score = u.c_l + sum_j LUT[j][code_j] (j in order).  MV = 16-byte code
+// words per row (m = 16 MV): a thread's rows are pipelined, the next one
+// requested before the current one is scored, and its first row before the
+// barriers; MV = 0: byte loads, any m.
+template <int MV>
+struct PqCodes {
+    u32x4 w[MV > 0 ? MV : 1];
+    int32_t rid;
+};
+
+template <int MV>
+__device__ __forceinline__ PqCodes<MV> pq_load(const uint8_t* __restrict__ codes, int m,
+                                               const int32_t* __restrict__ row_ids, int64_t r) {
+    PqCodes<MV> c;
+#pragma unroll
+    for (int v = 0; v < MV; ++v) c.w[v] = ((const u32x4*)(codes + r * m))[v];
+    c.rid = row_ids[r];
+    return c;
+}
+
+template <int KD, int MV>
 __global__ __launch_bounds__(kIvfThreads) void ivf_scan_pq_kernel(
-    const uint8_t* __restrict__ codes_sorted, int m, int ksub, const float* __restrict__ lut,
-    const float* __restrict__ ip, int nlist, const int32_t* __restrict__ row_ids,
-    const int64_t* __restrict__ offsets, const int64_t* __restrict__ probe, int nprobe,
-    const int32_t* __restrict__ base, int64_t cap, uint64_t* __restrict__ cand) {
+    const uint8_t* __restrict__ codes_sorted, int m, int ksub, const float* __restrict__ queries,
+    int d, int cosine, const float* __restrict__ codebooks, const float* __restrict__ ip,
+    int nlist, const int32_t* __restrict__ row_ids, const int64_t* __restrict__ offsets,
+    const int64_t* __restrict__ probe, int nprobe, int32_t* __restrict__ count, int64_t cap,
+    uint64_t* __restrict__ cand) {
     extern __shared__ float s_lut[];   // m * ksub
-    const int p = blockIdx.x, q = blockIdx.y;
-    const float* lq = lut + (int64_t)q * m * ksub;
-    for (int e = threadIdx.x; e < m * ksub; e += kIvfThreads) s_lut[e] = lq[e];
+    __shared__ float s_u[KD];
+    __shared__ int32_t s_size[kMaxK], s_pre[kMaxK];
+    __shared__ int64_t s_r0[kMaxK];
+    __shared__ float s_qc[kMaxK];
+    __shared__ float s_part[kIvfThreads / 64];
+    const int q = blockIdx.y, tid = threadIdx.x, lane = tid & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int G = gridDim.x;
+    const int64_t* pq = probe + (int64_t)q * nprobe;
+    // First row of this thread: probe blockIdx.x, row f0 + tid (clamped to
+    // a real row; rows past the list end are never scored from it).
+    int p = blockIdx.x;
+    const int64_t lf = pq[p];
+    const int64_t f0 = offsets[lf], f1 = offsets[lf + 1];
+    int64_t r = f0 + tid, r1 = f1;
+    PqCodes<MV> cur{};
+    if constexpr (MV > 0) {
+        const int64_t rc = r < r1 ? r : (r1 > f0 ? r1 - 1 : 0);
+        cur = pq_load<MV>(codes_sorted, m, row_ids, rc);
+    }
+    const float uq = queries[(int64_t)q * d + (tid < d ? tid : 0)];
+    const int dsub = d / m;
+    const int cc = tid < ksub ? tid : 0;
+    float cbv[KD];
+    {
+        // element e = j * dsub + t of code cc lives at C[(j * ksub + cc) * dsub + t]
+        int j = 0, t = 0;
+#pragma unroll
+        for (int e = 0; e < KD; ++e) {
+            const int64_t at = ((int64_t)j * ksub + cc) * dsub + t;
+            cbv[e] = codebooks[e < d ? at : 0];
+            if (++t == dsub) {
+                t = 0;
+                ++j;
+            }
+        }
+    }
+    load_probe_sizes(pq, nprobe, offsets, s_size, s_r0, ip + (int64_t)q * nlist, s_qc);
+    if (tid < KD) s_u[tid] = tid < d ? uq : 0.0f;
+    const float sq = wsum(tid < d ? uq * uq : 0.0f);
+    if (lane == 0) s_part[wv] = sq;
     __syncthreads();
-    const int64_t l = probe[(int64_t)q * nprobe + p];
-    const int64_t r0 = offsets[l], r1 = offsets[l + 1];
-    const float qc = ip[(int64_t)q * nlist + l];
-    uint64_t* out = cand + (int64_t)q * cap + base[(int64_t)q * nprobe + p] - r0;
-    for (int64_t r = r0 + threadIdx.x; r < r1; r += kIvfThreads) {
-        const uint8_t* cr = codes_sorted + r * m;
-        float s = 0.0f;
-        for (int j = 0; j < m; ++j) s += s_lut[j * ksub + cr[j]];
-        out[r] = pack_key(qc + s, (uint32_t)row_ids[r]);
+    if (tid < 64) {
+        const int32_t total = scan_probe_sizes(s_size, s_pre, nprobe);
+        if (blockIdx.x == 0 && tid == 0) count[q] = total;
+    }
+    float qq = 0.0f;
+#pragma unroll
+    for (int w = 0; w < kIvfThreads / 64; ++w) qq += s_part[w];
+    const float scale = cosine ? ((qq > 0.0f) ? 1.0f / __builtin_sqrtf(qq) : 0.0f) : 1.0f;
+    if (tid < ksub) {
+        int j = 0, t = 0;
+        float a = 0.0f;
+#pragma unroll
+        for (int e = 0; e < KD; ++e) {
+            if (e < d) {
+                a = __builtin_fmaf(s_u[e] * scale, cbv[e], a);
+                if (++t == dsub) {
+                    s_lut[j * ksub + tid] = a;
+                    a = 0.0f;
+                    t = 0;
+                    ++j;
+                }
+            }
+        }
+    }
+    __syncthreads();
+    if constexpr (MV > 0) {
+        // Lanes past the end of their first list move on to their next probe.
+        bool moved = false;
+        while (p < nprobe && r >= r1) {
+            p += G;
+            if (p < nprobe) {
+                r = s_r0[p] + tid;
+                r1 = s_r0[p] + s_size[p];
+                moved = true;
+            }
+        }
+        if (moved && p < nprobe) cur = pq_load<MV>(codes_sorted, m, row_ids, r);
+        while (p < nprobe) {
+            int pn = p;
+            int64_t rn = r + kIvfThreads, r1n = r1;
+            while (pn < nprobe && rn >= r1n) {
+                pn += G;
+                if (pn < nprobe) {
+                    rn = s_r0[pn] + tid;
+                    r1n = s_r0[pn] + s_size[pn];
+                }
+            }
+            const PqCodes<MV> nxt = pq_load<MV>(codes_sorted, m, row_ids, pn < nprobe ? rn : r);
+            float sc = 0.0f;
+#pragma unroll
+            for (int j = 0; j < 16 * MV; ++j) {
+                const uint32_t code = (cur.w[j / 16][(j / 4) % 4] >> (8 * (j % 4))) & 0xFFu;
+                sc += s_lut[j * ksub + code];
+            }
+            cand[(int64_t)q * cap + s_pre[p] + (r - s_r0[p])] = pack_key(s_qc[p] + sc, (uint32_t)cur.rid);
+            p = pn;
+            r = rn;
+            r1 = r1n;
+            cur = nxt;
+        }
+    } else {
+        for (p = blockIdx.x; p < nprobe; p += G) {
+            const int64_t r0 = s_r0[p], re = r0 + s_size[p];
+            uint64_t* out = cand + (int64_t)q * cap + s_pre[p] - r0;
+            for (int64_t rr = r0 + tid; rr < re; rr += kIvfThreads) {
+                const uint8_t* cr = codes_sorted + rr * m;
+                float sc = 0.0f;
+                for (int j = 0; j < m; ++j) sc += s_lut[j * ksub + cr[j]];
+                out[rr] = pack_key(s_qc[p] + sc, (uint32_t)row_ids[rr]);
+            }
+        }
     }
 }
 
@@ -484,37 +668,57 @@ hipError_t launch_ivf_layout(const int32_t* list_ids, int64_t n, int nlist, cons
 
 hipError_t launch_ivf_search(const IvfSearch& s, hipStream_t stream) {
     hipError_t e;
-    hipLaunchKernelGGL(ivf_coarse_kernel,
-                       dim3((unsigned)((s.nlist + kIvfThreads / 64 - 1) / (kIvfThreads / 64)),
-                            (unsigned)s.nq),
-                       dim3(kIvfThreads), 0, stream, s.queries, s.d, s.centroids, s.cen_inv,
-                       s.nlist, s.cosine, s.coarse, s.codes_sorted ? s.coarse_ip : nullptr);
+    constexpr int qpb = (kIvfThreads / 64) * kCoarseQ;
+    const dim3 cgrid((unsigned)((s.nlist + kCoarseTile - 1) / kCoarseTile),
+                     (unsigned)((s.nq + qpb - 1) / qpb));
+    float* ip = s.codes_sorted ? s.coarse_ip : nullptr;
+    if (s.d <= 64)
+        hipLaunchKernelGGL(ivf_coarse_kernel<64>, cgrid, dim3(kIvfThreads), 0, stream, s.queries,
+                           s.d, s.nq, s.centroids, s.cen_inv, s.nlist, s.cosine, s.coarse, ip);
+    else
+        hipLaunchKernelGGL(ivf_coarse_kernel<128>, cgrid, dim3(kIvfThreads), 0, stream, s.queries,
+                           s.d, s.nq, s.centroids, s.cen_inv, s.nlist, s.cosine, s.coarse, ip);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     // Probes: top-nprobe lists per query (ids only).
     if ((e = launch_topk_gather(s.coarse, s.nlist, s.nq, s.nprobe, nullptr, nullptr, 1, 1,
                                 s.probe, nullptr, nullptr, nullptr, s.probe_ws, stream)) !=
         hipSuccess)
         return e;
-    hipLaunchKernelGGL(ivf_offsets_kernel, dim3((unsigned)s.nq), dim3(kIvfThreads), 0, stream,
-                       s.probe, s.nprobe, s.offsets, s.base, s.count);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    const dim3 grid((unsigned)s.nprobe, (unsigned)s.nq);
     if (s.codes_sorted) {
-        hipLaunchKernelGGL(ivf_lut_kernel, dim3((unsigned)s.nq, (unsigned)s.m), dim3(kIvfThreads), 0, stream,
-                           s.queries, s.d, s.cosine, s.codebooks, s.m, s.ksub, s.lut);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-        hipLaunchKernelGGL(ivf_scan_pq_kernel, grid, dim3(kIvfThreads),
-                           (size_t)s.m * s.ksub * sizeof(float), stream, s.codes_sorted, s.m,
-                           s.ksub, s.lut, s.coarse_ip, s.nlist, s.row_ids, s.offsets, s.probe,
-                           s.nprobe, s.base, s.cap, s.cand);
-    } else if (s.key_dtype == DT_BF16) {
-        hipLaunchKernelGGL(ivf_scan_flat_kernel<DT_BF16>, grid, dim3(kIvfThreads), 0, stream,
-                           (const uint16_t*)s.keys_sorted, s.d, s.inv_norm, s.row_ids, s.offsets,
-                           s.queries, s.probe, s.nprobe, s.base, s.cap, s.cand);
+        // Each block builds the query's tables once, so with many queries a
+        // block takes several probes (about two blocks per compute unit).
+        int g = (2 * cus() + s.nq - 1) / s.nq;
+        g = g < 1 ? 1 : (g > s.nprobe ? s.nprobe : g);
+        const dim3 grid((unsigned)g, (unsigned)s.nq);
+        const size_t lds = (size_t)s.m * s.ksub * sizeof(float);
+        const int mv = (s.m % 16 == 0 && s.m <= 64) ? s.m / 16 : 0;
+#define SENSE_PQ_SCAN(KD, MV)                                                                   \
+    hipLaunchKernelGGL((ivf_scan_pq_kernel<KD, MV>), grid, dim3(kIvfThreads), lds, stream,       \
+                       s.codes_sorted, s.m, s.ksub, s.queries, s.d, s.cosine, s.codebooks,      \
+                       s.coarse_ip, s.nlist, s.row_ids, s.offsets, s.probe, s.nprobe, s.count, \
+                       s.cap, s.cand)
+        if (s.d <= 64) {
+            if (mv == 1) SENSE_PQ_SCAN(64, 1);
+            else if (mv == 2) SENSE_PQ_SCAN(64, 2);
+            else if (mv == 4) SENSE_PQ_SCAN(64, 4);
+            else SENSE_PQ_SCAN(64, 0);
+        } else {
+            if (mv == 1) SENSE_PQ_SCAN(128, 1);
+            else if (mv == 2) SENSE_PQ_SCAN(128, 2);
+            else if (mv == 4) SENSE_PQ_SCAN(128, 4);
+            else SENSE_PQ_SCAN(128, 0);
+        }
+#undef SENSE_PQ_SCAN
     } else {
-        hipLaunchKernelGGL(ivf_scan_flat_kernel<DT_F16>, grid, dim3(kIvfThreads), 0, stream,
-                           (const uint16_t*)s.keys_sorted, s.d, s.inv_norm, s.row_ids, s.offsets,
-                           s.queries, s.probe, s.nprobe, s.base, s.cap, s.cand);
+        const dim3 grid((unsigned)s.nprobe, (unsigned)s.nq);
+        if (s.key_dtype == DT_BF16)
+            hipLaunchKernelGGL(ivf_scan_flat_kernel<DT_BF16>, grid, dim3(kIvfThreads), 0, stream,
+                               (const uint16_t*)s.keys_sorted, s.d, s.inv_norm, s.row_ids,
+                               s.offsets, s.queries, s.probe, s.nprobe, s.count, s.cap, s.cand);
+        else
+            hipLaunchKernelGGL(ivf_scan_flat_kernel<DT_F16>, grid, dim3(kIvfThreads), 0, stream,
+                               (const uint16_t*)s.keys_sorted, s.d, s.inv_norm, s.row_ids,
+                               s.offsets, s.queries, s.probe, s.nprobe, s.count, s.cap, s.cand);
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
     return launch_topk_keys(s.cand, s.cap, s.nq, s.k, s.spans, s.span_len, s.max_span,

@@ -1023,8 +1023,7 @@ SENSE_EXPORT sense_status_t sense_build_ivf_index(const sense_ivf_desc_t* desc, 
 namespace {
 
 struct IvfLayout {
-    size_t q_off, coarse_off, ip_off, probe_off, pws_off, base_off, cnt_off, lut_off, cand_off,
-        fws_off, total;
+    size_t q_off, coarse_off, ip_off, probe_off, pws_off, cnt_off, cand_off, fws_off, total;
     int64_t cap;
 };
 
@@ -1044,9 +1043,7 @@ IvfLayout ivf_layout(const sense_index* ix, int nq, int k, int nprobe) {
     l.ip_off = take(ix->pq_m ? (size_t)nq * ix->nlist * sizeof(float) : 0);
     l.probe_off = take((size_t)nq * nprobe * sizeof(int64_t));
     l.pws_off = take(sense::topk_workspace_bytes(ix->nlist, nq, nprobe));
-    l.base_off = take((size_t)nq * nprobe * sizeof(int32_t));
     l.cnt_off = take((size_t)nq * sizeof(int32_t));
-    l.lut_off = take(ix->pq_m ? (size_t)nq * ix->pq_m * ix->pq_ksub * sizeof(float) : 0);
     l.cand_off = take((size_t)nq * cap * sizeof(uint64_t));
     l.fws_off = take(sense::topk_workspace_bytes(cap, nq, k));
     l.total = at;
@@ -1120,7 +1117,6 @@ SENSE_EXPORT sense_status_t sense_ivf_search(const sense_index_t* ix, const void
     S.probe_ws = ws + L.pws_off;
     S.nprobe = nprobe;
     S.offsets = ix->offsets;
-    S.base = (int32_t*)(ws + L.base_off);
     S.count = (int32_t*)(ws + L.cnt_off);
     S.cap = L.cap;
     S.cand = (uint64_t*)(ws + L.cand_off);
@@ -1128,7 +1124,6 @@ SENSE_EXPORT sense_status_t sense_ivf_search(const sense_index_t* ix, const void
     S.m = ix->pq_m;
     S.ksub = ix->pq_ksub;
     S.codebooks = ix->codebooks;
-    S.lut = ix->pq_m ? (float*)(ws + L.lut_off) : nullptr;
     S.keys_sorted = ix->owned_keys;
     S.key_dtype = ix->key_dtype;
     S.inv_norm = ix->inv_norm;

@@ -102,6 +102,12 @@ IVF_CASES = [
     (12000, 32, "f16", 64, 8, 16, 4, "ip", (8, 64)),
     (5000, 128, "bf16", 50, 50, 20, 1, "cosine", None),      # nprobe = nlist
     (4000, 64, "bf16", 400, 2, 100, 2, "cosine", None),       # fewer candidates than k
+    # enough queries that a PQ scan block takes several probes of its query
+    # (16, 32 and 64 codes per row in 16-byte words; 8 codes, byte loads)
+    (30000, 64, "bf16", 256, 32, 64, 40, "cosine", (16, 256)),
+    (20000, 128, "bf16", 128, 64, 32, 24, "ip", (32, 128)),
+    (12000, 64, "f16", 64, 48, 16, 16, "ip", (64, 256)),
+    (12000, 32, "f16", 64, 40, 16, 20, "cosine", (8, 64)),
 ]
 
 
