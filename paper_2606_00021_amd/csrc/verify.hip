@@ -5,16 +5,18 @@
 // row; everything else is per-row scalars.  Two kernels:
 //
 // verify_rows: one block of 256 threads per (row, vocabulary slice).  A
-//   slice is what the block can hold in registers: every thread issues all
-//   of its sixteen 16-byte loads at once (deep memory-level parallelism, no
-//   dependent chain), then
+//   slice is what the block holds in registers: every thread issues all of
+//   its eight 16-byte loads at once (no dependent chain; small blocks keep
+//   the register count low, so many blocks share a compute unit and one's
+//   arithmetic hides another's loads), then
 //     phase 1: m = max of the slice (wave max, then the four waves);
 //     phase 2: with t = (x - m) log2 e,
 //       S   = sum 2^t                 (= sum e^(x-m)),
 //       T2  = sum 2^t * t             (= log2 e * sum e^(x-m)(x-m)),
 //       cnt = #{v : x_v > x_d} + #{v < d : x_v = x_d},  x_d the draft token's
 //             logit, counted as x_v >= x_d left of d and x_v >= next(x_d)
-//             from d on (one compare per element).
+//             from d on (one compare per element; in a full slice a wave
+//             ballot per element, counted on the scalar unit).
 //   and stores one 16-byte partial (m, S, T2, cnt) per (row, slice).  With
 //   p = softmax(x), E = -sum p ln p = ln S - ln2 * T2 / S.  The draft token
 //   is the first argmax exactly when cnt = 0 and is in the top-k set exactly
@@ -34,7 +36,8 @@ namespace sense {
 namespace {
 
 constexpr int kRowThreads = 256;
-constexpr int kNV = 16;            // 16-byte vectors per thread per slice
+constexpr int kRowWaves = kRowThreads / 64;
+constexpr int kNV = 8;             // 16-byte vectors per thread per slice
 constexpr int kScalarPer = 32;     // elements per thread per slice, unaligned rows
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
@@ -144,18 +147,38 @@ __device__ __forceinline__ float next_up(float x) {
     return __builtin_bit_cast(float, x > 0.0f ? u + 1u : u - 1u);
 }
 
+// Maximum and fixed-order pairwise sums over the block's per-wave values.
+__device__ __forceinline__ float waves_max(const float* s) {
+    float m = s[0];
+#pragma unroll
+    for (int w = 1; w < kRowWaves; ++w) m = __builtin_fmaxf(m, s[w]);
+    return m;
+}
+template <int N, typename T, typename Get>
+__device__ __forceinline__ T pair_sum(Get get, int off) {
+    if constexpr (N == 1) {
+        return get(off);
+    } else {
+        return pair_sum<N / 2, T>(get, off) + pair_sum<N / 2, T>(get, off + N / 2);
+    }
+}
+
 struct Acc {
     float s = 0.0f, t2 = 0.0f;
-    int cnt = 0;
+    int cnt = 0;        // per lane
+    uint32_t wcnt = 0;  // per wave (already summed over its lanes)
 };
 
 // One element of phase 2.  The clamp keeps a -inf logit at weight 0 and
 // contribution 0 (instead of 0 * -inf).
-__device__ __forceinline__ void absorb(Acc& a, float x, float nm, float thr) {
+__device__ __forceinline__ void absorb_sum(Acc& a, float x, float nm) {
     const float t = __builtin_fmaxf(__builtin_fmaf(x, kLog2e, nm), -256.0f);
     const float e = fast_exp2(t);
     a.s += e;
     a.t2 = __builtin_fmaf(e, t, a.t2);
+}
+__device__ __forceinline__ void absorb(Acc& a, float x, float nm, float thr) {
+    absorb_sum(a, x, nm);
     a.cnt += (x >= thr) ? 1 : 0;
 }
 
@@ -205,7 +228,7 @@ __global__ __launch_bounds__(kRowThreads) void verify_rows_kernel(
     const int v1 = (v0 + slice_len < vocab) ? v0 + slice_len : vocab;
     Acc acc;
     float mx = -__builtin_inff();
-    __shared__ float s_max[kRowThreads / 64];
+    __shared__ float s_max[kRowWaves];
 
     if constexpr (VEC) {
         const int nvec = (v1 - v0) / VW;
@@ -237,22 +260,42 @@ __global__ __launch_bounds__(kRowThreads) void verify_rows_kernel(
         const float wm = wave_max_f(mx);
         if ((tid & 63) == 0) s_max[tid >> 6] = wm;
         __syncthreads();
-        const float m = __builtin_fmaxf(__builtin_fmaxf(s_max[0], s_max[1]),
-                                        __builtin_fmaxf(s_max[2], s_max[3]));
+        const float m = waves_max(s_max);
         mx = m;
         {
             // An all -inf slice keeps weight 0 (t clamps) but still counts ties.
             const float nm = (m == -__builtin_inff()) ? 0.0f : -m * kLog2e;
+            if (nvec >= kNV * kRowThreads) {
+                // A full slice (every one but a row's last): no lane is
+                // idle, so the rank count is a wave ballot per element,
+                // counted on the scalar unit (one vector compare each).
+                uint32_t wc = 0;
 #pragma unroll
-            for (int k = 0; k < kNV; ++k) {
-                const int i = tid + k * kRowThreads;
-                if (i < nvec) {
+                for (int k = 0; k < kNV; ++k) {
+                    const int i = tid + k * kRowThreads;
                     float x[VW];
                     unpack<LT>(buf[k], x);
                     const int vb = v0 + i * VW;
                     const float thr = (vb + VW <= tk) ? thr_lo : thr_hi;
 #pragma unroll
-                    for (int u = 0; u < VW; ++u) absorb(acc, x[u], nm, thr);
+                    for (int u = 0; u < VW; ++u) {
+                        absorb_sum(acc, x[u], nm);
+                        wc += (uint32_t)__popcll(__ballot(x[u] >= thr));
+                    }
+                }
+                acc.wcnt = wc;
+            } else {
+#pragma unroll
+                for (int k = 0; k < kNV; ++k) {
+                    const int i = tid + k * kRowThreads;
+                    if (i < nvec) {
+                        float x[VW];
+                        unpack<LT>(buf[k], x);
+                        const int vb = v0 + i * VW;
+                        const float thr = (vb + VW <= tk) ? thr_lo : thr_hi;
+#pragma unroll
+                        for (int u = 0; u < VW; ++u) absorb(acc, x[u], nm, thr);
+                    }
                 }
             }
             if (has_t) absorb(acc, xt, nm, vt < tk ? thr_lo : thr_hi);
@@ -289,8 +332,7 @@ __global__ __launch_bounds__(kRowThreads) void verify_rows_kernel(
         const float wm = wave_max_f(mx);
         if ((tid & 63) == 0) s_max[tid >> 6] = wm;
         __syncthreads();
-        const float m = __builtin_fmaxf(__builtin_fmaxf(s_max[0], s_max[1]),
-                                        __builtin_fmaxf(s_max[2], s_max[3]));
+        const float m = waves_max(s_max);
         mx = m;
         {
             const float nm = (m == -__builtin_inff()) ? 0.0f : -m * kLog2e;
@@ -304,14 +346,14 @@ __global__ __launch_bounds__(kRowThreads) void verify_rows_kernel(
 
     // Block sums in a fixed order.
     const float ws = wave_sum_f(acc.s), wt = wave_sum_f(acc.t2);
-    const int wc = wave_sum_i(acc.cnt);
-    __shared__ Partial s_w[kRowThreads / 64];
+    const int wc = wave_sum_i(acc.cnt) + (int)acc.wcnt;
+    __shared__ Partial s_w[kRowWaves];
     if ((tid & 63) == 0) s_w[tid >> 6] = Partial{mx, ws, wt, wc};
     __syncthreads();
     if (tid == 0) {
-        Partial p{mx, (s_w[0].s + s_w[1].s) + (s_w[2].s + s_w[3].s),
-                  (s_w[0].t2 + s_w[1].t2) + (s_w[2].t2 + s_w[3].t2),
-                  (s_w[0].cnt + s_w[1].cnt) + (s_w[2].cnt + s_w[3].cnt)};
+        Partial p{mx, pair_sum<kRowWaves, float>([&](int w) { return s_w[w].s; }, 0),
+                  pair_sum<kRowWaves, float>([&](int w) { return s_w[w].t2; }, 0),
+                  pair_sum<kRowWaves, int>([&](int w) { return s_w[w].cnt; }, 0)};
         partial[(int64_t)item * n_slices + slice] = p;
     }
 }
