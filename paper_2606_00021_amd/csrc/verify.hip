@@ -239,14 +239,16 @@ __global__ __launch_bounds__(kRowThreads) void verify_rows_kernel(
             const int i = tid + k * kRowThreads;
             buf[k] = (i < nvec) ? __builtin_nontemporal_load(vp + i) : u32x4{0u, 0u, 0u, 0u};
         }
-        // Fewer than VW trailing elements (last slice only).
+        // Fewer than VW trailing elements (last slice only), and the judged
+        // token's logit: both requested unconditionally (clamped to a real
+        // element) together with the slice, so that no load waits for
+        // another.
         const int vt = v0 + nvec * VW + tid;
         const bool has_t = vt < v1;
-        const float xt = has_t ? load_one<LT>(rowp, vt) : -__builtin_inff();
-        // The judged token's logit, requested after the slice (it is first
-        // needed in phase 2).
-        const float xd = valid ? load_one<LT>(rowp, tok) : 0.0f;
-        const float thr_lo = xd, thr_hi = next_up(xd);   // left of d / from d on
+        const float xt_raw = load_one<LT>(rowp, has_t ? vt : v0);
+        const float xd_raw = load_one<LT>(rowp, valid ? tok : v0);
+        __builtin_amdgcn_sched_barrier(0);
+        const float xt = has_t ? xt_raw : -__builtin_inff();
 #pragma unroll
         for (int k = 0; k < kNV; ++k) {
             if (tid + k * kRowThreads < nvec) {
@@ -262,6 +264,11 @@ __global__ __launch_bounds__(kRowThreads) void verify_rows_kernel(
         __syncthreads();
         const float m = waves_max(s_max);
         mx = m;
+        // The thresholds of the rank count (left of d / from d on), formed
+        // only here, so that the judged logit's load is not waited for
+        // before phase 1.
+        const float xd = valid ? xd_raw : 0.0f;
+        const float thr_lo = xd, thr_hi = next_up(xd);
         {
             // An all -inf slice keeps weight 0 (t clamps) but still counts ties.
             const float nm = (m == -__builtin_inff()) ? 0.0f : -m * kLog2e;
@@ -301,12 +308,16 @@ __global__ __launch_bounds__(kRowThreads) void verify_rows_kernel(
             if (has_t) absorb(acc, xt, nm, vt < tk ? thr_lo : thr_hi);
             // The vector holding d was counted with x > x_d throughout; its
             // elements left of d equal to x_d also rank above d.  Only the
-            // thread that loaded it adds them, from a second (cached) read,
-            // so no other element pays for the test.
+            // thread that holds it adds them (its registers, picked by
+            // selects), so no other element pays for the test.
             const int id = (tk - v0) / VW;
             if (tk > v0 && id < nvec && id % kRowThreads == tid && tk - (v0 + id * VW) > 0) {
+                const int kd = id / kRowThreads;
+                u32x4 w = buf[0];
+#pragma unroll
+                for (int k = 1; k < kNV; ++k) w = (k == kd) ? buf[k] : w;
                 float x[VW];
-                unpack<LT>(vp[id], x);
+                unpack<LT>(w, x);
                 const int nl = tk - (v0 + id * VW);
 #pragma unroll
                 for (int u = 0; u < VW; ++u) acc.cnt += (u < nl && x[u] == xd) ? 1 : 0;
@@ -321,19 +332,21 @@ __global__ __launch_bounds__(kRowThreads) void verify_rows_kernel(
             const int v = v0 + tid + k * kRowThreads;
             x[k] = load_one<LT>(rowp, v < v1 ? v : v0);
         }
+        const float xd_raw = load_one<LT>(rowp, valid ? tok : v0);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int k = 0; k < kScalarPer; ++k) {
             const int v = v0 + tid + k * kRowThreads;
             if (v >= v1) x[k] = -__builtin_inff();
             mx = __builtin_fmaxf(mx, x[k]);
         }
-        const float xd = valid ? load_one<LT>(rowp, tok) : 0.0f;
-        const float thr_lo = xd, thr_hi = next_up(xd);   // left of d / from d on
         const float wm = wave_max_f(mx);
         if ((tid & 63) == 0) s_max[tid >> 6] = wm;
         __syncthreads();
         const float m = waves_max(s_max);
         mx = m;
+        const float xd = valid ? xd_raw : 0.0f;
+        const float thr_lo = xd, thr_hi = next_up(xd);   // left of d / from d on
         {
             const float nm = (m == -__builtin_inff()) ? 0.0f : -m * kLog2e;
 #pragma unroll
