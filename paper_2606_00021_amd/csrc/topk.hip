@@ -46,14 +46,14 @@ struct ChunkStats {
     uint64_t all_and, any_or;
 };
 
-template <int T>
-__device__ ChunkStats chunk_stats(const uint64_t (&key)[kPer], uint32_t* s_nzw, uint64_t* s_andw,
+template <int T, int P>
+__device__ ChunkStats chunk_stats(const uint64_t (&key)[P], uint32_t* s_nzw, uint64_t* s_andw,
                                   uint64_t* s_orw) {
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
     uint32_t nz = 0;
     uint64_t a = ~0ull, o = 0ull;
 #pragma unroll
-    for (int e = 0; e < kPer; ++e) {
+    for (int e = 0; e < P; ++e) {
         nz += (uint32_t)__popcll(__ballot(key[e] != 0));
         if (key[e] != 0) {
             a &= key[e];
@@ -81,7 +81,7 @@ __device__ ChunkStats chunk_stats(const uint64_t (&key)[kPer], uint32_t* s_nzw, 
     return r;
 }
 
-// Finds prefix/mask such that exactly `need` of the block's keys (kPer per
+// Finds prefix/mask such that exactly `need` of the block's keys (P per
 // thread, held in registers; unused slots hold the padding key 0) satisfy
 // (key & mask) >= prefix.  Requires 1 <= need < cs.nz (the number of real
 // keys).  All threads of the block must call it.
@@ -92,8 +92,8 @@ __device__ ChunkStats chunk_stats(const uint64_t (&key)[kPer], uint32_t* s_nzw, 
 // plain LDS atomics (starting below the shared bits spreads the keys over
 // the digit values, so same-address collisions inside an instruction stay
 // few).
-template <int T>
-__device__ SelectState radix_select(const uint64_t (&key)[kPer], int need, const ChunkStats& cs,
+template <int T, int P>
+__device__ SelectState radix_select(const uint64_t (&key)[P], int need, const ChunkStats& cs,
                                     uint32_t* s_hist, uint32_t* s_tot, uint32_t* s_info) {
     const int tid = threadIdx.x;
     const int wv = tid >> 6;
@@ -110,7 +110,7 @@ __device__ SelectState radix_select(const uint64_t (&key)[kPer], int need, const
         const int lo = hi >= 7 ? hi - 7 : 0;
         const uint32_t dmask = (1u << (hi - lo + 1)) - 1u;
 #pragma unroll
-        for (int e = 0; e < kPer; ++e) {
+        for (int e = 0; e < P; ++e) {
             const bool act = (key[e] & mask) == prefix;
             const uint32_t dg = (uint32_t)(key[e] >> lo) & dmask;
             if (act) atomicAdd(&my[dg], 1u);
@@ -168,13 +168,13 @@ __device__ SelectState radix_select(const uint64_t (&key)[kPer], int need, const
 
 // Writes the block's taken keys to dst[0 .. min(taken, cap)) in some order,
 // positions from ballot prefix sums; returns the number taken (all threads).
-template <int T, typename Taken>
-__device__ uint32_t compact_taken(const uint64_t (&key)[kPer], Taken taken, uint64_t* dst,
+template <int T, int P, typename Taken>
+__device__ uint32_t compact_taken(const uint64_t (&key)[P], Taken taken, uint64_t* dst,
                                   int cap, uint32_t* s_wc) {
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
     uint32_t mine = 0;
 #pragma unroll
-    for (int e = 0; e < kPer; ++e) mine += (uint32_t)__popcll(__ballot(taken(e)));
+    for (int e = 0; e < P; ++e) mine += (uint32_t)__popcll(__ballot(taken(e)));
     if (lane == 0) s_wc[wv] = mine;
     __syncthreads();
     uint32_t base = 0, total = 0;
@@ -186,7 +186,7 @@ __device__ uint32_t compact_taken(const uint64_t (&key)[kPer], Taken taken, uint
     }
     const uint64_t below = (1ull << lane) - 1ull;
 #pragma unroll
-    for (int e = 0; e < kPer; ++e) {
+    for (int e = 0; e < P; ++e) {
         const bool t = taken(e);
         const uint64_t m = __ballot(t);
         const uint32_t pos = base + (uint32_t)__popcll(m & below);
@@ -268,7 +268,9 @@ __device__ void final_output(uint64_t* s_sel, uint64_t* s_sorted, int nt, int k,
 // One block per (chunk, query).  FROM_SCORES: input is the fp32 score matrix
 // (nq x count, row index = position); otherwise packed keys (nq x count).
 // FINAL: exactly one chunk per query; writes sorted ids/scores and drafts.
-template <bool FROM_SCORES, bool FINAL>
+// P keys per thread: chunks of kThreads * P keys (kSelectChunk for P = 16;
+// a smaller P serves a single chunk of fewer keys with less work).
+template <bool FROM_SCORES, bool FINAL, int P>
 __global__ __launch_bounds__(kThreads) void select_kernel(
     const float* __restrict__ scores, const uint64_t* __restrict__ in_keys, int64_t count,
     int k, uint64_t* __restrict__ out_keys, int64_t* __restrict__ out_ids,
@@ -284,9 +286,10 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
     __shared__ uint32_t s_nzw[kWaves], s_wc[kWaves];
     __shared__ uint64_t s_andw[kWaves], s_orw[kWaves];
 
+    constexpr int CH = kThreads * P;
     const int tid = threadIdx.x;
     const int q = blockIdx.y;
-    const int64_t start = (int64_t)blockIdx.x * kSelectChunk;
+    const int64_t start = (int64_t)blockIdx.x * CH;
     // dev_count: a per-query count on the device (at most count).
     const int64_t cnt_q = (dev_count && dev_count[q] < count) ? dev_count[q] : count;
     const int64_t remain = cnt_q - start;
@@ -294,60 +297,60 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
         // With device counts the next level reads only the chunks that hold
         // keys: their number is published, and empty chunks write nothing.
         if (dev_count) {
-            const int kk0 = k < kSelectChunk ? k : kSelectChunk;
+            const int kk0 = k < CH ? k : CH;
             if (blockIdx.x == 0 && threadIdx.x == 0)
-                next_count[q] = (int32_t)(((cnt_q + kSelectChunk - 1) / kSelectChunk) * kk0);
+                next_count[q] = (int32_t)(((cnt_q + CH - 1) / CH) * kk0);
             if (remain <= 0) return;                 // uniform over the block
         }
     }
-    const int len = (int)(remain < kSelectChunk ? remain : kSelectChunk);
-    const int kk = k < kSelectChunk ? k : kSelectChunk;
+    const int len = (int)(remain < CH ? remain : CH);
+    const int kk = k < CH ? k : CH;
 
     // Key i of the chunk is held by thread i % kThreads; slots past the chunk
     // hold the padding key 0.  Scores are loaded unconditionally (positions
     // past the chunk re-read its last one, a chunk is never empty here) so
     // that all loads are in flight at once: a load under a branch makes the
     // thread wait for it before issuing the next.
-    uint64_t key[kPer];
+    uint64_t key[P];
     if constexpr (FROM_SCORES) {
         const float* src = scores + (int64_t)q * count + start;
         const int last = len > 0 ? len - 1 : 0;
-        float sv[kPer];
+        float sv[P];
 #pragma unroll
-        for (int e = 0; e < kPer; ++e) {
+        for (int e = 0; e < P; ++e) {
             const int i = tid + e * kThreads;
             sv[e] = src[i < len ? i : last];
         }
 #pragma unroll
-        for (int e = 0; e < kPer; ++e) {
+        for (int e = 0; e < P; ++e) {
             const int i = tid + e * kThreads;
             key[e] = i < len ? pack_key(sv[e], (uint32_t)(start + i)) : 0;
         }
     } else {
 #pragma unroll
-        for (int e = 0; e < kPer; ++e) {
+        for (int e = 0; e < P; ++e) {
             const int i = tid + e * kThreads;
             key[e] = i < len ? in_keys[(int64_t)q * count + start + i] : 0;
         }
     }
-    const ChunkStats cs = chunk_stats<kThreads>(key, s_nzw, s_andw, s_orw);
+    const ChunkStats cs = chunk_stats<kThreads, P>(key, s_nzw, s_andw, s_orw);
 
     // Keys taken: every real one if there are no more than kk, else the kk
     // largest (then more than kk keys are real, as the radix select needs).
     SelectState st{0, 0};
     const bool all = cs.nz <= (uint32_t)kk;
-    if (!all) st = radix_select<kThreads>(key, kk, cs, s_hist, s_tot, s_info);
+    if (!all) st = radix_select<kThreads, P>(key, kk, cs, s_hist, s_tot, s_info);
     auto taken = [&](int e) {
         return all ? (key[e] != 0) : ((key[e] & st.mask) >= st.prefix);
     };
 
     if constexpr (!FINAL) {
         uint64_t* out = out_keys + ((int64_t)q * gridDim.x + blockIdx.x) * kk;
-        const uint32_t tot = compact_taken<kThreads>(key, taken, out, kk, s_wc);
+        const uint32_t tot = compact_taken<kThreads, P>(key, taken, out, kk, s_wc);
         const int nt = (int)tot < kk ? (int)tot : kk;
         for (int i = nt + tid; i < kk; i += kThreads) out[i] = 0;  // padding key
     } else {
-        const uint32_t tot = compact_taken<kThreads>(key, taken, s_sel, kk, s_wc);
+        const uint32_t tot = compact_taken<kThreads, P>(key, taken, s_sel, kk, s_wc);
         const int nt = (int)tot < kk ? (int)tot : kk;
         final_output<kThreads>(s_sel, s_sorted, nt, k, q, out_ids, out_scores, out_drafts,
                                out_draft_len, spans, span_len, max_span, span_stride);
@@ -356,11 +359,65 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
 
 // One block per query over a key list whose length is a per-query count on
 // the device (candidate buffers: most of the capacity is unused): rounds of
-// kStreamKeys keys, each holding the running top k and the next new keys,
-// reduced to the top k by the same radix select; then the final output.  The
-// common case (the count fits one round) is one launch; any count is exact.
+// kStreamThreads * P keys, each holding the running top k and the next new
+// keys, reduced to the top k by the same radix select; then the final
+// output.  P (keys per thread) is chosen per query from its count, so a short
+// list is walked with less work; a count that fits one round of the largest
+// P is one round, and any count is exact.
 constexpr int kStreamThreads = 1024;
-constexpr int kStreamKeys = kStreamThreads * kPer;
+constexpr int kStreamPer = kPer;                       // the largest P
+
+struct StreamLds {
+    uint32_t* s_hist;
+    uint32_t* s_tot;
+    uint32_t* s_info;
+    uint32_t* s_nzw;
+    uint32_t* s_wc;
+    uint64_t* s_andw;
+    uint64_t* s_orw;
+};
+
+template <int P>
+__device__ int stream_rounds(const uint64_t* __restrict__ src, int64_t count, int64_t cnt_q,
+                             int kk, uint64_t* s_sel, const StreamLds& L) {
+    constexpr int R = kStreamThreads * P;              // keys per round
+    const int tid = threadIdx.x;
+    int nt = 0;                                        // running top keys in s_sel
+    int64_t pos = 0;
+    do {
+        const int64_t left = cnt_q - pos;
+        const int take = (int)((R - nt) < left ? (R - nt) : left);
+        // New keys on clamped positions (no branch around a load), the
+        // running ones from LDS.
+        uint64_t key[P];
+#pragma unroll
+        for (int e = 0; e < P; ++e) {
+            const int i = tid + e * kStreamThreads;
+            const int64_t j = pos + (i - nt);
+            const int64_t jc = j < 0 ? 0 : (j < count ? j : count - 1);
+            key[e] = src[jc];
+        }
+#pragma unroll
+        for (int e = 0; e < P; ++e) {
+            const int i = tid + e * kStreamThreads;
+            if (i < nt) key[e] = s_sel[i];
+            else if (i - nt >= take) key[e] = 0;
+        }
+        __syncthreads();                               // s_sel read before it is rewritten
+        const ChunkStats cs = chunk_stats<kStreamThreads, P>(key, L.s_nzw, L.s_andw, L.s_orw);
+        SelectState st{0, 0};
+        const bool all = cs.nz <= (uint32_t)kk;
+        if (!all) st = radix_select<kStreamThreads, P>(key, kk, cs, L.s_hist, L.s_tot, L.s_info);
+        auto taken = [&](int e) {
+            return all ? (key[e] != 0) : ((key[e] & st.mask) >= st.prefix);
+        };
+        const uint32_t tot = compact_taken<kStreamThreads, P>(key, taken, s_sel, kk, L.s_wc);
+        nt = (int)tot < kk ? (int)tot : kk;
+        pos += take;
+        __syncthreads();                               // s_sel complete for the next round
+    } while (pos < cnt_q);
+    return nt;
+}
 
 __global__ __launch_bounds__(kStreamThreads) void select_stream_kernel(
     const uint64_t* __restrict__ in_keys, int64_t count, int k,
@@ -376,51 +433,43 @@ __global__ __launch_bounds__(kStreamThreads) void select_stream_kernel(
     __shared__ uint32_t s_info[4];
     __shared__ uint32_t s_nzw[W], s_wc[W];
     __shared__ uint64_t s_andw[W], s_orw[W];
-    const int tid = threadIdx.x;
+    const StreamLds L{s_hist, s_tot, s_info, s_nzw, s_wc, s_andw, s_orw};
     const int q = blockIdx.x;
-    const int kk = k;                                  // k <= kMaxK < kStreamKeys
+    const int kk = k;                                  // k <= kMaxK < kStreamThreads * 4
     int64_t cnt_q = dev_count ? (int64_t)dev_count[q] : count;
     cnt_q = cnt_q < 0 ? 0 : (cnt_q > count ? count : cnt_q);
     const uint64_t* src = in_keys + (int64_t)q * count;
-    int nt = 0;                                        // running top keys in s_sel
-    int64_t pos = 0;
-    do {
-        const int64_t left = cnt_q - pos;
-        const int take = (int)((kStreamKeys - nt) < left ? (kStreamKeys - nt) : left);
-        // New keys on clamped positions (no branch around a load), the
-        // running ones from LDS.
-        uint64_t key[kPer];
-#pragma unroll
-        for (int e = 0; e < kPer; ++e) {
-            const int i = tid + e * kStreamThreads;
-            const int64_t j = pos + (i - nt);
-            const int64_t jc = j < 0 ? 0 : (j < count ? j : count - 1);
-            key[e] = src[jc];
-        }
-#pragma unroll
-        for (int e = 0; e < kPer; ++e) {
-            const int i = tid + e * kStreamThreads;
-            if (i < nt) key[e] = s_sel[i];
-            else if (i - nt >= take) key[e] = 0;
-        }
-        __syncthreads();                               // s_sel read before it is rewritten
-        const ChunkStats cs = chunk_stats<kStreamThreads>(key, s_nzw, s_andw, s_orw);
-        SelectState st{0, 0};
-        const bool all = cs.nz <= (uint32_t)kk;
-        if (!all) st = radix_select<kStreamThreads>(key, kk, cs, s_hist, s_tot, s_info);
-        auto taken = [&](int e) {
-            return all ? (key[e] != 0) : ((key[e] & st.mask) >= st.prefix);
-        };
-        const uint32_t tot = compact_taken<kStreamThreads>(key, taken, s_sel, kk, s_wc);
-        nt = (int)tot < kk ? (int)tot : kk;
-        pos += take;
-        __syncthreads();                               // s_sel complete for the next round
-    } while (pos < cnt_q);
+    // The branch is uniform over the block.
+    int nt;
+    if (cnt_q <= (int64_t)kStreamThreads * 4)
+        nt = stream_rounds<4>(src, count, cnt_q, kk, s_sel, L);
+    else if (cnt_q <= (int64_t)kStreamThreads * 8)
+        nt = stream_rounds<8>(src, count, cnt_q, kk, s_sel, L);
+    else
+        nt = stream_rounds<kStreamPer>(src, count, cnt_q, kk, s_sel, L);
     final_output<kStreamThreads>(s_sel, s_sorted, nt, k, q, out_ids, out_scores, out_drafts,
                                  out_draft_len, spans, span_len, max_span, span_stride);
 }
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// The final level over one chunk of keys (count <= kSelectChunk): eight
+// keys per thread when they fit.
+void launch_final_keys(const uint64_t* keys, int64_t count, int nq, int k, const int32_t* spans,
+                       const int32_t* span_len, int max_span, int64_t span_stride,
+                       int64_t* out_ids, float* out_scores, int32_t* out_drafts,
+                       int32_t* out_draft_len, const int32_t* counts, hipStream_t stream) {
+    if (count <= (int64_t)kThreads * 8)
+        hipLaunchKernelGGL((select_kernel<false, true, 8>), dim3(1, nq), dim3(kThreads), 0,
+                           stream, nullptr, keys, count, k, nullptr, out_ids, out_scores,
+                           out_drafts, out_draft_len, spans, span_len, max_span, span_stride,
+                           counts, nullptr);
+    else
+        hipLaunchKernelGGL((select_kernel<false, true, kPer>), dim3(1, nq), dim3(kThreads), 0,
+                           stream, nullptr, keys, count, k, nullptr, out_ids, out_scores,
+                           out_drafts, out_draft_len, spans, span_len, max_span, span_stride,
+                           counts, nullptr);
+}
 
 }  // namespace
 
@@ -447,14 +496,22 @@ hipError_t launch_topk_gather(const float* scores, int64_t n, int nq, int k,
     const int64_t kk = k < kSelectChunk ? k : kSelectChunk;
     int64_t chunks = ceil_div(n, kSelectChunk);
     if (chunks <= 1) {
-        hipLaunchKernelGGL((select_kernel<true, true>), dim3(1, nq), dim3(kThreads), 0, stream,
-                           scores, nullptr, n, k, nullptr, out_ids, out_scores, out_drafts,
-                           out_draft_len, spans, span_len, max_span, span_stride, nullptr, nullptr);
+        // One chunk; up to kThreads * 8 scores take eight per thread.
+        if (n <= (int64_t)kThreads * 8)
+            hipLaunchKernelGGL((select_kernel<true, true, 8>), dim3(1, nq), dim3(kThreads), 0,
+                               stream, scores, nullptr, n, k, nullptr, out_ids, out_scores,
+                               out_drafts, out_draft_len, spans, span_len, max_span, span_stride,
+                               nullptr, nullptr);
+        else
+            hipLaunchKernelGGL((select_kernel<true, true, kPer>), dim3(1, nq), dim3(kThreads), 0,
+                               stream, scores, nullptr, n, k, nullptr, out_ids, out_scores,
+                               out_drafts, out_draft_len, spans, span_len, max_span, span_stride,
+                               nullptr, nullptr);
         return hipGetLastError();
     }
     const size_t one = key_buffer_bytes(n, nq, k);
     uint64_t* buf[2] = {(uint64_t*)workspace, (uint64_t*)((char*)workspace + one)};
-    hipLaunchKernelGGL((select_kernel<true, false>), dim3((unsigned)chunks, nq), dim3(kThreads),
+    hipLaunchKernelGGL((select_kernel<true, false, kPer>), dim3((unsigned)chunks, nq), dim3(kThreads),
                        0, stream, scores, nullptr, n, k, buf[0], nullptr, nullptr, nullptr,
                        nullptr, nullptr, nullptr, 0, 0, nullptr, nullptr);
     hipError_t e = hipGetLastError();
@@ -462,7 +519,7 @@ hipError_t launch_topk_gather(const float* scores, int64_t n, int nq, int k,
     int64_t count = chunks * kk;
     int cur = 0;
     while ((chunks = ceil_div(count, kSelectChunk)) > 1) {
-        hipLaunchKernelGGL((select_kernel<false, false>), dim3((unsigned)chunks, nq),
+        hipLaunchKernelGGL((select_kernel<false, false, kPer>), dim3((unsigned)chunks, nq),
                            dim3(kThreads), 0, stream, nullptr, buf[cur], count, k, buf[cur ^ 1],
                            nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 0, 0, nullptr,
                            nullptr);
@@ -470,9 +527,8 @@ hipError_t launch_topk_gather(const float* scores, int64_t n, int nq, int k,
         count = chunks * kk;
         cur ^= 1;
     }
-    hipLaunchKernelGGL((select_kernel<false, true>), dim3(1, nq), dim3(kThreads), 0, stream,
-                       nullptr, buf[cur], count, k, nullptr, out_ids, out_scores, out_drafts,
-                       out_draft_len, spans, span_len, max_span, span_stride, nullptr, nullptr);
+    launch_final_keys(buf[cur], count, nq, k, spans, span_len, max_span, span_stride, out_ids,
+                      out_scores, out_drafts, out_draft_len, nullptr, stream);
     return hipGetLastError();
 }
 
@@ -504,7 +560,7 @@ hipError_t launch_topk_keys(const uint64_t* keys, int64_t count, int nq, int k,
     int cc = 0;
     while (chunks > 1) {
         int32_t* next = counts ? cnt_buf[cc] : nullptr;
-        hipLaunchKernelGGL((select_kernel<false, false>), dim3((unsigned)chunks, nq),
+        hipLaunchKernelGGL((select_kernel<false, false, kPer>), dim3((unsigned)chunks, nq),
                            dim3(kThreads), 0, stream, nullptr, cur_in, cur_count, k, buf[cur],
                            nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 0, 0, counts,
                            next);
@@ -516,9 +572,8 @@ hipError_t launch_topk_keys(const uint64_t* keys, int64_t count, int nq, int k,
         cur ^= 1;
         chunks = ceil_div(cur_count, kSelectChunk);
     }
-    hipLaunchKernelGGL((select_kernel<false, true>), dim3(1, nq), dim3(kThreads), 0, stream,
-                       nullptr, cur_in, cur_count, k, nullptr, out_ids, out_scores, out_drafts,
-                       out_draft_len, spans, span_len, max_span, span_stride, counts, nullptr);
+    launch_final_keys(cur_in, cur_count, nq, k, spans, span_len, max_span, span_stride, out_ids,
+                      out_scores, out_drafts, out_draft_len, counts, stream);
     return hipGetLastError();
 }
 
