@@ -201,6 +201,27 @@ def test_ivf_flat_probing_everything_many_rounds(k):
     flat.close()
 
 
+@pytest.mark.parametrize("n", [4096, 4097, 8192, 8193, 16384, 16385, 20000])
+def test_ivf_candidate_counts_at_selection_boundaries(n):
+    """Probing every list makes the candidate count n: the candidate
+    selection takes 4, 8 or 16 keys per thread by the count (one round up to
+    16384, then several); each must equal the exact retrieval."""
+    w, ds = store(n, 32, "bf16", 17)
+    q, _ = synth.make_queries(w, ds, 17, n_queries=2)
+    cen, _ = synth.fit_ivf(ds.keys, 17, 16, iters=2)
+    lists = sense.sense_ivf_assign(ds.keys, cen, "cosine")
+    index = sense.sense_build_ivf_index(ds.keys, ds.spans, cen, lists)
+    ids, sc, dr, _ = sense.sense_ivf_search(index, q, 100, 16)
+    flat = sense.sense_build_index(ds.keys, ds.spans)
+    e_ids, e_sc, e_dr, _ = sense.sense_retrieve(flat, q, 100)
+    torch.cuda.synchronize()
+    assert torch.equal(ids, e_ids)
+    assert torch.allclose(sc, e_sc, rtol=1e-6, atol=0)
+    assert torch.equal(dr, e_dr)
+    index.close()
+    flat.close()
+
+
 def test_ivf_rejects_bad_list_ids():
     w, ds = store(1000, 64, "bf16", 2)
     cen, _ = synth.fit_ivf(ds.keys, 2, 16, iters=1)

@@ -60,6 +60,12 @@ SMALL = [
     ("tiny-n-d8", 40, 8, "bf16", 40),               # k = n, one partial load chunk
     ("d8192-bf16", 20000, 8192, "bf16", 128),
     ("k1024", 30000, 512, "bf16", 1024),
+    # one chunk of 4096 scores takes eight per thread, 4097 sixteen
+    ("one-chunk-4096-d256", 4096, 256, "bf16", 64),
+    ("one-chunk-4097-d256", 4097, 256, "bf16", 64),
+    ("k1024-n4096", 4096, 128, "f16", 1024),
+    # a final level of 5 x 1024 keys (more than 4096: sixteen per thread)
+    ("k1024-5chunks", 5 * 8192 - 3, 128, "bf16", 1024),
 ]
 
 
