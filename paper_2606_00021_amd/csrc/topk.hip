@@ -9,11 +9,13 @@
 // largest keys" and ties need no special handling.
 //
 // Selection is hierarchical.  A block of 512 threads takes a chunk of 8192
-// keys into registers (16 per thread).  One reduction gives the number of
-// real (non-padding) keys and the AND and OR of them: the bits above the
-// highest bit where they differ are shared by all, so the radix select
-// starts right below them (scores of one query share their sign and most of
-// their exponent, which a fixed top-down start would spend a whole pass on).
+// keys into registers (16 per thread; a single chunk of at most 4096 keys
+// takes 8 per thread, since every phase costs its per-thread key loop).
+// One reduction gives the number of real (non-padding) keys and the AND and
+// OR of them: the bits above the highest bit where they differ are shared by
+// all, so the radix select starts right below them (scores of one query
+// share their sign and most of their exponent, which a fixed top-down start
+// would spend a whole pass on).
 // Each pass builds a 256-bin LDS histogram of the next 8-bit digit among the
 // keys that still match the chosen prefix, then one wave finds the digit
 // holding the k-th key with a suffix scan; the loop stops as soon as that
