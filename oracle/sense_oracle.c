@@ -518,17 +518,41 @@ int oracle_ivf_assign(const void *keys, int key_dtype, int64_t n, int32_t d, int
     if (!keys || !centroids || !out_list || nlist < 1 || d < 1 || key_stride < d ||
         !dtype_ok(key_dtype))
         return -1;
+    /* The same sums as sim_row, term for term and in the same order, with
+     * each centroid's squared norm formed once and each key decoded once
+     * (every similarity is the value sim_row gives). */
+    double *vn = malloc((size_t)nlist * sizeof(double));
+    if (!vn) return -1;
+    for (int32_t l = 0; l < nlist; ++l) {
+        const double *v = centroids + (int64_t)l * d;
+        double s = 0.0;
+        for (int32_t t = 0; t < d; ++t) s += v[t] * v[t];
+        vn[l] = s;
+    }
 #pragma omp parallel for schedule(static)
     for (int64_t i = 0; i < n; ++i) {
+        double *x = malloc((size_t)d * sizeof(double));
+        double kn = 0.0;
+        for (int32_t t = 0; t < d; ++t) {
+            x[t] = elem(keys, key_dtype, i * key_stride + t);
+            kn += x[t] * x[t];
+        }
         int32_t best = 0;
         double bs = -INFINITY;
         for (int32_t l = 0; l < nlist; ++l) {
-            double s = sim_row(keys, key_dtype, i * key_stride, d, centroids + (int64_t)l * d, metric);
+            const double *v = centroids + (int64_t)l * d;
+            double dot = 0.0;
+            for (int32_t t = 0; t < d; ++t) dot += x[t] * v[t];
+            double s = dot;
+            if (metric != 0)
+                s = (kn == 0.0 || vn[l] == 0.0) ? 0.0 : dot / (sqrt(kn) * sqrt(vn[l]));
             if (s > bs) { bs = s; best = l; }
         }
         out_list[i] = best;
         if (out_score) out_score[i] = bs;
+        free(x);
     }
+    free(vn);
     return 0;
 }
 

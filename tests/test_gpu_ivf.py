@@ -222,6 +222,53 @@ def test_ivf_candidate_counts_at_selection_boundaries(n):
     flat.close()
 
 
+def test_full_size_ivf_pq_bench_shape():
+    """IVF-PQ at the bench's shape: 1M x 64 bf16 keys, nlist 4096, nprobe 32,
+    pq_m 16 (ksub 256), k = 64, searched with one query and with a batch of
+    64 (the launch configurations timed), on an index built from the
+    oracle's own list ids and codes; each query as in the small cases."""
+    n, d, nlist, nprobe, m, k = 1 << 20, 64, 4096, 32, 16, 64
+    print(f"[ivf] full size n={n} d={d} nlist={nlist} nprobe={nprobe} pq_m={m}", flush=True)
+    w, ds = store(n, d, "bf16", 23, clusters=4096)
+    q, _ = synth.make_queries(w, ds, 23, n_queries=64)
+    cen, books = synth.fit_ivf(ds.keys, 23, nlist, pq_m=m)
+    kb = host_bits(ds.keys)
+    cen_h = cen.cpu().numpy().astype(np.float64)
+    books_h = books.cpu().numpy().astype(np.float64)
+    lists, _ = oracle.ivf_assign(kb, "bf16", cen_h, "cosine")
+    codes = oracle.pq_encode(kb, "bf16", cen_h, lists, books_h)
+    print("[ivf] oracle assignment and codes done", flush=True)
+    index = sense.sense_build_ivf_index(None, ds.spans, cen, torch.from_numpy(lists).to(DEV),
+                                        codebooks=books, codes=torch.from_numpy(codes).to(DEV),
+                                        key_dtype=ds.keys.dtype)
+    qh = q.cpu().numpy().astype(np.float64)
+    spans = ds.spans.cpu().numpy()
+    # reconstructed keys (centroid + codewords), the PQ scores' row vectors
+    rec = cen_h[lists] + np.concatenate([books_h[j][codes[:, j]] for j in range(m)], axis=1)
+    for nq in (1, 64):
+        ids, sc, dr, dl, probe = sense.sense_ivf_search(index, q[:nq], k, nprobe,
+                                                        want_probe=True)
+        torch.cuda.synchronize()
+        for qq in range(nq):
+            o_probe, coarse, o_ids, o_sc = oracle.ivf_search(
+                qh[qq], cen_h, lists, nprobe, k, "cosine", codes=codes, codebooks=books_h)
+            g_probe = probe[qq].cpu().numpy()
+            kth = coarse[o_probe[-1]]
+            assert len(set(g_probe.tolist())) == nprobe
+            for l in set(g_probe.tolist()) - set(o_probe.tolist()):
+                assert coarse[l] >= kth - 1e-5 * abs(kth), f"query {qq}: list {l} not a near tie"
+            inside = np.isin(lists, g_probe)
+            u = qh[qq] / np.linalg.norm(qh[qq])
+            cs = np.where(inside, rec @ u, -np.inf)
+            g_ids = ids[qq].cpu().numpy()
+            check_topk(g_ids, sc[qq].cpu().numpy(), cs, k)
+            if set(g_probe.tolist()) == set(o_probe.tolist()):
+                np.testing.assert_allclose(np.sort(o_sc), np.sort(cs[o_ids]), rtol=1e-12)
+            assert np.array_equal(dr[qq].cpu().numpy(), spans[g_ids])
+        print(f"[ivf] {nq} queries ok", flush=True)
+    index.close()
+
+
 def test_ivf_rejects_bad_list_ids():
     w, ds = store(1000, 64, "bf16", 2)
     cen, _ = synth.fit_ivf(ds.keys, 2, 16, iters=1)

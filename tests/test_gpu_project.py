@@ -186,3 +186,52 @@ def test_batched_short_scan_when_every_row_passes_the_threshold():
     o_s = oracle.scores(host_bits(keys[:200]), "bf16", q.cpu().numpy(), "f32", "cosine")
     np.testing.assert_allclose(sc[:, 0].cpu().numpy(), o_s[:, 1], rtol=1e-3)
     index.close()
+
+
+def test_full_size_store_projection():
+    """The store projection at the bench's shape: 1M x 4096 bf16 hidden
+    states -> 64 bf16, normalised (matrix-core route), 512 seeded sample rows
+    against the oracle; the 64 fp32 queries of the batched shape (direct
+    route) in full."""
+    w = synth.WORKLOADS["store-1m-pca64-q64"]
+    seed = 1000 + list(synth.WORKLOADS).index(w.name)
+    print(f"[project] full size n={w.n} d={w.d} -> {w.proj}", flush=True)
+    ds = synth.make_datastore(w, seed, DEV)
+    q, _ = synth.make_queries(w, ds, seed)
+    mean, basis = synth.make_pca_basis(ds, seed, w.proj)
+    keys64 = sense.sense_project(ds.keys, basis, mean, True, out_dtype=torch.bfloat16)
+    q64 = sense.sense_project(q, basis, mean, True, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    rows = np.sort(np.random.default_rng(seed).choice(w.n, 512, replace=False))
+    rows_t = torch.from_numpy(rows).to(DEV)
+    check_projection(keys64[rows_t], host_bits(ds.keys[rows_t]), "bf16", basis, mean, True,
+                     "bf16")
+    check_projection(q64, q.cpu().numpy(), "f32", basis, mean, True, "f32")
+    print("[project] sampled store rows and all queries ok", flush=True)
+    del ds, keys64
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("nq", [1, 64])
+def test_full_size_short_key_retrieval(nq):
+    """Retrieval over a projected-shape store at the bench's size: 1M x 64
+    bf16 keys, k = 64; one query takes the short-key scan, 64 the batched
+    path with the sampled threshold.  Every query against the oracle's
+    scores of all rows."""
+    n, d, k = 1 << 20, 64, 64
+    print(f"[short-scan] full size n={n} d={d} Q={nq} k={k}", flush=True)
+    w = synth.scaled(synth.WORKLOADS["tiny-16k-d4096"], n=n, d=d, key_dtype="bf16", k=k,
+                     n_clusters=4096, n_outliers=2)
+    ds = synth.make_datastore(w, 53, DEV)
+    q, src = synth.make_queries(w, ds, 53, n_queries=nq)
+    index = sense.sense_build_index(ds.keys, ds.spans)
+    ids, sc, dr, _ = sense.sense_retrieve(index, q, k)
+    torch.cuda.synchronize()
+    o_s = oracle.scores(host_bits(ds.keys), "bf16", q.cpu().numpy(), "f32")
+    spans = ds.spans.cpu().numpy()
+    for qq in range(nq):
+        g_ids = ids[qq].cpu().numpy()
+        check_topk(g_ids, sc[qq].cpu().numpy(), o_s[qq], k)
+        assert np.array_equal(dr[qq].cpu().numpy(), oracle.gather(spans, None, g_ids)[0])
+    print(f"[short-scan] {nq} queries ok", flush=True)
+    index.close()
