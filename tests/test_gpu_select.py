@@ -228,6 +228,7 @@ def check_selection(g_src, o_comp, o_sim, beta, top_n):
 @pytest.mark.parametrize("wname,scale,ctx_len,k_dyn,top_n", [
     ("tiny-16k-d4096", {}, 512, 8, 8),
     ("store-1m-d4096", {"n": 40000, "n_clusters": 160}, 4096, 16, 64),
+    ("store-1m-d4096", {}, 4096, 16, 64),          # the bench's SEN step at full size
 ])
 def test_sen_chain(wname, scale, ctx_len, k_dyn, top_n):
     """Static retrieval + dynamic retrieval + selection + verification, as a
