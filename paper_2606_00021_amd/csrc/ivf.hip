@@ -369,24 +369,48 @@ __device__ __forceinline__ int32_t scan_probe_sizes(const int32_t* s_size, int32
     return carry;
 }
 
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float x) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x),
+                                                                 CTRL, 0xF, 0xF, false));
+}
+
+// Sum over each aligned group of LPR lanes (the sums of an xor butterfly,
+// every lane of a group with the same bits): quad xor 1, xor 2, half-row
+// mirror, row mirror.
+template <int LPR>
+__device__ __forceinline__ float group_sum(float x) {
+    static_assert(LPR == 1 || LPR == 2 || LPR == 4 || LPR == 8 || LPR == 16, "group size");
+    if constexpr (LPR >= 2) x += dpp_f<0xB1>(x);
+    if constexpr (LPR >= 4) x += dpp_f<0x4E>(x);
+    if constexpr (LPR >= 8) x += dpp_f<0x141>(x);
+    if constexpr (LPR >= 16) x += dpp_f<0x140>(x);
+    return x;
+}
+
 // IVF-Flat list scan: block (p, q) scans probe p of query q; LPR lanes per
-// row as in the short-key scan (d <= 128, 16 bytes per lane).
-template <int KT>
+// row (16 bytes per lane, d <= 128).  Each wave takes runs of kFlatLoads
+// load instructions' rows (64 / LPR rows each), and requests every key,
+// norm and row id of a run together on clamped rows (rows past the list
+// re-read its last row and store nothing), so a list of a few hundred rows
+// is one round of loads.
+constexpr int kFlatLoads = 8;
+
+template <int KT, int LPR>
 __global__ __launch_bounds__(kIvfThreads) void ivf_scan_flat_kernel(
     const uint16_t* __restrict__ keys_sorted, int d, const float* __restrict__ inv_norm,
     const int32_t* __restrict__ row_ids, const int64_t* __restrict__ offsets,
     const float* __restrict__ queries, const int64_t* __restrict__ probe, int nprobe,
     int32_t* __restrict__ count, int64_t cap, uint64_t* __restrict__ cand) {
+    constexpr int RPI = 64 / LPR;                   // rows per load instruction
+    constexpr int RUN = RPI * kFlatLoads;           // rows per wave and round
     __shared__ int32_t s_size[kMaxK], s_pre[kMaxK];
     __shared__ int64_t s_r0[kMaxK];
     const int q = blockIdx.y;
     const int64_t* pq = probe + (int64_t)q * nprobe;
-    const int lanes = (d + 7) / 8;
-    int lpr = 1;
-    while (lpr < lanes) lpr <<= 1;
-    const int rpi = 64 / lpr;
-    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-    const int g = lane / lpr, c = lane % lpr, e = c * 8;
+    const int lane = threadIdx.x & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int g = lane / LPR, c = lane % LPR, e = c * 8;
     const bool col = e < d;
     const float* qv = queries + (int64_t)q * d;
     float qf[8];
@@ -399,7 +423,7 @@ __global__ __launch_bounds__(kIvfThreads) void ivf_scan_flat_kernel(
     float qq = 0.0f;
 #pragma unroll
     for (int t = 0; t < 8; ++t) qq = __builtin_fmaf(qf[t], qf[t], qq);
-    for (int off = 1; off < lpr; off <<= 1) qq += __shfl_xor(qq, off, 64);
+    qq = group_sum<LPR>(qq);
     const float inv_q = (qq > 0.0f) ? 1.0f / __builtin_sqrtf(qq) : 0.0f;
     __syncthreads();
     if (threadIdx.x < 64) {
@@ -407,37 +431,46 @@ __global__ __launch_bounds__(kIvfThreads) void ivf_scan_flat_kernel(
         if (blockIdx.x == 0 && threadIdx.x == 0) count[q] = total;
     }
     __syncthreads();
-    {
-        const int p = blockIdx.x;                   // one probe per block
-        const int64_t r0 = s_r0[p], r1 = r0 + s_size[p];
-        uint64_t* out = cand + (int64_t)q * cap + s_pre[p] - r0;
-        for (int64_t r = r0 + (int64_t)wv * rpi + g; r - g < r1;
-             r += (int64_t)(kIvfThreads / 64) * rpi) {
-            float a0 = 0.0f, a1 = 0.0f;
-            if (col && r < r1) {
-                const u32x4 v =
-                    __builtin_nontemporal_load((const u32x4*)(keys_sorted + r * d + e));
+    const int p = blockIdx.x;                       // one probe per block
+    const int64_t r0 = s_r0[p], r1 = r0 + s_size[p];
+    uint64_t* out = cand + (int64_t)q * cap + s_pre[p] - r0;
+    // Without norms the norm load reads the query's first value (unused).
+    const float* nsrc = inv_norm ? inv_norm : qv;
+    const int64_t nstep = inv_norm ? 1 : 0;
+    for (int64_t b0 = r0 + (int64_t)wv * RUN; b0 < r1; b0 += (int64_t)(kIvfThreads / 64) * RUN) {
+        u32x4 v[kFlatLoads];
+        float nv[kFlatLoads];
+        int32_t rid[kFlatLoads];
 #pragma unroll
-                for (int w = 0; w < 4; ++w) {
-                    const uint32_t u = v[w];
-                    float lo, hi;
-                    if constexpr (KT == DT_BF16) {
-                        lo = __builtin_bit_cast(float, u << 16);
-                        hi = __builtin_bit_cast(float, u & 0xFFFF0000u);
-                    } else {
-                        lo = (float)__builtin_bit_cast(_Float16, (uint16_t)(u & 0xFFFFu));
-                        hi = (float)__builtin_bit_cast(_Float16, (uint16_t)(u >> 16));
-                    }
-                    a0 = __builtin_fmaf(lo, qf[2 * w], a0);
-                    a1 = __builtin_fmaf(hi, qf[2 * w + 1], a1);
+        for (int u = 0; u < kFlatLoads; ++u) {
+            const int64_t r = b0 + u * RPI + g;
+            const int64_t rc = r < r1 ? r : r1 - 1;
+            v[u] = __builtin_nontemporal_load((const u32x4*)(keys_sorted + rc * d + (col ? e : 0)));
+            nv[u] = nsrc[rc * nstep];
+            rid[u] = row_ids[rc];
+        }
+#pragma unroll
+        for (int u = 0; u < kFlatLoads; ++u) {
+            const u32x4 w = col ? v[u] : u32x4{0u, 0u, 0u, 0u};
+            float a0 = 0.0f, a1 = 0.0f;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const uint32_t x = w[k];
+                float lo, hi;
+                if constexpr (KT == DT_BF16) {
+                    lo = __builtin_bit_cast(float, x << 16);
+                    hi = __builtin_bit_cast(float, x & 0xFFFF0000u);
+                } else {
+                    lo = (float)__builtin_bit_cast(_Float16, (uint16_t)(x & 0xFFFFu));
+                    hi = (float)__builtin_bit_cast(_Float16, (uint16_t)(x >> 16));
                 }
+                a0 = __builtin_fmaf(lo, qf[2 * k], a0);
+                a1 = __builtin_fmaf(hi, qf[2 * k + 1], a1);
             }
-            float s = a0 + a1;
-            for (int off = 1; off < lpr; off <<= 1) s += __shfl_xor(s, off, 64);
-            if (c == 0 && r < r1) {
-                if (inv_norm) s = (s * inv_norm[r]) * inv_q;
-                out[r] = pack_key(s, (uint32_t)row_ids[r]);
-            }
+            float sc = group_sum<LPR>(a0 + a1);
+            if (inv_norm) sc = (sc * nv[u]) * inv_q;
+            const int64_t r = b0 + u * RPI + g;
+            if (c == 0 && r < r1) out[r] = pack_key(sc, (uint32_t)rid[u]);
         }
     }
 }
@@ -711,14 +744,27 @@ hipError_t launch_ivf_search(const IvfSearch& s, hipStream_t stream) {
 #undef SENSE_PQ_SCAN
     } else {
         const dim3 grid((unsigned)s.nprobe, (unsigned)s.nq);
-        if (s.key_dtype == DT_BF16)
-            hipLaunchKernelGGL(ivf_scan_flat_kernel<DT_BF16>, grid, dim3(kIvfThreads), 0, stream,
-                               (const uint16_t*)s.keys_sorted, s.d, s.inv_norm, s.row_ids,
-                               s.offsets, s.queries, s.probe, s.nprobe, s.count, s.cap, s.cand);
-        else
-            hipLaunchKernelGGL(ivf_scan_flat_kernel<DT_F16>, grid, dim3(kIvfThreads), 0, stream,
-                               (const uint16_t*)s.keys_sorted, s.d, s.inv_norm, s.row_ids,
-                               s.offsets, s.queries, s.probe, s.nprobe, s.count, s.cap, s.cand);
+        const int lanes = (s.d + 7) / 8;
+        const int lpr = lanes <= 1 ? 1 : lanes <= 2 ? 2 : lanes <= 4 ? 4 : lanes <= 8 ? 8 : 16;
+#define SENSE_FLAT_SCAN(KT, LPR)                                                                \
+    hipLaunchKernelGGL((ivf_scan_flat_kernel<KT, LPR>), grid, dim3(kIvfThreads), 0, stream,      \
+                       (const uint16_t*)s.keys_sorted, s.d, s.inv_norm, s.row_ids, s.offsets,   \
+                       s.queries, s.probe, s.nprobe, s.count, s.cap, s.cand)
+#define SENSE_FLAT_LPR(KT)                                                                      \
+    switch (lpr) {                                                                              \
+        case 1: SENSE_FLAT_SCAN(KT, 1); break;                                                  \
+        case 2: SENSE_FLAT_SCAN(KT, 2); break;                                                  \
+        case 4: SENSE_FLAT_SCAN(KT, 4); break;                                                  \
+        case 8: SENSE_FLAT_SCAN(KT, 8); break;                                                  \
+        default: SENSE_FLAT_SCAN(KT, 16); break;                                                \
+    }
+        if (s.key_dtype == DT_BF16) {
+            SENSE_FLAT_LPR(DT_BF16)
+        } else {
+            SENSE_FLAT_LPR(DT_F16)
+        }
+#undef SENSE_FLAT_LPR
+#undef SENSE_FLAT_SCAN
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
     return launch_topk_keys(s.cand, s.cap, s.nq, s.k, s.spans, s.span_len, s.max_span,
