@@ -482,7 +482,10 @@ __global__ __launch_bounds__(kIvfThreads) void ivf_scan_flat_kernel(
 // score = u.c_l + sum_j LUT[j][code_j] (j in order).  MV = 16-byte code
 // words per row (m = 16 MV): a thread's rows are pipelined, the next one
 // requested before the current one is scored, and its first row before the
-// barriers; MV = 0: byte loads, any m.
+// barriers; MV = 0: byte loads, any m.  DS = 4: sub-vectors of 4 dims (the
+// implementation details' 64 dims / 16), each code's rows requested as
+// 16-byte words and each table entry one chain of 4 FMAs; DS = 0: any
+// sub-vector length.
 template <int MV>
 struct PqCodes {
     u32x4 w[MV > 0 ? MV : 1];
@@ -499,7 +502,7 @@ __device__ __forceinline__ PqCodes<MV> pq_load(const uint8_t* __restrict__ codes
     return c;
 }
 
-template <int KD, int MV>
+template <int KD, int MV, int DS>
 __global__ __launch_bounds__(kIvfThreads) void ivf_scan_pq_kernel(
     const uint8_t* __restrict__ codes_sorted, int m, int ksub, const float* __restrict__ queries,
     int d, int cosine, const float* __restrict__ codebooks, const float* __restrict__ ip,
@@ -507,7 +510,7 @@ __global__ __launch_bounds__(kIvfThreads) void ivf_scan_pq_kernel(
     const int64_t* __restrict__ probe, int nprobe, int32_t* __restrict__ count, int64_t cap,
     uint64_t* __restrict__ cand) {
     extern __shared__ float s_lut[];   // m * ksub
-    __shared__ float s_u[KD];
+    __shared__ __attribute__((aligned(16))) float s_u[KD];
     __shared__ int32_t s_size[kMaxK], s_pre[kMaxK];
     __shared__ int64_t s_r0[kMaxK];
     __shared__ float s_qc[kMaxK];
@@ -530,8 +533,17 @@ __global__ __launch_bounds__(kIvfThreads) void ivf_scan_pq_kernel(
     const float uq = queries[(int64_t)q * d + (tid < d ? tid : 0)];
     const int dsub = d / m;
     const int cc = tid < ksub ? tid : 0;
-    float cbv[KD];
-    {
+    constexpr int MJ = KD / 4;                      // most 4-dim sub-vectors
+    float4 cb4[DS == 4 ? MJ : 1];
+    float cbv[DS == 4 ? 1 : KD];
+    if constexpr (DS == 4) {
+        // code cc of sub-space j: C[(j * ksub + cc) * 4 .. + 4]
+#pragma unroll
+        for (int j = 0; j < MJ; ++j) {
+            const int jj = j < m ? j : 0;
+            cb4[j] = *(const float4*)(codebooks + ((int64_t)jj * ksub + cc) * 4);
+        }
+    } else {
         // element e = j * dsub + t of code cc lives at C[(j * ksub + cc) * dsub + t]
         int j = 0, t = 0;
 #pragma unroll
@@ -558,17 +570,31 @@ __global__ __launch_bounds__(kIvfThreads) void ivf_scan_pq_kernel(
     for (int w = 0; w < kIvfThreads / 64; ++w) qq += s_part[w];
     const float scale = cosine ? ((qq > 0.0f) ? 1.0f / __builtin_sqrtf(qq) : 0.0f) : 1.0f;
     if (tid < ksub) {
-        int j = 0, t = 0;
-        float a = 0.0f;
+        if constexpr (DS == 4) {
 #pragma unroll
-        for (int e = 0; e < KD; ++e) {
-            if (e < d) {
-                a = __builtin_fmaf(s_u[e] * scale, cbv[e], a);
-                if (++t == dsub) {
+            for (int j = 0; j < MJ; ++j) {
+                if (j < m) {
+                    const float4 u4 = *(const float4*)(s_u + 4 * j);
+                    float a = __builtin_fmaf(u4.x * scale, cb4[j].x, 0.0f);
+                    a = __builtin_fmaf(u4.y * scale, cb4[j].y, a);
+                    a = __builtin_fmaf(u4.z * scale, cb4[j].z, a);
+                    a = __builtin_fmaf(u4.w * scale, cb4[j].w, a);
                     s_lut[j * ksub + tid] = a;
-                    a = 0.0f;
-                    t = 0;
-                    ++j;
+                }
+            }
+        } else {
+            int j = 0, t = 0;
+            float a = 0.0f;
+#pragma unroll
+            for (int e = 0; e < KD; ++e) {
+                if (e < d) {
+                    a = __builtin_fmaf(s_u[e] * scale, cbv[e], a);
+                    if (++t == dsub) {
+                        s_lut[j * ksub + tid] = a;
+                        a = 0.0f;
+                        t = 0;
+                        ++j;
+                    }
                 }
             }
         }
@@ -725,22 +751,25 @@ hipError_t launch_ivf_search(const IvfSearch& s, hipStream_t stream) {
         const dim3 grid((unsigned)g, (unsigned)s.nq);
         const size_t lds = (size_t)s.m * s.ksub * sizeof(float);
         const int mv = (s.m % 16 == 0 && s.m <= 64) ? s.m / 16 : 0;
-#define SENSE_PQ_SCAN(KD, MV)                                                                   \
-    hipLaunchKernelGGL((ivf_scan_pq_kernel<KD, MV>), grid, dim3(kIvfThreads), lds, stream,       \
+#define SENSE_PQ_SCAN(KD, MV, DS)                                                               \
+    hipLaunchKernelGGL((ivf_scan_pq_kernel<KD, MV, DS>), grid, dim3(kIvfThreads), lds, stream,   \
                        s.codes_sorted, s.m, s.ksub, s.queries, s.d, s.cosine, s.codebooks,      \
                        s.coarse_ip, s.nlist, s.row_ids, s.offsets, s.probe, s.nprobe, s.count, \
                        s.cap, s.cand)
+#define SENSE_PQ_MV(KD, DS)                                                                     \
+    switch (mv) {                                                                               \
+        case 1: SENSE_PQ_SCAN(KD, 1, DS); break;                                                \
+        case 2: SENSE_PQ_SCAN(KD, 2, DS); break;                                                \
+        case 4: SENSE_PQ_SCAN(KD, 4, DS); break;                                                \
+        default: SENSE_PQ_SCAN(KD, 0, DS); break;                                               \
+    }
+        const bool ds4 = s.d == 4 * s.m;
         if (s.d <= 64) {
-            if (mv == 1) SENSE_PQ_SCAN(64, 1);
-            else if (mv == 2) SENSE_PQ_SCAN(64, 2);
-            else if (mv == 4) SENSE_PQ_SCAN(64, 4);
-            else SENSE_PQ_SCAN(64, 0);
+            if (ds4) SENSE_PQ_MV(64, 4) else SENSE_PQ_MV(64, 0)
         } else {
-            if (mv == 1) SENSE_PQ_SCAN(128, 1);
-            else if (mv == 2) SENSE_PQ_SCAN(128, 2);
-            else if (mv == 4) SENSE_PQ_SCAN(128, 4);
-            else SENSE_PQ_SCAN(128, 0);
+            if (ds4) SENSE_PQ_MV(128, 4) else SENSE_PQ_MV(128, 0)
         }
+#undef SENSE_PQ_MV
 #undef SENSE_PQ_SCAN
     } else {
         const dim3 grid((unsigned)s.nprobe, (unsigned)s.nq);
