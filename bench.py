@@ -25,6 +25,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0   # MI355X HBM3E, published
+MFMA_PEAK_TFLOPS = 2500.0   # MI355X dense fp16/bf16 matrix-core peak (published)
 METRIC = "retrieval+verify queries/sec and achieved HBM GB/s (% of peak) at N=1M, d=4096"
 
 
@@ -129,6 +130,21 @@ def cpu_baseline(w, ds, q, logits, drafts, budget_s: float):
     t_verify_pos = (time.perf_counter() - t0) / (c_s * drafts.shape[1])
     pos_per_query = w.n_cand * w.span / w.n_queries
     t_query = t_scan_row * w.n + t_sort + t_verify_pos * pos_per_query
+    # The same oracle on one core (its OpenMP loops on one thread), on a
+    # sample as many times smaller as there are cores; the sort is one thread
+    # in both.
+    prev = oracle.set_threads(1)
+    try:
+        rows1 = max(cal, rows // max(1, cores))
+        t0 = time.perf_counter()
+        oracle.scores(keys_s[:rows1], kb_dt, qh[:1], "f32", metric=w.metric)
+        t_scan_row1 = (time.perf_counter() - t0) / rows1
+        t0 = time.perf_counter()
+        oracle.soft_gate_verify(lg[:1], dt_name, drafts[:1].cpu().numpy())
+        t_verify_pos1 = (time.perf_counter() - t0) / drafts.shape[1]
+    finally:
+        oracle.set_threads(prev)
+    t_query1 = t_scan_row1 * w.n + t_sort + t_verify_pos1 * pos_per_query
     cpu_model = None
     try:
         with open("/proc/cpuinfo") as f:
@@ -147,6 +163,11 @@ def cpu_baseline(w, ds, q, logits, drafts, budget_s: float):
                    f"({t_sort:.3f} s), verify of {c_s}x{drafts.shape[1]} positions x "
                    f"V={w.vocab} ({t_verify_pos * 1e3:.2f} ms/position); scaled to one "
                    f"query = {w.n} rows + sort + {pos_per_query:.0f} positions"),
+        "value_1core": 1.0 / t_query1,
+        "sample_1core": (f"the same oracle on one thread: scan of {rows1} rows "
+                         f"({t_scan_row1 * 1e6:.3f} us/row), verify of 1x{drafts.shape[1]} "
+                         f"positions ({t_verify_pos1 * 1e3:.2f} ms/position), the same sort; "
+                         f"scaled to one query alike"),
     }
 
 
@@ -579,6 +600,20 @@ def main():
                      "traffic": (traffic_from_profiles(name, scan_kernel)
                                  if scan_kernel in SCAN_SOURCES else None)},
     }
+    if scan_kernel == "scan_mfma_kernel":
+        # Matrix-core utilisation of the batched scan (bound by HBM, so a share
+        # of the dense peak, reported beside GB/s): the instructions issue
+        # whole 16-query tiles and 32-dimension steps, twice with fp32 queries
+        # (hi + lo halves in the key type).
+        qpad = 16 * ((nq + 15) // 16)
+        dpad = 32 * ((d_idx + 31) // 32)
+        halves = 2 if q.dtype == torch.float32 else 1
+        issued = 2.0 * w.n * dpad * qpad * halves
+        res["mfma"] = {"dtype": w.key_dtype, "issued_flops": issued,
+                       "useful_flops": 2.0 * w.n * d_idx * nq,
+                       "achieved_tflops": issued / (scan_ms * 1e-3) / 1e12,
+                       "peak_tflops": MFMA_PEAK_TFLOPS,
+                       "frac": issued / (scan_ms * 1e-3) / 1e12 / MFMA_PEAK_TFLOPS}
     if ivf_info is not None:
         res["config"]["ivf"] = ivf_info["kind"]
         res["ivf"] = ivf_info

@@ -75,6 +75,17 @@ def _load():
     return _lib
 
 
+def set_threads(n: int) -> int:
+    """Threads the oracle's OpenMP loops use from now on (the host baseline is
+    timed on all cores and on one); returns the previous count."""
+    lib = _load()
+    lib.omp_get_max_threads.restype = ctypes.c_int
+    lib.omp_set_num_threads.argtypes = [ctypes.c_int]
+    prev = int(lib.omp_get_max_threads())
+    lib.omp_set_num_threads(int(n))
+    return prev
+
+
 def _ptr(a):
     return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
 
