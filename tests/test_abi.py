@@ -396,3 +396,94 @@ def test_project_workspace_sizes(lib):
                                             ctypes.byref(size)) == 0
     assert size.value == 0
     assert lib.sense_project(ctypes.byref(d), None, 2, 0, 4096, None, 2, 64, None, 0, None) == 0
+
+
+# ---------------------------------------------------------------- inverted file
+
+@pytest.mark.parametrize("args,status", [
+    (dict(kdt=sense.SENSE_F32), INVALID),
+    (dict(n=0), INVALID),
+    (dict(d=100), INVALID),          # not a multiple of 8
+    (dict(d=136), INVALID),          # above the largest key dimension
+    (dict(ks=32), INVALID),          # stride below d
+    (dict(keys=p(FAKE + 2)), MISALIGNED),
+    (dict(ks=68), MISALIGNED),       # stride % 8 != 0
+    (dict(keys=None), INVALID),
+    (dict(cen=None), INVALID),
+    (dict(out=None), INVALID),
+    (dict(nlist=0), INVALID),
+    (dict(nlist=65537), INVALID),
+    (dict(metric=7), INVALID),
+    (dict(cen=p(FAKE + 2)), MISALIGNED),
+])
+def test_ivf_assign_rejects(lib, args, status):
+    a = dict(keys=p(FAKE), kdt=sense.SENSE_BF16, n=1000, d=64, ks=64, cen=p(FAKE), nlist=16,
+             metric=1, out=p(FAKE))
+    a.update(args)
+    assert lib.sense_ivf_assign(a["keys"], a["kdt"], a["n"], a["d"], a["ks"], a["cen"], a["nlist"],
+                                a["metric"], a["out"], None) == status
+    assert lib.sense_last_error_message()
+
+
+@pytest.mark.parametrize("args,status", [
+    (dict(m=0), INVALID),
+    (dict(m=3), INVALID),            # does not divide d = 64
+    (dict(m=2), INVALID),            # 32-dim sub-vectors: above 16
+    (dict(ksub=0), INVALID),
+    (dict(ksub=257), INVALID),
+    (dict(d=128, ksub=256), INVALID),   # ksub * d > 16384
+    (dict(lists=None), INVALID),
+    (dict(books=None), INVALID),
+    (dict(out=None), INVALID),
+    (dict(nlist=0), INVALID),
+    (dict(books=p(FAKE + 2)), MISALIGNED),
+    (dict(lists=p(FAKE + 2)), MISALIGNED),
+])
+def test_pq_encode_rejects(lib, args, status):
+    a = dict(keys=p(FAKE), kdt=sense.SENSE_BF16, n=1000, d=64, ks=64, cen=p(FAKE), nlist=16,
+             lists=p(FAKE), books=p(FAKE), m=16, ksub=256, out=p(FAKE))
+    a.update(args)
+    assert lib.sense_pq_encode(a["keys"], a["kdt"], a["n"], a["d"], a["ks"], a["cen"], a["nlist"],
+                               a["lists"], a["books"], a["m"], a["ksub"], a["out"], None) == status
+    assert lib.sense_last_error_message()
+
+
+def ivf_desc(**kw):
+    base = dict(keys=FAKE, key_dtype=sense.SENSE_BF16, n=1000, d=64, key_stride=64, spans=FAKE,
+                max_span=8, span_len=None, metric=1, centroids=FAKE, nlist=16, list_ids=FAKE,
+                pq_codebooks=None, pq_m=0, pq_ksub=0, pq_codes=None)
+    base.update(kw)
+    return sense.IvfDesc(**base)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(d=100), INVALID),
+    (dict(n=0), INVALID),
+    (dict(keys=None), INVALID),                      # IVF-Flat needs its keys
+    (dict(spans=None), INVALID),
+    (dict(centroids=None), INVALID),
+    (dict(list_ids=None), INVALID),
+    (dict(nlist=0), INVALID),
+    (dict(nlist=70000), INVALID),
+    (dict(max_span=0), INVALID),
+    (dict(max_span=65), INVALID),
+    (dict(metric=5), INVALID),
+    (dict(keys=FAKE + 2), MISALIGNED),
+    (dict(pq_codebooks=FAKE, pq_m=16, pq_ksub=256, pq_codes=None, keys=None), INVALID),
+    (dict(pq_codebooks=FAKE, pq_m=3, pq_ksub=256, pq_codes=FAKE, keys=None), INVALID),
+    (dict(pq_codebooks=FAKE, pq_m=16, pq_ksub=300, pq_codes=FAKE, keys=None), INVALID),
+])
+def test_build_ivf_index_rejects(lib, kw, status):
+    d = ivf_desc(**kw)
+    out = ctypes.c_void_p(1234)
+    assert lib.sense_build_ivf_index(ctypes.byref(d), None, ctypes.byref(out)) == status
+    assert out.value is None                          # cleared before validation fails
+    assert lib.sense_last_error_message()
+
+
+def test_ivf_search_rejects_null_index(lib):
+    size = ctypes.c_size_t()
+    assert lib.sense_ivf_search_workspace_size(None, 1, 64, 32, ctypes.byref(size)) == INVALID
+    assert lib.sense_ivf_search(None, p(FAKE), sense.SENSE_F32, 1, 64, 32, p(FAKE), p(FAKE),
+                                None, None, None, p(FAKE), 1 << 20, None) == INVALID
+    assert lib.sense_build_ivf_index(None, None, None) == INVALID
