@@ -189,6 +189,21 @@ struct IvfSearch {
 };
 hipError_t launch_ivf_search(const IvfSearch& s, hipStream_t stream);
 
+// Compute units of the current device, queried once per process (every GPU
+// this library drives is the same MI355X part).
+int device_cus();
+
+// Resident blocks of `kern` per compute unit at `threads` threads and no
+// dynamic LDS, or `fallback` when the query fails; callers keep it in a
+// function-local static (initialised once, also under concurrent calls).
+template <typename Kernel>
+int blocks_per_cu(Kernel kern, int threads, int fallback) {
+    int v = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, kern, threads, 0) != hipSuccess || v < 1)
+        v = fallback;
+    return v;
+}
+
 // The queries of a batch padded to qpad = 16*ceil(nq/16) rows and split
 // into hi + lo halves of the key type (a scratch of scan_mfma_scratch_bytes),
 // with inv_qn[q] = 1/||q|| (cosine), 1 (inner product), 0 (padding).

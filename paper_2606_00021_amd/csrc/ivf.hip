@@ -649,22 +649,9 @@ __global__ __launch_bounds__(kIvfThreads) void ivf_scan_pq_kernel(
     }
 }
 
-int cus() {
-    static int c = 0;
-    if (c == 0) {
-        int dev = 0;
-        hipDeviceProp_t prop;
-        c = (hipGetDevice(&dev) == hipSuccess && hipGetDeviceProperties(&prop, dev) == hipSuccess &&
-             prop.multiProcessorCount > 0)
-                ? prop.multiProcessorCount
-                : 256;
-    }
-    return c;
-}
-
 unsigned grid_for(int64_t n, int threads) {
     int64_t b = (n + threads - 1) / threads;
-    const int64_t cap = (int64_t)cus() * 16;
+    const int64_t cap = (int64_t)device_cus() * 16;
     if (b > cap) b = cap;
     return (unsigned)(b < 1 ? 1 : b);
 }
@@ -746,7 +733,7 @@ hipError_t launch_ivf_search(const IvfSearch& s, hipStream_t stream) {
     if (s.codes_sorted) {
         // Each block builds the query's tables once, so with many queries a
         // block takes several probes (about two blocks per compute unit).
-        int g = (2 * cus() + s.nq - 1) / s.nq;
+        int g = (2 * device_cus() + s.nq - 1) / s.nq;
         g = g < 1 ? 1 : (g > s.nprobe ? s.nprobe : g);
         const dim3 grid((unsigned)g, (unsigned)s.nq);
         const size_t lds = (size_t)s.m * s.ksub * sizeof(float);

@@ -33,13 +33,8 @@ __global__ __launch_bounds__(256) void stream_read_kernel(const u32x4* __restric
 }  // namespace
 
 hipError_t launch_stream_read(const void* buf, size_t bytes, uint32_t* sink, hipStream_t stream) {
-    int dev = 0, cus = 256;
-    hipDeviceProp_t prop;
-    if (hipGetDevice(&dev) == hipSuccess && hipGetDeviceProperties(&prop, dev) == hipSuccess &&
-        prop.multiProcessorCount > 0)
-        cus = prop.multiProcessorCount;
     const int64_t n16 = (int64_t)(bytes / 16);
-    hipLaunchKernelGGL(stream_read_kernel, dim3((unsigned)(cus * 8)), dim3(256), 0, stream,
+    hipLaunchKernelGGL(stream_read_kernel, dim3((unsigned)(device_cus() * 8)), dim3(256), 0, stream,
                        (const u32x4*)buf, n16, sink);
     return hipGetLastError();
 }

@@ -188,31 +188,12 @@ __global__ void query_to_f32_kernel(const uint16_t* __restrict__ q, int64_t coun
     }
 }
 
-int g_num_cus = 0;
-
-int num_cus() {
-    if (g_num_cus == 0) {
-        int dev = 0;
-        hipDeviceProp_t prop;
-        if (hipGetDevice(&dev) == hipSuccess &&
-            hipGetDeviceProperties(&prop, dev) == hipSuccess && prop.multiProcessorCount > 0)
-            g_num_cus = prop.multiProcessorCount;
-        else
-            g_num_cus = 256;
-    }
-    return g_num_cus;
-}
-
 template <int KT, int NC>
 hipError_t launch_gemv_nc(const void* keys, int64_t n, int d, int64_t ld, const float* query,
                           const float* inv_norm, float* scores, hipStream_t stream) {
     auto kern = scan_gemv_kernel<KT, NC>;
-    static int per_cu = 0;  // resident blocks per CU, queried once per instantiation
-    if (per_cu < 1 &&
-        (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, 256, 0) != hipSuccess ||
-         per_cu < 1))
-        per_cu = 2;
-    const int64_t max_blocks = (int64_t)num_cus() * per_cu;
+    static const int per_cu = blocks_per_cu(kern, 256, 2);
+    const int64_t max_blocks = (int64_t)device_cus() * per_cu;
     // Rows per wave: an equal share for a single resident wave of blocks,
     // never fewer than 8 rows.
     int64_t rpw = (n + max_blocks * 4 - 1) / (max_blocks * 4);
@@ -241,10 +222,22 @@ hipError_t launch_gemv(const void* keys, int64_t n, int d, int64_t ld, const flo
 
 }  // namespace
 
+int device_cus() {
+    static const int cus = [] {
+        int dev = 0;
+        hipDeviceProp_t prop;
+        if (hipGetDevice(&dev) == hipSuccess && hipGetDeviceProperties(&prop, dev) == hipSuccess &&
+            prop.multiProcessorCount > 0)
+            return prop.multiProcessorCount;
+        return 256;
+    }();
+    return cus;
+}
+
 hipError_t launch_key_norms(const void* keys, int key_dtype, int64_t n, int d, int64_t ld,
                             float* inv_norm, hipStream_t stream) {
     int64_t blocks = (n + 3) / 4;
-    const int64_t cap = (int64_t)num_cus() * 8;
+    const int64_t cap = (int64_t)device_cus() * 8;
     if (blocks > cap) blocks = cap;
     if (key_dtype == DT_BF16)
         hipLaunchKernelGGL(key_norms_kernel<DT_BF16>, dim3((unsigned)blocks), dim3(256), 0,

@@ -324,31 +324,15 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
     }
 }
 
-int g_cus = 0;
-int cus() {
-    if (g_cus == 0) {
-        int dev = 0;
-        hipDeviceProp_t prop;
-        g_cus = (hipGetDevice(&dev) == hipSuccess &&
-                 hipGetDeviceProperties(&prop, dev) == hipSuccess && prop.multiProcessorCount > 0)
-                    ? prop.multiProcessorCount
-                    : 256;
-    }
-    return g_cus;
-}
 
 template <int KT, int MT, int T, int P, bool SPLIT>
 hipError_t launch_tile(const void* keys, int64_t n, int d, int64_t ld, const uint16_t* qhi,
                        const uint16_t* qlo, const float* inv_qn, int nq, const float* inv_norm,
                        float* scores, hipStream_t stream) {
     auto kern = scan_mfma_kernel<KT, MT, T, P, SPLIT>;
-    static int per_cu = 0;
-    if (per_cu < 1 &&
-        (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, 256, 0) != hipSuccess ||
-         per_cu < 1))
-        per_cu = 1;
+    static const int per_cu = blocks_per_cu(kern, 256, 1);
     const int64_t nblk = (n + 64 * T - 1) / (64 * T);
-    const int64_t groups_max = (int64_t)cus() * per_cu;
+    const int64_t groups_max = (int64_t)device_cus() * per_cu;
     int64_t bpg = (nblk + groups_max - 1) / groups_max;
     if (bpg < 1) bpg = 1;
     const int64_t groups = (nblk + bpg - 1) / bpg;

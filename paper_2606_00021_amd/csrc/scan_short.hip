@@ -259,26 +259,9 @@ __global__ void short_tau_kernel(const int64_t* __restrict__ ids, const float* _
     counts[q] = slot_area;          // overflow entries follow the wave slots
 }
 
-int g_cus_short = 0;
-
 template <int KT, int NT, int KS, bool SPLIT, bool FILTER>
 hipError_t launch_variant(const ShortScan& s, hipStream_t stream) {
     auto kern = scan_short_kernel<KT, NT, KS, SPLIT, FILTER>;
-    static int per_cu = 0;
-    if (per_cu < 1 &&
-        (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, kShortThreads, 0) !=
-             hipSuccess ||
-         per_cu < 1))
-        per_cu = 2;
-    if (g_cus_short == 0) {
-        int dev = 0;
-        hipDeviceProp_t prop;
-        g_cus_short = (hipGetDevice(&dev) == hipSuccess &&
-                       hipGetDeviceProperties(&prop, dev) == hipSuccess &&
-                       prop.multiProcessorCount > 0)
-                          ? prop.multiProcessorCount
-                          : 256;
-    }
     const int64_t rpw = short_rows_per_wave(s.n_rows);
     const int64_t waves = (s.n_rows + rpw - 1) / rpw;
     const int64_t blocks = (waves + (kShortThreads / 64) - 1) / (kShortThreads / 64);
@@ -309,17 +292,8 @@ hipError_t launch_tiles(const ShortScan& s, hipStream_t stream) {
 }  // namespace
 
 int64_t short_rows_per_wave(int64_t n_rows) {
-    if (g_cus_short == 0) {
-        int dev = 0;
-        hipDeviceProp_t prop;
-        g_cus_short = (hipGetDevice(&dev) == hipSuccess &&
-                       hipGetDeviceProperties(&prop, dev) == hipSuccess &&
-                       prop.multiProcessorCount > 0)
-                          ? prop.multiProcessorCount
-                          : 256;
-    }
     // Two resident waves per SIMD (the kernels' register use allows two).
-    const int64_t waves_max = (int64_t)g_cus_short * 8;
+    const int64_t waves_max = (int64_t)device_cus() * 8;
     int64_t rpw = (n_rows + waves_max - 1) / waves_max;
     return (rpw + 16 * kShortDepth - 1) / (16 * kShortDepth) * (16 * kShortDepth);
 }

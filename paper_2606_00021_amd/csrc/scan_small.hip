@@ -155,27 +155,13 @@ __global__ __launch_bounds__(256) void scan_small_kernel(
     }
 }
 
-int g_cus = 0;
-
 template <int KT, int LPR>
 hipError_t launch_small_lpr(const void* keys, int64_t n, int d, int64_t ld, const float* query,
                             const float* inv_norm, float* scores, hipStream_t stream) {
     auto kern = scan_small_kernel<KT, LPR>;
-    static int per_cu = 0;
-    if (per_cu < 1 &&
-        (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, 256, 0) != hipSuccess ||
-         per_cu < 1))
-        per_cu = 2;
-    if (g_cus == 0) {
-        int dev = 0;
-        hipDeviceProp_t prop;
-        g_cus = (hipGetDevice(&dev) == hipSuccess &&
-                 hipGetDeviceProperties(&prop, dev) == hipSuccess && prop.multiProcessorCount > 0)
-                    ? prop.multiProcessorCount
-                    : 256;
-    }
+    static const int per_cu = blocks_per_cu(kern, 256, 2);
     constexpr int64_t rpit = kSmallLoads * (64 / LPR);
-    const int64_t max_waves = (int64_t)g_cus * per_cu * 4;
+    const int64_t max_waves = (int64_t)device_cus() * per_cu * 4;
     const int64_t row_blocks = (n + rpit - 1) / rpit;
     const int64_t waves = row_blocks < max_waves ? row_blocks : max_waves;
     const int64_t blocks = (waves + 3) / 4;
