@@ -13,9 +13,12 @@
 // takes 8 per thread, since every phase costs its per-thread key loop).
 // One reduction gives the number of real (non-padding) keys and the AND and
 // OR of them: the bits above the highest bit where they differ are shared by
-// all, so the radix select starts right below them (scores of one query
+// all, so the radix select starts right below them (survivors of a level
 // share their sign and most of their exponent, which a fixed top-down start
-// would spend a whole pass on).
+// would spend a whole pass on).  A chunk of raw scores holds both signs, so
+// the first level also bounds the k-th largest key from below by the
+// smallest of k or more group maxima and starts below the bits that this
+// bound and the largest key share: every key of the top k lies between them.
 // Each pass builds a 256-bin LDS histogram of the next 8-bit digit among the
 // keys that still match the chosen prefix, then one wave finds the digit
 // holding the k-th key with a suffix scan; the loop stops as soon as that
@@ -42,18 +45,38 @@ constexpr int kPer = kSelectChunk / kThreads;   // keys per thread
 
 // Real keys of the block (non-zero; a candidate buffer may hold padding keys
 // anywhere, so a chunk's length alone does not tell) and the AND / OR of
-// them.  All threads of the block must call it.
+// them.  With BOUND, also the score words (high 32 bits) of the largest key
+// and of a lower bound on the kk-th largest: the threads are cut into
+// G >= kk groups of g consecutive lanes, and `low` is the smallest of the G
+// group maxima.  Those maxima are G distinct keys (or one is the padding key
+// and low = 0), so at least kk keys are >= low; the score word of a maximum
+// (minimum) is the maximum (minimum) of the score words.  All threads of the
+// block must call it.
 struct ChunkStats {
     uint32_t nz;
     uint64_t all_and, any_or;
+    uint32_t low32, high32;
 };
 
-template <int T, int P>
-__device__ ChunkStats chunk_stats(const uint64_t (&key)[P], uint32_t* s_nzw, uint64_t* s_andw,
-                                  uint64_t* s_orw) {
+struct StatsLds {
+    uint32_t* nzw;
+    uint64_t* andw;
+    uint64_t* orw;
+    uint32_t* loww;
+    uint32_t* highw;
+};
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u(uint32_t x) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xF, 0xF, false);
+}
+
+template <int T, int P, bool BOUND>
+__device__ ChunkStats chunk_stats(const uint64_t (&key)[P], int kk, const StatsLds& L) {
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
     uint32_t nz = 0;
     uint64_t a = ~0ull, o = 0ull;
+    uint32_t mx = 0u;
 #pragma unroll
     for (int e = 0; e < P; ++e) {
         nz += (uint32_t)__popcll(__ballot(key[e] != 0));
@@ -61,25 +84,64 @@ __device__ ChunkStats chunk_stats(const uint64_t (&key)[P], uint32_t* s_nzw, uin
             a &= key[e];
             o |= key[e];
         }
+        if constexpr (BOUND) {
+            const uint32_t h = (uint32_t)(key[e] >> 32);
+            mx = h > mx ? h : mx;
+        }
     }
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
         a &= __shfl_xor(a, off, 64);
         o |= __shfl_xor(o, off, 64);
     }
+    uint32_t lo = 0u, hi = 0u;
+    if constexpr (BOUND) {
+        // Group size g: the largest power of two <= 64 with T / g >= kk; none
+        // (low = 0) when kk > T.  One max ladder over groups of 2, 4, ..., 64
+        // lanes (quad swaps, half-row and row mirrors, then xor 16 and 32),
+        // keeping the group maxima at size g; then the min ladder of those.
+        const int gq = T / (kk > 0 ? kk : 1);
+        const int g = gq >= 64 ? 64 : (gq > 0 ? 1 << (31 - __clz(gq)) : 0);
+        uint32_t v = mx, gm = (g == 1) ? mx : 0u;
+        auto mxs = [](uint32_t x, uint32_t y) { return x > y ? x : y; };
+        auto mns = [](uint32_t x, uint32_t y) { return x < y ? x : y; };
+        v = mxs(v, dpp_u<0xB1>(v));  gm = (g == 2) ? v : gm;
+        v = mxs(v, dpp_u<0x4E>(v));  gm = (g == 4) ? v : gm;
+        v = mxs(v, dpp_u<0x141>(v)); gm = (g == 8) ? v : gm;
+        v = mxs(v, dpp_u<0x140>(v)); gm = (g == 16) ? v : gm;
+        v = mxs(v, (uint32_t)__shfl_xor((int)v, 16, 64)); gm = (g == 32) ? v : gm;
+        v = mxs(v, (uint32_t)__shfl_xor((int)v, 32, 64)); gm = (g == 64) ? v : gm;
+        hi = v;
+        lo = gm;
+        lo = mns(lo, dpp_u<0xB1>(lo));
+        lo = mns(lo, dpp_u<0x4E>(lo));
+        lo = mns(lo, dpp_u<0x141>(lo));
+        lo = mns(lo, dpp_u<0x140>(lo));
+        lo = mns(lo, (uint32_t)__shfl_xor((int)lo, 16, 64));
+        lo = mns(lo, (uint32_t)__shfl_xor((int)lo, 32, 64));
+    }
     if (lane == 0) {
-        s_nzw[wv] = nz;
-        s_andw[wv] = a;
-        s_orw[wv] = o;
+        L.nzw[wv] = nz;
+        L.andw[wv] = a;
+        L.orw[wv] = o;
+        if constexpr (BOUND) {
+            L.loww[wv] = lo;
+            L.highw[wv] = hi;
+        }
     }
     __syncthreads();
-    ChunkStats r{0u, ~0ull, 0ull};
+    ChunkStats r{0u, ~0ull, 0ull, ~0u, 0u};
 #pragma unroll
     for (int w = 0; w < T / 64; ++w) {
-        r.nz += s_nzw[w];
-        r.all_and &= s_andw[w];
-        r.any_or |= s_orw[w];
+        r.nz += L.nzw[w];
+        r.all_and &= L.andw[w];
+        r.any_or |= L.orw[w];
+        if constexpr (BOUND) {
+            r.low32 = L.loww[w] < r.low32 ? L.loww[w] : r.low32;
+            r.high32 = L.highw[w] > r.high32 ? L.highw[w] : r.high32;
+        }
     }
+    if constexpr (!BOUND) r.low32 = r.high32 = 0u;
     return r;
 }
 
@@ -94,7 +156,7 @@ __device__ ChunkStats chunk_stats(const uint64_t (&key)[P], uint32_t* s_nzw, uin
 // plain LDS atomics (starting below the shared bits spreads the keys over
 // the digit values, so same-address collisions inside an instruction stay
 // few).
-template <int T, int P>
+template <int T, int P, bool BOUND>
 __device__ SelectState radix_select(const uint64_t (&key)[P], int need, const ChunkStats& cs,
                                     uint32_t* s_hist, uint32_t* s_tot, uint32_t* s_info) {
     const int tid = threadIdx.x;
@@ -102,10 +164,21 @@ __device__ SelectState radix_select(const uint64_t (&key)[P], int need, const Ch
     uint32_t* my = s_hist + wv * 256;
     const uint64_t diff = cs.all_and ^ cs.any_or;
     if (diff == 0) return SelectState{cs.all_and, ~0ull};   // every real key is the same
-    const int hb = 63 - __clzll((long long)diff);
-    // Bits above hb are common to every real key (2 << 63 wraps to 0: no bits).
+    // Bits above hb are common to every real key (2 << 63 wraps to 0: no
+    // bits).  With BOUND they are also common to every key in [low, high],
+    // which holds the need largest: the score-word bits above the highest
+    // one where low and high differ (the whole score word if none does).
+    int hb = 63 - __clzll((long long)diff);
+    if constexpr (BOUND) {
+        const uint32_t span = cs.low32 ^ cs.high32;
+        const int hs = span ? 63 - __clz(span) : 31;
+        hb = hs < hb ? hs : hb;
+    }
     uint64_t mask = ~((2ull << hb) - 1ull);
-    uint64_t prefix = cs.all_and & mask;
+    // Above bit 31 the bits are the largest key's score word; below, every
+    // real key shares them (hb < 31 only when all share the score word).
+    uint64_t prefix = (BOUND ? (((uint64_t)cs.high32 << 32) | (cs.all_and & 0xFFFFFFFFull))
+                             : cs.all_and) & mask;
     for (int b = tid; b < (T / 64) * 256; b += T) s_hist[b] = 0;
     __syncthreads();
     for (int hi = hb; hi >= 0; hi -= 8) {
@@ -287,6 +360,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
     __shared__ uint32_t s_info[4];
     __shared__ uint32_t s_nzw[kWaves], s_wc[kWaves];
     __shared__ uint64_t s_andw[kWaves], s_orw[kWaves];
+    __shared__ uint32_t s_loww[kWaves], s_highw[kWaves];
 
     constexpr int CH = kThreads * P;
     const int tid = threadIdx.x;
@@ -335,13 +409,18 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
             key[e] = i < len ? in_keys[(int64_t)q * count + start + i] : 0;
         }
     }
-    const ChunkStats cs = chunk_stats<kThreads, P>(key, s_nzw, s_andw, s_orw);
+    // The group-maxima bound pays where a chunk holds raw scores of both
+    // signs (its keys share no leading bits); later levels hold survivors
+    // that already share them.
+    constexpr bool kBound = FROM_SCORES && !FINAL;
+    const ChunkStats cs =
+        chunk_stats<kThreads, P, kBound>(key, kk, StatsLds{s_nzw, s_andw, s_orw, s_loww, s_highw});
 
     // Keys taken: every real one if there are no more than kk, else the kk
     // largest (then more than kk keys are real, as the radix select needs).
     SelectState st{0, 0};
     const bool all = cs.nz <= (uint32_t)kk;
-    if (!all) st = radix_select<kThreads, P>(key, kk, cs, s_hist, s_tot, s_info);
+    if (!all) st = radix_select<kThreads, P, kBound>(key, kk, cs, s_hist, s_tot, s_info);
     auto taken = [&](int e) {
         return all ? (key[e] != 0) : ((key[e] & st.mask) >= st.prefix);
     };
@@ -406,10 +485,12 @@ __device__ int stream_rounds(const uint64_t* __restrict__ src, int64_t count, in
             else if (i - nt >= take) key[e] = 0;
         }
         __syncthreads();                               // s_sel read before it is rewritten
-        const ChunkStats cs = chunk_stats<kStreamThreads, P>(key, L.s_nzw, L.s_andw, L.s_orw);
+        const ChunkStats cs = chunk_stats<kStreamThreads, P, false>(
+            key, kk, StatsLds{L.s_nzw, L.s_andw, L.s_orw, nullptr, nullptr});
         SelectState st{0, 0};
         const bool all = cs.nz <= (uint32_t)kk;
-        if (!all) st = radix_select<kStreamThreads, P>(key, kk, cs, L.s_hist, L.s_tot, L.s_info);
+        if (!all)
+            st = radix_select<kStreamThreads, P, false>(key, kk, cs, L.s_hist, L.s_tot, L.s_info);
         auto taken = [&](int e) {
             return all ? (key[e] != 0) : ((key[e] & st.mask) >= st.prefix);
         };

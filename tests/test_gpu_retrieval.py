@@ -124,6 +124,62 @@ def test_batched_key_typed_queries():
     index.close()
 
 
+def _exact_score_columns(n, rng):
+    """Eight score patterns, one per key column, each exactly representable in
+    bf16: mixed signs with many ties, one value for every row, a narrow
+    positive band, five levels including zero, a wide exponent range,
+    negatives only, four integers, and scores rising with the row."""
+    cols = [
+        rng.normal(0.0, 0.05, n),
+        np.full(n, 0.25),
+        0.1 + rng.normal(0.0, 1e-3, n),
+        rng.choice([-1.0, -0.5, 0.0, 0.5, 1.0], n),
+        np.clip(rng.standard_cauchy(n), -1e30, 1e30),
+        -np.abs(rng.normal(0.0, 1.0, n)),
+        rng.integers(0, 4, n).astype(np.float64),
+        np.arange(n, dtype=np.float64) / n,
+    ]
+    return torch.tensor(np.stack(cols, axis=1), dtype=torch.float32).to(torch.bfloat16)
+
+
+@pytest.mark.parametrize("n,k,nq", [
+    (3 * 8192 + 777, 1, 8),      # selection levels over raw scores, group size 64
+    (3 * 8192 + 777, 64, 8),     # groups of 8 lanes
+    (3 * 8192 + 777, 100, 2),    # groups of 4 lanes, the single-query scan
+    (5 * 8192 - 3, 600, 8),      # k above the threads of a block: no group bound
+    (5 * 8192 - 3, 1024, 1),     # two levels of 1024-key survivors
+    (8192, 64, 8),               # one chunk
+])
+def test_exact_scores_select_exactly(n, k, nq):
+    """Inner products of one-hot fp32 queries with bf16 keys are exact, so the
+    top-k (score descending, row ascending) and the drafts must equal the
+    oracle's exactly, ties included, with no near-tie allowance."""
+    print(f"[case] exact scores n={n} k={k} nq={nq}", flush=True)
+    rng = np.random.default_rng(zlib.crc32(f"exact-{n}-{k}-{nq}".encode()))
+    d = 128
+    keys = torch.zeros(n, d, dtype=torch.bfloat16)
+    keys[:, :8] = _exact_score_columns(n, rng)
+    q = torch.zeros(nq, d, dtype=torch.float32)
+    for i in range(nq):
+        q[i, i % 8] = 1.0
+    spans = torch.tensor(rng.integers(0, 32000, (n, 8)), dtype=torch.int32)
+    span_len = torch.tensor(rng.integers(0, 9, n), dtype=torch.int32)
+    index = sense.sense_build_index(keys.to(DEV), spans.to(DEV), span_len.to(DEV), metric="ip")
+    ids, scores, drafts, dlen = sense.sense_retrieve(index, q.to(DEV), k)
+    torch.cuda.synchronize()
+    o_s = oracle.scores(host_bits(keys), "bf16", q.numpy(), "f32", metric="ip", key_stride=d, d=d)
+    ids_h, sc_h = ids.cpu().numpy(), scores.cpu().numpy()
+    dr_h, dl_h = drafts.cpu().numpy(), dlen.cpu().numpy()
+    for qi in range(nq):
+        o_ids, o_sc = oracle.topk(o_s[qi], k)
+        assert np.array_equal(ids_h[qi], o_ids), f"query {qi} (column {qi % 8}): ids differ"
+        assert np.array_equal(sc_h[qi].astype(np.float64), o_sc), f"query {qi}: scores differ"
+        o_dr, o_dl = oracle.gather(spans.numpy(), span_len.numpy(), ids_h[qi])
+        assert np.array_equal(dr_h[qi], o_dr) and np.array_equal(dl_h[qi], o_dl)
+    index.close()
+    print("[case] ok", flush=True)
+
+
 def test_planted_exact_copy_ranks_first():
     w = synth.scaled(synth.WORKLOADS["tiny-16k-d4096"], n=12345, d=768, k=4, n_clusters=48)
     ds = synth.make_datastore(w, 3, DEV)
