@@ -142,21 +142,29 @@ def _exact_score_columns(n, rng):
     return torch.tensor(np.stack(cols, axis=1), dtype=torch.float32).to(torch.bfloat16)
 
 
-@pytest.mark.parametrize("n,k,nq", [
-    (3 * 8192 + 777, 1, 8),      # selection levels over raw scores, group size 64
-    (3 * 8192 + 777, 64, 8),     # groups of 8 lanes
-    (3 * 8192 + 777, 100, 2),    # groups of 4 lanes, the single-query scan
-    (5 * 8192 - 3, 600, 8),      # k above the threads of a block: no group bound
-    (5 * 8192 - 3, 1024, 1),     # two levels of 1024-key survivors
-    (8192, 64, 8),               # one chunk
+@pytest.mark.parametrize("n,k,nq,d", [
+    (3 * 8192 + 777, 1, 8, 128),      # selection levels over raw scores, group size 64
+    (3 * 8192 + 777, 64, 8, 128),     # groups of 8 lanes
+    (3 * 8192 + 777, 100, 2, 128),    # groups of 4 lanes, the single-query scan
+    (5 * 8192 - 3, 600, 8, 128),      # k above the threads of a block: no group bound
+    (5 * 8192 - 3, 1024, 1, 128),     # two levels of 1024-key survivors
+    (8192, 64, 8, 128),               # one chunk
+    # short keys: one query (short-row scan), a batch over a direct store
+    # (n <= 131072), and batches whose threshold comes from a strided sample's
+    # k-th best key, so that ties at the threshold decide the survivors
+    (140_007, 100, 1, 64),
+    (100_000, 64, 8, 64),
+    (140_007, 64, 8, 64),
+    (140_007, 1, 8, 16),
+    (140_007, 1024, 8, 64),
+    (300_001, 64, 64, 32),
 ])
-def test_exact_scores_select_exactly(n, k, nq):
+def test_exact_scores_select_exactly(n, k, nq, d):
     """Inner products of one-hot fp32 queries with bf16 keys are exact, so the
     top-k (score descending, row ascending) and the drafts must equal the
     oracle's exactly, ties included, with no near-tie allowance."""
-    print(f"[case] exact scores n={n} k={k} nq={nq}", flush=True)
-    rng = np.random.default_rng(zlib.crc32(f"exact-{n}-{k}-{nq}".encode()))
-    d = 128
+    print(f"[case] exact scores n={n} k={k} nq={nq} d={d}", flush=True)
+    rng = np.random.default_rng(zlib.crc32(f"exact-{n}-{k}-{nq}-{d}".encode()))
     keys = torch.zeros(n, d, dtype=torch.bfloat16)
     keys[:, :8] = _exact_score_columns(n, rng)
     q = torch.zeros(nq, d, dtype=torch.float32)
