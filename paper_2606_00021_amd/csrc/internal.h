@@ -129,13 +129,14 @@ hipError_t launch_project(const void* x, int x_dtype, int64_t n, int d_in, int64
                           hipStream_t stream);
 
 // Top-k of packed keys (nq x count, padding key 0) in the order of the
-// keys, with the gather; ids of padding keys are -1.  dev_count (optional,
-// device): query q has only its first dev_count[q] <= count keys.
+// keys, with the gather; ids of padding keys are -1.  Query q has only its
+// first dev_count[q] <= count keys (dev_count: nq counts on the device).  No
+// workspace.
 hipError_t launch_topk_keys(const uint64_t* keys, int64_t count, int nq, int k,
                             const int32_t* spans, const int32_t* span_len, int max_span,
                             int64_t span_stride, int64_t* out_ids, float* out_scores,
-                            int32_t* out_drafts, int32_t* out_draft_len, void* workspace,
-                            hipStream_t stream, const int32_t* dev_count = nullptr);
+                            int32_t* out_drafts, int32_t* out_draft_len,
+                            const int32_t* dev_count, hipStream_t stream);
 
 // Inverted file (ivf.hip).
 hipError_t launch_ivf_assign(const void* keys, int key_dtype, int64_t n, int d, int64_t ld,
@@ -185,7 +186,6 @@ struct IvfSearch {
     float* out_scores;
     int32_t* out_drafts;
     int32_t* out_draft_len;
-    void* final_ws;
 };
 hipError_t launch_ivf_search(const IvfSearch& s, hipStream_t stream);
 

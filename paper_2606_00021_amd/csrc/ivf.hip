@@ -785,7 +785,7 @@ hipError_t launch_ivf_search(const IvfSearch& s, hipStream_t stream) {
     if ((e = hipGetLastError()) != hipSuccess) return e;
     return launch_topk_keys(s.cand, s.cap, s.nq, s.k, s.spans, s.span_len, s.max_span,
                             s.span_stride, s.out_ids, s.out_scores, s.out_drafts,
-                            s.out_draft_len, s.final_ws, stream, s.count);
+                            s.out_draft_len, s.count, stream);
 }
 
 }  // namespace sense

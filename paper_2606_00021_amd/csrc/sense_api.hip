@@ -465,8 +465,8 @@ static hipError_t retrieve_short(const sense_index* ix, const float* qptr, int n
         S.cap = slot_area + n;
         if ((e = sense::launch_scan_short(S, st)) != hipSuccess) return e;
         if ((e = sense::launch_topk_keys(S.cand, S.cap, ng, k, ix->spans, ix->span_len,
-                                         ix->max_span, ix->span_stride, gid, gsc, gdr, gdl,
-                                         ws + L.fws_off, st, cnt)) != hipSuccess)
+                                         ix->max_span, ix->span_stride, gid, gsc, gdr, gdl, cnt,
+                                         st)) != hipSuccess)
             return e;
     }
     return timer_mark(SENSE_TIMER_SCAN, 1, st);
@@ -1023,7 +1023,7 @@ SENSE_EXPORT sense_status_t sense_build_ivf_index(const sense_ivf_desc_t* desc, 
 namespace {
 
 struct IvfLayout {
-    size_t q_off, coarse_off, ip_off, probe_off, pws_off, cnt_off, cand_off, fws_off, total;
+    size_t q_off, coarse_off, ip_off, probe_off, pws_off, cnt_off, cand_off, total;
     int64_t cap;
 };
 
@@ -1045,7 +1045,6 @@ IvfLayout ivf_layout(const sense_index* ix, int nq, int k, int nprobe) {
     l.pws_off = take(sense::topk_workspace_bytes(ix->nlist, nq, nprobe));
     l.cnt_off = take((size_t)nq * sizeof(int32_t));
     l.cand_off = take((size_t)nq * cap * sizeof(uint64_t));
-    l.fws_off = take(sense::topk_workspace_bytes(cap, nq, k));
     l.total = at;
     return l;
 }
@@ -1137,7 +1136,6 @@ SENSE_EXPORT sense_status_t sense_ivf_search(const sense_index_t* ix, const void
     S.out_scores = out_scores;
     S.out_drafts = out_drafts;
     S.out_draft_len = out_draft_len;
-    S.final_ws = ws + L.fws_off;
     if ((e = timer_mark(SENSE_TIMER_IVF, 0, st)) != hipSuccess) return hip_fail(e, "timer");
     if ((e = sense::launch_ivf_search(S, st)) != hipSuccess) return hip_fail(e, "ivf search");
     if ((e = timer_mark(SENSE_TIMER_IVF, 1, st)) != hipSuccess) return hip_fail(e, "timer");

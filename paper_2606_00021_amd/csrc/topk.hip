@@ -351,8 +351,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
     int k, uint64_t* __restrict__ out_keys, int64_t* __restrict__ out_ids,
     float* __restrict__ out_scores, int32_t* __restrict__ out_drafts,
     int32_t* __restrict__ out_draft_len, const int32_t* __restrict__ spans,
-    const int32_t* __restrict__ span_len, int max_span, int64_t span_stride,
-    const int32_t* __restrict__ dev_count, int32_t* __restrict__ next_count) {
+    const int32_t* __restrict__ span_len, int max_span, int64_t span_stride) {
     __shared__ uint64_t s_sel[kMaxK];
     __shared__ uint64_t s_sorted[FINAL ? kMaxK : 1];
     __shared__ uint32_t s_hist[kWaves * 256];
@@ -366,19 +365,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
     const int tid = threadIdx.x;
     const int q = blockIdx.y;
     const int64_t start = (int64_t)blockIdx.x * CH;
-    // dev_count: a per-query count on the device (at most count).
-    const int64_t cnt_q = (dev_count && dev_count[q] < count) ? dev_count[q] : count;
-    const int64_t remain = cnt_q - start;
-    if constexpr (!FINAL) {
-        // With device counts the next level reads only the chunks that hold
-        // keys: their number is published, and empty chunks write nothing.
-        if (dev_count) {
-            const int kk0 = k < CH ? k : CH;
-            if (blockIdx.x == 0 && threadIdx.x == 0)
-                next_count[q] = (int32_t)(((cnt_q + CH - 1) / CH) * kk0);
-            if (remain <= 0) return;                 // uniform over the block
-        }
-    }
+    const int64_t remain = count - start;
     const int len = (int)(remain < CH ? remain : CH);
     const int kk = k < CH ? k : CH;
 
@@ -541,17 +528,15 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 void launch_final_keys(const uint64_t* keys, int64_t count, int nq, int k, const int32_t* spans,
                        const int32_t* span_len, int max_span, int64_t span_stride,
                        int64_t* out_ids, float* out_scores, int32_t* out_drafts,
-                       int32_t* out_draft_len, const int32_t* counts, hipStream_t stream) {
+                       int32_t* out_draft_len, hipStream_t stream) {
     if (count <= (int64_t)kThreads * 8)
         hipLaunchKernelGGL((select_kernel<false, true, 8>), dim3(1, nq), dim3(kThreads), 0,
                            stream, nullptr, keys, count, k, nullptr, out_ids, out_scores,
-                           out_drafts, out_draft_len, spans, span_len, max_span, span_stride,
-                           counts, nullptr);
+                           out_drafts, out_draft_len, spans, span_len, max_span, span_stride);
     else
         hipLaunchKernelGGL((select_kernel<false, true, kPer>), dim3(1, nq), dim3(kThreads), 0,
                            stream, nullptr, keys, count, k, nullptr, out_ids, out_scores,
-                           out_drafts, out_draft_len, spans, span_len, max_span, span_stride,
-                           counts, nullptr);
+                           out_drafts, out_draft_len, spans, span_len, max_span, span_stride);
 }
 
 }  // namespace
@@ -568,8 +553,7 @@ size_t topk_workspace_bytes(int64_t n, int nq, int k) {
     if (chunks <= 1) return 0;
     const int64_t kk = k < kSelectChunk ? k : kSelectChunk;
     const size_t one = (size_t)nq * (size_t)chunks * (size_t)kk * sizeof(uint64_t);
-    // two key buffers, then two per-query count buffers (device-count inputs)
-    return 2 * ((one + 255) / 256 * 256) + 2 * (((size_t)nq * 4 + 255) / 256 * 256);
+    return 2 * ((one + 255) / 256 * 256);                // the two key buffers
 }
 
 hipError_t launch_topk_gather(const float* scores, int64_t n, int nq, int k,
@@ -583,20 +567,18 @@ hipError_t launch_topk_gather(const float* scores, int64_t n, int nq, int k,
         if (n <= (int64_t)kThreads * 8)
             hipLaunchKernelGGL((select_kernel<true, true, 8>), dim3(1, nq), dim3(kThreads), 0,
                                stream, scores, nullptr, n, k, nullptr, out_ids, out_scores,
-                               out_drafts, out_draft_len, spans, span_len, max_span, span_stride,
-                               nullptr, nullptr);
+                               out_drafts, out_draft_len, spans, span_len, max_span, span_stride);
         else
             hipLaunchKernelGGL((select_kernel<true, true, kPer>), dim3(1, nq), dim3(kThreads), 0,
                                stream, scores, nullptr, n, k, nullptr, out_ids, out_scores,
-                               out_drafts, out_draft_len, spans, span_len, max_span, span_stride,
-                               nullptr, nullptr);
+                               out_drafts, out_draft_len, spans, span_len, max_span, span_stride);
         return hipGetLastError();
     }
     const size_t one = key_buffer_bytes(n, nq, k);
     uint64_t* buf[2] = {(uint64_t*)workspace, (uint64_t*)((char*)workspace + one)};
     hipLaunchKernelGGL((select_kernel<true, false, kPer>), dim3((unsigned)chunks, nq), dim3(kThreads),
                        0, stream, scores, nullptr, n, k, buf[0], nullptr, nullptr, nullptr,
-                       nullptr, nullptr, nullptr, 0, 0, nullptr, nullptr);
+                       nullptr, nullptr, nullptr, 0, 0);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     int64_t count = chunks * kk;
@@ -604,59 +586,25 @@ hipError_t launch_topk_gather(const float* scores, int64_t n, int nq, int k,
     while ((chunks = ceil_div(count, kSelectChunk)) > 1) {
         hipLaunchKernelGGL((select_kernel<false, false, kPer>), dim3((unsigned)chunks, nq),
                            dim3(kThreads), 0, stream, nullptr, buf[cur], count, k, buf[cur ^ 1],
-                           nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 0, 0, nullptr,
-                           nullptr);
+                           nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 0, 0);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         count = chunks * kk;
         cur ^= 1;
     }
     launch_final_keys(buf[cur], count, nq, k, spans, span_len, max_span, span_stride, out_ids,
-                      out_scores, out_drafts, out_draft_len, nullptr, stream);
+                      out_scores, out_drafts, out_draft_len, stream);
     return hipGetLastError();
 }
 
 hipError_t launch_topk_keys(const uint64_t* keys, int64_t count, int nq, int k,
                             const int32_t* spans, const int32_t* span_len, int max_span,
                             int64_t span_stride, int64_t* out_ids, float* out_scores,
-                            int32_t* out_drafts, int32_t* out_draft_len, void* workspace,
-                            hipStream_t stream, const int32_t* dev_count) {
-    const int64_t kk = k < kSelectChunk ? k : kSelectChunk;
-    int64_t chunks = ceil_div(count, kSelectChunk);
-    const uint64_t* cur_in = keys;
-    int64_t cur_count = count;
-    const size_t one = key_buffer_bytes(count, nq, k);
-    uint64_t* buf[2] = {(uint64_t*)workspace, (uint64_t*)((char*)workspace + one)};
-    int cur = 0;
-    hipError_t e;
-    // Per-query counts on the device, level by level (ping-pong after the
-    // key buffers).
-    int32_t* cnt_buf[2] = {(int32_t*)((char*)workspace + 2 * one),
-                           (int32_t*)((char*)workspace + 2 * one + ((size_t)nq * 4 + 255) / 256 * 256)};
-    if (dev_count) {
-        // One block per query walks its own count.
-        hipLaunchKernelGGL(select_stream_kernel, dim3(nq), dim3(kStreamThreads), 0, stream, keys,
-                           count, k, dev_count, out_ids, out_scores, out_drafts, out_draft_len,
-                           spans, span_len, max_span, span_stride);
-        return hipGetLastError();
-    }
-    const int32_t* counts = dev_count;
-    int cc = 0;
-    while (chunks > 1) {
-        int32_t* next = counts ? cnt_buf[cc] : nullptr;
-        hipLaunchKernelGGL((select_kernel<false, false, kPer>), dim3((unsigned)chunks, nq),
-                           dim3(kThreads), 0, stream, nullptr, cur_in, cur_count, k, buf[cur],
-                           nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 0, 0, counts,
-                           next);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-        counts = next;
-        cc ^= 1;
-        cur_in = buf[cur];
-        cur_count = chunks * kk;
-        cur ^= 1;
-        chunks = ceil_div(cur_count, kSelectChunk);
-    }
-    launch_final_keys(cur_in, cur_count, nq, k, spans, span_len, max_span, span_stride, out_ids,
-                      out_scores, out_drafts, out_draft_len, counts, stream);
+                            int32_t* out_drafts, int32_t* out_draft_len,
+                            const int32_t* dev_count, hipStream_t stream) {
+    // One block per query walks its own count.
+    hipLaunchKernelGGL(select_stream_kernel, dim3(nq), dim3(kStreamThreads), 0, stream, keys,
+                       count, k, dev_count, out_ids, out_scores, out_drafts, out_draft_len, spans,
+                       span_len, max_span, span_stride);
     return hipGetLastError();
 }
 
