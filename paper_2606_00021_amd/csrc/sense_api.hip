@@ -1027,7 +1027,7 @@ struct IvfLayout {
     int64_t cap;
 };
 
-IvfLayout ivf_layout(const sense_index* ix, int nq, int k, int nprobe) {
+IvfLayout ivf_layout(const sense_index* ix, int nq, int nprobe) {
     IvfLayout l;
     int64_t cap = ix->cap_prefix[nprobe];
     if (cap < 1) cap = 1;
@@ -1070,7 +1070,7 @@ SENSE_EXPORT sense_status_t sense_ivf_search_workspace_size(const sense_index_t*
     if (!bytes) return fail(SENSE_ERR_INVALID_ARGUMENT, "bytes is NULL");
     const sense_status_t s = check_ivf_search(ix, nq, k, nprobe);
     if (s != SENSE_OK) return s;
-    *bytes = ivf_layout(ix, nq, k, nprobe).total;
+    *bytes = ivf_layout(ix, nq, nprobe).total;
     return ok();
 }
 
@@ -1087,7 +1087,7 @@ SENSE_EXPORT sense_status_t sense_ivf_search(const sense_index_t* ix, const void
     if (!dtype_ok(q_dtype)) return fail(SENSE_ERR_INVALID_ARGUMENT, "unknown q_dtype %d", (int)q_dtype);
     if (!aligned(queries, q_dtype == SENSE_F32 ? 16 : 2))
         return fail(SENSE_ERR_MISALIGNED, "fp32 queries must be 16-byte aligned");
-    const IvfLayout L = ivf_layout(ix, nq, k, nprobe);
+    const IvfLayout L = ivf_layout(ix, nq, nprobe);
     if (!workspace || workspace_bytes < L.total)
         return fail(SENSE_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", L.total,
                     workspace ? workspace_bytes : (size_t)0);
