@@ -188,6 +188,44 @@ def test_exact_scores_select_exactly(n, k, nq, d):
     print("[case] ok", flush=True)
 
 
+@pytest.mark.parametrize("n,k,nq,d,n_finite", [
+    (40, 40, 1, 128, 35),                 # k = n: every NaN row is returned
+    (3 * 8192 + 777, 1024, 8, 128, 600),  # NaN rows fill the tail, matrix-core scan
+    (3 * 8192 + 777, 1024, 2, 128, 600),  # the same through the single-query scan
+    (140_007, 64, 8, 64, 30),             # short keys: the sampled threshold is a NaN key
+])
+def test_nan_scores_rank_last_by_row(n, k, nq, d, n_finite):
+    """Rows whose score is NaN rank after every number, among themselves by
+    row, and are reported with a NaN score; the other rows are exact."""
+    print(f"[case] NaN rows n={n} k={k} nq={nq} d={d} finite={n_finite}", flush=True)
+    rng = np.random.default_rng(zlib.crc32(f"nan-{n}-{k}-{nq}-{d}".encode()))
+    keys = torch.zeros(n, d, dtype=torch.bfloat16)
+    vals = torch.full((n, 8), float("nan"))
+    fin = rng.choice(n, n_finite, replace=False)
+    vals[fin] = torch.tensor(rng.normal(0.0, 1.0, (n_finite, 8)), dtype=torch.float32)
+    keys[:, :8] = vals.to(torch.bfloat16)
+    q = torch.zeros(nq, d, dtype=torch.float32)
+    for i in range(nq):
+        q[i, i % 8] = 1.0
+    spans = torch.tensor(rng.integers(0, 32000, (n, 4)), dtype=torch.int32)
+    index = sense.sense_build_index(keys.to(DEV), spans.to(DEV), None, metric="ip")
+    ids, scores, drafts, dlen = sense.sense_retrieve(index, q.to(DEV), k)
+    torch.cuda.synchronize()
+    o_s = oracle.scores(host_bits(keys), "bf16", q.numpy(), "f32", metric="ip", key_stride=d, d=d)
+    ids_h, sc_h = ids.cpu().numpy(), scores.cpu().numpy().astype(np.float64)
+    dr_h, dl_h = drafts.cpu().numpy(), dlen.cpu().numpy()
+    for qi in range(nq):
+        o_ids, o_sc = oracle.topk(o_s[qi], k)
+        assert np.array_equal(ids_h[qi], o_ids), f"query {qi}: ids differ"
+        nan = np.isnan(o_sc)
+        assert nan.sum() == k - min(k, n_finite)
+        assert np.array_equal(np.isnan(sc_h[qi]), nan) and np.array_equal(sc_h[qi][~nan], o_sc[~nan])
+        o_dr, o_dl = oracle.gather(spans.numpy(), None, ids_h[qi])
+        assert np.array_equal(dr_h[qi], o_dr) and np.array_equal(dl_h[qi], o_dl)
+    index.close()
+    print("[case] ok", flush=True)
+
+
 def test_planted_exact_copy_ranks_first():
     w = synth.scaled(synth.WORKLOADS["tiny-16k-d4096"], n=12345, d=768, k=4, n_clusters=48)
     ds = synth.make_datastore(w, 3, DEV)
