@@ -66,6 +66,9 @@ SMALL = [
     ("k1024-n4096", 4096, 128, "f16", 1024),
     # a final level of 5 x 1024 keys (more than 4096: sixteen per thread)
     ("k1024-5chunks", 5 * 8192 - 3, 128, "bf16", 1024),
+    # two full selection chunks; then a last chunk of a single score
+    ("two-chunks-16384", 16384, 256, "bf16", 64),
+    ("last-chunk-of-one-16385", 16385, 256, "f16", 64),
 ]
 
 
@@ -149,6 +152,8 @@ def _exact_score_columns(n, rng):
     (5 * 8192 - 3, 600, 8, 128),      # k above the threads of a block: no group bound
     (5 * 8192 - 3, 1024, 1, 128),     # two levels of 1024-key survivors
     (8192, 64, 8, 128),               # one chunk
+    (16384, 64, 8, 128),              # two full chunks
+    (16385, 1024, 2, 128),            # a last chunk of one score
     # short keys: one query (short-row scan), a batch over a direct store
     # (n <= 131072), and batches whose threshold comes from a strided sample's
     # k-th best key, so that ties at the threshold decide the survivors
