@@ -12,10 +12,10 @@
 // last drafts (a draft of length 0 then has length 1), so both start with the
 // model's greedy token.
 //
-// One block per query.  The pool is at most kMaxPool members, so the whole
-// ranking is one bitonic sort of packed 64-bit keys (score bits, complemented
-// position) in LDS; the gather copies the chosen rows with one thread per
-// output token.
+// One block per query.  The pool is at most kMaxPool members, ranked as
+// packed 64-bit keys (score bits, complemented position) in LDS: up to 256
+// members by rank (each counts the members above it), more by a bitonic
+// sort; the gather copies the chosen rows, one thread per output token.
 #include "internal.h"
 
 namespace sense {
@@ -37,44 +37,84 @@ __global__ __launch_bounds__(kSelThreads) void select_candidates_kernel(
     while (p < n_all) p <<= 1;
     const int32_t anchor = anchors[q];
 
+    // Member i's row: static hits first, then the dynamic ones.  Loads are
+    // unconditional (a missing length table reads the draft's first token,
+    // a valid address, and is then ignored), so each thread's loads are in
+    // flight together.
+    auto member = [&](int i, int64_t& row, const int32_t*& dsrc, int& len) {
+        const bool dyn = i >= n_s;
+        row = (int64_t)q * (dyn ? n_d : n_s) + (dyn ? i - n_s : i);
+        dsrc = (dyn ? drafts_d : drafts_s) + row * max_len;
+        const int32_t* lens = dyn ? len_d : len_s;
+        const int lraw = *(lens ? lens + row : dsrc);
+        len = lens ? lraw : max_len;
+    };
     for (int i = threadIdx.x; i < p; i += kSelThreads) {
-        uint64_t key = 0;  // padding: below every member
-        if (i < n_all) {
-            const bool dyn = i >= n_s;
-            const int r = dyn ? i - n_s : i;
-            const int64_t row = (int64_t)q * (dyn ? n_d : n_s) + r;
-            const int32_t* lens = dyn ? len_d : len_s;
-            const int len = lens ? lens[row] : max_len;
-            const int32_t first = (dyn ? drafts_d : drafts_s)[row * max_len];
-            const bool match = len > 0 && first == anchor;
-            const float s = dyn ? scores_d[row] + sp.delta : scores_s[row];
-            const float S = __builtin_fmaf(sp.beta, s, match ? sp.alpha : 0.0f);
-            key = pack_key(S, (uint32_t)i);
-        }
-        s_key[i] = key;
+        const int ic = i < n_all ? i : n_all - 1;
+        int64_t row;
+        const int32_t* dsrc;
+        int len;
+        member(ic, row, dsrc, len);
+        const bool dyn = ic >= n_s;
+        const int32_t first = dsrc[0];
+        const float sv = (dyn ? scores_d : scores_s)[row];
+        const bool match = len > 0 && first == anchor;
+        const float sc = dyn ? sv + sp.delta : sv;
+        const float S = __builtin_fmaf(sp.beta, sc, match ? sp.alpha : 0.0f);
+        s_key[i] = i < n_all ? pack_key(S, (uint32_t)i) : 0;   // padding: below every member
     }
     __syncthreads();
-    bitonic_desc<kSelThreads>(s_key, p);
+    if (n_all <= kSelThreads) {
+        // Rank sort: each member counts the members above it (LDS broadcast
+        // reads; keys are unique, so the ranks are a permutation).
+        uint64_t mine = 0;
+        int rank = 0;
+        if (threadIdx.x < n_all) {
+            mine = s_key[threadIdx.x];
+            for (int j = 0; j < n_all; ++j) rank += s_key[j] > mine ? 1 : 0;
+        }
+        __syncthreads();
+        if (threadIdx.x < n_all) s_key[rank] = mine;
+        __syncthreads();
+    } else {
+        bitonic_desc<kSelThreads>(s_key, p);
+    }
 
-    for (int t = threadIdx.x; t < top_n * max_len; t += kSelThreads) {
-        const int r = t / max_len, j = t - r * max_len;
-        const uint64_t key = s_key[r];
-        const int i = (int)key_row(key);
-        const bool dyn = i >= n_s;
-        const int src = dyn ? i - n_s : i;
-        const int64_t row = (int64_t)q * (dyn ? n_d : n_s) + src;
-        const int32_t* lens = dyn ? len_d : len_s;
-        int len = lens ? lens[row] : max_len;
-        len = len < 0 ? 0 : (len > max_len ? max_len : len);
-        int32_t v = j < len ? (dyn ? drafts_d : drafts_s)[row * max_len + j] : -1;
-        const bool pinned = sp.anchor_override && (r == 0 || r == top_n - 1);
-        if (pinned && j == 0) v = anchor;
-        const int64_t o = (int64_t)q * top_n + r;
-        out_drafts[o * max_len + j] = v;
-        if (j == 0) {
-            out_len[o] = (pinned && len < 1) ? 1 : len;
-            if (out_source) out_source[o] = i;
-            if (out_score) out_score[o] = key_score((uint32_t)(key >> 32));
+    // Gather: kOut outputs per thread and round, every load requested before
+    // any store (rank r < top_n <= n_all holds a member).
+    constexpr int kOut = 4;
+    const int total = top_n * max_len;
+    for (int t0 = 0; t0 < total; t0 += kOut * kSelThreads) {
+        int32_t dv[kOut], lv[kOut], iv[kOut];
+#pragma unroll
+        for (int u = 0; u < kOut; ++u) {
+            const int t = t0 + threadIdx.x + u * kSelThreads;
+            const int tc = t < total ? t : total - 1;
+            const int r = tc / max_len, j = tc - r * max_len;
+            const int i = (int)key_row(s_key[r]);
+            int64_t row;
+            const int32_t* dsrc;
+            member(i, row, dsrc, lv[u]);
+            dv[u] = dsrc[j];
+            iv[u] = i;
+        }
+#pragma unroll
+        for (int u = 0; u < kOut; ++u) {
+            const int t = t0 + threadIdx.x + u * kSelThreads;
+            if (t >= total) continue;
+            const int r = t / max_len, j = t - r * max_len;
+            int len = lv[u];
+            len = len < 0 ? 0 : (len > max_len ? max_len : len);
+            int32_t v = j < len ? dv[u] : -1;
+            const bool pinned = sp.anchor_override && (r == 0 || r == top_n - 1);
+            if (pinned && j == 0) v = anchor;
+            const int64_t o = (int64_t)q * top_n + r;
+            out_drafts[o * max_len + j] = v;
+            if (j == 0) {
+                out_len[o] = (pinned && len < 1) ? 1 : len;
+                if (out_source) out_source[o] = iv[u];
+                if (out_score) out_score[o] = key_score((uint32_t)(s_key[r] >> 32));
+            }
         }
     }
 }
