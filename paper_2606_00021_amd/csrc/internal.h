@@ -307,11 +307,12 @@ hipError_t launch_select_candidates(const float* scores_s, const int32_t* drafts
 
 // Appends `count` rows to a dynamic cache of n_old rows: keys (count x d of
 // src_dtype, converted to key_dtype) into keys (row stride d), tokens into
-// the history, and the continuation lengths min(max_span, n - p).
+// the history, the continuation lengths min(max_span, n - p), and, when
+// inv_norm is not NULL, each new row's 1/||k|| (as the index build forms it).
 hipError_t launch_append_rows(const void* src, int src_dtype, int key_dtype,
                               const int32_t* tokens, int d, int64_t n_old, int count,
                               int max_span, void* keys, int32_t* hist, int32_t* span_len,
-                              hipStream_t stream);
+                              float* inv_norm, hipStream_t stream);
 
 // Outputs of the loose-trie build (device pointers; NULL = not wanted for
 // the optional ones).  Per group g of gs drafts of m tokens, nodes = gs * m

@@ -328,15 +328,11 @@ SENSE_EXPORT sense_status_t sense_index_append(sense_index_t* ix, const void* ke
     if (!aligned(keys, (size_t)elem_size(keys_dtype)) || !aligned(tokens, 4))
         return fail(SENSE_ERR_MISALIGNED, "keys or tokens not aligned to their element size");
     hipStream_t st = (hipStream_t)stream;
+    // The new rows' 1/||k|| (cosine) are formed by the same launch.
     hipError_t e = sense::launch_append_rows(keys, keys_dtype, ix->key_dtype, tokens, ix->d, ix->n,
                                              count, ix->max_span, ix->owned_keys, ix->owned_hist,
-                                             ix->owned_span_len, st);
+                                             ix->owned_span_len, ix->inv_norm, st);
     if (e != hipSuccess) return hip_fail(e, "append");
-    if (ix->inv_norm) {
-        e = sense::launch_key_norms((const char*)ix->owned_keys + (size_t)ix->n * ix->d * 2,
-                                    ix->key_dtype, count, ix->d, ix->d, ix->inv_norm + ix->n, st);
-        if (e != hipSuccess) return hip_fail(e, "append norms");
-    }
     ix->n += count;
     return ok();
 }

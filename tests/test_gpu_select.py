@@ -171,6 +171,18 @@ def test_dynamic_cache_retrieval(case):
             o_dr, o_dl = oracle.gather(spans, lens, g_ids)
             assert np.array_equal(dr[qq].cpu().numpy(), o_dr), "dynamic drafts differ"
             assert np.array_equal(dl[qq].cpu().numpy(), o_dl), "dynamic lengths differ"
+    if at >= k:
+        # Appended rows carry the norms an index build forms: a static index
+        # over the same rows returns the same ids and bit-identical scores.
+        static = sense.sense_build_index(keys_now.to(DEV).contiguous(),
+                                         torch.zeros(at, m, dtype=torch.int32, device=DEV),
+                                         metric=metric)
+        ids2, sc2, _, _ = sense.sense_retrieve(static, q, k)
+        torch.cuda.synchronize()
+        assert torch.equal(ids2, ids), "appended vs rebuilt index: ids differ"
+        assert torch.equal(sc2.view(torch.int32), sc.view(torch.int32)), \
+            "appended vs rebuilt index: scores differ in bits"
+        static.close()
     cache.close()
 
 
