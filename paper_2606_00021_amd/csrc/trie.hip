@@ -13,7 +13,8 @@
 //     3. tree extraction and index map: an exclusive block scan of the
 //        "new token" flags in row-major order numbers the tree tokens; a
 //        shared position takes the latest number above it in its column
-//        (a max-scan down the rows, log2 N doubling steps);
+//        (a max-scan down the rows: across the lanes of one wave per column
+//        for up to 64 drafts, else log2 N doubling steps);
 //     4. outputs: the permutation, Gamma, and per tree token its id, parent,
 //        depth and the sorted draft that creates it (the inverse map).
 //   Numbering in row-major order of lexicographically sorted drafts visits
@@ -161,8 +162,24 @@ __global__ __launch_bounds__(kTrieThreads) void trie_build_kernel(
     __syncthreads();
     const int L = total;
 
-    // 3b. Max-scan down the rows of every column (Hillis-Steele doubling).
-    for (int s = 1; s < gs; s <<= 1) {
+    // 3b. Max-scan down the rows of every column.  Up to 64 rows: one wave
+    //     per column, lane r holding row r, an inclusive max-scan across the
+    //     lanes (columns are independent).  More rows: Hillis-Steele doubling
+    //     over the block.
+    if (gs <= 64) {
+        for (int j = wv; j < m; j += kTrieThreads / 64) {
+            const int t = lane * m + j;
+            int v = lane < gs ? s_idx[t] : -1;
+#pragma unroll
+            for (int off = 1; off < 64; off <<= 1) {
+                const int y = __shfl_up(v, off, 64);
+                if (lane >= off) v = v > y ? v : y;
+            }
+            if (lane < gs) s_idx[t] = v;
+        }
+        __syncthreads();
+    }
+    for (int s = 1; s < (gs <= 64 ? 1 : gs); s <<= 1) {
         int v[kTriePer];
 #pragma unroll
         for (int e = 0; e < kTriePer; ++e) {
