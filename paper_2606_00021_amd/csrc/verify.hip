@@ -544,15 +544,16 @@ __global__ __launch_bounds__(kFinThreads) void verify_finalize_tree_kernel(
         // Every load of the node first (the partials of a node that is not
         // judged were not written and are not used).
         const int tok = tree_tokens[item];
+        const int par = tree_parent[item];
         Stats st;
         int cnt;
         merge_partials(partial + (int64_t)item * n_slices, n_slices, &st, &cnt);
-        int64_t row;
         uint8_t bits = 0;
         float score = 0.0f;
         int rank = vocab;
-        if (tree_item(item, nodes, tree_parent, tree_len, &row))
-            bits = 8 | item_bits(st, cnt, tok, vocab, gp, &score, &rank);
+        // u < L: the node exists; it is judged when its parent is in range
+        // (the rows kernel's test for the same node).
+        if (par >= -1 && par < nodes) bits = 8 | item_bits(st, cnt, tok, vocab, gp, &score, &rank);
         s_bits[u] = bits;
         s_score[u] = score;
         s_rank[u] = rank;
