@@ -182,22 +182,11 @@ __device__ __forceinline__ void absorb(Acc& a, float x, float nm, float thr) {
     a.cnt += (x >= thr) ? 1 : 0;
 }
 
-// A tree node is judged when it lies below the group's node count and its
-// parent is a node of the group (or none): then its logits row is
-// 1 + parent within the group's 1 + nodes rows.
-__device__ __forceinline__ bool tree_item(int item, int nodes, const int32_t* tree_parent,
-                                          const int32_t* tree_len, int64_t* row) {
-    const int g = item / nodes, u = item - g * nodes;
-    if (u >= tree_len[g]) return false;
-    const int par = tree_parent[item];
-    if (par < -1 || par >= nodes) return false;
-    *row = (int64_t)g * (nodes + 1) + 1 + par;
-    return true;
-}
-
 // One block per (item, vocabulary slice).  Dense: item = candidate * max_len
 // + position, its own logits row, token drafts[item].  TREE: item = group *
-// nodes + tree node, token tree_tokens[item], row from tree_item.
+// nodes + u, token tree_tokens[item]; it is judged when u < tree_len[group]
+// and its parent is a node of the group (or none), and its logits row is
+// 1 + parent within the group's 1 + nodes rows.
 template <int LT, bool VEC, bool TREE>
 __global__ __launch_bounds__(kRowThreads) void verify_rows_kernel(
     const void* __restrict__ logits, int64_t row_stride, const int32_t* __restrict__ drafts,
@@ -210,8 +199,15 @@ __global__ __launch_bounds__(kRowThreads) void verify_rows_kernel(
     const int slice = blockIdx.y;
     const int tid = threadIdx.x;
     int64_t row = item;
+    // The row's token and the loads that decide whether the row is judged
+    // are requested together (every index is in range either way).
+    const int tok = drafts[item];
     if constexpr (TREE) {
-        if (!tree_item(item, nodes, tree_parent, tree_len, &row)) return;   // uniform
+        const int g = item / nodes, u = item - g * nodes;
+        const int tl = tree_len[g];
+        const int par = tree_parent[item];
+        if (u >= tl || par < -1 || par >= nodes) return;   // uniform over the block
+        row = (int64_t)g * (nodes + 1) + 1 + par;
     } else {
         const int c = item / max_len, j = item - c * max_len;
         int len = draft_len ? draft_len[c] : max_len;
@@ -219,7 +215,6 @@ __global__ __launch_bounds__(kRowThreads) void verify_rows_kernel(
         if (j >= len) return;                        // uniform over the block
     }
 
-    const int tok = drafts[item];
     const bool valid = tok >= 0 && tok < vocab;
     const char* rowp = (const char*)logits + row * row_stride * ES;
     const int tk = valid ? tok : -1;                 // -1: the count is unused
