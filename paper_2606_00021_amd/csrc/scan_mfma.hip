@@ -120,6 +120,16 @@ __device__ __forceinline__ void dma16(const void* g, void* lds) {
     asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(base)
                  : "memory", "m0");
 }
+// The same with the non-temporal hint, for the key stream: every key byte is
+// used once per scan, and without the hint the stream evicts the query
+// fragments, which every block re-reads, from L2 (at 64 queries with the
+// hi/lo split those are 2 MiB per XCD; measured: 16 % more HBM traffic than
+// the keys alone).
+__device__ __forceinline__ void dma16_nt(const void* g, void* lds) {
+    const uint32_t base = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off nt" ::"v"(g), "s"(base)
+                 : "memory", "m0");
+}
 #pragma clang diagnostic pop
 
 // Workgroup barrier without the memory fence __syncthreads() adds (the fence
@@ -236,7 +246,7 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
 #pragma unroll
             for (int t = 0; t < T; ++t)
 #pragma unroll
-                for (int i = 0; i < 2; ++i) dma16(kp[t][i] + ko, &kring[slot][wv][t][i * kTileSecond]);
+                for (int i = 0; i < 2; ++i) dma16_nt(kp[t][i] + ko, &kring[slot][wv][t][i * kTileSecond]);
 #pragma unroll
             for (int j = 0; j < NA_W; ++j) {
                 const int qd = (sc * 2 + qstep[j]) * 32 + grp * 8;

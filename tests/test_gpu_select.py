@@ -2,13 +2,16 @@
 cache (Sec. 3.2 Eqs. 6 and 8; Alg. 1's retriever update; Alg. 2's hybrid
 retrieval, composite score, Top-N and anchor override).
 
-Selection alone is compared element by element with the oracle taking the
-composite score in binary32 (the precision the kernel decides the order in):
-drafts, lengths, sources and scores must be identical.  The dynamic cache is
-compared with the oracle's exact retrieval over the same rounded keys and the
-continuation table of the token history.  The full SEN chain (static and
-dynamic retrieval, selection, soft-gated verification) is compared with the
-oracle's chain in double precision.
+Selection is compared with the oracle's definition in double precision: the
+selected members, their order, drafts, lengths and composite scores must be
+the oracle's, except that two members may trade places where their exact
+composite scores lie within the rounding the kernel's binary32 evaluation
+can cause (a derived near-tie allowance, ~1e-7 relative); the same inputs are
+also compared with the oracle taking the score in binary32, which must agree
+exactly.  The dynamic cache is compared with the oracle's exact retrieval
+over the same rounded keys and the continuation table of the token history.
+The full SEN chain (static and dynamic retrieval, selection, soft-gated
+verification) is compared with the oracle's chain in double precision.
 """
 import numpy as np
 import pytest
@@ -17,7 +20,7 @@ import torch
 import oracle
 from oracle import trie as otrie
 from paper_2606_00021_amd import sense, synth
-from parity import REL_TIE, check_topk, check_verify, dt_name, host_bits
+from parity import check_topk, check_verify, dt_name, host_bits, query_bounds
 
 pytestmark = pytest.mark.gpu
 
@@ -66,6 +69,67 @@ SELECT_CASES = [
 ]
 
 
+def composite_err(s_member, comp, alpha, beta, delta_member):
+    """Bound on |binary32 composite - exact composite| for one member: the
+    kernel rounds alpha, beta and delta to binary32, forms fl(s + delta) and
+    one fused multiply-add; first-order terms, doubled."""
+    u = 2.0 ** -24
+    return 2 * u * (3 * abs(beta) * (abs(s_member) + abs(delta_member)) + abs(alpha)
+                    + abs(comp)) + 1e-300
+
+
+def check_selection_f64(g_src, g_dr, g_ln, g_sc, pools, anchor, top_n, alpha, beta, delta,
+                        override):
+    """One query's GPU selection against the exact (f64) definition.  pools =
+    (scores_s, drafts_s, len_s, scores_d, drafts_d, len_d) on the host.
+    Returns the number of ranks excused as near ties."""
+    ss, ds, ls, sd, dd, ld = pools
+    n_s = 0 if ss is None else ss.shape[0]
+    n_d = 0 if sd is None else sd.shape[0]
+    n_all = n_s + n_d
+    m = (ds if ds is not None else dd).shape[1]
+    if ss is None:
+        ss, ds = np.zeros(0), np.zeros((0, m), dtype=np.int32)
+    o_dr, o_ln, o_src, o_comp = oracle.select_candidates(
+        ss, ds, ls, anchor, n_all, alpha, beta, delta, anchor_override=False, scores_d=sd,
+        drafts_d=dd, len_d=ld, precision="f64")
+    rank_of = np.empty(n_all, dtype=np.int64)
+    rank_of[o_src] = np.arange(n_all)
+    comp_of = o_comp[rank_of]
+    sim = np.r_[ss, sd if sd is not None else np.zeros(0)]
+    dl = np.r_[np.zeros(n_s), np.full(n_d, delta)]
+    err_of = np.array([composite_err(sim[i], comp_of[i], alpha, beta, dl[i])
+                       for i in range(n_all)])
+    assert len(set(g_src.tolist())) == top_n, "a member selected twice"
+    excused = 0
+    for r in range(top_n):
+        a, b = int(g_src[r]), int(o_src[r])
+        if a == b:
+            continue
+        ca, cb = comp_of[a], comp_of[b]
+        ok = np.isfinite(ca) and np.isfinite(cb) and abs(ca - cb) <= err_of[a] + err_of[b]
+        assert ok, (f"rank {r}: member {a} (composite {ca!r}) vs the definition's {b} ({cb!r}); "
+                    f"{excused} ranks excused before it")
+        excused += 1
+    for r in range(top_n):
+        i = int(g_src[r])
+        want_dr = o_dr[rank_of[i]].copy()
+        want_ln = int(o_ln[rank_of[i]])
+        if override and r in (0, top_n - 1):
+            want_dr[0] = anchor
+            want_ln = max(want_ln, 1)
+        assert np.array_equal(g_dr[r], want_dr), f"rank {r}: drafts of member {i}"
+        assert g_ln[r] == want_ln, f"rank {r}: length of member {i}"
+        c = comp_of[i]
+        if np.isnan(c):
+            assert np.isnan(g_sc[r]), f"rank {r}: composite score of member {i}"
+        elif np.isinf(c):
+            assert g_sc[r] == c, f"rank {r}: composite score of member {i}"
+        else:
+            assert abs(float(g_sc[r]) - c) <= err_of[i], f"rank {r}: composite score of member {i}"
+    return excused
+
+
 @pytest.mark.parametrize("case", SELECT_CASES, ids=[str(i) for i in range(len(SELECT_CASES))])
 @pytest.mark.parametrize("with_len", [True, False])
 def test_select_matches_oracle(case, with_len):
@@ -82,15 +146,28 @@ def test_select_matches_oracle(case, with_len):
                                  with_len)
     torch.cuda.synchronize()
     dr, ln, src, sc = dr.cpu().numpy(), ln.cpu().numpy(), src.cpu().numpy(), sc.cpu().numpy()
+
+    def host(pool, qq):
+        if pool is None or pool.scores.shape[1] == 0:
+            return None, None, None
+        return (pool.scores[qq].cpu().numpy().astype(np.float64), pool.drafts[qq].cpu().numpy(),
+                pool.lengths[qq].cpu().numpy() if with_len else None)
+    excused = 0
     for q in range(nq):
+        pools = (*host(pool_s, q), *host(pool_d, q))
+        excused += check_selection_f64(src[q], dr[q], ln[q], sc[q], pools, int(anchors[q]), top_n,
+                                       alpha, beta, delta, override)
+        # the same inputs with the composite taken in binary32: identical
         o_dr, o_ln, o_src, o_sc = oracle_select_query(pool_s, pool_d, q, int(anchors[q]), top_n,
                                                       alpha, beta, delta, override, with_len)
-        assert np.array_equal(src[q], o_src), f"query {q}: order differs"
-        assert np.array_equal(dr[q], o_dr), f"query {q}: drafts differ"
-        assert np.array_equal(ln[q], o_ln), f"query {q}: lengths differ"
+        assert np.array_equal(src[q], o_src), f"query {q}: order differs from binary32"
+        assert np.array_equal(dr[q], o_dr), f"query {q}: drafts differ from binary32"
+        assert np.array_equal(ln[q], o_ln), f"query {q}: lengths differ from binary32"
         o32 = o_sc.astype(np.float32)
         same = (sc[q] == o32) | (np.isnan(sc[q]) & np.isnan(o32))
-        assert same.all(), f"query {q}: composite scores differ"
+        assert same.all(), f"query {q}: composite scores differ from binary32"
+    print(f"[select] ok: ranks excused as near ties of the exact composite: {excused}",
+          flush=True)
 
 
 def test_select_is_deterministic():
@@ -162,12 +239,13 @@ def test_dynamic_cache_retrieval(case):
         # the oracle sees the same rounded keys (source types that round
         # through fp32 to the key type give the same bits)
         keys_now = to_key_dtype(ctx.keys[:at].to(sdt).float(), kdt)
-        o_s = oracle.scores(host_bits(keys_now), dt_name(keys_now), q.cpu().numpy(), "f32",
-                            metric)
+        kb_now = host_bits(keys_now)
+        o_s = oracle.scores(kb_now, dt_name(keys_now), q.cpu().numpy(), "f32", metric)
+        bounds = query_bounds(kb_now, dt_name(keys_now), q.cpu().numpy(), metric)
         spans, lens = oracle.dynamic_spans(ctx.tokens[:at].cpu().numpy(), m)
         for qq in range(nq):
             g_ids = ids[qq].cpu().numpy()
-            check_topk(g_ids, sc[qq].cpu().numpy(), o_s[qq], k)
+            check_topk(g_ids, sc[qq].cpu().numpy(), o_s[qq], k, bounds[qq])
             o_dr, o_dl = oracle.gather(spans, lens, g_ids)
             assert np.array_equal(dr[qq].cpu().numpy(), o_dr), "dynamic drafts differ"
             assert np.array_equal(dl[qq].cpu().numpy(), o_dl), "dynamic lengths differ"
@@ -223,18 +301,23 @@ def test_dynamic_cache_limits():
 
 # ------------------------------------------------------------------ SEN chain
 
-def check_selection(g_src, o_comp, o_sim, beta, top_n):
+def check_selection(g_src, o_comp, o_sim, alpha, beta, delta_of, sim_err, top_n):
     """The GPU's pool positions (ordered) against the oracle's composite
-    scores of the same pool: identical except where two composite scores are
-    within REL_TIE of the similarity term (a near tie)."""
+    scores of the same pool: identical except where two composite scores lie
+    within the allowance of a near tie: the binary32 composite rounding plus
+    beta times the retrieval score bound of each member (the GPU selects on
+    its own retrieval scores, the oracle on exact ones)."""
     o_order = sorted(range(len(o_comp)), key=lambda i: (-o_comp[i], i))[:top_n]
-    tol = lambda a, b: REL_TIE * abs(beta) * max(abs(o_sim[a]), abs(o_sim[b]), 1e-30)
+    allow = [composite_err(o_sim[i], o_comp[i], alpha, beta, delta_of[i]) + abs(beta) * sim_err[i]
+             for i in range(len(o_comp))]
     assert len(set(g_src.tolist())) == top_n
+    excused = 0
     for r in range(top_n):
         a, b = int(g_src[r]), o_order[r]
         if a != b:
-            assert abs(o_comp[a] - o_comp[b]) <= tol(a, b), f"rank {r}: {a} vs {b}"
-    return o_order
+            assert abs(o_comp[a] - o_comp[b]) <= allow[a] + allow[b], f"rank {r}: {a} vs {b}"
+            excused += 1
+    return o_order, excused
 
 
 @pytest.mark.parametrize("wname,scale,ctx_len,k_dyn,top_n", [
@@ -264,11 +347,15 @@ def test_sen_chain(wname, scale, ctx_len, k_dyn, top_n):
     torch.cuda.synchronize()
 
     # oracle chain, double precision throughout
-    o_ss = oracle.scores(host_bits(ds.keys), w.key_dtype, q.cpu().numpy(), "f32")[0]
+    kb_s = host_bits(ds.keys)
+    o_ss = oracle.scores(kb_s, w.key_dtype, q.cpu().numpy(), "f32")[0]
     keys_d = to_key_dtype(ctx.keys, synth.DTYPES[w.key_dtype])
-    o_sd = oracle.scores(host_bits(keys_d), w.key_dtype, q.cpu().numpy(), "f32")[0]
-    assert check_topk(hs[0][0].cpu().numpy(), hs[1][0].cpu().numpy(), o_ss, w.k) == 0
-    assert check_topk(hd[0][0].cpu().numpy(), hd[1][0].cpu().numpy(), o_sd, k_dyn) == 0
+    kb_d = host_bits(keys_d)
+    o_sd = oracle.scores(kb_d, w.key_dtype, q.cpu().numpy(), "f32")[0]
+    b_s = query_bounds(kb_s, w.key_dtype, q.cpu().numpy(), "cosine")[0]
+    b_d = query_bounds(kb_d, w.key_dtype, q.cpu().numpy(), "cosine")[0]
+    assert check_topk(hs[0][0].cpu().numpy(), hs[1][0].cpu().numpy(), o_ss, w.k, b_s) == 0
+    assert check_topk(hd[0][0].cpu().numpy(), hd[1][0].cpu().numpy(), o_sd, k_dyn, b_d) == 0
     o_ids_s, o_sc_s = oracle.topk(o_ss, w.k)
     o_ids_d, o_sc_d = oracle.topk(o_sd, k_dyn)
     o_dr_s, o_dl_s = oracle.gather(ds.spans.cpu().numpy(), None, o_ids_s)
@@ -279,8 +366,12 @@ def test_sen_chain(wname, scale, ctx_len, k_dyn, top_n):
         scores_d=o_sc_d, drafts_d=o_dr_d, len_d=o_dl_d)
     comp_of = np.empty(w.k + k_dyn)
     comp_of[o_src] = o_comp
-    sim_of = np.r_[o_sc_s, o_sc_d + delta]
-    check_selection(src[0].cpu().numpy(), comp_of, sim_of, beta, top_n)
+    sim_of = np.r_[o_sc_s, o_sc_d]
+    delta_of = np.r_[np.zeros(w.k), np.full(k_dyn, delta)]
+    sim_err = np.r_[b_s(o_ids_s), b_d(o_ids_d)]
+    _, excused = check_selection(src[0].cpu().numpy(), comp_of, sim_of, alpha, beta, delta_of,
+                                 sim_err, top_n)
+    print(f"[sen-chain] selection ranks excused as near ties: {excused}", flush=True)
     o_dr, o_ln, o_src, _ = oracle.select_candidates(
         o_sc_s, o_dr_s, o_dl_s, anchor, top_n, alpha, beta, delta, scores_d=o_sc_d,
         drafts_d=o_dr_d, len_d=o_dl_d)
