@@ -225,6 +225,28 @@ sense_status_t sense_retrieve(const sense_index_t *index, const void *queries,
                               int32_t *out_draft_len, void *workspace,
                               size_t workspace_bytes, void *stream);
 
+/* Retrieval for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation):
+ * sense_retrieve with its scratch taken from a static device array inside the
+ * library instead of a caller workspace.  Arguments, results and errors are
+ * those of sense_retrieve, plus UNSUPPORTED when the call needs more than
+ * sense_retrieve_noalloc_max_bytes() of scratch (64 MiB: e.g. one query over
+ * up to ~15M rows, or 16 queries over 1M rows; use sense_retrieve with a
+ * workspace beyond that).  It calls no allocator.  The device current on the
+ * calling thread must be the one `stream` belongs to; each device has its own
+ * copy of the array (held until the process ends), and its address is taken
+ * once per device at the first call there.  Every call on a device shares
+ * that device's array, which keeps the last call's contents: calls that may
+ * overlap on one device (other streams, other threads) race and must be
+ * serialised by the caller. */
+sense_status_t sense_retrieve_noalloc(const sense_index_t *index, const void *queries,
+                                      sense_dtype_t q_dtype, int32_t n_queries, int32_t k,
+                                      int64_t *out_ids, float *out_scores, int32_t *out_drafts,
+                                      int32_t *out_draft_len, void *stream);
+
+/* Bytes of the static scratch sense_retrieve_noalloc draws on. */
+size_t sense_retrieve_noalloc_max_bytes(void);
+
 /* Soft-gate hyper-parameters (Alg. 4 inputs; Sec. 3.3; defaults of the
  * paper's experiments: gamma 0.05, top-k 3, W 6).
  *   gamma              entropy threshold: B_ent = I(E' > gamma)

@@ -8,6 +8,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <new>
 
 #include "internal.h"
@@ -522,6 +523,60 @@ SENSE_EXPORT sense_status_t sense_retrieve(const sense_index_t* ix, const void* 
     if ((e = timer_mark(SENSE_TIMER_TOPK, 1, st)) != hipSuccess) return hip_fail(e, "timer");
     return ok();
 }
+
+// ---------------------------------------------------------------- retrieval
+// without a caller workspace.  The scratch lives in this file-scope device
+// array; every GPU the library runs on holds its own copy until the process
+// ends.  In host code the array's name is only a stand-in for the symbol: the
+// device address of each GPU's copy comes from hipGetSymbolAddress, taken
+// once per device with that device current, and only that address is ever
+// handed to a kernel.
+static constexpr size_t kNoAllocScratchBytes = (size_t)64 << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+namespace {
+constexpr int kMaxScratchDevices = 64;
+void* g_scratch_ptr[kMaxScratchDevices];
+hipError_t g_scratch_err[kMaxScratchDevices];
+std::once_flag g_scratch_once[kMaxScratchDevices];
+}  // namespace
+
+static sense_status_t scratch_of_current_device(void** out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev < 0 || dev >= kMaxScratchDevices)
+        return fail(SENSE_ERR_UNSUPPORTED, "device %d beyond the %d the static scratch serves",
+                    dev, kMaxScratchDevices);
+    std::call_once(g_scratch_once[dev], [dev] {
+        g_scratch_err[dev] = hipGetSymbolAddress(&g_scratch_ptr[dev], HIP_SYMBOL(scratch));
+    });
+    if (g_scratch_err[dev] != hipSuccess) return hip_fail(g_scratch_err[dev], "hipGetSymbolAddress");
+    if (!g_scratch_ptr[dev] || !aligned(g_scratch_ptr[dev], 256))
+        return fail(SENSE_ERR_HIP, "static scratch of device %d has no usable address", dev);
+    *out = g_scratch_ptr[dev];
+    return SENSE_OK;
+}
+
+SENSE_EXPORT sense_status_t sense_retrieve_noalloc(const sense_index_t* ix, const void* queries,
+                                                   sense_dtype_t q_dtype, int32_t nq, int32_t k,
+                                                   int64_t* out_ids, float* out_scores,
+                                                   int32_t* out_drafts, int32_t* out_draft_len,
+                                                   void* stream) {
+    sense_status_t s = check_retrieve_sizes(ix, nq, k);
+    if (s != SENSE_OK) return s;
+    const size_t need = retrieve_layout(ix, nq, k).total;
+    if (need > kNoAllocScratchBytes)
+        return fail(SENSE_ERR_UNSUPPORTED,
+                    "this retrieval needs %zu bytes of scratch; the static scratch holds %zu "
+                    "(call sense_retrieve with a workspace)", need, kNoAllocScratchBytes);
+    void* ws = nullptr;
+    if ((s = scratch_of_current_device(&ws)) != SENSE_OK) return s;
+    return sense_retrieve(ix, queries, q_dtype, nq, k, out_ids, out_scores, out_drafts,
+                          out_draft_len, ws, kNoAllocScratchBytes, stream);
+}
+
+SENSE_EXPORT size_t sense_retrieve_noalloc_max_bytes(void) { return kNoAllocScratchBytes; }
 
 static sense_status_t check_verify_sizes(int32_t n_cand, int32_t max_len, int32_t vocab) {
     if (n_cand < 0) return fail(SENSE_ERR_INVALID_ARGUMENT, "n_cand = %d < 0", n_cand);

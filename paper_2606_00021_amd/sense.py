@@ -39,6 +39,8 @@ EXPORTED = (
     "sense_index_info",
     "sense_retrieve_workspace_size",
     "sense_retrieve",
+    "sense_retrieve_noalloc",
+    "sense_retrieve_noalloc_max_bytes",
     "sense_soft_gate_verify_workspace_size",
     "sense_soft_gate_verify",
     "sense_build_dynamic_index",
@@ -189,6 +191,7 @@ def load_library() -> ctypes.CDLL:
                              ctypes.POINTER(ctypes.c_int)],
         "sense_retrieve_workspace_size": [P, I32, I32, PSZ],
         "sense_retrieve": [P, P, ctypes.c_int, I32, I32, P, P, P, P, P, SZ, P],
+        "sense_retrieve_noalloc": [P, P, ctypes.c_int, I32, I32, P, P, P, P, P],
         "sense_soft_gate_verify_workspace_size": [I32, I32, I32, PSZ],
         "sense_build_dynamic_index": [ctypes.POINTER(DynamicIndexDesc), PP],
         "sense_index_append": [P, P, ctypes.c_int, P, I32, P],
@@ -450,6 +453,36 @@ def sense_retrieve(index: Index, queries: torch.Tensor, k: int, workspace: torch
                               _dev_ptr(workspace, "workspace"), workspace.numel(),
                               _stream_handle(stream)),
            "sense_retrieve")
+    return ids, scores, drafts, dlen
+
+
+def sense_retrieve_noalloc_max_bytes() -> int:
+    """Bytes of the library's static scratch that sense_retrieve_noalloc uses."""
+    lib = load_library()
+    lib.sense_retrieve_noalloc_max_bytes.restype = ctypes.c_size_t
+    lib.sense_retrieve_noalloc_max_bytes.argtypes = []
+    return int(lib.sense_retrieve_noalloc_max_bytes())
+
+
+def sense_retrieve_noalloc(index: Index, queries: torch.Tensor, k: int, out: tuple,
+                           stream=None):
+    """sense_retrieve with the library's static scratch instead of a
+    workspace: allocates nothing, so ``out`` (ids, scores, drafts, draft_len)
+    is required.  Calls overlapping on one device race on that scratch."""
+    lib = load_library()
+    if queries.dim() == 1:
+        queries = queries.unsqueeze(0)
+    if queries.dtype not in _TORCH_DTYPE or not queries.is_contiguous():
+        raise ValueError("queries must be a contiguous float32/float16/bfloat16 tensor")
+    if queries.shape[1] != index.d:
+        raise ValueError(f"queries have d={queries.shape[1]}, index has d={index.d}")
+    ids, scores, drafts, dlen = out
+    _check(lib.sense_retrieve_noalloc(index.handle, _dev_ptr(queries, "queries"),
+                                      _TORCH_DTYPE[queries.dtype], queries.shape[0], k,
+                                      _dev_ptr(ids, "out_ids"), _dev_ptr(scores, "out_scores"),
+                                      _dev_ptr(drafts, "out_drafts"),
+                                      _dev_ptr(dlen, "out_draft_len"), _stream_handle(stream)),
+           "sense_retrieve_noalloc")
     return ids, scores, drafts, dlen
 
 

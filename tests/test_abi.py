@@ -103,6 +103,13 @@ def test_retrieve_rejects_null_index(lib):
     assert lib.sense_retrieve(None, p(FAKE), 0, 1, 8, p(FAKE), None, None, None, p(FAKE),
                               1 << 30, None) == INVALID
     assert lib.sense_destroy_index(None) == 0
+    assert lib.sense_retrieve_noalloc(None, p(FAKE), 0, 1, 8, p(FAKE), None, None, None,
+                                      None) == INVALID
+
+
+def test_noalloc_scratch_size(lib):
+    lib.sense_retrieve_noalloc_max_bytes.restype = ctypes.c_size_t
+    assert lib.sense_retrieve_noalloc_max_bytes() == 64 << 20
 
 
 def verify_call(lib, **kw):
