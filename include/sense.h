@@ -70,7 +70,17 @@
 extern "C" {
 #endif
 
-typedef enum {
+/* The enumerations below are int-sized.  A C caller may pass any int where one
+ * is expected (an unknown code is rejected with INVALID_ARGUMENT, or
+ * described as "unknown" by sense_status_string); C++ sees each with int as
+ * its fixed underlying type, so every int value is a valid value of it. */
+#ifdef __cplusplus
+#define SENSE_ENUM_BASE : int
+#else
+#define SENSE_ENUM_BASE
+#endif
+
+typedef enum SENSE_ENUM_BASE {
     SENSE_OK = 0,
     SENSE_ERR_INVALID_ARGUMENT = 1, /* NULL pointer, size out of range, mismatch */
     SENSE_ERR_MISALIGNED = 2,       /* pointer or stride breaks the 16-byte layout */
@@ -80,12 +90,12 @@ typedef enum {
     SENSE_ERR_HIP = 6               /* the HIP runtime reported an error */
 } sense_status_t;
 
-typedef enum { SENSE_F32 = 0, SENSE_F16 = 1, SENSE_BF16 = 2 } sense_dtype_t;
+typedef enum SENSE_ENUM_BASE { SENSE_F32 = 0, SENSE_F16 = 1, SENSE_BF16 = 2 } sense_dtype_t;
 
 /* Similarity of Sec. 3.2 Eq. 8.  COSINE is the inner product of the
  * L2-normalised query and key (the paper L2-normalises both before search);
  * the key norms are those of the stored fp16/bf16 values. */
-typedef enum { SENSE_METRIC_IP = 0, SENSE_METRIC_COSINE = 1 } sense_metric_t;
+typedef enum SENSE_ENUM_BASE { SENSE_METRIC_IP = 0, SENSE_METRIC_COSINE = 1 } sense_metric_t;
 
 /* Index flag: keep an owned, re-laid-out copy of the keys instead of
  * borrowing the caller's buffer (needed when the caller's row stride or base
@@ -605,7 +615,7 @@ sense_status_t sense_ivf_search(const sense_index_t *index, const void *queries,
 
 /* Diagnostics for benchmarks and profilers.  Which part of the path a pair
  * of timing events brackets. */
-typedef enum {
+typedef enum SENSE_ENUM_BASE {
     SENSE_TIMER_SCAN = 0,   /* similarity scan kernel(s) of sense_retrieve */
     SENSE_TIMER_TOPK = 1,   /* top-k selection + gather kernels of sense_retrieve */
     SENSE_TIMER_VERIFY = 2, /* both kernels of sense_soft_gate_verify(_tree) */

@@ -31,7 +31,13 @@ METRICS = {"ip": 0, "cosine": 1}
 
 
 def build(force: bool = False) -> str:
-    """Compile the oracle with the host C compiler (OpenMP over rows)."""
+    """Compile the oracle with the host C compiler (OpenMP over rows).  The
+    environment variable SENSE_ORACLE_LIB names a library built elsewhere
+    (the sanitizer and planted-mistake checks of the test-suite) to load
+    instead."""
+    alt = os.environ.get("SENSE_ORACLE_LIB")
+    if alt:
+        return alt
     if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
         tmp = _LIB + ".tmp%d" % os.getpid()
         subprocess.check_call(

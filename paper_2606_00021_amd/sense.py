@@ -14,7 +14,10 @@ from dataclasses import dataclass
 
 import torch
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsense.so")
+# SENSE_LIB names another build of the same library to load instead (the
+# test-suite's host-sanitizer build); by default the in-tree libsense.so.
+LIB_PATH = os.environ.get("SENSE_LIB") or os.path.join(
+    os.path.dirname(os.path.abspath(__file__)), "libsense.so")
 
 SENSE_OK = 0
 STATUS_NAMES = {

@@ -143,3 +143,15 @@ def test_override_gives_the_first_and_last_draft_an_accepted_token():
     logits[:, 0, :] = shared
     out = oracle.soft_gate_verify(logits, "f32", dr, lns, gamma=10.0)
     assert out["accept_len"][0] >= 1 and out["accept_len"][-1] >= 1
+
+
+def test_empty_draft_gets_no_anchor_bonus():
+    """I(s[0] = anchor) needs a first token: a continuation of length 0 has
+    none, so its composite score is beta * s even when its stored row starts
+    with the anchor."""
+    s = np.array([0.5, 0.25])
+    d = np.array([[9, 1, 2], [9, 3, 4]], dtype=np.int32)
+    ln = np.array([0, 2], dtype=np.int32)
+    _, _, src, sc = oracle.select_candidates(s, d, ln, 9, 2, 10.0, 1.0, anchor_override=False)
+    assert src.tolist() == [1, 0]
+    assert sc.tolist() == [10.25, 0.5]

@@ -263,3 +263,20 @@ def test_candidate_permutation_permutes_lengths():
     assert np.array_equal(b["accept_len"], a["accept_len"][perm])
     n = b["accept_len"]
     assert b["best"][0] == int(np.flatnonzero(n == n.max())[0])
+
+
+def test_entropy_gate_is_strict():
+    """Alg. 4 gates on a strict comparison, E / ln|V| > gamma.  A row with a
+    single finite logit (the rest -inf) has softmax (1, 0, ..., 0) and entropy
+    exactly 0, so at gamma = 0 the entropy bit is 0 in both entropy modes, and
+    a mismatching draft with a clean look-ahead window is rejected."""
+    v, m = 16, 4
+    logits = np.full((1, m, v), -np.inf, dtype=np.float32)
+    logits[0, :, 7] = 1.0
+    drafts = np.array([[3, 7, 7, 7]], dtype=np.int32)        # position 0 mismatches
+    for norm in (True, False):
+        out = oracle.soft_gate_verify(logits, "f32", drafts, gamma=0.0, topk=v, window=2, tau=0,
+                                      entropy_normalized=norm)
+        assert out["gate_score"][0, 0] == 0.0
+        assert (out["masks"][0] & ENT == 0).all()
+        assert out["accept_len"][0] == 0
