@@ -553,18 +553,19 @@ def main():
         scan_kernel = "ivf_search"
     else:
         scan_ms = dur["scan"]
-        if nq >= 4 and d_idx <= 64:
+        if nq >= 2 and d_idx <= 64:
             # The library's scan events wrap the whole batched short-key
             # retrieval: query split, sample pass, sample top-k, thresholds,
             # filtered pass over every row and the survivors' top-k.
             scan_kernel = "short_key_retrieval"
-        elif nq >= 4:
+        elif nq >= 2:
             scan_kernel = "scan_mfma_kernel"
         elif d_idx <= 64:
             scan_kernel = "scan_small_kernel"
         else:
             scan_kernel = "scan_gemv_kernel"
     step_bytes = scan_bytes + gather_bytes + verify_bytes
+    traffic = traffic_from_profiles(name, scan_kernel) if scan_kernel in SCAN_SOURCES else None
     scan_gbps = scan_bytes / (scan_ms * 1e-3) / 1e9
     res = {
         "metric": METRIC,
@@ -597,9 +598,13 @@ def main():
                         if scan_kernel in ("short_key_retrieval", "ivf_search") else {}),
                      "achieved": scan_gbps,
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": scan_gbps / HBM_PEAK_GBPS,
-                     "traffic": (traffic_from_profiles(name, scan_kernel)
-                                 if scan_kernel in SCAN_SOURCES else None)},
+                     "traffic": traffic},
     }
+    if traffic is not None:
+        res["roofline"]["traffic_source"] = (
+            f"profiles/{scan_kernel}_{name}.md: rocprofv3 FETCH_SIZE + WRITE_SIZE per launch, "
+            f"each scaled by what the counter reads for a 1 GiB device copy; taken on the "
+            f"current kernel source (its digest matches), not in this run")
     if scan_kernel == "scan_mfma_kernel":
         # Matrix-core utilisation of the batched scan (bound by HBM, so a share
         # of the dense peak, reported beside GB/s): the instructions issue

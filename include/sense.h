@@ -301,6 +301,12 @@ sense_status_t sense_soft_gate_verify_workspace_size(int32_t n_cand, int32_t max
  * j >= draft_len count as mismatches); R[j] = sum_{u=1..W} B-bar[j+u];
  * B_con = I(R <= tau); G = B_em | (B_ent & (B_topk | B_con)), forced to 0 at
  * j >= draft_len; the accepted length n_c = number of leading ones of G.
+ * Domain: logits are finite or -inf (a token of probability 0).  A +inf logit
+ * still ranks exactly (the order above; equal +inf values by index), but
+ * softmax of a row holding +inf is not a distribution of finite numbers: its
+ * E' is NaN and B_ent 0.  NaN logits are outside the domain: such a row's
+ * rank and gate bits are unspecified (every output stays in its range; the
+ * call neither faults nor reads outside the row).
  * Outputs:
  *   out_accept_len n_cand int32, n_c in [0, draft_len[c]] (required).  The
  *                  paper's L of Alg. 4 is n_c - 1.

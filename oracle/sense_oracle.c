@@ -221,13 +221,19 @@ int oracle_row_stats(const void *row, int dtype, int32_t vocab, int32_t tok,
         e[v].v = v;
         if (e[v].x > m) { m = e[v].x; y = v; }
     }
-    /* softmax p_v = exp(x_v - m) / sum_u exp(x_u - m); entropy -sum p ln p */
-    double z = 0.0;
-    for (int32_t v = 0; v < vocab; ++v) z += exp(e[v].x - m);
+    /* softmax p_v = exp(x_v - m) / sum_u exp(x_u - m); entropy -sum p ln p.
+     * With m = +inf the weights exp(x_v - m) are undefined (+inf - +inf), so
+     * the entropy is too: NaN (never above gamma). */
     double ent = 0.0;
-    for (int32_t v = 0; v < vocab; ++v) {
-        double p = exp(e[v].x - m) / z;
-        if (p > 0.0) ent -= p * log(p);
+    if (isinf(m) && m > 0) {
+        ent = NAN;
+    } else {
+        double z = 0.0;
+        for (int32_t v = 0; v < vocab; ++v) z += exp(e[v].x - m);
+        for (int32_t v = 0; v < vocab; ++v) {
+            double p = exp(e[v].x - m) / z;
+            if (p > 0.0) ent -= p * log(p);
+        }
     }
     int32_t rank = vocab;
     if (tok >= 0 && tok < vocab) {

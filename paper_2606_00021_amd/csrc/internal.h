@@ -17,6 +17,11 @@ enum : int { DT_F32 = 0, DT_F16 = 1, DT_BF16 = 2 };
 constexpr int kLaneElems = 8;
 constexpr int kWaveElems = 64 * kLaneElems;
 constexpr int kMaxDim = 8192;       // 16 chunks of 512 elements per lane
+// Verification launches one 256-thread block per judged row along the grid's
+// x dimension, and one dispatch holds fewer than 2^32 work-items per
+// dimension: at most this many (candidate, position) rows per call.
+constexpr int kVerifyRowThreads = 256;
+constexpr int64_t kMaxVerifyRows = (((int64_t)1 << 32) / kVerifyRowThreads) - 1;
 constexpr int kMaxK = 1024;         // largest retrieval top-k
 constexpr int kMaxLen = 64;         // longest draft
 constexpr int kSelectChunk = 8192;  // elements per top-k selection block
@@ -98,9 +103,10 @@ __device__ inline void bitonic_desc(uint64_t* s, int p) {
 hipError_t launch_key_norms(const void* keys, int key_dtype, int64_t n, int d, int64_t ld,
                             float* inv_norm, hipStream_t stream);
 
-// Query batches of at least this many run as an MFMA contraction; smaller
-// ones run the single-query GEMV once per query.
-constexpr int kMfmaMinQueries = 4;
+// Query batches of at least this many run as an MFMA contraction, which
+// reads the store once for the whole batch (a 16-query tile, padded); a
+// single query runs the GEMV, whose fp32 query needs no hi/lo split.
+constexpr int kMfmaMinQueries = 2;
 
 // scores[q * n + i] = similarity of query q and row i for q in [0, nq).
 // queries: nq x d fp32 (already converted).  inv_norm NULL for IP.  split:

@@ -584,8 +584,12 @@ static sense_status_t check_verify_sizes(int32_t n_cand, int32_t max_len, int32_
         return fail(SENSE_ERR_INVALID_ARGUMENT, "max_len = %d outside [1, %d]", max_len,
                     sense::kMaxLen);
     if (vocab < 1) return fail(SENSE_ERR_INVALID_ARGUMENT, "vocab = %d < 1", vocab);
-    if ((int64_t)n_cand * max_len > 0x7FFFFFFFLL)
-        return fail(SENSE_ERR_UNSUPPORTED, "n_cand * max_len too large");
+    if ((int64_t)n_cand * max_len > sense::kMaxVerifyRows)
+        return fail(SENSE_ERR_UNSUPPORTED,
+                    "n_cand * max_len = %lld rows; one call judges at most %lld (one block of "
+                    "%d threads per row, under 2^32 work-items per dispatch)",
+                    (long long)n_cand * max_len, (long long)sense::kMaxVerifyRows,
+                    sense::kVerifyRowThreads);
     return SENSE_OK;
 }
 

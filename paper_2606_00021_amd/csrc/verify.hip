@@ -35,7 +35,7 @@
 namespace sense {
 namespace {
 
-constexpr int kRowThreads = 256;
+constexpr int kRowThreads = kVerifyRowThreads;
 constexpr int kRowWaves = kRowThreads / 64;
 constexpr int kNV = 8;             // 16-byte vectors per thread per slice
 constexpr int kScalarPer = 32;     // elements per thread per slice, unaligned rows
@@ -139,9 +139,13 @@ __device__ __forceinline__ void unpack(const u32x4& w, float (&x)[LT == DT_F32 ?
     }
 }
 
-// Smallest float above x (x finite); +inf and NaN map to themselves.
+// Threshold of "x > x_d" as "x >= next_up(x_d)": the smallest float above a
+// finite or -inf x.  Nothing lies above +inf, so there it is NaN, which no
+// comparison reaches (elements from d on that equal +inf rank below d, as in
+// the stable order); NaN maps to itself.
 __device__ __forceinline__ float next_up(float x) {
-    if (x != x || x == __builtin_inff()) return x;
+    if (x != x) return x;
+    if (x == __builtin_inff()) return __builtin_nanf("");
     if (x == 0.0f) return __builtin_bit_cast(float, 1u);
     const uint32_t u = __builtin_bit_cast(uint32_t, x);
     return __builtin_bit_cast(float, x > 0.0f ? u + 1u : u - 1u);

@@ -123,9 +123,9 @@ class ScoreBound:
 
 def retrieval_path(n_queries: int, d: int) -> str:
     """The scan sense_retrieve runs for a static index: single queries on the
-    vector ALUs (the short-row scan for d <= 64), batches of four or more on
+    vector ALUs (the short-row scan for d <= 64), batches of two or more on
     the matrix cores."""
-    if n_queries >= 4:
+    if n_queries >= 2:
         return "mfma"
     return "short" if d <= 64 else "gemv"
 

@@ -107,6 +107,14 @@ def test_retrieve_rejects_null_index(lib):
                                       None) == INVALID
 
 
+def test_verify_row_limit_in_workspace_query(lib):
+    size = ctypes.c_size_t()
+    assert lib.sense_soft_gate_verify_workspace_size(1 << 18, 64, 1000,
+                                                     ctypes.byref(size)) == UNSUPPORTED
+    assert lib.sense_soft_gate_verify_workspace_size((1 << 18) - 1, 64, 1000,
+                                                     ctypes.byref(size)) == 0
+
+
 def test_noalloc_scratch_size(lib):
     lib.sense_retrieve_noalloc_max_bytes.restype = ctypes.c_size_t
     assert lib.sense_retrieve_noalloc_max_bytes() == 64 << 20
@@ -136,6 +144,9 @@ def verify_call(lib, **kw):
     (dict(dtype=5), INVALID),
     (dict(n_groups=3), INVALID),                     # 8 % 3 != 0
     (dict(n_groups=0), INVALID),
+    # 2^24 rows: one 256-thread block each would pass 2^32 work-items
+    (dict(n_cand=1 << 18, max_len=64), UNSUPPORTED),
+    (dict(n_cand=(1 << 24) + 3, max_len=1), UNSUPPORTED),
     (dict(logits=None), INVALID),
     (dict(drafts=None), INVALID),
     (dict(acc=None), INVALID),

@@ -89,9 +89,12 @@ def test_strided_rows_and_copy():
     run_case(w, seed=6, key_stride=1028, copy_keys=True)   # breaks 16-byte rows: copied
 
 
-def test_several_queries_gemv_loop():
+@pytest.mark.parametrize("nq", [2, 3])
+def test_small_query_batches(nq):
+    """Two or three queries: one matrix-core pass over the store for the batch
+    (a padded 16-query tile), not one scan per query."""
     w = synth.scaled(synth.WORKLOADS["tiny-16k-d4096"], name="multi-q", n=20000, d=2048, k=16,
-                     n_queries=3, n_clusters=80)
+                     n_queries=nq, n_clusters=80)
     run_case(w, seed=9)
 
 
@@ -152,7 +155,8 @@ def _exact_score_columns(n, rng):
 @pytest.mark.parametrize("n,k,nq,d", [
     (3 * 8192 + 777, 1, 8, 128),      # selection levels over raw scores, group size 64
     (3 * 8192 + 777, 64, 8, 128),     # groups of 8 lanes
-    (3 * 8192 + 777, 100, 2, 128),    # groups of 4 lanes, the single-query scan
+    (3 * 8192 + 777, 100, 2, 128),    # groups of 4 lanes, a two-query batch
+    (3 * 8192 + 777, 100, 1, 128),    # the single-query scan
     (5 * 8192 - 3, 600, 8, 128),      # k above the threads of a block: no group bound
     (5 * 8192 - 3, 1024, 1, 128),     # two levels of 1024-key survivors
     (8192, 64, 8, 128),               # one chunk
@@ -200,7 +204,8 @@ def test_exact_scores_select_exactly(n, k, nq, d):
 @pytest.mark.parametrize("n,k,nq,d,n_finite", [
     (40, 40, 1, 128, 35),                 # k = n: every NaN row is returned
     (3 * 8192 + 777, 1024, 8, 128, 600),  # NaN rows fill the tail, matrix-core scan
-    (3 * 8192 + 777, 1024, 2, 128, 600),  # the same through the single-query scan
+    (3 * 8192 + 777, 1024, 1, 128, 600),  # the same through the single-query scan
+    (3 * 8192 + 777, 1024, 3, 128, 600),  # a three-query batch on the matrix cores
     (140_007, 64, 8, 64, 30),             # short keys: the sampled threshold is a NaN key
 ])
 def test_nan_scores_rank_last_by_row(n, k, nq, d, n_finite):

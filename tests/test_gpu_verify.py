@@ -146,3 +146,56 @@ def test_full_size_batched_groups(name):
     logits.scatter_add_(2, drafts.long().unsqueeze(-1), (sharp.to(logits.dtype) * 40).unsqueeze(-1))
     dl = torch.randint(0, w.span + 1, (w.n_cand,), generator=g, device=DEV, dtype=torch.int32)
     run(logits.cpu(), drafts.cpu(), dl.cpu().numpy(), n_groups=w.verify_queries)
+
+
+@pytest.mark.parametrize("dtype,v", [("f32", 3000), ("bf16", 152064), ("f16", 3001)])
+def test_plus_inf_logits_rank_in_stable_order(dtype, v):
+    """+inf logits take their place in the order (logit desc, index asc) like
+    any value: equal +inf values right of the draft token rank below it, left
+    of it above it, in the draft's own 16-byte vector, in others and in other
+    vocabulary slices; such a row's entropy is NaN on both sides (B_ent 0)."""
+    logits, drafts = structured(41, 6, 4, v, dtype="f32")
+    inf = float("inf")
+    d = int(v * 0.6) | 1
+    drafts[:, :] = d
+    logits[0, 0, d] = inf                           # d alone at +inf: rank 0
+    logits[0, 1, d] = inf
+    logits[0, 1, d + 1] = inf                       # right of d, same vector
+    logits[0, 1, v - 1] = inf                       # right of d, another slice
+    logits[0, 2, d] = inf
+    logits[0, 2, d - 1] = inf                       # left of d, same vector: rank 1
+    logits[0, 3, d] = inf
+    logits[0, 3, 5] = inf                           # left of d, first slice
+    logits[0, 3, d - 2] = inf                       # rank 2
+    logits[1, 0, d] = 1e4                           # d the largest finite logit
+    logits[1, 0, 7] = inf                           # one +inf elsewhere: rank 1
+    logits[1, 1, d] = 1e4
+    logits[1, 1, v - 1] = inf
+    logits[1, 1, 0] = inf                           # two above d
+    logits = logits.to(TDT[dtype])
+    out, ref = run(logits, drafts, gamma=0.05, topk=3, window=2)
+    want = {(0, 0): 0, (0, 1): 0, (0, 2): 1, (0, 3): 2, (1, 0): 1, (1, 1): 2}
+    for (cc, jj), r in want.items():
+        assert ref["rank"][cc, jj] == r                 # the oracle's stable order
+    sense_rank = out["rank"].cpu().numpy()
+    for (cc, jj), r in want.items():
+        assert sense_rank[cc, jj] == r
+
+
+def test_nan_logits_stay_in_range():
+    """NaN logits are outside the domain: the call still completes with every
+    output in its range."""
+    c, m, v = 8, 6, 4000
+    logits, drafts = structured(43, c, m, v)
+    logits[0, 0, :] = float("nan")
+    logits[1, 2, 17] = float("nan")
+    logits[2, 1, int(drafts[2, 1])] = float("nan")
+    lens = torch.tensor([6, 6, 3, 0, 6, 2, 6, 6], dtype=torch.int32)
+    out = sense.sense_soft_gate_verify(logits.to(DEV), drafts.to(DEV), lens.to(DEV), n_groups=2)
+    torch.cuda.synchronize()
+    acc = out["accept_len"].cpu().numpy()
+    assert ((acc >= 0) & (acc <= lens.numpy())).all()
+    best = out["best"].cpu().numpy()
+    assert ((best >= 0) & (best < c // 2)).all()
+    rank = out["rank"].cpu().numpy()
+    assert ((rank >= 0) & (rank <= v)).all()

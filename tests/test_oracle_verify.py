@@ -280,3 +280,22 @@ def test_entropy_gate_is_strict():
         assert out["gate_score"][0, 0] == 0.0
         assert (out["masks"][0] & ENT == 0).all()
         assert out["accept_len"][0] == 0
+
+
+def test_plus_inf_logits():
+    """+inf logits keep the stable order (logit desc, index asc) for the rank;
+    the softmax of a row whose maximum is +inf is undefined, so its entropy is
+    NaN and the entropy bit is 0 (the draft is then accepted only as the
+    exact match)."""
+    v = 10
+    x = np.zeros((1, 3, v), dtype=np.float32)
+    x[0, 0, 4] = np.inf                      # the draft itself: rank 0, B_em
+    x[0, 1, [2, 4, 7]] = np.inf              # one +inf left of the draft: rank 1
+    x[0, 2, 9] = np.inf                      # the draft finite: 1 above + 4 equal left = 5
+    drafts = np.full((1, 3), 4, dtype=np.int32)
+    out = oracle.soft_gate_verify(x, "f32", drafts, gamma=-1.0, topk=2, window=0)
+    assert out["rank"].tolist() == [[0, 1, 5]]
+    assert np.isnan(out["gate_score"]).all()
+    assert ((out["masks"] & ENT) == 0).all()
+    assert out["masks"][0, 0] & EM and not out["masks"][0, 1] & EM
+    assert out["accept_len"][0] == 1
