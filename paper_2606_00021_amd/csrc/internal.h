@@ -116,6 +116,35 @@ hipError_t launch_scan(const void* keys, int key_dtype, int64_t n, int d, int64_
                        const float* queries, int nq, bool split, const float* inv_norm,
                        float* scores, void* scratch, hipStream_t stream);
 size_t scan_mfma_scratch_bytes(int nq, int d);
+// One query group (<= 64 queries, already split) of the batched scan over
+// rows 0, row_step, 2 row_step, ... (n_rows of them) of a store of row
+// stride ld.  WRITE mode (scores != NULL): scores[q * n_rows + i].  FILTER
+// mode (cand != NULL): rows whose score reaches the score of tau[q] go to
+// query q's candidate list cand + q * cap as packed (score, row) keys: slots
+// [w * kMfmaSlots, (w + 1) * kMfmaSlots) of wave w (the rest padding keys),
+// then an overflow list whose next position is counts[q] (to be initialised
+// to the slot area, mfma_scan_waves(n_rows) * kMfmaSlots).
+struct MfmaScan {
+    const void* keys;
+    int key_dtype;
+    int64_t ld;
+    int64_t n_rows;
+    int64_t row_step;
+    int d;
+    const uint16_t* qhi;
+    const uint16_t* qlo;
+    const float* inv_qn;
+    int nq;
+    const float* inv_norm;
+    float* scores;            // WRITE mode
+    const uint64_t* tau;      // FILTER mode
+    int32_t* counts;
+    uint64_t* cand;
+    int64_t cap;
+};
+constexpr int kMfmaSlots = 32;
+hipError_t launch_scan_mfma_rows(const MfmaScan& s, bool split, hipStream_t stream);
+int64_t mfma_scan_waves(int64_t n_rows);
 hipError_t launch_scan_mfma(const void* keys, int key_dtype, int64_t n, int d, int64_t ld,
                             const float* queries, int nq, bool split, const float* inv_norm,
                             float* scores, void* scratch, hipStream_t stream);

@@ -153,7 +153,8 @@ constexpr int kTileSecond = 72;               // first entry of rows 8-15
 
 // One workgroup (4 waves) per contiguous run of key blocks; a block is 4*T
 // tiles of 16 keys, T tiles per wave; MT tiles of 16 queries (nq <= 16*MT of
-// them are real).
+// them are real).  The scanned rows are rows 0, row_step, 2 row_step, ... of
+// the store (a strided sample when row_step > 1).
 //
 // Everything the matrix cores read goes through LDS, filled by
 // global_load_lds_dwordx4 (HBM/L2 -> LDS without registers) into a ring of P
@@ -169,12 +170,17 @@ constexpr int kTileSecond = 72;               // first entry of rows 8-15
 // and would otherwise drain the whole pipeline.  Rows past n load the last
 // row (their outputs are never stored); dimensions past d occur only in the
 // last stage, load a clamped address and are zeroed at use.
-template <int KT, int MT, int T, int P, bool SPLIT>
-__global__ __launch_bounds__(256) void scan_mfma_kernel(
-    const uint16_t* __restrict__ keys, int64_t ld, int64_t n, int d,
-    const uint16_t* __restrict__ qhi, const uint16_t* __restrict__ qlo,
-    const float* __restrict__ inv_qn, int nq, const float* __restrict__ inv_norm,
-    float* __restrict__ scores, int64_t blocks_per_group) {
+//
+// Epilogue per block: WRITE mode stores every score; FILTER mode keeps only
+// rows whose score reaches the query's threshold (tau, the packed key of the
+// k-th best row of a sample: every row of the true top k reaches it) as
+// packed (score, row) keys in the query's candidate list: this wave's
+// kMfmaSlots slots first (positions from ballot prefix counts), then the
+// query's overflow list (atomic position).  At Q = 64 the score matrix would
+// be 64 x 4 bytes per row of 16 KiB, few bytes but scattered 64-byte writes
+// that cut the scan's read rate by a fifth; the survivors are ~k*row_step.
+template <int KT, int MT, int T, int P, bool SPLIT, bool FILTER>
+__global__ __launch_bounds__(256) void scan_mfma_kernel(MfmaScan s, int64_t blocks_per_group) {
     constexpr int NA = MT * (SPLIT ? 2 : 1);      // query fragments per step
     constexpr int NAS = 2 * NA;                   // per stage
     constexpr int NA_W = (NAS + 3) / 4;           // loaded per wave
@@ -183,6 +189,10 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
     static_assert((P - 2) * OPS < 64, "vmcnt range");
     __shared__ __attribute__((aligned(16))) u32x4 kring[P][4][T][kTileVec];
     __shared__ __attribute__((aligned(16))) u32x4 aring[P][NA_W * 4][64];
+    const uint16_t* __restrict__ keys = (const uint16_t*)s.keys;
+    const int d = s.d;
+    const int64_t n = s.n_rows;
+    const int64_t rstride = s.ld * s.row_step;    // elements between scanned rows
     const int lane = threadIdx.x & 63;
     const int wv = threadIdx.x >> 6;
     const int col = lane & 15, grp = lane >> 4;
@@ -190,7 +200,6 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
     const int du = ((lane & 7) + dp) & 7;         // DMA: 16-byte unit fetched
     const int64_t nblk = (n + KB - 1) / KB;
     const int64_t b0 = (int64_t)blockIdx.x * blocks_per_group;
-    if (b0 >= nblk) return;                       // uniform over the workgroup
     const int64_t b1 = (b0 + blocks_per_group < nblk) ? b0 + blocks_per_group : nblk;
     const int nks = (d + 31) / 32;
     const int nst = (nks + 1) / 2;
@@ -205,20 +214,32 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
         int fs = wv + 4 * j;
         if (fs >= NAS) fs = NAS - 1;              // idle slot: harmless duplicate
         const int f = fs % NA;
-        const uint16_t* base = (f < MT) ? qhi : qlo;
+        const uint16_t* base = (f < MT) ? s.qhi : s.qlo;
         const int mt = f % MT;
         qsrc[j] = base + (int64_t)(mt * 16 + col) * d + grp * 8;
         qstep[j] = fs / NA;
     }
-    // 1/|q| of this lane's output rows, once: the batch is padded to whole
-    // 16-query tiles, so every index is in bounds.  (Loaded per block under
-    // the q < nq test, each load would wait for the one before it, with no
-    // other workgroup on the CU to cover the wait.)
-    float iq[MT][4];
+    // 1/|q| of this lane's output rows, once (the batch is padded to whole
+    // 16-query tiles, so every index is in bounds), and in FILTER mode their
+    // threshold scores (+inf for padding queries: nothing passes; a NaN
+    // threshold, from a sample of fewer than k rows, lets every row pass).
+    float iq[MT][4], th[MT][4];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) iq[mt][i] = inv_qn[mt * 16 + grp * 4 + i];
+        for (int i = 0; i < 4; ++i) {
+            const int q = mt * 16 + grp * 4 + i;
+            iq[mt][i] = s.inv_qn[q];
+            if constexpr (FILTER)
+                th[mt][i] = q < s.nq ? key_score((uint32_t)(s.tau[q] >> 32)) : __builtin_inff();
+        }
+    // FILTER: survivors so far of this wave per query (equal in a 16-lane group).
+    int cnt[MT][4];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) cnt[mt][i] = 0;
+    const int64_t wave_slot = ((int64_t)blockIdx.x * 4 + wv) * kMfmaSlots;
     // B-operand entry of this lane inside a key tile, for unit u = 4*step + grp.
     const int ri = col >> 3, rp = col & 7;
     auto bentry = [&](int step) { return ri * kTileSecond + 8 * rp + (((4 * step + grp) - rp) & 7); };
@@ -234,7 +255,7 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
             for (int i = 0; i < 2; ++i) {
                 int64_t row = key0 + t * 16 + 8 * i + dp;
                 if (row >= n) row = n - 1;
-                kp[t][i] = keys + row * ld + du * 8;
+                kp[t][i] = keys + row * rstride + du * 8;
             }
         }
         auto issue = [&](int st) {
@@ -261,7 +282,7 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
             for (int mt = 0; mt < MT; ++mt) acc[t][mt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 
 #pragma unroll
-        for (int s = 0; s < P - 1; ++s) issue(s);
+        for (int st = 0; st < P - 1; ++st) issue(st);
         for (int st = 0; st < nst; ++st) {
             // Loads issued after stage st: stages st+1 .. st+P-2.
             wait_vmcnt<(P - 2) * OPS>();
@@ -303,7 +324,7 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
 #pragma unroll
         for (int t = 0; t < T; ++t) {
             const int64_t key = key0 + t * 16 + col;
-            kscale[t] = inv_norm ? inv_norm[key < n ? key : n - 1] : 1.0f;
+            kscale[t] = s.inv_norm ? s.inv_norm[(key < n ? key : n - 1) * s.row_step] : 1.0f;
         }
         // Take delivery of the scales here, once: a load still pending when
         // the conditional stores start would cost a full wait before each
@@ -317,49 +338,107 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(
 #pragma unroll
         for (int t = 0; t < T; ++t) {
             const int64_t key = key0 + t * 16 + col;
-            if (!kv[t]) continue;
+            if constexpr (!FILTER) {
+                if (!kv[t]) continue;
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt) {
+                for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int q = mt * 16 + grp * 4 + i;
-                    if (q < nq) {
-                        float v = acc[t][mt][i];
-                        if (inv_norm) v = v * kscale[t];
-                        scores[(int64_t)q * n + key] = v * iq[mt][i];
+                    for (int i = 0; i < 4; ++i) {
+                        const int q = mt * 16 + grp * 4 + i;
+                        if (q < s.nq) {
+                            float v = acc[t][mt][i];
+                            if (s.inv_norm) v = v * kscale[t];
+                            s.scores[(int64_t)q * n + key] = v * iq[mt][i];
+                        }
+                    }
+                }
+            } else {
+                // One compare per score, then a branch per (query, tile) only
+                // where something passed.
+                float v[MT][4];
+                uint64_t bal[MT][4];
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        v[mt][i] = acc[t][mt][i];
+                        if (s.inv_norm) v[mt][i] = v[mt][i] * kscale[t];
+                        v[mt][i] = v[mt][i] * iq[mt][i];
+                        bal[mt][i] = __ballot(kv[t] & !(v[mt][i] < th[mt][i]));
+                    }
+                const uint32_t orig = (uint32_t)(key * s.row_step);
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        if (bal[mt][i] == 0) continue;
+                        const int q = mt * 16 + grp * 4 + i;
+                        const bool pass = (bal[mt][i] >> lane) & 1;
+                        const uint32_t gm = (uint32_t)(bal[mt][i] >> (16 * grp)) & 0xFFFFu;
+                        const int slot = cnt[mt][i] + __popc(gm & ((1u << col) - 1u));
+                        if (pass && q < s.nq) {
+                            uint64_t* cq = s.cand + (int64_t)q * s.cap;
+                            const uint64_t pk = pack_key(v[mt][i], orig);
+                            if (slot < kMfmaSlots) {
+                                cq[wave_slot + slot] = pk;
+                            } else {
+                                const int pos = atomicAdd(&s.counts[q], 1);
+                                cq[pos] = pk;
+                            }
+                        }
+                        cnt[mt][i] += __popc(gm);
                     }
                 }
             }
         }
     }
+    if constexpr (FILTER) {
+        // Unused slots become padding keys.  Lane col 0 of each group saw
+        // every tile its group saw, so its counts are the group's.
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int c0 = __shfl(cnt[mt][i], lane & ~15, 64);
+                const int q = mt * 16 + grp * 4 + i;
+                if (q < s.nq)
+                    for (int j = col; j < kMfmaSlots; j += 16)
+                        if (j >= c0) s.cand[(int64_t)q * s.cap + wave_slot + j] = 0;
+            }
+    }
 }
 
-
-template <int KT, int MT, int T, int P, bool SPLIT>
-hipError_t launch_tile(const void* keys, int64_t n, int d, int64_t ld, const uint16_t* qhi,
-                       const uint16_t* qlo, const float* inv_qn, int nq, const float* inv_norm,
-                       float* scores, hipStream_t stream) {
-    auto kern = scan_mfma_kernel<KT, MT, T, P, SPLIT>;
-    static const int per_cu = blocks_per_cu(kern, 256, 1);
-    const int64_t nblk = (n + 64 * T - 1) / (64 * T);
-    const int64_t groups_max = (int64_t)device_cus() * per_cu;
+// Grid of the batched scan: one resident workgroup per compute unit (the
+// kernels' LDS ring allows one), an equal run of blocks each.
+int64_t mfma_groups(int64_t n_rows, int T) {
+    const int64_t nblk = (n_rows + 64 * T - 1) / (64 * T);
+    const int64_t groups_max = (int64_t)device_cus();
     int64_t bpg = (nblk + groups_max - 1) / groups_max;
     if (bpg < 1) bpg = 1;
-    const int64_t groups = (nblk + bpg - 1) / bpg;
-    hipLaunchKernelGGL(kern, dim3((unsigned)groups), dim3(256), 0, stream, (const uint16_t*)keys,
-                       ld, n, d, qhi, qlo, inv_qn, nq, inv_norm, scores, bpg);
+    return (nblk + bpg - 1) / bpg;
+}
+
+template <int KT, int MT, int T, int P, bool SPLIT>
+hipError_t launch_tile(const MfmaScan& s, hipStream_t stream) {
+    const int64_t nblk = (s.n_rows + 64 * T - 1) / (64 * T);
+    const int64_t groups = mfma_groups(s.n_rows, T);
+    const int64_t bpg = (nblk + groups - 1) / groups;
+    if (s.cand)
+        hipLaunchKernelGGL((scan_mfma_kernel<KT, MT, T, P, SPLIT, true>), dim3((unsigned)groups),
+                           dim3(256), 0, stream, s, bpg);
+    else
+        hipLaunchKernelGGL((scan_mfma_kernel<KT, MT, T, P, SPLIT, false>), dim3((unsigned)groups),
+                           dim3(256), 0, stream, s, bpg);
     return hipGetLastError();
 }
 
 template <int KT, bool SPLIT>
-hipError_t launch_group(const void* keys, int64_t n, int d, int64_t ld, const uint16_t* qhi,
-                        const uint16_t* qlo, const float* inv_qn, int nq, const float* inv_norm,
-                        float* scores, hipStream_t stream) {
-    switch ((nq + 15) / 16) {
-        case 1: return launch_tile<KT, 1, 4, 4, SPLIT>(keys, n, d, ld, qhi, qlo, inv_qn, nq, inv_norm, scores, stream);
-        case 2: return launch_tile<KT, 2, 4, 3, SPLIT>(keys, n, d, ld, qhi, qlo, inv_qn, nq, inv_norm, scores, stream);
-        case 3: return launch_tile<KT, 3, 4, 3, SPLIT>(keys, n, d, ld, qhi, qlo, inv_qn, nq, inv_norm, scores, stream);
-        default: return launch_tile<KT, 4, 4, 3, SPLIT>(keys, n, d, ld, qhi, qlo, inv_qn, nq, inv_norm, scores, stream);
+hipError_t launch_group(const MfmaScan& s, hipStream_t stream) {
+    switch ((s.nq + 15) / 16) {
+        case 1: return launch_tile<KT, 1, 4, 4, SPLIT>(s, stream);
+        case 2: return launch_tile<KT, 2, 4, 3, SPLIT>(s, stream);
+        case 3: return launch_tile<KT, 3, 4, 3, SPLIT>(s, stream);
+        default: return launch_tile<KT, 4, 4, 3, SPLIT>(s, stream);
     }
 }
 
@@ -390,28 +469,36 @@ hipError_t launch_query_split(const float* queries, int nq, int d, int key_dtype
     return hipGetLastError();
 }
 
+int64_t mfma_scan_waves(int64_t n_rows) { return mfma_groups(n_rows, 4) * 4; }
+
+hipError_t launch_scan_mfma_rows(const MfmaScan& s, bool split, hipStream_t stream) {
+    if (s.key_dtype == DT_BF16)
+        return split ? launch_group<DT_BF16, true>(s, stream) : launch_group<DT_BF16, false>(s, stream);
+    return split ? launch_group<DT_F16, true>(s, stream) : launch_group<DT_F16, false>(s, stream);
+}
+
 hipError_t launch_scan_mfma(const void* keys, int key_dtype, int64_t n, int d, int64_t ld,
                             const float* queries, int nq, bool split, const float* inv_norm,
                             float* scores, void* scratch, hipStream_t stream) {
     const QuerySplit p = query_split_parts(scratch, nq, d);
-    uint16_t* qhi = p.hi;
-    uint16_t* qlo = p.lo;
-    float* inv_qn = p.inv_qn;
     hipError_t e = launch_query_split(queries, nq, d, key_dtype, inv_norm != nullptr, scratch,
                                       stream);
     if (e != hipSuccess) return e;
     for (int g0 = 0; g0 < nq; g0 += 64) {
-        const int ng = (nq - g0 < 64) ? nq - g0 : 64;
-        const uint16_t* h = qhi + (int64_t)g0 * d;
-        const uint16_t* lo = qlo + (int64_t)g0 * d;
-        float* sc = scores + (int64_t)g0 * n;
-        if (key_dtype == DT_BF16)
-            e = split ? launch_group<DT_BF16, true>(keys, n, d, ld, h, lo, inv_qn + g0, ng, inv_norm, sc, stream)
-                      : launch_group<DT_BF16, false>(keys, n, d, ld, h, lo, inv_qn + g0, ng, inv_norm, sc, stream);
-        else
-            e = split ? launch_group<DT_F16, true>(keys, n, d, ld, h, lo, inv_qn + g0, ng, inv_norm, sc, stream)
-                      : launch_group<DT_F16, false>(keys, n, d, ld, h, lo, inv_qn + g0, ng, inv_norm, sc, stream);
-        if (e != hipSuccess) return e;
+        MfmaScan s{};
+        s.keys = keys;
+        s.key_dtype = key_dtype;
+        s.ld = ld;
+        s.n_rows = n;
+        s.row_step = 1;
+        s.d = d;
+        s.qhi = p.hi + (int64_t)g0 * d;
+        s.qlo = p.lo + (int64_t)g0 * d;
+        s.inv_qn = p.inv_qn + g0;
+        s.nq = (nq - g0 < 64) ? nq - g0 : 64;
+        s.inv_norm = inv_norm;
+        s.scores = scores + (int64_t)g0 * n;
+        if ((e = launch_scan_mfma_rows(s, split, stream)) != hipSuccess) return e;
     }
     return hipSuccess;
 }

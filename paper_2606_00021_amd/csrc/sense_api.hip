@@ -101,13 +101,30 @@ bool short_batched(const sense_index* ix, int nq) {
     return ix->d <= sense::kSmallDim && nq >= sense::kMfmaMinQueries;
 }
 
+// Long keys, query batches: the matrix-core scan.  Stores of more than
+// kBatchDirectMax rows are searched like the short keys (a strided sample's
+// k-th best as the threshold of a filtered pass), smaller ones through the
+// plain score matrix.
+constexpr int64_t kBatchSample = 32768;
+constexpr int64_t kBatchDirectMax = 131072;
+
+bool long_batched(const sense_index* ix, int nq) {
+    return ix->d > sense::kSmallDim && nq >= sense::kMfmaMinQueries;
+}
+
 struct ShortLayout {
     size_t q_off, m_off, ss_off, sid_off, ssc_off, sws_off, tau_off, cnt_off, cand_off, fws_off,
         total;
 };
 
+// Workspace of the sampled-threshold retrieval (short keys, or long keys in
+// batches): query split, sample scores and top-k, thresholds and counts, the
+// candidate lists (wave slots + an overflow list of up to every row) or, for
+// a store searched directly, the plain score matrix in the same area.
 ShortLayout short_layout(const sense_index* ix, int nq, int k) {
     ShortLayout l;
+    const bool long_keys = ix->d > sense::kSmallDim;
+    const int64_t sample = long_keys ? kBatchSample : kShortSample;
     const int64_t rows = ix->capacity > 0 ? ix->capacity : ix->n;
     const int g = nq < 64 ? nq : 64;
     size_t at = 0;
@@ -118,15 +135,16 @@ ShortLayout short_layout(const sense_index* ix, int nq, int k) {
     };
     l.q_off = take((size_t)nq * ix->d * sizeof(float));
     l.m_off = take(sense::scan_mfma_scratch_bytes(nq, ix->d));
-    l.ss_off = take((size_t)g * kShortSample * sizeof(float));
+    l.ss_off = take((size_t)g * sample * sizeof(float));
     l.sid_off = take((size_t)g * k * sizeof(int64_t));
     l.ssc_off = take((size_t)g * k * sizeof(float));
-    l.sws_off = take(sense::topk_workspace_bytes(kShortSample, g, k));
+    l.sws_off = take(sense::topk_workspace_bytes(sample, g, k));
     l.tau_off = take((size_t)g * sizeof(uint64_t));
     l.cnt_off = take((size_t)g * sizeof(int32_t));
     // candidates per query: the wave slots, then an overflow list of up to
     // every row; also the plain score matrix of small stores
-    const int64_t cap = sense::short_scan_waves(rows) * sense::kShortSlots + rows;
+    const int64_t cap = long_keys ? sense::mfma_scan_waves(rows) * sense::kMfmaSlots + rows
+                                  : sense::short_scan_waves(rows) * sense::kShortSlots + rows;
     l.cand_off = take((size_t)g * cap * sizeof(uint64_t));
     l.fws_off = take(sense::topk_workspace_bytes(cap, g, k));
     l.total = at;
@@ -135,7 +153,7 @@ ShortLayout short_layout(const sense_index* ix, int nq, int k) {
 
 RetrieveLayout retrieve_layout(const sense_index* ix, int nq, int k) {
     RetrieveLayout l;
-    if (short_batched(ix, nq)) {
+    if (short_batched(ix, nq) || long_batched(ix, nq)) {
         const ShortLayout sl = short_layout(ix, nq, k);
         l.q_off = sl.q_off;
         l.m_off = sl.m_off;
@@ -469,6 +487,92 @@ static hipError_t retrieve_short(const sense_index* ix, const float* qptr, int n
     return timer_mark(SENSE_TIMER_SCAN, 1, st);
 }
 
+// Long keys, query batch: per group of <= 64 queries either plain scores +
+// top-k (stores of up to kBatchDirectMax rows) or a strided sample's k-th
+// best key as a threshold, a filtered matrix-core pass over every row, and
+// the top-k of the survivors (exact: every row of the true top k reaches the
+// threshold).  The scan timer spans the sample, its top-k and the filtered
+// pass; the top-k timer the final selection.
+static hipError_t retrieve_batched(const sense_index* ix, const float* qptr, int nq, int k,
+                                   bool split, int64_t* out_ids, float* out_scores,
+                                   int32_t* out_drafts, int32_t* out_draft_len, char* ws,
+                                   hipStream_t st) {
+    const ShortLayout L = short_layout(ix, nq, k);
+    const int64_t n = ix->n;
+    hipError_t e;
+    if ((e = timer_mark(SENSE_TIMER_SCAN, 0, st)) != hipSuccess) return e;
+    if ((e = sense::launch_query_split(qptr, nq, ix->d, ix->key_dtype, ix->inv_norm != nullptr,
+                                       ws + L.m_off, st)) != hipSuccess)
+        return e;
+    const sense::QuerySplit qs = sense::query_split_parts(ws + L.m_off, nq, ix->d);
+    const bool sample = n > kBatchDirectMax;
+    const int64_t step = sample ? n / kBatchSample : 1;
+    const int64_t slot_area = sense::mfma_scan_waves(n) * sense::kMfmaSlots;
+    for (int g0 = 0; g0 < nq; g0 += 64) {
+        const int ng = nq - g0 < 64 ? nq - g0 : 64;
+        sense::MfmaScan S{};
+        S.keys = ix->keys;
+        S.key_dtype = ix->key_dtype;
+        S.ld = ix->ld;
+        S.d = ix->d;
+        S.qhi = qs.hi + (int64_t)g0 * ix->d;
+        S.qlo = qs.lo + (int64_t)g0 * ix->d;
+        S.inv_qn = qs.inv_qn + g0;
+        S.nq = ng;
+        S.inv_norm = ix->inv_norm;
+        int64_t* gid = out_ids + (int64_t)g0 * k;
+        float* gsc = out_scores ? out_scores + (int64_t)g0 * k : nullptr;
+        int32_t* gdr = out_drafts ? out_drafts + (int64_t)g0 * k * ix->max_span : nullptr;
+        int32_t* gdl = out_draft_len ? out_draft_len + (int64_t)g0 * k : nullptr;
+        const bool last = g0 + 64 >= nq;
+        if (!sample) {
+            S.n_rows = n;
+            S.row_step = 1;
+            S.scores = (float*)(ws + L.cand_off);
+            if ((e = sense::launch_scan_mfma_rows(S, split, st)) != hipSuccess) return e;
+            if (last && (e = timer_mark(SENSE_TIMER_SCAN, 1, st)) != hipSuccess) return e;
+            if (last && (e = timer_mark(SENSE_TIMER_TOPK, 0, st)) != hipSuccess) return e;
+            if ((e = sense::launch_topk_gather(S.scores, n, ng, k, ix->spans, ix->span_len,
+                                               ix->max_span, ix->span_stride, gid, gsc, gdr,
+                                               gdl, ws + L.fws_off, st)) != hipSuccess)
+                return e;
+            continue;
+        }
+        // Threshold from the sample rows 0, step, 2 step, ...
+        S.n_rows = kBatchSample;
+        S.row_step = step;
+        S.scores = (float*)(ws + L.ss_off);
+        if ((e = sense::launch_scan_mfma_rows(S, split, st)) != hipSuccess) return e;
+        int64_t* sid = (int64_t*)(ws + L.sid_off);
+        float* ssc = (float*)(ws + L.ssc_off);
+        if ((e = sense::launch_topk_gather(S.scores, kBatchSample, ng, k, nullptr, nullptr, 1, 1,
+                                           sid, ssc, nullptr, nullptr, ws + L.sws_off, st)) !=
+            hipSuccess)
+            return e;
+        uint64_t* tau = (uint64_t*)(ws + L.tau_off);
+        int32_t* cnt = (int32_t*)(ws + L.cnt_off);
+        if ((e = sense::launch_short_tau(sid, ssc, ng, k, step, (int32_t)slot_area, tau, cnt,
+                                         st)) != hipSuccess)
+            return e;
+        // Every row; only keys whose score reaches tau's are kept.
+        S.n_rows = n;
+        S.row_step = 1;
+        S.scores = nullptr;
+        S.tau = tau;
+        S.counts = cnt;
+        S.cand = (uint64_t*)(ws + L.cand_off);
+        S.cap = slot_area + n;
+        if ((e = sense::launch_scan_mfma_rows(S, split, st)) != hipSuccess) return e;
+        if (last && (e = timer_mark(SENSE_TIMER_SCAN, 1, st)) != hipSuccess) return e;
+        if (last && (e = timer_mark(SENSE_TIMER_TOPK, 0, st)) != hipSuccess) return e;
+        if ((e = sense::launch_topk_keys(S.cand, S.cap, ng, k, ix->spans, ix->span_len,
+                                         ix->max_span, ix->span_stride, gid, gsc, gdr, gdl, cnt,
+                                         st)) != hipSuccess)
+            return e;
+    }
+    return timer_mark(SENSE_TIMER_TOPK, 1, st);
+}
+
 SENSE_EXPORT sense_status_t sense_retrieve(const sense_index_t* ix, const void* queries,
                                            sense_dtype_t q_dtype, int32_t nq, int32_t k,
                                            int64_t* out_ids, float* out_scores,
@@ -504,6 +608,12 @@ SENSE_EXPORT sense_status_t sense_retrieve(const sense_index_t* ix, const void* 
         if ((e = retrieve_short(ix, qptr, nq, k, split, out_ids, out_scores, out_drafts,
                                 out_draft_len, ws, st)) != hipSuccess)
             return hip_fail(e, "short-key batched retrieval");
+        return ok();
+    }
+    if (long_batched(ix, nq)) {
+        if ((e = retrieve_batched(ix, qptr, nq, k, split, out_ids, out_scores, out_drafts,
+                                  out_draft_len, ws, st)) != hipSuccess)
+            return hip_fail(e, "batched retrieval");
         return ok();
     }
     if ((e = timer_mark(SENSE_TIMER_SCAN, 0, st)) != hipSuccess) return hip_fail(e, "timer");

@@ -106,6 +106,12 @@ BATCHED = [
     ("q40-d4096-bf16", 9000, 4096, "bf16", 40, 8),
     ("q64-d8192-bf16", 5000, 8192, "bf16", 64, 128),
     ("q70-d512-bf16", 3000, 512, "bf16", 70, 16),         # two query groups of <= 64
+    # stores of more than 131072 rows: a strided sample's k-th best score is
+    # each query's threshold and the full pass keeps only the rows reaching it
+    ("q8-sampled-d256-bf16", 140_007, 256, "bf16", 8, 64),
+    ("q5-sampled-d1000-bf16", 150_001, 1000, "bf16", 5, 16),   # ragged 32-dim step
+    ("q64-sampled-d128-f16", 200_003, 128, "f16", 64, 128),
+    ("q70-sampled-d96-bf16", 135_000, 96, "bf16", 70, 32),     # two sampled query groups
 ]
 
 
@@ -171,6 +177,12 @@ def _exact_score_columns(n, rng):
     (140_007, 1, 8, 16),
     (140_007, 1024, 8, 64),
     (300_001, 64, 64, 32),
+    # long keys, batches over more than 131072 rows: the matrix-core scan's
+    # sampled threshold, with ties at the threshold
+    (140_007, 64, 8, 128),
+    (140_007, 1, 16, 128),
+    (140_007, 1024, 8, 128),
+    (300_001, 64, 64, 96),
 ])
 def test_exact_scores_select_exactly(n, k, nq, d):
     """Inner products of one-hot fp32 queries with bf16 keys are exact, so the
@@ -207,6 +219,7 @@ def test_exact_scores_select_exactly(n, k, nq, d):
     (3 * 8192 + 777, 1024, 1, 128, 600),  # the same through the single-query scan
     (3 * 8192 + 777, 1024, 3, 128, 600),  # a three-query batch on the matrix cores
     (140_007, 64, 8, 64, 30),             # short keys: the sampled threshold is a NaN key
+    (140_007, 64, 8, 128, 30),            # long keys, matrix-core scan: the same
 ])
 def test_nan_scores_rank_last_by_row(n, k, nq, d, n_finite):
     """Rows whose score is NaN rank after every number, among themselves by
