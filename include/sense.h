@@ -628,7 +628,10 @@ typedef enum SENSE_ENUM_BASE {
     SENSE_TIMER_SELECT = 3, /* the kernel of sense_select_candidates */
     SENSE_TIMER_TRIE = 4,   /* the kernels of sense_build_loose_trie */
     SENSE_TIMER_PROJECT = 5, /* the kernels of sense_project */
-    SENSE_TIMER_IVF = 6      /* the kernels of sense_ivf_search */
+    SENSE_TIMER_IVF = 6,     /* the kernels of sense_ivf_search */
+    SENSE_TIMER_FILTER = 7   /* the filtered full pass over the store of a
+                                sampled-threshold batched sense_retrieve
+                                (first group of 64 queries); a part of SCAN */
 } sense_timer_t;
 
 /* Register two hipEvent_t handles (created by the caller with timing

@@ -241,11 +241,14 @@ int blocks_per_cu(Kernel kern, int threads, int fallback) {
 
 // The queries of a batch padded to qpad = 16*ceil(nq/16) rows and split
 // into hi + lo halves of the key type (a scratch of scan_mfma_scratch_bytes),
-// with inv_qn[q] = 1/||q|| (cosine), 1 (inner product), 0 (padding).
+// with inv_qn[q] = 1/||q|| (cosine), 1 (inner product), 0 (padding), and
+// margin[q] (cosine): twice a bound on |hi-only matrix-core score - fp32
+// rescore| of any row.
 struct QuerySplit {
     uint16_t* hi;
     uint16_t* lo;
     float* inv_qn;
+    float* margin;
     int qpad;
 };
 QuerySplit query_split_parts(void* scratch, int nq, int d);
@@ -282,10 +285,21 @@ struct ShortScan {
 };
 hipError_t launch_scan_short(const ShortScan& s, hipStream_t stream);
 // tau[q] = packed key of the k-th best row of a strided sample (the sample
-// top-k's ids are sample positions; row = id * row_step).
+// top-k's ids are sample positions; row = id * row_step), its score lowered
+// by margin[q] when margin is not NULL; counts[q] = slot_area.
 hipError_t launch_short_tau(const int64_t* ids, const float* scores, int nq, int k,
-                            int64_t row_step, int32_t slot_area, uint64_t* tau, int32_t* counts,
-                            hipStream_t stream);
+                            int64_t row_step, int32_t slot_area, const float* margin,
+                            uint64_t* tau, int32_t* counts, hipStream_t stream);
+// The band and rescore stages of a hi-only filtered search (scan_mfma.hip):
+// launch_band keeps the candidates whose approximate score reaches
+// kth[q * k + k - 1] - margin[q] (counts become the band sizes);
+// launch_rescore replaces each band entry by its fp32 rescore.
+hipError_t launch_band(uint64_t* cand, int64_t cap, int nq, const float* kth, int k,
+                       const float* margin, int32_t* counts, hipStream_t stream);
+hipError_t launch_rescore(uint64_t* cand, int64_t cap, int nq, const int32_t* counts,
+                          const void* keys, int key_dtype, int64_t ld, int d,
+                          const float* queries, const float* inv_norm, const float* inv_qn,
+                          hipStream_t stream);
 
 // Plain streaming read of a device buffer (bandwidth probe).
 hipError_t launch_stream_read(const void* buf, size_t bytes, uint32_t* sink, hipStream_t stream);

@@ -63,15 +63,25 @@ __device__ __forceinline__ float from_key_bits(uint16_t b) {
 
 // Pads the query batch to qpad rows and splits each fp32 value into hi + lo
 // in the key type; inv_qn[q] = 1/||q|| (cosine), 1 (inner product), 0 for
-// padding rows.  One block (256 threads) per padded query row.
+// padding rows.  margin[q] (cosine; 0 otherwise) is twice a bound on the
+// difference between a score taken with the hi half alone on the matrix
+// cores and the fp32 rescore of the same row (rescore_kernel):
+//   |A - R| <= ||q - hi|| / ||q||                      (Cauchy-Schwarz)
+//            + fp32 rounding of both sums, the norms and the products,
+// the rounding terms doubled for safety and the split term raised by 1 %
+// (its own fp32 evaluation is good to ~d * 2^-24).  Scores are cosines, so
+// every term is relative to 1.  An overflowing split (an f16 hi half of
+// |x| > 65504) gives an infinite or NaN margin: every row then passes.
+// One block (256 threads) per padded query row.
 template <int KT>
 __global__ __launch_bounds__(256) void query_split_kernel(const float* __restrict__ q, int nq,
                                                           int d, bool cosine,
                                                           uint16_t* __restrict__ qhi,
                                                           uint16_t* __restrict__ qlo,
-                                                          float* __restrict__ inv_qn) {
+                                                          float* __restrict__ inv_qn,
+                                                          float* __restrict__ margin) {
     const int row = blockIdx.x;
-    float ss = 0.0f;
+    float ss = 0.0f, ll = 0.0f;
     for (int t = threadIdx.x; t < d; t += 256) {
         const float x = row < nq ? q[(int64_t)row * d + t] : 0.0f;
         const uint16_t hb = to_key_bits<KT>(x);
@@ -79,20 +89,35 @@ __global__ __launch_bounds__(256) void query_split_kernel(const float* __restric
         qhi[(int64_t)row * d + t] = hb;
         qlo[(int64_t)row * d + t] = to_key_bits<KT>(lo);
         ss = __builtin_fmaf(x, x, ss);
+        ll = __builtin_fmaf(lo, lo, ll);
     }
-    __shared__ float s_part[256];
-    s_part[threadIdx.x] = ss;
+    __shared__ float s_part[2][256];
+    s_part[0][threadIdx.x] = ss;
+    s_part[1][threadIdx.x] = ll;
     __syncthreads();
     for (int off = 128; off > 0; off >>= 1) {
-        if ((int)threadIdx.x < off) s_part[threadIdx.x] += s_part[threadIdx.x + off];
+        if ((int)threadIdx.x < off) {
+            s_part[0][threadIdx.x] += s_part[0][threadIdx.x + off];
+            s_part[1][threadIdx.x] += s_part[1][threadIdx.x + off];
+        }
         __syncthreads();
     }
     if (threadIdx.x == 0) {
-        const float s = s_part[0];
+        const float s = s_part[0][0];
         float v = 1.0f;
         if (row >= nq) v = 0.0f;
         else if (cosine) v = (s > 0.0f) ? 1.0f / __builtin_sqrtf(s) : 0.0f;
         inv_qn[row] = v;
+        float m = 0.0f;
+        if (row < nq && cosine) {
+            // summation depth of the hi-only matrix-core sum, of the rescore,
+            // and of each fp32 inverse norm, plus the final products
+            const float depth = (float)((d + 31) / 32 + 8) + (float)(d / 128 + 8) +
+                                2.0f * (float)(d / 64 + 16) + 4.0f;
+            const float rnd = depth * 5.9604645e-8f;          // x 2^-24
+            m = 2.0f * (1.01f * __builtin_sqrtf(s_part[1][0]) * v + 2.0f * 1.01f * rnd);
+        }
+        margin[row] = m;
     }
 }
 
@@ -442,19 +467,144 @@ hipError_t launch_group(const MfmaScan& s, hipStream_t stream) {
     }
 }
 
+// Band of a hi-only filtered search: keeps, in place, the entries of query
+// q's candidate list (packed (approximate score, row) keys, padding keys 0)
+// whose approximate score is not below kth[q * k + k - 1] - margin[q], the
+// k-th best approximate score of the list less twice the bound on
+// |approximate - rescored|; a NaN on either side keeps the entry.  Every row
+// whose rescored value can reach the rescored k-th best is kept.  counts[q]
+// (the list's length) becomes the number kept; the order of the kept entries
+// is not specified.  One block of 1024 threads per query.  Writes go only to
+// positions already read: the kept count never exceeds the entries read, and
+// every read of a round returns (its value decides a ballot) before the
+// barrier that precedes the round's writes.
+constexpr int kBandThreads = 1024;
+constexpr int kBandPer = 4;
+__global__ __launch_bounds__(kBandThreads) void band_kernel(uint64_t* __restrict__ cand,
+                                                            int64_t cap,
+                                                            const float* __restrict__ kth, int k,
+                                                            const float* __restrict__ margin,
+                                                            int32_t* __restrict__ counts) {
+    const int q = blockIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63;
+    uint64_t* __restrict__ list = cand + (int64_t)q * cap;
+    int64_t cnt = counts[q];
+    cnt = cnt < 0 ? 0 : (cnt > cap ? cap : cnt);
+    const float th = kth[(int64_t)q * k + (k - 1)] - margin[q];
+    __shared__ int s_next;
+    if (tid == 0) s_next = 0;
+    __syncthreads();
+    for (int64_t c0 = 0; c0 < cnt; c0 += (int64_t)kBandThreads * kBandPer) {
+        uint64_t key[kBandPer];
+#pragma unroll
+        for (int j = 0; j < kBandPer; ++j) {
+            const int64_t i = c0 + (int64_t)j * kBandThreads + tid;
+            key[j] = i < cnt ? list[i] : 0ull;
+        }
+        uint64_t bal[kBandPer];
+        int wb[kBandPer];
+#pragma unroll
+        for (int j = 0; j < kBandPer; ++j) {
+            const bool keep = key[j] != 0ull && !(key_score((uint32_t)(key[j] >> 32)) < th);
+            bal[j] = __ballot(keep);
+            int b = 0;
+            if (lane == 0 && bal[j]) b = atomicAdd(&s_next, __popcll(bal[j]));
+            wb[j] = __shfl(b, 0, 64);
+        }
+        __syncthreads();
+        const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+#pragma unroll
+        for (int j = 0; j < kBandPer; ++j)
+            if ((bal[j] >> lane) & 1ull) list[wb[j] + __popcll(bal[j] & below)] = key[j];
+    }
+    __syncthreads();
+    if (tid == 0) counts[q] = s_next;
+}
+
+// Rescore of a band: entry e < counts[q] of query q's list (a packed key
+// whose row r is what matters) becomes pack_key(R, r) with
+//   R = ((sum_t q_t K[r, t]) * inv_norm[r]) * inv_qn[q]
+// from the fp32 query and the stored key, as the single-query scan forms it:
+// lane l takes the 16-byte units l, l + 64, ... of the row, alternately into
+// two fp32 FMA chains (element order inside a unit), the chains are added
+// and the wave sums its 64 lanes by butterfly.  One wave per entry; blocks
+// (4 waves) stride over the entries of their query (blockIdx.y).
+template <int KT>
+__global__ __launch_bounds__(256) void rescore_kernel(uint64_t* __restrict__ cand, int64_t cap,
+                                                      const int32_t* __restrict__ counts,
+                                                      const uint16_t* __restrict__ keys,
+                                                      int64_t ld, int d,
+                                                      const float* __restrict__ queries,
+                                                      const float* __restrict__ inv_norm,
+                                                      const float* __restrict__ inv_qn) {
+    const int q = blockIdx.y;
+    const int lane = threadIdx.x & 63;
+    uint64_t* __restrict__ list = cand + (int64_t)q * cap;
+    int64_t cnt = counts[q];
+    cnt = cnt < 0 ? 0 : (cnt > cap ? cap : cnt);
+    const float* __restrict__ qrow = queries + (int64_t)q * d;
+    const float iq = inv_qn[q];
+    const int nu = d / 8;
+    for (int64_t e = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); e < cnt;
+         e += (int64_t)gridDim.x * 4) {
+        const uint32_t r = key_row(list[e]);
+        const uint16_t* __restrict__ krow = keys + (int64_t)r * ld;
+        float a0 = 0.0f, a1 = 0.0f;
+        for (int u = lane; u < nu; u += 128) {
+            {
+                const u32x4 kv = *(const u32x4*)(krow + (int64_t)u * 8);
+                const f32x4 q0 = *(const f32x4*)(qrow + u * 8);
+                const f32x4 q1 = *(const f32x4*)(qrow + u * 8 + 4);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    a0 = __builtin_fmaf(q0[i], from_key_bits<KT>((uint16_t)(kv[i / 2] >> (16 * (i & 1)))), a0);
+                }
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    a0 = __builtin_fmaf(q1[i], from_key_bits<KT>((uint16_t)(kv[2 + i / 2] >> (16 * (i & 1)))), a0);
+                }
+            }
+            const int u2 = u + 64;
+            if (u2 < nu) {
+                const u32x4 kv = *(const u32x4*)(krow + (int64_t)u2 * 8);
+                const f32x4 q0 = *(const f32x4*)(qrow + u2 * 8);
+                const f32x4 q1 = *(const f32x4*)(qrow + u2 * 8 + 4);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    a1 = __builtin_fmaf(q0[i], from_key_bits<KT>((uint16_t)(kv[i / 2] >> (16 * (i & 1)))), a1);
+                }
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    a1 = __builtin_fmaf(q1[i], from_key_bits<KT>((uint16_t)(kv[2 + i / 2] >> (16 * (i & 1)))), a1);
+                }
+            }
+        }
+        float a = a0 + a1;
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) a += __shfl_xor(a, off, 64);
+        if (lane == 0) {
+            float v = a;
+            if (inv_norm) v = v * inv_norm[r];
+            list[e] = pack_key(v * iq, r);
+        }
+    }
+}
+
 }  // namespace
 
 size_t scan_mfma_scratch_bytes(int nq, int d) {
     const size_t qpad = (size_t)((nq + 15) / 16) * 16;
     const size_t half = (qpad * (size_t)d * 2 + 255) / 256 * 256;
-    return 2 * half + (qpad * 4 + 255) / 256 * 256;
+    return 2 * half + 2 * ((qpad * 4 + 255) / 256 * 256);
 }
 
 QuerySplit query_split_parts(void* scratch, int nq, int d) {
     const int qpad = (nq + 15) / 16 * 16;
     const size_t half = ((size_t)qpad * d * 2 + 255) / 256 * 256;
+    const size_t vec = ((size_t)qpad * 4 + 255) / 256 * 256;
     return QuerySplit{(uint16_t*)scratch, (uint16_t*)((char*)scratch + half),
-                      (float*)((char*)scratch + 2 * half), qpad};
+                      (float*)((char*)scratch + 2 * half),
+                      (float*)((char*)scratch + 2 * half + vec), qpad};
 }
 
 hipError_t launch_query_split(const float* queries, int nq, int d, int key_dtype, bool cosine,
@@ -462,10 +612,10 @@ hipError_t launch_query_split(const float* queries, int nq, int d, int key_dtype
     const QuerySplit p = query_split_parts(scratch, nq, d);
     if (key_dtype == DT_BF16)
         hipLaunchKernelGGL(query_split_kernel<DT_BF16>, dim3(p.qpad), dim3(256), 0, stream,
-                           queries, nq, d, cosine, p.hi, p.lo, p.inv_qn);
+                           queries, nq, d, cosine, p.hi, p.lo, p.inv_qn, p.margin);
     else
         hipLaunchKernelGGL(query_split_kernel<DT_F16>, dim3(p.qpad), dim3(256), 0, stream,
-                           queries, nq, d, cosine, p.hi, p.lo, p.inv_qn);
+                           queries, nq, d, cosine, p.hi, p.lo, p.inv_qn, p.margin);
     return hipGetLastError();
 }
 
@@ -501,6 +651,27 @@ hipError_t launch_scan_mfma(const void* keys, int key_dtype, int64_t n, int d, i
         if ((e = launch_scan_mfma_rows(s, split, stream)) != hipSuccess) return e;
     }
     return hipSuccess;
+}
+
+hipError_t launch_band(uint64_t* cand, int64_t cap, int nq, const float* kth, int k,
+                       const float* margin, int32_t* counts, hipStream_t stream) {
+    hipLaunchKernelGGL(band_kernel, dim3((unsigned)nq), dim3(kBandThreads), 0, stream, cand, cap,
+                       kth, k, margin, counts);
+    return hipGetLastError();
+}
+
+hipError_t launch_rescore(uint64_t* cand, int64_t cap, int nq, const int32_t* counts,
+                          const void* keys, int key_dtype, int64_t ld, int d,
+                          const float* queries, const float* inv_norm, const float* inv_qn,
+                          hipStream_t stream) {
+    const dim3 grid(16, (unsigned)nq);
+    if (key_dtype == DT_BF16)
+        hipLaunchKernelGGL(rescore_kernel<DT_BF16>, grid, dim3(256), 0, stream, cand, cap, counts,
+                           (const uint16_t*)keys, ld, d, queries, inv_norm, inv_qn);
+    else
+        hipLaunchKernelGGL(rescore_kernel<DT_F16>, grid, dim3(256), 0, stream, cand, cap, counts,
+                           (const uint16_t*)keys, ld, d, queries, inv_norm, inv_qn);
+    return hipGetLastError();
 }
 
 }  // namespace sense

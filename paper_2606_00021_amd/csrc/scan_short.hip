@@ -250,12 +250,16 @@ __global__ __launch_bounds__(kShortThreads, 2) void scan_short_kernel(ShortScan 
 
 __global__ void short_tau_kernel(const int64_t* __restrict__ ids, const float* __restrict__ scores,
                                  int nq, int k, int64_t row_step, int32_t slot_area,
-                                 uint64_t* __restrict__ tau, int32_t* __restrict__ counts) {
+                                 const float* __restrict__ margin, uint64_t* __restrict__ tau,
+                                 int32_t* __restrict__ counts) {
     const int q = blockIdx.x * blockDim.x + threadIdx.x;
     if (q >= nq) return;
     const int64_t id = ids[(int64_t)q * k + (k - 1)];
     // A sample shorter than k leaves a padding id: then every row passes.
-    tau[q] = id < 0 ? 0ull : pack_key(scores[(int64_t)q * k + (k - 1)], (uint32_t)(id * row_step));
+    // With approximate scores the threshold is lowered by the margin.
+    float s = scores[(int64_t)q * k + (k - 1)];
+    if (margin) s = s - margin[q];
+    tau[q] = id < 0 ? 0ull : pack_key(s, (uint32_t)(id * row_step));
     counts[q] = slot_area;          // overflow entries follow the wave slots
 }
 
@@ -311,10 +315,10 @@ hipError_t launch_scan_short(const ShortScan& s, hipStream_t stream) {
 }
 
 hipError_t launch_short_tau(const int64_t* ids, const float* scores, int nq, int k,
-                            int64_t row_step, int32_t slot_area, uint64_t* tau, int32_t* counts,
-                            hipStream_t stream) {
+                            int64_t row_step, int32_t slot_area, const float* margin,
+                            uint64_t* tau, int32_t* counts, hipStream_t stream) {
     hipLaunchKernelGGL(short_tau_kernel, dim3((unsigned)((nq + 63) / 64)), dim3(64), 0, stream,
-                       ids, scores, nq, k, row_step, slot_area, tau, counts);
+                       ids, scores, nq, k, row_step, slot_area, margin, tau, counts);
     return hipGetLastError();
 }
 

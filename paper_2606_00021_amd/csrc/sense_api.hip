@@ -53,7 +53,7 @@ namespace {
 thread_local char g_msg[512];
 
 // Timing events per sense_timer_t, set by sense_set_timer_events.
-constexpr int kTimers = 7;
+constexpr int kTimers = 8;
 thread_local hipEvent_t g_timer[kTimers][2] = {};
 
 hipError_t timer_mark(int which, int edge, hipStream_t st) {
@@ -467,8 +467,8 @@ static hipError_t retrieve_short(const sense_index* ix, const float* qptr, int n
         uint64_t* tau = (uint64_t*)(ws + L.tau_off);
         int32_t* cnt = (int32_t*)(ws + L.cnt_off);
         const int64_t slot_area = sense::short_scan_waves(n) * sense::kShortSlots;
-        if ((e = sense::launch_short_tau(sid, ssc, ng, k, step, (int32_t)slot_area, tau, cnt,
-                                         st)) != hipSuccess)
+        if ((e = sense::launch_short_tau(sid, ssc, ng, k, step, (int32_t)slot_area, nullptr,
+                                         tau, cnt, st)) != hipSuccess)
             return e;
         // Every row; only keys >= tau are kept.
         S.n_rows = n;
@@ -491,8 +491,24 @@ static hipError_t retrieve_short(const sense_index* ix, const float* qptr, int n
 // top-k (stores of up to kBatchDirectMax rows) or a strided sample's k-th
 // best key as a threshold, a filtered matrix-core pass over every row, and
 // the top-k of the survivors (exact: every row of the true top k reaches the
-// threshold).  The scan timer spans the sample, its top-k and the filtered
-// pass; the top-k timer the final selection.
+// threshold).
+//
+// Cosine with a sampled threshold runs the matrix cores on the hi half of
+// the query alone (half the instructions and query fragments of the hi + lo
+// split; the split measured 1.3x slower at 64 queries) and makes up for it
+// exactly: with b a bound on |approximate score A - fp32 rescore R| of any
+// row (margin = 2b, per query),
+//   threshold  = (sample's k-th best A) - 2b: the k sample rows reaching it
+//                have R >= that + b, so the k-th best R is at least that + b
+//                and every row of the R-top-k has A >= it;
+//   band       = survivors with A >= (k-th best A of the survivors) - 2b:
+//                the same argument over the survivors, which hold the A-top-k;
+//   rescore    = R of every band row (fp32, as the single-query scan);
+//   result     = the top k of the band by (R desc, row asc).
+// Inner product keeps the split (a bound would need every key's norm).
+//
+// Timers: SCAN spans the query split, the sample, its top-k and the filtered
+// pass; FILTER the first query group's filtered pass alone; TOPK the rest.
 static hipError_t retrieve_batched(const sense_index* ix, const float* qptr, int nq, int k,
                                    bool split, int64_t* out_ids, float* out_scores,
                                    int32_t* out_drafts, int32_t* out_draft_len, char* ws,
@@ -506,6 +522,8 @@ static hipError_t retrieve_batched(const sense_index* ix, const float* qptr, int
         return e;
     const sense::QuerySplit qs = sense::query_split_parts(ws + L.m_off, nq, ix->d);
     const bool sample = n > kBatchDirectMax;
+    const bool rescore = sample && ix->inv_norm != nullptr;
+    const bool mfma_split = split && !rescore;
     const int64_t step = sample ? n / kBatchSample : 1;
     const int64_t slot_area = sense::mfma_scan_waves(n) * sense::kMfmaSlots;
     for (int g0 = 0; g0 < nq; g0 += 64) {
@@ -524,12 +542,12 @@ static hipError_t retrieve_batched(const sense_index* ix, const float* qptr, int
         float* gsc = out_scores ? out_scores + (int64_t)g0 * k : nullptr;
         int32_t* gdr = out_drafts ? out_drafts + (int64_t)g0 * k * ix->max_span : nullptr;
         int32_t* gdl = out_draft_len ? out_draft_len + (int64_t)g0 * k : nullptr;
-        const bool last = g0 + 64 >= nq;
+        const bool first = g0 == 0, last = g0 + 64 >= nq;
         if (!sample) {
             S.n_rows = n;
             S.row_step = 1;
             S.scores = (float*)(ws + L.cand_off);
-            if ((e = sense::launch_scan_mfma_rows(S, split, st)) != hipSuccess) return e;
+            if ((e = sense::launch_scan_mfma_rows(S, mfma_split, st)) != hipSuccess) return e;
             if (last && (e = timer_mark(SENSE_TIMER_SCAN, 1, st)) != hipSuccess) return e;
             if (last && (e = timer_mark(SENSE_TIMER_TOPK, 0, st)) != hipSuccess) return e;
             if ((e = sense::launch_topk_gather(S.scores, n, ng, k, ix->spans, ix->span_len,
@@ -542,7 +560,7 @@ static hipError_t retrieve_batched(const sense_index* ix, const float* qptr, int
         S.n_rows = kBatchSample;
         S.row_step = step;
         S.scores = (float*)(ws + L.ss_off);
-        if ((e = sense::launch_scan_mfma_rows(S, split, st)) != hipSuccess) return e;
+        if ((e = sense::launch_scan_mfma_rows(S, mfma_split, st)) != hipSuccess) return e;
         int64_t* sid = (int64_t*)(ws + L.sid_off);
         float* ssc = (float*)(ws + L.ssc_off);
         if ((e = sense::launch_topk_gather(S.scores, kBatchSample, ng, k, nullptr, nullptr, 1, 1,
@@ -551,8 +569,9 @@ static hipError_t retrieve_batched(const sense_index* ix, const float* qptr, int
             return e;
         uint64_t* tau = (uint64_t*)(ws + L.tau_off);
         int32_t* cnt = (int32_t*)(ws + L.cnt_off);
-        if ((e = sense::launch_short_tau(sid, ssc, ng, k, step, (int32_t)slot_area, tau, cnt,
-                                         st)) != hipSuccess)
+        const float* margin = rescore ? qs.margin + g0 : nullptr;
+        if ((e = sense::launch_short_tau(sid, ssc, ng, k, step, (int32_t)slot_area, margin, tau,
+                                         cnt, st)) != hipSuccess)
             return e;
         // Every row; only keys whose score reaches tau's are kept.
         S.n_rows = n;
@@ -562,9 +581,24 @@ static hipError_t retrieve_batched(const sense_index* ix, const float* qptr, int
         S.counts = cnt;
         S.cand = (uint64_t*)(ws + L.cand_off);
         S.cap = slot_area + n;
-        if ((e = sense::launch_scan_mfma_rows(S, split, st)) != hipSuccess) return e;
+        if (first && (e = timer_mark(SENSE_TIMER_FILTER, 0, st)) != hipSuccess) return e;
+        if ((e = sense::launch_scan_mfma_rows(S, mfma_split, st)) != hipSuccess) return e;
+        if (first && (e = timer_mark(SENSE_TIMER_FILTER, 1, st)) != hipSuccess) return e;
         if (last && (e = timer_mark(SENSE_TIMER_SCAN, 1, st)) != hipSuccess) return e;
         if (last && (e = timer_mark(SENSE_TIMER_TOPK, 0, st)) != hipSuccess) return e;
+        if (rescore) {
+            // k-th best approximate score of the survivors, the band, R.
+            if ((e = sense::launch_topk_keys(S.cand, S.cap, ng, k, nullptr, nullptr, 1, 1, sid,
+                                             ssc, nullptr, nullptr, cnt, st)) != hipSuccess)
+                return e;
+            if ((e = sense::launch_band(S.cand, S.cap, ng, ssc, k, margin, cnt, st)) !=
+                hipSuccess)
+                return e;
+            if ((e = sense::launch_rescore(S.cand, S.cap, ng, cnt, ix->keys, ix->key_dtype,
+                                           ix->ld, ix->d, qptr + (int64_t)g0 * ix->d,
+                                           ix->inv_norm, S.inv_qn, st)) != hipSuccess)
+                return e;
+        }
         if ((e = sense::launch_topk_keys(S.cand, S.cap, ng, k, ix->spans, ix->span_len,
                                          ix->max_span, ix->span_stride, gid, gsc, gdr, gdl, cnt,
                                          st)) != hipSuccess)

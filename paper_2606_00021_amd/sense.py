@@ -65,7 +65,7 @@ EXPORTED = (
     "sense_last_error_message",
 )
 SENSE_TIMER_SCAN, SENSE_TIMER_TOPK, SENSE_TIMER_VERIFY, SENSE_TIMER_SELECT = 0, 1, 2, 3
-SENSE_TIMER_TRIE, SENSE_TIMER_PROJECT, SENSE_TIMER_IVF = 4, 5, 6
+SENSE_TIMER_TRIE, SENSE_TIMER_PROJECT, SENSE_TIMER_IVF, SENSE_TIMER_FILTER = 4, 5, 6, 7
 
 
 class SenseError(RuntimeError):

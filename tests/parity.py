@@ -121,20 +121,36 @@ class ScoreBound:
         return np.array([self.cache[int(r)] for r in rows])
 
 
-def retrieval_path(n_queries: int, d: int) -> str:
-    """The scan sense_retrieve runs for a static index: single queries on the
-    vector ALUs (the short-row scan for d <= 64), batches of two or more on
-    the matrix cores."""
+# Stores of more than this many rows are searched in batches through a
+# sampled threshold; with cosine, the returned scores are then fp32 rescores
+# of the band around the k-th (the single-query scan's arithmetic).
+BATCH_DIRECT_MAX = 131072
+
+
+def retrieval_path(n_queries: int, d: int, n: int = 0, metric: str = "cosine") -> str:
+    """The arithmetic of the scores sense_retrieve returns for a static index:
+    single queries from the vector ALUs (the short-row scan for d <= 64),
+    batches of two or more from the matrix cores, except cosine batches of
+    long keys over more than BATCH_DIRECT_MAX rows, whose returned scores
+    are fp32 rescores (the single-query scan's sum order)."""
     if n_queries >= 2:
+        if d > 64 and n > BATCH_DIRECT_MAX and metric == "cosine":
+            return "gemv"
         return "mfma"
     return "short" if d <= 64 else "gemv"
 
 
+def _rows_of(keys_rows) -> int:
+    t = keys_rows.t if isinstance(keys_rows, DeviceRows) else keys_rows
+    return int(t.shape[0])
+
+
 def query_bounds(keys_rows, key_dtype: str, queries, metric: str, q_in_key_type: bool = False):
     """One ScoreBound per query row of `queries` (float64-convertible array,
-    Q x d) for the path sense_retrieve takes with this batch."""
+    Q x d) for the path sense_retrieve takes with this batch over the rows
+    of keys_rows (the whole store)."""
     q = np.asarray(queries, dtype=np.float64)
-    path = retrieval_path(q.shape[0], q.shape[1])
+    path = retrieval_path(q.shape[0], q.shape[1], _rows_of(keys_rows), metric)
     return [ScoreBound(keys_rows, key_dtype, q[i], metric, path, q_in_key_type)
             for i in range(q.shape[0])]
 

@@ -272,7 +272,8 @@ def test_timer_ids(lib):
     assert lib.sense_set_timer_events(sense.SENSE_TIMER_TRIE, None, None) == 0
     assert lib.sense_set_timer_events(sense.SENSE_TIMER_PROJECT, None, None) == 0
     assert lib.sense_set_timer_events(sense.SENSE_TIMER_IVF, None, None) == 0
-    assert lib.sense_set_timer_events(7, None, None) == INVALID
+    assert lib.sense_set_timer_events(sense.SENSE_TIMER_FILTER, None, None) == 0
+    assert lib.sense_set_timer_events(8, None, None) == INVALID
 
 
 def trie_desc(**kw):
