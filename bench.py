@@ -50,6 +50,9 @@ def parse():
                     help="skip the candidate-selection leg (dynamic cache + composite Top-N)")
     ap.add_argument("--sen-context", type=int, default=4096,
                     help="rows of generation context in the dynamic cache of the SEN leg")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="time the headline workload only (by default every other "
+                         "configuration of the metric follows it)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after the timed region, run one plain device copy of this many MiB "
                          "(a reference kernel of known traffic for HBM counter runs)")
@@ -336,23 +339,22 @@ def sen_leg(args, w, ds, q, src_rows, K, dev):
             "append4_us": append_ms * 1e3}
 
 
-def main():
-    args = parse()
-    world = int(os.environ.get("WORLD_SIZE", "1"))
-    if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU only: the library has no multi-GPU path "
-              "(its row-sharded design is not built); run with --gpus 1",
-              file=sys.stderr)
-        sys.exit(2)
+# The configurations the metric's workload is quoted beside: besides the
+# headline, the tiny store, the LLaMA-3-8B and Qwen2-7B shapes (one query),
+# and the 13B-shaped (16 queries) and 70B-shaped (64 queries) batches.
+CONFIG_WORKLOADS = ["tiny-16k-d4096", "llama3-8b-262k-d4096", "qwen2-7b-1m-d3584",
+                    "13b-batched-4m-d5120", "70b-8m-d8192"]
+BATCH_DIRECT_MAX = 131072    # larger stores take the sampled-threshold batched search
 
+
+def run_workload(name, args, dev, K, warmup, graph=False, copy_probe_mib=0):
+    """Builds workload `name`, times K steps after `warmup` untimed ones and
+    returns (result dict, context for the SEN leg and the CPU baseline)."""
     import torch
 
     from paper_2606_00021_amd import sense, synth
 
-    name = args.workload or synth.HEADLINE
     w = synth.WORKLOADS[name]
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
     log(f"[bench] workload {name}: n={w.n} d={w.d} {w.key_dtype} Q={w.n_queries} k={w.k} "
         f"M={w.span} V={w.vocab} {w.logits_dtype}")
     t0 = time.perf_counter()
@@ -458,11 +460,9 @@ def main():
         sense.sense_soft_gate_verify(logits, drafts, dlen, n_groups=vq, gamma=0.05, topk=3,
                                      window=6, tau=0, workspace=ws_v, out=out_v)
 
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         step()
     torch.cuda.synchronize()
-
-    K = args.steps
 
     def time_steps(run):
         # Timed region: exactly K steps between two events, nothing else
@@ -481,7 +481,7 @@ def main():
     ms_eager, wall_eager = time_steps(step)
     ms_step, wall_step = ms_eager, wall_eager
     launch = "eager"
-    if args.graph:
+    if graph:
         # The step as one HIP graph: every entry point allocates nothing and
         # records no memset, so the captured kernels replay the same work
         # without the host's per-call launch cost.
@@ -501,11 +501,15 @@ def main():
     # Per-kernel durations: a second pass of K steps with hipEvents recorded
     # by the library around the scan, top-k and verify kernels (the events
     # themselves add a little time, so this pass is not the step time).
+    # A batch of long keys over a sampled store: the filtered full pass is
+    # the dominant kernel; its own events time it for the roofline.
+    filtered = (ivf is None and nq >= 2 and d_idx > 64 and w.n > BATCH_DIRECT_MAX)
     timed_parts = ((("ivf",) if ivf is not None else ("scan", "topk")) + ("verify",)
-                   + (("project",) if w.proj else ()))
+                   + (("project",) if w.proj else ()) + (("filter",) if filtered else ()))
     ev = {t: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
               for _ in range(K)] for t in timed_parts}
     timer_id = {"scan": sense.SENSE_TIMER_SCAN, "topk": sense.SENSE_TIMER_TOPK,
+                "filter": sense.SENSE_TIMER_FILTER,
                 "verify": sense.SENSE_TIMER_VERIFY, "project": sense.SENSE_TIMER_PROJECT,
                 "ivf": sense.SENSE_TIMER_IVF}
     # torch creates the underlying hipEvent_t lazily at the first record():
@@ -525,6 +529,8 @@ def main():
     dur = {t: sum(a.elapsed_time(b) for a, b in ev[t]) / K for t in ev}
     parts = (f"inverted-file search {dur['ivf']:.4f} ms" if ivf is not None
              else f"scan {dur['scan']:.4f} ms, topk {dur['topk']:.4f} ms")
+    if filtered:
+        parts += f" (filtered pass {dur['filter']:.4f} ms)"
     log(f"[bench] {K} steps ({launch}): {ms_step:.4f} ms/step (wall {wall * 1e3:.4f} ms/step; "
         f"eager launches {ms_eager:.4f} ms/step); {parts}, verify {dur['verify']:.4f} ms"
         + (f", query projection {dur['project']:.4f} ms" if w.proj else ""))
@@ -560,6 +566,10 @@ def main():
             scan_kernel = "short_key_retrieval"
         elif nq >= 2:
             scan_kernel = "scan_mfma_kernel"
+            if filtered:
+                # The roofline is the filtered full pass's own: one launch
+                # that reads every key (and norm) once.
+                scan_ms = dur["filter"]
         elif d_idx <= 64:
             scan_kernel = "scan_small_kernel"
         else:
@@ -573,7 +583,7 @@ def main():
         "unit": "queries/s",
         "n_gpus": 1,
         "steps": K,
-        "warmup": args.warmup,
+        "warmup": warmup,
         "ms_per_step": ms_step,
         "launch": launch,
         "ms_per_step_eager": ms_eager,
@@ -590,12 +600,18 @@ def main():
         "hbm_frac": step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS,
         **({"ivf_search_ms": dur["ivf"]} if ivf is not None
            else {"scan_ms": dur["scan"], "topk_ms": dur["topk"]}),
+        **({"filter_ms": dur["filter"],
+            "retrieval_scan_gbps": scan_bytes / (dur["scan"] * 1e-3) / 1e9} if filtered else {}),
         "verify_ms": dur["verify"],
         **({"project_ms": dur["project"]} if w.proj else {}),
         "verify_gbps": verify_bytes / (dur["verify"] * 1e-3) / 1e9 if dur["verify"] > 0 else None,
         "roofline": {"bound": "hbm", "kernel": scan_kernel,
                      **({"timed": "every kernel of the retrieval (scan, selection, gather)"}
                         if scan_kernel in ("short_key_retrieval", "ivf_search") else {}),
+                     **({"timed": "the filtered full pass alone (one launch over every row); "
+                                  "scan_ms adds the query split and the strided sample's pass "
+                                  "and top-k, topk_ms the survivors' selection"}
+                        if filtered else {}),
                      "achieved": scan_gbps,
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": scan_gbps / HBM_PEAK_GBPS,
                      "traffic": traffic},
@@ -609,10 +625,12 @@ def main():
         # Matrix-core utilisation of the batched scan (bound by HBM, so a share
         # of the dense peak, reported beside GB/s): the instructions issue
         # whole 16-query tiles and 32-dimension steps, twice with fp32 queries
-        # (hi + lo halves in the key type).
+        # (hi + lo halves in the key type) except in a cosine filtered pass,
+        # which takes the hi half alone and rescores a band in fp32.
         qpad = 16 * ((nq + 15) // 16)
         dpad = 32 * ((d_idx + 31) // 32)
-        halves = 2 if q.dtype == torch.float32 else 1
+        halves = 2 if (q.dtype == torch.float32
+                       and not (filtered and w.metric == "cosine")) else 1
         issued = 2.0 * w.n * dpad * qpad * halves
         res["mfma"] = {"dtype": w.key_dtype, "issued_flops": issued,
                        "useful_flops": 2.0 * w.n * d_idx * nq,
@@ -641,26 +659,85 @@ def main():
     res["scan_frac_of_read_ceiling"] = scan_gbps / ceiling
     log(f"[bench] plain streaming read of the keys: {ceiling:.0f} GB/s; scan at "
         f"{scan_gbps / ceiling * 100:.1f} % of it")
-    if args.copy_probe_mib > 0:
-        n_el = args.copy_probe_mib * (1 << 20) // 4
+    if copy_probe_mib > 0:
+        n_el = copy_probe_mib * (1 << 20) // 4
         src = torch.ones(n_el, dtype=torch.float32, device=dev)
         dst = torch.empty_like(src)
         torch.cuda.synchronize()
         dst.copy_(src)
         torch.cuda.synchronize()
-        log(f"[bench] copy probe: {args.copy_probe_mib} MiB read + {args.copy_probe_mib} MiB "
+        log(f"[bench] copy probe: {copy_probe_mib} MiB read + {copy_probe_mib} MiB "
             f"written by one copy kernel")
         del src, dst
+    ctx = {"w": w, "ds": ds, "q": q, "src_rows": src_rows, "logits": logits, "drafts": drafts,
+           "index": index, "ivf": ivf}
+    return res, ctx
+
+
+def close_workload(ctx):
+    import torch
+
+    ctx["index"].close()
+    if ctx["ivf"] is not None:
+        ctx["ivf"].close()
+    ctx.clear()
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+def config_summary(res):
+    """The figures of one configuration's run kept in the headline line."""
+    keep = ("ms_per_step", "value", "scan_ms", "filter_ms", "topk_ms", "verify_ms",
+            "hbm_gbps", "hbm_read_ceiling_gbps", "roofline", "mfma", "retrieval_scan_gbps")
+    out = {k: res[k] for k in keep if k in res}
+    out["queries_per_s"] = out.pop("value")
+    c = res["config"]
+    out["config"] = {k: c[k] for k in ("n", "d", "key_dtype", "n_queries", "k", "span", "vocab",
+                                       "logits_dtype", "verify_candidates")}
+    return out
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
+              "(its row-sharded design is not built); run with --gpus 1",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2606_00021_amd import synth
+
+    name = args.workload or synth.HEADLINE
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    K = args.steps
+    res, ctx = run_workload(name, args, dev, K, args.warmup, graph=args.graph,
+                            copy_probe_mib=args.copy_probe_mib)
+    w = ctx["w"]
     if not args.no_sen and not w.proj:
-        res["sen"] = sen_leg(args, w, ds, q, src_rows, K, dev)
+        res["sen"] = sen_leg(args, w, ctx["ds"], ctx["q"], ctx["src_rows"], K, dev)
     if not args.no_cpu_baseline:
         log("[bench] timing the oracle on the host (cpu_baseline)")
         t0 = time.perf_counter()
-        res["cpu_baseline"] = cpu_baseline(w, ds, q, logits, drafts, args.cpu_seconds)
+        res["cpu_baseline"] = cpu_baseline(w, ctx["ds"], ctx["q"], ctx["logits"], ctx["drafts"],
+                                           args.cpu_seconds)
         log(f"[bench] cpu_baseline took {time.perf_counter() - t0:.1f} s")
-    index.close()
-    if ivf is not None:
-        ivf.close()
+    close_workload(ctx)
+    del ctx
+    if args.workload is None and not args.no_configs:
+        # Every other configuration once, on the same device, after the
+        # headline (its own steps, fewer of them; no SEN leg or CPU baseline).
+        res["configs"] = {}
+        for cname in CONFIG_WORKLOADS:
+            if cname == name:
+                continue
+            r, c = run_workload(cname, args, dev, min(K, 10), min(args.warmup, 2))
+            close_workload(c)
+            del c
+            res["configs"][cname] = config_summary(r)
     print(json.dumps(res), flush=True)
 
 
