@@ -163,6 +163,16 @@ def test_ivf_search_matches_oracle(case):
     index.close()
 
 
+def exact_per_query(flat, q, k):
+    """The exact retrieval one query at a time: the single-query scan sums a
+    row in fp32 like the inverted file's list scan (a batch would take the
+    matrix cores, whose hi + lo split rounds differently)."""
+    parts = [sense.sense_retrieve(flat, q[i:i + 1].contiguous(), k) for i in range(q.shape[0])]
+    torch.cuda.synchronize()
+    return (torch.cat([p[0] for p in parts]), torch.cat([p[1] for p in parts]),
+            torch.cat([p[2] for p in parts]))
+
+
 def test_ivf_flat_probing_everything_equals_exact_retrieval():
     w, ds = store(8000, 64, "bf16", 9)
     q, _ = synth.make_queries(w, ds, 9, n_queries=2)
@@ -171,8 +181,7 @@ def test_ivf_flat_probing_everything_equals_exact_retrieval():
     index = sense.sense_build_ivf_index(ds.keys, ds.spans, cen, lists)
     ids, sc, dr, _ = sense.sense_ivf_search(index, q, 40, 32)
     flat = sense.sense_build_index(ds.keys, ds.spans)
-    e_ids, e_sc, e_dr, _ = sense.sense_retrieve(flat, q, 40)
-    torch.cuda.synchronize()
+    e_ids, e_sc, e_dr = exact_per_query(flat, q, 40)
     assert torch.equal(ids, e_ids)
     assert torch.allclose(sc, e_sc, rtol=1e-6, atol=0)
     assert torch.equal(dr, e_dr)
@@ -192,8 +201,7 @@ def test_ivf_flat_probing_everything_many_rounds(k):
     index = sense.sense_build_ivf_index(ds.keys, ds.spans, cen, lists)
     ids, sc, dr, _ = sense.sense_ivf_search(index, q, k, 64)
     flat = sense.sense_build_index(ds.keys, ds.spans)
-    e_ids, e_sc, e_dr, _ = sense.sense_retrieve(flat, q, k)
-    torch.cuda.synchronize()
+    e_ids, e_sc, e_dr = exact_per_query(flat, q, k)
     assert torch.equal(ids, e_ids)
     assert torch.allclose(sc, e_sc, rtol=1e-6, atol=0)
     assert torch.equal(dr, e_dr)
@@ -213,8 +221,7 @@ def test_ivf_candidate_counts_at_selection_boundaries(n):
     index = sense.sense_build_ivf_index(ds.keys, ds.spans, cen, lists)
     ids, sc, dr, _ = sense.sense_ivf_search(index, q, 100, 16)
     flat = sense.sense_build_index(ds.keys, ds.spans)
-    e_ids, e_sc, e_dr, _ = sense.sense_retrieve(flat, q, 100)
-    torch.cuda.synchronize()
+    e_ids, e_sc, e_dr = exact_per_query(flat, q, 100)
     assert torch.equal(ids, e_ids)
     assert torch.allclose(sc, e_sc, rtol=1e-6, atol=0)
     assert torch.equal(dr, e_dr)
