@@ -117,3 +117,69 @@ def test_bound_rejects_a_real_error():
     got = cosine_scale(k, q, mfma_emulate(k, q, kdt, split=False))
     b = ScoreBound(kb, kdt, q, "cosine", "mfma")(np.arange(n))
     assert (np.abs(got - exact) > b).any()
+
+
+# The batched cosine search over large stores ranks by a fp32 rescore of a
+# band chosen with hi-only matrix-core scores; query_split_kernel's margin
+# (restated below) must bound |hi-only score - rescore| twice over, also for
+# rows built to make the hi half's error as large as Cauchy-Schwarz allows.
+
+def rescore_emulate(k, q):
+    """rescore_kernel's sum: lane l takes the 8-element units l, l + 64, ...;
+    units l + 128 i go to chain 0 and l + 64 + 128 i to chain 1 (element
+    order inside a unit, one FMA each), chains added, 64-lane butterfly."""
+    n, d = k.shape
+    nu = d // 8
+    nup = -(-nu // 128) * 128
+    kp = np.zeros((n, nup * 8))
+    kp[:, :d] = k
+    qp = np.zeros(nup * 8)
+    qp[:d] = q
+    kp = kp.reshape(n, nup // 128, 2, 64, 8)      # [row, i, chain, lane, element]
+    qp = qp.reshape(nup // 128, 2, 64, 8)
+    acc = np.zeros((n, 2, 64), f32)
+    for i in range(nup // 128):
+        for e in range(8):
+            acc = (acc.astype(np.float64) + kp[:, i, :, :, e] * qp[i, :, :, e]).astype(f32)
+    a = (acc[:, 0] + acc[:, 1]).astype(f32)
+    for off in (32, 16, 8, 4, 2, 1):                # butterfly: lane l adds lane l ^ off
+        a = (a + a[:, np.arange(64) ^ off]).astype(f32)
+    return a[:, 0]
+
+
+def kernel_margin(q, kdt, d):
+    hi = decode_rows(to_bits(q, kdt), kdt)
+    ll = f32(((q - hi) ** 2).sum())
+    inv_q = f32(1.0) / np.sqrt(f32((q * q).sum()))
+    depth = (-(-d // 32) + 8) + (d // 128 + 8) + 2 * (d // 64 + 16) + 4
+    return 2.0 * (1.01 * float(np.sqrt(ll)) * float(inv_q) + 2.0 * 1.01 * depth * 2.0 ** -24)
+
+
+@pytest.mark.parametrize("d,kdt", [(128, "bf16"), (1000, "f16"), (4096, "bf16"),
+                                   (5120, "f16"), (8192, "bf16")])
+def test_batched_margin_bounds_hi_only_against_rescore(d, kdt):
+    rng = np.random.default_rng(d * 3 + len(kdt))
+    kb = make_rows(rng, 120, d, kdt)
+    k = decode_rows(kb, kdt)
+    q = (k[7] + rng.normal(0.0, 0.05, d)).astype(f32).astype(np.float64)
+    lo = q - decode_rows(to_bits(q, kdt), kdt)
+    qn, lon = np.linalg.norm(q), np.linalg.norm(lo)
+    # rows along q with the hi half's error direction mixed in, and rows along
+    # that direction alone: |sum (q - hi) k| / (|q| |k|) reaches |q - hi| / |q|
+    adv = [q + a * lo / lon * qn for a in (0.003, 0.03, 0.3, 1.0)]
+    adv += [lo / lon * s for s in (1.0, 1e3)]
+    adv += [np.sign(lo) * np.abs(k[j]) for j in range(4)]
+    kb = np.concatenate([kb, to_bits(np.array(adv), kdt)])
+    k = decode_rows(kb, kdt)
+    a = cosine_scale(k, q, mfma_emulate(k, q, kdt, split=False)).astype(np.float64)
+    r = cosine_scale(k, q, rescore_emulate(k, q)).astype(np.float64)
+    m = kernel_margin(q, kdt, d)
+    gap = np.abs(a - r)
+    assert (gap <= m / 2).all(), f"row {np.argmax(gap > m / 2)}: |A - R| {gap.max():.3g} > {m / 2:.3g}"
+    # the adversarial rows use a large part of the allowance: the margin is
+    # not loose by orders of magnitude (a band that holds the whole store)
+    assert gap[-len(adv):].max() > 0.25 * (m / 2), (gap[-len(adv):].max(), m)
+    # and the rescore is the single-query scan's accuracy
+    exact = oracle.scores(kb, kdt, q.astype(np.float32)[None, :], "f32", metric="cosine")[0]
+    b = ScoreBound(kb, kdt, q, "cosine", "gemv")(np.arange(k.shape[0]))
+    assert (np.abs(r - exact) <= b).all()
