@@ -135,9 +135,11 @@ typedef struct {
     uint32_t flags;
 } sense_index_desc_t;
 
-/* Build an index over the datastore.  For COSINE it computes the fp32 side
- * table 1/||k_i|| (0 for a zero row) with one read of the keys, enqueued on
- * `stream`.  The index owns only that table (N * 4 bytes) and, with
+/* Build an index over the datastore.  With one read of the keys, enqueued
+ * on `stream`, it computes for COSINE the fp32 side table 1/||k_i|| (0 for a
+ * zero row), for IP the largest fp32 ||k_i|| that is a number (it bounds the
+ * error of the batched search's first pass, see sense_retrieve).  The index
+ * owns only that table (N * 4 bytes) or value (4 bytes) and, with
  * SENSE_INDEX_COPY_KEYS, the key copy.  *out receives the handle; a static
  * index is immutable afterwards, so concurrent sense_retrieve calls on
  * different streams with separate workspaces are safe.
@@ -213,7 +215,13 @@ sense_status_t sense_retrieve_workspace_size(const sense_index_t *index, int32_t
  *   s[q, i] = that / (||q|| ||K_i||), 0 if a norm is 0   (COSINE)
  * accumulated in fp32 from the stored fp16/bf16 keys and the query as given;
  * the k rows with the largest s in the order (score desc, row index asc),
- * and their continuations.
+ * and their continuations.  One query is scored by fp32 FMA chains; a batch
+ * of two or more on the matrix cores (an fp32 query as hi + lo halves of the
+ * key type).  A batch of keys longer than 64 over more than 131072 rows
+ * first takes every row's score from the query's hi half alone, keeps the
+ * rows that a per-query bound on that score's error cannot exclude from the
+ * top k, and returns fp32 rescores of those (the one-query arithmetic): the
+ * same top k, with the one-query scan's rounding.
  *   queries      n_queries x d, dtype q_dtype (F32, or the key dtype),
  *                row-major, 16-byte aligned.
  *   n_queries    >= 1.   k: 1 <= k <= min(n, 1024) (an empty dynamic cache

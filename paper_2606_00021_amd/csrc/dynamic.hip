@@ -66,7 +66,7 @@ __global__ __launch_bounds__(kAppendThreads) void append_rows_kernel(
     const void* __restrict__ src, int src_dtype, int key_dtype,
     const int32_t* __restrict__ tokens, int d, int64_t n_old, int64_t n_new, int max_span,
     uint16_t* __restrict__ keys, int32_t* __restrict__ hist, int32_t* __restrict__ span_len,
-    float* __restrict__ inv_norm) {
+    float* __restrict__ inv_norm, uint32_t* __restrict__ max_norm_bits) {
     const int64_t b = blockIdx.x;
     const int64_t row = n_old + b;
     uint16_t* dst = keys + row * d;
@@ -84,7 +84,7 @@ __global__ __launch_bounds__(kAppendThreads) void append_rows_kernel(
             span_len[r] = (int32_t)(left < max_span ? left : max_span);
         }
     }
-    if (inv_norm != nullptr) {                      // uniform over the grid
+    if (inv_norm != nullptr || max_norm_bits != nullptr) {   // uniform over the grid
         // 1/||k|| of the stored row, summed exactly as the index build sums
         // it (lane l takes 8 elements in every 512, even and odd elements in
         // two chains, then the wave sum), so an appended row's value is
@@ -104,7 +104,12 @@ __global__ __launch_bounds__(kAppendThreads) void append_rows_kernel(
                 }
             }
             const float s = norm_wave_sum(a0 + a1);
-            if (lane == 0) inv_norm[row] = (s > 0.0f) ? 1.0f / __builtin_sqrtf(s) : 0.0f;
+            if (inv_norm != nullptr && lane == 0)
+                inv_norm[row] = (s > 0.0f) ? 1.0f / __builtin_sqrtf(s) : 0.0f;
+            // inner product: the cache's largest key norm (rows whose norm is
+            // a number), as the index build keeps it
+            if (max_norm_bits != nullptr && lane == 0 && s == s)
+                atomicMax(max_norm_bits, __builtin_bit_cast(uint32_t, __builtin_sqrtf(s)));
         }
     }
 }
@@ -114,10 +119,10 @@ __global__ __launch_bounds__(kAppendThreads) void append_rows_kernel(
 hipError_t launch_append_rows(const void* src, int src_dtype, int key_dtype,
                               const int32_t* tokens, int d, int64_t n_old, int count,
                               int max_span, void* keys, int32_t* hist, int32_t* span_len,
-                              float* inv_norm, hipStream_t stream) {
+                              float* inv_norm, uint32_t* max_norm_bits, hipStream_t stream) {
     hipLaunchKernelGGL(append_rows_kernel, dim3((unsigned)count), dim3(kAppendThreads),
                        0, stream, src, src_dtype, key_dtype, tokens, d, n_old, n_old + count,
-                       max_span, (uint16_t*)keys, hist, span_len, inv_norm);
+                       max_span, (uint16_t*)keys, hist, span_len, inv_norm, max_norm_bits);
     return hipGetLastError();
 }
 

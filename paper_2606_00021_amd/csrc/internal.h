@@ -99,9 +99,11 @@ __device__ inline void bitonic_desc(uint64_t* s, int p) {
 // Each returns hipSuccess or the launch error.  Shapes are validated by the
 // caller (sense_api.hip) before these are reached.
 
-// inv_norm[i] = 1 / ||keys[i, :d]|| (0 for a zero row), fp32 accumulation.
+// inv_norm[i] = 1 / ||keys[i, :d]|| (0 for a zero row), fp32 accumulation,
+// when inv_norm is not NULL; the largest ||keys[i, :d]|| that is a number
+// atomically maxed (as bits) into *max_norm_bits when that is not NULL.
 hipError_t launch_key_norms(const void* keys, int key_dtype, int64_t n, int d, int64_t ld,
-                            float* inv_norm, hipStream_t stream);
+                            float* inv_norm, uint32_t* max_norm_bits, hipStream_t stream);
 
 // Query batches of at least this many run as an MFMA contraction, which
 // reads the store once for the whole batch (a 16-query tile, padded); a
@@ -242,8 +244,8 @@ int blocks_per_cu(Kernel kern, int threads, int fallback) {
 // The queries of a batch padded to qpad = 16*ceil(nq/16) rows and split
 // into hi + lo halves of the key type (a scratch of scan_mfma_scratch_bytes),
 // with inv_qn[q] = 1/||q|| (cosine), 1 (inner product), 0 (padding), and
-// margin[q] (cosine): twice a bound on |hi-only matrix-core score - fp32
-// rescore| of any row.
+// margin[q]: twice a bound on |hi-only matrix-core score - fp32 rescore| of
+// any row (cosine; inner product given the store's largest key norm; else 0).
 struct QuerySplit {
     uint16_t* hi;
     uint16_t* lo;
@@ -252,8 +254,10 @@ struct QuerySplit {
     int qpad;
 };
 QuerySplit query_split_parts(void* scratch, int nq, int d);
+// key_norm_max (inner product, may be NULL): the store's largest key norm,
+// which scales the inner-product margin.
 hipError_t launch_query_split(const float* queries, int nq, int d, int key_dtype, bool cosine,
-                              void* scratch, hipStream_t stream);
+                              const float* key_norm_max, void* scratch, hipStream_t stream);
 
 // Batched scan of short keys (d <= kSmallDim) on the matrix cores, for at
 // most 64 queries of a split batch (see scan_short.hip).  Row r of the scan
@@ -357,11 +361,12 @@ hipError_t launch_select_candidates(const float* scores_s, const int32_t* drafts
 // Appends `count` rows to a dynamic cache of n_old rows: keys (count x d of
 // src_dtype, converted to key_dtype) into keys (row stride d), tokens into
 // the history, the continuation lengths min(max_span, n - p), and, when
-// inv_norm is not NULL, each new row's 1/||k|| (as the index build forms it).
+// inv_norm is not NULL, each new row's 1/||k|| (as the index build forms it);
+// when max_norm_bits is not NULL, the new rows' norms maxed into it.
 hipError_t launch_append_rows(const void* src, int src_dtype, int key_dtype,
                               const int32_t* tokens, int d, int64_t n_old, int count,
                               int max_span, void* keys, int32_t* hist, int32_t* span_len,
-                              float* inv_norm, hipStream_t stream);
+                              float* inv_norm, uint32_t* max_norm_bits, hipStream_t stream);
 
 // Outputs of the loose-trie build (device pointers; NULL = not wanted for
 // the optional ones).  Per group g of gs drafts of m tokens, nodes = gs * m

@@ -154,13 +154,18 @@ __global__ __launch_bounds__(256) void scan_gemv_kernel(
     }
 }
 
-// inv_norm[i] = 1/||row i||, one wave per row (build-time, one pass).
+// inv_norm[i] = 1/||row i|| (when inv_norm is not NULL) and the largest
+// ||row i|| over the rows whose norm is a number, as raw bits atomically
+// maxed into *max_norm_bits (when not NULL; non-negative floats order like
+// their bits).  One wave per row (build-time, one pass).
 template <int KT>
 __global__ __launch_bounds__(256) void key_norms_kernel(const uint16_t* __restrict__ keys,
                                                         int64_t ld, int64_t n, int d,
-                                                        float* __restrict__ inv_norm) {
+                                                        float* __restrict__ inv_norm,
+                                                        uint32_t* __restrict__ max_norm_bits) {
     const int lane = threadIdx.x & 63;
     const int64_t waves = (int64_t)gridDim.x * 4;
+    float wmax = 0.0f;
     for (int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); r < n; r += waves) {
         float a0 = 0.0f, a1 = 0.0f;
         for (int e = lane * kLaneElems; e < d; e += kWaveElems) {
@@ -173,8 +178,12 @@ __global__ __launch_bounds__(256) void key_norms_kernel(const uint16_t* __restri
             }
         }
         const float s = wave_sum(a0 + a1);
-        if (lane == 0) inv_norm[r] = (s > 0.0f) ? 1.0f / __builtin_sqrtf(s) : 0.0f;
+        if (inv_norm != nullptr && lane == 0)
+            inv_norm[r] = (s > 0.0f) ? 1.0f / __builtin_sqrtf(s) : 0.0f;
+        if (s == s) wmax = __builtin_fmaxf(wmax, __builtin_sqrtf(s));
     }
+    if (max_norm_bits != nullptr && lane == 0)
+        atomicMax(max_norm_bits, __builtin_bit_cast(uint32_t, wmax));
 }
 
 template <int QT>
@@ -235,16 +244,16 @@ int device_cus() {
 }
 
 hipError_t launch_key_norms(const void* keys, int key_dtype, int64_t n, int d, int64_t ld,
-                            float* inv_norm, hipStream_t stream) {
+                            float* inv_norm, uint32_t* max_norm_bits, hipStream_t stream) {
     int64_t blocks = (n + 3) / 4;
     const int64_t cap = (int64_t)device_cus() * 8;
     if (blocks > cap) blocks = cap;
     if (key_dtype == DT_BF16)
         hipLaunchKernelGGL(key_norms_kernel<DT_BF16>, dim3((unsigned)blocks), dim3(256), 0,
-                           stream, (const uint16_t*)keys, ld, n, d, inv_norm);
+                           stream, (const uint16_t*)keys, ld, n, d, inv_norm, max_norm_bits);
     else
         hipLaunchKernelGGL(key_norms_kernel<DT_F16>, dim3((unsigned)blocks), dim3(256), 0,
-                           stream, (const uint16_t*)keys, ld, n, d, inv_norm);
+                           stream, (const uint16_t*)keys, ld, n, d, inv_norm, max_norm_bits);
     return hipGetLastError();
 }
 

@@ -63,22 +63,26 @@ __device__ __forceinline__ float from_key_bits(uint16_t b) {
 
 // Pads the query batch to qpad rows and splits each fp32 value into hi + lo
 // in the key type; inv_qn[q] = 1/||q|| (cosine), 1 (inner product), 0 for
-// padding rows.  margin[q] (cosine; 0 otherwise) is twice a bound on the
-// difference between a score taken with the hi half alone on the matrix
-// cores and the fp32 rescore of the same row (rescore_kernel):
+// padding rows.  margin[q] is twice a bound on the difference between a
+// score taken with the hi half alone on the matrix cores and the fp32
+// rescore of the same row (rescore_kernel).  Cosine:
 //   |A - R| <= ||q - hi|| / ||q||                      (Cauchy-Schwarz)
-//            + fp32 rounding of both sums, the norms and the products,
-// the rounding terms doubled for safety and the split term raised by 1 %
-// (its own fp32 evaluation is good to ~d * 2^-24).  Scores are cosines, so
-// every term is relative to 1.  An overflowing split (an f16 hi half of
-// |x| > 65504) gives an infinite or NaN margin: every row then passes.
-// One block (256 threads) per padded query row.
+//            + fp32 rounding of both sums, the norms and the products
+// (scores are cosines, so every term is relative to 1); inner product, with
+// K the store's largest key norm (key_norm_max, NULL: margin 0):
+//   |A - R| <= (||q - hi|| + rounding * ||q||) * K,
+// K raised by 0.1 % for its own fp32 evaluation.  The rounding terms are
+// doubled for safety and the split term raised by 1 % (its own fp32
+// evaluation is good to ~d * 2^-24).  An overflowing split (an f16 hi half
+// of |x| > 65504) or an infinite key gives an infinite or NaN margin: every
+// row then passes.  One block (256 threads) per padded query row.
 template <int KT>
 __global__ __launch_bounds__(256) void query_split_kernel(const float* __restrict__ q, int nq,
                                                           int d, bool cosine,
                                                           uint16_t* __restrict__ qhi,
                                                           uint16_t* __restrict__ qlo,
                                                           float* __restrict__ inv_qn,
+                                                          const float* __restrict__ key_norm_max,
                                                           float* __restrict__ margin) {
     const int row = blockIdx.x;
     float ss = 0.0f, ll = 0.0f;
@@ -108,15 +112,18 @@ __global__ __launch_bounds__(256) void query_split_kernel(const float* __restric
         if (row >= nq) v = 0.0f;
         else if (cosine) v = (s > 0.0f) ? 1.0f / __builtin_sqrtf(s) : 0.0f;
         inv_qn[row] = v;
+        // summation depth of the hi-only matrix-core sum, of the rescore, and
+        // of each fp32 inverse norm, plus the final products
+        const float depth = (float)((d + 31) / 32 + 8) + (float)(d / 128 + 8) +
+                            2.0f * (float)(d / 64 + 16) + 4.0f;
+        const float rnd = depth * 5.9604645e-8f;              // x 2^-24
+        const float lon = __builtin_sqrtf(s_part[1][0]);       // ||q - hi||
         float m = 0.0f;
-        if (row < nq && cosine) {
-            // summation depth of the hi-only matrix-core sum, of the rescore,
-            // and of each fp32 inverse norm, plus the final products
-            const float depth = (float)((d + 31) / 32 + 8) + (float)(d / 128 + 8) +
-                                2.0f * (float)(d / 64 + 16) + 4.0f;
-            const float rnd = depth * 5.9604645e-8f;          // x 2^-24
-            m = 2.0f * (1.01f * __builtin_sqrtf(s_part[1][0]) * v + 2.0f * 1.01f * rnd);
-        }
+        if (row < nq && cosine)
+            m = 2.0f * (1.01f * lon * v + 2.0f * 1.01f * rnd);
+        else if (row < nq && key_norm_max != nullptr)
+            m = 2.0f * (1.01f * lon + 2.0f * 1.01f * rnd * __builtin_sqrtf(s)) *
+                (1.001f * key_norm_max[0]);
         margin[row] = m;
     }
 }
@@ -608,14 +615,14 @@ QuerySplit query_split_parts(void* scratch, int nq, int d) {
 }
 
 hipError_t launch_query_split(const float* queries, int nq, int d, int key_dtype, bool cosine,
-                              void* scratch, hipStream_t stream) {
+                              const float* key_norm_max, void* scratch, hipStream_t stream) {
     const QuerySplit p = query_split_parts(scratch, nq, d);
     if (key_dtype == DT_BF16)
         hipLaunchKernelGGL(query_split_kernel<DT_BF16>, dim3(p.qpad), dim3(256), 0, stream,
-                           queries, nq, d, cosine, p.hi, p.lo, p.inv_qn, p.margin);
+                           queries, nq, d, cosine, p.hi, p.lo, p.inv_qn, key_norm_max, p.margin);
     else
         hipLaunchKernelGGL(query_split_kernel<DT_F16>, dim3(p.qpad), dim3(256), 0, stream,
-                           queries, nq, d, cosine, p.hi, p.lo, p.inv_qn, p.margin);
+                           queries, nq, d, cosine, p.hi, p.lo, p.inv_qn, key_norm_max, p.margin);
     return hipGetLastError();
 }
 
@@ -631,8 +638,8 @@ hipError_t launch_scan_mfma(const void* keys, int key_dtype, int64_t n, int d, i
                             const float* queries, int nq, bool split, const float* inv_norm,
                             float* scores, void* scratch, hipStream_t stream) {
     const QuerySplit p = query_split_parts(scratch, nq, d);
-    hipError_t e = launch_query_split(queries, nq, d, key_dtype, inv_norm != nullptr, scratch,
-                                      stream);
+    hipError_t e = launch_query_split(queries, nq, d, key_dtype, inv_norm != nullptr, nullptr,
+                                      scratch, stream);
     if (e != hipSuccess) return e;
     for (int g0 = 0; g0 < nq; g0 += 64) {
         MfmaScan s{};

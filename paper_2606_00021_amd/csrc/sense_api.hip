@@ -29,6 +29,7 @@ struct sense_index {
     int64_t span_stride;    // elements between consecutive rows of `spans`
     int metric;
     float* inv_norm;        // owned; NULL for the inner-product metric
+    uint32_t* key_norm_max; // owned, inner product only: the largest key norm (float bits)
     // Dynamic context cache only: capacity > 0, owned token history (the
     // span table, row stride 1) and continuation lengths.
     int64_t capacity;
@@ -262,19 +263,26 @@ SENSE_EXPORT sense_status_t sense_build_index(const sense_index_desc_t* desc, vo
         ix->keys = D.keys;
         ix->ld = D.key_stride;
     }
-    if (D.metric == SENSE_METRIC_COSINE) {
-        if ((e = hipMalloc(&ix->inv_norm, (size_t)D.n * sizeof(float))) != hipSuccess) {
-            if (ix->owned_keys) (void)hipFree(ix->owned_keys);
-            delete ix;
-            return fail(SENSE_ERR_OUT_OF_MEMORY, "norm table: %s", hipGetErrorString(e));
-        }
-        e = sense::launch_key_norms(ix->keys, ix->key_dtype, ix->n, ix->d, ix->ld, ix->inv_norm, st);
-        if (e != hipSuccess) {
-            (void)hipFree(ix->inv_norm);
-            if (ix->owned_keys) (void)hipFree(ix->owned_keys);
-            delete ix;
-            return hip_fail(e, "key norms");
-        }
+    // Cosine: the inverse-norm table.  Inner product: the largest key norm,
+    // which bounds the error of the batched search's hi-only pass.
+    const bool cos = D.metric == SENSE_METRIC_COSINE;
+    e = cos ? hipMalloc(&ix->inv_norm, (size_t)D.n * sizeof(float))
+            : hipMalloc((void**)&ix->key_norm_max, sizeof(uint32_t));
+    if (e != hipSuccess) {
+        if (ix->owned_keys) (void)hipFree(ix->owned_keys);
+        delete ix;
+        return fail(SENSE_ERR_OUT_OF_MEMORY, "norm table: %s", hipGetErrorString(e));
+    }
+    if (!cos) e = hipMemsetAsync(ix->key_norm_max, 0, sizeof(uint32_t), st);
+    if (e == hipSuccess)
+        e = sense::launch_key_norms(ix->keys, ix->key_dtype, ix->n, ix->d, ix->ld, ix->inv_norm,
+                                    ix->key_norm_max, st);
+    if (e != hipSuccess) {
+        if (ix->inv_norm) (void)hipFree(ix->inv_norm);
+        if (ix->key_norm_max) (void)hipFree(ix->key_norm_max);
+        if (ix->owned_keys) (void)hipFree(ix->owned_keys);
+        delete ix;
+        return hip_fail(e, "key norms");
     }
     *out = ix;
     return ok();
@@ -314,11 +322,19 @@ SENSE_EXPORT sense_status_t sense_build_dynamic_index(const sense_dynamic_index_
     if (e == hipSuccess) e = hipMalloc((void**)&ix->owned_span_len, rows * sizeof(int32_t));
     if (e == hipSuccess && D.metric == SENSE_METRIC_COSINE)
         e = hipMalloc((void**)&ix->inv_norm, rows * sizeof(float));
+    if (e == hipSuccess && D.metric != SENSE_METRIC_COSINE) {
+        // zeroed by a synchronous copy: the cache's appends may come on any stream
+        const uint32_t zero = 0;
+        e = hipMalloc((void**)&ix->key_norm_max, sizeof(uint32_t));
+        if (e == hipSuccess)
+            e = hipMemcpy(ix->key_norm_max, &zero, sizeof(uint32_t), hipMemcpyHostToDevice);
+    }
     if (e != hipSuccess) {
         if (ix->owned_keys) (void)hipFree(ix->owned_keys);
         if (ix->owned_hist) (void)hipFree(ix->owned_hist);
         if (ix->owned_span_len) (void)hipFree(ix->owned_span_len);
         if (ix->inv_norm) (void)hipFree(ix->inv_norm);
+        if (ix->key_norm_max) (void)hipFree(ix->key_norm_max);
         delete ix;
         return fail(SENSE_ERR_OUT_OF_MEMORY, "dynamic cache of %lld rows: %s",
                     (long long)D.capacity, hipGetErrorString(e));
@@ -350,7 +366,8 @@ SENSE_EXPORT sense_status_t sense_index_append(sense_index_t* ix, const void* ke
     // The new rows' 1/||k|| (cosine) are formed by the same launch.
     hipError_t e = sense::launch_append_rows(keys, keys_dtype, ix->key_dtype, tokens, ix->d, ix->n,
                                              count, ix->max_span, ix->owned_keys, ix->owned_hist,
-                                             ix->owned_span_len, ix->inv_norm, st);
+                                             ix->owned_span_len, ix->inv_norm, ix->key_norm_max,
+                                             st);
     if (e != hipSuccess) return hip_fail(e, "append");
     ix->n += count;
     return ok();
@@ -360,6 +377,7 @@ SENSE_EXPORT sense_status_t sense_destroy_index(sense_index_t* ix) {
     if (!ix) return ok();
     hipError_t e = hipDeviceSynchronize();
     if (ix->inv_norm) (void)hipFree(ix->inv_norm);
+    if (ix->key_norm_max) (void)hipFree(ix->key_norm_max);
     if (ix->owned_keys) (void)hipFree(ix->owned_keys);
     if (ix->owned_hist) (void)hipFree(ix->owned_hist);
     if (ix->owned_span_len) (void)hipFree(ix->owned_span_len);
@@ -420,7 +438,7 @@ static hipError_t retrieve_short(const sense_index* ix, const float* qptr, int n
     hipError_t e;
     if ((e = timer_mark(SENSE_TIMER_SCAN, 0, st)) != hipSuccess) return e;
     if ((e = sense::launch_query_split(qptr, nq, ix->d, ix->key_dtype, ix->inv_norm != nullptr,
-                                       ws + L.m_off, st)) != hipSuccess)
+                                       nullptr, ws + L.m_off, st)) != hipSuccess)
         return e;
     const sense::QuerySplit qs = sense::query_split_parts(ws + L.m_off, nq, ix->d);
     const bool sample = n > kShortDirectMax;
@@ -493,11 +511,12 @@ static hipError_t retrieve_short(const sense_index* ix, const float* qptr, int n
 // the top-k of the survivors (exact: every row of the true top k reaches the
 // threshold).
 //
-// Cosine with a sampled threshold runs the matrix cores on the hi half of
-// the query alone (half the instructions and query fragments of the hi + lo
-// split; the split measured 1.3x slower at 64 queries) and makes up for it
+// A sampled threshold runs the matrix cores on the hi half of the query
+// alone (half the instructions and query fragments of the hi + lo split;
+// the split measured 1.3x slower at 64 queries) and makes up for it
 // exactly: with b a bound on |approximate score A - fp32 rescore R| of any
-// row (margin = 2b, per query),
+// row (margin = 2b, per query; for inner product through the store's
+// largest key norm),
 //   threshold  = (sample's k-th best A) - 2b: the k sample rows reaching it
 //                have R >= that + b, so the k-th best R is at least that + b
 //                and every row of the R-top-k has A >= it;
@@ -505,7 +524,6 @@ static hipError_t retrieve_short(const sense_index* ix, const float* qptr, int n
 //                the same argument over the survivors, which hold the A-top-k;
 //   rescore    = R of every band row (fp32, as the single-query scan);
 //   result     = the top k of the band by (R desc, row asc).
-// Inner product keeps the split (a bound would need every key's norm).
 //
 // Timers: SCAN spans the query split, the sample, its top-k and the filtered
 // pass; FILTER the first query group's filtered pass alone; TOPK the rest.
@@ -518,11 +536,12 @@ static hipError_t retrieve_batched(const sense_index* ix, const float* qptr, int
     hipError_t e;
     if ((e = timer_mark(SENSE_TIMER_SCAN, 0, st)) != hipSuccess) return e;
     if ((e = sense::launch_query_split(qptr, nq, ix->d, ix->key_dtype, ix->inv_norm != nullptr,
-                                       ws + L.m_off, st)) != hipSuccess)
+                                       (const float*)ix->key_norm_max, ws + L.m_off, st)) !=
+        hipSuccess)
         return e;
     const sense::QuerySplit qs = sense::query_split_parts(ws + L.m_off, nq, ix->d);
     const bool sample = n > kBatchDirectMax;
-    const bool rescore = sample && ix->inv_norm != nullptr;
+    const bool rescore = sample;
     const bool mfma_split = split && !rescore;
     const int64_t step = sample ? n / kBatchSample : 1;
     const int64_t slot_area = sense::mfma_scan_waves(n) * sense::kMfmaSlots;
@@ -1194,7 +1213,8 @@ SENSE_EXPORT sense_status_t sense_build_ivf_index(const sense_ivf_desc_t* desc, 
                                      ix->cursor, ix->row_ids, pq ? nullptr : ix->owned_keys,
                                      ix->codes_sorted, st);
     if (e == hipSuccess && ix->inv_norm)
-        e = sense::launch_key_norms(ix->owned_keys, D.key_dtype, D.n, D.d, D.d, ix->inv_norm, st);
+        e = sense::launch_key_norms(ix->owned_keys, D.key_dtype, D.n, D.d, D.d, ix->inv_norm,
+                                    nullptr, st);
     if (e == hipSuccess) e = hipStreamSynchronize(st);
     if (e == hipSuccess)
         e = hipMemcpy(host_counts, ix->counts, (nl + 2) * sizeof(int32_t), hipMemcpyDeviceToHost);

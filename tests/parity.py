@@ -122,19 +122,20 @@ class ScoreBound:
 
 
 # Stores of more than this many rows are searched in batches through a
-# sampled threshold; with cosine, the returned scores are then fp32 rescores
-# of the band around the k-th (the single-query scan's arithmetic).
+# sampled threshold; for long keys the returned scores are then fp32
+# rescores of the band around the k-th (the single-query scan's arithmetic).
 BATCH_DIRECT_MAX = 131072
 
 
 def retrieval_path(n_queries: int, d: int, n: int = 0, metric: str = "cosine") -> str:
     """The arithmetic of the scores sense_retrieve returns for a static index:
     single queries from the vector ALUs (the short-row scan for d <= 64),
-    batches of two or more from the matrix cores, except cosine batches of
-    long keys over more than BATCH_DIRECT_MAX rows, whose returned scores
-    are fp32 rescores (the single-query scan's sum order)."""
+    batches of two or more from the matrix cores, except batches of long keys
+    over more than BATCH_DIRECT_MAX rows, whose returned scores are fp32
+    rescores (the single-query scan's sum order).  (metric: either; kept for
+    callers that name it.)"""
     if n_queries >= 2:
-        if d > 64 and n > BATCH_DIRECT_MAX and metric == "cosine":
+        if d > 64 and n > BATCH_DIRECT_MAX:
             return "gemv"
         return "mfma"
     return "short" if d <= 64 else "gemv"

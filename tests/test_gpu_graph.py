@@ -59,3 +59,51 @@ def test_graph_replay_matches_eager():
         step()                                    # eager work between replays
         torch.cuda.synchronize()
     index.close()
+
+
+@pytest.mark.parametrize("metric", ["cosine", "ip"])
+def test_graph_replay_batched_sampled_retrieval(metric):
+    """A batch over a store large enough for the sampled threshold (query
+    split, sample pass and top-k, threshold, filtered pass with atomic
+    overflow positions, survivors' top-k; for cosine also the band and its
+    rescore) captured once and replayed: every replay equals the eager call."""
+    dev = torch.device("cuda")
+    w = synth.scaled(synth.WORKLOADS["13b-batched-4m-d5120"], n=140_007, d=256, k=64,
+                     n_queries=16, n_clusters=600)
+    ds = synth.make_datastore(w, 23, dev)
+    q, _ = synth.make_queries(w, ds, 23)
+    index = sense.sense_build_index(ds.keys, ds.spans, metric=metric)
+    nq, k, m = w.n_queries, w.k, w.span
+    ws = torch.empty(sense.sense_retrieve_workspace_size(index, nq, k), dtype=torch.uint8,
+                     device=dev)
+    outs = (torch.empty((nq, k), dtype=torch.int64, device=dev),
+            torch.empty((nq, k), dtype=torch.float32, device=dev),
+            torch.empty((nq, k, m), dtype=torch.int32, device=dev),
+            torch.empty((nq, k), dtype=torch.int32, device=dev))
+
+    def step(stream=None):
+        sense.sense_retrieve(index, q, k, workspace=ws, out=outs, stream=stream)
+
+    step()
+    torch.cuda.synchronize()
+    ref = [t.clone() for t in outs]
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            step(stream=s)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    for _ in range(4):
+        for t in outs:
+            t.zero_()
+        ws.fill_(0xA5)                            # stale scratch must not matter
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for x, y in zip(outs, ref):
+            assert torch.equal(x, y)
+        step()
+        torch.cuda.synchronize()
+    index.close()

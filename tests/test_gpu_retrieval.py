@@ -112,6 +112,7 @@ BATCHED = [
     ("q5-sampled-d1000-bf16", 150_001, 1000, "bf16", 5, 16),   # ragged 32-dim step
     ("q64-sampled-d128-f16", 200_003, 128, "f16", 64, 128),
     ("q70-sampled-d96-bf16", 135_000, 96, "bf16", 70, 32),     # two sampled query groups
+    ("q8-sampled-k1024-d128-bf16", 140_007, 128, "bf16", 8, 1024),
 ]
 
 
@@ -213,20 +214,22 @@ def test_exact_scores_select_exactly(n, k, nq, d):
     print("[case] ok", flush=True)
 
 
-@pytest.mark.parametrize("n,d,dt,nq,k", [
-    (140_007, 128, "bf16", 4, 64),
-    (150_001, 256, "f16", 16, 100),
-    (140_007, 1000, "bf16", 64, 32),
+@pytest.mark.parametrize("n,d,dt,nq,k,metric", [
+    (140_007, 128, "bf16", 4, 64, "cosine"),
+    (150_001, 256, "f16", 16, 100, "cosine"),
+    (140_007, 1000, "bf16", 64, 32, "cosine"),
+    (140_007, 128, "bf16", 4, 64, "ip"),
+    (150_001, 512, "f16", 16, 100, "ip"),
 ])
-def test_rescored_band_restores_exact_order(n, d, dt, nq, k):
-    """Cosine batches over a sampled store take the matrix cores on the
-    query's hi half alone, then rescore a band around the k-th in fp32.  Here
-    one tight cluster holds more rows than k with cosines to the queries
-    spread far less than the hi-only error (the approximate order is
-    scrambled), so only a complete band and a correct rescore return the
-    oracle's top k.  Five identical rows copied from the query, rounded to
-    the key type, score equally and must come first in row order."""
-    print(f"[case] rescored band n={n} d={d} {dt} Q={nq} k={k}", flush=True)
+def test_rescored_band_restores_exact_order(n, d, dt, nq, k, metric):
+    """Batches over a sampled store take the matrix cores on the query's hi
+    half alone, then rescore a band around the k-th in fp32.  Here one tight
+    cluster holds more rows than k with cosines to the queries spread far
+    less than the hi-only error (the approximate order is scrambled), so only
+    a complete band and a correct rescore return the oracle's top k.  Five
+    identical rows, twice the first query rounded to the key type, score
+    equally and must come first in row order."""
+    print(f"[case] rescored band n={n} d={d} {dt} Q={nq} k={k} {metric}", flush=True)
     rng = np.random.default_rng(zlib.crc32(f"band-{n}-{d}-{nq}".encode()))
     cen = rng.normal(0.0, 1.0, d)
     keys = rng.normal(0.0, 1.0, (n, d))
@@ -237,14 +240,14 @@ def test_rescored_band_restores_exact_order(n, d, dt, nq, k):
     kt = torch.tensor(keys, dtype=torch.float32).to(tdt)
     planted = np.sort(rng.choice(np.setdiff1d(np.arange(n), mates), 5, replace=False))
     qt = torch.tensor(q, dtype=torch.float32)
-    kt[torch.as_tensor(planted)] = qt[0].to(tdt)
+    kt[torch.as_tensor(planted)] = qt[0].to(tdt) * 2
     spans = torch.tensor(rng.integers(0, 32000, (n, 6)), dtype=torch.int32)
-    index = sense.sense_build_index(kt.to(DEV), spans.to(DEV), None)
+    index = sense.sense_build_index(kt.to(DEV), spans.to(DEV), None, metric=metric)
     ids, scores, drafts, _ = sense.sense_retrieve(index, qt.to(DEV), k)
     torch.cuda.synchronize()
     kb = host_bits(kt)
-    o_s = oracle.scores(kb, dt, q.astype(np.float32), "f32")
-    bounds = query_bounds(kb, dt, q.astype(np.float32), "cosine")
+    o_s = oracle.scores(kb, dt, q.astype(np.float32), "f32", metric=metric)
+    bounds = query_bounds(kb, dt, q.astype(np.float32), metric)
     ids_h, sc_h = ids.cpu().numpy(), scores.cpu().numpy()
     assert np.array_equal(ids_h[0, :5], planted), f"planted copies {planted} vs {ids_h[0, :5]}"
     assert len(set(sc_h[0, :5].tolist())) == 1, "identical rows scored differently"
@@ -256,6 +259,46 @@ def test_rescored_band_restores_exact_order(n, d, dt, nq, k):
     print(f"[case] ok: ranks excused as near ties within the derived bounds: {excused}",
           flush=True)
     index.close()
+
+
+@pytest.mark.parametrize("metric", ["ip", "cosine"])
+def test_dynamic_cache_batched_sampled(metric):
+    """A dynamic cache grown past 131072 rows by appends, searched by a batch:
+    the sampled threshold, the hi-only pass and the band rescore run on the
+    cache.  For inner product the margin scales with the cache's largest key
+    norm, which the appends keep: the second append brings rows four times
+    longer than the first's, among them the queries' best matches."""
+    n1, n2, d, nq, k, m = 70_000, 70_007, 128, 8, 64, 6
+    print(f"[case] dynamic cache {n1}+{n2} rows d={d} Q={nq} {metric}", flush=True)
+    rng = np.random.default_rng(31)
+    k1 = rng.normal(0.0, 1.0, (n1, d))
+    k2 = rng.normal(0.0, 1.0, (n2, d)) * 4.0
+    q = rng.normal(0.0, 1.0, (nq, d))
+    best = rng.choice(n2, nq * 40, replace=False)
+    for i in range(nq):                            # rows close to each query
+        k2[best[i * 40:(i + 1) * 40]] = 4.0 * (q[i] + rng.normal(0.0, 0.05, (40, d)))
+    tok = torch.tensor(rng.integers(0, 32000, n1 + n2), dtype=torch.int32)
+    cache = sense.sense_build_dynamic_index(d, n1 + n2 + 5, m, key_dtype=torch.bfloat16,
+                                            metric=metric)
+    sense.sense_index_append(cache, torch.tensor(k1, dtype=torch.float32).to(DEV), tok[:n1].to(DEV))
+    sense.sense_index_append(cache, torch.tensor(k2, dtype=torch.float32).to(DEV), tok[n1:].to(DEV))
+    qt = torch.tensor(q, dtype=torch.float32).to(DEV)
+    ids, scores, drafts, dlen = sense.sense_retrieve(cache, qt, k)
+    torch.cuda.synchronize()
+    kb = host_bits(torch.tensor(np.concatenate([k1, k2]), dtype=torch.float32).to(torch.bfloat16))
+    o_s = oracle.scores(kb, "bf16", q.astype(np.float32), "f32", metric=metric)
+    bounds = query_bounds(kb, "bf16", q.astype(np.float32), metric)
+    spans, lens = oracle.dynamic_spans(tok.numpy(), m)
+    excused = 0
+    for qi in range(nq):
+        excused += check_topk(ids[qi].cpu().numpy(), scores[qi].cpu().numpy(), o_s[qi], k,
+                              bounds[qi])
+        o_dr, o_dl = oracle.gather(spans, lens, ids[qi].cpu().numpy())
+        assert np.array_equal(drafts[qi].cpu().numpy(), o_dr)
+        assert np.array_equal(dlen[qi].cpu().numpy(), o_dl)
+    print(f"[case] ok: ranks excused as near ties within the derived bounds: {excused}",
+          flush=True)
+    cache.close()
 
 
 def test_rescored_band_nan_rows():

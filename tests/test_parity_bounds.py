@@ -119,10 +119,11 @@ def test_bound_rejects_a_real_error():
     assert (np.abs(got - exact) > b).any()
 
 
-# The batched cosine search over large stores ranks by a fp32 rescore of a
-# band chosen with hi-only matrix-core scores; query_split_kernel's margin
-# (restated below) must bound |hi-only score - rescore| twice over, also for
-# rows built to make the hi half's error as large as Cauchy-Schwarz allows.
+# The batched search over large stores ranks by a fp32 rescore of a band
+# chosen with hi-only matrix-core scores; query_split_kernel's margin
+# (restated below; inner product through the store's largest key norm) must
+# bound |hi-only score - rescore| twice over, also for rows built to make the
+# hi half's error as large as Cauchy-Schwarz allows.
 
 def rescore_emulate(k, q):
     """rescore_kernel's sum: lane l takes the 8-element units l, l + 64, ...;
@@ -147,17 +148,24 @@ def rescore_emulate(k, q):
     return a[:, 0]
 
 
-def kernel_margin(q, kdt, d):
+def kernel_margin(q, kdt, d, kmax=None):
+    """Cosine (kmax None), or inner product with the store's largest key norm."""
     hi = decode_rows(to_bits(q, kdt), kdt)
     ll = f32(((q - hi) ** 2).sum())
-    inv_q = f32(1.0) / np.sqrt(f32((q * q).sum()))
+    ss = f32((q * q).sum())
+    inv_q = f32(1.0) / np.sqrt(ss)
     depth = (-(-d // 32) + 8) + (d // 128 + 8) + 2 * (d // 64 + 16) + 4
-    return 2.0 * (1.01 * float(np.sqrt(ll)) * float(inv_q) + 2.0 * 1.01 * depth * 2.0 ** -24)
+    rnd = depth * 2.0 ** -24
+    if kmax is None:
+        return 2.0 * (1.01 * float(np.sqrt(ll)) * float(inv_q) + 2.0 * 1.01 * rnd)
+    return 2.0 * (1.01 * float(np.sqrt(ll)) + 2.0 * 1.01 * rnd * float(np.sqrt(ss))) * (
+        1.001 * float(f32(kmax)))
 
 
+@pytest.mark.parametrize("metric", ["cosine", "ip"])
 @pytest.mark.parametrize("d,kdt", [(128, "bf16"), (1000, "f16"), (4096, "bf16"),
                                    (5120, "f16"), (8192, "bf16")])
-def test_batched_margin_bounds_hi_only_against_rescore(d, kdt):
+def test_batched_margin_bounds_hi_only_against_rescore(d, kdt, metric):
     rng = np.random.default_rng(d * 3 + len(kdt))
     kb = make_rows(rng, 120, d, kdt)
     k = decode_rows(kb, kdt)
@@ -171,15 +179,21 @@ def test_batched_margin_bounds_hi_only_against_rescore(d, kdt):
     adv += [np.sign(lo) * np.abs(k[j]) for j in range(4)]
     kb = np.concatenate([kb, to_bits(np.array(adv), kdt)])
     k = decode_rows(kb, kdt)
-    a = cosine_scale(k, q, mfma_emulate(k, q, kdt, split=False)).astype(np.float64)
-    r = cosine_scale(k, q, rescore_emulate(k, q)).astype(np.float64)
-    m = kernel_margin(q, kdt, d)
+    a = mfma_emulate(k, q, kdt, split=False)
+    r = rescore_emulate(k, q)
+    if metric == "cosine":
+        a, r = cosine_scale(k, q, a), cosine_scale(k, q, r)
+        m = kernel_margin(q, kdt, d)
+    else:
+        # the index's largest key norm: fp32 sums of squares, rounded sqrt
+        m = kernel_margin(q, kdt, d, kmax=np.sqrt(pairwise_f32(k * k)).astype(f32).max())
+    a, r = a.astype(np.float64), r.astype(np.float64)
     gap = np.abs(a - r)
     assert (gap <= m / 2).all(), f"row {np.argmax(gap > m / 2)}: |A - R| {gap.max():.3g} > {m / 2:.3g}"
     # the adversarial rows use a large part of the allowance: the margin is
     # not loose by orders of magnitude (a band that holds the whole store)
     assert gap[-len(adv):].max() > 0.25 * (m / 2), (gap[-len(adv):].max(), m)
     # and the rescore is the single-query scan's accuracy
-    exact = oracle.scores(kb, kdt, q.astype(np.float32)[None, :], "f32", metric="cosine")[0]
-    b = ScoreBound(kb, kdt, q, "cosine", "gemv")(np.arange(k.shape[0]))
+    exact = oracle.scores(kb, kdt, q.astype(np.float32)[None, :], "f32", metric=metric)[0]
+    b = ScoreBound(kb, kdt, q, metric, "gemv")(np.arange(k.shape[0]))
     assert (np.abs(r - exact) <= b).all()
