@@ -113,6 +113,8 @@ BATCHED = [
     ("q64-sampled-d128-f16", 200_003, 128, "f16", 64, 128),
     ("q70-sampled-d96-bf16", 135_000, 96, "bf16", 70, 32),     # two sampled query groups
     ("q8-sampled-k1024-d128-bf16", 140_007, 128, "bf16", 8, 1024),
+    ("q20-sampled-d1024-f16", 140_007, 1024, "f16", 20, 32),   # two query tiles
+    ("q40-sampled-d512-bf16", 140_007, 512, "bf16", 40, 16),   # three query tiles
 ]
 
 
