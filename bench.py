@@ -43,6 +43,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="approximate CPU time spent timing the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--config-cpu-seconds", type=float, default=3.0,
+                    help="approximate CPU time for the oracle timing of each other configuration")
     ap.add_argument("--graph", action="store_true",
                     help="also time replays of the step captured as one HIP graph (on this "
                          "ROCm the replays measured a few us slower than eager launches)")
@@ -94,7 +96,7 @@ def traffic_from_profiles(workload: str, kernel: str = "scan_gemv_kernel"):
     return int(fields["bytes_per_launch"])
 
 
-def cpu_baseline(w, ds, q, logits, drafts, budget_s: float):
+def cpu_baseline(w, ds, q, logits, drafts, budget_s: float, max_sample_bytes=None):
     """The oracle as it stands, timed on this host on a bounded sample of the
     same workload, scaled to one query (its scan + sort + gather + verify)."""
     import numpy as np
@@ -112,6 +114,8 @@ def cpu_baseline(w, ds, q, logits, drafts, budget_s: float):
     oracle.scores(keys_cal, kb_dt, qh[:1], "f32", metric=w.metric)
     per_row = (time.perf_counter() - t0) / cal
     rows = int(min(w.n, max(cal, 0.6 * budget_s / max(per_row, 1e-9))))
+    if max_sample_bytes is not None:          # keys copied to the host for the sample
+        rows = max(cal, min(rows, int(max_sample_bytes // (ds.keys.shape[1] * 2))))
     keys_s = ds.keys[:rows].cpu().view(torch.int16).numpy().view(np.uint16)
     t0 = time.perf_counter()
     oracle.scores(keys_s, kb_dt, qh[:1], "f32", metric=w.metric)
@@ -688,7 +692,8 @@ def close_workload(ctx):
 def config_summary(res):
     """The figures of one configuration's run kept in the headline line."""
     keep = ("ms_per_step", "value", "scan_ms", "filter_ms", "topk_ms", "verify_ms",
-            "hbm_gbps", "hbm_read_ceiling_gbps", "roofline", "mfma", "retrieval_scan_gbps")
+            "hbm_gbps", "hbm_read_ceiling_gbps", "roofline", "mfma", "retrieval_scan_gbps",
+            "cpu_baseline")
     out = {k: res[k] for k in keep if k in res}
     out["queries_per_s"] = out.pop("value")
     c = res["config"]
@@ -729,12 +734,18 @@ def main():
     del ctx
     if args.workload is None and not args.no_configs:
         # Every other configuration once, on the same device, after the
-        # headline (its own steps, fewer of them; no SEN leg or CPU baseline).
+        # headline (its own steps, fewer of them; no SEN leg; the oracle timed
+        # on a smaller sample).
         res["configs"] = {}
         for cname in CONFIG_WORKLOADS:
             if cname == name:
                 continue
             r, c = run_workload(cname, args, dev, min(K, 10), min(args.warmup, 2))
+            if not args.no_cpu_baseline:
+                # the oracle per query on this workload, a smaller sample
+                r["cpu_baseline"] = cpu_baseline(c["w"], c["ds"], c["q"], c["logits"],
+                                                 c["drafts"], args.config_cpu_seconds,
+                                                 max_sample_bytes=2e9)
             close_workload(c)
             del c
             res["configs"][cname] = config_summary(r)
