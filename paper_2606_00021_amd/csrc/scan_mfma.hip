@@ -464,8 +464,25 @@ hipError_t launch_tile(const MfmaScan& s, hipStream_t stream) {
     return hipGetLastError();
 }
 
+// WRITE passes over few rows (a strided sample, a small store) with the hi
+// half alone: blocks of 128 keys, so that every compute unit gets one (a
+// block of 256 keys per unit would leave half of them idle on a 32768-row
+// sample, and one unit streams a block at a fraction of the chip's rate).
+template <int KT>
+hipError_t launch_group_narrow(const MfmaScan& s, hipStream_t stream) {
+    switch ((s.nq + 15) / 16) {
+        case 1: return launch_tile<KT, 1, 2, 4, false>(s, stream);
+        case 2: return launch_tile<KT, 2, 2, 4, false>(s, stream);
+        case 3: return launch_tile<KT, 3, 2, 4, false>(s, stream);
+        default: return launch_tile<KT, 4, 2, 4, false>(s, stream);
+    }
+}
+
 template <int KT, bool SPLIT>
 hipError_t launch_group(const MfmaScan& s, hipStream_t stream) {
+    if constexpr (!SPLIT)
+        if (s.cand == nullptr && mfma_groups(s.n_rows, 4) < (int64_t)device_cus())
+            return launch_group_narrow<KT>(s, stream);
     switch ((s.nq + 15) / 16) {
         case 1: return launch_tile<KT, 1, 4, 4, SPLIT>(s, stream);
         case 2: return launch_tile<KT, 2, 4, 3, SPLIT>(s, stream);
