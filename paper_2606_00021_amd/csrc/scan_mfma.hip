@@ -549,11 +549,14 @@ __global__ __launch_bounds__(kBandThreads) void band_kernel(uint64_t* __restrict
 // whose row r is what matters) becomes pack_key(R, r) with
 //   R = ((sum_t q_t K[r, t]) * inv_norm[r]) * inv_qn[q]
 // from the fp32 query and the stored key, as the single-query scan forms it:
-// lane l takes the 16-byte units l, l + 64, ... of the row, alternately into
-// two fp32 FMA chains (element order inside a unit), the chains are added
-// and the wave sums its 64 lanes by butterfly.  One wave per entry; blocks
-// (4 waves) stride over the entries of their query (blockIdx.y).
-template <int KT>
+// lane l takes the 16-byte units l + 64 c (c < NC = ceil(d / 512)) of the
+// row, units with even c into one fp32 FMA chain and odd c into another
+// (element order inside a unit), the chains are added and the wave sums its
+// 64 lanes by butterfly.  One wave per entry; blocks (4 waves) stride over
+// the entries of their query (blockIdx.y).  The lane's query values stay in
+// registers, and a row's NC loads are all requested before the first
+// product, so a row costs one round trip.
+template <int KT, int NC>
 __global__ __launch_bounds__(256) void rescore_kernel(uint64_t* __restrict__ cand, int64_t cap,
                                                       const int32_t* __restrict__ counts,
                                                       const uint16_t* __restrict__ keys,
@@ -569,39 +572,42 @@ __global__ __launch_bounds__(256) void rescore_kernel(uint64_t* __restrict__ can
     const float* __restrict__ qrow = queries + (int64_t)q * d;
     const float iq = inv_qn[q];
     const int nu = d / 8;
+    float qv[NC][8];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+        const int u = lane + 64 * c;
+        f32x4 q0 = f32x4{0.0f, 0.0f, 0.0f, 0.0f}, q1 = q0;
+        if (u < nu) {
+            q0 = *(const f32x4*)(qrow + u * 8);
+            q1 = *(const f32x4*)(qrow + u * 8 + 4);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            qv[c][i] = q0[i];
+            qv[c][4 + i] = q1[i];
+        }
+    }
     for (int64_t e = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); e < cnt;
          e += (int64_t)gridDim.x * 4) {
         const uint32_t r = key_row(list[e]);
         const uint16_t* __restrict__ krow = keys + (int64_t)r * ld;
+        u32x4 kv[NC];
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            // a unit past the row (last chunk only) re-reads unit 0; its
+            // query values are 0 and its products are skipped below
+            const int u = lane + 64 * c;
+            kv[c] = *(const u32x4*)(krow + (int64_t)(u < nu ? u : 0) * 8);
+        }
         float a0 = 0.0f, a1 = 0.0f;
-        for (int u = lane; u < nu; u += 128) {
-            {
-                const u32x4 kv = *(const u32x4*)(krow + (int64_t)u * 8);
-                const f32x4 q0 = *(const f32x4*)(qrow + u * 8);
-                const f32x4 q1 = *(const f32x4*)(qrow + u * 8 + 4);
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    a0 = __builtin_fmaf(q0[i], from_key_bits<KT>((uint16_t)(kv[i / 2] >> (16 * (i & 1)))), a0);
-                }
+        for (int c = 0; c < NC; ++c) {
+            if (c == NC - 1 && lane + 64 * c >= nu) break;
+            float& a = (c & 1) ? a1 : a0;
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    a0 = __builtin_fmaf(q1[i], from_key_bits<KT>((uint16_t)(kv[2 + i / 2] >> (16 * (i & 1)))), a0);
-                }
-            }
-            const int u2 = u + 64;
-            if (u2 < nu) {
-                const u32x4 kv = *(const u32x4*)(krow + (int64_t)u2 * 8);
-                const f32x4 q0 = *(const f32x4*)(qrow + u2 * 8);
-                const f32x4 q1 = *(const f32x4*)(qrow + u2 * 8 + 4);
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    a1 = __builtin_fmaf(q0[i], from_key_bits<KT>((uint16_t)(kv[i / 2] >> (16 * (i & 1)))), a1);
-                }
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    a1 = __builtin_fmaf(q1[i], from_key_bits<KT>((uint16_t)(kv[2 + i / 2] >> (16 * (i & 1)))), a1);
-                }
-            }
+            for (int i = 0; i < 8; ++i)
+                a = __builtin_fmaf(qv[c][i],
+                                   from_key_bits<KT>((uint16_t)(kv[c][i / 2] >> (16 * (i & 1)))), a);
         }
         float a = a0 + a1;
 #pragma unroll
@@ -611,6 +617,32 @@ __global__ __launch_bounds__(256) void rescore_kernel(uint64_t* __restrict__ can
             if (inv_norm) v = v * inv_norm[r];
             list[e] = pack_key(v * iq, r);
         }
+    }
+}
+
+template <int KT, int NC>
+hipError_t launch_rescore_nc(uint64_t* cand, int64_t cap, int nq, const int32_t* counts,
+                             const void* keys, int64_t ld, int d, const float* queries,
+                             const float* inv_norm, const float* inv_qn, hipStream_t stream) {
+    hipLaunchKernelGGL((rescore_kernel<KT, NC>), dim3(16, (unsigned)nq), dim3(256), 0, stream,
+                       cand, cap, counts, (const uint16_t*)keys, ld, d, queries, inv_norm, inv_qn);
+    return hipGetLastError();
+}
+
+template <int KT>
+hipError_t launch_rescore_kt(uint64_t* cand, int64_t cap, int nq, const int32_t* counts,
+                             const void* keys, int64_t ld, int d, const float* queries,
+                             const float* inv_norm, const float* inv_qn, hipStream_t stream) {
+    switch ((d + 511) / 512) {
+#define SENSE_NC(N)                                                                           \
+    case N:                                                                                   \
+        return launch_rescore_nc<KT, N>(cand, cap, nq, counts, keys, ld, d, queries, inv_norm, \
+                                        inv_qn, stream);
+        SENSE_NC(1) SENSE_NC(2) SENSE_NC(3) SENSE_NC(4) SENSE_NC(5) SENSE_NC(6) SENSE_NC(7)
+        SENSE_NC(8) SENSE_NC(9) SENSE_NC(10) SENSE_NC(11) SENSE_NC(12) SENSE_NC(13)
+        SENSE_NC(14) SENSE_NC(15) SENSE_NC(16)
+#undef SENSE_NC
+        default: return hipErrorInvalidValue;
     }
 }
 
@@ -688,14 +720,11 @@ hipError_t launch_rescore(uint64_t* cand, int64_t cap, int nq, const int32_t* co
                           const void* keys, int key_dtype, int64_t ld, int d,
                           const float* queries, const float* inv_norm, const float* inv_qn,
                           hipStream_t stream) {
-    const dim3 grid(16, (unsigned)nq);
     if (key_dtype == DT_BF16)
-        hipLaunchKernelGGL(rescore_kernel<DT_BF16>, grid, dim3(256), 0, stream, cand, cap, counts,
-                           (const uint16_t*)keys, ld, d, queries, inv_norm, inv_qn);
-    else
-        hipLaunchKernelGGL(rescore_kernel<DT_F16>, grid, dim3(256), 0, stream, cand, cap, counts,
-                           (const uint16_t*)keys, ld, d, queries, inv_norm, inv_qn);
-    return hipGetLastError();
+        return launch_rescore_kt<DT_BF16>(cand, cap, nq, counts, keys, ld, d, queries, inv_norm,
+                                          inv_qn, stream);
+    return launch_rescore_kt<DT_F16>(cand, cap, nq, counts, keys, ld, d, queries, inv_norm,
+                                     inv_qn, stream);
 }
 
 }  // namespace sense
