@@ -126,10 +126,12 @@ def test_batched_queries(name, n, d, dt, nq, k, metric):
     run_case(w, seed=zlib.crc32(name.encode()) % 1000 + 1, metric=metric, ragged_spans=True)
 
 
-def test_batched_key_typed_queries():
-    """Queries given in the key type use one MFMA per tile (no lo half)."""
-    w = synth.scaled(synth.WORKLOADS["13b-batched-4m-d5120"], n=6000, d=2048, k=32, n_queries=16,
-                     key_dtype="bf16", n_clusters=60)
+@pytest.mark.parametrize("n,nq", [(6000, 16), (140_007, 40)])
+def test_batched_key_typed_queries(n, nq):
+    """Queries given in the key type use one MFMA per tile (no lo half); over
+    a sampled store the band is then decided by rounding alone."""
+    w = synth.scaled(synth.WORKLOADS["13b-batched-4m-d5120"], n=n, d=2048 if n < 10000 else 512,
+                     k=32, n_queries=nq, key_dtype="bf16", n_clusters=max(60, n // 128))
     ds = synth.make_datastore(w, 12, DEV)
     q, _ = synth.make_queries(w, ds, 12)
     index = sense.sense_build_index(ds.keys, ds.spans)
@@ -138,7 +140,7 @@ def test_batched_key_typed_queries():
     kb = host_bits(ds.keys)
     o_s = oracle.scores(kb, "bf16", host_bits(qq), "bf16")
     bounds = query_bounds(kb, "bf16", qq.float().cpu().numpy(), "cosine", q_in_key_type=True)
-    for qi in range(16):
+    for qi in range(nq):
         check_topk(ids[qi].cpu().numpy(), scores[qi].cpu().numpy(), o_s[qi], w.k, bounds[qi])
     index.close()
 
