@@ -14,7 +14,7 @@ import torch
 
 import oracle
 from paper_2606_00021_amd import sense, synth
-from parity import DeviceRows, check_topk, dt_name, host_bits, query_bounds
+from parity import DeviceRows, ScoreBound, check_topk, dt_name, host_bits, query_bounds
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -303,6 +303,32 @@ def test_dynamic_cache_batched_sampled(metric):
     print(f"[case] ok: ranks excused as near ties within the derived bounds: {excused}",
           flush=True)
     cache.close()
+
+
+@pytest.mark.parametrize("metric", ["cosine", "ip"])
+def test_batched_sampled_all_rows_tie(metric):
+    """Every stored row the same key: every row reaches the sampled threshold
+    and the band, the overflow lists hold nearly the whole store, every row
+    is rescored to the same bits, and the top k are rows 0 .. k-1 in order."""
+    n, d, nq, k = 140_007, 128, 8, 100
+    rng = np.random.default_rng(5)
+    row = torch.tensor(rng.normal(0.0, 1.0, d), dtype=torch.float32).to(torch.bfloat16)
+    keys = row.expand(n, d).contiguous().to(DEV)
+    spans = torch.arange(n * 3, dtype=torch.int32).view(n, 3).to(DEV)
+    index = sense.sense_build_index(keys, spans, None, metric=metric)
+    q = torch.tensor(rng.normal(0.0, 1.0, (nq, d)), dtype=torch.float32).to(DEV)
+    ids, scores, drafts, _ = sense.sense_retrieve(index, q, k)
+    torch.cuda.synchronize()
+    want = torch.arange(k, device=DEV).expand(nq, k)
+    assert torch.equal(ids, want)
+    assert torch.equal(scores, scores[:, :1].expand(nq, k))
+    assert torch.equal(drafts, spans[:k].unsqueeze(0).expand(nq, k, 3))
+    o = oracle.scores(host_bits(keys[:1]), "bf16", q.cpu().numpy(), "f32", metric=metric)[:, 0]
+    # the returned scores are fp32 rescores (the single-query scan's sums)
+    b = [ScoreBound(host_bits(keys[:1]), "bf16", qq, metric, "gemv")(np.array([0]))[0]
+         for qq in q.cpu().numpy().astype(np.float64)]
+    assert (np.abs(scores[:, 0].cpu().numpy().astype(np.float64) - o) <= np.array(b)).all()
+    index.close()
 
 
 def test_rescored_band_nan_rows():
