@@ -175,13 +175,17 @@ __device__ __forceinline__ void barrier_no_fence() { asm volatile("s_barrier" ::
 // bandwidth near 4-5 TB/s on this device; runs of 128 bytes (8 rows per
 // instruction) reach the ~7 TB/s ceiling.  So each DMA instruction fetches 8
 // rows x 128 bytes and the operand layout is produced in LDS: rows 0-7 of a
-// tile go to entries [0, 64), rows 8-15 to [72, 136) (16-byte entries); lane
+// tile go to entries [0, 64), rows 8-15 to [64, 128) (16-byte entries); lane
 // L = 8p + w of an instruction writes entry w of row p and fetches unit
 // (w + p) mod 8 of that row, so unit u of row p sits at entry (u - p) mod 8.
-// The rotation and the 72-entry offset of the second instruction make the
-// 16 rows a matrix-core read touches fall in 16 distinct 16-byte bank groups.
-constexpr int kTileVec = 136;                 // 16-byte entries per key tile
-constexpr int kTileSecond = 72;               // first entry of rows 8-15
+// The rotation spreads the 8 rows of each half that a matrix-core read
+// touches over 8 distinct 16-byte groups of a 128-byte line.  Measured with
+// the LDS bank-conflict counter on this device: no conflicts with the second
+// half at entry 64 (or 80), but a sixth of the read cycles in conflict with
+// it at entry 72, an offset chosen for a 64-bank model in which lanes 0-15
+// are served together.
+constexpr int kTileVec = 128;                 // 16-byte entries per key tile
+constexpr int kTileSecond = 64;               // first entry of rows 8-15
 
 // One workgroup (4 waves) per contiguous run of key blocks; a block is 4*T
 // tiles of 16 keys, T tiles per wave; MT tiles of 16 queries (nq <= 16*MT of
