@@ -234,7 +234,9 @@ sense_status_t sense_retrieve_workspace_size(const sense_index_t *index, int32_t
  *   out_draft_len n_queries x k int32 span lengths, or NULL.
  *   workspace    device scratch of at least sense_retrieve_workspace_size
  *                bytes, 256-byte aligned; its contents are not preserved.
- * Errors: INVALID_ARGUMENT, UNSUPPORTED (k > 1024), MISALIGNED,
+ * Errors: INVALID_ARGUMENT, UNSUPPORTED (k > 1024; a batch of two or more
+ * queries over a store so large that a query's candidate list, up to every
+ * row plus 32 slots per scan wave, would pass 2^31 - 1 entries), MISALIGNED,
  * WORKSPACE, HIP.  An inverted-file index is searched with sense_ivf_search
  * instead (INVALID_ARGUMENT here). */
 sense_status_t sense_retrieve(const sense_index_t *index, const void *queries,

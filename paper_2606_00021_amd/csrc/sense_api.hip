@@ -116,6 +116,7 @@ bool long_batched(const sense_index* ix, int nq) {
 struct ShortLayout {
     size_t q_off, m_off, ss_off, sid_off, ssc_off, sws_off, tau_off, cnt_off, cand_off, fws_off,
         total;
+    int64_t cap;    // entries of one query's candidate list
 };
 
 // Workspace of the sampled-threshold retrieval (short keys, or long keys in
@@ -146,6 +147,7 @@ ShortLayout short_layout(const sense_index* ix, int nq, int k) {
     // every row; also the plain score matrix of small stores
     const int64_t cap = long_keys ? sense::mfma_scan_waves(rows) * sense::kMfmaSlots + rows
                                   : sense::short_scan_waves(rows) * sense::kShortSlots + rows;
+    l.cap = cap;
     l.cand_off = take((size_t)g * cap * sizeof(uint64_t));
     l.fws_off = take(sense::topk_workspace_bytes(cap, g, k));
     l.total = at;
@@ -414,6 +416,16 @@ static sense_status_t check_retrieve_sizes(const sense_index_t* ix, int32_t nq, 
     if ((int64_t)k > ix->n)
         return fail(SENSE_ERR_INVALID_ARGUMENT, "k = %d exceeds the %lld stored rows", k,
                     (long long)ix->n);
+    // Batches keep per-query candidate lists (wave slots, then up to every
+    // row) whose positions are 32-bit.
+    if (short_batched(ix, nq) || long_batched(ix, nq)) {
+        const ShortLayout L = short_layout(ix, nq, k);
+        if (L.cap > (int64_t)INT32_MAX)
+            return fail(SENSE_ERR_UNSUPPORTED,
+                        "a batch over %lld rows needs candidate lists of %lld entries (at most "
+                        "2^31 - 1): search it one query at a time",
+                        (long long)(ix->capacity > 0 ? ix->capacity : ix->n), (long long)L.cap);
+    }
     return SENSE_OK;
 }
 
