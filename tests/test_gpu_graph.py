@@ -107,3 +107,43 @@ def test_graph_replay_batched_sampled_retrieval(metric):
         step()
         torch.cuda.synchronize()
     index.close()
+
+
+def test_concurrent_batched_retrievals_on_two_streams():
+    """Two batched searches of one index on two streams with their own
+    workspaces, enqueued so that they can overlap on the device, return
+    exactly what each returns alone (the library keeps no global state
+    between the kernels of a search)."""
+    dev = torch.device("cuda")
+    w = synth.scaled(synth.WORKLOADS["13b-batched-4m-d5120"], n=140_007, d=256, k=64,
+                     n_queries=24, n_clusters=600)
+    ds = synth.make_datastore(w, 29, dev)
+    q, _ = synth.make_queries(w, ds, 29)
+    index = sense.sense_build_index(ds.keys, ds.spans)
+    qa, qb = q[:16].contiguous(), q[16:].contiguous()
+
+    def bufs(nq):
+        return (torch.empty((nq, w.k), dtype=torch.int64, device=dev),
+                torch.empty((nq, w.k), dtype=torch.float32, device=dev),
+                torch.empty((nq, w.k, w.span), dtype=torch.int32, device=dev),
+                torch.empty((nq, w.k), dtype=torch.int32, device=dev))
+    ws_a = torch.empty(sense.sense_retrieve_workspace_size(index, 16, w.k), dtype=torch.uint8,
+                       device=dev)
+    ws_b = torch.empty(sense.sense_retrieve_workspace_size(index, 8, w.k), dtype=torch.uint8,
+                       device=dev)
+    ref_a, ref_b = bufs(16), bufs(8)
+    sense.sense_retrieve(index, qa, w.k, workspace=ws_a, out=ref_a)
+    sense.sense_retrieve(index, qb, w.k, workspace=ws_b, out=ref_b)
+    torch.cuda.synchronize()
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    for _ in range(3):
+        out_a, out_b = bufs(16), bufs(8)
+        torch.cuda.synchronize()
+        sense.sense_retrieve(index, qa, w.k, workspace=ws_a, out=out_a, stream=sa)
+        sense.sense_retrieve(index, qb, w.k, workspace=ws_b, out=out_b, stream=sb)
+        torch.cuda.synchronize()
+        for x, y in zip(out_a, ref_a):
+            assert torch.equal(x, y)
+        for x, y in zip(out_b, ref_b):
+            assert torch.equal(x, y)
+    index.close()
