@@ -28,6 +28,8 @@ def _outs(nq, k, m):
     # (n, d, n_queries, k): the second call is smaller in every size
     ((300_000, 1024, 1, 64), (30_000, 512, 1, 16)),
     ((120_000, 2048, 8, 32), (9_000, 256, 4, 8)),
+    # a batch over a sampled store (threshold, filtered pass, band, rescore)
+    ((140_007, 256, 8, 32), (20_000, 128, 3, 16)),
 ])
 def test_noalloc_matches_workspace_call(first, second):
     for case, (n, d, nq, k) in (("first", first), ("second", second)):
