@@ -528,9 +528,11 @@ sense_status_t sense_project_workspace_size(const sense_projection_t *proj,
  *              F16 or BF16); only the first d_out of each row are written.
  * 16-bit rows that are 16-byte aligned with x_stride % 8 == 0, 256 rows or
  * more, run as a matrix-core contraction (the basis split into a hi and a lo
- * half of the key type, ~16 mantissa bits for bf16, ~22 for fp16); other
- * inputs run one block per (row, output) in fp32.  Needs workspace (256-byte
- * aligned, sense_project_workspace_size bytes).
+ * half of the key type, ~16 mantissa bits for bf16, ~22 for fp16; up to 64
+ * outputs the centring, normalisation and store happen in the same pass, so
+ * the workspace holds no n_rows x d_out intermediate); other inputs run one
+ * block per (row, output) in fp32.  Needs workspace (256-byte aligned,
+ * sense_project_workspace_size bytes).
  * Errors: INVALID_ARGUMENT, MISALIGNED, WORKSPACE, HIP. */
 sense_status_t sense_project(const sense_projection_t *proj, const void *x,
                              sense_dtype_t x_dtype, int64_t n_rows, int64_t x_stride, void *out,

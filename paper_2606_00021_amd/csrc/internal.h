@@ -143,6 +143,12 @@ struct MfmaScan {
     int32_t* counts;
     uint64_t* cand;
     int64_t cap;
+    const float* centre;      // PROJECT mode (proj_out set): out[key][o] =
+    void* proj_out;           // (acc - centre[o]) * (normalize ? 1 / ||row|| : 1)
+    int proj_dtype;
+    int64_t proj_stride;
+    int normalize;
+    int proj_vec;             // 4 outputs per store (16-byte base, stride % 4, nq % 4)
 };
 constexpr int kMfmaSlots = 32;
 hipError_t launch_scan_mfma_rows(const MfmaScan& s, bool split, hipStream_t stream);
@@ -160,6 +166,13 @@ hipError_t launch_scan_small(const void* keys, int key_dtype, int64_t n, int d, 
 // PCA projection (+ L2 normalisation) of n rows; see project.hip.
 bool project_uses_mfma(int x_dtype, const void* x, int64_t x_stride, int64_t n);
 size_t project_workspace_bytes(int x_dtype, int64_t n, int d_in, int d_out);
+// Fused projection of 16-bit rows onto at most kMfmaProjOut basis rows on the
+// matrix cores: centring, normalisation and the store in the epilogue.
+constexpr int kMfmaProjOut = 64;
+hipError_t launch_project_mfma(const void* x, int x_dtype, int64_t n, int d_in, int64_t x_stride,
+                               const float* basis, int d_out, const float* centre, int normalize,
+                               void* out, int out_dtype, int64_t out_stride, void* scratch,
+                               hipStream_t stream);
 hipError_t launch_project(const void* x, int x_dtype, int64_t n, int d_in, int64_t x_stride,
                           const float* mean, const float* basis, int d_out, int normalize,
                           void* out, int out_dtype, int64_t out_stride, void* workspace,

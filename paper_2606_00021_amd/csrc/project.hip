@@ -8,9 +8,10 @@
 //   * many 16-bit rows (building a projected datastore) is a dense
 //     contraction N x d_in x d_out: it runs on the matrix cores through the
 //     batched similarity kernel with the basis rows as the "queries" (fp32
-//     basis split into hi + lo halves of the key type), giving
-//     S[o][i] = x_i . w_o; then project_finish subtracts mean . w_o,
-//     normalises each row and stores it transposed in the output type;
+//     basis split into hi + lo halves of the key type).  Up to 64 outputs
+//     its epilogue subtracts mean . w_o, normalises each row and stores it
+//     in the output type; beyond that it writes S[o][i] = x_i . w_o and
+//     project_finish does the same from S;
 //   * a few rows (queries) or fp32 / unaligned rows: blocks of 2 rows x 16
 //     outputs centre their rows in LDS and form the dot products (one wave
 //     per output, fixed-order sums); then one wave per row normalises and
@@ -237,13 +238,18 @@ bool project_uses_mfma(int x_dtype, const void* x, int64_t x_stride, int64_t n) 
            x_stride % 8 == 0;
 }
 
-// Workspace: [centre (d_out fp32) | S (d_out x n fp32) | MFMA scratch].
+// Workspace: [centre (d_out fp32) | S (d_out x n fp32; not for a fused
+// projection) | MFMA scratch].
 static size_t up256(size_t x) { return (x + 255) / 256 * 256; }
+
+static bool project_fused(int d_out) { return d_out <= kMfmaProjOut; }
 
 size_t project_workspace_bytes(int x_dtype, int64_t n, int d_in, int d_out) {
     if (n == 0) return 0;
-    size_t bytes = up256((size_t)d_out * sizeof(float)) + up256((size_t)d_out * n * sizeof(float));
-    if (x_dtype != DT_F32 && n >= kProjMfmaMinRows) bytes += up256(scan_mfma_scratch_bytes(d_out, d_in));
+    const bool mfma = x_dtype != DT_F32 && n >= kProjMfmaMinRows;
+    size_t bytes = up256((size_t)d_out * sizeof(float));
+    if (!(mfma && project_fused(d_out))) bytes += up256((size_t)d_out * n * sizeof(float));
+    if (mfma) bytes += up256(scan_mfma_scratch_bytes(d_out, d_in));
     return bytes;
 }
 
@@ -256,7 +262,6 @@ hipError_t launch_project(const void* x, int x_dtype, int64_t n, int d_in, int64
     const size_t c_bytes = up256((size_t)d_out * sizeof(float));
     float* centre = mean ? (float*)ws : nullptr;
     float* s = (float*)(ws + c_bytes);
-    void* scratch = ws + c_bytes + up256((size_t)d_out * n * sizeof(float));
     hipError_t e;
     if (!project_uses_mfma(x_dtype, x, x_stride, n)) {
         if (x_dtype == DT_F32)
@@ -276,6 +281,10 @@ hipError_t launch_project(const void* x, int x_dtype, int64_t n, int d_in, int64
                            dim3(kProjThreads), 0, stream, mean, basis, d_in, d_out, centre);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
+    if (project_fused(d_out))
+        return launch_project_mfma(x, x_dtype, n, d_in, x_stride, basis, d_out, centre, normalize,
+                                   out, out_dtype, out_stride, ws + c_bytes, stream);
+    void* scratch = ws + c_bytes + up256((size_t)d_out * n * sizeof(float));
     if ((e = launch_scan_mfma(x, x_dtype, n, d_in, x_stride, basis, d_out, true, nullptr, s,
                               scratch, stream)) != hipSuccess)
         return e;

@@ -27,6 +27,7 @@ namespace {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 
@@ -207,7 +208,11 @@ constexpr int kTileSecond = 64;               // first entry of rows 8-15
 // row (their outputs are never stored); dimensions past d occur only in the
 // last stage, load a clamped address and are zeroed at use.
 //
-// Epilogue per block: WRITE mode stores every score; FILTER mode keeps only
+// Epilogue per block (MODE): WRITE stores every score; PROJECT (the basis
+// rows of a PCA projection as the queries, up to 64 of them) subtracts each
+// output's centre, normalises the key's row of outputs (the four lanes
+// holding it add their squares) and stores it row-major in the output type;
+// FILTER keeps only
 // rows whose score reaches the query's threshold (tau, the packed key of the
 // k-th best row of a sample: every row of the true top k reaches it) as
 // packed (score, row) keys in the query's candidate list: this wave's
@@ -215,8 +220,11 @@ constexpr int kTileSecond = 64;               // first entry of rows 8-15
 // query's overflow list (atomic position).  At Q = 64 the score matrix would
 // be 64 x 4 bytes per row of 16 KiB, few bytes but scattered 64-byte writes
 // that cut the scan's read rate by a fifth; the survivors are ~k*row_step.
-template <int KT, int MT, int T, int P, bool SPLIT, bool FILTER>
+constexpr int kModeWrite = 0, kModeFilter = 1, kModeProject = 2;
+
+template <int KT, int MT, int T, int P, bool SPLIT, int MODE>
 __global__ __launch_bounds__(256) void scan_mfma_kernel(MfmaScan s, int64_t blocks_per_group) {
+    constexpr bool FILTER = MODE == kModeFilter;
     constexpr int NA = MT * (SPLIT ? 2 : 1);      // query fragments per step
     constexpr int NAS = 2 * NA;                   // per stage
     constexpr int NA_W = (NAS + 3) / 4;           // loaded per wave
@@ -268,6 +276,8 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(MfmaScan s, int64_t bloc
             iq[mt][i] = s.inv_qn[q];
             if constexpr (FILTER)
                 th[mt][i] = q < s.nq ? key_score((uint32_t)(s.tau[q] >> 32)) : __builtin_inff();
+            if constexpr (MODE == kModeProject)   // the output's centre, mean . basis row
+                th[mt][i] = (s.centre != nullptr && q < s.nq) ? s.centre[q] : 0.0f;
         }
     // FILTER: survivors so far of this wave per query (equal in a 16-lane group).
     int cnt[MT][4];
@@ -374,7 +384,55 @@ __global__ __launch_bounds__(256) void scan_mfma_kernel(MfmaScan s, int64_t bloc
 #pragma unroll
         for (int t = 0; t < T; ++t) {
             const int64_t key = key0 + t * 16 + col;
-            if constexpr (!FILTER) {
+            if constexpr (MODE == kModeProject) {
+                // out[key][o] = (acc - centre[o]) / ||row||: the key's 16 * MT
+                // outputs sit in the four lanes col, col + 16, col + 32, col + 48.
+                float v[MT][4];
+                float ss = 0.0f;
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        v[mt][i] = acc[t][mt][i] - th[mt][i];
+                        if (mt * 16 + grp * 4 + i < s.nq) ss = __builtin_fmaf(v[mt][i], v[mt][i], ss);
+                    }
+                ss += __shfl_xor(ss, 16, 64);
+                ss += __shfl_xor(ss, 32, 64);
+                float inv = 1.0f;
+                if (s.normalize) inv = (ss > 0.0f) ? 1.0f / __builtin_sqrtf(ss) : 0.0f;
+                if (!kv[t]) continue;
+                if (s.proj_vec) {
+#pragma unroll
+                    for (int mt = 0; mt < MT; ++mt) {
+                        const int o = mt * 16 + grp * 4;
+                        if (o >= s.nq) continue;
+                        const int64_t at = key * s.proj_stride + o;
+                        const float y0 = v[mt][0] * inv, y1 = v[mt][1] * inv;
+                        const float y2 = v[mt][2] * inv, y3 = v[mt][3] * inv;
+                        if (s.proj_dtype == DT_F32) {
+                            *(f32x4*)((float*)s.proj_out + at) = f32x4{y0, y1, y2, y3};
+                        } else {
+                            const int dt = s.proj_dtype;
+                            *(u32x2*)((uint16_t*)s.proj_out + at) =
+                                u32x2{(uint32_t)to_bits16(y0, dt) | ((uint32_t)to_bits16(y1, dt) << 16),
+                                      (uint32_t)to_bits16(y2, dt) | ((uint32_t)to_bits16(y3, dt) << 16)};
+                        }
+                    }
+                } else {
+#pragma unroll
+                    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            const int o = mt * 16 + grp * 4 + i;
+                            if (o < s.nq) {
+                                const int64_t at = key * s.proj_stride + o;
+                                const float y = v[mt][i] * inv;
+                                if (s.proj_dtype == DT_F32) ((float*)s.proj_out)[at] = y;
+                                else ((uint16_t*)s.proj_out)[at] = to_bits16(y, s.proj_dtype);
+                            }
+                        }
+                }
+            } else if constexpr (!FILTER) {
                 if (!kv[t]) continue;
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) {
@@ -460,11 +518,17 @@ hipError_t launch_tile(const MfmaScan& s, hipStream_t stream) {
     const int64_t groups = mfma_groups(s.n_rows, T);
     const int64_t bpg = (nblk + groups - 1) / groups;
     if (s.cand)
-        hipLaunchKernelGGL((scan_mfma_kernel<KT, MT, T, P, SPLIT, true>), dim3((unsigned)groups),
-                           dim3(256), 0, stream, s, bpg);
-    else
-        hipLaunchKernelGGL((scan_mfma_kernel<KT, MT, T, P, SPLIT, false>), dim3((unsigned)groups),
-                           dim3(256), 0, stream, s, bpg);
+        hipLaunchKernelGGL((scan_mfma_kernel<KT, MT, T, P, SPLIT, kModeFilter>),
+                           dim3((unsigned)groups), dim3(256), 0, stream, s, bpg);
+    else if (s.proj_out) {
+        if constexpr (SPLIT && T == 4)   // projections split the fp32 basis
+            hipLaunchKernelGGL((scan_mfma_kernel<KT, MT, T, P, SPLIT, kModeProject>),
+                               dim3((unsigned)groups), dim3(256), 0, stream, s, bpg);
+        else
+            return hipErrorInvalidValue;
+    } else
+        hipLaunchKernelGGL((scan_mfma_kernel<KT, MT, T, P, SPLIT, kModeWrite>),
+                           dim3((unsigned)groups), dim3(256), 0, stream, s, bpg);
     return hipGetLastError();
 }
 
@@ -711,6 +775,34 @@ hipError_t launch_scan_mfma(const void* keys, int key_dtype, int64_t n, int d, i
         if ((e = launch_scan_mfma_rows(s, split, stream)) != hipSuccess) return e;
     }
     return hipSuccess;
+}
+
+hipError_t launch_project_mfma(const void* x, int x_dtype, int64_t n, int d_in, int64_t x_stride,
+                               const float* basis, int d_out, const float* centre, int normalize,
+                               void* out, int out_dtype, int64_t out_stride, void* scratch,
+                               hipStream_t stream) {
+    if (d_out < 1 || d_out > kMfmaProjOut) return hipErrorInvalidValue;
+    const QuerySplit p = query_split_parts(scratch, d_out, d_in);
+    hipError_t e = launch_query_split(basis, d_out, d_in, x_dtype, false, nullptr, scratch, stream);
+    if (e != hipSuccess) return e;
+    MfmaScan s{};
+    s.keys = x;
+    s.key_dtype = x_dtype;
+    s.ld = x_stride;
+    s.n_rows = n;
+    s.row_step = 1;
+    s.d = d_in;
+    s.qhi = p.hi;
+    s.qlo = p.lo;
+    s.inv_qn = p.inv_qn;
+    s.nq = d_out;
+    s.centre = centre;
+    s.proj_out = out;
+    s.proj_dtype = out_dtype;
+    s.proj_stride = out_stride;
+    s.normalize = normalize;
+    s.proj_vec = ((uintptr_t)out % 16) == 0 && out_stride % 4 == 0 && d_out % 4 == 0;
+    return launch_scan_mfma_rows(s, true, stream);
 }
 
 hipError_t launch_band(uint64_t* cand, int64_t cap, int nq, const float* kth, int k,

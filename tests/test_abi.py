@@ -407,7 +407,13 @@ def test_project_workspace_sizes(lib):
     d = proj()
     assert lib.sense_project_workspace_size(ctypes.byref(d), sense.SENSE_BF16, 1 << 20,
                                             ctypes.byref(size)) == 0
-    assert size.value >= 64 * (1 << 20) * 4                # S = d_out x n fp32
+    # matrix-core route, up to 64 outputs: centring and normalisation in the
+    # scan's epilogue, no d_out x n intermediate
+    assert 0 < size.value < 64 * (1 << 20) * 4
+    wide = proj(d_out=100)
+    assert lib.sense_project_workspace_size(ctypes.byref(wide), sense.SENSE_BF16, 1 << 20,
+                                            ctypes.byref(size)) == 0
+    assert size.value >= 100 * (1 << 20) * 4               # S = d_out x n fp32
     assert lib.sense_project_workspace_size(ctypes.byref(d), sense.SENSE_F32, 1 << 20,
                                             ctypes.byref(size)) == 0
     assert size.value >= 64 * (1 << 20) * 4                # fp32 rows: raw results

@@ -51,8 +51,11 @@ def check_projection(gpu, x_bits, x_dt, basis, mean, normalize, out_dt, x_stride
 
 PROJ_CASES = [
     # n, d_in, d_out, x dtype, out dtype, mean, normalize
-    (4096, 4096, 64, "bf16", "bf16", True, True),     # matrix-core route
+    (4096, 4096, 64, "bf16", "bf16", True, True),     # matrix-core route, fused epilogue
     (3000, 1024, 64, "f16", "f16", True, True),
+    (2001, 2048, 30, "bf16", "bf16", True, True),     # fused, one output per store
+    (1500, 1000, 64, "f16", "f32", False, True),      # fused, fp32 16-byte stores, ragged d
+    (999, 1024, 4, "bf16", "bf16", True, False),      # fused, one 4-output store per row
     (700, 4096, 100, "bf16", "f32", False, False),    # two query groups on the matrix cores
     (2500, 512, 256, "bf16", "f32", True, True),
     (7, 4096, 64, "bf16", "f32", True, True),         # direct route (few rows)
@@ -89,6 +92,23 @@ def test_project_strided_rows_and_output_stride():
     check_projection(out[:, :48], host_bits(store), "f16", basis, mean, True, "f32",
                      x_stride=1012, d_in=1000)
     assert (out[:, 48:] == 5.0).all()
+
+
+@pytest.mark.parametrize("cols", [42, 44])
+def test_project_matrix_core_output_stride(cols):
+    """The matrix-core route (16-byte aligned rows, row stride a multiple of
+    8) into a wider output: 40 outputs per row at a stride of 42 (one
+    output per store) or 44 (four per store); the columns past 40 keep
+    their values."""
+    w = synth.scaled(synth.WORKLOADS["tiny-16k-d4096"], n=2000, d=1024, key_dtype="bf16",
+                     n_clusters=8)
+    ds = synth.make_datastore(w, 7, DEV)
+    mean, basis = synth.make_pca_basis(ds, 7, 40)
+    out = torch.full((2000, cols), 5.0, dtype=torch.bfloat16, device=DEV)
+    sense.sense_project(ds.keys, basis, mean, True, out=out[:, :40])
+    torch.cuda.synchronize()
+    check_projection(out[:, :40], host_bits(ds.keys), "bf16", basis, mean, True, "bf16")
+    assert (out[:, 40:] == 5.0).all()
 
 
 def test_project_routes_agree():
