@@ -48,6 +48,20 @@ def test_library_is_gfx950_only():
         assert other not in data
 
 
+def test_c_driver_refuses_bad_invocations_before_any_device_call():
+    """The plain C caller (built with the library) prints its usage without an
+    argument and rejects a directory without params.txt, both before its
+    first HIP call, so this runs without a GPU."""
+    import subprocess
+    drv = os.path.join(ROOT, "tests", "c_abi", "sense_c_driver")
+    assert os.access(drv, os.X_OK), "build the C driver first (__graft_entry__.build())"
+    r = subprocess.run([drv], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 2 and "usage" in r.stderr
+    r = subprocess.run([drv, os.path.join(ROOT, "tests", "c_abi", "no-such-dir")],
+                       capture_output=True, text=True, timeout=60)
+    assert r.returncode == 1 and "params.txt" in r.stderr
+
+
 def test_status_strings(lib):
     for code in range(7):
         assert lib.sense_status_string(code)
