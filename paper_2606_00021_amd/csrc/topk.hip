@@ -397,9 +397,9 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
         }
     }
     // The group-maxima bound pays where a chunk holds raw scores of both
-    // signs (its keys share no leading bits); later levels hold survivors
-    // that already share them.
-    constexpr bool kBound = FROM_SCORES && !FINAL;
+    // signs (its keys share no leading bits), first levels and single-chunk
+    // finals alike; later levels hold survivors that already share them.
+    constexpr bool kBound = FROM_SCORES;
     const ChunkStats cs =
         chunk_stats<kThreads, P, kBound>(key, kk, StatsLds{s_nzw, s_andw, s_orw, s_loww, s_highw});
 
@@ -562,8 +562,15 @@ hipError_t launch_topk_gather(const float* scores, int64_t n, int nq, int k,
                               int32_t* out_draft_len, void* workspace, hipStream_t stream) {
     const int64_t kk = k < kSelectChunk ? k : kSelectChunk;
     int64_t chunks = ceil_div(n, kSelectChunk);
-    if (chunks <= 1) {
-        // One chunk; up to kThreads * 8 scores take eight per thread.
+    if (chunks <= 2) {
+        // One block: up to kThreads * 8 scores take eight per thread, up to
+        // two chunks' worth 32 (one launch instead of a level and a final).
+        if (n > kSelectChunk) {
+            hipLaunchKernelGGL((select_kernel<true, true, 2 * kPer>), dim3(1, nq), dim3(kThreads),
+                               0, stream, scores, nullptr, n, k, nullptr, out_ids, out_scores,
+                               out_drafts, out_draft_len, spans, span_len, max_span, span_stride);
+            return hipGetLastError();
+        }
         if (n <= (int64_t)kThreads * 8)
             hipLaunchKernelGGL((select_kernel<true, true, 8>), dim3(1, nq), dim3(kThreads), 0,
                                stream, scores, nullptr, n, k, nullptr, out_ids, out_scores,

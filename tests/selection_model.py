@@ -403,17 +403,18 @@ def select_block(keys_in: list, k: int, threads: int, per: int, bound: bool, fin
 
 def select_launch(scores: np.ndarray, k: int, rng: np.random.Generator, per: int = 16,
                   threads: int = 512):
-    """All levels of launch_topk_gather for one query's scores: the first
-    level from scores (with the group-maxima bound), survivor levels, the
-    final level.  Returns the ordered top-k rows (-1 for padding)."""
+    """All levels of launch_topk_gather for one query's scores: up to two
+    chunks one final block (with the group-maxima bound); more, the first
+    level from scores (with the bound), survivor levels, the final level.
+    Returns the ordered top-k rows (-1 for padding)."""
     n = len(scores)
     CH = threads * per
     keys = pack_keys(scores, np.arange(n))
     kk = min(k, 8192)
     chunks = -(-n // 8192)
-    if chunks <= 1:
-        p = 8 if n <= threads * 8 else per
-        out, _ = select_block(keys, k, threads, p, bound=False, final=True, rng=rng)
+    if chunks <= 2:
+        p = 8 if n <= threads * 8 else (per if chunks == 1 else 2 * per)
+        out, _ = select_block(keys, k, threads, p, bound=True, final=True, rng=rng)
         return [(-1 if x == 0 else key_row(x)) for x in out]
     level = []
     for c in range(chunks):

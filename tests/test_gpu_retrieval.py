@@ -171,7 +171,9 @@ def _exact_score_columns(n, rng):
     (5 * 8192 - 3, 600, 8, 128),      # k above the threads of a block: no group bound
     (5 * 8192 - 3, 1024, 1, 128),     # two levels of 1024-key survivors
     (8192, 64, 8, 128),               # one chunk
-    (16384, 64, 8, 128),              # two full chunks
+    (16384, 64, 8, 128),              # two full chunks: one block, 32 keys per thread
+    (12000, 100, 1, 128),             # the same for the single-query scan
+    (16384, 1024, 2, 128),            # ... with k above the threads of a block
     (16385, 1024, 2, 128),            # a last chunk of one score
     # short keys: one query (short-row scan), a batch over a direct store
     # (n <= 131072), and batches whose threshold comes from a strided sample's

@@ -41,7 +41,7 @@ def make_scores(rng, n, kind):
 
 
 CASES = [
-    # n, k, kind: one chunk (8 and 16 keys per thread), the first level with
+    # n, k, kind: one block (8, 16 and 32 keys per thread), the first level with
     # the bound (groups of 64 .. 1 lanes, and none for k > 512), survivor
     # levels, rank (k <= 256) and bitonic (k > 256) finals
     (40, 40, "normal"),
@@ -49,6 +49,8 @@ CASES = [
     (4097, 100, "specials"),
     (8192, 1, "one-value"),
     (8193, 64, "normal"),
+    (12000, 64, "specials"),
+    (16384, 1024, "ties"),
     (3 * 8192 + 777, 8, "ties"),
     (3 * 8192 + 777, 300, "specials"),
     (3 * 8192 + 777, 1024, "mostly-nan"),
