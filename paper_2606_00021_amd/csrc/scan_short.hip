@@ -248,6 +248,198 @@ __global__ __launch_bounds__(kShortThreads, 2) void scan_short_kernel(ShortScan 
     }
 }
 
+// The filtered pass over 64-dim keys with the keys staged in LDS.  Loading
+// the matrix-core operand layout straight from HBM (above) reads 64 bytes of
+// each of 16 rows per load instruction, a pattern this device serves well
+// below its streaming rate, and holds every tile in flight in registers (four
+// per wave at most).  Here global_load_lds_dwordx4 moves whole 128-byte rows
+// (8 rows per instruction) into a private ring of kRing tile slots per wave,
+// kRing - 1 tiles ahead of the products, and each lane reads its operand
+// from LDS: lane L = 8p + w of an instruction writes entry w of row p and
+// fetches unit (w + p) mod 8 of that row (unit u of row p sits at entry
+// (u - p) mod 8, rows 8-15 at entries 64 + ...), so the 8 rows a matrix-core
+// read touches in each half fall on 8 distinct 16-byte groups.  A tile's 16
+// key norms come the same way (global_load_lds_dword; inner product loads a
+// valid dummy word and uses a scale of 1).  Every iteration issues the same
+// three loads (tiles past the end reload the last one), so the wait for a
+// tile is a fixed count; the loop holds no load into registers, whose waits
+// the compiler would take for every load in flight.  The products and the
+// filter are those of scan_short_kernel in the same order: the same bits.
+// The pass is bound by its per-score instructions, not by HBM; the register
+// room the ring frees lets the epilogue take the key scale and the
+// row-valid mask once per tile instead of once per score.
+constexpr int kRing = 8;           // tile slots per wave
+constexpr int kDmaOps = 3;         // loads per tile: two key halves, the norms
+
+// Waits until at most N vector-memory operations of this wave are
+// outstanding (loads complete in issue order); a compiler barrier too.
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+// Global -> LDS without registers: lane l's 16 (or 4) bytes land at
+// lds + 16*l (4*l); lds is wave-uniform.  Inline assembly keeps these loads
+// out of the compiler's wait-count model (the waits above are explicit); m0
+// is reserved, set here right before its use.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void lds_load16_nt(const void* g, void* lds) {
+    const uint32_t base = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off nt" ::"v"(g), "s"(base)
+                 : "memory", "m0");
+}
+__device__ __forceinline__ void lds_load4(const void* g, void* lds) {
+    const uint32_t base = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" ::"v"(g), "s"(base)
+                 : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+template <int KT, int NT, bool SPLIT>
+__global__ __launch_bounds__(kShortThreads, 2) void scan_short_lds_kernel(ShortScan s,
+                                                                      int64_t rows_per_wave) {
+    __shared__ float2 s_qt[64];
+    __shared__ __attribute__((aligned(16))) u32x4 s_key[kShortThreads / 64][kRing][128];
+    __shared__ __attribute__((aligned(16))) float s_norm[kShortThreads / 64][kRing][64];
+    if (threadIdx.x < 64) {
+        const int q = threadIdx.x;
+        const float th = q < s.nq ? key_score((uint32_t)(s.tau[q] >> 32)) : __builtin_inff();
+        s_qt[q] = float2{q < 16 * NT ? s.inv_qn[q] : 0.0f, th};
+    }
+    __syncthreads();
+    const int lane = threadIdx.x & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t wave = (int64_t)blockIdx.x * (kShortThreads / 64) + wv;
+    const int64_t r0 = wave * rows_per_wave;
+    if (r0 >= s.n_rows) return;                      // uniform over the wave
+    const int64_t r1 = (r0 + rows_per_wave < s.n_rows) ? r0 + rows_per_wave : s.n_rows;
+    const int64_t ntiles = (r1 - r0 + 15) / 16;
+    const int col = lane & 15, grp = lane >> 4;
+
+    // Query fragments (d = 64: two k-steps), taken into registers before the
+    // first LDS load is issued.
+    u32x4 ahi[NT][2], alo[NT][2];
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            const int64_t qoff = (int64_t)(16 * t + col) * 64 + 8 * grp + 32 * ks;
+            ahi[t][ks] = *(const u32x4*)(s.qhi + qoff);
+            if constexpr (SPLIT) alo[t][ks] = *(const u32x4*)(s.qlo + qoff);
+        }
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            asm volatile("" : "+v"(ahi[t][ks]));
+            if constexpr (SPLIT) asm volatile("" : "+v"(alo[t][ks]));
+        }
+    int cnt[NT][4];       // survivors so far per query (same in a 16-lane group)
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) cnt[t][i] = 0;
+
+    const uint16_t* keys = (const uint16_t*)s.keys;
+    const int64_t rstride = s.row_step * s.ld;
+    const bool cos = s.inv_norm != nullptr;
+    const int dp = lane >> 3;                        // row within a load instruction
+    const int du = ((lane & 7) + dp) & 7;            // 16-byte unit it fetches
+    auto issue = [&](int64_t tile) {
+        const int64_t tc = tile < ntiles ? tile : ntiles - 1;
+        const int slot = (int)(tile % kRing);
+        const int64_t base = r0 + tc * 16;
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            int64_t row = base + 8 * i + dp;
+            if (row >= r1) row = r1 - 1;
+            lds_load16_nt(keys + row * rstride + du * 8, &s_key[wv][slot][64 * i]);
+        }
+        int64_t nrow = base + col;
+        if (nrow >= r1) nrow = r1 - 1;
+        lds_load4(cos ? (const void*)(s.inv_norm + nrow * s.row_step) : (const void*)s.inv_qn,
+                  &s_norm[wv][slot][0]);
+    };
+    // Operand entry of this lane in a tile for k-step ks: row col, unit
+    // grp + 4 ks.
+    auto entry = [&](int ks) {
+        const int p = col & 7;
+        return 64 * (col >> 3) + 8 * p + (((grp + 4 * ks) - p) & 7);
+    };
+    const int e0 = entry(0), e1 = entry(1);
+
+#pragma unroll
+    for (int t = 0; t < kRing - 1; ++t) issue(t);
+    for (int64_t t = 0; t < ntiles; ++t) {
+        wait_vm<(kRing - 2) * kDmaOps>();           // tile t is in LDS
+        issue(t + kRing - 1);                       // the slot read at t - 1
+        const int slot = (int)(t % kRing);
+        const u32x4 b0 = s_key[wv][slot][e0], b1 = s_key[wv][slot][e1];
+        const float kn = s_norm[wv][slot][col];
+        f32x4 acc[NT];
+#pragma unroll
+        for (int q = 0; q < NT; ++q) {
+            acc[q] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+            acc[q] = mfma<KT>(ahi[q][0], b0, acc[q]);
+            if constexpr (SPLIT) acc[q] = mfma<KT>(alo[q][0], b0, acc[q]);
+            acc[q] = mfma<KT>(ahi[q][1], b1, acc[q]);
+            if constexpr (SPLIT) acc[q] = mfma<KT>(alo[q][1], b1, acc[q]);
+        }
+        const int64_t r = r0 + t * 16 + col;
+        // Inner product scales by 1 (x * 1 is x: the same bits as no scale).
+        const float ks = cos ? kn : 1.0f;
+        const uint64_t okm = __ballot(r < r1);
+        float v[NT][4];
+#pragma unroll
+        for (int q = 0; q < NT; ++q)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) v[q][i] = (acc[q][i] * ks) * s_qt[16 * q + 4 * grp + i].x;
+        uint64_t bal[NT][4];
+#pragma unroll
+        for (int q = 0; q < NT; ++q)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                bal[q][i] = __ballot(!(v[q][i] < s_qt[16 * q + 4 * grp + i].y)) & okm;
+        const int64_t orig = r * s.row_step;
+#pragma unroll
+        for (int q = 0; q < NT; ++q) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                if (bal[q][i] == 0) continue;
+                const int qi = 16 * q + 4 * grp + i;
+                const bool pass = (bal[q][i] >> lane) & 1;
+                const uint32_t gm = (uint32_t)(bal[q][i] >> (16 * grp)) & 0xFFFFu;
+                const int slot_i = cnt[q][i] + __popc(gm & ((1u << col) - 1u));
+                if (pass && qi < s.nq) {
+                    const uint64_t key = pack_key(v[q][i], (uint32_t)orig);
+                    uint64_t* cq = s.cand + (int64_t)qi * s.cap;
+                    if (slot_i < kShortSlots) {
+                        cq[wave * kShortSlots + slot_i] = key;
+                    } else {
+                        const int pos = atomicAdd(&s.counts[qi], 1);
+                        cq[pos] = key;
+                        __asm__ volatile("" ::: "memory");
+                    }
+                }
+                cnt[q][i] += __popc(gm);
+            }
+        }
+    }
+    wait_vm<0>();
+    // Unused slots become padding keys (lane col 0 of each group saw every
+    // tile its group saw).
+#pragma unroll
+    for (int q = 0; q < NT; ++q)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int c0 = __shfl(cnt[q][i], lane & ~15, 64);
+            const int qi = 16 * q + 4 * grp + i;
+            if (qi < s.nq && col >= c0 && col < kShortSlots)
+                s.cand[(int64_t)qi * s.cap + wave * kShortSlots + col] = 0;
+        }
+}
+
 __global__ void short_tau_kernel(const int64_t* __restrict__ ids, const float* __restrict__ scores,
                                  int nq, int k, int64_t row_step, int32_t slot_area,
                                  const float* __restrict__ margin, uint64_t* __restrict__ tau,
@@ -276,6 +468,21 @@ hipError_t launch_variant(const ShortScan& s, hipStream_t stream) {
 template <int KT, int NT, int KS>
 hipError_t launch_mode(const ShortScan& s, hipStream_t stream) {
     const bool filter = s.cand != nullptr;
+    if constexpr (KS == 2) {
+        // 64-dim keys, filtered: the LDS-staged pass (16-byte aligned rows).
+        if (filter && s.d == 64 && ((uintptr_t)s.keys % 16) == 0 && (s.row_step * s.ld) % 8 == 0) {
+            const int64_t rpw = short_rows_per_wave(s.n_rows);
+            const int64_t waves = (s.n_rows + rpw - 1) / rpw;
+            const int64_t blocks = (waves + (kShortThreads / 64) - 1) / (kShortThreads / 64);
+            if (s.split)
+                hipLaunchKernelGGL((scan_short_lds_kernel<KT, NT, true>), dim3((unsigned)blocks),
+                                   dim3(kShortThreads), 0, stream, s, rpw);
+            else
+                hipLaunchKernelGGL((scan_short_lds_kernel<KT, NT, false>), dim3((unsigned)blocks),
+                                   dim3(kShortThreads), 0, stream, s, rpw);
+            return hipGetLastError();
+        }
+    }
     if (s.split)
         return filter ? launch_variant<KT, NT, KS, true, true>(s, stream)
                       : launch_variant<KT, NT, KS, true, false>(s, stream);

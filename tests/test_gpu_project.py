@@ -138,6 +138,8 @@ SMALL_SCAN = [
     (200003, 32, "f16", 5, 100, "ip"),
     (150001, 64, "bf16", 70, 16, "cosine"),     # two query groups
     (140000, 48, "bf16", 4, 1024, "cosine"),    # largest k
+    (180001, 64, "f16", 8, 32, "ip"),           # filtered pass over 64-dim keys, inner product
+    (262147, 64, "bf16", 40, 100, "cosine"),    # ... three query tiles, a ragged last wave
 ]
 
 
