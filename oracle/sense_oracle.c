@@ -2,7 +2,7 @@
  * sense_oracle.c -- plain, slow, obviously-correct CPU reference for the
  * SENSE retrieval + soft-gated evaluation hot path.
  *
- * TEST INFRASTRUCTURE ONLY.  This file is the checker, not the product: only
+ * TEST INFRASTRUCTURE ONLY.  This file is the oracle, not the product: only
  * the test-suite, the smoke check and the benchmark's CPU-baseline leg may
  * load it.  It shares no source, header, table or helper with the HIP library
  * and includes nothing from it.

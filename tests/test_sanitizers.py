@@ -2,7 +2,7 @@
 
 * The oracle (plain C) built with AddressSanitizer + UndefinedBehaviorSanitizer
   runs its pin tests: no out-of-bounds access, use after free or undefined
-  arithmetic anywhere in the checker.
+  arithmetic anywhere in the oracle.
 * The HIP library's host code (argument validation, layouts, launch set-up)
   built with the same sanitizers through hipcc (-Xarch_host: device code is
   never instrumented) runs the ABI tests, which exercise every validation
