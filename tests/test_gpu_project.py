@@ -160,6 +160,32 @@ def test_short_key_scan_matches_oracle(case):
     index.close()
 
 
+def test_batched_short_keys_strided_store_equals_dense_copy():
+    """64-dim keys at a row stride of 72 elements (144-byte rows, still
+    16-byte aligned) take the same LDS-staged filtered pass as a dense
+    store: the same ids and the same score bits as a dense copy of the
+    keys, and the oracle's top k."""
+    n, d, nq, k = 150_001, 64, 16, 64
+    w = synth.scaled(synth.WORKLOADS["tiny-16k-d4096"], n=n, d=d, key_dtype="bf16",
+                     n_clusters=64, n_outliers=2, metric="cosine")
+    ds = synth.make_datastore(w, 17, DEV, key_stride=72)
+    assert ds.keys.stride(0) == 72
+    q, _ = synth.make_queries(w, ds, 17, n_queries=nq)
+    dense = ds.keys.contiguous()
+    a = sense.sense_build_index(ds.keys, ds.spans, metric="cosine")
+    b = sense.sense_build_index(dense, ds.spans, metric="cosine")
+    ids_a, sc_a, _, _ = sense.sense_retrieve(a, q, k)
+    ids_b, sc_b, _, _ = sense.sense_retrieve(b, q, k)
+    torch.cuda.synchronize()
+    assert torch.equal(ids_a, ids_b)
+    assert torch.equal(sc_a.view(torch.int32), sc_b.view(torch.int32))
+    o_s = oracle.scores(host_bits(dense), "bf16", q.cpu().numpy(), "f32", "cosine")
+    for qq in range(nq):
+        check_topk(ids_a[qq].cpu().numpy(), sc_a[qq].cpu().numpy(), o_s[qq], k)
+    a.close()
+    b.close()
+
+
 def test_pca_retrieval_chain():
     """Project a 4096-dim store to 64 dims (bf16, normalised) and the query
     (fp32), search the projected store: against the oracle's own projection
