@@ -343,7 +343,7 @@ __global__ __launch_bounds__(kShortThreads, 2) void scan_short_lds_kernel(ShortS
 
     const uint16_t* keys = (const uint16_t*)s.keys;
     const int64_t rstride = s.row_step * s.ld;
-    const bool cos = s.inv_norm != nullptr;
+    const bool cosine = s.inv_norm != nullptr;
     const int dp = lane >> 3;                        // row within a load instruction
     const int du = ((lane & 7) + dp) & 7;            // 16-byte unit it fetches
     auto issue = [&](int64_t tile) {
@@ -358,7 +358,7 @@ __global__ __launch_bounds__(kShortThreads, 2) void scan_short_lds_kernel(ShortS
         }
         int64_t nrow = base + col;
         if (nrow >= r1) nrow = r1 - 1;
-        lds_load4(cos ? (const void*)(s.inv_norm + nrow * s.row_step) : (const void*)s.inv_qn,
+        lds_load4(cosine ? (const void*)(s.inv_norm + nrow * s.row_step) : (const void*)s.inv_qn,
                   &s_norm[wv][slot][0]);
     };
     // Operand entry of this lane in a tile for k-step ks: row col, unit
@@ -388,7 +388,7 @@ __global__ __launch_bounds__(kShortThreads, 2) void scan_short_lds_kernel(ShortS
         }
         const int64_t r = r0 + t * 16 + col;
         // Inner product scales by 1 (x * 1 is x: the same bits as no scale).
-        const float ks = cos ? kn : 1.0f;
+        const float ks = cosine ? kn : 1.0f;
         const uint64_t okm = __ballot(r < r1);
         float v[NT][4];
 #pragma unroll
