@@ -68,6 +68,10 @@ SMALL = [
     ("k1024-n4096", 4096, 128, "f16", 1024),
     # a final level of 5 x 1024 keys (more than 4096: sixteen per thread)
     ("k1024-5chunks", 5 * 8192 - 3, 128, "bf16", 1024),
+    # up to two chunks' worth of scores: one block, 32 per thread (rank and
+    # bitonic finals)
+    ("one-block-9000", 9000, 256, "f16", 100),
+    ("one-block-12001-k1024", 12001, 128, "bf16", 1024),
     # two full selection chunks; then a last chunk of a single score
     ("two-chunks-16384", 16384, 256, "bf16", 64),
     ("last-chunk-of-one-16385", 16385, 256, "f16", 64),
