@@ -9,12 +9,13 @@
  *
  * Directory layout (little-endian raw arrays):
  *   params.txt     n d max_span n_queries k metric key_dtype vocab
- *                  gamma topk window tau
+ *                  gamma topk window tau logits_dtype
  *   keys.bin       n x d uint16 (fp16 or bf16 bits, per key_dtype)
  *   spans.bin      n x max_span int32
  *   span_len.bin   n int32
  *   queries.bin    n_queries x d float32
- *   logits.bin     (n_queries * k) x max_span x vocab float32
+ *   logits.bin     (n_queries * k) x max_span x vocab, float32 or the
+ *                  16-bit bits of logits_dtype
  * Outputs:
  *   ids.bin (int64), scores.bin (float32), drafts.bin, draft_len.bin,
  *   accept_len.bin, best.bin, rank.bin (int32), gate_score.bin (float32).
@@ -117,24 +118,26 @@ int main(int argc, char **argv) {
     }
     const char *dir = argv[1];
     long long n, nq, k;
-    int d, m, metric, key_dtype, vocab, topk, window, tau;
+    int d, m, metric, key_dtype, vocab, topk, window, tau, logits_dtype;
     float gamma;
     FILE *pf = fopen(path(dir, "params.txt"), "r");
     if (!pf) {
         fprintf(stderr, "cannot open %s\n", path_buf);
         return 1;
     }
-    const int fields = fscanf(pf, "%lld %d %d %lld %lld %d %d %d %f %d %d %d", &n, &d, &m, &nq,
-                              &k, &metric, &key_dtype, &vocab, &gamma, &topk, &window, &tau);
+    const int fields = fscanf(pf, "%lld %d %d %lld %lld %d %d %d %f %d %d %d %d", &n, &d, &m,
+                              &nq, &k, &metric, &key_dtype, &vocab, &gamma, &topk, &window, &tau,
+                              &logits_dtype);
     fclose(pf);
-    if (fields != 12 || n < 1 || d < 1 || m < 1 || nq < 1 || k < 1 || vocab < 1) {
-        fprintf(stderr, "params.txt: expected 12 fields with positive sizes\n");
+    if (fields != 13 || n < 1 || d < 1 || m < 1 || nq < 1 || k < 1 || vocab < 1 ||
+        logits_dtype < SENSE_F32 || logits_dtype > SENSE_BF16) {
+        fprintf(stderr, "params.txt: expected 13 fields with positive sizes\n");
         return 1;
     }
     const long long n_cand = nq * k;
     const size_t key_bytes = (size_t)n * d * 2, span_bytes = (size_t)n * m * 4;
     const size_t q_bytes = (size_t)nq * d * 4;
-    const size_t logit_bytes = (size_t)n_cand * m * vocab * 4;
+    const size_t logit_bytes = (size_t)n_cand * m * vocab * (logits_dtype == SENSE_F32 ? 4 : 2);
     void *h_keys = read_all(dir, "keys.bin", key_bytes);
     void *h_spans = read_all(dir, "spans.bin", span_bytes);
     void *h_span_len = read_all(dir, "span_len.bin", (size_t)n * 4);
@@ -200,7 +203,8 @@ int main(int argc, char **argv) {
     HIP_OK(hipMalloc(&gate_score, (size_t)n_cand * m * 4));
     HIP_OK(hipMalloc(&rank, (size_t)n_cand * m * 4));
     HIP_OK(hipMalloc(&workspace_v, ws_v ? ws_v : 1));
-    SENSE_OK_(sense_soft_gate_verify(logits, SENSE_F32, vocab, (const int32_t *)drafts,
+    SENSE_OK_(sense_soft_gate_verify(logits, (sense_dtype_t)logits_dtype, vocab,
+                                     (const int32_t *)drafts,
                                      (const int32_t *)draft_len, (int32_t)n_cand, m, vocab,
                                      (int32_t)nq, &gp, (int32_t *)accept_len, (int32_t *)best,
                                      (float *)gate_score, NULL, (int32_t *)rank, workspace_v,

@@ -26,17 +26,18 @@ DTYPE = {"f16": 1, "bf16": 2}
 GATE = dict(gamma=0.05, topk=3, window=6, tau=0)
 
 CASES = [
-    # n, d, key dtype, n_queries, k, metric
-    (20000, 512, "bf16", 1, 16, "cosine"),      # one query: the vector-ALU scan
-    (30011, 256, "f16", 3, 32, "ip"),           # a batch: the matrix-core scan
+    # n, d, key dtype, n_queries, k, metric, logits dtype
+    (20000, 512, "bf16", 1, 16, "cosine", "f32"),     # one query: the vector-ALU scan
+    (30011, 256, "f16", 3, 32, "ip", "bf16"),         # a batch: the matrix-core scan
 ]
+LOGITS = {"f32": (0,), "f16": (1,), "bf16": (2,)}
 
 
 @pytest.mark.parametrize("case", CASES, ids=[str(i) for i in range(len(CASES))])
 def test_c_driver_matches_oracle(case, tmp_path):
     if not os.access(DRIVER, os.X_OK):
         pytest.fail(f"{DRIVER} is not built: run __graft_entry__.build()")
-    n, d, kdt, nq, k, metric = case
+    n, d, kdt, nq, k, metric, ldt = case
     print(f"[c-abi] case={case}", flush=True)
     w = synth.scaled(synth.WORKLOADS["tiny-16k-d4096"], n=n, d=d, key_dtype=kdt, n_queries=nq,
                      k=k, vocab=3000, n_clusters=64)
@@ -51,16 +52,18 @@ def test_c_driver_matches_oracle(case, tmp_path):
     # Logits row-aligned with the oracle's drafts (the draft token boosted at
     # some positions, so that accepted prefixes vary).
     o_ids, _, o_dr, _ = oracle.retrieve(keys, kdt, queries, "f32", k, spans, span_len, metric)
-    logits = synth.make_logits(w, torch.from_numpy(o_dr.reshape(nq * k, m)), 61).numpy()
+    logits_t = synth.make_logits(w, torch.from_numpy(o_dr.reshape(nq * k, m)), 61, dtype=ldt)
+    logits = host_bits(logits_t)          # float32 values, or 16-bit bit patterns
 
     with open(tmp_path / "params.txt", "w") as f:
         f.write(f"{n} {d} {m} {nq} {k} {METRIC[metric]} {DTYPE[kdt]} {vocab} "
-                f"{GATE['gamma']} {GATE['topk']} {GATE['window']} {GATE['tau']}\n")
+                f"{GATE['gamma']} {GATE['topk']} {GATE['window']} {GATE['tau']} "
+                f"{LOGITS[ldt][0]}\n")
     keys.tofile(tmp_path / "keys.bin")
     spans.astype(np.int32).tofile(tmp_path / "spans.bin")
     span_len.astype(np.int32).tofile(tmp_path / "span_len.bin")
     queries.tofile(tmp_path / "queries.bin")
-    logits.astype(np.float32).tofile(tmp_path / "logits.bin")
+    logits.tofile(tmp_path / "logits.bin")
 
     run = subprocess.run([DRIVER, str(tmp_path)], capture_output=True, text=True, timeout=120)
     assert run.returncode == 0, f"driver exit {run.returncode}: {run.stderr[-2000:]}"
@@ -83,7 +86,7 @@ def test_c_driver_matches_oracle(case, tmp_path):
         assert np.array_equal(dlen[i], g_dl), f"query {i}: draft lengths differ"
 
     flat_dr, flat_dl = drafts.reshape(nq * k, m), dlen.reshape(nq * k)
-    ref = oracle.soft_gate_verify(logits, "f32", flat_dr, flat_dl, n_groups=nq, **GATE)
+    ref = oracle.soft_gate_verify(logits, ldt, flat_dr, flat_dl, n_groups=nq, **GATE)
     gpu = {"accept_len": torch.from_numpy(out("accept_len.bin", np.int32, (nq * k,))),
            "best": torch.from_numpy(out("best.bin", np.int32, (nq,))),
            "gate_score": torch.from_numpy(out("gate_score.bin", np.float32, (nq * k, m))),
