@@ -23,6 +23,7 @@
 // Every true top-k row passes, so the result is exact; the scores of both
 // passes come from the same instructions, hence the same bits.
 #include "internal.h"
+#include "lds_dma.h"
 
 namespace sense {
 
@@ -271,31 +272,6 @@ __global__ __launch_bounds__(kShortThreads, 2) void scan_short_kernel(ShortScan 
 constexpr int kRing = 8;           // tile slots per wave
 constexpr int kDmaOps = 3;         // loads per tile: two key halves, the norms
 
-// Waits until at most N vector-memory operations of this wave are
-// outstanding (loads complete in issue order); a compiler barrier too.
-template <int N>
-__device__ __forceinline__ void wait_vm() {
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
-// Global -> LDS without registers: lane l's 16 (or 4) bytes land at
-// lds + 16*l (4*l); lds is wave-uniform.  Inline assembly keeps these loads
-// out of the compiler's wait-count model (the waits above are explicit); m0
-// is reserved, set here right before its use.
-#pragma clang diagnostic push
-#pragma clang diagnostic ignored "-Winline-asm"
-__device__ __forceinline__ void lds_load16_nt(const void* g, void* lds) {
-    const uint32_t base = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
-    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off nt" ::"v"(g), "s"(base)
-                 : "memory", "m0");
-}
-__device__ __forceinline__ void lds_load4(const void* g, void* lds) {
-    const uint32_t base = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
-    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" ::"v"(g), "s"(base)
-                 : "memory", "m0");
-}
-#pragma clang diagnostic pop
-
 template <int KT, int NT, bool SPLIT>
 __global__ __launch_bounds__(kShortThreads, 2) void scan_short_lds_kernel(ShortScan s,
                                                                       int64_t rows_per_wave) {
@@ -354,11 +330,11 @@ __global__ __launch_bounds__(kShortThreads, 2) void scan_short_lds_kernel(ShortS
         for (int i = 0; i < 2; ++i) {
             int64_t row = base + 8 * i + dp;
             if (row >= r1) row = r1 - 1;
-            lds_load16_nt(keys + row * rstride + du * 8, &s_key[wv][slot][64 * i]);
+            dma16_nt(keys + row * rstride + du * 8, &s_key[wv][slot][64 * i]);
         }
         int64_t nrow = base + col;
         if (nrow >= r1) nrow = r1 - 1;
-        lds_load4(cosine ? (const void*)(s.inv_norm + nrow * s.row_step) : (const void*)s.inv_qn,
+        dma4(cosine ? (const void*)(s.inv_norm + nrow * s.row_step) : (const void*)s.inv_qn,
                   &s_norm[wv][slot][0]);
     };
     // Operand entry of this lane in a tile for k-step ks: row col, unit
@@ -372,7 +348,7 @@ __global__ __launch_bounds__(kShortThreads, 2) void scan_short_lds_kernel(ShortS
 #pragma unroll
     for (int t = 0; t < kRing - 1; ++t) issue(t);
     for (int64_t t = 0; t < ntiles; ++t) {
-        wait_vm<(kRing - 2) * kDmaOps>();           // tile t is in LDS
+        wait_vmcnt<(kRing - 2) * kDmaOps>();           // tile t is in LDS
         issue(t + kRing - 1);                       // the slot read at t - 1
         const int slot = (int)(t % kRing);
         const u32x4 b0 = s_key[wv][slot][e0], b1 = s_key[wv][slot][e1];
@@ -426,7 +402,7 @@ __global__ __launch_bounds__(kShortThreads, 2) void scan_short_lds_kernel(ShortS
             }
         }
     }
-    wait_vm<0>();
+    wait_vmcnt<0>();
     // Unused slots become padding keys (lane col 0 of each group saw every
     // tile its group saw).
 #pragma unroll
