@@ -86,8 +86,10 @@ WORKLOADS = {
         Workload("store-1m-pca64-ivfflat", 1_048_576, 4096, "bf16", 1, 64, 8, 152_064, "bf16",
                  4096, 8, 1, proj=64, ivf_nlist=4096, ivf_nprobe=32),
         # 64-dim keys straight from the cluster generator (no projection): the
-        # batched short-key path without a PCA fit in the set-up.
+        # short-key paths without a PCA fit in the set-up.
         Workload("store-1m-d64-q64", 1_048_576, 64, "bf16", 64, 64, 8, 152_064, "bf16",
+                 4096, 2, 1),
+        Workload("store-1m-d64", 1_048_576, 64, "bf16", 1, 64, 8, 152_064, "bf16",
                  4096, 2, 1),
     ]
 }
