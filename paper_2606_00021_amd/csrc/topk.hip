@@ -11,22 +11,25 @@
 // Selection is hierarchical.  A block of 512 threads takes a chunk of 8192
 // keys into registers (16 per thread; a single chunk of at most 4096 keys
 // takes 8 per thread, since every phase costs its per-thread key loop).
-// One reduction gives the number of real (non-padding) keys and the AND and
-// OR of them: the bits above the highest bit where they differ are shared by
+// The block is one compute unit, so every per-key instruction counts.  One
+// reduction gives the number of real (non-padding) keys and the AND and OR
+// of them: the bits above the highest bit where they differ are shared by
 // all, so the radix select starts right below them (survivors of a level
 // share their sign and most of their exponent, which a fixed top-down start
-// would spend a whole pass on).  A chunk of raw scores holds both signs, so
-// the first level also bounds the k-th largest key from below by the
-// smallest of k or more group maxima and starts below the bits that this
-// bound and the largest key share: every key of the top k lies between them.
-// Each pass builds a 256-bin LDS histogram of the next 8-bit digit among the
-// keys that still match the chosen prefix, then one wave finds the digit
-// holding the k-th key with a suffix scan; the loop stops as soon as that
-// digit's bucket is taken whole.  The taken keys are compacted by ballot
-// prefix sums (no atomics).  The k survivors of every chunk form the next
-// level's input until one chunk remains; its keys are put in order by rank
-// (each key counts the keys above it, all reads LDS broadcasts) and written
-// out together with the gathered continuations.
+// would spend a whole pass on).  For a chunk of raw scores the AND and OR
+// come from the score words alone, the row words being a contiguous range.
+// A chunk of raw scores holds both signs, so the first level also bounds the
+// k-th largest key from below by the smallest of k or more group maxima and
+// starts below the bits that this bound and the largest key share: every
+// key of the top k lies between them.  Each pass builds a 256-bin LDS
+// histogram of the next 8-bit digit among the keys that still match the
+// chosen prefix, then one wave finds the digit holding the k-th key with a
+// suffix scan; the loop stops as soon as that digit's bucket is taken
+// whole.  The taken keys are compacted by ballot prefix sums (no atomics).
+// The k survivors of every chunk form the next level's input until one
+// chunk remains; its keys are put in order by rank (each key counts the
+// keys above it, all reads LDS broadcasts) and written out together with
+// the gathered continuations.
 #include "internal.h"
 
 namespace sense {
@@ -71,55 +74,44 @@ __device__ __forceinline__ uint32_t dpp_u(uint32_t x) {
     return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xF, 0xF, false);
 }
 
-template <int T, int P, bool BOUND>
-__device__ ChunkStats chunk_stats(const uint64_t (&key)[P], int kk, const StatsLds& L) {
+// The group-maxima bound of the comment above from each lane's largest
+// score word mx: hi = the largest mx of the wave, lo = the smallest of its
+// group maxima (wave-uniform results).  Group size g: the largest power
+// of two <= 64 with T / g >= kk; none (lo = 0) when kk > T.  One max ladder
+// over groups of 2, 4, ..., 64 lanes (quad swaps, half-row and row mirrors,
+// then xor 16 and 32), keeping the group maxima at size g; then the min
+// ladder of those.
+template <int T>
+__device__ __forceinline__ void group_bound(uint32_t mx, int kk, uint32_t* lo_out,
+                                            uint32_t* hi_out) {
+    const int gq = T / (kk > 0 ? kk : 1);
+    const int g = gq >= 64 ? 64 : (gq > 0 ? 1 << (31 - __clz(gq)) : 0);
+    uint32_t v = mx, gm = (g == 1) ? mx : 0u;
+    auto mxs = [](uint32_t x, uint32_t y) { return x > y ? x : y; };
+    auto mns = [](uint32_t x, uint32_t y) { return x < y ? x : y; };
+    v = mxs(v, dpp_u<0xB1>(v));  gm = (g == 2) ? v : gm;
+    v = mxs(v, dpp_u<0x4E>(v));  gm = (g == 4) ? v : gm;
+    v = mxs(v, dpp_u<0x141>(v)); gm = (g == 8) ? v : gm;
+    v = mxs(v, dpp_u<0x140>(v)); gm = (g == 16) ? v : gm;
+    v = mxs(v, (uint32_t)__shfl_xor((int)v, 16, 64)); gm = (g == 32) ? v : gm;
+    v = mxs(v, (uint32_t)__shfl_xor((int)v, 32, 64)); gm = (g == 64) ? v : gm;
+    uint32_t lo = gm;
+    lo = mns(lo, dpp_u<0xB1>(lo));
+    lo = mns(lo, dpp_u<0x4E>(lo));
+    lo = mns(lo, dpp_u<0x141>(lo));
+    lo = mns(lo, dpp_u<0x140>(lo));
+    lo = mns(lo, (uint32_t)__shfl_xor((int)lo, 16, 64));
+    lo = mns(lo, (uint32_t)__shfl_xor((int)lo, 32, 64));
+    *lo_out = lo;
+    *hi_out = v;
+}
+
+// Block-wide combination of the per-wave statistics (wave-uniform inputs).
+template <int T, bool BOUND>
+__device__ __forceinline__ ChunkStats combine_waves(uint32_t nz, uint64_t a, uint64_t o,
+                                                    uint32_t lo, uint32_t hi,
+                                                    const StatsLds& L) {
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-    uint32_t nz = 0;
-    uint64_t a = ~0ull, o = 0ull;
-    uint32_t mx = 0u;
-#pragma unroll
-    for (int e = 0; e < P; ++e) {
-        nz += (uint32_t)__popcll(__ballot(key[e] != 0));
-        if (key[e] != 0) {
-            a &= key[e];
-            o |= key[e];
-        }
-        if constexpr (BOUND) {
-            const uint32_t h = (uint32_t)(key[e] >> 32);
-            mx = h > mx ? h : mx;
-        }
-    }
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        a &= __shfl_xor(a, off, 64);
-        o |= __shfl_xor(o, off, 64);
-    }
-    uint32_t lo = 0u, hi = 0u;
-    if constexpr (BOUND) {
-        // Group size g: the largest power of two <= 64 with T / g >= kk; none
-        // (low = 0) when kk > T.  One max ladder over groups of 2, 4, ..., 64
-        // lanes (quad swaps, half-row and row mirrors, then xor 16 and 32),
-        // keeping the group maxima at size g; then the min ladder of those.
-        const int gq = T / (kk > 0 ? kk : 1);
-        const int g = gq >= 64 ? 64 : (gq > 0 ? 1 << (31 - __clz(gq)) : 0);
-        uint32_t v = mx, gm = (g == 1) ? mx : 0u;
-        auto mxs = [](uint32_t x, uint32_t y) { return x > y ? x : y; };
-        auto mns = [](uint32_t x, uint32_t y) { return x < y ? x : y; };
-        v = mxs(v, dpp_u<0xB1>(v));  gm = (g == 2) ? v : gm;
-        v = mxs(v, dpp_u<0x4E>(v));  gm = (g == 4) ? v : gm;
-        v = mxs(v, dpp_u<0x141>(v)); gm = (g == 8) ? v : gm;
-        v = mxs(v, dpp_u<0x140>(v)); gm = (g == 16) ? v : gm;
-        v = mxs(v, (uint32_t)__shfl_xor((int)v, 16, 64)); gm = (g == 32) ? v : gm;
-        v = mxs(v, (uint32_t)__shfl_xor((int)v, 32, 64)); gm = (g == 64) ? v : gm;
-        hi = v;
-        lo = gm;
-        lo = mns(lo, dpp_u<0xB1>(lo));
-        lo = mns(lo, dpp_u<0x4E>(lo));
-        lo = mns(lo, dpp_u<0x141>(lo));
-        lo = mns(lo, dpp_u<0x140>(lo));
-        lo = mns(lo, (uint32_t)__shfl_xor((int)lo, 16, 64));
-        lo = mns(lo, (uint32_t)__shfl_xor((int)lo, 32, 64));
-    }
     if (lane == 0) {
         L.nzw[wv] = nz;
         L.andw[wv] = a;
@@ -142,6 +134,71 @@ __device__ ChunkStats chunk_stats(const uint64_t (&key)[P], int kk, const StatsL
         }
     }
     if constexpr (!BOUND) r.low32 = r.high32 = 0u;
+    return r;
+}
+
+template <int T, int P, bool BOUND>
+__device__ ChunkStats chunk_stats(const uint64_t (&key)[P], int kk, const StatsLds& L) {
+    uint32_t nz = 0;
+    uint64_t a = ~0ull, o = 0ull;
+    uint32_t mx = 0u;
+#pragma unroll
+    for (int e = 0; e < P; ++e) {
+        nz += (uint32_t)__popcll(__ballot(key[e] != 0));
+        if (key[e] != 0) {
+            a &= key[e];
+            o |= key[e];
+        }
+        if constexpr (BOUND) {
+            const uint32_t h = (uint32_t)(key[e] >> 32);
+            mx = h > mx ? h : mx;
+        }
+    }
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        a &= __shfl_xor(a, off, 64);
+        o |= __shfl_xor(o, off, 64);
+    }
+    uint32_t lo = 0u, hi = 0u;
+    if constexpr (BOUND) group_bound<T>(mx, kk, &lo, &hi);
+    return combine_waves<T, BOUND>(nz, a, o, lo, hi, L);
+}
+
+// chunk_stats with the bound for a chunk of raw scores, rows start ..
+// start + len - 1 (len >= 1), without a conditional per key.  sw[e] is the
+// score word of slot e's row, past the chunk a copy of the last row's (a
+// copy changes no AND or OR); the high word of key[e] is 0 past the chunk
+// (for the maxima, which must be distinct keys).  Every slot before len is
+// a real key.  The row words are the complements of a contiguous range of
+// indices: above the highest bit where the first and the last differ all
+// share their bits, and below it both values occur at every bit (the range
+// holds the two indices on either side of the carry into that bit), so
+// their AND and OR follow from the two ends.
+template <int T, int P>
+__device__ ChunkStats score_stats(const uint32_t (&sw)[P], const uint64_t (&key)[P], int kk,
+                                  int64_t start, int len, const StatsLds& L) {
+    uint32_t a = ~0u, o = 0u, mx = 0u;
+#pragma unroll
+    for (int e = 0; e < P; ++e) {
+        a &= sw[e];
+        o |= sw[e];
+        const uint32_t h = (uint32_t)(key[e] >> 32);
+        mx = h > mx ? h : mx;
+    }
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        a &= (uint32_t)__shfl_xor((int)a, off, 64);
+        o |= (uint32_t)__shfl_xor((int)o, off, 64);
+    }
+    uint32_t lo, hi;
+    group_bound<T>(mx, kk, &lo, &hi);
+    ChunkStats r = combine_waves<T, true>(0u, (uint64_t)a << 32, (uint64_t)o << 32, lo, hi, L);
+    const uint32_t first = 0xFFFFFFFFu - (uint32_t)start;
+    const uint32_t x = first ^ (0xFFFFFFFFu - (uint32_t)(start + len - 1));
+    const uint32_t below = x ? (0xFFFFFFFFu >> __clz(x)) : 0u;   // bits up to the highest of x
+    r.nz = (uint32_t)len;
+    r.all_and |= first & ~below;
+    r.any_or |= first | below;
     return r;
 }
 
@@ -241,15 +298,18 @@ __device__ SelectState radix_select(const uint64_t (&key)[P], int need, const Ch
     return SelectState{prefix, mask};
 }
 
-// Writes the block's taken keys to dst[0 .. min(taken, cap)) in some order,
-// positions from ballot prefix sums; returns the number taken (all threads).
-template <int T, int P, typename Taken>
-__device__ uint32_t compact_taken(const uint64_t (&key)[P], Taken taken, uint64_t* dst,
-                                  int cap, uint32_t* s_wc) {
+// Writes the block's taken keys, those with (key & tmask) >= tpre, to
+// dst[0 .. min(taken, cap)) in some order, positions from ballot prefix sums
+// (each wave's count, then its lanes' ranks inside each key slot); returns
+// the number taken (all threads).  One masked compare per key and slot; a
+// slot where the wave takes nothing is skipped on the scalar unit.
+template <int T, int P>
+__device__ uint32_t compact_taken(const uint64_t (&key)[P], uint64_t tmask, uint64_t tpre,
+                                  uint64_t* dst, int cap, uint32_t* s_wc) {
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
     uint32_t mine = 0;
 #pragma unroll
-    for (int e = 0; e < P; ++e) mine += (uint32_t)__popcll(__ballot(taken(e)));
+    for (int e = 0; e < P; ++e) mine += (uint32_t)__popcll(__ballot((key[e] & tmask) >= tpre));
     if (lane == 0) s_wc[wv] = mine;
     __syncthreads();
     uint32_t base = 0, total = 0;
@@ -259,14 +319,18 @@ __device__ uint32_t compact_taken(const uint64_t (&key)[P], Taken taken, uint64_
         base += (w < wv) ? c : 0u;
         total += c;
     }
-    const uint64_t below = (1ull << lane) - 1ull;
+    if (mine != 0u) {                                  // uniform over the wave
+        const uint64_t below = (1ull << lane) - 1ull;
 #pragma unroll
-    for (int e = 0; e < P; ++e) {
-        const bool t = taken(e);
-        const uint64_t m = __ballot(t);
-        const uint32_t pos = base + (uint32_t)__popcll(m & below);
-        if (t && pos < (uint32_t)cap) dst[pos] = key[e];
-        base += (uint32_t)__popcll(m);
+        for (int e = 0; e < P; ++e) {
+            const bool t = (key[e] & tmask) >= tpre;
+            const uint64_t m = __ballot(t);
+            if (m != 0ull) {
+                const uint32_t pos = base + (uint32_t)__popcll(m & below);
+                if (t && pos < (uint32_t)cap) dst[pos] = key[e];
+                base += (uint32_t)__popcll(m);
+            }
+        }
     }
     return total;
 }
@@ -326,15 +390,17 @@ __device__ void final_output(uint64_t* s_sel, uint64_t* s_sorted, int nt, int k,
         for (int t = tid; t < k * max_span; t += T) {
             const int r = t / max_span, j = t - r * max_span;
             const uint64_t key = sorted[r];
-            const int64_t id = (int64_t)key_row(key);
             // A padding key (0) surfaces only when fewer than k
             // candidates exist (an inverted-file search of short lists):
-            // id -1, score NaN, an empty draft.
+            // id -1, score NaN, an empty draft.  Its loads read row 0 so that
+            // the length and the token are both in flight at once.
+            const int64_t id = key == 0 ? 0 : (int64_t)key_row(key);
+            const int tok = out_drafts ? spans[id * span_stride + j] : 0;
             int len_r = (key == 0) ? 0 : (span_len ? span_len[id] : max_span);
             len_r = len_r < 0 ? 0 : (len_r > max_span ? max_span : len_r);
             const int64_t o = ((int64_t)q * k + r);
             if (out_drafts)
-                out_drafts[o * max_span + j] = (j < len_r) ? spans[id * span_stride + j] : -1;
+                out_drafts[o * max_span + j] = (j < len_r) ? tok : -1;
             if (out_draft_len && j == 0) out_draft_len[o] = len_r;
         }
     }
@@ -374,7 +440,13 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
     // past the chunk re-read its last one, a chunk is never empty here) so
     // that all loads are in flight at once: a load under a branch makes the
     // thread wait for it before issuing the next.
+    // The group-maxima bound pays where a chunk holds raw scores of both
+    // signs (its keys share no leading bits), first levels and single-chunk
+    // finals alike; later levels hold survivors that already share them.
+    constexpr bool kBound = FROM_SCORES;
+    const StatsLds lds{s_nzw, s_andw, s_orw, s_loww, s_highw};
     uint64_t key[P];
+    ChunkStats cs;
     if constexpr (FROM_SCORES) {
         const float* src = scores + (int64_t)q * count + start;
         const int last = len > 0 ? len - 1 : 0;
@@ -384,41 +456,38 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
             const int i = tid + e * kThreads;
             sv[e] = src[i < len ? i : last];
         }
+        uint32_t sw[P];
 #pragma unroll
         for (int e = 0; e < P; ++e) {
             const int i = tid + e * kThreads;
-            key[e] = i < len ? pack_key(sv[e], (uint32_t)(start + i)) : 0;
+            sw[e] = score_key(sv[e]);
+            key[e] = i < len ? (((uint64_t)sw[e] << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)(start + i)))
+                             : 0ull;
         }
+        cs = score_stats<kThreads, P>(sw, key, kk, start, len, lds);
     } else {
 #pragma unroll
         for (int e = 0; e < P; ++e) {
             const int i = tid + e * kThreads;
             key[e] = i < len ? in_keys[(int64_t)q * count + start + i] : 0;
         }
+        cs = chunk_stats<kThreads, P, kBound>(key, kk, lds);
     }
-    // The group-maxima bound pays where a chunk holds raw scores of both
-    // signs (its keys share no leading bits), first levels and single-chunk
-    // finals alike; later levels hold survivors that already share them.
-    constexpr bool kBound = FROM_SCORES;
-    const ChunkStats cs =
-        chunk_stats<kThreads, P, kBound>(key, kk, StatsLds{s_nzw, s_andw, s_orw, s_loww, s_highw});
 
-    // Keys taken: every real one if there are no more than kk, else the kk
-    // largest (then more than kk keys are real, as the radix select needs).
-    SelectState st{0, 0};
+    // Keys taken: every real (non-zero) one if there are no more than kk,
+    // else the kk largest (then more than kk keys are real, as the radix
+    // select needs); both as (key & mask) >= prefix.
+    SelectState st{1ull, ~0ull};
     const bool all = cs.nz <= (uint32_t)kk;
     if (!all) st = radix_select<kThreads, P, kBound>(key, kk, cs, s_hist, s_tot, s_info);
-    auto taken = [&](int e) {
-        return all ? (key[e] != 0) : ((key[e] & st.mask) >= st.prefix);
-    };
 
     if constexpr (!FINAL) {
         uint64_t* out = out_keys + ((int64_t)q * gridDim.x + blockIdx.x) * kk;
-        const uint32_t tot = compact_taken<kThreads, P>(key, taken, out, kk, s_wc);
+        const uint32_t tot = compact_taken<kThreads, P>(key, st.mask, st.prefix, out, kk, s_wc);
         const int nt = (int)tot < kk ? (int)tot : kk;
         for (int i = nt + tid; i < kk; i += kThreads) out[i] = 0;  // padding key
     } else {
-        const uint32_t tot = compact_taken<kThreads, P>(key, taken, s_sel, kk, s_wc);
+        const uint32_t tot = compact_taken<kThreads, P>(key, st.mask, st.prefix, s_sel, kk, s_wc);
         const int nt = (int)tot < kk ? (int)tot : kk;
         final_output<kThreads>(s_sel, s_sorted, nt, k, q, out_ids, out_scores, out_drafts,
                                out_draft_len, spans, span_len, max_span, span_stride);
@@ -474,14 +543,12 @@ __device__ int stream_rounds(const uint64_t* __restrict__ src, int64_t count, in
         __syncthreads();                               // s_sel read before it is rewritten
         const ChunkStats cs = chunk_stats<kStreamThreads, P, false>(
             key, kk, StatsLds{L.s_nzw, L.s_andw, L.s_orw, nullptr, nullptr});
-        SelectState st{0, 0};
+        SelectState st{1ull, ~0ull};                   // all real keys, as above
         const bool all = cs.nz <= (uint32_t)kk;
         if (!all)
             st = radix_select<kStreamThreads, P, false>(key, kk, cs, L.s_hist, L.s_tot, L.s_info);
-        auto taken = [&](int e) {
-            return all ? (key[e] != 0) : ((key[e] & st.mask) >= st.prefix);
-        };
-        const uint32_t tot = compact_taken<kStreamThreads, P>(key, taken, s_sel, kk, L.s_wc);
+        const uint32_t tot =
+            compact_taken<kStreamThreads, P>(key, st.mask, st.prefix, s_sel, kk, L.s_wc);
         nt = (int)tot < kk ? (int)tot : kk;
         pos += take;
         __syncthreads();                               // s_sel complete for the next round

@@ -195,6 +195,65 @@ def chunk_stats(B: Block, key, kk: int, bound: bool):
     return res
 
 
+def score_stats(B: Block, key, kk: int, start: int, n_real: int):
+    """chunk_stats with the bound for a chunk of raw scores (rows start ..
+    start + n_real - 1): AND / OR over the score words, where a slot past
+    the chunk holds a copy of the last real slot's; the row words' AND / OR
+    from the two ends of the row range.  Checked against the direct
+    statistics of the real keys."""
+    T, P = B.T, len(key[0])
+    last_word = key[(n_real - 1) % T][(n_real - 1) // T] >> 32
+    per_wave = []
+    for lanes in wave_lanes(T):
+        a, o = 0xFFFFFFFF, 0
+        mx = []
+        for t in lanes:
+            for e in range(P):
+                w = (key[t][e] >> 32) if t + e * T < n_real else last_word
+                a &= w
+                o |= w
+            mx.append(max((key[t][e] >> 32) for e in range(P)))
+        gq = T // (kk if kk > 0 else 1)
+        g = 64 if gq >= 64 else ((1 << (31 - clz32(gq))) if gq > 0 else 0)
+        v, gm = dpp_max_ladder(mx, g)
+        per_wave.append((0, a << 32, o << 32, min(gm), v[0]))
+    for t in B.order():
+        if t % 64 == 0:
+            w = t // 64
+            nz, a, o, lo, hi = per_wave[w]
+            B.wr(t, "nzw", w, nz)
+            B.wr(t, "andw", w, a)
+            B.wr(t, "orw", w, o)
+            B.wr(t, "loww", w, lo)
+            B.wr(t, "highw", w, hi)
+    B.sync()
+    res = None
+    for t in B.order():
+        r = [0, M64, 0, 0xFFFFFFFF, 0]
+        for w in range(B.W):
+            r[0] += B.rd(t, "nzw", w)
+            r[1] &= B.rd(t, "andw", w)
+            r[2] |= B.rd(t, "orw", w)
+            r[3] = min(r[3], B.rd(t, "loww", w))
+            r[4] = max(r[4], B.rd(t, "highw", w))
+        first = 0xFFFFFFFF - start
+        x = first ^ (0xFFFFFFFF - (start + n_real - 1))
+        below = (0xFFFFFFFF >> clz32(x)) if x else 0
+        r[0] = n_real
+        r[1] |= first & ~below & 0xFFFFFFFF
+        r[2] |= first | below
+        assert res is None or res == r, "threads disagree on the chunk statistics"
+        res = r
+    real = [key[t][e] for t in range(T) for e in range(P) if t + e * T < n_real]
+    a = o = None
+    for x in real:
+        a = x if a is None else a & x
+        o = x if o is None else o | x
+    assert all(x != 0 for x in real) and (res[0], res[1], res[2]) == (len(real), a, o), \
+        "score-word statistics differ from the direct ones"
+    return res
+
+
 def radix_select(B: Block, key, need: int, cs, bound: bool):
     T, P, W = B.T, len(key[0]), B.W
     nz, all_and, any_or, low32, high32 = cs
@@ -269,10 +328,12 @@ def radix_select(B: Block, key, need: int, cs, bound: bool):
     return prefix, mask
 
 
-def compact_taken(B: Block, key, taken, dst, cap: int):
-    """dst: ("lds", name) or a Python list (global memory)."""
+def compact_taken(B: Block, key, tmask: int, tpre: int, dst, cap: int):
+    """Keys with (key & tmask) >= tpre to dst[0 .. min(taken, cap)) by
+    ballot prefix sums; dst: ("lds", name) or a Python list (global
+    memory)."""
     T, P = B.T, len(key[0])
-    tk = [[taken(t, e) for e in range(P)] for t in range(T)]
+    tk = [[(key[t][e] & tmask) >= tpre for e in range(P)] for t in range(T)]
     for t in B.order():
         if t % 64 == 0:
             w = t // 64
@@ -362,11 +423,12 @@ def final_output(B: Block, nt: int, k: int, rank_max: int = 256):
 
 
 def select_block(keys_in: list, k: int, threads: int, per: int, bound: bool, final: bool,
-                 rng: np.random.Generator):
+                 rng: np.random.Generator, score_start=None):
     """One block of select_kernel over one chunk (a list of packed keys, at
-    most threads * per; missing slots are padding).  Returns (out, block):
-    the kk survivor keys (padded with 0) or, when final, the k output keys
-    in order."""
+    most threads * per; missing slots are padding).  score_start: the chunk
+    holds raw scores of rows score_start .. (the score-word statistics).
+    Returns (out, block): the kk survivor keys (padded with 0) or, when
+    final, the k output keys in order."""
     T, P = threads, per
     CH = T * P
     assert len(keys_in) <= CH
@@ -378,23 +440,23 @@ def select_block(keys_in: list, k: int, threads: int, per: int, bound: bool, fin
     key = [[keys_in[t + e * T] if t + e * T < len(keys_in) else 0 for e in range(P)]
            for t in range(T)]
     kk = min(k, CH)
-    cs = chunk_stats(B, key, kk, bound)
+    if score_start is not None:
+        cs = score_stats(B, key, kk, score_start, len(keys_in))
+    else:
+        cs = chunk_stats(B, key, kk, bound)
     allk = cs[0] <= kk
-    prefix = mask = 0
+    prefix, mask = 1, M64                  # every real key
     if not allk:
         prefix, mask = radix_select(B, key, kk, cs, bound)
-
-    def taken(t, e):
-        return key[t][e] != 0 if allk else (key[t][e] & mask) >= prefix
     if not final:
         out = [None] * kk
-        tot = compact_taken(B, key, taken, out, kk)
+        tot = compact_taken(B, key, mask, prefix, out, kk)
         nt = min(tot, kk)
         for i in range(nt, kk):
             out[i] = 0
         B.check()
         return out, B
-    tot = compact_taken(B, key, taken, ("lds", "sel"), kk)
+    tot = compact_taken(B, key, mask, prefix, ("lds", "sel"), kk)
     nt = min(tot, kk)
     out = final_output(B, nt, k)
     B.check()
@@ -414,12 +476,13 @@ def select_launch(scores: np.ndarray, k: int, rng: np.random.Generator, per: int
     chunks = -(-n // 8192)
     if chunks <= 2:
         p = 8 if n <= threads * 8 else (per if chunks == 1 else 2 * per)
-        out, _ = select_block(keys, k, threads, p, bound=True, final=True, rng=rng)
+        out, _ = select_block(keys, k, threads, p, bound=True, final=True, rng=rng,
+                              score_start=0)
         return [(-1 if x == 0 else key_row(x)) for x in out]
     level = []
     for c in range(chunks):
         o, _ = select_block(keys[c * 8192:(c + 1) * 8192], k, threads, 16, bound=True,
-                            final=False, rng=rng)
+                            final=False, rng=rng, score_start=c * 8192)
         level += o
     while -(-len(level) // 8192) > 1:
         nxt = []
@@ -465,13 +528,10 @@ def stream_launch(keys_in: list, count: int, k: int, rng: np.random.Generator,
         B.sync()
         cs = chunk_stats(B, key, kk, False)
         allk = cs[0] <= kk
-        prefix = mask = 0
+        prefix, mask = 1, M64              # every real key
         if not allk:
             prefix, mask = radix_select(B, key, kk, cs, False)
-
-        def taken(t, e, allk=allk, prefix=prefix, mask=mask, key=key):
-            return key[t][e] != 0 if allk else (key[t][e] & mask) >= prefix
-        tot = compact_taken(B, key, taken, ("lds", "sel"), kk)
+        tot = compact_taken(B, key, mask, prefix, ("lds", "sel"), kk)
         nt = min(tot, kk)
         pos += take
         B.sync()

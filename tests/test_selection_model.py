@@ -9,7 +9,8 @@ cross-thread read/write conflict, no word may be read before this launch
 wrote it, every radix pass must have exactly one lane writing the digit
 record, and the rows must equal a plain sort's.  The detector itself is
 checked by planting two hazards: a missing barrier and a radix pass whose
-digit record nobody writes."""
+digit record nobody writes.  The score-word statistics of first-level
+chunks are checked against the direct ones on every launch."""
 import numpy as np
 import pytest
 
@@ -83,6 +84,25 @@ def test_stream_kernel_rounds_are_race_free(count, cap, k):
     want = [sm.key_row(x) for x in sorted(live, reverse=True)[:k]]
     want += [-1] * (k - len(want))
     assert got == want
+
+
+@pytest.mark.parametrize("start,length", [(0, 1), (5, 2), (7, 2), (1023, 3), (4096, 4096),
+                                          ((1 << 20) - 5, 8192), ((1 << 31) - 8195, 8192),
+                                          ((1 << 31) - 1, 1), (12345, 777)])
+def test_score_chunk_statistics_match_the_direct_ones(start, length):
+    """The row words' AND / OR of a first-level chunk come from the ends of
+    its row range (score_stats asserts them equal to the direct statistics
+    of the real keys); chunks that start anywhere, cross carries into high
+    bits or hold one or two rows select exactly."""
+    rng = np.random.default_rng(start + length)
+    s = make_scores(rng, length, "ties")
+    keys = sm.pack_keys(s, np.arange(start, start + length))
+    per = 16 if length > 4096 else 8
+    for k in (1, 8, min(length, 1024)):
+        kk = min(k, length)
+        out, _ = sm.select_block(keys, kk, 512, per, bound=True, final=True,
+                                 rng=np.random.default_rng(k), score_start=start)
+        assert out == sorted(keys, reverse=True)[:kk]
 
 
 def test_detector_flags_a_missing_barrier(monkeypatch):
