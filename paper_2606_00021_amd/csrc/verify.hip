@@ -27,9 +27,11 @@
 // verify_finalize: one block per candidate group.  Phase 1 gives every
 //   (candidate, position) row its own thread, which merges the row's slices
 //   in slice order and forms the exact-match / entropy / top-k bits; phase 2
-//   gives every candidate a thread that counts window mismatches with a
-//   popcount over 64-bit masks and finds the leading run of accepted
-//   positions; the block then picks the group's first longest candidate.
+//   gives every row a thread again, which counts its window's mismatches
+//   with one popcount over the candidate's 64-bit exact-match mask and forms
+//   its gate bit; phase 3 gives every candidate a thread that takes the
+//   leading run of its gate mask; the block then picks the group's first
+//   longest candidate.
 #include "internal.h"
 
 namespace sense {
@@ -372,7 +374,7 @@ __global__ __launch_bounds__(kRowThreads) void verify_rows_kernel(
 
 constexpr int kFinThreads = 512;
 constexpr int kFinChunkRows = 4096;   // (candidate, position) rows per LDS chunk
-constexpr int kGammaBatch = 16;       // tree finalize: Gamma entries loaded together
+constexpr int kFinChunkCands = 1024;  // candidates per LDS chunk
 
 __device__ __forceinline__ uint64_t bits_upto(int x) {  // bits 0..x set (x may be -1)
     return (x >= 63) ? ~0ull : ((x < 0) ? 0ull : ((1ull << (x + 1)) - 1ull));
@@ -418,64 +420,63 @@ __device__ __forceinline__ uint8_t item_bits(const Stats& a, int cnt, int tok, i
                      (valid && *rank < gp.topk ? 4 : 0));
 }
 
-// The gate of one draft from its per-position bits (Alg. 4's window,
-// cascade and leading run).  Writes the masks row if asked; returns n.
-__device__ __forceinline__ int gate_draft(uint64_t em, uint64_t ent, uint64_t tkm, int len,
-                                          int max_len, const GateParams& gp,
-                                          uint8_t* masks_row) {
-    // Mismatches: 1 - B_em inside the draft, and W padding ones after it.
-    const uint64_t notem = ~em & bits_upto(max_len - 1);
-    int n = 0;
-    bool still = true;
-    for (int jj = 0; jj < max_len; ++jj) {
-        const int hi = jj + gp.window;
-        const int in_hi = hi < max_len - 1 ? hi : max_len - 1;
-        const uint64_t range = bits_upto(in_hi) & ~bits_upto(jj);
-        const int r = __popcll(notem & range) + (hi > max_len - 1 ? hi - (max_len - 1) : 0);
-        const bool con = r <= gp.tau;
-        const bool bem = (em >> jj) & 1, bent = (ent >> jj) & 1, btk = (tkm >> jj) & 1;
-        const bool gate = (jj < len) && (bem || (bent && (btk || con)));
-        if (still && gate) ++n; else still = false;
-        if (masks_row)
-            masks_row[jj] = (uint8_t)((int)bem | ((int)bent << 1) | ((int)btk << 2) |
-                                      ((int)con << 3) | ((int)gate << 4));
-    }
-    return n;
-}
-
 // First candidate with the largest n in the block (all threads call it).
+// A thread's (n, i) is one key, n + 1 above the complemented index, so the
+// largest key has the largest n and then the smallest i (a thread that saw
+// no candidate has n = -1, below every real one); each wave takes its
+// maximum with lane swaps and thread 0 the waves'.
 __device__ void group_best(int best_n, int best_i, int32_t* out) {
-    __shared__ int s_n[kFinThreads], s_i[kFinThreads];
-    s_n[threadIdx.x] = best_n;
-    s_i[threadIdx.x] = best_i;
-    __syncthreads();
-    for (int off = kFinThreads / 2; off > 0; off >>= 1) {
-        if ((int)threadIdx.x < off) {
-            const int on = s_n[threadIdx.x + off], oi = s_i[threadIdx.x + off];
-            if (on > s_n[threadIdx.x] || (on == s_n[threadIdx.x] && oi < s_i[threadIdx.x])) {
-                s_n[threadIdx.x] = on;
-                s_i[threadIdx.x] = oi;
-            }
-        }
-        __syncthreads();
+    __shared__ uint64_t s_w[kFinThreads / 64];
+    uint64_t key = ((uint64_t)(uint32_t)(best_n + 1) << 32) |
+                   (uint64_t)(0xFFFFFFFFu - (uint32_t)best_i);
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        const uint64_t o = __shfl_xor(key, off, 64);
+        key = o > key ? o : key;
     }
-    if (threadIdx.x == 0) *out = s_i[0];
+    if ((threadIdx.x & 63) == 0) s_w[threadIdx.x >> 6] = key;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint64_t m = s_w[0];
+#pragma unroll
+        for (int w = 1; w < kFinThreads / 64; ++w) m = s_w[w] > m ? s_w[w] : m;
+        *out = (int32_t)(0xFFFFFFFFu - (uint32_t)m);
+    }
 }
 
+// Dense finalize, one block per group, in chunks of candidates.  Phase 1
+// gives every (candidate, position) row a thread: the row's bits into LDS
+// and its exact-match bit into the candidate's 64-bit mask.  Phase 2 gives
+// every row a thread again: the mismatches in its window from the mask (one
+// popcount), its gate bit (Alg. 4's cascade) into the candidate's gate
+// mask.  Phase 3 gives every candidate a thread: the leading run of the gate
+// mask is the accepted length.  No thread walks a draft's positions, so the
+// cost does not grow with the draft length.
 __global__ __launch_bounds__(kFinThreads) void verify_finalize_kernel(
     const Partial* __restrict__ partial, int n_slices, const int32_t* __restrict__ drafts,
     const int32_t* __restrict__ draft_len, int max_len, int vocab, int group_size,
     GateParams gp, int32_t* __restrict__ out_accept_len, int32_t* __restrict__ out_best,
     float* __restrict__ out_gate_score, uint8_t* __restrict__ out_masks,
     int32_t* __restrict__ out_rank) {
-    __shared__ uint8_t s_bits[kFinChunkRows];   // em | ent<<1 | topk<<2 per row
+    __shared__ uint8_t s_bits[kFinChunkRows];     // em | ent<<1 | topk<<2 per row
+    __shared__ uint8_t s_len[kFinChunkCands];     // clamped draft length per candidate
+    __shared__ uint64_t s_em[kFinChunkCands];     // exact-match bit per position
+    __shared__ uint64_t s_gate[kFinChunkCands];   // gate bit per position
     const int g = blockIdx.x;
-    const int chunk_cands = kFinChunkRows / max_len;
+    const int by_rows = kFinChunkRows / max_len;
+    const int chunk_cands = by_rows < kFinChunkCands ? by_rows : kFinChunkCands;
+    const uint64_t in_draft = bits_upto(max_len - 1);
+    for (int cl = threadIdx.x; cl < kFinChunkCands; cl += kFinThreads) {
+        s_em[cl] = 0ull;
+        s_gate[cl] = 0ull;
+    }
+    __syncthreads();
     int best_n = -1, best_i = 0;
     for (int cc0 = 0; cc0 < group_size; cc0 += chunk_cands) {
         const int ncc = (group_size - cc0 < chunk_cands) ? group_size - cc0 : chunk_cands;
-        // Phase 1: one thread per (candidate, position).
-        for (int r = threadIdx.x; r < ncc * max_len; r += kFinThreads) {
+        const int rows = ncc * max_len;
+        // Phase 1: the row statistics.
+        for (int r = threadIdx.x; r < rows; r += kFinThreads) {
             const int cl = r / max_len, jj = r - cl * max_len;
             const int c = g * group_size + cc0 + cl;
             const int64_t row = (int64_t)c * max_len + jj;
@@ -494,37 +495,58 @@ __global__ __launch_bounds__(kFinThreads) void verify_finalize_kernel(
             if (out_gate_score) out_gate_score[row] = score;
             if (out_rank) out_rank[row] = rank;
             s_bits[r] = bits;
+            if (jj == 0) s_len[cl] = (uint8_t)len;
+            if (bits & 1) atomicOr((unsigned long long*)&s_em[cl], 1ull << jj);
         }
         __syncthreads();
-        // Phase 2: one thread per candidate.
-        for (int cl = threadIdx.x; cl < ncc; cl += kFinThreads) {
-            const int c = g * group_size + cc0 + cl;
-            int len = draft_len ? draft_len[c] : max_len;
-            len = len < 0 ? 0 : (len > max_len ? max_len : len);
-            uint64_t em = 0, ent = 0, tkm = 0;
-            for (int jj = 0; jj < max_len; ++jj) {
-                const uint8_t b = s_bits[cl * max_len + jj];
-                em |= (uint64_t)(b & 1) << jj;
-                ent |= (uint64_t)((b >> 1) & 1) << jj;
-                tkm |= (uint64_t)((b >> 2) & 1) << jj;
+        // Phase 2: each row's window and gate.  Mismatches are 1 - B_em
+        // inside the draft (every position past its length included) and
+        // W padding ones past the last position.
+        for (int r = threadIdx.x; r < rows; r += kFinThreads) {
+            const int cl = r / max_len, jj = r - cl * max_len;
+            const uint8_t b = s_bits[r];
+            const uint64_t notem = ~s_em[cl] & in_draft;
+            const int hi = jj + gp.window;
+            const int in_hi = hi < max_len - 1 ? hi : max_len - 1;
+            const uint64_t range = bits_upto(in_hi) & ~bits_upto(jj);
+            const int mis = __popcll(notem & range) + (hi > max_len - 1 ? hi - (max_len - 1) : 0);
+            const bool con = mis <= gp.tau;
+            const bool bem = b & 1, bent = (b >> 1) & 1, btk = (b >> 2) & 1;
+            const bool gate = (jj < (int)s_len[cl]) && (bem || (bent && (btk || con)));
+            if (out_masks) {
+                const int64_t row = (int64_t)(g * group_size + cc0 + cl) * max_len + jj;
+                out_masks[row] = (uint8_t)((int)bem | ((int)bent << 1) | ((int)btk << 2) |
+                                           ((int)con << 3) | ((int)gate << 4));
             }
-            const int n = gate_draft(em, ent, tkm, len, max_len, gp,
-                                     out_masks ? out_masks + (int64_t)c * max_len : nullptr);
-            out_accept_len[c] = n;
+            if (gate) atomicOr((unsigned long long*)&s_gate[cl], 1ull << jj);
+        }
+        __syncthreads();
+        // Phase 3: the accepted length, and the masks cleared for the next
+        // chunk (each candidate's words by its own thread).
+        for (int cl = threadIdx.x; cl < ncc; cl += kFinThreads) {
+            const uint64_t open = ~s_gate[cl];
+            const int n = open == 0ull ? 64 : __builtin_ctzll(open);
+            out_accept_len[g * group_size + cc0 + cl] = n;
             if (n > best_n) {
                 best_n = n;
                 best_i = cc0 + cl;
             }
+            s_em[cl] = 0ull;
+            s_gate[cl] = 0ull;
         }
         __syncthreads();
     }
     group_best(best_n, best_i, out_best + g);
 }
 
-// Tree variant, one block per group: phase 1 gives every tree node of the
-// group a thread (bits, score and rank into LDS); phase 2 gives every draft
-// a thread that reads its positions' nodes through Gamma.  A draft's length
-// is its leading run of positions with a judged node.
+// Tree variant, one block per group.  Phase 1 gives every tree node of the
+// group a thread (bits, score and rank into LDS).  Then every (draft,
+// position) row gets a thread in three phases: its node through Gamma and
+// whether that node is judged (into the draft's 64-bit mask); the draft's
+// length, the leading run of that mask, and the row's bits and outputs
+// (exact-match bit into the draft's mask); its window and gate bit, as in
+// the dense finalize.  Last, every draft a thread for the leading run of its
+// gate mask.
 __global__ __launch_bounds__(kFinThreads) void verify_finalize_tree_kernel(
     const Partial* __restrict__ partial, int n_slices, const int32_t* __restrict__ tree_tokens,
     const int32_t* __restrict__ tree_parent, const int32_t* __restrict__ tree_len,
@@ -532,12 +554,24 @@ __global__ __launch_bounds__(kFinThreads) void verify_finalize_tree_kernel(
     int32_t* __restrict__ out_accept_len, int32_t* __restrict__ out_best,
     float* __restrict__ out_gate_score, uint8_t* __restrict__ out_masks,
     int32_t* __restrict__ out_rank) {
-    __shared__ uint8_t s_bits[kMaxNodes];       // em | ent<<1 | topk<<2 | judged<<3
+    __shared__ uint8_t s_bits[kMaxNodes];       // em | ent<<1 | topk<<2 | judged<<3 per node
     __shared__ float s_score[kMaxNodes];
     __shared__ int32_t s_rank[kMaxNodes];
+    __shared__ int16_t s_node[kMaxNodes];       // per row: its judged node, else -1
+    __shared__ uint8_t s_rbits[kMaxNodes];      // per row: its node's bits inside the draft
+    __shared__ uint64_t s_run[kMaxGroup];       // per draft: positions with a judged node
+    __shared__ uint64_t s_em[kMaxGroup];        // per draft: exact-match bits
+    __shared__ uint64_t s_gate[kMaxGroup];      // per draft: gate bits
+    __shared__ uint8_t s_len[kMaxGroup];        // per draft: its length
     const int g = blockIdx.x;
     const int nodes = group_size * max_len;
     const int L = tree_len[g] < nodes ? tree_len[g] : nodes;
+    const uint64_t in_draft = bits_upto(max_len - 1);
+    for (int cl = threadIdx.x; cl < group_size; cl += kFinThreads) {
+        s_run[cl] = 0ull;
+        s_em[cl] = 0ull;
+        s_gate[cl] = 0ull;
+    }
     for (int u = threadIdx.x; u < L; u += kFinThreads) {
         const int item = g * nodes + u;
         // Every load of the node first (the partials of a node that is not
@@ -558,41 +592,62 @@ __global__ __launch_bounds__(kFinThreads) void verify_finalize_tree_kernel(
         s_rank[u] = rank;
     }
     __syncthreads();
+    // Rows: the node of each draft position, and whether it is judged.
+    for (int r = threadIdx.x; r < nodes; r += kFinThreads) {
+        const int cl = r / max_len, jj = r - cl * max_len;
+        const int u = gamma[(int64_t)(g * group_size + cl) * max_len + jj];
+        const bool judged = u >= 0 && u < L && (s_bits[u] & 8);
+        s_node[r] = judged ? (int16_t)u : (int16_t)-1;
+        if (judged) atomicOr((unsigned long long*)&s_run[cl], 1ull << jj);
+    }
+    __syncthreads();
+    // Rows: a draft's length is its leading run of judged positions; the
+    // bits and outputs of the positions inside it.
+    for (int r = threadIdx.x; r < nodes; r += kFinThreads) {
+        const int cl = r / max_len, jj = r - cl * max_len;
+        const uint64_t unjudged = ~s_run[cl];
+        const int len = unjudged == 0ull ? 64 : __builtin_ctzll(unjudged);
+        const bool inside = jj < len;
+        const int u = s_node[r];
+        const uint8_t b = inside ? s_bits[u] : 0;
+        const int64_t o = (int64_t)(g * group_size + cl) * max_len + jj;
+        if (out_gate_score) out_gate_score[o] = inside ? s_score[u] : 0.0f;
+        if (out_rank) out_rank[o] = inside ? s_rank[u] : vocab;
+        s_rbits[r] = b;
+        if (jj == 0) s_len[cl] = (uint8_t)len;
+        if (b & 1) atomicOr((unsigned long long*)&s_em[cl], 1ull << jj);
+    }
+    __syncthreads();
+    // Rows: window and gate.
+    for (int r = threadIdx.x; r < nodes; r += kFinThreads) {
+        const int cl = r / max_len, jj = r - cl * max_len;
+        const uint8_t b = s_rbits[r];
+        const uint64_t notem = ~s_em[cl] & in_draft;
+        const int hi = jj + gp.window;
+        const int in_hi = hi < max_len - 1 ? hi : max_len - 1;
+        const uint64_t range = bits_upto(in_hi) & ~bits_upto(jj);
+        const int mis = __popcll(notem & range) + (hi > max_len - 1 ? hi - (max_len - 1) : 0);
+        const bool con = mis <= gp.tau;
+        const bool bem = b & 1, bent = (b >> 1) & 1, btk = (b >> 2) & 1;
+        const bool gate = (jj < (int)s_len[cl]) && (bem || (bent && (btk || con)));
+        if (out_masks) {
+            const int64_t o = (int64_t)(g * group_size + cl) * max_len + jj;
+            out_masks[o] = (uint8_t)((int)bem | ((int)bent << 1) | ((int)btk << 2) |
+                                     ((int)con << 3) | ((int)gate << 4));
+        }
+        if (gate) atomicOr((unsigned long long*)&s_gate[cl], 1ull << jj);
+    }
+    __syncthreads();
     int best_n = -1, best_i = 0;
     for (int cl = threadIdx.x; cl < group_size; cl += kFinThreads) {
-        const int c = g * group_size + cl;
-        uint64_t em = 0, ent = 0, tkm = 0;
-        int len = 0;
-        bool run = true;
-        int gb[kGammaBatch];
-        for (int jj = 0; jj < max_len; ++jj) {
-            // Gamma of the next kGammaBatch positions, requested together.
-            if (jj % kGammaBatch == 0) {
-#pragma unroll
-                for (int t = 0; t < kGammaBatch; ++t)
-                    gb[t] = gamma[(int64_t)c * max_len + ((jj + t < max_len) ? jj + t : max_len - 1)];
-            }
-            const int u = gb[jj % kGammaBatch];
-            const bool judged = run && u >= 0 && u < L && (s_bits[u] & 8);
-            run = judged;
-            const uint8_t b = judged ? s_bits[u] : 0;
-            len += judged ? 1 : 0;
-            em |= (uint64_t)(b & 1) << jj;
-            ent |= (uint64_t)((b >> 1) & 1) << jj;
-            tkm |= (uint64_t)((b >> 2) & 1) << jj;
-            const int64_t o = (int64_t)c * max_len + jj;
-            if (out_gate_score) out_gate_score[o] = judged ? s_score[u] : 0.0f;
-            if (out_rank) out_rank[o] = judged ? s_rank[u] : vocab;
-        }
-        const int n = gate_draft(em, ent, tkm, len, max_len, gp,
-                                 out_masks ? out_masks + (int64_t)c * max_len : nullptr);
-        out_accept_len[c] = n;
+        const uint64_t open = ~s_gate[cl];
+        const int n = open == 0ull ? 64 : __builtin_ctzll(open);
+        out_accept_len[g * group_size + cl] = n;
         if (n > best_n) {
             best_n = n;
             best_i = cl;
         }
     }
-    __syncthreads();
     group_best(best_n, best_i, out_best + g);
 }
 
