@@ -138,6 +138,37 @@ def test_verify_tree_matches_oracle(case):
         check_verify(sub, ref, 0.05, SL)
 
 
+def test_verify_tree_full_length():
+    """Groups of 16 drafts of 64 tokens (1024 tree rows) that pass the gate
+    at every judged position (gamma below every entropy score, top-k over
+    the whole vocabulary): every draft accepts all 64 positions through
+    Gamma, and the result meets the oracle's dense verification."""
+    G, gs, m, vocab = 2, 16, 64, 1000
+    drafts, lens = synth.make_drafts(43, G * gs, m, 3, DEV, 0.8, False, n_groups=G)
+    tr = sense.sense_build_loose_trie(drafts, None, n_groups=G)
+    D = drafts.cpu().numpy()
+    groups = [oracle_group(D, np.full(G * gs, m), g, gs, m) for g in range(G)]
+    nodes = gs * m
+    tok_h = [np.r_[gr[3], -np.ones(nodes - gr[3].shape[0], dtype=np.int64)] for gr in groups]
+    par_h = [np.r_[gr[6], -np.ones(nodes - gr[3].shape[0], dtype=np.int64)] for gr in groups]
+    tl_h = [gr[3].shape[0] for gr in groups]
+    logits = synth.make_tree_logits(vocab, "bf16", G, nodes, tok_h, par_h, tl_h, 47, DEV)
+    out = sense.sense_soft_gate_verify_tree(logits, tr, n_groups=G, gamma=-1.0, topk=1 << 20,
+                                            window=3)
+    torch.cuda.synchronize()
+    bits = host_bits(logits)
+    for g, (order, S, SL, T, gamma, mask, parent, depth, cand) in enumerate(groups):
+        dense = otrie.aligned_logits(bits[g], gamma)
+        ref = oracle.soft_gate_verify(dense, "bf16", S.astype(np.int32), SL.astype(np.int32),
+                                      gamma=-1.0, topk=1 << 20, window=3)
+        sl = slice(g * gs, (g + 1) * gs)
+        sub = {"accept_len": out["accept_len"][sl], "best": out["best"][g:g + 1],
+               "gate_score": out["gate_score"][sl], "masks": out["masks"][sl],
+               "rank": out["rank"][sl]}
+        check_verify(sub, ref, -1.0, SL)
+    assert (out["accept_len"].cpu() == m).all()
+
+
 def test_verify_tree_equals_dense_verify_bitwise():
     """The same row statistics read through Gamma or from a dense copy of
     the aligned rows give identical bits."""

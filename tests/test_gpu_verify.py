@@ -57,6 +57,22 @@ def run(logits, drafts, draft_len=None, n_groups=1, gamma=0.05, topk=3, window=6
     return out, ref
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_full_length_acceptance(dtype):
+    """Drafts of 64 tokens (the longest) that pass the gate at every
+    position: greedy drafts, gamma below every entropy score and the tied
+    (or, in 16 bits, rounded-together) rows inside the top 10, so every
+    candidate accepts its whole length
+    (all 64 gate bits set) and the first one is the best; with ragged
+    lengths each accepts exactly its own length."""
+    logits, drafts = structured(37, 6, 64, 512, p_match=1.0, dtype=dtype)
+    out, ref = run(logits, drafts, gamma=-1.0, topk=10, window=6)
+    assert (out["accept_len"].cpu() == 64).all() and int(out["best"][0]) == 0
+    lens = np.array([64, 63, 1, 0, 40, 64], dtype=np.int32)
+    out, ref = run(logits, drafts, draft_len=lens, n_groups=2, gamma=-1.0, topk=10, window=6)
+    assert np.array_equal(out["accept_len"].cpu().numpy(), lens)
+
+
 @pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
 @pytest.mark.parametrize("v", [32000, 1001, 77])
 def test_structured(dtype, v):
