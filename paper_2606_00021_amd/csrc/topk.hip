@@ -23,9 +23,9 @@
 // starts below the bits that this bound and the largest key share: every
 // key of the top k lies between them.  Each pass builds a 256-bin LDS
 // histogram of the next 8-bit digit among the keys that still match the
-// chosen prefix, then one wave finds the digit holding the k-th key with a
-// suffix scan; the loop stops as soon as that digit's bucket is taken
-// whole.  The taken keys are compacted by ballot prefix sums (no atomics).
+// chosen prefix, then one wave totals the waves' histograms and finds the
+// digit holding the k-th key with a suffix scan; the loop stops as soon as
+// that digit's bucket is taken whole.  The taken keys are compacted by ballot prefix sums (no atomics).
 // The k survivors of every chunk form the next level's input until one
 // chunk remains; its keys are put in order by rank (each key counts the
 // keys above it, all reads LDS broadcasts) and written out together with
@@ -215,7 +215,7 @@ __device__ ChunkStats score_stats(const uint32_t (&sw)[P], const uint64_t (&key)
 // few).
 template <int T, int P, bool BOUND>
 __device__ SelectState radix_select(const uint64_t (&key)[P], int need, const ChunkStats& cs,
-                                    uint32_t* s_hist, uint32_t* s_tot, uint32_t* s_info) {
+                                    uint32_t* s_hist, uint32_t* s_info) {
     const int tid = threadIdx.x;
     const int wv = tid >> 6;
     uint32_t* my = s_hist + wv * 256;
@@ -248,21 +248,20 @@ __device__ SelectState radix_select(const uint64_t (&key)[P], int need, const Ch
             if (act) atomicAdd(&my[dg], 1u);
         }
         __syncthreads();
-        // Totals; the per-wave histograms are cleared for the next pass.
-        for (int b = tid; b < 256; b += T) {
-            uint32_t t = 0;
-#pragma unroll
-            for (int w = 0; w < T / 64; ++w) {
-                t += s_hist[w * 256 + b];
-                s_hist[w * 256 + b] = 0;
-            }
-            s_tot[b] = t;
-        }
-        __syncthreads();
+        // Wave 0: the totals of its lane's four digits over the waves'
+        // histograms (16-byte LDS reads; the histograms cleared for the next
+        // pass), then the digit holding the need-th key by a suffix scan.
         if (tid < 64) {
             const int l = tid;
-            const uint32_t h0 = s_tot[4 * l], h1 = s_tot[4 * l + 1], h2 = s_tot[4 * l + 2],
-                           h3 = s_tot[4 * l + 3];
+            typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+            u32x4_t h = {0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int w = 0; w < T / 64; ++w) {
+                u32x4_t* p = (u32x4_t*)(s_hist + w * 256 + 4 * l);
+                h += *p;
+                *p = u32x4_t{0u, 0u, 0u, 0u};
+            }
+            const uint32_t h0 = h[0], h1 = h[1], h2 = h[2], h3 = h[3];
             const uint32_t local = h0 + h1 + h2 + h3;
             // inclusive suffix sum over lanes l..63 (higher digits)
             uint32_t incl = local;
@@ -420,8 +419,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
     const int32_t* __restrict__ span_len, int max_span, int64_t span_stride) {
     __shared__ uint64_t s_sel[kMaxK];
     __shared__ uint64_t s_sorted[FINAL ? kMaxK : 1];
-    __shared__ uint32_t s_hist[kWaves * 256];
-    __shared__ uint32_t s_tot[256];
+    __shared__ __align__(16) uint32_t s_hist[kWaves * 256];   // read 16 bytes at a time
     __shared__ uint32_t s_info[4];
     __shared__ uint32_t s_nzw[kWaves], s_wc[kWaves];
     __shared__ uint64_t s_andw[kWaves], s_orw[kWaves];
@@ -479,7 +477,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
     // select needs); both as (key & mask) >= prefix.
     SelectState st{1ull, ~0ull};
     const bool all = cs.nz <= (uint32_t)kk;
-    if (!all) st = radix_select<kThreads, P, kBound>(key, kk, cs, s_hist, s_tot, s_info);
+    if (!all) st = radix_select<kThreads, P, kBound>(key, kk, cs, s_hist, s_info);
 
     if constexpr (!FINAL) {
         uint64_t* out = out_keys + ((int64_t)q * gridDim.x + blockIdx.x) * kk;
@@ -506,7 +504,6 @@ constexpr int kStreamPer = kPer;                       // the largest P
 
 struct StreamLds {
     uint32_t* s_hist;
-    uint32_t* s_tot;
     uint32_t* s_info;
     uint32_t* s_nzw;
     uint32_t* s_wc;
@@ -546,7 +543,7 @@ __device__ int stream_rounds(const uint64_t* __restrict__ src, int64_t count, in
         SelectState st{1ull, ~0ull};                   // all real keys, as above
         const bool all = cs.nz <= (uint32_t)kk;
         if (!all)
-            st = radix_select<kStreamThreads, P, false>(key, kk, cs, L.s_hist, L.s_tot, L.s_info);
+            st = radix_select<kStreamThreads, P, false>(key, kk, cs, L.s_hist, L.s_info);
         const uint32_t tot =
             compact_taken<kStreamThreads, P>(key, st.mask, st.prefix, s_sel, kk, L.s_wc);
         nt = (int)tot < kk ? (int)tot : kk;
@@ -565,12 +562,11 @@ __global__ __launch_bounds__(kStreamThreads) void select_stream_kernel(
     constexpr int W = kStreamThreads / 64;
     __shared__ uint64_t s_sel[kMaxK];
     __shared__ uint64_t s_sorted[kMaxK];
-    __shared__ uint32_t s_hist[W * 256];
-    __shared__ uint32_t s_tot[256];
+    __shared__ __align__(16) uint32_t s_hist[W * 256];        // read 16 bytes at a time
     __shared__ uint32_t s_info[4];
     __shared__ uint32_t s_nzw[W], s_wc[W];
     __shared__ uint64_t s_andw[W], s_orw[W];
-    const StreamLds L{s_hist, s_tot, s_info, s_nzw, s_wc, s_andw, s_orw};
+    const StreamLds L{s_hist, s_info, s_nzw, s_wc, s_andw, s_orw};
     const int q = blockIdx.x;
     const int kk = k;                                  // k <= kMaxK < kStreamThreads * 4
     int64_t cnt_q = dev_count ? (int64_t)dev_count[q] : count;

@@ -281,19 +281,19 @@ def radix_select(B: Block, key, need: int, cs, bound: bool):
                 if (key[t][e] & mask) == prefix:
                     B.atomic_add(t, "hist", my + ((key[t][e] >> lo) & dmask), 1)
         B.sync()
-        for t in B.order():
-            for b in range(t, 256, T):
-                tot = 0
-                for w in range(W):
-                    tot += B.rd(t, "hist", w * 256 + b)
-                    B.wr(t, "hist", w * 256 + b, 0)
-                B.wr(t, "tot", b, tot)
-        B.sync()
-        # wave 0: four digits per lane, suffix sums over lanes (registers)
+        # wave 0: each lane totals its four digits over the waves'
+        # histograms (clearing them), then suffix sums over lanes (registers)
         local = {}
         for t in B.order():
             if t < 64:
-                local[t] = [B.rd(t, "tot", 4 * t + j) for j in range(4)]
+                h = []
+                for j in range(4):
+                    tot = 0
+                    for w in range(W):
+                        tot += B.rd(t, "hist", w * 256 + 4 * t + j)
+                        B.wr(t, "hist", w * 256 + 4 * t + j, 0)
+                    h.append(tot)
+                local[t] = h
         incl = [sum(sum(local[m]) for m in range(l, 64)) for l in range(64)]
         writers = 0
         for t in B.order():
