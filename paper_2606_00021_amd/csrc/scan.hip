@@ -203,10 +203,17 @@ hipError_t launch_gemv_nc(const void* keys, int64_t n, int d, int64_t ld, const 
     auto kern = scan_gemv_kernel<KT, NC>;
     static const int per_cu = blocks_per_cu(kern, 256, 2);
     const int64_t max_blocks = (int64_t)device_cus() * per_cu;
-    // Rows per wave: an equal share for a single resident wave of blocks,
-    // never fewer than 2 (a small store is spread over more waves, each with
-    // its next row in flight: 4096 rows of 4096 dims 21 -> 19 us).
+    // Rows per wave: about 32 KiB of keys (4 rows of 4096 dims, 5 of 3584),
+    // at most an equal share for a single resident wave of blocks, never
+    // fewer than 2 (a small store is spread over more waves, each with its
+    // next row in flight: 4096 rows of 4096 dims 21 -> 19 us).  Many rounds
+    // of short-lived blocks read faster than one resident round walking
+    // long row runs: 1M x 4096 in 1.20 ms against 1.26 ms, 262K x 4096 in
+    // 300 us against 320 us.
+    const int64_t row_bytes = 2 * (int64_t)d;
     int64_t rpw = (n + max_blocks * 4 - 1) / (max_blocks * 4);
+    const int64_t by_bytes = (32768 + row_bytes - 1) / row_bytes;
+    if (rpw > by_bytes) rpw = by_bytes;
     if (rpw < 2) rpw = 2;
     const int64_t waves = (n + rpw - 1) / rpw;
     const int64_t blocks = (waves + 3) / 4;
